@@ -1,0 +1,187 @@
+/*
+ * mxq.h -- C ABI of libmxq, mixed-mantissa MXINT (4/6/8-bit) activation
+ * quantization and MXINT GEMM on AMD MI355X (gfx950).
+ *
+ * The operations follow MXSens (arXiv 2607.17733):
+ *   - MXINT (Section 2): blocks of 32 consecutive values along the reduction
+ *     dimension K share one power-of-two scale stored as an 8-bit exponent
+ *     (Section 5.1: +0.25 bit per element); elements are fixed-point
+ *     integers, so a block dot product is an integer multiply-accumulate
+ *     followed by a power-of-two scaling.
+ *   - Mixed mantissas (Section 4.1, Algorithm 2): each block has exactly one
+ *     mantissa width out of {4, 6, 8}; columns are permuted so that
+ *     same-width columns fill whole blocks.  The widths and the permutation
+ *     are the output of the offline sensitivity analysis (Algorithms 1-3,
+ *     Theorem A.1) and are inputs here.  Weights and activations of a linear
+ *     share one width map (Section 3.1: one sensitivity metric for both).
+ *
+ * Quantization of one block x[0..31] with width m (m counts the sign bit):
+ *   e = floor(log2(max|x|)) clamped to [-127, 127], stored as E = e + 127;
+ *   s = e - (m - 2) is the weight of the mantissa LSB;
+ *   q = clamp(round(x / 2^s)) with round = nearest-even (default) or
+ *   nearest-away, clamp = symmetric +-(2^(m-1)-1) (default) or full
+ *   [-2^(m-1), 2^(m-1)-1].
+ *   A block whose maximum is zero or subnormal has E = 0 (e clamps to
+ *   -127); a block holding Inf or NaN has E = 255 and zero mantissas.
+ * GEMM: Y[i][j] = sum_b P[i][j][b] * 2^(sa[i][b] + sw[j][b]) where
+ *   P[i][j][b] = sum_t qa[i][32b+t] * qw[j][32b+t] is computed exactly in
+ *   int32 on int8 matrix cores, and Y is accumulated in fp32.  Any block with
+ *   E == 255 on either side makes the outputs it touches NaN.  Results whose
+ *   magnitude is below fp32's range (2^-149) flush towards zero.
+ *
+ * Conventions for every entry point:
+ *   - All functions are thread-safe and reentrant.  Device work is enqueued
+ *     on `stream` (a hipStream_t; NULL = the default stream) and runs
+ *     asynchronously; nothing synchronizes, allocates or frees memory.
+ *   - The caller owns every buffer.  "DEVICE" pointers are device memory of
+ *     the current HIP device; "HOST" pointers are read during the call only.
+ *   - Device pointers must be 16-byte aligned.  Leading dimensions (lda,
+ *     ldw, ldy) are in elements.
+ *   - On invalid arguments a nonzero mxq_status is returned before anything
+ *     is enqueued and no output is touched.  A failed kernel launch returns
+ *     MXQ_ERR_DEVICE.  No C++ exception crosses the ABI.
+ *   - M == 0 or N == 0 is valid and enqueues nothing.
+ */
+#ifndef MXQ_H
+#define MXQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MXQ_ABI_VERSION 1
+#define MXQ_BLOCK 32
+/* mxq_gemm uses the weight-streaming decode kernel for M <= this. */
+#define MXQ_DECODE_MAX_M 16
+
+typedef enum {
+  MXQ_OK = 0,
+  MXQ_ERR_NULL = 1,        /* a required pointer is NULL */
+  MXQ_ERR_SHAPE = 2,       /* K % 32 != 0, K <= 0, negative sizes, ld < K/N */
+  MXQ_ERR_WIDTHS = 3,      /* a width not in {4,6,8}, or widths not grouped 4s,6s,8s */
+  MXQ_ERR_PERM = 4,        /* reserved: permutations are not validated (see below) */
+  MXQ_ERR_ALIGN = 5,       /* a device pointer is not 16-byte aligned */
+  MXQ_ERR_UNSUPPORTED = 6, /* block != 32, unknown round/clamp mode */
+  MXQ_ERR_DEVICE = 7       /* kernel launch or device query failed */
+} mxq_status;
+
+typedef enum { MXQ_ROUND_NEAREST_EVEN = 0, MXQ_ROUND_NEAREST_AWAY = 1 } mxq_round;
+typedef enum { MXQ_CLAMP_SYMMETRIC = 0, MXQ_CLAMP_FULL = 1 } mxq_clamp;
+
+/*
+ * Format of one quantized linear (shared by its activations and weights).
+ *   K       reduction length, a positive multiple of 32.
+ *   block   must be 32.
+ *   round   mxq_round.   clamp   mxq_clamp.
+ *   widths  HOST, K/32 entries, each 4, 6 or 8, non-decreasing (all 4-bit
+ *           blocks, then all 6-bit, then all 8-bit; any count may be zero).
+ *   perm    DEVICE int32[K] or NULL (identity).  Position p of the quantized
+ *           row holds source column perm[p].  Entries outside [0, K) are read
+ *           as +0.0 (never dereferenced); duplicates are allowed.
+ */
+typedef struct {
+  int64_t K;
+  int32_t block;
+  int32_t round;
+  int32_t clamp;
+  int32_t reserved;        /* must be 0 */
+  const uint8_t *widths;
+  const int32_t *perm;
+} mxq_fmt;
+
+int mxq_abi_version(void);
+const char *mxq_status_str(int status);
+
+/*
+ * Sizes (bytes) of the packed buffers; negative mxq_status on a bad format.
+ *
+ * Packed activations (canonical layout, the output of mxq_quantize_act):
+ *   a_mant row r starts at r * mxq_act_row_bytes(fmt); the row holds the
+ *   blocks in permuted order, block b taking 4 * m_b bytes, padded with
+ *   zero bytes to a multiple of 16:
+ *     4-bit: byte j holds element 2j in bits 0-3 and element 2j+1 in bits 4-7;
+ *     6-bit: 16 bytes of low nibbles in the 4-bit layout, then two 32-bit
+ *            words of the signed top two bits: word d covers elements
+ *            16d..16d+15, its byte j holds element 16d+2j in bits 6-7,
+ *            16d+2j+1 in bits 4-5, 16d+8+2j in bits 2-3, 16d+9+2j in bits 0-1;
+ *     8-bit: one two's-complement byte per element.
+ *   a_exp row r starts at r * mxq_exp_row_bytes(fmt); byte b is E of block b;
+ *   the row is padded with zeros to a multiple of 16.
+ * Packed weights (mxq_pack_weights) use a GEMM-tiled layout: columns are
+ * grouped in slabs of 16 (N rounded up; padding columns are zero), each slab
+ * holds its blocks grouped by four within each width segment, interleaved in
+ * matrix-core operand order.  The exponents are stored block-major,
+ * w_exp[b * Npad + j].  The layout is opaque: use mxq_unpack_weights to read
+ * it back in canonical form.
+ */
+int64_t mxq_act_row_bytes(const mxq_fmt *fmt);
+int64_t mxq_exp_row_bytes(const mxq_fmt *fmt);
+int64_t mxq_weight_bytes(const mxq_fmt *fmt, int64_t N);
+int64_t mxq_weight_exp_bytes(const mxq_fmt *fmt, int64_t N);
+
+/*
+ * Online activation quantization (paper: Section 5, activations of every
+ * decoder linear and the KV cache are quantized to MXINT; Section 4.1 widths).
+ *   a       DEVICE bf16 [M][lda], lda >= K, read only.
+ *   a_mant  DEVICE uint8 [M][mxq_act_row_bytes], written (canonical layout).
+ *   a_exp   DEVICE uint8 [M][mxq_exp_row_bytes], written.
+ */
+mxq_status mxq_quantize_act(const mxq_fmt *fmt, const uint16_t *a, int64_t M,
+                            int64_t lda, uint8_t *a_mant, uint8_t *a_exp,
+                            void *stream);
+
+/*
+ * Offline weight quantization and packing (same quantizer as the
+ * activations; paper Section 5: weights of every decoder linear).
+ *   w       DEVICE bf16 [N][ldw] (torch.nn.Linear layout: row j is output
+ *           column j), ldw >= K.
+ *   w_mant  DEVICE uint8 [mxq_weight_bytes(fmt, N)], written.
+ *   w_exp   DEVICE uint8 [mxq_weight_exp_bytes(fmt, N)], written.
+ */
+mxq_status mxq_pack_weights(const mxq_fmt *fmt, const uint16_t *w, int64_t N,
+                            int64_t ldw, uint8_t *w_mant, uint8_t *w_exp,
+                            void *stream);
+
+/*
+ * MXINT GEMM, Y = Ahat * What^T in fp32 (paper Sections 2 and 6: integer
+ * block products, power-of-two block scales).
+ *   a_mant/a_exp  DEVICE, from mxq_quantize_act with the same fmt, M rows.
+ *   w_mant/w_exp  DEVICE, from mxq_pack_weights with the same fmt, N columns.
+ *   y             DEVICE float [M][ldy], ldy >= N; every y[i][j] with i < M,
+ *                 j < N is written, nothing else.
+ * M <= MXQ_DECODE_MAX_M runs the weight-streaming decode kernel, larger M the
+ * tiled prefill kernel; both give the same int32 block sums.
+ */
+mxq_status mxq_gemm(const mxq_fmt *fmt, int64_t M, int64_t N,
+                    const uint8_t *a_mant, const uint8_t *a_exp,
+                    const uint8_t *w_mant, const uint8_t *w_exp, float *y,
+                    int64_t ldy, void *stream);
+
+/*
+ * Debug / parity entry points (not on the hot path).
+ * mxq_unpack_act / mxq_unpack_weights: packed -> canonical mantissas
+ *   q DEVICE int8 [rows][K] (permuted order) and exponents e DEVICE uint8
+ *   [rows][K/32].
+ * mxq_gemm_partials: the exact per-block int32 sums
+ *   p DEVICE int32 [M][N][K/32], computed by the same unpack and matrix-core
+ *   path as mxq_gemm (prefill tiling).
+ */
+mxq_status mxq_unpack_act(const mxq_fmt *fmt, int64_t rows,
+                          const uint8_t *a_mant, const uint8_t *a_exp,
+                          int8_t *q, uint8_t *e, void *stream);
+mxq_status mxq_unpack_weights(const mxq_fmt *fmt, int64_t N,
+                              const uint8_t *w_mant, const uint8_t *w_exp,
+                              int8_t *q, uint8_t *e, void *stream);
+mxq_status mxq_gemm_partials(const mxq_fmt *fmt, int64_t M, int64_t N,
+                             const uint8_t *a_mant, const uint8_t *a_exp,
+                             const uint8_t *w_mant, const uint8_t *w_exp,
+                             int32_t *p, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MXQ_H */

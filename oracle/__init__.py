@@ -78,6 +78,8 @@ def _declare(lib):
     lib.oracle_act_row_bytes.argtypes = [P, I64]
     lib.oracle_act_row_bytes.restype = I64
     lib.oracle_pack_act.argtypes = [P, I64, I64, P, P]
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = I
     for f in ("oracle_quantize", "oracle_dequantize", "oracle_block_partials",
               "oracle_gemm", "oracle_gemm_absbound", "oracle_pack_act"):
         getattr(lib, f).restype = I
@@ -187,3 +189,8 @@ def pack_act(q, widths):
     if rc:
         raise ValueError("oracle_pack_act failed")
     return out
+
+
+def num_threads() -> int:
+    """Threads the oracle's OpenMP loops use."""
+    return int(_load().oracle_num_threads())

@@ -37,6 +37,9 @@
  * bf16 input.
  */
 #include <fenv.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
@@ -294,4 +297,13 @@ int oracle_pack_act(const int8_t *q, int64_t rows, int64_t K,
     }
   }
   return 0;
+}
+
+/* Number of threads the OpenMP loops above use (1 without OpenMP). */
+int oracle_num_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
 }

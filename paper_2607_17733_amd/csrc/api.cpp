@@ -1,0 +1,243 @@
+// api.cpp -- the C ABI of libmxq (declared in include/mxq.h): argument
+// validation, width-map segment derivation and kernel dispatch.  Every check
+// happens before anything is enqueued; nothing here allocates, frees or
+// synchronizes.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include "../../include/mxq.h"
+#include "mxq_device.h"
+#include "mxq_internal.h"
+
+namespace {
+
+using mxq::Segs;
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+// Validate a format and derive its width segments (MXSens Section 4.1: one
+// width per block; the permutation groups same-width columns, ordered
+// 4-bit, 6-bit, 8-bit).
+mxq_status check_fmt(const mxq_fmt *f, Segs *s) {
+  if (!f) return MXQ_ERR_NULL;
+  if (f->block != MXQ_BLOCK) return MXQ_ERR_UNSUPPORTED;
+  if (f->round != MXQ_ROUND_NEAREST_EVEN && f->round != MXQ_ROUND_NEAREST_AWAY)
+    return MXQ_ERR_UNSUPPORTED;
+  if (f->clamp != MXQ_CLAMP_SYMMETRIC && f->clamp != MXQ_CLAMP_FULL)
+    return MXQ_ERR_UNSUPPORTED;
+  if (f->reserved != 0) return MXQ_ERR_UNSUPPORTED;
+  if (f->K <= 0 || f->K % MXQ_BLOCK != 0) return MXQ_ERR_SHAPE;
+  if (f->K / MXQ_BLOCK > (int64_t)(1 << 24)) return MXQ_ERR_SHAPE;
+  if (!f->widths) return MXQ_ERR_NULL;
+  if (f->perm && !aligned16(f->perm)) return MXQ_ERR_ALIGN;
+  const int64_t nb = f->K / MXQ_BLOCK;
+  int n[3] = {0, 0, 0};
+  int prev = 0;
+  for (int64_t b = 0; b < nb; ++b) {
+    const int m = f->widths[b];
+    if (m != 4 && m != 6 && m != 8) return MXQ_ERR_WIDTHS;
+    if (m < prev) return MXQ_ERR_WIDTHS;
+    prev = m;
+    ++n[(m - 4) / 2];
+  }
+  s->n4 = n[0];
+  s->n6 = n[1];
+  s->n8 = n[2];
+  return MXQ_OK;
+}
+
+int64_t row_used(const Segs &s) { return 16LL * s.n4 + 24LL * s.n6 + 32LL * s.n8; }
+int64_t act_rb(const Segs &s) { return round_up(row_used(s), 16); }
+int64_t exp_rb(const mxq_fmt *f) { return round_up(f->K / MXQ_BLOCK, 16); }
+
+mxq_status launched(hipError_t e) { return e == hipSuccess ? MXQ_OK : MXQ_ERR_DEVICE; }
+
+mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows,
+                           int64_t ld, uint8_t *mant, uint8_t *exp, void *stream,
+                           bool weights) {
+  Segs s;
+  mxq_status st = check_fmt(fmt, &s);
+  if (st != MXQ_OK) return st;
+  if (rows < 0 || ld < fmt->K) return MXQ_ERR_SHAPE;
+  if (rows == 0) return MXQ_OK;
+  if (!src || !mant || !exp) return MXQ_ERR_NULL;
+  if (!aligned16(src) || !aligned16(mant) || !aligned16(exp)) return MXQ_ERR_ALIGN;
+  mxq::QuantArgs a{};
+  a.src = src;
+  a.ld = ld;
+  a.src_rows = rows;
+  a.out_rows = weights ? round_up(rows, 16) : rows;
+  a.K = fmt->K;
+  a.perm = fmt->perm;
+  a.n4 = s.n4;
+  a.n6 = s.n6;
+  a.n8 = s.n8;
+  a.ties_away = fmt->round == MXQ_ROUND_NEAREST_AWAY;
+  a.full_clamp = fmt->clamp == MXQ_CLAMP_FULL;
+  a.mant = mant;
+  a.exp = exp;
+  a.out_rb = act_rb(s);
+  a.out_erb = exp_rb(fmt);
+  a.row_used = row_used(s);
+  a.vec16 = (ld % 8 == 0) ? 1 : 0;
+  // Stage source rows in LDS for the permutation gather while they fit in
+  // 64 KB of LDS; longer rows gather straight from global memory.
+  a.stage = (fmt->perm && fmt->K <= 32768) ? 1 : 0;
+  return launched(mxq::launch_quantize(a, weights, (hipStream_t)stream));
+}
+
+mxq_status gemm_args(const mxq_fmt *fmt, int64_t M, int64_t N, const uint8_t *a_mant,
+                     const uint8_t *a_exp, const uint8_t *w_mant, const uint8_t *w_exp,
+                     const void *out, mxq::GemmArgs *g) {
+  Segs s;
+  mxq_status st = check_fmt(fmt, &s);
+  if (st != MXQ_OK) return st;
+  if (M < 0 || N < 0) return MXQ_ERR_SHAPE;
+  if (M == 0 || N == 0) return MXQ_OK;
+  if (!a_mant || !a_exp || !w_mant || !w_exp || !out) return MXQ_ERR_NULL;
+  if (!aligned16(a_mant) || !aligned16(a_exp) || !aligned16(w_mant) ||
+      !aligned16(w_exp) || !aligned16(out))
+    return MXQ_ERR_ALIGN;
+  *g = mxq::GemmArgs{};
+  g->a_mant = a_mant;
+  g->a_exp = a_exp;
+  g->w_mant = w_mant;
+  g->w_exp = w_exp;
+  g->M = M;
+  g->N = N;
+  g->a_rb = act_rb(s);
+  g->a_erb = exp_rb(fmt);
+  g->npad = round_up(N, 16);
+  g->n4 = s.n4;
+  g->n6 = s.n6;
+  g->n8 = s.n8;
+  return MXQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mxq_abi_version(void) { return MXQ_ABI_VERSION; }
+
+const char *mxq_status_str(int status) {
+  switch (status) {
+    case MXQ_OK: return "ok";
+    case MXQ_ERR_NULL: return "null pointer";
+    case MXQ_ERR_SHAPE: return "invalid shape or leading dimension";
+    case MXQ_ERR_WIDTHS: return "invalid width map (widths must be 4, 6 or 8, grouped 4s, 6s, 8s)";
+    case MXQ_ERR_PERM: return "invalid permutation";
+    case MXQ_ERR_ALIGN: return "device pointer not 16-byte aligned";
+    case MXQ_ERR_UNSUPPORTED: return "unsupported block size, rounding or clamp mode";
+    case MXQ_ERR_DEVICE: return "device launch failure";
+    default: return "unknown status";
+  }
+}
+
+int64_t mxq_act_row_bytes(const mxq_fmt *fmt) {
+  Segs s;
+  const mxq_status st = check_fmt(fmt, &s);
+  return st == MXQ_OK ? act_rb(s) : -(int64_t)st;
+}
+
+int64_t mxq_exp_row_bytes(const mxq_fmt *fmt) {
+  Segs s;
+  const mxq_status st = check_fmt(fmt, &s);
+  return st == MXQ_OK ? exp_rb(fmt) : -(int64_t)st;
+}
+
+int64_t mxq_weight_bytes(const mxq_fmt *fmt, int64_t N) {
+  Segs s;
+  const mxq_status st = check_fmt(fmt, &s);
+  if (st != MXQ_OK) return -(int64_t)st;
+  if (N < 0) return -(int64_t)MXQ_ERR_SHAPE;
+  return round_up(N, 16) * row_used(s);
+}
+
+int64_t mxq_weight_exp_bytes(const mxq_fmt *fmt, int64_t N) {
+  Segs s;
+  const mxq_status st = check_fmt(fmt, &s);
+  if (st != MXQ_OK) return -(int64_t)st;
+  if (N < 0) return -(int64_t)MXQ_ERR_SHAPE;
+  return round_up(N, 16) * (fmt->K / MXQ_BLOCK);
+}
+
+mxq_status mxq_quantize_act(const mxq_fmt *fmt, const uint16_t *a, int64_t M,
+                            int64_t lda, uint8_t *a_mant, uint8_t *a_exp,
+                            void *stream) {
+  return quantize_common(fmt, a, M, lda, a_mant, a_exp, stream, false);
+}
+
+mxq_status mxq_pack_weights(const mxq_fmt *fmt, const uint16_t *w, int64_t N,
+                            int64_t ldw, uint8_t *w_mant, uint8_t *w_exp,
+                            void *stream) {
+  return quantize_common(fmt, w, N, ldw, w_mant, w_exp, stream, true);
+}
+
+mxq_status mxq_gemm(const mxq_fmt *fmt, int64_t M, int64_t N, const uint8_t *a_mant,
+                    const uint8_t *a_exp, const uint8_t *w_mant, const uint8_t *w_exp,
+                    float *y, int64_t ldy, void *stream) {
+  mxq::GemmArgs g;
+  mxq_status st = gemm_args(fmt, M, N, a_mant, a_exp, w_mant, w_exp, y, &g);
+  if (st != MXQ_OK) return st;
+  if (M == 0 || N == 0) return MXQ_OK;
+  if (ldy < N) return MXQ_ERR_SHAPE;
+  g.y = y;
+  g.ldy = ldy;
+  hipStream_t s = (hipStream_t)stream;
+  return launched(M <= MXQ_DECODE_MAX_M ? mxq::launch_gemm_decode(g, s)
+                                        : mxq::launch_gemm_prefill(g, s));
+}
+
+mxq_status mxq_gemm_partials(const mxq_fmt *fmt, int64_t M, int64_t N,
+                             const uint8_t *a_mant, const uint8_t *a_exp,
+                             const uint8_t *w_mant, const uint8_t *w_exp, int32_t *p,
+                             void *stream) {
+  mxq::GemmArgs g;
+  mxq_status st = gemm_args(fmt, M, N, a_mant, a_exp, w_mant, w_exp, p, &g);
+  if (st != MXQ_OK) return st;
+  if (M == 0 || N == 0) return MXQ_OK;
+  g.p = p;
+  return launched(mxq::launch_gemm_partials(g, (hipStream_t)stream));
+}
+
+static mxq_status unpack_common(const mxq_fmt *fmt, int64_t rows, const uint8_t *mant,
+                                const uint8_t *exp, int8_t *q, uint8_t *e, void *stream,
+                                bool weights) {
+  Segs s;
+  mxq_status st = check_fmt(fmt, &s);
+  if (st != MXQ_OK) return st;
+  if (rows < 0) return MXQ_ERR_SHAPE;
+  if (rows == 0) return MXQ_OK;
+  if (!mant || !exp || !q || !e) return MXQ_ERR_NULL;
+  if (!aligned16(mant) || !aligned16(exp)) return MXQ_ERR_ALIGN;
+  mxq::UnpackArgs a{};
+  a.mant = mant;
+  a.exp = exp;
+  a.q = q;
+  a.e = e;
+  a.rows = rows;
+  a.K = fmt->K;
+  a.a_rb = act_rb(s);
+  a.a_erb = exp_rb(fmt);
+  a.npad = round_up(rows, 16);
+  a.n4 = s.n4;
+  a.n6 = s.n6;
+  a.n8 = s.n8;
+  return launched(mxq::launch_unpack(a, weights, (hipStream_t)stream));
+}
+
+mxq_status mxq_unpack_act(const mxq_fmt *fmt, int64_t rows, const uint8_t *a_mant,
+                          const uint8_t *a_exp, int8_t *q, uint8_t *e, void *stream) {
+  return unpack_common(fmt, rows, a_mant, a_exp, q, e, stream, false);
+}
+
+mxq_status mxq_unpack_weights(const mxq_fmt *fmt, int64_t N, const uint8_t *w_mant,
+                              const uint8_t *w_exp, int8_t *q, uint8_t *e, void *stream) {
+  return unpack_common(fmt, N, w_mant, w_exp, q, e, stream, true);
+}
+
+}  // extern "C"

@@ -1,0 +1,59 @@
+// mxq_internal.h -- argument blocks and launchers shared between the host
+// API (api.cpp) and the kernel translation units.  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mxq {
+
+struct QuantArgs {
+  const uint16_t *src;     // bf16 rows [src_rows][ld]
+  int64_t ld;
+  int64_t src_rows;        // rows with data (M, or N for weights)
+  int64_t out_rows;        // rows written (M, or N rounded up to 16)
+  int64_t K;
+  const int32_t *perm;     // device, K entries, or nullptr
+  int n4, n6, n8;
+  int ties_away, full_clamp;
+  uint8_t *mant;
+  uint8_t *exp;
+  int64_t out_rb;          // packed activation row bytes (activations only)
+  int64_t out_erb;         // exponent row bytes (activations only)
+  int64_t row_used;        // unpadded packed bytes per row
+  int stage;               // stage source rows in LDS before the gather
+  int vec16;               // 16-byte source loads are aligned
+  int rows_per_wg;         // filled by the launcher
+};
+
+struct GemmArgs {
+  const uint8_t *a_mant;
+  const uint8_t *a_exp;
+  const uint8_t *w_mant;
+  const uint8_t *w_exp;
+  float *y;                // [M][ldy] (gemm)
+  int32_t *p;              // [M][N][nb] (partials)
+  int64_t M, N, ldy;
+  int64_t a_rb, a_erb;     // activation row bytes / exponent row bytes
+  int64_t npad;            // N rounded up to 16
+  int n4, n6, n8;
+};
+
+struct UnpackArgs {
+  const uint8_t *mant;
+  const uint8_t *exp;
+  int8_t *q;               // [rows][K]
+  uint8_t *e;              // [rows][nb]
+  int64_t rows, K;
+  int64_t a_rb, a_erb;     // activation layout
+  int64_t npad;            // weight layout
+  int n4, n6, n8;
+};
+
+hipError_t launch_quantize(const QuantArgs &args, bool weights, hipStream_t s);
+hipError_t launch_gemm_prefill(const GemmArgs &args, hipStream_t s);
+hipError_t launch_gemm_partials(const GemmArgs &args, hipStream_t s);
+hipError_t launch_gemm_decode(const GemmArgs &args, hipStream_t s);
+hipError_t launch_unpack(const UnpackArgs &args, bool weights, hipStream_t s);
+
+}  // namespace mxq

@@ -1,0 +1,201 @@
+"""Python binding of libmxq (include/mxq.h): argument marshalling only.
+
+Every step of the quantize / pack / GEMM path runs in the HIP kernels of
+``libmxq.so``; torch provides device memory and the current stream.  There
+is no fallback: if the library is missing the calls raise ``MxqError``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmxq.so")
+BLOCK = 32
+DECODE_MAX_M = 16
+
+
+class MxqError(RuntimeError):
+    pass
+
+
+class _Fmt(ctypes.Structure):
+    _fields_ = [("K", ctypes.c_int64), ("block", ctypes.c_int32),
+                ("round", ctypes.c_int32), ("clamp", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("widths", ctypes.c_void_p),
+                ("perm", ctypes.c_void_p)]
+
+
+_lib = None
+
+# name -> (restype, argtypes)
+_P, _I64 = ctypes.c_void_p, ctypes.c_int64
+_SIGS = {
+    "mxq_abi_version": (ctypes.c_int, []),
+    "mxq_status_str": (ctypes.c_char_p, [ctypes.c_int]),
+    "mxq_act_row_bytes": (_I64, [_P]),
+    "mxq_exp_row_bytes": (_I64, [_P]),
+    "mxq_weight_bytes": (_I64, [_P, _I64]),
+    "mxq_weight_exp_bytes": (_I64, [_P, _I64]),
+    "mxq_quantize_act": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P]),
+    "mxq_pack_weights": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P]),
+    "mxq_gemm": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P, _P, _P, _I64, _P]),
+    "mxq_gemm_partials": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P, _P, _P, _P]),
+    "mxq_unpack_act": (ctypes.c_int, [_P, _I64, _P, _P, _P, _P, _P]),
+    "mxq_unpack_weights": (ctypes.c_int, [_P, _I64, _P, _P, _P, _P, _P]),
+}
+
+
+def lib(path: str = LIB_PATH):
+    """Load libmxq.so (once).  Raises MxqError if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(path):
+            raise MxqError("libmxq.so is not built (%s); run __graft_entry__.build()"
+                           % path)
+        handle = ctypes.CDLL(path)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def _check(status: int, what: str):
+    if status != 0:
+        msg = lib().mxq_status_str(status).decode()
+        raise MxqError("%s failed: %s (status %d)" % (what, msg, status))
+
+
+def _size(v: int, what: str) -> int:
+    if v < 0:
+        _check(int(-v), what)
+    return int(v)
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+class Format:
+    """Width map + permutation of one quantized linear (include/mxq.h mxq_fmt).
+
+    widths: K/32 entries in {4, 6, 8}, grouped 4s then 6s then 8s.
+    perm:   None (identity) or an int32 device tensor of K source columns.
+    """
+
+    def __init__(self, K: int, widths, perm=None, round: str = "rne",
+                 clamp: str = "sym"):
+        self.K = int(K)
+        self.widths = np.ascontiguousarray(np.asarray(widths, dtype=np.uint8))
+        if perm is not None:
+            if not (isinstance(perm, torch.Tensor) and perm.is_cuda
+                    and perm.dtype == torch.int32 and perm.is_contiguous()):
+                raise MxqError("perm must be a contiguous int32 device tensor")
+        self.perm = perm
+        self.round = {"rne": 0, "rna": 1}[round]
+        self.clamp = {"sym": 0, "full": 1}[clamp]
+        self._c = _Fmt(self.K, BLOCK, self.round, self.clamp, 0,
+                       self.widths.ctypes.data_as(ctypes.c_void_p).value,
+                       None if perm is None else perm.data_ptr())
+
+    @property
+    def ref(self):
+        return ctypes.byref(self._c)
+
+    @property
+    def nb(self) -> int:
+        return self.K // BLOCK
+
+    def act_row_bytes(self) -> int:
+        return _size(lib().mxq_act_row_bytes(self.ref), "mxq_act_row_bytes")
+
+    def exp_row_bytes(self) -> int:
+        return _size(lib().mxq_exp_row_bytes(self.ref), "mxq_exp_row_bytes")
+
+    def weight_bytes(self, N: int) -> int:
+        return _size(lib().mxq_weight_bytes(self.ref, N), "mxq_weight_bytes")
+
+    def weight_exp_bytes(self, N: int) -> int:
+        return _size(lib().mxq_weight_exp_bytes(self.ref, N), "mxq_weight_exp_bytes")
+
+
+def _bf16_2d(t, K, what):
+    if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == torch.bfloat16
+            and t.dim() == 2 and t.stride(1) == 1):
+        raise MxqError("%s must be a 2-D bf16 device tensor with unit column stride"
+                       % what)
+    if t.shape[1] < K:
+        raise MxqError("%s has fewer than K columns" % what)
+    return t
+
+
+def quantize_act(a, fmt: Format, out=None):
+    """Online activation quantization: bf16 [M, >=K] -> (mant [M, row_bytes]
+    uint8, exp [M, exp_row_bytes] uint8) on the current stream."""
+    _bf16_2d(a, fmt.K, "activations")
+    M = a.shape[0]
+    if out is None:
+        mant = torch.empty((M, fmt.act_row_bytes()), dtype=torch.uint8, device=a.device)
+        exp = torch.empty((M, fmt.exp_row_bytes()), dtype=torch.uint8, device=a.device)
+    else:
+        mant, exp = out
+    _check(lib().mxq_quantize_act(fmt.ref, _ptr(a), M, a.stride(0), _ptr(mant),
+                                  _ptr(exp), _stream()), "mxq_quantize_act")
+    return mant, exp
+
+
+def pack_weights(w, fmt: Format):
+    """Offline weight quantization into the GEMM-tiled packed layout."""
+    _bf16_2d(w, fmt.K, "weights")
+    N = w.shape[0]
+    mant = torch.empty(fmt.weight_bytes(N), dtype=torch.uint8, device=w.device)
+    exp = torch.empty(fmt.weight_exp_bytes(N), dtype=torch.uint8, device=w.device)
+    _check(lib().mxq_pack_weights(fmt.ref, _ptr(w), N, w.stride(0), _ptr(mant),
+                                  _ptr(exp), _stream()), "mxq_pack_weights")
+    return mant, exp
+
+
+def gemm(a_mant, a_exp, w_mant, w_exp, fmt: Format, M: int, N: int, out=None):
+    """Y = Ahat @ What^T, fp32 [M, N]."""
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=a_mant.device)
+    if out.dim() != 2 or out.stride(1) != 1 or out.dtype != torch.float32:
+        raise MxqError("out must be a 2-D fp32 tensor with unit column stride")
+    _check(lib().mxq_gemm(fmt.ref, M, N, _ptr(a_mant), _ptr(a_exp), _ptr(w_mant),
+                          _ptr(w_exp), _ptr(out), out.stride(0), _stream()),
+           "mxq_gemm")
+    return out
+
+
+def gemm_partials(a_mant, a_exp, w_mant, w_exp, fmt: Format, M: int, N: int):
+    """Exact per-block int32 sums P[M, N, K/32] (debug / parity)."""
+    p = torch.empty((M, N, fmt.nb), dtype=torch.int32, device=a_mant.device)
+    _check(lib().mxq_gemm_partials(fmt.ref, M, N, _ptr(a_mant), _ptr(a_exp),
+                                   _ptr(w_mant), _ptr(w_exp), _ptr(p), _stream()),
+           "mxq_gemm_partials")
+    return p
+
+
+def unpack_act(mant, exp, fmt: Format, rows: int):
+    q = torch.empty((rows, fmt.K), dtype=torch.int8, device=mant.device)
+    e = torch.empty((rows, fmt.nb), dtype=torch.uint8, device=mant.device)
+    _check(lib().mxq_unpack_act(fmt.ref, rows, _ptr(mant), _ptr(exp), _ptr(q), _ptr(e),
+                                _stream()), "mxq_unpack_act")
+    return q, e
+
+
+def unpack_weights(w_mant, w_exp, fmt: Format, N: int):
+    q = torch.empty((N, fmt.K), dtype=torch.int8, device=w_mant.device)
+    e = torch.empty((N, fmt.nb), dtype=torch.uint8, device=w_mant.device)
+    _check(lib().mxq_unpack_weights(fmt.ref, N, _ptr(w_mant), _ptr(w_exp), _ptr(q),
+                                    _ptr(e), _stream()), "mxq_unpack_weights")
+    return q, e

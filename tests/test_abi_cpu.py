@@ -1,0 +1,105 @@
+"""CPU-side checks of the C ABI: the library loads, exports every function
+declared in include/mxq.h, and its host-only entry points (sizes, argument
+validation) behave as documented.  No device work is enqueued here: every
+call either computes a size or fails validation before any launch."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mxq.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mxq_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2607_17733_amd import mxq
+    if not os.path.exists(mxq.LIB_PATH):
+        from paper_2607_17733_amd import build
+        build.build()
+    return mxq.lib()
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("mxq_quantize_act", "mxq_pack_weights", "mxq_gemm",
+              "mxq_unpack_act", "mxq_unpack_weights", "mxq_gemm_partials"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def _fmt(K, widths, round_=0, clamp=0, block=32, reserved=0):
+    from paper_2607_17733_amd.mxq import _Fmt
+    w = np.ascontiguousarray(widths, dtype=np.uint8)
+    f = _Fmt(K, block, round_, clamp, reserved, w.ctypes.data_as(ctypes.c_void_p).value, None)
+    return f, w
+
+
+def test_sizes(lib):
+    f, _w = _fmt(256, [4] * 6 + [6, 8])
+    assert lib.mxq_abi_version() == 1
+    assert lib.mxq_act_row_bytes(ctypes.byref(f)) == 160
+    assert lib.mxq_exp_row_bytes(ctypes.byref(f)) == 16
+    assert lib.mxq_weight_bytes(ctypes.byref(f), 256) == 256 * 152
+    assert lib.mxq_weight_bytes(ctypes.byref(f), 250) == 256 * 152
+    assert lib.mxq_weight_exp_bytes(ctypes.byref(f), 17) == 32 * 8
+    f2, _w2 = _fmt(4096, [4] * 102 + [6] * 13 + [8] * 13)
+    assert lib.mxq_act_row_bytes(ctypes.byref(f2)) == 2368   # 2360 rounded up to 16
+    assert lib.mxq_exp_row_bytes(ctypes.byref(f2)) == 128
+
+
+def test_size_functions_match_oracle_layout(lib, oracle_lib):
+    for widths in ([4] * 3 + [6] * 1, [6] * 3, [8] * 5, [4] * 7 + [8]):
+        f, _w = _fmt(32 * len(widths), widths)
+        assert lib.mxq_act_row_bytes(ctypes.byref(f)) == oracle_lib.act_row_bytes(widths)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(K=250, widths=[4] * 8), 2),            # K % 32
+    (dict(K=64, widths=[4, 5]), 3),              # bad width
+    (dict(K=64, widths=[8, 4]), 3),              # not grouped
+    (dict(K=64, widths=[6, 4]), 3),
+    (dict(K=64, widths=[4, 4], block=16), 6),
+    (dict(K=64, widths=[4, 4], round_=2), 6),
+    (dict(K=64, widths=[4, 4], clamp=7), 6),
+    (dict(K=64, widths=[4, 4], reserved=1), 6),
+])
+def test_bad_formats_rejected(lib, kwargs, status):
+    f, _w = _fmt(**kwargs)
+    assert lib.mxq_act_row_bytes(ctypes.byref(f)) == -status
+    # the quantizer rejects the format before touching any pointer
+    dummy = ctypes.c_void_p(16)
+    assert lib.mxq_quantize_act(ctypes.byref(f), dummy, 4, 4096, dummy, dummy, None) == status
+
+
+def test_argument_validation_before_launch(lib):
+    f, _w = _fmt(64, [4, 8])
+    fr = ctypes.byref(f)
+    p16 = ctypes.c_void_p(4096)          # never dereferenced: validation fails first
+    bad = ctypes.c_void_p(4097)
+    assert lib.mxq_quantize_act(None, p16, 4, 64, p16, p16, None) == 1
+    assert lib.mxq_quantize_act(fr, None, 4, 64, p16, p16, None) == 1
+    assert lib.mxq_quantize_act(fr, p16, 4, 63, p16, p16, None) == 2
+    assert lib.mxq_quantize_act(fr, p16, -1, 64, p16, p16, None) == 2
+    assert lib.mxq_quantize_act(fr, bad, 4, 64, p16, p16, None) == 5
+    assert lib.mxq_quantize_act(fr, p16, 0, 64, None, None, None) == 0   # empty: no-op
+    assert lib.mxq_pack_weights(fr, p16, 4, 64, bad, p16, None) == 5
+    assert lib.mxq_gemm(fr, 4, 4, p16, p16, p16, p16, p16, 3, None) == 2   # ldy < N
+    assert lib.mxq_gemm(fr, 4, 4, p16, None, p16, p16, p16, 4, None) == 1
+    assert lib.mxq_gemm(fr, 0, 4, None, None, None, None, None, 4, None) == 0
+    assert lib.mxq_gemm(fr, -1, 4, p16, p16, p16, p16, p16, 4, None) == 2
+    assert lib.mxq_gemm_partials(fr, 4, 4, p16, p16, p16, p16, bad, None) == 5
+    assert lib.mxq_unpack_act(fr, 4, p16, p16, None, p16, None) == 1
+    assert lib.mxq_status_str(5).decode().startswith("device pointer")
