@@ -98,26 +98,43 @@ const char *mxq_status_str(int status);
 /*
  * Sizes (bytes) of the packed buffers; negative mxq_status on a bad format.
  *
- * Packed activations (canonical layout, the output of mxq_quantize_act):
- *   a_mant row r starts at r * mxq_act_row_bytes(fmt); the row holds the
- *   blocks in permuted order, block b taking 4 * m_b bytes, padded with
- *   zero bytes to a multiple of 16:
+ * Activations (the output of mxq_quantize_act):
+ *   a_mant row r starts at r * mxq_act_row_bytes(fmt) and holds two sections.
+ *   (1) The bit-packed mantissas, mxq_act_packed_bytes(fmt) bytes: the blocks
+ *   in permuted order, block b taking 4 * m_b bytes, padded with zero bytes
+ *   to a multiple of 16:
  *     4-bit: byte j holds element 2j in bits 0-3 and element 2j+1 in bits 4-7;
  *     6-bit: 16 bytes of low nibbles in the 4-bit layout, then two 32-bit
  *            words of the signed top two bits: word d covers elements
  *            16d..16d+15, its byte j holds element 16d+2j in bits 6-7,
  *            16d+2j+1 in bits 4-5, 16d+8+2j in bits 2-3, 16d+9+2j in bits 0-1;
  *     8-bit: one two's-complement byte per element.
- *   a_exp row r starts at r * mxq_exp_row_bytes(fmt); byte b is E of block b;
- *   the row is padded with zeros to a multiple of 16.
+ *   (2) The matrix-core operand image, K bytes: the same mantissas unpacked
+ *   to int8 and aligned to a reference exponent ref >= E per block, so that
+ *   block b of the row equals operand * 2^(ref - 133).  Element t of block b
+ *   is at byte 32b + 8(t/8) + (t%8)/2 + 4(t%2) for 4- and 6-bit blocks (the
+ *   even elements of each group of eight, then the odd ones) and at 32b + t
+ *   for 8-bit blocks; its value is q * 2^(8 - m - (ref - E)).  Within every
+ *   chunk of 16 consecutive blocks of one width (counted from the start of
+ *   the width's blocks) ref = max E of the chunk when max E - min E <= 8 - m,
+ *   else ref = E.  The GEMM reads only this section; the decode GEMM and
+ *   mxq_unpack_act read section (1).
+ *   a_exp row r starts at r * mxq_exp_row_bytes(fmt): exponent_row bytes of
+ *   block exponents E (byte b for block b, zero padded to a multiple of 16),
+ *   then as many bytes of reference exponents ref.
+ * Here exponent_row = K/32 rounded up to a multiple of 16, and
+ * mxq_exp_row_bytes(fmt) = 2 * exponent_row.
  * Packed weights (mxq_pack_weights) use a GEMM-tiled layout: columns are
  * grouped in slabs of 16 (N rounded up; padding columns are zero), each slab
  * holds its blocks grouped by four within each width segment, interleaved in
- * matrix-core operand order.  The exponents are stored block-major,
- * w_exp[b * Npad + j].  The layout is opaque: use mxq_unpack_weights to read
- * it back in canonical form.
+ * matrix-core operand order.  The weight exponents are one row of
+ * exponent_row bytes per (padded) column: w_exp[j * exponent_row + b].
+ * The mantissa layout is opaque (mxq_weight_bytes includes 64 bytes of tail
+ * padding that the GEMM may read but never uses): use mxq_unpack_weights to
+ * read it back in canonical form.
  */
 int64_t mxq_act_row_bytes(const mxq_fmt *fmt);
+int64_t mxq_act_packed_bytes(const mxq_fmt *fmt);
 int64_t mxq_exp_row_bytes(const mxq_fmt *fmt);
 int64_t mxq_weight_bytes(const mxq_fmt *fmt, int64_t N);
 int64_t mxq_weight_exp_bytes(const mxq_fmt *fmt, int64_t N);

@@ -18,6 +18,8 @@ bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
 int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
+constexpr int64_t kWeightTailPad = 64;
+
 // Validate a format and derive its width segments (MXSens Section 4.1: one
 // width per block; the permutation groups same-width columns, ordered
 // 4-bit, 6-bit, 8-bit).
@@ -50,8 +52,13 @@ mxq_status check_fmt(const mxq_fmt *f, Segs *s) {
 }
 
 int64_t row_used(const Segs &s) { return 16LL * s.n4 + 24LL * s.n6 + 32LL * s.n8; }
-int64_t act_rb(const Segs &s) { return round_up(row_used(s), 16); }
+// canonical packed section and per-row exponent section
+int64_t canon_rb(const Segs &s) { return round_up(row_used(s), 16); }
 int64_t exp_rb(const mxq_fmt *f) { return round_up(f->K / MXQ_BLOCK, 16); }
+// activation rows: canonical section followed by the K-byte operand image;
+// activation exponent rows: exponents followed by reference exponents
+int64_t act_rb(const mxq_fmt *f, const Segs &s) { return canon_rb(s) + f->K; }
+int64_t act_erb(const mxq_fmt *f) { return 2 * exp_rb(f); }
 
 mxq_status launched(hipError_t e) { return e == hipSuccess ? MXQ_OK : MXQ_ERR_DEVICE; }
 
@@ -79,13 +86,22 @@ mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows
   a.full_clamp = fmt->clamp == MXQ_CLAMP_FULL;
   a.mant = mant;
   a.exp = exp;
-  a.out_rb = act_rb(s);
-  a.out_erb = exp_rb(fmt);
+  a.canon_rb = canon_rb(s);
+  a.canon_erb = exp_rb(fmt);
+  a.out_rb = weights ? 0 : act_rb(fmt, s);
+  a.out_erb = weights ? exp_rb(fmt) : act_erb(fmt);
   a.row_used = row_used(s);
+  a.tail_pad = weights ? (int)kWeightTailPad : 0;
   a.vec16 = (ld % 8 == 0) ? 1 : 0;
-  // Stage source rows in LDS for the permutation gather while they fit in
-  // 64 KB of LDS; longer rows gather straight from global memory.
-  a.stage = (fmt->perm && fmt->K <= 32768) ? 1 : 0;
+  // Stage source rows in LDS for the permutation gather when they fit;
+  // longer rows gather straight from global memory.
+  const int R = mxq::quantize_rows_per_wg(fmt->K);
+  if (weights) {
+    a.stage = (fmt->perm && (int64_t)R * fmt->K * 2 <= mxq::kMaxLds) ? 1 : 0;
+  } else {
+    a.stage = (fmt->perm && mxq::quantize_act_lds(1, R, fmt->K) <= mxq::kMaxLds) ? 1 : 0;
+    if (mxq::quantize_act_lds(a.stage, R, fmt->K) > mxq::kMaxLds) return MXQ_ERR_UNSUPPORTED;
+  }
   return launched(mxq::launch_quantize(a, weights, (hipStream_t)stream));
 }
 
@@ -108,8 +124,11 @@ mxq_status gemm_args(const mxq_fmt *fmt, int64_t M, int64_t N, const uint8_t *a_
   g->w_exp = w_exp;
   g->M = M;
   g->N = N;
-  g->a_rb = act_rb(s);
-  g->a_erb = exp_rb(fmt);
+  g->a_rb = act_rb(fmt, s);
+  g->a_erb = act_erb(fmt);
+  g->a_op = canon_rb(s);
+  g->a_ref = exp_rb(fmt);
+  g->w_erb = exp_rb(fmt);
   g->npad = round_up(N, 16);
   g->n4 = s.n4;
   g->n6 = s.n6;
@@ -140,13 +159,19 @@ const char *mxq_status_str(int status) {
 int64_t mxq_act_row_bytes(const mxq_fmt *fmt) {
   Segs s;
   const mxq_status st = check_fmt(fmt, &s);
-  return st == MXQ_OK ? act_rb(s) : -(int64_t)st;
+  return st == MXQ_OK ? act_rb(fmt, s) : -(int64_t)st;
 }
 
 int64_t mxq_exp_row_bytes(const mxq_fmt *fmt) {
   Segs s;
   const mxq_status st = check_fmt(fmt, &s);
-  return st == MXQ_OK ? exp_rb(fmt) : -(int64_t)st;
+  return st == MXQ_OK ? act_erb(fmt) : -(int64_t)st;
+}
+
+int64_t mxq_act_packed_bytes(const mxq_fmt *fmt) {
+  Segs s;
+  const mxq_status st = check_fmt(fmt, &s);
+  return st == MXQ_OK ? canon_rb(s) : -(int64_t)st;
 }
 
 int64_t mxq_weight_bytes(const mxq_fmt *fmt, int64_t N) {
@@ -154,7 +179,9 @@ int64_t mxq_weight_bytes(const mxq_fmt *fmt, int64_t N) {
   const mxq_status st = check_fmt(fmt, &s);
   if (st != MXQ_OK) return -(int64_t)st;
   if (N < 0) return -(int64_t)MXQ_ERR_SHAPE;
-  return round_up(N, 16) * row_used(s);
+  // plus tail padding: the GEMM reads whole 16-byte words past the last
+  // lane's data of a slab
+  return round_up(N, 16) * row_used(s) + kWeightTailPad;
 }
 
 int64_t mxq_weight_exp_bytes(const mxq_fmt *fmt, int64_t N) {
@@ -162,7 +189,7 @@ int64_t mxq_weight_exp_bytes(const mxq_fmt *fmt, int64_t N) {
   const mxq_status st = check_fmt(fmt, &s);
   if (st != MXQ_OK) return -(int64_t)st;
   if (N < 0) return -(int64_t)MXQ_ERR_SHAPE;
-  return round_up(N, 16) * (fmt->K / MXQ_BLOCK);
+  return round_up(N, 16) * exp_rb(fmt);
 }
 
 mxq_status mxq_quantize_act(const mxq_fmt *fmt, const uint16_t *a, int64_t M,
@@ -221,8 +248,8 @@ static mxq_status unpack_common(const mxq_fmt *fmt, int64_t rows, const uint8_t 
   a.e = e;
   a.rows = rows;
   a.K = fmt->K;
-  a.a_rb = act_rb(s);
-  a.a_erb = exp_rb(fmt);
+  a.a_rb = act_rb(fmt, s);
+  a.a_erb = weights ? exp_rb(fmt) : act_erb(fmt);
   a.npad = round_up(rows, 16);
   a.n4 = s.n4;
   a.n6 = s.n6;

@@ -18,9 +18,12 @@ struct QuantArgs {
   int ties_away, full_clamp;
   uint8_t *mant;
   uint8_t *exp;
-  int64_t out_rb;          // packed activation row bytes (activations only)
-  int64_t out_erb;         // exponent row bytes (activations only)
+  int64_t out_rb;          // activation row stride (canonical + operand sections)
+  int64_t out_erb;         // exponent row stride
+  int64_t canon_rb;        // canonical packed section bytes per row
+  int64_t canon_erb;       // exponent section bytes per row
   int64_t row_used;        // unpadded packed bytes per row
+  int tail_pad;            // weights: zero bytes after the last slab
   int stage;               // stage source rows in LDS before the gather
   int vec16;               // 16-byte source loads are aligned
   int rows_per_wg;         // filled by the launcher
@@ -34,7 +37,9 @@ struct GemmArgs {
   float *y;                // [M][ldy] (gemm)
   int32_t *p;              // [M][N][nb] (partials)
   int64_t M, N, ldy;
-  int64_t a_rb, a_erb;     // activation row bytes / exponent row bytes
+  int64_t a_rb, a_erb;     // activation row stride / exponent row stride
+  int64_t a_op, a_ref;     // offsets of the operand image / reference exponents
+  int64_t w_erb;           // weight exponent row stride
   int64_t npad;            // N rounded up to 16
   int n4, n6, n8;
 };
@@ -50,7 +55,11 @@ struct UnpackArgs {
   int n4, n6, n8;
 };
 
+constexpr int64_t kMaxLds = 160 * 1024;   // LDS per workgroup on gfx950
+
 hipError_t launch_quantize(const QuantArgs &args, bool weights, hipStream_t s);
+int64_t quantize_act_lds(int stage, int rows_per_wg, int64_t K);
+int quantize_rows_per_wg(int64_t K);
 hipError_t launch_gemm_prefill(const GemmArgs &args, hipStream_t s);
 hipError_t launch_gemm_partials(const GemmArgs &args, hipStream_t s);
 hipError_t launch_gemm_decode(const GemmArgs &args, hipStream_t s);

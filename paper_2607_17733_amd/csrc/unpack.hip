@@ -69,7 +69,7 @@ __global__ __launch_bounds__(kThreads) void unpack_kernel(UnpackArgs a) {
     lo = *(const uint32_t *)(slab + w.lo);
     if (bi.m == 8) second = *(const uint32_t *)(slab + w.lo + 4);
     if (bi.m == 6) second = *(const uint32_t *)(slab + w.hi);
-    E = a.exp[(int64_t)b * a.npad + row];
+    E = a.exp[row * a.a_erb + b];
   }
   if (bi.m == 6 && (kg & 1)) second <<= 4;
   int8_t out[8];

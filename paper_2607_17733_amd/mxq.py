@@ -37,6 +37,7 @@ _SIGS = {
     "mxq_abi_version": (ctypes.c_int, []),
     "mxq_status_str": (ctypes.c_char_p, [ctypes.c_int]),
     "mxq_act_row_bytes": (_I64, [_P]),
+    "mxq_act_packed_bytes": (_I64, [_P]),
     "mxq_exp_row_bytes": (_I64, [_P]),
     "mxq_weight_bytes": (_I64, [_P, _I64]),
     "mxq_weight_exp_bytes": (_I64, [_P, _I64]),
@@ -117,6 +118,10 @@ class Format:
 
     def act_row_bytes(self) -> int:
         return _size(lib().mxq_act_row_bytes(self.ref), "mxq_act_row_bytes")
+
+    def act_packed_bytes(self) -> int:
+        """Bytes of the bit-packed section at the start of each activation row."""
+        return _size(lib().mxq_act_packed_bytes(self.ref), "mxq_act_packed_bytes")
 
     def exp_row_bytes(self) -> int:
         return _size(lib().mxq_exp_row_bytes(self.ref), "mxq_exp_row_bytes")

@@ -79,15 +79,61 @@ def check_y(Y, Yref, S, nb, what=""):
     return normwise
 
 
+def operand_order(widths):
+    """Position of each element of a row inside the operand image."""
+    pos = []
+    for b, m in enumerate(widths):
+        for t in range(BLOCK):
+            if m == 8:
+                pos.append(32 * b + t)
+            else:
+                pos.append(32 * b + 8 * (t // 8) + (t % 8) // 2 + 4 * (t % 2))
+    return np.array(pos)
+
+
+def check_operand_image(am, ae, qa, ea, widths, canon, erb):
+    """The quantizer's matrix-core operand image: every element equals
+    q * 2^(8 - m - (ref - E)) exactly, 0 <= ref - E <= 8 - m, and the
+    reference is shared over each 16-block chunk whose exponent spread fits
+    8 - m (else ref = E)."""
+    nb = len(widths)
+    K = nb * BLOCK
+    op = am[:, canon:canon + K].view(np.int8).astype(np.int64)
+    ref = ae[:, erb:erb + nb].astype(np.int64)
+    E = ea.astype(np.int64)
+    m = np.asarray(widths, dtype=np.int64)
+    sh = ref - E
+    assert np.all(sh >= 0) and np.all(sh <= 8 - m[None, :]), "reference out of range"
+    mult = np.repeat(8 - m[None, :] - sh, BLOCK, axis=1)
+    want = qa.astype(np.int64) * (1 << mult)
+    got = op[:, operand_order(widths)]
+    assert np.array_equal(got, want), "operand image differs"
+    # chunk rule
+    start = 0
+    for w in (4, 6, 8):
+        n = int((m == w).sum())
+        for c0 in range(0, n, 16):
+            sl = slice(start + c0, start + min(n, c0 + 16))
+            spread = E[:, sl].max(axis=1) - E[:, sl].min(axis=1)
+            shared = spread <= 8 - w
+            assert np.all(ref[shared, sl] == E[shared, sl].max(axis=1)[:, None])
+            assert np.all(ref[~shared, sl] == E[~shared, sl])
+        start += n
+    assert not ae[:, erb + nb:].any()
+
+
 def check_quant_act(case, out, qa, ea, fmt):
     am = out["a_mant"].cpu().numpy()
     ae = out["a_exp"].cpu().numpy()
     nb = case.K // BLOCK
+    canon = fmt.act_packed_bytes()
+    erb = fmt.exp_row_bytes() // 2
     ref_bytes = oracle.pack_act(qa, case.widths)
-    assert am.shape == ref_bytes.shape
-    assert np.array_equal(am, ref_bytes), "packed activation bytes differ"
+    assert am.shape == (case.M, canon + case.K) and ref_bytes.shape == (case.M, canon)
+    assert np.array_equal(am[:, :canon], ref_bytes), "packed activation bytes differ"
     assert np.array_equal(ae[:, :nb], ea), "activation exponents differ"
-    assert not ae[:, nb:].any()
+    assert not ae[:, nb:erb].any()
+    check_operand_image(am, ae, qa, ea, case.widths, canon, erb)
     q, e = mxq.unpack_act(out["a_mant"], out["a_exp"], fmt, case.M)
     assert np.array_equal(q.cpu().numpy(), qa) and np.array_equal(e.cpu().numpy(), ea)
 

@@ -50,20 +50,22 @@ def _fmt(K, widths, round_=0, clamp=0, block=32, reserved=0):
 def test_sizes(lib):
     f, _w = _fmt(256, [4] * 6 + [6, 8])
     assert lib.mxq_abi_version() == 1
-    assert lib.mxq_act_row_bytes(ctypes.byref(f)) == 160
-    assert lib.mxq_exp_row_bytes(ctypes.byref(f)) == 16
-    assert lib.mxq_weight_bytes(ctypes.byref(f), 256) == 256 * 152
-    assert lib.mxq_weight_bytes(ctypes.byref(f), 250) == 256 * 152
-    assert lib.mxq_weight_exp_bytes(ctypes.byref(f), 17) == 32 * 8
+    assert lib.mxq_act_packed_bytes(ctypes.byref(f)) == 160
+    assert lib.mxq_act_row_bytes(ctypes.byref(f)) == 160 + 256      # + operand image
+    assert lib.mxq_exp_row_bytes(ctypes.byref(f)) == 32             # exponents + refs
+    assert lib.mxq_weight_bytes(ctypes.byref(f), 256) == 256 * 152 + 64   # tail pad
+    assert lib.mxq_weight_bytes(ctypes.byref(f), 250) == 256 * 152 + 64
+    assert lib.mxq_weight_exp_bytes(ctypes.byref(f), 17) == 32 * 16
     f2, _w2 = _fmt(4096, [4] * 102 + [6] * 13 + [8] * 13)
-    assert lib.mxq_act_row_bytes(ctypes.byref(f2)) == 2368   # 2360 rounded up to 16
-    assert lib.mxq_exp_row_bytes(ctypes.byref(f2)) == 128
+    assert lib.mxq_act_packed_bytes(ctypes.byref(f2)) == 2368   # 2360 rounded up to 16
+    assert lib.mxq_act_row_bytes(ctypes.byref(f2)) == 2368 + 4096
+    assert lib.mxq_exp_row_bytes(ctypes.byref(f2)) == 256
 
 
 def test_size_functions_match_oracle_layout(lib, oracle_lib):
     for widths in ([4] * 3 + [6] * 1, [6] * 3, [8] * 5, [4] * 7 + [8]):
         f, _w = _fmt(32 * len(widths), widths)
-        assert lib.mxq_act_row_bytes(ctypes.byref(f)) == oracle_lib.act_row_bytes(widths)
+        assert lib.mxq_act_packed_bytes(ctypes.byref(f)) == oracle_lib.act_row_bytes(widths)
 
 
 @pytest.mark.parametrize("kwargs,status", [
