@@ -52,13 +52,23 @@ mxq_status check_fmt(const mxq_fmt *f, Segs *s) {
 }
 
 int64_t row_used(const Segs &s) { return 16LL * s.n4 + 24LL * s.n6 + 32LL * s.n8; }
-// canonical packed section and per-row exponent section
+// packed section and per-row exponent section
 int64_t canon_rb(const Segs &s) { return round_up(row_used(s), 16); }
 int64_t exp_rb(const mxq_fmt *f) { return round_up(f->K / MXQ_BLOCK, 16); }
-// activation rows: canonical section followed by the K-byte operand image;
-// activation exponent rows: exponents followed by reference exponents
-int64_t act_rb(const mxq_fmt *f, const Segs &s) { return canon_rb(s) + f->K; }
-int64_t act_erb(const mxq_fmt *f) { return 2 * exp_rb(f); }
+mxq::OpGeo op_geo(const Segs &s) { return mxq::OpGeo(s.n4, s.n6, s.n8); }
+// activation rows: packed section followed by the matrix-core operand image;
+// activation exponent rows: exponents followed by the per-step scale bytes
+int64_t act_rb(const mxq_fmt *, const Segs &s) {
+  return canon_rb(s) + op_geo(s).row_bytes + mxq::kActOpTail;
+}
+int64_t act_erb(const mxq_fmt *f, const Segs &s) {
+  return exp_rb(f) + round_up(4LL * op_geo(s).nsteps, 16);
+}
+// weights: packed slabs (N rounded to 16), tail padding, then the operand
+// image (N rounded to 128)
+int64_t w_packed(const Segs &s, int64_t N) { return round_up(N, 16) * row_used(s); }
+int64_t w_op_off(const Segs &s, int64_t N) { return w_packed(s, N) + kWeightTailPad; }
+int64_t w_tile(const Segs &s) { return mxq::op_tile_bytes(op_geo(s)); }
 
 mxq_status launched(hipError_t e) { return e == hipSuccess ? MXQ_OK : MXQ_ERR_DEVICE; }
 
@@ -76,7 +86,10 @@ mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows
   a.src = src;
   a.ld = ld;
   a.src_rows = rows;
-  a.out_rows = weights ? round_up(rows, 16) : rows;
+  a.out_rows = weights ? round_up(rows, mxq::kOpCols) : rows;
+  a.slab_rows = round_up(rows, 16);
+  a.w_op = weights ? w_op_off(s, rows) : 0;
+  a.w_tile = w_tile(s);
   a.K = fmt->K;
   a.perm = fmt->perm;
   a.n4 = s.n4;
@@ -89,7 +102,7 @@ mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows
   a.canon_rb = canon_rb(s);
   a.canon_erb = exp_rb(fmt);
   a.out_rb = weights ? 0 : act_rb(fmt, s);
-  a.out_erb = weights ? exp_rb(fmt) : act_erb(fmt);
+  a.out_erb = weights ? exp_rb(fmt) : act_erb(fmt, s);
   a.row_used = row_used(s);
   a.tail_pad = weights ? (int)kWeightTailPad : 0;
   a.vec16 = (ld % 8 == 0) ? 1 : 0;
@@ -125,10 +138,12 @@ mxq_status gemm_args(const mxq_fmt *fmt, int64_t M, int64_t N, const uint8_t *a_
   g->M = M;
   g->N = N;
   g->a_rb = act_rb(fmt, s);
-  g->a_erb = act_erb(fmt);
+  g->a_erb = act_erb(fmt, s);
   g->a_op = canon_rb(s);
-  g->a_ref = exp_rb(fmt);
+  g->a_sc = exp_rb(fmt);
   g->w_erb = exp_rb(fmt);
+  g->w_op = w_op_off(s, N);
+  g->w_tile = w_tile(s);
   g->npad = round_up(N, 16);
   g->n4 = s.n4;
   g->n6 = s.n6;
@@ -165,7 +180,7 @@ int64_t mxq_act_row_bytes(const mxq_fmt *fmt) {
 int64_t mxq_exp_row_bytes(const mxq_fmt *fmt) {
   Segs s;
   const mxq_status st = check_fmt(fmt, &s);
-  return st == MXQ_OK ? act_erb(fmt) : -(int64_t)st;
+  return st == MXQ_OK ? act_erb(fmt, s) : -(int64_t)st;
 }
 
 int64_t mxq_act_packed_bytes(const mxq_fmt *fmt) {
@@ -179,9 +194,7 @@ int64_t mxq_weight_bytes(const mxq_fmt *fmt, int64_t N) {
   const mxq_status st = check_fmt(fmt, &s);
   if (st != MXQ_OK) return -(int64_t)st;
   if (N < 0) return -(int64_t)MXQ_ERR_SHAPE;
-  // plus tail padding: the GEMM reads whole 16-byte words past the last
-  // lane's data of a slab
-  return round_up(N, 16) * row_used(s) + kWeightTailPad;
+  return w_op_off(s, N) + round_up(N, mxq::kOpCols) / mxq::kOpCols * w_tile(s);
 }
 
 int64_t mxq_weight_exp_bytes(const mxq_fmt *fmt, int64_t N) {
@@ -249,7 +262,7 @@ static mxq_status unpack_common(const mxq_fmt *fmt, int64_t rows, const uint8_t 
   a.rows = rows;
   a.K = fmt->K;
   a.a_rb = act_rb(fmt, s);
-  a.a_erb = weights ? exp_rb(fmt) : act_erb(fmt);
+  a.a_erb = weights ? exp_rb(fmt) : act_erb(fmt, s);
   a.npad = round_up(rows, 16);
   a.n4 = s.n4;
   a.n6 = s.n6;

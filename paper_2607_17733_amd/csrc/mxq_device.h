@@ -212,4 +212,108 @@ __device__ inline uint64_t load_w_operand(const uint8_t *slab, const Segs &s,
   return (uint64_t)p[0] | ((uint64_t)p[1] << 32);
 }
 
+// ---------------------------------------------------------------------------
+// Matrix-core operand layout for the block-scaled MFMA
+// (V_MFMA_SCALE_F32_32X32X64_F8F6F4).  That instruction multiplies FP6/FP8
+// elements and applies one E8M0 scale per 32-element K-block of each operand
+// in hardware.  An MXINT mantissa becomes one or two exactly representable
+// "digits" whose weights are folded into the element values, so the block's
+// E8M0 scale byte is the MXINT shared exponent E itself (MXSens Section 2:
+// value = q * 2^(E - 127 - (m - 2))):
+//   m = 4: one FP6 e3m2 element q/4;
+//   m = 6: h = floor(q / 8), l = q - 8h: FP6 e3m2 elements h/2 and l/16;
+//   m = 8: h = floor(q / 16), l = q - 16h: FP8 e4m3 elements h/4 and l/64.
+// The product of two 6-bit (8-bit) blocks is the sum of the four digit
+// products, computed by four (two) instructions over the same registers.
+//
+// K is walked in "steps", each one K-group of the instruction per lane half:
+//   4-bit: 4 blocks (two instructions, block pairs (4t, 4t+1), (4t+2, 4t+3));
+//   6-bit: a block pair, 8-bit: one block.
+// 4-bit blocks are padded to a multiple of 4 and 6-bit blocks to a multiple
+// of 2 with zero blocks.  Lane half h (lanes 32h..32h+31) of a step holds:
+//   4-bit step t: blocks 4t+h then 4t+2+h, 24 bytes each (48 bytes);
+//   6-bit pair p: block 2p+h as its h-digit plane then its l-digit plane
+//                 (24 bytes each);
+//   8-bit block:  h digits of elements 16h..16h+15, then their l digits
+//                 (32 bytes; weights repeat the h digits: 48 bytes).
+// FP6 elements are packed little-endian, element e of a block at bits 6e.
+// ---------------------------------------------------------------------------
+struct OpGeo {
+  int n4, n6, n8;
+  int n4p, n6p;          // padded segment lengths
+  int s4, s6, s8;        // steps per segment
+  int nsteps;
+  int64_t off6, off8;    // byte offsets of the 6- and 8-bit segments in a row
+  int64_t row_bytes;     // activation operand bytes per row
+  __host__ __device__ OpGeo(int a, int b, int c)
+      : n4(a), n6(b), n8(c), n4p((a + 3) & ~3), n6p((b + 1) & ~1), s4(n4p / 4),
+        s6(n6p / 2), s8(c), nsteps(s4 + s6 + c), off6(24LL * n4p),
+        off8(24LL * n4p + 48LL * n6p), row_bytes(24LL * n4p + 48LL * n6p + 64LL * c) {}
+  __host__ __device__ int seg(int st) const { return st < s4 ? 0 : (st < s4 + s6 ? 1 : 2); }
+  // Byte offset of lane half h's data of step st inside an activation row.
+  __host__ __device__ int64_t act_off(int st, int h) const {
+    if (st < s4) return 96LL * st + 48 * h;
+    if (st < s4 + s6) return off6 + 96LL * (st - s4) + 48 * h;
+    return off8 + 64LL * (st - s4 - s6) + 32 * h;
+  }
+};
+
+// Weight operand image: 128-column tiles, each a run of per-step chunks of
+// kOpChunk bytes; a chunk holds three 16-byte parts of every (half, column)
+// lane and the lane's scale dword (byte 0: first scale, byte 1: second scale
+// of a 4-bit step), laid out as the prefill GEMM keeps it in LDS:
+//   part j at j * 4096 + h * 2048 + c * 16, scales at 12288 + h * 512 + c * 4.
+constexpr int kOpCols = 128;
+constexpr int kActOpTail = 16;   // zero bytes after an activation operand row
+constexpr int kOpChunk = 13312;
+constexpr int kOpPart = 4096;
+
+__host__ __device__ inline int64_t op_tile_bytes(const OpGeo &o) {
+  return (int64_t)kOpChunk * o.nsteps;
+}
+
+// Location (relative to its tile) of byte `o` (0..47) of lane (h, c) of step st.
+__host__ __device__ inline int64_t w_op_loc(int st, int h, int c, int o) {
+  return (int64_t)kOpChunk * st + (o >> 4) * kOpPart + h * 2048 + c * 16 + (o & 15);
+}
+__host__ __device__ inline int64_t w_op_scale(int st, int h, int c) {
+  return (int64_t)kOpChunk * st + 3 * kOpPart + h * 512 + c * 4;
+}
+
+// FP6 e3m2 code of n/16 (|n| <= 32, n exactly representable).
+__host__ __device__ inline uint32_t e3m2_sixteenths(int n) {
+  const uint32_t a = (uint32_t)(n < 0 ? -n : n);
+  uint32_t mag = a;
+  if (a >= 4) {
+    const int e = 30 - __builtin_clz(a);      // floor(log2 a) - 1
+    mag = ((uint32_t)e << 2) | ((a >> (e - 1)) - 4u);
+  }
+  return (n < 0 ? 32u : 0u) | mag;
+}
+
+// FP8 e4m3 code of n/64 (|n| <= 128, n exactly representable).
+__host__ __device__ inline uint32_t e4m3_sixtyfourths(int n) {
+  const uint32_t a = (uint32_t)(n < 0 ? -n : n);
+  if (a == 0) return 0;
+  const int e = 32 - __builtin_clz(a);        // floor(log2 a) + 1
+  const uint32_t mant = ((a << 3) >> (e - 1)) - 8u;
+  return (n < 0 ? 128u : 0u) | ((uint32_t)e << 3) | mant;
+}
+
+// Digits of one mantissa: d0 (the only one for m = 4) and d1.
+__host__ __device__ inline void mxint_digits(int q, int m, uint32_t &d0, uint32_t &d1) {
+  if (m == 4) {
+    d0 = e3m2_sixteenths(4 * q);
+    d1 = 0;
+  } else if (m == 6) {
+    const int h = q >> 3;                     // arithmetic: floor(q / 8)
+    d0 = e3m2_sixteenths(8 * h);
+    d1 = e3m2_sixteenths(q - 8 * h);
+  } else {
+    const int h = q >> 4;
+    d0 = e4m3_sixtyfourths(16 * h);
+    d1 = e4m3_sixtyfourths(q - 16 * h);
+  }
+}
+
 }  // namespace mxq

@@ -18,11 +18,14 @@ struct QuantArgs {
   int ties_away, full_clamp;
   uint8_t *mant;
   uint8_t *exp;
-  int64_t out_rb;          // activation row stride (canonical + operand sections)
+  int64_t out_rb;          // activation row stride (packed + operand sections)
   int64_t out_erb;         // exponent row stride
-  int64_t canon_rb;        // canonical packed section bytes per row
-  int64_t canon_erb;       // exponent section bytes per row
+  int64_t canon_rb;        // packed section bytes per row
+  int64_t canon_erb;       // exponent section bytes per row (scale bytes follow)
   int64_t row_used;        // unpadded packed bytes per row
+  int64_t slab_rows;       // weights: columns in the packed slabs (N rounded to 16)
+  int64_t w_op;            // weights: offset of the operand image in the buffer
+  int64_t w_tile;          // weights: bytes per 128-column operand tile
   int tail_pad;            // weights: zero bytes after the last slab
   int stage;               // stage source rows in LDS before the gather
   int vec16;               // 16-byte source loads are aligned
@@ -38,8 +41,10 @@ struct GemmArgs {
   int32_t *p;              // [M][N][nb] (partials)
   int64_t M, N, ldy;
   int64_t a_rb, a_erb;     // activation row stride / exponent row stride
-  int64_t a_op, a_ref;     // offsets of the operand image / reference exponents
+  int64_t a_op, a_sc;      // offsets of the operand image / the scale bytes
   int64_t w_erb;           // weight exponent row stride
+  int64_t w_op;            // offset of the weight operand image in w_mant
+  int64_t w_tile;          // bytes per 128-column tile of that image
   int64_t npad;            // N rounded up to 16
   int n4, n6, n8;
 };

@@ -13,14 +13,11 @@
 // stages its source rows in LDS with 16-byte coalesced loads and gathers from
 // LDS, so the permutation never turns into scattered global loads.
 //
-// Activations additionally get a matrix-core operand image (second pass):
-// every mantissa unpacked to int8 and shifted to a per-(row, chunk) reference
-// exponent, so the prefill GEMM reads ready operands instead of unpacking the
-// same row once per column tile.  A chunk is up to 16 blocks of one width; its
-// blocks share the reference ref = max E when max E - min E <= 8 - m (the
-// spare top bits of the byte), else each block keeps ref = E.  The operand of
-// element q is q * 2^(8 - m - (ref - E)), exact, and the block's value is
-// operand * 2^(ref - 133).
+// Every row also gets its matrix-core operand image (FP6/FP8 digits of each
+// mantissa, the layout described with OpGeo) and the per-step E8M0 scale
+// bytes, so the prefill GEMM reads ready operands: activations right after
+// the packed section of the row, weights as 128-column tiles after the packed
+// slabs.
 #include "mxq_device.h"
 #include "mxq_internal.h"
 
@@ -29,14 +26,6 @@ namespace mxq {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kChunk = 16;
-
-// Arithmetic right shift of every byte of v by s in [0, 4] (low s bits of
-// every byte are zero).
-__device__ inline uint32_t sar8(uint32_t v, uint32_t s) {
-  const uint32_t S = v & 0x80808080u;
-  return (v >> s) | ((S - (S >> s)) << 1);
-}
 
 template <bool WEIGHTS>
 __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
@@ -48,12 +37,9 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
   const int R = q.rows_per_wg;
   const int64_t row0 = (int64_t)blockIdx.x * R;
   const Segs s{q.n4, q.n6, q.n8};
-  // LDS: [R][K] staged bf16 source (permuted path), then for activations
-  // [R][K] int8 mantissas, [R][nb] exponents, [R][nb] reference exponents.
+  // LDS: [R][K] staged bf16 source rows (permuted path only).
   uint16_t *srow = (uint16_t *)smem;
-  int8_t *qrow = (int8_t *)(smem + (q.stage ? (int64_t)R * K * 2 : 0));
-  uint8_t *erow = (uint8_t *)(qrow + (WEIGHTS ? 0 : (int64_t)R * K));
-  uint8_t *rrow = erow + (int64_t)R * nb;
+  const OpGeo og(q.n4, q.n6, q.n8);
 
   // Stage the workgroup's source rows in LDS (permuted path only).
   if (q.stage) {
@@ -151,6 +137,16 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
       lo8 |= ((uint32_t)qv[u] & 255u) << (8 * u);
       hi8 |= ((uint32_t)qv[4 + u] & 255u) << (8 * u);
     }
+    // digit codes of the 8 mantissas (MXINT -> FP6 / FP8 elements)
+    uint32_t d0[8], d1[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) mxint_digits(qv[u], bi.m, d0[u], d1[u]);
+    // step, lane half and (4-bit) pair of this block
+    int st, h, j = 0;
+    if (bi.m == 4) { st = bi.idx >> 2; h = bi.idx & 1; j = (bi.idx >> 1) & 1; }
+    else if (bi.m == 6) { st = og.s4 + (bi.idx >> 1); h = bi.idx & 1; }
+    else { st = og.s4 + og.s6 + bi.idx; h = kg >> 1; }
+
     if (!WEIGHTS) {
       uint8_t *dst = q.mant + row * q.out_rb + bi.aoff;
       if (bi.m == 4) {
@@ -161,92 +157,141 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
       } else {
         *(uint2 *)(dst + 8 * kg) = make_uint2(lo8, hi8);
       }
-      if (kg == 0) q.exp[row * q.out_erb + b] = (uint8_t)E;
+      uint8_t *erow_g = q.exp + row * q.out_erb;
+      if (kg == 0) erow_g[b] = (uint8_t)E;
+      // operand image
+      uint8_t *op = q.mant + row * q.out_rb + q.canon_rb;
+      if (bi.m == 8) {
+        uint32_t h0 = 0, h1 = 0, l0 = 0, l1 = 0;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          h0 |= d0[u] << (8 * u); h1 |= d0[4 + u] << (8 * u);
+          l0 |= d1[u] << (8 * u); l1 |= d1[4 + u] << (8 * u);
+        }
+        uint8_t *p = op + og.act_off(st, h) + 8 * (kg & 1);
+        *(uint2 *)p = make_uint2(h0, h1);
+        *(uint2 *)(p + 16) = make_uint2(l0, l1);
+      } else {
+        uint64_t v0 = 0, v1 = 0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          v0 |= (uint64_t)d0[u] << (6 * u);
+          v1 |= (uint64_t)d1[u] << (6 * u);
+        }
+        uint8_t *p = op + og.act_off(st, h) + (bi.m == 4 ? 24 * j : 0) + 6 * kg;
+#pragma unroll
+        for (int k = 0; k < 3; ++k) ((uint16_t *)p)[k] = (uint16_t)(v0 >> (16 * k));
+        if (bi.m == 6)
+#pragma unroll
+          for (int k = 0; k < 3; ++k) ((uint16_t *)(p + 24))[k] = (uint16_t)(v1 >> (16 * k));
+      }
+      // E8M0 scale bytes of the step: [step][half][2]
+      uint8_t *sc = erow_g + q.canon_erb + 4LL * st;
+      if (kg == 0) {
+        if (bi.m == 4) sc[2 * h + j] = (uint8_t)E;
+        else if (bi.m == 6) *(uint16_t *)(sc + 2 * h) = (uint16_t)E;
+        else *(uint32_t *)sc = (uint32_t)E | ((uint32_t)E << 16);
+      }
       if (g == 0) {                          // zero the row padding
         for (int64_t z = q.row_used; z < q.canon_rb; ++z)
           q.mant[row * q.out_rb + z] = 0;
-        for (int64_t z = nb; z < q.canon_erb; ++z) {
-          q.exp[row * q.out_erb + z] = 0;
-          q.exp[row * q.out_erb + q.canon_erb + z] = 0;
+        for (int64_t z = nb; z < q.canon_erb; ++z) erow_g[z] = 0;
+        for (int z = 0; z < kActOpTail; ++z) op[og.row_bytes + z] = 0;
+        for (int64_t z = 4LL * og.nsteps; z < q.out_erb - q.canon_erb; ++z)
+          erow_g[q.canon_erb + z] = 0;
+        for (int i = og.n4; i < og.n4p; ++i) {   // 4-bit pad blocks
+          const int pst = i >> 2, ph = i & 1, pj = (i >> 1) & 1;
+          uint8_t *pp = op + og.act_off(pst, ph) + 24 * pj;
+          for (int z = 0; z < 24; ++z) pp[z] = 0;
+          erow_g[q.canon_erb + 4LL * pst + 2 * ph + pj] = 0;
+        }
+        if (og.n6p > og.n6) {                  // 6-bit pad block (odd count)
+          const int pst = og.s4 + (og.n6 >> 1);
+          uint8_t *pp = op + og.act_off(pst, 1);
+          for (int z = 0; z < 48; ++z) pp[z] = 0;
+          *(uint16_t *)(erow_g + q.canon_erb + 4LL * pst + 2) = 0;
         }
       }
-      // keep the mantissas and the exponent for the operand pass
-      *(uint2 *)(qrow + (int64_t)lr * K + p0) = make_uint2(lo8, hi8);
-      if (kg == 0) erow[lr * nb + b] = (uint8_t)E;
     } else {
-      const int64_t slab = row >> 4;
-      const int c = (int)(row & 15);
-      uint8_t *base = q.mant + slab * slab_bytes(s);
-      const WLoc w = w_loc(s, bi, kg, c);
-      if (bi.m == 4) {
-        *(uint32_t *)(base + w.lo) = nib;
-      } else if (bi.m == 6) {
-        *(uint32_t *)(base + w.lo) = nib;
-        if (!(kg & 1)) *(uint32_t *)(base + w.hi) = top;
-      } else {
-        *(uint32_t *)(base + w.lo) = lo8;
-        *(uint32_t *)(base + w.lo + 4) = hi8;
+      const int c = (int)(row % kOpCols);
+      uint8_t *tile = q.mant + q.w_op + (row / kOpCols) * q.w_tile;
+      if (row < q.slab_rows) {
+        const int64_t slab = row >> 4;
+        uint8_t *base = q.mant + slab * slab_bytes(s);
+        const WLoc w = w_loc(s, bi, kg, (int)(row & 15));
+        if (bi.m == 4) {
+          *(uint32_t *)(base + w.lo) = nib;
+        } else if (bi.m == 6) {
+          *(uint32_t *)(base + w.lo) = nib;
+          if (!(kg & 1)) *(uint32_t *)(base + w.hi) = top;
+        } else {
+          *(uint32_t *)(base + w.lo) = lo8;
+          *(uint32_t *)(base + w.lo + 4) = hi8;
+        }
+        if (kg == 0) q.exp[row * q.out_erb + b] = (uint8_t)E;
+        if (g == 0)                          // zero the exponent row padding
+          for (int64_t z = nb; z < q.out_erb; ++z) q.exp[row * q.out_erb + z] = 0;
       }
-      if (kg == 0) q.exp[row * q.out_erb + b] = (uint8_t)E;
-      if (g == 0)                            // zero the exponent row padding
-        for (int64_t z = nb; z < q.out_erb; ++z) q.exp[row * q.out_erb + z] = 0;
-      if (row == 0 && g == 0)                // and the buffer's tail padding
+      if (row == 0 && g == 0)                // the packed section's tail padding
         for (int z = 0; z < q.tail_pad; ++z)
-          q.mant[(q.out_rows >> 4) * slab_bytes(s) + z] = 0;
-    }
-  }
-  if (WEIGHTS) return;
-
-  // ---- operand image: chunk references, then shifted int8 operands.
-  __syncthreads();
-  const int c4 = (q.n4 + kChunk - 1) / kChunk, c6 = (q.n6 + kChunk - 1) / kChunk;
-  const int nch = c4 + c6 + (q.n8 + kChunk - 1) / kChunk;
-  for (int f = t; f < R * nch; f += kThreads) {
-    const int lr = f / nch, c = f - lr * nch;
-    int b0, b1, H;
-    if (c < c4) { b0 = c * kChunk; b1 = min(q.n4, b0 + kChunk); H = 4; }
-    else if (c < c4 + c6) { b0 = q.n4 + (c - c4) * kChunk; b1 = min(q.n4 + q.n6, b0 + kChunk); H = 2; }
-    else { b0 = q.n4 + q.n6 + (c - c4 - c6) * kChunk; b1 = min(nb, b0 + kChunk); H = 0; }
-    int emin = 255, emax = 0;
-    for (int b = b0; b < b1; ++b) {
-      const int e = erow[lr * nb + b];
-      emin = min(emin, e);
-      emax = max(emax, e);
-    }
-    const bool shared = emax - emin <= H;
-    for (int b = b0; b < b1; ++b)
-      rrow[lr * nb + b] = (uint8_t)(shared ? emax : erow[lr * nb + b]);
-  }
-  __syncthreads();
-  for (int64_t f = t; f < (int64_t)R * G; f += kThreads) {
-    const int lr = (int)(f / G);
-    const int g = (int)(f - (int64_t)lr * G);
-    const int64_t row = row0 + lr;
-    if (row >= q.out_rows) continue;
-    const int b = g >> 2, kg = g & 3;
-    const BlockInfo bi = block_info(s, b);
-    const int E = erow[lr * nb + b], ref = rrow[lr * nb + b];
-    const uint32_t sh = (uint32_t)(ref - E);
-    const uint2 qq = *(const uint2 *)(qrow + (int64_t)lr * K + (int64_t)b * kBlock + 8 * kg);
-    uint32_t ev, od;
-    if (bi.m == 8) {
-      ev = qq.x;
-      od = qq.y;
-    } else {
-      // even / odd elements of the group, placed at the top of the byte
-      ev = __builtin_amdgcn_perm(qq.y, qq.x, 0x06040200u);
-      od = __builtin_amdgcn_perm(qq.y, qq.x, 0x07050301u);
-      if (bi.m == 4) {
-        ev = sar8((ev << 4) & 0xF0F0F0F0u, sh);
-        od = sar8((od << 4) & 0xF0F0F0F0u, sh);
+          q.mant[q.slab_rows / 16 * slab_bytes(s) + z] = 0;
+      // operand image (128-column tiles of per-step chunks)
+      if (bi.m == 8) {
+        uint32_t h0 = 0, h1 = 0, l0 = 0, l1 = 0;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          h0 |= d0[u] << (8 * u); h1 |= d0[4 + u] << (8 * u);
+          l0 |= d1[u] << (8 * u); l1 |= d1[4 + u] << (8 * u);
+        }
+        const int o = 8 * (kg & 1);
+        *(uint2 *)(tile + w_op_loc(st, h, c, o)) = make_uint2(h0, h1);
+        *(uint2 *)(tile + w_op_loc(st, h, c, 16 + o)) = make_uint2(l0, l1);
+        *(uint2 *)(tile + w_op_loc(st, h, c, 32 + o)) = make_uint2(h0, h1);
       } else {
-        ev = sar8((ev << 2) & 0xFCFCFCFCu, sh);
-        od = sar8((od << 2) & 0xFCFCFCFCu, sh);
+        uint64_t v0 = 0, v1 = 0;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          v0 |= (uint64_t)d0[u] << (6 * u);
+          v1 |= (uint64_t)d1[u] << (6 * u);
+        }
+        const int o = (bi.m == 4 ? 24 * j : 0) + 6 * kg;
+#pragma unroll
+        for (int k = 0; k < 3; ++k)
+          *(uint16_t *)(tile + w_op_loc(st, h, c, o + 2 * k)) = (uint16_t)(v0 >> (16 * k));
+        if (bi.m == 6)
+#pragma unroll
+          for (int k = 0; k < 3; ++k)
+            *(uint16_t *)(tile + w_op_loc(st, h, c, 24 + o + 2 * k)) = (uint16_t)(v1 >> (16 * k));
+      }
+      if (kg == 0) {                         // scale dword of the lane: bytes su0, su1, 0, 0
+        if (bi.m == 4) {
+          uint8_t *sp = tile + w_op_scale(st, h, c);
+          sp[j] = (uint8_t)E;
+          if (j == 0) *(uint16_t *)(sp + 2) = 0;
+        } else if (bi.m == 6) {
+          *(uint32_t *)(tile + w_op_scale(st, h, c)) = (uint32_t)E;
+        } else {
+          *(uint32_t *)(tile + w_op_scale(st, 0, c)) = (uint32_t)E;
+          *(uint32_t *)(tile + w_op_scale(st, 1, c)) = (uint32_t)E;
+        }
+      }
+      if (g == 0) {                          // zero the pad blocks of the column
+        for (int i = og.n4; i < og.n4p; ++i) {
+          const int pst = i >> 2, ph = i & 1, pj = (i >> 1) & 1;
+          for (int z = 0; z < 24; z += 2)
+            *(uint16_t *)(tile + w_op_loc(pst, ph, c, 24 * pj + z)) = 0;
+          uint8_t *sp = tile + w_op_scale(pst, ph, c);
+          sp[pj] = 0;
+          if (pj == 0) *(uint16_t *)(sp + 2) = 0;
+        }
+        if (og.n6p > og.n6) {
+          const int pst = og.s4 + (og.n6 >> 1);
+          for (int z = 0; z < 48; z += 2)
+            *(uint16_t *)(tile + w_op_loc(pst, 1, c, z)) = 0;
+          *(uint32_t *)(tile + w_op_scale(pst, 1, c)) = 0;
+        }
       }
     }
-    *(uint2 *)(q.mant + row * q.out_rb + q.canon_rb + (int64_t)b * kBlock + 8 * kg) =
-        make_uint2(ev, od);
-    if (kg == 0) q.exp[row * q.out_erb + q.canon_erb + b] = (uint8_t)ref;
   }
 }
 
@@ -281,7 +326,8 @@ hipError_t launch_quantize(const QuantArgs &args, bool weights,
 
 int64_t quantize_act_lds(int stage, int rows_per_wg, int64_t K) {
   const int64_t nb = K / kBlock;
-  return (int64_t)rows_per_wg * ((stage ? 2 * K : 0) + K + 2 * nb);
+  (void)nb;
+  return stage ? (int64_t)rows_per_wg * 2 * K : 0;
 }
 
 int quantize_rows_per_wg(int64_t K) {

@@ -8,6 +8,7 @@ import numpy as np
 import torch
 
 import oracle
+from operand_decode import CHUNK, TILE_COLS, Geo, decode_act, decode_weights
 from paper_2607_17733_amd import mxq
 from paper_2607_17733_amd.workloads import LinearCase
 
@@ -55,71 +56,65 @@ def gpu_run(case: LinearCase, fmt, want_partials=False, M=None):
     return out
 
 
-def check_y(Y, Yref, S, nb, what=""):
-    """The GEMM tolerance: relative error 1e-5 against the fp64 oracle,
-    normwise and elementwise (with a small absolute floor for outputs that
-    cancel), plus a hard bound from fp32 summation of the block terms."""
+def digit_absbound(qa, ea, qw, ew, widths, rows=None, cols=None):
+    """T[i, j] = sum_k (|qa|+c)(|qw|+c) 2^(Ea+Ew-254-2(m-2)), an upper bound of
+    the sum of |digit products| the matrix core accumulates for Y[i, j]: an
+    m-bit mantissa q splits into digits with |8h| + |l| <= |q| + 14 (m = 6)
+    and |16h| + |l| <= |q| + 30 (m = 8); 4-bit mantissas are not split."""
+    wb = np.asarray(widths)
+    c = np.repeat(np.select([wb == 4, wb == 6], [0, 14], 30), BLOCK).astype(np.float64)
+    off = 127 + (wb - 2)
+    rows = np.arange(qa.shape[0]) if rows is None else np.asarray(rows)
+    cols = np.arange(qw.shape[0]) if cols is None else np.asarray(cols)
+    sa = np.repeat(np.clip(ea[rows].astype(np.float64), 0, 254) - off, BLOCK, axis=1)
+    sw = np.repeat(np.clip(ew[cols].astype(np.float64), 0, 254) - off, BLOCK, axis=1)
+    A = (np.abs(qa[rows].astype(np.float64)) + c) * np.exp2(sa)
+    Wm = (np.abs(qw[cols].astype(np.float64)) + c) * np.exp2(sw)
+    return A @ Wm.T
+
+
+def mma_steps(widths):
+    """Matrix-core instructions accumulated into each output by the prefill
+    GEMM: two per 4-bit step, four per 6-bit pair, two per 8-bit block."""
+    g = Geo(widths)
+    return 2 * g.s4 + 4 * g.s6 + 2 * g.s8
+
+
+def check_y(Y, Yref, S, nb, what="", T=None, steps=0):
+    """The GEMM tolerance: relative error 1e-5 (normwise) against the fp64
+    oracle, and elementwise a bound derived from the arithmetic:
+      - decode path (exact int32 block sums, one fp32 rescale-add each):
+        (nb + 2) 2^-24 S with S = sum_b |P_b| 2^(sa+sw);
+      - prefill path (exact digit products, fp32 accumulation inside each
+        matrix-core instruction): 2 * steps * 2^-24 * T, T from
+        digit_absbound, i.e. at most two roundings of the running absolute
+        sum per instruction;
+    plus nb 2^-126 for terms below fp32's normal range."""
     Y = Y.astype(np.float64)
     assert Y.shape == Yref.shape
     nan_ref = np.isnan(Yref)
     assert np.array_equal(np.isnan(Y), nan_ref), what + ": NaN pattern differs"
-    Y, Yref, S = Y[~nan_ref], Yref[~nan_ref], S[~nan_ref]
+    keep = ~nan_ref
+    Y, Yref, S = Y[keep], Yref[keep], S[keep]
     if Yref.size == 0:
         return
     err = np.abs(Y - Yref)
-    ref_inf = np.abs(Yref).max()
     normwise = np.linalg.norm(Y - Yref) / max(np.linalg.norm(Yref), 1e-300)
     assert normwise <= 1e-5, "%s: normwise %.3g" % (what, normwise)
-    assert np.all(err <= 1e-5 * np.abs(Yref) + 1e-7 * ref_inf), \
-        "%s: elementwise max rel %.3g" % (what, (err / np.maximum(np.abs(Yref), 1e-300)).max())
-    # fp32 accumulation of nb exact block terms, any order; 2^-126 covers
-    # terms below fp32's normal range
     bound = (nb + 2) * 2.0 ** -24 * S + nb * 2.0 ** -126
-    assert np.all(err <= bound), "%s: exceeds fp32 summation bound" % what
+    if T is not None:
+        bound = np.maximum(bound, 2 * steps * 2.0 ** -24 * T[keep] + nb * 2.0 ** -126)
+    worst = (err / bound).max()
+    assert np.all(err <= bound), "%s: exceeds the accumulation bound (x%.3g)" % (what, worst)
     return normwise
 
 
-def operand_order(widths):
-    """Position of each element of a row inside the operand image."""
-    pos = []
-    for b, m in enumerate(widths):
-        for t in range(BLOCK):
-            if m == 8:
-                pos.append(32 * b + t)
-            else:
-                pos.append(32 * b + 8 * (t // 8) + (t % 8) // 2 + 4 * (t % 2))
-    return np.array(pos)
-
-
-def check_operand_image(am, ae, qa, ea, widths, canon, erb):
-    """The quantizer's matrix-core operand image: every element equals
-    q * 2^(8 - m - (ref - E)) exactly, 0 <= ref - E <= 8 - m, and the
-    reference is shared over each 16-block chunk whose exponent spread fits
-    8 - m (else ref = E)."""
-    nb = len(widths)
-    K = nb * BLOCK
-    op = am[:, canon:canon + K].view(np.int8).astype(np.int64)
-    ref = ae[:, erb:erb + nb].astype(np.int64)
-    E = ea.astype(np.int64)
-    m = np.asarray(widths, dtype=np.int64)
-    sh = ref - E
-    assert np.all(sh >= 0) and np.all(sh <= 8 - m[None, :]), "reference out of range"
-    mult = np.repeat(8 - m[None, :] - sh, BLOCK, axis=1)
-    want = qa.astype(np.int64) * (1 << mult)
-    got = op[:, operand_order(widths)]
-    assert np.array_equal(got, want), "operand image differs"
-    # chunk rule
-    start = 0
-    for w in (4, 6, 8):
-        n = int((m == w).sum())
-        for c0 in range(0, n, 16):
-            sl = slice(start + c0, start + min(n, c0 + 16))
-            spread = E[:, sl].max(axis=1) - E[:, sl].min(axis=1)
-            shared = spread <= 8 - w
-            assert np.all(ref[shared, sl] == E[shared, sl].max(axis=1)[:, None])
-            assert np.all(ref[~shared, sl] == E[~shared, sl])
-        start += n
-    assert not ae[:, erb + nb:].any()
+def check_gemm(Y, Yref, qa, ea, qw, ew, widths, what, rows=None, cols=None):
+    """check_y with both accumulation bounds computed from the oracle's
+    mantissas and exponents."""
+    S = oracle.gemm_absbound(qa, ea, qw, ew, widths, rows=rows, cols=cols)
+    T = digit_absbound(qa, ea, qw, ew, widths, rows=rows, cols=cols)
+    return check_y(Y, Yref, S, len(widths), what, T=T, steps=mma_steps(widths))
 
 
 def check_quant_act(case, out, qa, ea, fmt):
@@ -127,18 +122,30 @@ def check_quant_act(case, out, qa, ea, fmt):
     ae = out["a_exp"].cpu().numpy()
     nb = case.K // BLOCK
     canon = fmt.act_packed_bytes()
-    erb = fmt.exp_row_bytes() // 2
+    cerb = -(-nb // 16) * 16
     ref_bytes = oracle.pack_act(qa, case.widths)
-    assert am.shape == (case.M, canon + case.K) and ref_bytes.shape == (case.M, canon)
+    assert am.shape == (case.M, fmt.act_row_bytes()) and ref_bytes.shape == (case.M, canon)
     assert np.array_equal(am[:, :canon], ref_bytes), "packed activation bytes differ"
     assert np.array_equal(ae[:, :nb], ea), "activation exponents differ"
-    assert not ae[:, nb:erb].any()
-    check_operand_image(am, ae, qa, ea, case.widths, canon, erb)
-    q, e = mxq.unpack_act(out["a_mant"], out["a_exp"], fmt, case.M)
-    assert np.array_equal(q.cpu().numpy(), qa) and np.array_equal(e.cpu().numpy(), ea)
+    assert not ae[:, nb:cerb].any()
+    q, E, pad_ok = decode_act(am[:, canon:], ae[:, cerb:], case.widths)
+    assert np.array_equal(q, qa), "activation operand image differs from the mantissas"
+    assert np.array_equal(E, ea.astype(np.int64)), "activation scale bytes differ"
+    assert pad_ok, "activation operand padding not zero"
+    qd, ed = mxq.unpack_act(out["a_mant"], out["a_exp"], fmt, case.M)
+    assert np.array_equal(qd.cpu().numpy(), qa) and np.array_equal(ed.cpu().numpy(), ea)
 
 
 def check_pack_w(case, out, qw, ew, fmt):
-    q, e = mxq.unpack_weights(out["w_mant"], out["w_exp"], fmt, case.N)
+    N = qw.shape[0]
+    q, e = mxq.unpack_weights(out["w_mant"], out["w_exp"], fmt, N)
     assert np.array_equal(q.cpu().numpy(), qw), "weight mantissas differ"
     assert np.array_equal(e.cpu().numpy(), ew), "weight exponents differ"
+    wm = out["w_mant"].cpu().numpy()
+    g = Geo(case.widths)
+    size = -(-N // TILE_COLS) * CHUNK * g.nsteps
+    qo, eo, ok = decode_weights(wm[wm.size - size:], case.widths, N)
+    assert ok, "weight operand image layout / padding"
+    assert np.array_equal(qo[:N], qw), "weight operand image differs from the mantissas"
+    assert np.array_equal(eo[:N], ew.astype(np.int64)), "weight scale bytes differ"
+    assert not qo[N:].any() and not eo[N:].any(), "padding columns not zero"

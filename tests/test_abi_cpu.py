@@ -47,19 +47,34 @@ def _fmt(K, widths, round_=0, clamp=0, block=32, reserved=0):
     return f, w
 
 
+def op_layout(widths):
+    """Operand-image geometry as include/mxq.h states it: 4-bit blocks padded
+    to a multiple of 4 (24 bytes each), 6-bit to a multiple of 2 (48 bytes
+    each), 8-bit 64 bytes each; steps = n4p/4 + n6p/2 + n8."""
+    n4, n6, n8 = (sum(1 for w in widths if w == m) for m in (4, 6, 8))
+    n4p, n6p = -(-n4 // 4) * 4, -(-n6 // 2) * 2
+    return 24 * n4p + 48 * n6p + 64 * n8, n4p // 4 + n6p // 2 + n8
+
+
 def test_sizes(lib):
     f, _w = _fmt(256, [4] * 6 + [6, 8])
     assert lib.mxq_abi_version() == 1
+    assert op_layout([4] * 6 + [6, 8]) == (352, 4)
     assert lib.mxq_act_packed_bytes(ctypes.byref(f)) == 160
-    assert lib.mxq_act_row_bytes(ctypes.byref(f)) == 160 + 256      # + operand image
-    assert lib.mxq_exp_row_bytes(ctypes.byref(f)) == 32             # exponents + refs
-    assert lib.mxq_weight_bytes(ctypes.byref(f), 256) == 256 * 152 + 64   # tail pad
-    assert lib.mxq_weight_bytes(ctypes.byref(f), 250) == 256 * 152 + 64
+    assert lib.mxq_act_row_bytes(ctypes.byref(f)) == 160 + 352 + 16  # + operand image + tail
+    assert lib.mxq_exp_row_bytes(ctypes.byref(f)) == 16 + 16         # exponents + scale bytes
+    # packed slabs (N to 16) + 64-byte tail + 128-column operand tiles of
+    # 13312 bytes per step
+    assert lib.mxq_weight_bytes(ctypes.byref(f), 256) == 256 * 152 + 64 + 2 * 4 * 13312
+    assert lib.mxq_weight_bytes(ctypes.byref(f), 250) == 256 * 152 + 64 + 2 * 4 * 13312
+    assert lib.mxq_weight_bytes(ctypes.byref(f), 129) == 144 * 152 + 64 + 2 * 4 * 13312
     assert lib.mxq_weight_exp_bytes(ctypes.byref(f), 17) == 32 * 16
-    f2, _w2 = _fmt(4096, [4] * 102 + [6] * 13 + [8] * 13)
+    w2 = [4] * 102 + [6] * 13 + [8] * 13
+    f2, _w2 = _fmt(4096, w2)
+    assert op_layout(w2) == (4000, 46)
     assert lib.mxq_act_packed_bytes(ctypes.byref(f2)) == 2368   # 2360 rounded up to 16
-    assert lib.mxq_act_row_bytes(ctypes.byref(f2)) == 2368 + 4096
-    assert lib.mxq_exp_row_bytes(ctypes.byref(f2)) == 256
+    assert lib.mxq_act_row_bytes(ctypes.byref(f2)) == 2368 + 4000 + 16
+    assert lib.mxq_exp_row_bytes(ctypes.byref(f2)) == 128 + 192  # 4 * 46 = 184 -> 192
 
 
 def test_size_functions_match_oracle_layout(lib, oracle_lib):

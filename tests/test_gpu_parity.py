@@ -1,9 +1,10 @@
 """GPU parity: the HIP path (through the C ABI) against the CPU oracle.
 
-Bit-exact: packed activation bytes, exponents, unpacked weight mantissas and
-exponents, and the per-block int32 sums.  GEMM outputs: relative error 1e-5
-against the fp64 oracle (normwise and elementwise) plus the fp32 summation
-bound.  Small shapes span several tiles and ragged tails; the workload
+Bit-exact: packed activation bytes, exponents, the matrix-core operand
+images of both operands (decoded on the host back to mantissas and scale
+bytes), unpacked weight mantissas and exponents, and the per-block int32
+sums.  GEMM outputs: relative error 1e-5 (normwise) against the fp64 oracle
+and, elementwise, the accumulation bound of the path that ran.  Small shapes span several tiles and ragged tails; the workload
 shapes run at full size with sampled GEMM outputs.
 """
 import numpy as np
@@ -13,7 +14,7 @@ import torch
 import oracle
 from paper_2607_17733_amd import mxq
 from paper_2607_17733_amd import workloads as W
-from parity_util import (check_pack_w, check_quant_act, check_y, fmt_for,
+from parity_util import (check_gemm, check_pack_w, check_quant_act, fmt_for,
                          gpu_run, oracle_quant, say, to_dev_bf16)
 
 pytestmark = pytest.mark.gpu
@@ -30,8 +31,7 @@ def _full_check(case, round_="rne", clamp="sym", identity=False, partials=True):
         P = oracle.block_partials(qa, qw)
         assert np.array_equal(out["p"].cpu().numpy(), P), "block partial sums differ"
     Yref = oracle.gemm(qa, ea, qw, ew, case.widths)
-    S = oracle.gemm_absbound(qa, ea, qw, ew, case.widths)
-    check_y(out["y"].cpu().numpy(), Yref, S, case.K // 32, case.name)
+    check_gemm(out["y"].cpu().numpy(), Yref, qa, ea, qw, ew, case.widths, case.name)
 
 
 def test_tiny_config():
@@ -106,9 +106,8 @@ def test_strided_inputs_and_outputs():
     assert np.array_equal(am.cpu().numpy()[:, :fmt.act_packed_bytes()],
                           oracle.pack_act(qa, case.widths))
     Yref = oracle.gemm(qa, ea, qw, ew, case.widths)
-    S = oracle.gemm_absbound(qa, ea, qw, ew, case.widths)
     yb = y_big.cpu().numpy()
-    check_y(yb[:, :40], Yref, S, 8, "strided")
+    check_gemm(yb[:, :40], Yref, qa, ea, qw, ew, case.widths, "strided")
     assert np.all(yb[:, 40:] == 7.0)          # nothing outside N written
 
 
@@ -159,9 +158,8 @@ def _sampled_check(case, n_rows=12, n_cols=384, seed=0):
     cols = np.unique(np.concatenate([[0, case.N - 1],
                                      g.choice(case.N, min(n_cols, case.N), replace=False)]))
     Yref = oracle.gemm(qa, ea, qw, ew, case.widths, rows=rows, cols=cols)
-    S = oracle.gemm_absbound(qa, ea, qw, ew, case.widths, rows=rows, cols=cols)
     Y = out["y"].cpu().numpy()[np.ix_(rows, cols)]
-    return check_y(Y, Yref, S, case.K // 32, case.name)
+    return check_gemm(Y, Yref, qa, ea, qw, ew, case.widths, case.name, rows=rows, cols=cols)
 
 
 def test_attn_proj_full():
@@ -197,8 +195,8 @@ def test_decode_full(which):
         torch.cuda.synchronize()
         qa, ea = oracle.quantize(a_bits, perm=base.perm, widths=base.widths)
         Yref = oracle.gemm(qa, ea, qw, ew, base.widths, cols=cols)
-        S = oracle.gemm_absbound(qa, ea, qw, ew, base.widths, cols=cols)
-        check_y(y.cpu().numpy()[:, cols], Yref, S, base.K // 32, "decode M=%d" % M)
+        check_gemm(y.cpu().numpy()[:, cols], Yref, qa, ea, qw, ew, base.widths,
+                   "decode M=%d" % M, cols=cols)
 
 
 def test_kv_cache_quantize():
