@@ -23,11 +23,14 @@
  *   [-2^(m-1), 2^(m-1)-1].
  *   A block whose maximum is zero or subnormal has E = 0 (e clamps to
  *   -127); a block holding Inf or NaN has E = 255 and zero mantissas.
- * GEMM: Y[i][j] = sum_b P[i][j][b] * 2^(sa[i][b] + sw[j][b]) where
- *   P[i][j][b] = sum_t qa[i][32b+t] * qw[j][32b+t] is computed exactly in
- *   int32 on int8 matrix cores, and Y is accumulated in fp32.  Any block with
- *   E == 255 on either side makes the outputs it touches NaN.  Results whose
- *   magnitude is below fp32's range (2^-149) flush towards zero.
+ * GEMM: Y[i][j] = sum_b P[i][j][b] * 2^(sa[i][b] + sw[j][b]) with
+ *   P[i][j][b] = sum_t qa[i][32b+t] * qw[j][32b+t] and s = E - 127 - (m - 2),
+ *   accumulated in fp32.  Every elementary product is exact; the prefill
+ *   kernel sums them on the block-scaled matrix cores (each block's E is the
+ *   hardware scale), the decode kernel forms each P exactly in int32 and
+ *   adds it scaled in fp32.  Any block with E == 255 on either side makes
+ *   the outputs it touches NaN.  Results whose magnitude is below fp32's
+ *   range (2^-149) flush towards zero.
  *
  * Conventions for every entry point:
  *   - All functions are thread-safe and reentrant.  Device work is enqueued
@@ -52,7 +55,7 @@
 extern "C" {
 #endif
 
-#define MXQ_ABI_VERSION 1
+#define MXQ_ABI_VERSION 2
 #define MXQ_BLOCK 32
 /* mxq_gemm uses the weight-streaming decode kernel for M <= this. */
 #define MXQ_DECODE_MAX_M 16
@@ -96,46 +99,67 @@ int mxq_abi_version(void);
 const char *mxq_status_str(int status);
 
 /*
- * Sizes (bytes) of the packed buffers; negative mxq_status on a bad format.
+ * Sizes (bytes) of the buffers; negative mxq_status on a bad format or a
+ * negative count.
  *
- * Activations (the output of mxq_quantize_act):
- *   a_mant row r starts at r * mxq_act_row_bytes(fmt) and holds two sections.
- *   (1) The bit-packed mantissas, mxq_act_packed_bytes(fmt) bytes: the blocks
- *   in permuted order, block b taking 4 * m_b bytes, padded with zero bytes
- *   to a multiple of 16:
+ * Activations (the output of mxq_quantize_act for M rows):
+ *   a_mant: M packed rows of mxq_act_packed_bytes(fmt) bytes each, then the
+ *   matrix-core operand image; mxq_act_bytes(fmt, M) in total.
+ *   (1) Packed row: the blocks in permuted order, block b taking 4 * m_b
+ *   bytes, zero padded to a multiple of 16:
  *     4-bit: byte j holds element 2j in bits 0-3 and element 2j+1 in bits 4-7;
  *     6-bit: 16 bytes of low nibbles in the 4-bit layout, then two 32-bit
  *            words of the signed top two bits: word d covers elements
  *            16d..16d+15, its byte j holds element 16d+2j in bits 6-7,
  *            16d+2j+1 in bits 4-5, 16d+8+2j in bits 2-3, 16d+9+2j in bits 0-1;
  *     8-bit: one two's-complement byte per element.
- *   (2) The matrix-core operand image, K bytes: the same mantissas unpacked
- *   to int8 and aligned to a reference exponent ref >= E per block, so that
- *   block b of the row equals operand * 2^(ref - 133).  Element t of block b
- *   is at byte 32b + 8(t/8) + (t%8)/2 + 4(t%2) for 4- and 6-bit blocks (the
- *   even elements of each group of eight, then the odd ones) and at 32b + t
- *   for 8-bit blocks; its value is q * 2^(8 - m - (ref - E)).  Within every
- *   chunk of 16 consecutive blocks of one width (counted from the start of
- *   the width's blocks) ref = max E of the chunk when max E - min E <= 8 - m,
- *   else ref = E.  The GEMM reads only this section; the decode GEMM and
- *   mxq_unpack_act read section (1).
- *   a_exp row r starts at r * mxq_exp_row_bytes(fmt): exponent_row bytes of
- *   block exponents E (byte b for block b, zero padded to a multiple of 16),
- *   then as many bytes of reference exponents ref.
- * Here exponent_row = K/32 rounded up to a multiple of 16, and
- * mxq_exp_row_bytes(fmt) = 2 * exponent_row.
- * Packed weights (mxq_pack_weights) use a GEMM-tiled layout: columns are
- * grouped in slabs of 16 (N rounded up; padding columns are zero), each slab
- * holds its blocks grouped by four within each width segment, interleaved in
- * matrix-core operand order.  The weight exponents are one row of
- * exponent_row bytes per (padded) column: w_exp[j * exponent_row + b].
- * The mantissa layout is opaque (mxq_weight_bytes includes 64 bytes of tail
- * padding that the GEMM may read but never uses): use mxq_unpack_weights to
- * read it back in canonical form.
+ *   (2) Operand image: every mantissa q of a block with width m as exact
+ *   FP6 / FP8 "digits" whose sum is q * 2^-(m - 2), so that the block's
+ *   E8M0 scale is E itself:
+ *     m = 4: one FP6 e3m2 element q/4;
+ *     m = 6: h = floor(q/8), l = q - 8h; FP6 e3m2 elements h/2 and l/16;
+ *     m = 8: h = floor(q/16), l = q - 16h; FP8 e4m3 elements h/4 and l/64.
+ *   K is walked in steps: the 4-bit blocks (padded with zero blocks to a
+ *   multiple of 4) four at a time, the 6-bit blocks (padded to a multiple of
+ *   2) two at a time, the 8-bit blocks one at a time; nsteps is the total.
+ *   Step s gives each row two halves h = 0, 1 of 48 bytes ("lane data"):
+ *     4-bit step: blocks 4s'+h then 4s'+2+h (s' = index within the
+ *       segment), each as 32 e3m2 codes packed little-endian (element t at
+ *       bits 6t of the 24 bytes);
+ *     6-bit step: block 2s'+h as its h-digit codes, then its l-digit codes;
+ *     8-bit step: the h codes of elements 16h..16h+15 (16 bytes), their l
+ *       codes (16 bytes), 16 zero bytes.
+ *   Rows are grouped in tiles of 32 (the last tile is padded; its rows past
+ *   M are unspecified).  Byte o of the lane data of (row r, step s, half h)
+ *   is at ((r / 32) * nsteps + s) * 3072 + (o / 16) * 1024 + h * 512
+ *   + (r % 32) * 16 + o % 16 of the operand image.
+ *   a_exp: M rows of mxq_exp_row_bytes(fmt) bytes (block exponents E, byte b
+ *   for block b, zero padded to a multiple of 16), then the operand image's
+ *   scale bytes: for (row r, step s, half h) two bytes at
+ *   ((r / 32) * nsteps + s) * 128 + h * 64 + (r % 32) * 2: the E of block
+ *   4s'+h and of block 4s'+2+h for a 4-bit step, the E of the half's block
+ *   and 0 for a 6-bit step, the block's E and 0 (both halves) for an 8-bit
+ *   step; zero for padding blocks.  mxq_act_exp_bytes(fmt, M) in total.
+ *   The prefill GEMM reads the operand image; the decode GEMM,
+ *   mxq_gemm_partials and mxq_unpack_act read the packed rows.
+ * Weights (mxq_pack_weights for N columns), mxq_weight_bytes(fmt, N):
+ *   (1) packed slabs: columns in slabs of 16 (N rounded up; padding columns
+ *   are zero), each slab holding its blocks grouped by four within each width
+ *   segment, interleaved in matrix-core operand order (opaque: read it back
+ *   with mxq_unpack_weights); 64 zero bytes follow;
+ *   (2) the operand image, tiled by 128 columns (N rounded up; padding
+ *   columns are zero): per tile, per step, 13312 bytes: lane data byte o of
+ *   (column c of the tile, half h) at (o / 16) * 4096 + h * 2048 + c * 16
+ *   + o % 16, then the lane's scale bytes (the two of the activation layout,
+ *   then two zero bytes) at 12288 + h * 512 + c * 4.  Weight lane data of an
+ *   8-bit step repeats the h codes in its last 16 bytes.
+ *   The weight exponents are one row of mxq_exp_row_bytes(fmt) bytes per
+ *   (padded to 16) column: w_exp[j * mxq_exp_row_bytes + b].
  */
-int64_t mxq_act_row_bytes(const mxq_fmt *fmt);
 int64_t mxq_act_packed_bytes(const mxq_fmt *fmt);
 int64_t mxq_exp_row_bytes(const mxq_fmt *fmt);
+int64_t mxq_act_bytes(const mxq_fmt *fmt, int64_t M);
+int64_t mxq_act_exp_bytes(const mxq_fmt *fmt, int64_t M);
 int64_t mxq_weight_bytes(const mxq_fmt *fmt, int64_t N);
 int64_t mxq_weight_exp_bytes(const mxq_fmt *fmt, int64_t N);
 
@@ -143,8 +167,8 @@ int64_t mxq_weight_exp_bytes(const mxq_fmt *fmt, int64_t N);
  * Online activation quantization (paper: Section 5, activations of every
  * decoder linear and the KV cache are quantized to MXINT; Section 4.1 widths).
  *   a       DEVICE bf16 [M][lda], lda >= K, read only.
- *   a_mant  DEVICE uint8 [M][mxq_act_row_bytes], written (canonical layout).
- *   a_exp   DEVICE uint8 [M][mxq_exp_row_bytes], written.
+ *   a_mant  DEVICE uint8 [mxq_act_bytes(fmt, M)], written.
+ *   a_exp   DEVICE uint8 [mxq_act_exp_bytes(fmt, M)], written.
  */
 mxq_status mxq_quantize_act(const mxq_fmt *fmt, const uint16_t *a, int64_t M,
                             int64_t lda, uint8_t *a_mant, uint8_t *a_exp,
@@ -165,12 +189,14 @@ mxq_status mxq_pack_weights(const mxq_fmt *fmt, const uint16_t *w, int64_t N,
 /*
  * MXINT GEMM, Y = Ahat * What^T in fp32 (paper Sections 2 and 6: integer
  * block products, power-of-two block scales).
- *   a_mant/a_exp  DEVICE, from mxq_quantize_act with the same fmt, M rows.
- *   w_mant/w_exp  DEVICE, from mxq_pack_weights with the same fmt, N columns.
+ *   a_mant/a_exp  DEVICE, from mxq_quantize_act with the same fmt and the
+ *                 same M (the operand image's offset depends on M).
+ *   w_mant/w_exp  DEVICE, from mxq_pack_weights with the same fmt and N.
  *   y             DEVICE float [M][ldy], ldy >= N; every y[i][j] with i < M,
  *                 j < N is written, nothing else.
- * M <= MXQ_DECODE_MAX_M runs the weight-streaming decode kernel, larger M the
- * tiled prefill kernel; both give the same int32 block sums.
+ * M <= MXQ_DECODE_MAX_M runs the weight-streaming decode kernel (packed
+ * weights, exact int32 block sums rescaled in fp32), larger M the tiled
+ * prefill kernel (operand images on the block-scaled matrix cores).
  */
 mxq_status mxq_gemm(const mxq_fmt *fmt, int64_t M, int64_t N,
                     const uint8_t *a_mant, const uint8_t *a_exp,
@@ -183,8 +209,8 @@ mxq_status mxq_gemm(const mxq_fmt *fmt, int64_t M, int64_t N,
  *   q DEVICE int8 [rows][K] (permuted order) and exponents e DEVICE uint8
  *   [rows][K/32].
  * mxq_gemm_partials: the exact per-block int32 sums
- *   p DEVICE int32 [M][N][K/32], computed by the same unpack and matrix-core
- *   path as mxq_gemm (prefill tiling).
+ *   p DEVICE int32 [M][N][K/32], from the packed mantissas on int8 matrix
+ *   cores (one exact int32 sum per block).
  */
 mxq_status mxq_unpack_act(const mxq_fmt *fmt, int64_t rows,
                           const uint8_t *a_mant, const uint8_t *a_exp,

@@ -56,13 +56,13 @@ int64_t row_used(const Segs &s) { return 16LL * s.n4 + 24LL * s.n6 + 32LL * s.n8
 int64_t canon_rb(const Segs &s) { return round_up(row_used(s), 16); }
 int64_t exp_rb(const mxq_fmt *f) { return round_up(f->K / MXQ_BLOCK, 16); }
 mxq::OpGeo op_geo(const Segs &s) { return mxq::OpGeo(s.n4, s.n6, s.n8); }
-// activation rows: packed section followed by the matrix-core operand image;
-// activation exponent rows: exponents followed by the per-step scale bytes
-int64_t act_rb(const mxq_fmt *, const Segs &s) {
-  return canon_rb(s) + op_geo(s).row_bytes + mxq::kActOpTail;
+// activation buffers: M packed rows, then the operand image (32-row tiles);
+// exponent buffers: M exponent rows, then the operand image's scale bytes
+int64_t act_bytes(const Segs &s, int64_t M) {
+  return M * canon_rb(s) + mxq::act_op_bytes(op_geo(s), M);
 }
-int64_t act_erb(const mxq_fmt *f, const Segs &s) {
-  return exp_rb(f) + round_up(4LL * op_geo(s).nsteps, 16);
+int64_t act_exp_bytes(const mxq_fmt *f, const Segs &s, int64_t M) {
+  return M * exp_rb(f) + mxq::act_sc_bytes(op_geo(s), M);
 }
 // weights: packed slabs (N rounded to 16), tail padding, then the operand
 // image (N rounded to 128)
@@ -101,8 +101,10 @@ mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows
   a.exp = exp;
   a.canon_rb = canon_rb(s);
   a.canon_erb = exp_rb(fmt);
-  a.out_rb = weights ? 0 : act_rb(fmt, s);
-  a.out_erb = weights ? exp_rb(fmt) : act_erb(fmt, s);
+  a.out_rb = weights ? 0 : canon_rb(s);
+  a.out_erb = exp_rb(fmt);
+  a.op_off = weights ? 0 : rows * canon_rb(s);
+  a.sc_off = weights ? 0 : rows * exp_rb(fmt);
   a.row_used = row_used(s);
   a.tail_pad = weights ? (int)kWeightTailPad : 0;
   a.vec16 = (ld % 8 == 0) ? 1 : 0;
@@ -137,10 +139,10 @@ mxq_status gemm_args(const mxq_fmt *fmt, int64_t M, int64_t N, const uint8_t *a_
   g->w_exp = w_exp;
   g->M = M;
   g->N = N;
-  g->a_rb = act_rb(fmt, s);
-  g->a_erb = act_erb(fmt, s);
-  g->a_op = canon_rb(s);
-  g->a_sc = exp_rb(fmt);
+  g->a_rb = canon_rb(s);
+  g->a_erb = exp_rb(fmt);
+  g->a_op = M * canon_rb(s);
+  g->a_sc = M * exp_rb(fmt);
   g->w_erb = exp_rb(fmt);
   g->w_op = w_op_off(s, N);
   g->w_tile = w_tile(s);
@@ -171,16 +173,26 @@ const char *mxq_status_str(int status) {
   }
 }
 
-int64_t mxq_act_row_bytes(const mxq_fmt *fmt) {
+int64_t mxq_act_bytes(const mxq_fmt *fmt, int64_t M) {
   Segs s;
   const mxq_status st = check_fmt(fmt, &s);
-  return st == MXQ_OK ? act_rb(fmt, s) : -(int64_t)st;
+  if (st != MXQ_OK) return -(int64_t)st;
+  if (M < 0) return -(int64_t)MXQ_ERR_SHAPE;
+  return act_bytes(s, M);
+}
+
+int64_t mxq_act_exp_bytes(const mxq_fmt *fmt, int64_t M) {
+  Segs s;
+  const mxq_status st = check_fmt(fmt, &s);
+  if (st != MXQ_OK) return -(int64_t)st;
+  if (M < 0) return -(int64_t)MXQ_ERR_SHAPE;
+  return act_exp_bytes(fmt, s, M);
 }
 
 int64_t mxq_exp_row_bytes(const mxq_fmt *fmt) {
   Segs s;
   const mxq_status st = check_fmt(fmt, &s);
-  return st == MXQ_OK ? act_erb(fmt, s) : -(int64_t)st;
+  return st == MXQ_OK ? exp_rb(fmt) : -(int64_t)st;
 }
 
 int64_t mxq_act_packed_bytes(const mxq_fmt *fmt) {
@@ -261,8 +273,8 @@ static mxq_status unpack_common(const mxq_fmt *fmt, int64_t rows, const uint8_t 
   a.e = e;
   a.rows = rows;
   a.K = fmt->K;
-  a.a_rb = act_rb(fmt, s);
-  a.a_erb = weights ? exp_rb(fmt) : act_erb(fmt, s);
+  a.a_rb = canon_rb(s);
+  a.a_erb = exp_rb(fmt);
   a.npad = round_up(rows, 16);
   a.n4 = s.n4;
   a.n6 = s.n6;

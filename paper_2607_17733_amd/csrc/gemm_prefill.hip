@@ -18,8 +18,9 @@
 //
 // Tiling: 256x128 outputs per workgroup of four waves (one per SIMD), each
 // wave 64 rows x 128 columns = 2x4 tiles of 32x32 with fp32 accumulators.
-//   - A: each lane loads its rows' step data (48 or 32 bytes) straight from
-//     the activation operand image into registers, two steps ahead.
+//   - A: each lane loads its rows' 48-byte step data straight from the
+//     activation operand image (32-row tiles: every load of the wave reads
+//     one contiguous kilobyte) into registers, two steps ahead.
 //   - W: the step's 13 KB chunk of the weight operand image (already in the
 //     LDS layout) is loaded to registers three steps ahead, stored to LDS one
 //     step ahead (double buffer), and read by the lanes with 16-byte reads.
@@ -82,13 +83,16 @@ __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mti
   const OpGeo og(g.n4, g.n6, g.n8);
   const int nsteps = og.nsteps;
 
-  // This lane's two A rows (rows past M read row M-1; never stored).
-  const int64_t r0 = row0 + wave * 64 + l32;
-  const int64_t ra = r0 < g.M ? r0 : g.M - 1, rb = r0 + 32 < g.M ? r0 + 32 : g.M - 1;
-  const uint8_t *aop0 = g.a_mant + ra * g.a_rb + g.a_op;
-  const uint8_t *aop1 = g.a_mant + rb * g.a_rb + g.a_op;
-  const uint8_t *asc0 = g.a_exp + ra * g.a_erb + g.a_sc + 2 * lh;
-  const uint8_t *asc1 = g.a_exp + rb * g.a_erb + g.a_sc + 2 * lh;
+  // This wave's two 32-row tiles of the activation operand image (tiles past
+  // the last one read the last tile; those rows are never stored).  Lane
+  // (h, r) reads its 16-byte pieces at part * 1024 + h * 512 + r * 16.
+  const int64_t last = (g.M - 1) / kActRows;
+  const int64_t ta = min((row0 + wave * 64) / kActRows, last);
+  const int64_t tb = min((row0 + wave * 64) / kActRows + 1, last);
+  const uint8_t *aop0 = g.a_mant + g.a_op + ta * nsteps * kActStep + lh * 512 + l32 * 16;
+  const uint8_t *aop1 = g.a_mant + g.a_op + tb * nsteps * kActStep + lh * 512 + l32 * 16;
+  const uint8_t *asc0 = g.a_exp + g.a_sc + ta * nsteps * kActScaleStep + lh * 64 + l32 * 2;
+  const uint8_t *asc1 = g.a_exp + g.a_sc + tb * nsteps * kActScaleStep + lh * 64 + l32 * 2;
   const uint8_t *wtile = g.w_mant + g.w_op + (int64_t)nt * g.w_tile;
 
   v16f acc[2][4];
@@ -114,15 +118,14 @@ __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mti
     for (int j = 0; j < 3; ++j) Wl[buf][j * 256 + t] = w[j];
     if (t < 64) Wl[buf][768 + t] = w[3];
   };
-  // 48 bytes per row and step (8-bit steps use 32; the row has a 16-byte
-  // zero tail so the read stays inside it).
+  // A lane data (48 bytes: three contiguous kilobytes per wave) and scales.
   auto load_a = [&](int st, u12 (&x)[2], uint32_t (&s)[2]) __attribute__((always_inline)) {
-    const int64_t off = og.act_off(st, lh);
-    const u4 *p0 = (const u4 *)(aop0 + off), *p1 = (const u4 *)(aop1 + off);
-    x[0] = cat3(p0[0], p0[1], p0[2]);
-    x[1] = cat3(p1[0], p1[1], p1[2]);
-    s[0] = *(const uint16_t *)(asc0 + 4LL * st);
-    s[1] = *(const uint16_t *)(asc1 + 4LL * st);
+    const u4 *p0 = (const u4 *)(aop0 + (int64_t)st * kActStep);
+    const u4 *p1 = (const u4 *)(aop1 + (int64_t)st * kActStep);
+    x[0] = cat3(p0[0], p0[64], p0[128]);
+    x[1] = cat3(p1[0], p1[64], p1[128]);
+    s[0] = *(const uint16_t *)(asc0 + (int64_t)st * kActScaleStep);
+    s[1] = *(const uint16_t *)(asc1 + (int64_t)st * kActScaleStep);
   };
   auto compute = [&](auto seg, const u12 (&x)[2], const uint32_t (&s)[2], int buf)
       __attribute__((always_inline)) {

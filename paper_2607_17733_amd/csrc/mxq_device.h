@@ -226,7 +226,8 @@ __device__ inline uint64_t load_w_operand(const uint8_t *slab, const Segs &s,
 // The product of two 6-bit (8-bit) blocks is the sum of the four digit
 // products, computed by four (two) instructions over the same registers.
 //
-// K is walked in "steps", each one K-group of the instruction per lane half:
+// K is walked in "steps", each one K-group of the instruction per lane half
+// (lanes 32h..32h+31 hold rows / columns 0..31 of a 32-wide tile):
 //   4-bit: 4 blocks (two instructions, block pairs (4t, 4t+1), (4t+2, 4t+3));
 //   6-bit: a block pair, 8-bit: one block.
 // 4-bit blocks are padded to a multiple of 4 and 6-bit blocks to a multiple
@@ -244,18 +245,11 @@ struct OpGeo {
   int s4, s6, s8;        // steps per segment
   int nsteps;
   int64_t off6, off8;    // byte offsets of the 6- and 8-bit segments in a row
-  int64_t row_bytes;     // activation operand bytes per row
   __host__ __device__ OpGeo(int a, int b, int c)
       : n4(a), n6(b), n8(c), n4p((a + 3) & ~3), n6p((b + 1) & ~1), s4(n4p / 4),
         s6(n6p / 2), s8(c), nsteps(s4 + s6 + c), off6(24LL * n4p),
-        off8(24LL * n4p + 48LL * n6p), row_bytes(24LL * n4p + 48LL * n6p + 64LL * c) {}
+        off8(24LL * n4p + 48LL * n6p) {}
   __host__ __device__ int seg(int st) const { return st < s4 ? 0 : (st < s4 + s6 ? 1 : 2); }
-  // Byte offset of lane half h's data of step st inside an activation row.
-  __host__ __device__ int64_t act_off(int st, int h) const {
-    if (st < s4) return 96LL * st + 48 * h;
-    if (st < s4 + s6) return off6 + 96LL * (st - s4) + 48 * h;
-    return off8 + 64LL * (st - s4 - s6) + 32 * h;
-  }
 };
 
 // Weight operand image: 128-column tiles, each a run of per-step chunks of
@@ -264,7 +258,25 @@ struct OpGeo {
 // of a 4-bit step), laid out as the prefill GEMM keeps it in LDS:
 //   part j at j * 4096 + h * 2048 + c * 16, scales at 12288 + h * 512 + c * 4.
 constexpr int kOpCols = 128;
-constexpr int kActOpTail = 16;   // zero bytes after an activation operand row
+constexpr int kActRows = 32;
+constexpr int kActStep = 3072;       // operand bytes per (32-row tile, step)
+constexpr int kActScaleStep = 128;   // scale bytes per (32-row tile, step)
+
+// Activation operand image: byte o (0..47) of lane data (row, st, h), and
+// scale byte j (0, 1) of (row, st, h).
+__host__ __device__ inline int64_t act_op_loc(int64_t row, int st, int nsteps, int h, int o) {
+  return ((row >> 5) * nsteps + st) * (int64_t)kActStep + (o >> 4) * 1024 + h * 512 +
+         (row & 31) * 16 + (o & 15);
+}
+__host__ __device__ inline int64_t act_sc_loc(int64_t row, int st, int nsteps, int h, int j) {
+  return ((row >> 5) * nsteps + st) * (int64_t)kActScaleStep + h * 64 + (row & 31) * 2 + j;
+}
+__host__ __device__ inline int64_t act_op_bytes(const OpGeo &o, int64_t rows) {
+  return (rows + kActRows - 1) / kActRows * o.nsteps * (int64_t)kActStep;
+}
+__host__ __device__ inline int64_t act_sc_bytes(const OpGeo &o, int64_t rows) {
+  return (rows + kActRows - 1) / kActRows * o.nsteps * (int64_t)kActScaleStep;
+}
 constexpr int kOpChunk = 13312;
 constexpr int kOpPart = 4096;
 

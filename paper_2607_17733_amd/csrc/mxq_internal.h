@@ -18,10 +18,12 @@ struct QuantArgs {
   int ties_away, full_clamp;
   uint8_t *mant;
   uint8_t *exp;
-  int64_t out_rb;          // activation row stride (packed + operand sections)
+  int64_t out_rb;          // packed row stride (activations)
   int64_t out_erb;         // exponent row stride
   int64_t canon_rb;        // packed section bytes per row
-  int64_t canon_erb;       // exponent section bytes per row (scale bytes follow)
+  int64_t canon_erb;       // exponent bytes per row
+  int64_t op_off, sc_off;  // activations: offsets of the operand image in mant
+                           // and of its scale bytes in exp
   int64_t row_used;        // unpadded packed bytes per row
   int64_t slab_rows;       // weights: columns in the packed slabs (N rounded to 16)
   int64_t w_op;            // weights: offset of the operand image in the buffer
@@ -40,8 +42,9 @@ struct GemmArgs {
   float *y;                // [M][ldy] (gemm)
   int32_t *p;              // [M][N][nb] (partials)
   int64_t M, N, ldy;
-  int64_t a_rb, a_erb;     // activation row stride / exponent row stride
-  int64_t a_op, a_sc;      // offsets of the operand image / the scale bytes
+  int64_t a_rb, a_erb;     // packed activation row stride / exponent row stride
+  int64_t a_op, a_sc;      // offsets of the operand image in a_mant / of its
+                           // scale bytes in a_exp
   int64_t w_erb;           // weight exponent row stride
   int64_t w_op;            // offset of the weight operand image in w_mant
   int64_t w_tile;          // bytes per 128-column tile of that image

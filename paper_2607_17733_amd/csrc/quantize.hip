@@ -159,8 +159,10 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
       }
       uint8_t *erow_g = q.exp + row * q.out_erb;
       if (kg == 0) erow_g[b] = (uint8_t)E;
-      // operand image
-      uint8_t *op = q.mant + row * q.out_rb + q.canon_rb;
+      // operand image (32-row tiles) and its scale bytes
+      uint8_t *op = q.mant + q.op_off;
+      uint8_t *sc = q.exp + q.sc_off;
+      const int ns = og.nsteps;
       if (bi.m == 8) {
         uint32_t h0 = 0, h1 = 0, l0 = 0, l1 = 0;
 #pragma unroll
@@ -168,9 +170,10 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
           h0 |= d0[u] << (8 * u); h1 |= d0[4 + u] << (8 * u);
           l0 |= d1[u] << (8 * u); l1 |= d1[4 + u] << (8 * u);
         }
-        uint8_t *p = op + og.act_off(st, h) + 8 * (kg & 1);
-        *(uint2 *)p = make_uint2(h0, h1);
-        *(uint2 *)(p + 16) = make_uint2(l0, l1);
+        const int o = 8 * (kg & 1);
+        *(uint2 *)(op + act_op_loc(row, st, ns, h, o)) = make_uint2(h0, h1);
+        *(uint2 *)(op + act_op_loc(row, st, ns, h, 16 + o)) = make_uint2(l0, l1);
+        if (!(kg & 1)) *(uint4 *)(op + act_op_loc(row, st, ns, h, 32)) = make_uint4(0, 0, 0, 0);
       } else {
         uint64_t v0 = 0, v1 = 0;
 #pragma unroll
@@ -178,38 +181,41 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
           v0 |= (uint64_t)d0[u] << (6 * u);
           v1 |= (uint64_t)d1[u] << (6 * u);
         }
-        uint8_t *p = op + og.act_off(st, h) + (bi.m == 4 ? 24 * j : 0) + 6 * kg;
+        const int o = (bi.m == 4 ? 24 * j : 0) + 6 * kg;
 #pragma unroll
-        for (int k = 0; k < 3; ++k) ((uint16_t *)p)[k] = (uint16_t)(v0 >> (16 * k));
+        for (int k = 0; k < 3; ++k)
+          *(uint16_t *)(op + act_op_loc(row, st, ns, h, o + 2 * k)) = (uint16_t)(v0 >> (16 * k));
         if (bi.m == 6)
 #pragma unroll
-          for (int k = 0; k < 3; ++k) ((uint16_t *)(p + 24))[k] = (uint16_t)(v1 >> (16 * k));
+          for (int k = 0; k < 3; ++k)
+            *(uint16_t *)(op + act_op_loc(row, st, ns, h, 24 + o + 2 * k)) =
+                (uint16_t)(v1 >> (16 * k));
       }
-      // E8M0 scale bytes of the step: [step][half][2]
-      uint8_t *sc = erow_g + q.canon_erb + 4LL * st;
-      if (kg == 0) {
-        if (bi.m == 4) sc[2 * h + j] = (uint8_t)E;
-        else if (bi.m == 6) *(uint16_t *)(sc + 2 * h) = (uint16_t)E;
-        else *(uint32_t *)sc = (uint32_t)E | ((uint32_t)E << 16);
+      if (kg == 0) {                         // scale bytes: [tile, step][half][row][2]
+        if (bi.m == 4) {
+          sc[act_sc_loc(row, st, ns, h, j)] = (uint8_t)E;
+        } else if (bi.m == 6) {
+          *(uint16_t *)(sc + act_sc_loc(row, st, ns, h, 0)) = (uint16_t)E;
+        } else {
+          *(uint16_t *)(sc + act_sc_loc(row, st, ns, 0, 0)) = (uint16_t)E;
+          *(uint16_t *)(sc + act_sc_loc(row, st, ns, 1, 0)) = (uint16_t)E;
+        }
       }
       if (g == 0) {                          // zero the row padding
         for (int64_t z = q.row_used; z < q.canon_rb; ++z)
           q.mant[row * q.out_rb + z] = 0;
         for (int64_t z = nb; z < q.canon_erb; ++z) erow_g[z] = 0;
-        for (int z = 0; z < kActOpTail; ++z) op[og.row_bytes + z] = 0;
-        for (int64_t z = 4LL * og.nsteps; z < q.out_erb - q.canon_erb; ++z)
-          erow_g[q.canon_erb + z] = 0;
         for (int i = og.n4; i < og.n4p; ++i) {   // 4-bit pad blocks
           const int pst = i >> 2, ph = i & 1, pj = (i >> 1) & 1;
-          uint8_t *pp = op + og.act_off(pst, ph) + 24 * pj;
-          for (int z = 0; z < 24; ++z) pp[z] = 0;
-          erow_g[q.canon_erb + 4LL * pst + 2 * ph + pj] = 0;
+          for (int z = 0; z < 24; z += 2)
+            *(uint16_t *)(op + act_op_loc(row, pst, ns, ph, 24 * pj + z)) = 0;
+          sc[act_sc_loc(row, pst, ns, ph, pj)] = 0;
         }
         if (og.n6p > og.n6) {                  // 6-bit pad block (odd count)
           const int pst = og.s4 + (og.n6 >> 1);
-          uint8_t *pp = op + og.act_off(pst, 1);
-          for (int z = 0; z < 48; ++z) pp[z] = 0;
-          *(uint16_t *)(erow_g + q.canon_erb + 4LL * pst + 2) = 0;
+          for (int z = 0; z < 48; z += 2)
+            *(uint16_t *)(op + act_op_loc(row, pst, ns, 1, z)) = 0;
+          *(uint16_t *)(sc + act_sc_loc(row, pst, ns, 1, 0)) = 0;
         }
       }
     } else {

@@ -36,9 +36,10 @@ _P, _I64 = ctypes.c_void_p, ctypes.c_int64
 _SIGS = {
     "mxq_abi_version": (ctypes.c_int, []),
     "mxq_status_str": (ctypes.c_char_p, [ctypes.c_int]),
-    "mxq_act_row_bytes": (_I64, [_P]),
     "mxq_act_packed_bytes": (_I64, [_P]),
     "mxq_exp_row_bytes": (_I64, [_P]),
+    "mxq_act_bytes": (_I64, [_P, _I64]),
+    "mxq_act_exp_bytes": (_I64, [_P, _I64]),
     "mxq_weight_bytes": (_I64, [_P, _I64]),
     "mxq_weight_exp_bytes": (_I64, [_P, _I64]),
     "mxq_quantize_act": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P]),
@@ -116,15 +117,21 @@ class Format:
     def nb(self) -> int:
         return self.K // BLOCK
 
-    def act_row_bytes(self) -> int:
-        return _size(lib().mxq_act_row_bytes(self.ref), "mxq_act_row_bytes")
-
     def act_packed_bytes(self) -> int:
-        """Bytes of the bit-packed section at the start of each activation row."""
+        """Bytes of one packed activation row."""
         return _size(lib().mxq_act_packed_bytes(self.ref), "mxq_act_packed_bytes")
 
     def exp_row_bytes(self) -> int:
+        """Bytes of one row of block exponents."""
         return _size(lib().mxq_exp_row_bytes(self.ref), "mxq_exp_row_bytes")
+
+    def act_bytes(self, M: int) -> int:
+        """Activation buffer: M packed rows, then the operand image."""
+        return _size(lib().mxq_act_bytes(self.ref, M), "mxq_act_bytes")
+
+    def act_exp_bytes(self, M: int) -> int:
+        """Exponent buffer: M exponent rows, then the operand scale bytes."""
+        return _size(lib().mxq_act_exp_bytes(self.ref, M), "mxq_act_exp_bytes")
 
     def weight_bytes(self, N: int) -> int:
         return _size(lib().mxq_weight_bytes(self.ref, N), "mxq_weight_bytes")
@@ -144,18 +151,32 @@ def _bf16_2d(t, K, what):
 
 
 def quantize_act(a, fmt: Format, out=None):
-    """Online activation quantization: bf16 [M, >=K] -> (mant [M, row_bytes]
-    uint8, exp [M, exp_row_bytes] uint8) on the current stream."""
+    """Online activation quantization: bf16 [M, >=K] -> (mant uint8
+    [act_bytes(M)], exp uint8 [act_exp_bytes(M)]) on the current stream."""
     _bf16_2d(a, fmt.K, "activations")
     M = a.shape[0]
     if out is None:
-        mant = torch.empty((M, fmt.act_row_bytes()), dtype=torch.uint8, device=a.device)
-        exp = torch.empty((M, fmt.exp_row_bytes()), dtype=torch.uint8, device=a.device)
+        mant = torch.empty(fmt.act_bytes(M), dtype=torch.uint8, device=a.device)
+        exp = torch.empty(fmt.act_exp_bytes(M), dtype=torch.uint8, device=a.device)
     else:
         mant, exp = out
+        if mant.numel() < fmt.act_bytes(M) or exp.numel() < fmt.act_exp_bytes(M):
+            raise MxqError("activation output buffers are too small")
     _check(lib().mxq_quantize_act(fmt.ref, _ptr(a), M, a.stride(0), _ptr(mant),
                                   _ptr(exp), _stream()), "mxq_quantize_act")
     return mant, exp
+
+
+def packed_rows(mant, fmt: Format, M: int):
+    """View of the packed activation rows [M, act_packed_bytes]."""
+    n = fmt.act_packed_bytes()
+    return mant[:M * n].view(M, n)
+
+
+def exp_rows(exp, fmt: Format, M: int):
+    """View of the activation block exponents [M, exp_row_bytes]."""
+    n = fmt.exp_row_bytes()
+    return exp[:M * n].view(M, n)
 
 
 def pack_weights(w, fmt: Format):

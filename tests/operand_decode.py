@@ -14,7 +14,6 @@ BLOCK = 32
 CHUNK = 13312          # bytes per step of a 128-column weight tile
 PART = 4096
 TILE_COLS = 128
-ACT_TAIL = 16
 
 
 def _e3m2_table():
@@ -62,17 +61,6 @@ class Geo:
         self.n6p = -(-self.n6 // 2) * 2
         self.s4, self.s6, self.s8 = self.n4p // 4, self.n6p // 2, self.n8
         self.nsteps = self.s4 + self.s6 + self.s8
-        self.off6 = 24 * self.n4p
-        self.off8 = self.off6 + 48 * self.n6p
-        self.row_bytes = self.off8 + 64 * self.n8
-
-    def lane_off(self, st, h):
-        """Offset of lane half h's data of step st in an activation row."""
-        if st < self.s4:
-            return 96 * st + 48 * h
-        if st < self.s4 + self.s6:
-            return self.off6 + 96 * (st - self.s4) + 48 * h
-        return self.off8 + 64 * (st - self.s4 - self.s6) + 32 * h
 
     def blocks_of_step(self, st):
         """[(block index or None for padding, half, position)] of step st.
@@ -93,51 +81,72 @@ class Geo:
         return out
 
 
-def _decode_lane_block(geo, st, lane_bytes_h, m_kind, j=0):
-    """q of one block from a lane half's bytes (4/6-bit)."""
-    if m_kind == 4:
-        return fp6_values(lane_bytes_h[..., 24 * j:24 * j + 24]) * 4
-    hv = fp6_values(lane_bytes_h[..., 0:24])
-    lv = fp6_values(lane_bytes_h[..., 24:48])
-    return (hv + lv) * 16
+def _decode_lane_block(lane, kind, j=0):
+    """q of one 4- or 6-bit block from a lane half's 48 bytes."""
+    if kind == 4:
+        return fp6_values(lane[..., 24 * j:24 * j + 24]) * 4
+    return (fp6_values(lane[..., 0:24]) + fp6_values(lane[..., 24:48])) * 16
 
 
-def decode_act(op: np.ndarray, sc: np.ndarray, widths):
-    """op: [rows, row_bytes + tail] operand section; sc: [rows, >= 4*nsteps]
-    scale bytes.  Returns (q [rows, K] int, E [rows, nb] int, pad_ok)."""
-    geo = Geo(widths)
-    rows = op.shape[0]
-    nb = len(widths)
+def _decode_steps(geo, nb, rows, lane_of, scale_of, weights):
+    """Rebuild q [rows, K] and E [rows, nb] from per-step lane data
+    lane_of(st, h) -> [rows, 48] and scale_of(st, h) -> [rows, >=2]."""
     q = np.zeros((rows, nb * BLOCK))
     E = np.full((rows, nb), -1, dtype=np.int64)
-    pad_ok = True
+    ok = True
     for st in range(geo.nsteps):
+        lanes = [lane_of(st, h) for h in (0, 1)]
+        scs = [scale_of(st, h) for h in (0, 1)]
         for (b, h, j) in geo.blocks_of_step(st):
             if st < geo.s4 + geo.s6:
-                lane = op[:, geo.lane_off(st, h):geo.lane_off(st, h) + 48]
                 kind = 4 if st < geo.s4 else 6
-                scale = sc[:, 4 * st + 2 * h + j].astype(np.int64)
+                scale = scs[h][:, j].astype(np.int64)
                 if b is None:
-                    part = lane[:, 24 * j:24 * j + 24] if kind == 4 else lane
-                    pad_ok &= not part.any() and not scale.any()
+                    part = lanes[h][:, 24 * j:24 * j + 24] if kind == 4 else lanes[h]
+                    ok &= not part.any() and not scale.any()
+                    if kind == 6:
+                        ok &= not scs[h][:, 1].any()
                     continue
-                q[:, BLOCK * b:BLOCK * b + BLOCK] = _decode_lane_block(geo, st, lane, kind, j)
+                q[:, BLOCK * b:BLOCK * b + BLOCK] = _decode_lane_block(lanes[h], kind, j)
                 E[:, b] = scale
                 if kind == 6:
-                    pad_ok &= not sc[:, 4 * st + 2 * h + 1].any()
+                    ok &= not scs[h][:, 1].any()
             else:
                 vals = []
                 for hf in (0, 1):
-                    lane = op[:, geo.lane_off(st, hf):geo.lane_off(st, hf) + 32]
-                    vals.append((fp8_values(lane[:, :16]) + fp8_values(lane[:, 16:32])) * 64)
+                    ln = lanes[hf]
+                    if weights:
+                        ok &= bool(np.array_equal(ln[:, :16], ln[:, 32:48]))
+                    else:
+                        ok &= not ln[:, 32:48].any()
+                    vals.append((fp8_values(ln[:, :16]) + fp8_values(ln[:, 16:32])) * 64)
                 q[:, BLOCK * b:BLOCK * b + BLOCK] = np.concatenate(vals, axis=1)
-                s = sc[:, 4 * st:4 * st + 4].astype(np.int64)
-                pad_ok &= bool(np.array_equal(s[:, 0], s[:, 2])) and not s[:, 1].any() \
-                    and not s[:, 3].any()
-                E[:, b] = s[:, 0]
-    pad_ok &= not op[:, geo.row_bytes:geo.row_bytes + ACT_TAIL].any()
-    pad_ok &= not sc[:, 4 * geo.nsteps:].any()
-    return q, E, pad_ok
+                ok &= bool(np.array_equal(scs[0][:, 0], scs[1][:, 0]))
+                ok &= not scs[0][:, 1].any() and not scs[1][:, 1].any()
+                E[:, b] = scs[0][:, 0]
+    return q, E, ok
+
+
+ACT_STEP, ACT_SCALE_STEP, ACT_ROWS = 3072, 128, 32
+
+
+def decode_act(op_img: np.ndarray, sc_img: np.ndarray, widths, M: int):
+    """Activation operand image (32-row tiles) and its scale bytes ->
+    (q [M, K], E [M, nb], layout_ok)."""
+    geo = Geo(widths)
+    nt = -(-M // ACT_ROWS)
+    assert op_img.size == nt * geo.nsteps * ACT_STEP
+    assert sc_img.size == nt * geo.nsteps * ACT_SCALE_STEP
+    t = op_img.reshape(nt, geo.nsteps, 3, 2, ACT_ROWS, 16)
+    sct = sc_img.reshape(nt, geo.nsteps, 2, ACT_ROWS, 2)
+
+    def lane_of(st, h):
+        return t[:, st, :, h].transpose(0, 2, 1, 3).reshape(nt * ACT_ROWS, 48)[:M]
+
+    def scale_of(st, h):
+        return sct[:, st, h].reshape(nt * ACT_ROWS, 2)[:M]
+
+    return _decode_steps(geo, len(widths), M, lane_of, scale_of, weights=False)
 
 
 def w_lane_bytes(img: np.ndarray, geo: Geo, st: int, h: int):
@@ -161,37 +170,13 @@ def w_scales(img: np.ndarray, geo: Geo, st: int, h: int):
 def decode_weights(img: np.ndarray, widths, N: int):
     """Weight operand image -> (q [Npad128, K], E [Npad128, nb], layout_ok)."""
     geo = Geo(widths)
-    nb = len(widths)
     tile = CHUNK * geo.nsteps
     ntiles = img.size // tile
-    cols = ntiles * TILE_COLS
-    q = np.zeros((cols, nb * BLOCK))
-    E = np.full((cols, nb), -1, dtype=np.int64)
     ok = True
     for st in range(geo.nsteps):
-        lanes = [w_lane_bytes(img, geo, st, h) for h in (0, 1)]
-        scs = [w_scales(img, geo, st, h) for h in (0, 1)]
-        ok &= not scs[0][:, 2:].any() and not scs[1][:, 2:].any()
-        for (b, h, j) in geo.blocks_of_step(st):
-            if st < geo.s4 + geo.s6:
-                kind = 4 if st < geo.s4 else 6
-                scale = scs[h][:, j].astype(np.int64)
-                if b is None:
-                    part = lanes[h][:, 24 * j:24 * j + 24] if kind == 4 else lanes[h]
-                    ok &= not part.any() and not scale.any()
-                    continue
-                q[:, BLOCK * b:BLOCK * b + BLOCK] = _decode_lane_block(geo, st, lanes[h], kind, j)
-                E[:, b] = scale
-                if kind == 6:
-                    ok &= not scs[h][:, 1].any()
-            else:
-                vals = []
-                for hf in (0, 1):
-                    ln = lanes[hf]
-                    ok &= bool(np.array_equal(ln[:, :16], ln[:, 32:48]))
-                    vals.append((fp8_values(ln[:, :16]) + fp8_values(ln[:, 16:32])) * 64)
-                q[:, BLOCK * b:BLOCK * b + BLOCK] = np.concatenate(vals, axis=1)
-                ok &= bool(np.array_equal(scs[0][:, 0], scs[1][:, 0]))
-                ok &= not scs[0][:, 1].any() and not scs[1][:, 1].any()
-                E[:, b] = scs[0][:, 0]
-    return q, E, ok
+        for h in (0, 1):
+            ok &= not w_scales(img, geo, st, h)[:, 2:].any()
+    q, E, ok2 = _decode_steps(geo, len(widths), ntiles * TILE_COLS,
+                              lambda st, h: w_lane_bytes(img, geo, st, h),
+                              lambda st, h: w_scales(img, geo, st, h), weights=True)
+    return q, E, ok and ok2

@@ -118,21 +118,28 @@ def check_gemm(Y, Yref, qa, ea, qw, ew, widths, what, rows=None, cols=None):
 
 
 def check_quant_act(case, out, qa, ea, fmt):
+    """Bit-exact activation buffers: packed rows against the oracle's
+    packing, exponents, the operand image decoded back to mantissas and
+    scale bytes, zero padding, and mxq_unpack_act."""
+    M = case.M
     am = out["a_mant"].cpu().numpy()
     ae = out["a_exp"].cpu().numpy()
     nb = case.K // BLOCK
     canon = fmt.act_packed_bytes()
-    cerb = -(-nb // 16) * 16
+    cerb = fmt.exp_row_bytes()
+    assert am.size == fmt.act_bytes(M) and ae.size == fmt.act_exp_bytes(M)
     ref_bytes = oracle.pack_act(qa, case.widths)
-    assert am.shape == (case.M, fmt.act_row_bytes()) and ref_bytes.shape == (case.M, canon)
-    assert np.array_equal(am[:, :canon], ref_bytes), "packed activation bytes differ"
-    assert np.array_equal(ae[:, :nb], ea), "activation exponents differ"
-    assert not ae[:, nb:cerb].any()
-    q, E, pad_ok = decode_act(am[:, canon:], ae[:, cerb:], case.widths)
+    assert ref_bytes.shape == (M, canon)
+    assert np.array_equal(am[:M * canon].reshape(M, canon), ref_bytes), \
+        "packed activation bytes differ"
+    erows = ae[:M * cerb].reshape(M, cerb)
+    assert np.array_equal(erows[:, :nb], ea), "activation exponents differ"
+    assert not erows[:, nb:].any()
+    q, E, pad_ok = decode_act(am[M * canon:], ae[M * cerb:], case.widths, M)
     assert np.array_equal(q, qa), "activation operand image differs from the mantissas"
     assert np.array_equal(E, ea.astype(np.int64)), "activation scale bytes differ"
     assert pad_ok, "activation operand padding not zero"
-    qd, ed = mxq.unpack_act(out["a_mant"], out["a_exp"], fmt, case.M)
+    qd, ed = mxq.unpack_act(out["a_mant"], out["a_exp"], fmt, M)
     assert np.array_equal(qd.cpu().numpy(), qa) and np.array_equal(ed.cpu().numpy(), ea)
 
 

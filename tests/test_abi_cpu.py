@@ -47,22 +47,29 @@ def _fmt(K, widths, round_=0, clamp=0, block=32, reserved=0):
     return f, w
 
 
-def op_layout(widths):
-    """Operand-image geometry as include/mxq.h states it: 4-bit blocks padded
-    to a multiple of 4 (24 bytes each), 6-bit to a multiple of 2 (48 bytes
-    each), 8-bit 64 bytes each; steps = n4p/4 + n6p/2 + n8."""
+def op_steps(widths):
+    """Steps of the operand images as include/mxq.h states them: 4-bit
+    blocks padded to a multiple of 4 taken four at a time, 6-bit padded to a
+    multiple of 2 taken two at a time, 8-bit one at a time."""
     n4, n6, n8 = (sum(1 for w in widths if w == m) for m in (4, 6, 8))
-    n4p, n6p = -(-n4 // 4) * 4, -(-n6 // 2) * 2
-    return 24 * n4p + 48 * n6p + 64 * n8, n4p // 4 + n6p // 2 + n8
+    return -(-n4 // 4) + -(-n6 // 2) + n8
 
 
 def test_sizes(lib):
-    f, _w = _fmt(256, [4] * 6 + [6, 8])
-    assert lib.mxq_abi_version() == 1
-    assert op_layout([4] * 6 + [6, 8]) == (352, 4)
+    w1 = [4] * 6 + [6, 8]
+    f, _w = _fmt(256, w1)
+    assert lib.mxq_abi_version() == 2
+    assert op_steps(w1) == 4
     assert lib.mxq_act_packed_bytes(ctypes.byref(f)) == 160
-    assert lib.mxq_act_row_bytes(ctypes.byref(f)) == 160 + 352 + 16  # + operand image + tail
-    assert lib.mxq_exp_row_bytes(ctypes.byref(f)) == 16 + 16         # exponents + scale bytes
+    assert lib.mxq_exp_row_bytes(ctypes.byref(f)) == 16
+    # M packed rows + 32-row operand tiles of 3072 bytes per step
+    assert lib.mxq_act_bytes(ctypes.byref(f), 16) == 16 * 160 + 1 * 4 * 3072
+    assert lib.mxq_act_bytes(ctypes.byref(f), 33) == 33 * 160 + 2 * 4 * 3072
+    assert lib.mxq_act_bytes(ctypes.byref(f), 0) == 0
+    assert lib.mxq_act_bytes(ctypes.byref(f), -1) == -2
+    # M exponent rows + 128 scale bytes per (tile, step)
+    assert lib.mxq_act_exp_bytes(ctypes.byref(f), 16) == 16 * 16 + 1 * 4 * 128
+    assert lib.mxq_act_exp_bytes(ctypes.byref(f), 64) == 64 * 16 + 2 * 4 * 128
     # packed slabs (N to 16) + 64-byte tail + 128-column operand tiles of
     # 13312 bytes per step
     assert lib.mxq_weight_bytes(ctypes.byref(f), 256) == 256 * 152 + 64 + 2 * 4 * 13312
@@ -71,10 +78,11 @@ def test_sizes(lib):
     assert lib.mxq_weight_exp_bytes(ctypes.byref(f), 17) == 32 * 16
     w2 = [4] * 102 + [6] * 13 + [8] * 13
     f2, _w2 = _fmt(4096, w2)
-    assert op_layout(w2) == (4000, 46)
+    assert op_steps(w2) == 26 + 7 + 13
     assert lib.mxq_act_packed_bytes(ctypes.byref(f2)) == 2368   # 2360 rounded up to 16
-    assert lib.mxq_act_row_bytes(ctypes.byref(f2)) == 2368 + 4000 + 16
-    assert lib.mxq_exp_row_bytes(ctypes.byref(f2)) == 128 + 192  # 4 * 46 = 184 -> 192
+    assert lib.mxq_exp_row_bytes(ctypes.byref(f2)) == 128
+    assert lib.mxq_act_bytes(ctypes.byref(f2), 2048) == 2048 * 2368 + 64 * 46 * 3072
+    assert lib.mxq_act_exp_bytes(ctypes.byref(f2), 2048) == 2048 * 128 + 64 * 46 * 128
 
 
 def test_size_functions_match_oracle_layout(lib, oracle_lib):
@@ -95,7 +103,8 @@ def test_size_functions_match_oracle_layout(lib, oracle_lib):
 ])
 def test_bad_formats_rejected(lib, kwargs, status):
     f, _w = _fmt(**kwargs)
-    assert lib.mxq_act_row_bytes(ctypes.byref(f)) == -status
+    assert lib.mxq_act_packed_bytes(ctypes.byref(f)) == -status
+    assert lib.mxq_act_bytes(ctypes.byref(f), 4) == -status
     # the quantizer rejects the format before touching any pointer
     dummy = ctypes.c_void_p(16)
     assert lib.mxq_quantize_act(ctypes.byref(f), dummy, 4, 4096, dummy, dummy, None) == status

@@ -84,9 +84,9 @@ def test_out_of_range_permutation_entries_read_zero():
     p2 = perm.copy()
     p2[[3, 100, 255]] = case.K
     qa, ea = oracle.quantize(src, K=case.K, perm=p2, widths=case.widths)
-    canon = fmtg.act_packed_bytes()
-    assert np.array_equal(am.cpu().numpy()[:, :canon], oracle.pack_act(qa, case.widths))
-    assert np.array_equal(ae.cpu().numpy()[:, :case.K // 32], ea)
+    assert np.array_equal(mxq.packed_rows(am, fmtg, case.M).cpu().numpy(),
+                          oracle.pack_act(qa, case.widths))
+    assert np.array_equal(mxq.exp_rows(ae, fmtg, case.M).cpu().numpy()[:, :case.K // 32], ea)
 
 
 def test_strided_inputs_and_outputs():
@@ -103,7 +103,7 @@ def test_strided_inputs_and_outputs():
     mxq.gemm(am, ae, wm, we, fmt, 48, 40, out=y_big[:, :40])
     torch.cuda.synchronize()
     qa, ea, qw, ew = oracle_quant(case)
-    assert np.array_equal(am.cpu().numpy()[:, :fmt.act_packed_bytes()],
+    assert np.array_equal(mxq.packed_rows(am, fmt, 48).cpu().numpy(),
                           oracle.pack_act(qa, case.widths))
     Yref = oracle.gemm(qa, ea, qw, ew, case.widths)
     yb = y_big.cpu().numpy()
@@ -208,6 +208,7 @@ def test_kv_cache_quantize():
         am, ae = mxq.quantize_act(to_dev_bf16(bits), fmt)
         torch.cuda.synchronize()
         q, e = oracle.quantize(bits, widths=[4, 4, 4, 4])
-        canon = fmt.act_packed_bytes()
-        assert np.array_equal(am.cpu().numpy()[:, :canon], oracle.pack_act(q, [4, 4, 4, 4]))
-        assert np.array_equal(ae.cpu().numpy()[:, :4], e)
+        rows = bits.shape[0]
+        assert np.array_equal(mxq.packed_rows(am, fmt, rows).cpu().numpy(),
+                              oracle.pack_act(q, [4, 4, 4, 4]))
+        assert np.array_equal(mxq.exp_rows(ae, fmt, rows).cpu().numpy()[:, :4], e)
