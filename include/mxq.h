@@ -135,11 +135,12 @@ const char *mxq_status_str(int status);
  *   + (r % 32) * 16 + o % 16 of the operand image.
  *   a_exp: M rows of mxq_exp_row_bytes(fmt) bytes (block exponents E, byte b
  *   for block b, zero padded to a multiple of 16), then the operand image's
- *   scale bytes: for (row r, step s, half h) two bytes at
- *   ((r / 32) * nsteps + s) * 128 + h * 64 + (r % 32) * 2: the E of block
+ *   scale bytes: for (row r, step s, half h) four bytes at
+ *   ((r / 32) * nsteps + s) * 256 + h * 128 + (r % 32) * 4: the E of block
  *   4s'+h and of block 4s'+2+h for a 4-bit step, the E of the half's block
  *   and 0 for a 6-bit step, the block's E and 0 (both halves) for an 8-bit
- *   step; zero for padding blocks.  mxq_act_exp_bytes(fmt, M) in total.
+ *   step, then two zero bytes; zero for padding blocks.
+ *   mxq_act_exp_bytes(fmt, M) in total.
  *   The prefill GEMM reads the operand image; the decode GEMM,
  *   mxq_gemm_partials and mxq_unpack_act read the packed rows.
  * Weights (mxq_pack_weights for N columns), mxq_weight_bytes(fmt, N):

@@ -16,14 +16,19 @@
 //   8-bit (1 block):  two FP8 instructions, [h|l].[h|l] and [h|l].[l|h].
 // The digit products are exact; only the fp32 accumulation rounds.
 //
-// Tiling: 256x128 outputs per workgroup of four waves (one per SIMD), each
-// wave 64 rows x 128 columns = 2x4 tiles of 32x32 with fp32 accumulators.
+// Tiling: 256x128 outputs per workgroup of eight waves in two K groups.
+// Group g (waves 4g..4g+3) takes the steps s with s % 2 == g; within a group
+// wave r computes rows 64r..64r+63 x all 128 columns = 2x4 tiles of 32x32
+// with fp32 accumulators.  Two waves per SIMD (one of each group) keep the
+// matrix core busy while the other waits on memory or LDS; at the end the
+// groups' partial sums meet in LDS (fixed order: even steps + odd steps).
 //   - A: each lane loads its rows' 48-byte step data straight from the
 //     activation operand image (32-row tiles: every load of the wave reads
-//     one contiguous kilobyte) into registers, two steps ahead.
-//   - W: the step's 13 KB chunk of the weight operand image (already in the
-//     LDS layout) is loaded to registers three steps ahead, stored to LDS one
-//     step ahead (double buffer), and read by the lanes with 16-byte reads.
+//     one contiguous kilobyte) into registers, one own step ahead.
+//   - W: each group loads its next step's 13 KB chunk of the weight operand
+//     image (already in the LDS layout) into registers, stores it to LDS one
+//     iteration later (double buffer per group), and its lanes read it with
+//     16-byte reads.
 // Workgroup ids are remapped so that each XCD works on a contiguous range of
 // column tiles: its share of the weights stays in its L2.
 #include "mxq_device.h"
@@ -38,9 +43,10 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 typedef unsigned u4 __attribute__((ext_vector_type(4)));
 typedef unsigned u12 __attribute__((ext_vector_type(12)));   // one lane's 48 bytes
 
-constexpr int BM = 256, BN = kOpCols, NT = 256;
+constexpr int BM = 256, BN = kOpCols, NT = 512;
 constexpr int kChunkVec = kOpChunk / 16;     // 16-byte pieces per chunk (832)
 constexpr int kFmtFp8 = 0, kFmtFp6 = 3;      // e4m3, e3m2
+constexpr int kSmemVec = BM * BN * 4 / 16;   // 128 KB: the end reduction (W buffers alias it)
 
 template <int S> struct Seg { static constexpr int v = S; };
 
@@ -63,9 +69,13 @@ __device__ inline v16f mma(const v8i &a, const v8i &b, v16f c, int sa, int sb) {
 
 __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mtiles,
                                                              int ntiles) {
-  __shared__ __attribute__((aligned(16))) u4 Wl[2][kChunkVec];
+  __shared__ __attribute__((aligned(16))) u4 smem[kSmemVec];
+  // W chunks during the K loop: [buffer][group][chunk]
+  u4 (*Wl)[2][kChunkVec] = (u4 (*)[2][kChunkVec])smem;
 
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);     // wave-uniform
+  const int kg = wave >> 2, rw = wave & 3, tg = t & 255;   // K group, row block, thread in group
   const int l32 = lane & 31, lh = lane >> 5;
   int mt, nt;
   {
@@ -82,17 +92,18 @@ __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mti
   const int64_t row0 = (int64_t)mt * BM, col0 = (int64_t)nt * BN;
   const OpGeo og(g.n4, g.n6, g.n8);
   const int nsteps = og.nsteps;
+  const int niter = (nsteps + 1) >> 1;     // iterations; group 1's last may be empty
 
   // This wave's two 32-row tiles of the activation operand image (tiles past
   // the last one read the last tile; those rows are never stored).  Lane
   // (h, r) reads its 16-byte pieces at part * 1024 + h * 512 + r * 16.
   const int64_t last = (g.M - 1) / kActRows;
-  const int64_t ta = min((row0 + wave * 64) / kActRows, last);
-  const int64_t tb = min((row0 + wave * 64) / kActRows + 1, last);
+  const int64_t ta = min((row0 + rw * 64) / kActRows, last);
+  const int64_t tb = min((row0 + rw * 64) / kActRows + 1, last);
   const uint8_t *aop0 = g.a_mant + g.a_op + ta * nsteps * kActStep + lh * 512 + l32 * 16;
   const uint8_t *aop1 = g.a_mant + g.a_op + tb * nsteps * kActStep + lh * 512 + l32 * 16;
-  const uint8_t *asc0 = g.a_exp + g.a_sc + ta * nsteps * kActScaleStep + lh * 64 + l32 * 2;
-  const uint8_t *asc1 = g.a_exp + g.a_sc + tb * nsteps * kActScaleStep + lh * 64 + l32 * 2;
+  const uint8_t *asc0 = g.a_exp + g.a_sc + ta * nsteps * kActScaleStep + lh * 128 + l32 * 4;
+  const uint8_t *asc1 = g.a_exp + g.a_sc + tb * nsteps * kActScaleStep + lh * 128 + l32 * 4;
   const uint8_t *wtile = g.w_mant + g.w_op + (int64_t)nt * g.w_tile;
 
   v16f acc[2][4];
@@ -101,144 +112,154 @@ __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mti
 #pragma unroll
     for (int n = 0; n < 4; ++n) acc[a][n] = v16f{};
 
-  // Register rings, indexed by the step's position relative to the start of
-  // the current segment: W staging (2 slots), A lane data and scales (3).
-  u4 ws[2][4];
-  u12 xa[3][2];
-  uint32_t xs[3][2];
+  // Per wave: W staging (one chunk piece set), A lane data and scales in a
+  // ring of two, indexed by the iteration's position relative to the start
+  // of the current segment.
+  u4 ws[4];
+  u12 xa[2][2];
+  uint32_t xs[2][2];
 
-  auto load_w = [&](int st, u4 (&w)[4]) __attribute__((always_inline)) {
+  // The group's own step of iteration i (clamped: past the end it refetches
+  // the last step, which is not multiplied).
+  auto own = [&](int i) __attribute__((always_inline)) { return min(2 * i + kg, nsteps - 1); };
+  auto load_w = [&](int st) __attribute__((always_inline)) {
     const u4 *src = (const u4 *)(wtile + (int64_t)st * kOpChunk);
 #pragma unroll
-    for (int j = 0; j < 3; ++j) w[j] = src[j * 256 + t];
-    if (t < 64) w[3] = src[768 + t];
+    for (int j = 0; j < 3; ++j) ws[j] = src[j * 256 + tg];
+    if (tg < 64) ws[3] = src[768 + tg];
   };
-  auto store_w = [&](const u4 (&w)[4], int buf) __attribute__((always_inline)) {
+  auto store_w = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
-    for (int j = 0; j < 3; ++j) Wl[buf][j * 256 + t] = w[j];
-    if (t < 64) Wl[buf][768 + t] = w[3];
+    for (int j = 0; j < 3; ++j) Wl[buf][kg][j * 256 + tg] = ws[j];
+    if (tg < 64) Wl[buf][kg][768 + tg] = ws[3];
   };
-  // A lane data (48 bytes: three contiguous kilobytes per wave) and scales.
   auto load_a = [&](int st, u12 (&x)[2], uint32_t (&s)[2]) __attribute__((always_inline)) {
     const u4 *p0 = (const u4 *)(aop0 + (int64_t)st * kActStep);
     const u4 *p1 = (const u4 *)(aop1 + (int64_t)st * kActStep);
     x[0] = cat3(p0[0], p0[64], p0[128]);
     x[1] = cat3(p1[0], p1[64], p1[128]);
-    s[0] = *(const uint16_t *)(asc0 + (int64_t)st * kActScaleStep);
-    s[1] = *(const uint16_t *)(asc1 + (int64_t)st * kActScaleStep);
+    s[0] = *(const uint32_t *)(asc0 + (int64_t)st * kActScaleStep);
+    s[1] = *(const uint32_t *)(asc1 + (int64_t)st * kActScaleStep);
   };
-  auto compute = [&](auto seg, const u12 (&x)[2], const uint32_t (&s)[2], int buf)
-      __attribute__((always_inline)) {
+  // One column tile of the step's instructions (both row tiles).
+  auto mul_tile = [&](auto seg, const u12 (&x)[2], const uint32_t (&s)[2], u12 w, int sw,
+                      int tn) __attribute__((always_inline)) {
     constexpr int SEG = decltype(seg)::v;
-    const uint32_t *scl = (const uint32_t *)&Wl[buf][768];
+    constexpr int NK = SEG == 1 ? 4 : 2;
 #pragma unroll
-    for (int tn = 0; tn < 4; ++tn) {
-      const int c = tn * 32 + l32;
-      const u12 w = cat3(Wl[buf][lh * 128 + c], Wl[buf][256 + lh * 128 + c],
-                         Wl[buf][512 + lh * 128 + c]);
-      const int sw = (int)scl[lh * 128 + c];
+    for (int k = 0; k < NK; ++k)
 #pragma unroll
       for (int tm = 0; tm < 2; ++tm) {
         const int sa = (int)s[tm];
-        if (SEG == 0) {            // two block pairs, scale bytes 0 and 1
-          acc[tm][tn] = mma<kFmtFp6, 0, 0>(fp6_lo(x[tm]), fp6_lo(w), acc[tm][tn], sa, sw);
-          acc[tm][tn] = mma<kFmtFp6, 1, 1>(fp6_hi(x[tm]), fp6_hi(w), acc[tm][tn], sa, sw);
-        } else if (SEG == 1) {     // digit products hh, ll, hl, lh
-          acc[tm][tn] = mma<kFmtFp6, 0, 0>(fp6_lo(x[tm]), fp6_lo(w), acc[tm][tn], sa, sw);
-          acc[tm][tn] = mma<kFmtFp6, 0, 0>(fp6_hi(x[tm]), fp6_hi(w), acc[tm][tn], sa, sw);
-          acc[tm][tn] = mma<kFmtFp6, 0, 0>(fp6_lo(x[tm]), fp6_hi(w), acc[tm][tn], sa, sw);
-          acc[tm][tn] = mma<kFmtFp6, 0, 0>(fp6_hi(x[tm]), fp6_lo(w), acc[tm][tn], sa, sw);
-        } else {                   // [h|l].[h|l] and [h|l].[l|h]
-          acc[tm][tn] = mma<kFmtFp8, 0, 0>(fp8_lo(x[tm]), fp8_lo(w), acc[tm][tn], sa, sw);
-          acc[tm][tn] = mma<kFmtFp8, 0, 0>(fp8_lo(x[tm]), fp8_hi(w), acc[tm][tn], sa, sw);
+        v16f &c = acc[tm][tn];
+        if (SEG == 0) {          // block pairs (4s', 4s'+1), (4s'+2, 4s'+3): scale bytes 0, 1
+          if (k == 0) c = mma<kFmtFp6, 0, 0>(fp6_lo(x[tm]), fp6_lo(w), c, sa, sw);
+          else c = mma<kFmtFp6, 1, 1>(fp6_hi(x[tm]), fp6_hi(w), c, sa, sw);
+        } else if (SEG == 1) {   // digit products hh, ll, hl, lh
+          const v8i av = (k == 0 || k == 2) ? fp6_lo(x[tm]) : fp6_hi(x[tm]);
+          const v8i wv = (k == 0 || k == 3) ? fp6_lo(w) : fp6_hi(w);
+          c = mma<kFmtFp6, 0, 0>(av, wv, c, sa, sw);
+        } else {                 // [h|l].[h|l], [h|l].[l|h]
+          c = mma<kFmtFp8, 0, 0>(fp8_lo(x[tm]), k == 0 ? fp8_lo(w) : fp8_hi(w), c, sa, sw);
         }
       }
+  };
+  auto compute = [&](auto seg, const u12 (&x)[2], const uint32_t (&s)[2], int buf)
+      __attribute__((always_inline)) {
+    const u4 *W = Wl[buf][kg];
+    const uint32_t *scl = (const uint32_t *)&W[768];
+#pragma unroll
+    for (int tn = 0; tn < 4; ++tn) {
+      const int c = tn * 32 + l32;
+      const u12 w = cat3(W[lh * 128 + c], W[256 + lh * 128 + c], W[512 + lh * 128 + c]);
+      mul_tile(seg, x, s, w, (int)scl[lh * 128 + c], tn);
+      // one column tile's operands live at a time (the other wave on the
+      // SIMD covers the LDS latency)
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
-  // Step st: W chunk st in Wl[st&1]; stage st+1 into the other buffer and
-  // fetch st+3; fetch A of st+2; multiply step st.
-  auto iteration = [&](auto seg, int st, u4 (&wst)[4], const u12 (&xc)[2],
-                       const uint32_t (&sc)[2], u12 (&xn)[2], uint32_t (&sn)[2])
-      __attribute__((always_inline)) {
+  // Iteration i: the group's chunk of step own(i) is in Wl[i & 1][kg] and
+  // its A data in xc; stage the chunk of own(i+1) into Wl[(i+1) & 1][kg],
+  // fetch the chunk of own(i+2) and the A data of own(i+1); multiply own(i)
+  // unless it lies past the last step.  Group 0 fetches first and group 1
+  // multiplies first, so that after each barrier one group streams memory
+  // while the other keeps the matrix cores busy.
+  auto iteration = [&](auto seg, int i, const u12 (&xc)[2], const uint32_t (&sc)[2],
+                       u12 (&xn)[2], uint32_t (&sn)[2]) __attribute__((always_inline)) {
     __syncthreads();
-    // Unconditional (clamped) so that every path issues the same memory
-    // operations: past the end they refetch the last step, which is unused.
-    store_w(wst, (st + 1) & 1);
-    load_w(min(st + 3, nsteps - 1), wst);
-    load_a(min(st + 2, nsteps - 1), xn, sn);
-    // keep the prefetches here: the compiler may not sink them to their uses
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_sched_barrier(0);
-    compute(seg, xc, sc, st & 1);
+    const bool mul = 2 * i + kg < nsteps;
+    if (kg == 1 && mul) compute(seg, xc, sc, i & 1);
+    store_w((i + 1) & 1);
+    load_w(own(i + 2));
+    load_a(own(i + 1), xn, sn);
+    if (kg == 0 && mul) compute(seg, xc, sc, i & 1);
   };
-  // Steps [begin, end) of one segment, six per trip so that the ring slots
-  // are compile-time registers (relative to begin).  Every iteration issues
-  // the same memory operations whatever the branches, which keeps the
-  // compiler's memory-counter waits tight.
-  auto run = [&](auto seg, int begin, int end) __attribute__((always_inline)) {
-    for (int st = begin; st < end; st += 6) {
-      iteration(seg, st, ws[1], xa[0], xs[0], xa[2], xs[2]);
-      if (st + 1 < end) iteration(seg, st + 1, ws[0], xa[1], xs[1], xa[0], xs[0]);
-      if (st + 2 < end) iteration(seg, st + 2, ws[1], xa[2], xs[2], xa[1], xs[1]);
-      if (st + 3 < end) iteration(seg, st + 3, ws[0], xa[0], xs[0], xa[2], xs[2]);
-      if (st + 4 < end) iteration(seg, st + 4, ws[1], xa[1], xs[1], xa[0], xs[0]);
-      if (st + 5 < end) iteration(seg, st + 5, ws[0], xa[2], xs[2], xa[1], xs[1]);
+  // Iterations [ib, ie) whose own steps lie in one segment; ring slots
+  // relative to ib.
+  auto run = [&](auto seg, int ib, int ie) __attribute__((always_inline)) {
+    for (int i = ib; i < ie; i += 2) {
+      iteration(seg, i, xa[0], xs[0], xa[1], xs[1]);
+      if (i + 1 < ie) iteration(seg, i + 1, xa[1], xs[1], xa[0], xs[0]);
     }
   };
-  // After a segment of n steps, step st sits in slot (st - begin) % 3 (A) and
-  // (st - begin) % 2 (W); the next segment numbers it st - end: rotate.
+  // After n iterations the next iteration's A data sits in slot n % 2.
   auto realign = [&](int n) __attribute__((always_inline)) {
-    const int ra3 = n % 3;
-    if (ra3 == 1) {                        // new slot k <- old slot (k + 1) % 3
-      const u12 t0 = xa[0][0], t1 = xa[0][1];
-      const uint32_t s0 = xs[0][0], s1 = xs[0][1];
-      xa[0][0] = xa[1][0]; xa[0][1] = xa[1][1]; xs[0][0] = xs[1][0]; xs[0][1] = xs[1][1];
-      xa[1][0] = xa[2][0]; xa[1][1] = xa[2][1]; xs[1][0] = xs[2][0]; xs[1][1] = xs[2][1];
-      xa[2][0] = t0; xa[2][1] = t1; xs[2][0] = s0; xs[2][1] = s1;
-    } else if (ra3 == 2) {                 // new slot k <- old slot (k + 2) % 3
-      const u12 t0 = xa[2][0], t1 = xa[2][1];
-      const uint32_t s0 = xs[2][0], s1 = xs[2][1];
-      xa[2][0] = xa[1][0]; xa[2][1] = xa[1][1]; xs[2][0] = xs[1][0]; xs[2][1] = xs[1][1];
-      xa[1][0] = xa[0][0]; xa[1][1] = xa[0][1]; xs[1][0] = xs[0][0]; xs[1][1] = xs[0][1];
-      xa[0][0] = t0; xa[0][1] = t1; xs[0][0] = s0; xs[0][1] = s1;
-    }
     if (n & 1) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const u4 tw = ws[0][j];
-        ws[0][j] = ws[1][j];
-        ws[1][j] = tw;
+      for (int j = 0; j < 2; ++j) {
+        const u12 tx = xa[0][j];
+        xa[0][j] = xa[1][j];
+        xa[1][j] = tx;
+        const uint32_t tsc = xs[0][j];
+        xs[0][j] = xs[1][j];
+        xs[1][j] = tsc;
       }
     }
   };
 
-  // Prologue: W chunks of steps 0, 1, 2 in flight, step 0 in LDS; A of 0, 1.
-  load_w(0, ws[0]);
-  if (nsteps > 1) load_w(1, ws[1]);
-  load_a(0, xa[0], xs[0]);
-  if (nsteps > 1) load_a(1, xa[1], xs[1]);
-  store_w(ws[0], 0);
-  if (nsteps > 2) load_w(2, ws[0]);
+  // Prologue: the group's chunk of own(0) in LDS, own(1)'s in the staging
+  // registers, A of own(0).
+  load_w(own(0));
+  load_a(own(0), xa[0], xs[0]);
+  store_w(0);
+  load_w(own(1));
 
+  // Iteration ranges of the group's own steps per segment: own step 2i+kg
+  // is in segment 0 while 2i+kg < e4, and so on.
   const int e4 = og.s4, e6 = og.s4 + og.s6;
-  run(Seg<0>{}, 0, e4);
-  realign(e4);
-  run(Seg<1>{}, e4, e6);
-  realign(e6 - e4);
-  run(Seg<2>{}, e6, nsteps);
+  const int i4 = (e4 - kg + 1) / 2, i6 = max(i4, (e6 - kg + 1) / 2);
+  run(Seg<0>{}, 0, i4);
+  realign(i4);
+  run(Seg<1>{}, i4, i6);
+  realign(i6 - i4);
+  run(Seg<2>{}, i6, niter);
 
+  // Sum the two groups: group g finishes row tile tm = g of its row block;
+  // each wave hands its other row tile to the partner wave through LDS.
+  __syncthreads();
+  float *red = (float *)smem;              // [row block][tm][tn][r][lane]
+  auto finish = [&](auto mine_tag) __attribute__((always_inline)) {
+    constexpr int MINE = decltype(mine_tag)::v, OTHER = 1 - MINE;
 #pragma unroll
-  for (int tm = 0; tm < 2; ++tm)
+    for (int tn = 0; tn < 4; ++tn)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        red[(((rw * 2 + OTHER) * 4 + tn) * 16 + r) * 64 + lane] = acc[OTHER][tn][r];
+    __syncthreads();
 #pragma unroll
     for (int tn = 0; tn < 4; ++tn) {
       const int64_t j = col0 + tn * 32 + l32;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t i = row0 + wave * 64 + tm * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-        if (i < g.M && j < g.N) g.y[i * g.ldy + j] = acc[tm][tn][r];
+        const float v = acc[MINE][tn][r] + red[(((rw * 2 + MINE) * 4 + tn) * 16 + r) * 64 + lane];
+        const int64_t i = row0 + rw * 64 + MINE * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+        if (i < g.M && j < g.N) g.y[i * g.ldy + j] = v;
       }
     }
+  };
+  if (kg == 0) finish(Seg<0>{});
+  else finish(Seg<1>{});
 }
 
 }  // namespace

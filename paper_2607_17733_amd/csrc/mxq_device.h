@@ -260,7 +260,7 @@ struct OpGeo {
 constexpr int kOpCols = 128;
 constexpr int kActRows = 32;
 constexpr int kActStep = 3072;       // operand bytes per (32-row tile, step)
-constexpr int kActScaleStep = 128;   // scale bytes per (32-row tile, step)
+constexpr int kActScaleStep = 256;   // scale bytes per (32-row tile, step)
 
 // Activation operand image: byte o (0..47) of lane data (row, st, h), and
 // scale byte j (0, 1) of (row, st, h).
@@ -269,7 +269,7 @@ __host__ __device__ inline int64_t act_op_loc(int64_t row, int st, int nsteps, i
          (row & 31) * 16 + (o & 15);
 }
 __host__ __device__ inline int64_t act_sc_loc(int64_t row, int st, int nsteps, int h, int j) {
-  return ((row >> 5) * nsteps + st) * (int64_t)kActScaleStep + h * 64 + (row & 31) * 2 + j;
+  return ((row >> 5) * nsteps + st) * (int64_t)kActScaleStep + h * 128 + (row & 31) * 4 + j;
 }
 __host__ __device__ inline int64_t act_op_bytes(const OpGeo &o, int64_t rows) {
   return (rows + kActRows - 1) / kActRows * o.nsteps * (int64_t)kActStep;

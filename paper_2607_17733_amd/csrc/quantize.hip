@@ -194,11 +194,12 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
       if (kg == 0) {                         // scale bytes: [tile, step][half][row][2]
         if (bi.m == 4) {
           sc[act_sc_loc(row, st, ns, h, j)] = (uint8_t)E;
+          if (j == 0) *(uint16_t *)(sc + act_sc_loc(row, st, ns, h, 2)) = 0;
         } else if (bi.m == 6) {
-          *(uint16_t *)(sc + act_sc_loc(row, st, ns, h, 0)) = (uint16_t)E;
+          *(uint32_t *)(sc + act_sc_loc(row, st, ns, h, 0)) = (uint32_t)E;
         } else {
-          *(uint16_t *)(sc + act_sc_loc(row, st, ns, 0, 0)) = (uint16_t)E;
-          *(uint16_t *)(sc + act_sc_loc(row, st, ns, 1, 0)) = (uint16_t)E;
+          *(uint32_t *)(sc + act_sc_loc(row, st, ns, 0, 0)) = (uint32_t)E;
+          *(uint32_t *)(sc + act_sc_loc(row, st, ns, 1, 0)) = (uint32_t)E;
         }
       }
       if (g == 0) {                          // zero the row padding
@@ -210,12 +211,13 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
           for (int z = 0; z < 24; z += 2)
             *(uint16_t *)(op + act_op_loc(row, pst, ns, ph, 24 * pj + z)) = 0;
           sc[act_sc_loc(row, pst, ns, ph, pj)] = 0;
+          if (pj == 0) *(uint16_t *)(sc + act_sc_loc(row, pst, ns, ph, 2)) = 0;
         }
         if (og.n6p > og.n6) {                  // 6-bit pad block (odd count)
           const int pst = og.s4 + (og.n6 >> 1);
           for (int z = 0; z < 48; z += 2)
             *(uint16_t *)(op + act_op_loc(row, pst, ns, 1, z)) = 0;
-          *(uint16_t *)(sc + act_sc_loc(row, pst, ns, 1, 0)) = 0;
+          *(uint32_t *)(sc + act_sc_loc(row, pst, ns, 1, 0)) = 0;
         }
       }
     } else {

@@ -127,7 +127,7 @@ def _decode_steps(geo, nb, rows, lane_of, scale_of, weights):
     return q, E, ok
 
 
-ACT_STEP, ACT_SCALE_STEP, ACT_ROWS = 3072, 128, 32
+ACT_STEP, ACT_SCALE_STEP, ACT_ROWS = 3072, 256, 32
 
 
 def decode_act(op_img: np.ndarray, sc_img: np.ndarray, widths, M: int):
@@ -138,15 +138,19 @@ def decode_act(op_img: np.ndarray, sc_img: np.ndarray, widths, M: int):
     assert op_img.size == nt * geo.nsteps * ACT_STEP
     assert sc_img.size == nt * geo.nsteps * ACT_SCALE_STEP
     t = op_img.reshape(nt, geo.nsteps, 3, 2, ACT_ROWS, 16)
-    sct = sc_img.reshape(nt, geo.nsteps, 2, ACT_ROWS, 2)
+    sct = sc_img.reshape(nt, geo.nsteps, 2, ACT_ROWS, 4)
 
     def lane_of(st, h):
         return t[:, st, :, h].transpose(0, 2, 1, 3).reshape(nt * ACT_ROWS, 48)[:M]
 
     def scale_of(st, h):
-        return sct[:, st, h].reshape(nt * ACT_ROWS, 2)[:M]
+        return sct[:, st, h].reshape(nt * ACT_ROWS, 4)[:M]
 
-    return _decode_steps(geo, len(widths), M, lane_of, scale_of, weights=False)
+    q, E, ok = _decode_steps(geo, len(widths), M, lane_of, scale_of, weights=False)
+    for st in range(geo.nsteps):
+        for h in (0, 1):
+            ok &= not scale_of(st, h)[:, 2:].any()
+    return q, E, ok
 
 
 def w_lane_bytes(img: np.ndarray, geo: Geo, st: int, h: int):

@@ -67,9 +67,9 @@ def test_sizes(lib):
     assert lib.mxq_act_bytes(ctypes.byref(f), 33) == 33 * 160 + 2 * 4 * 3072
     assert lib.mxq_act_bytes(ctypes.byref(f), 0) == 0
     assert lib.mxq_act_bytes(ctypes.byref(f), -1) == -2
-    # M exponent rows + 128 scale bytes per (tile, step)
-    assert lib.mxq_act_exp_bytes(ctypes.byref(f), 16) == 16 * 16 + 1 * 4 * 128
-    assert lib.mxq_act_exp_bytes(ctypes.byref(f), 64) == 64 * 16 + 2 * 4 * 128
+    # M exponent rows + 256 scale bytes per (tile, step)
+    assert lib.mxq_act_exp_bytes(ctypes.byref(f), 16) == 16 * 16 + 1 * 4 * 256
+    assert lib.mxq_act_exp_bytes(ctypes.byref(f), 64) == 64 * 16 + 2 * 4 * 256
     # packed slabs (N to 16) + 64-byte tail + 128-column operand tiles of
     # 13312 bytes per step
     assert lib.mxq_weight_bytes(ctypes.byref(f), 256) == 256 * 152 + 64 + 2 * 4 * 13312
@@ -82,7 +82,7 @@ def test_sizes(lib):
     assert lib.mxq_act_packed_bytes(ctypes.byref(f2)) == 2368   # 2360 rounded up to 16
     assert lib.mxq_exp_row_bytes(ctypes.byref(f2)) == 128
     assert lib.mxq_act_bytes(ctypes.byref(f2), 2048) == 2048 * 2368 + 64 * 46 * 3072
-    assert lib.mxq_act_exp_bytes(ctypes.byref(f2), 2048) == 2048 * 128 + 64 * 46 * 128
+    assert lib.mxq_act_exp_bytes(ctypes.byref(f2), 2048) == 2048 * 128 + 64 * 46 * 256
 
 
 def test_size_functions_match_oracle_layout(lib, oracle_lib):
