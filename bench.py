@@ -11,9 +11,9 @@ before timing (offline step, reported separately).
 Printed as one JSON line: the step throughput (effective TOPS = 2*M*N*K per
 step time), the GEMM kernel against the int8 matrix-core roofline (its
 duration from HIP events on the launch stream inside the timed region), the
-decode-shape GEMM against the HBM roofline (K=8192, N=28672, M=16, four
-weight copies rotated so the 256 MB last-level cache cannot hold them), and
-the CPU oracle timed on the host on a bounded sample.
+decode-shape GEMMs against the HBM roofline (M = 1, 4, 16 against both
+LLaMA-2-70B shapes, four weight copies rotated so the 256 MB last-level cache
+cannot hold them), and the CPU oracle timed on the host on a bounded sample.
 """
 from __future__ import annotations
 
@@ -30,6 +30,14 @@ if ROOT not in sys.path:
 INT8_PEAK_TOPS = 5000.0          # MI355X dense int8 matrix-core peak
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
 
+# Sources of the prefill GEMM kernel: the HBM traffic stored under profiles/
+# was counted on a build of exactly these files (sha256 of their contents).
+GEMM_SOURCES = ("paper_2607_17733_amd/csrc/gemm_prefill.hip",
+                "paper_2607_17733_amd/csrc/mxq_device.h",
+                "paper_2607_17733_amd/csrc/mxq_internal.h",
+                "paper_2607_17733_amd/csrc/api.cpp")
+TRAFFIC_FILE = "profiles/traffic_gemm_prefill_attn_2048x4096x4096.json"
+
 
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
@@ -39,6 +47,43 @@ def bf16_dev(bits, dev):
     import numpy as np
     import torch
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
+
+
+def sources_sha256(paths=GEMM_SOURCES) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(p.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per launch of the prefill GEMM from the committed counter
+    summary (FETCH_SIZE + WRITE_SIZE, scaled by the same counters on a plain
+    copy of known size), or None when the kernel sources changed since."""
+    path = os.path.join(ROOT, TRAFFIC_FILE)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("sources_sha256") != sources_sha256():
+        return None
+    return rec.get("traffic_bytes")
+
+
+def copy_calibration(dev, mib: int = 512, reps: int = 5):
+    """A plain device-to-device copy of known size, for scaling the HBM
+    byte counters (run under rocprofv3 --pmc)."""
+    import torch
+    n = mib << 20
+    src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "reps": reps}),
+          flush=True)
 
 
 def cpu_baseline(case, budget_s: float = 12.0):
@@ -69,12 +114,14 @@ def cpu_baseline(case, budget_s: float = 12.0):
                       (case.M, t_quant, rows, case.M, t_gemm)}
 
 
-def decode_bench(dev, reps: int = 50):
-    """Decode GEMM (M=16, K=8192, N=28672) streaming packed weights."""
+def decode_bench(dev, which: str = "up", reps: int = 50):
+    """Decode GEMM (M in 1, 4, 16) streaming packed weights of one
+    LLaMA-2-70B-shaped linear ("up": K=8192, N=28672; "down": K=28672,
+    N=8192)."""
     import torch
     from paper_2607_17733_amd import mxq
     from paper_2607_17733_amd import workloads as W
-    case = W.decode(16, "up")
+    case = W.decode(16, which)
     fmt = mxq.Format(case.K, case.widths, torch.from_numpy(case.perm).to(dev))
     wm0, we0 = mxq.pack_weights(bf16_dev(case.w_bits, dev), fmt)
     copies = [(wm0, we0)] + [(wm0.clone(), we0.clone()) for _ in range(3)]
@@ -103,9 +150,11 @@ def decode_bench(dev, reps: int = 50):
         gbs = w_bytes / (ms * 1e-3) / 1e9
         out["M%d" % M] = {"us": ms * 1e3, "packed_weight_GBps": gbs,
                           "frac_hbm_peak": gbs / HBM_PEAK_GBS}
-    out["workload"] = "llama2_70b up-proj decode K=8192 N=28672 widths 217/26/13, " \
+    out["workload"] = "LLaMA-2-70B %s-projection decode K=%d N=%d widths %d/%d/%d, " \
                       "4 weight buffers rotated (%.1f MB of packed weights and " \
-                      "exponents streamed per launch)" % (w_bytes / 1e6)
+                      "exponents streamed per launch)" % (
+                          which, case.K, case.N, case.meta["n4"], case.meta["n6"],
+                          case.meta["n8"], w_bytes / 1e6)
     out["packed_weight_bytes"] = w_bytes
     return out
 
@@ -117,6 +166,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 512 MiB device copy (counter scaling)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the MXINT quantize + GEMM path is "
@@ -132,6 +183,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     log("device", torch.cuda.get_device_name(dev))
+    if args.copy_calibration:
+        copy_calibration(dev)
+        return
     case = W.attn_proj()
     M, K, N = case.M, case.K, case.N
     log("workload", case.name, M, K, N, case.meta)
@@ -220,7 +274,7 @@ def main():
             "peak": INT8_PEAK_TOPS,
             "unit": "TOP/s",
             "frac": gemm_tops / INT8_PEAK_TOPS,
-            "traffic": None,
+            "traffic": measured_traffic(),
             "algorithmic": "2*M*N*K = %.4g ops per launch (MXINT multiply-adds, "
                            "against the dense int8 peak)" % ops,
             "avg_launch_us": gemm_ms * 1e3,
@@ -234,7 +288,8 @@ def main():
     }
     if not args.no_decode:
         log("decode bench")
-        result["decode"] = decode_bench(dev)
+        result["decode"] = {"up": decode_bench(dev, "up"),
+                            "down": decode_bench(dev, "down")}
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         result["cpu_baseline"] = cpu_baseline(case)
