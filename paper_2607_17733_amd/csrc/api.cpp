@@ -108,16 +108,19 @@ mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows
   a.row_used = row_used(s);
   a.tail_pad = weights ? (int)kWeightTailPad : 0;
   a.vec16 = (ld % 8 == 0) ? 1 : 0;
+  if (!weights) {
+    // the activation quantizer stages its rows in LDS: one row must fit
+    const mxq::OpGeo og = op_geo(s);
+    if (mxq::quantize_act_lds(fmt->K, og.n4p + og.n6p + og.n8, fmt->perm != nullptr) >
+        mxq::kMaxLds)
+      return MXQ_ERR_UNSUPPORTED;
+    return launched(mxq::launch_quantize_act(a, (hipStream_t)stream));
+  }
   // Stage source rows in LDS for the permutation gather when they fit;
   // longer rows gather straight from global memory.
   const int R = mxq::quantize_rows_per_wg(fmt->K);
-  if (weights) {
-    a.stage = (fmt->perm && (int64_t)R * fmt->K * 2 <= mxq::kMaxLds) ? 1 : 0;
-  } else {
-    a.stage = (fmt->perm && mxq::quantize_act_lds(1, R, fmt->K) <= mxq::kMaxLds) ? 1 : 0;
-    if (mxq::quantize_act_lds(a.stage, R, fmt->K) > mxq::kMaxLds) return MXQ_ERR_UNSUPPORTED;
-  }
-  return launched(mxq::launch_quantize(a, weights, (hipStream_t)stream));
+  a.stage = (fmt->perm && (int64_t)R * fmt->K * 2 <= mxq::kMaxLds) ? 1 : 0;
+  return launched(mxq::launch_quantize(a, true, (hipStream_t)stream));
 }
 
 mxq_status gemm_args(const mxq_fmt *fmt, int64_t M, int64_t N, const uint8_t *a_mant,

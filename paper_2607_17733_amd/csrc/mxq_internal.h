@@ -29,9 +29,11 @@ struct QuantArgs {
   int64_t w_op;            // weights: offset of the operand image in the buffer
   int64_t w_tile;          // weights: bytes per 128-column operand tile
   int tail_pad;            // weights: zero bytes after the last slab
-  int stage;               // stage source rows in LDS before the gather
+  int stage;               // weights: stage source rows in LDS before the gather;
+                           // activations: stage the permutation in LDS
   int vec16;               // 16-byte source loads are aligned
   int rows_per_wg;         // filled by the launcher
+  int lg_rows;             // activations: log2 of the rows per group
 };
 
 struct GemmArgs {
@@ -66,8 +68,10 @@ struct UnpackArgs {
 constexpr int64_t kMaxLds = 160 * 1024;   // LDS per workgroup on gfx950
 
 hipError_t launch_quantize(const QuantArgs &args, bool weights, hipStream_t s);
-int64_t quantize_act_lds(int stage, int rows_per_wg, int64_t K);
 int quantize_rows_per_wg(int64_t K);
+hipError_t launch_quantize_act(const QuantArgs &args, hipStream_t s);
+int quantize_act_rows(int64_t K, int padded_blocks, bool perm);
+int64_t quantize_act_lds(int64_t K, int padded_blocks, bool perm);
 hipError_t launch_gemm_prefill(const GemmArgs &args, hipStream_t s);
 hipError_t launch_gemm_partials(const GemmArgs &args, hipStream_t s);
 hipError_t launch_gemm_decode(const GemmArgs &args, hipStream_t s);

@@ -1,9 +1,8 @@
-// quantize.hip -- fused MXINT quantize + bit-pack of bf16 rows.
+// quantize.hip -- offline MXINT quantize + pack of bf16 weight rows.
 //
-// One kernel serves the online activation quantizer and the offline weight
-// packer.  MXSens (arXiv 2607.17733) Section 2 and Section 4.1: every
-// 32-element block of the permuted row gets one shared exponent and one
-// mantissa width.
+// MXSens (arXiv 2607.17733) Section 2 and Section 4.1: every 32-element
+// block of the permuted weight row (one output column) gets one shared
+// exponent and one mantissa width, the same quantizer as the activations.
 //
 // Work decomposition: a thread owns 8 consecutive elements of a block (a
 // "group"), so the 4 threads of a block are adjacent lanes; the block
@@ -13,11 +12,10 @@
 // stages its source rows in LDS with 16-byte coalesced loads and gathers from
 // LDS, so the permutation never turns into scattered global loads.
 //
-// Every row also gets its matrix-core operand image (FP6/FP8 digits of each
-// mantissa, the layout described with OpGeo) and the per-step E8M0 scale
-// bytes, so the prefill GEMM reads ready operands: activations right after
-// the packed section of the row, weights as 128-column tiles after the packed
-// slabs.
+// Every column is written twice: into the packed 16-column slabs the decode
+// GEMM streams, and into the 128-column tiles of the matrix-core operand
+// image (FP6/FP8 digits of each mantissa, the layout described with OpGeo)
+// with their E8M0 scale bytes, which the prefill GEMM reads.
 #include "mxq_device.h"
 #include "mxq_internal.h"
 
@@ -27,7 +25,6 @@ namespace {
 
 constexpr int kThreads = 256;
 
-template <bool WEIGHTS>
 __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int t = threadIdx.x;
@@ -147,80 +144,7 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
     else if (bi.m == 6) { st = og.s4 + (bi.idx >> 1); h = bi.idx & 1; }
     else { st = og.s4 + og.s6 + bi.idx; h = kg >> 1; }
 
-    if (!WEIGHTS) {
-      uint8_t *dst = q.mant + row * q.out_rb + bi.aoff;
-      if (bi.m == 4) {
-        *(uint32_t *)(dst + 4 * kg) = nib;
-      } else if (bi.m == 6) {
-        *(uint32_t *)(dst + 4 * kg) = nib;
-        if (!(kg & 1)) *(uint32_t *)(dst + 16 + 4 * (kg >> 1)) = top;
-      } else {
-        *(uint2 *)(dst + 8 * kg) = make_uint2(lo8, hi8);
-      }
-      uint8_t *erow_g = q.exp + row * q.out_erb;
-      if (kg == 0) erow_g[b] = (uint8_t)E;
-      // operand image (32-row tiles) and its scale bytes
-      uint8_t *op = q.mant + q.op_off;
-      uint8_t *sc = q.exp + q.sc_off;
-      const int ns = og.nsteps;
-      if (bi.m == 8) {
-        uint32_t h0 = 0, h1 = 0, l0 = 0, l1 = 0;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          h0 |= d0[u] << (8 * u); h1 |= d0[4 + u] << (8 * u);
-          l0 |= d1[u] << (8 * u); l1 |= d1[4 + u] << (8 * u);
-        }
-        const int o = 8 * (kg & 1);
-        *(uint2 *)(op + act_op_loc(row, st, ns, h, o)) = make_uint2(h0, h1);
-        *(uint2 *)(op + act_op_loc(row, st, ns, h, 16 + o)) = make_uint2(l0, l1);
-        if (!(kg & 1)) *(uint4 *)(op + act_op_loc(row, st, ns, h, 32)) = make_uint4(0, 0, 0, 0);
-      } else {
-        uint64_t v0 = 0, v1 = 0;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          v0 |= (uint64_t)d0[u] << (6 * u);
-          v1 |= (uint64_t)d1[u] << (6 * u);
-        }
-        const int o = (bi.m == 4 ? 24 * j : 0) + 6 * kg;
-#pragma unroll
-        for (int k = 0; k < 3; ++k)
-          *(uint16_t *)(op + act_op_loc(row, st, ns, h, o + 2 * k)) = (uint16_t)(v0 >> (16 * k));
-        if (bi.m == 6)
-#pragma unroll
-          for (int k = 0; k < 3; ++k)
-            *(uint16_t *)(op + act_op_loc(row, st, ns, h, 24 + o + 2 * k)) =
-                (uint16_t)(v1 >> (16 * k));
-      }
-      if (kg == 0) {                         // scale bytes: [tile, step][half][row][2]
-        if (bi.m == 4) {
-          sc[act_sc_loc(row, st, ns, h, j)] = (uint8_t)E;
-          if (j == 0) *(uint16_t *)(sc + act_sc_loc(row, st, ns, h, 2)) = 0;
-        } else if (bi.m == 6) {
-          *(uint32_t *)(sc + act_sc_loc(row, st, ns, h, 0)) = (uint32_t)E;
-        } else {
-          *(uint32_t *)(sc + act_sc_loc(row, st, ns, 0, 0)) = (uint32_t)E;
-          *(uint32_t *)(sc + act_sc_loc(row, st, ns, 1, 0)) = (uint32_t)E;
-        }
-      }
-      if (g == 0) {                          // zero the row padding
-        for (int64_t z = q.row_used; z < q.canon_rb; ++z)
-          q.mant[row * q.out_rb + z] = 0;
-        for (int64_t z = nb; z < q.canon_erb; ++z) erow_g[z] = 0;
-        for (int i = og.n4; i < og.n4p; ++i) {   // 4-bit pad blocks
-          const int pst = i >> 2, ph = i & 1, pj = (i >> 1) & 1;
-          for (int z = 0; z < 24; z += 2)
-            *(uint16_t *)(op + act_op_loc(row, pst, ns, ph, 24 * pj + z)) = 0;
-          sc[act_sc_loc(row, pst, ns, ph, pj)] = 0;
-          if (pj == 0) *(uint16_t *)(sc + act_sc_loc(row, pst, ns, ph, 2)) = 0;
-        }
-        if (og.n6p > og.n6) {                  // 6-bit pad block (odd count)
-          const int pst = og.s4 + (og.n6 >> 1);
-          for (int z = 0; z < 48; z += 2)
-            *(uint16_t *)(op + act_op_loc(row, pst, ns, 1, z)) = 0;
-          *(uint32_t *)(sc + act_sc_loc(row, pst, ns, 1, 0)) = 0;
-        }
-      }
-    } else {
+    {
       const int c = (int)(row % kOpCols);
       uint8_t *tile = q.mant + q.w_op + (row / kOpCols) * q.w_tile;
       if (row < q.slab_rows) {
@@ -307,6 +231,7 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
 
 hipError_t launch_quantize(const QuantArgs &args, bool weights,
                            hipStream_t stream) {
+  if (!weights) return hipErrorInvalidValue;     // activations: launch_quantize_act
   const int64_t K = args.K;
   const int nb = (int)(K / kBlock);
   const int G = 4 * nb;
@@ -314,28 +239,13 @@ hipError_t launch_quantize(const QuantArgs &args, bool weights,
   a.rows_per_wg = G >= kThreads ? 1 : kThreads / G;
   const int64_t grid = (a.out_rows + a.rows_per_wg - 1) / a.rows_per_wg;
   if (grid <= 0) return hipSuccess;
-  if (weights) {
-    const int64_t lds = a.stage ? (int64_t)a.rows_per_wg * K * 2 : 0;
-    if (lds > kMaxLds) return hipErrorInvalidValue;
-    (void)hipFuncSetAttribute((const void *)quantize_kernel<true>,
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
-    hipLaunchKernelGGL(quantize_kernel<true>, dim3((unsigned)grid), dim3(kThreads),
-                       (size_t)lds, stream, a);
-  } else {
-    const int64_t lds = quantize_act_lds(a.stage, a.rows_per_wg, K);
-    if (lds > kMaxLds) return hipErrorInvalidValue;
-    (void)hipFuncSetAttribute((const void *)quantize_kernel<false>,
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
-    hipLaunchKernelGGL(quantize_kernel<false>, dim3((unsigned)grid), dim3(kThreads),
-                       (size_t)lds, stream, a);
-  }
+  const int64_t lds = a.stage ? (int64_t)a.rows_per_wg * K * 2 : 0;
+  if (lds > kMaxLds) return hipErrorInvalidValue;
+  (void)hipFuncSetAttribute((const void *)quantize_kernel,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
+  hipLaunchKernelGGL(quantize_kernel, dim3((unsigned)grid), dim3(kThreads),
+                     (size_t)lds, stream, a);
   return hipGetLastError();
-}
-
-int64_t quantize_act_lds(int stage, int rows_per_wg, int64_t K) {
-  const int64_t nb = K / kBlock;
-  (void)nb;
-  return stage ? (int64_t)rows_per_wg * 2 * K : 0;
 }
 
 int quantize_rows_per_wg(int64_t K) {

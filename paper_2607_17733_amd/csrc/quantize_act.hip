@@ -1,0 +1,383 @@
+// quantize_act.hip -- online MXINT quantization of bf16 activation rows.
+//
+// MXSens (arXiv 2607.17733) Section 2 and Section 4.1: every 32-element
+// block of the permuted row gets one shared exponent E = floor(log2 max|x|)
+// + 127 and mantissas of its own width m in {4, 6, 8}.
+//
+// Work decomposition.  A workgroup owns R consecutive rows (4 for K = 4096,
+// fewer for longer rows, up to 64 for short ones) and stages them in LDS with
+// 16-byte loads, together with the column permutation (as byte offsets into
+// a staged row) when it fits, so the permutation becomes an LDS gather.  A
+// thread owns one (row, block) and the workgroup has as many threads as
+// items (up to 1024), two workgroups per CU.  Lanes run over rows fastest,
+// so the rows of a block write contiguous runs of the 32-row operand tiles,
+// and consecutive workgroups (whole tiles) run on one XCD, whose L2 then
+// completes every line of the tile.
+//
+// Arithmetic.  The block maximum is taken on the integer |bf16| patterns (two
+// per register); the mantissas are computed in fp32, where every step is
+// exact: x * 2^-s scales an 8-bit significand by a power of two, rint and the
+// clamp act on integers below 2^8.  The packed row is assembled from the
+// integers' low bytes, four elements per register.  The operand image uses the gfx950 scaled FP6/FP8 conversions (the values
+// are exact in the target format, so they never round).
+#include "mxq_device.h"
+#include "mxq_internal.h"
+
+namespace mxq {
+
+namespace {
+
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef unsigned v6u __attribute__((ext_vector_type(6)));
+typedef short v2s __attribute__((ext_vector_type(2)));
+typedef unsigned short v2us __attribute__((ext_vector_type(2)));
+typedef unsigned u4 __attribute__((ext_vector_type(4)));
+typedef unsigned u2 __attribute__((ext_vector_type(2)));
+
+constexpr int kMaxThreads = 1024;
+constexpr int kLdsBudget = 72 * 1024;   // two workgroups per CU
+constexpr int kRowPad = 8;              // zero bf16 elements after each staged row
+
+// A block of 32 values kept as its even and odd elements (the register
+// layout the FP6 conversion takes).
+struct Blk {
+  v16f e, o;
+  __device__ float operator[](int t) const { return (t & 1) ? o[t >> 1] : e[t >> 1]; }
+};
+
+// 32 values / div as FP6 e3m2 codes, element t at bits 6t of 24 bytes (the
+// conversion interleaves its two 16-element inputs).
+__device__ inline v6u to_e3m2(const Blk &v, float div) {
+  return __builtin_amdgcn_cvt_scalef32_2xpk16_bf6_f32(v.e, v.o, div);
+}
+
+// Elements 16h..16h+15 / div as FP8 e4m3 codes, one byte each.
+__device__ inline u4 to_e4m3(const Blk &v, int h, float div) {
+  u4 r;
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const int t = 16 * h + 4 * d;
+    v2s z = {0, 0};
+    z = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(z, v[t], v[t + 1], div, false);
+    z = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(z, v[t + 2], v[t + 3], div, true);
+    r[d] = ((uint32_t)(uint16_t)z[1] << 16) | (uint16_t)z[0];
+  }
+  return r;
+}
+
+// Low bytes of the integers of elements t0, t0+step, t0+2step, t0+3step.
+__device__ inline uint32_t byte_lanes(const Blk &v, int t0, int step) {
+  return ((uint32_t)(int)v[t0] & 255u) | (((uint32_t)(int)v[t0 + step] & 255u) << 8) |
+         (((uint32_t)(int)v[t0 + 2 * step] & 255u) << 16) |
+         ((uint32_t)(int)v[t0 + 3 * step] << 24);
+}
+
+// Two's-complement nibbles of elements t0..t0+7 (element t0+t at bits 4t):
+// byte j takes element t0+2j in its low and t0+2j+1 in its high nibble.
+__device__ inline uint32_t nibbles8(const Blk &v, int t0) {
+  const uint32_t ev = byte_lanes(v, t0, 2), od = byte_lanes(v, t0 + 1, 2);
+  return (ev & 0x0F0F0F0Fu) | ((od & 0x0F0F0F0Fu) << 4);
+}
+
+// Two's-complement bytes of elements t0..t0+3.
+__device__ inline uint32_t bytes4(const Blk &v, int t0) { return byte_lanes(v, t0, 1); }
+
+// Top-bit word d of a 6-bit block (canonical packed layout): byte j holds
+// the signed top two bits (bits 4-5) of elements 16d+2j, 16d+2j+1,
+// 16d+8+2j, 16d+9+2j in bits 6-7, 4-5, 2-3, 0-1.
+__device__ inline uint32_t top_word(const Blk &v, int d) {
+  const uint32_t a = byte_lanes(v, 16 * d, 2), b = byte_lanes(v, 16 * d + 1, 2);
+  const uint32_t c = byte_lanes(v, 16 * d + 8, 2), e = byte_lanes(v, 16 * d + 9, 2);
+  return ((a & 0x30303030u) << 2) | (b & 0x30303030u) | ((c & 0x30303030u) >> 2) |
+         ((e & 0x30303030u) >> 4);
+}
+
+// One (row, block) item: gather, quantize, pack, write.  sr is the staged
+// row in LDS, soff the staged permutation (byte offsets) or null.
+template <bool RNA>
+__device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp,
+                                     int64_t row, const uint8_t *sr, const int32_t *soff) {
+  const int K = (int)q.K;
+  const int ns = og.nsteps;
+  int seg, idx, n;
+  if (bp < og.n4p) { seg = 0; idx = bp; n = og.n4; }
+  else if (bp < og.n4p + og.n6p) { seg = 1; idx = bp - og.n4p; n = og.n6; }
+  else { seg = 2; idx = bp - og.n4p - og.n6p; n = og.n8; }
+  const bool pad = idx >= n;
+  const int m = 4 + 2 * seg;
+  const int b = seg == 0 ? idx : (seg == 1 ? og.n4 + idx : og.n4 + og.n6 + idx);
+
+  // gather: pr[i] holds elements 2i (low half) and 2i+1 (high half)
+  uint32_t pr[16];
+  const int p0 = b * kBlock;
+  if (pad) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) pr[i] = 0;
+  } else if (!q.perm) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const u4 d = *(const u4 *)(sr + 2 * (p0 + 8 * u));
+#pragma unroll
+      for (int k = 0; k < 4; ++k) pr[4 * u + k] = d[k];
+    }
+  } else if (q.stage) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int4 o = *(const int4 *)(soff + p0 + 4 * u);
+      const uint32_t e0 = *(const uint16_t *)(sr + o.x);
+      const uint32_t e1 = *(const uint16_t *)(sr + o.y);
+      const uint32_t e2 = *(const uint16_t *)(sr + o.z);
+      const uint32_t e3 = *(const uint16_t *)(sr + o.w);
+      pr[2 * u] = e0 | (e1 << 16);
+      pr[2 * u + 1] = e2 | (e3 << 16);
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int4 p = *(const int4 *)(q.perm + p0 + 4 * u);
+      const int src[4] = {p.x, p.y, p.z, p.w};
+      uint32_t e[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        e[k] = (unsigned)src[k] < (unsigned)K ? *(const uint16_t *)(sr + 2 * src[k]) : 0u;
+      pr[2 * u] = e[0] | (e[1] << 16);
+      pr[2 * u + 1] = e[2] | (e[3] << 16);
+    }
+  }
+
+  // block exponent from the integer maximum of |bits|, two lanes at a time
+  v2us mx = {0, 0};
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const uint32_t a = pr[i] & 0x7FFF7FFFu;
+    mx = __builtin_elementwise_max(mx, __builtin_bit_cast(v2us, a));
+  }
+  const uint32_t amax = mx.x > mx.y ? mx.x : mx.y;
+  const int E = block_exponent(amax);
+
+  // mantissas as exact integer-valued floats: rint(x * 2^(127 + m - 2 - E)),
+  // clamped; a block holding Inf or NaN (E = 255) quantizes to zeros
+  Blk v;
+  if (E == 255) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v.e[i] = v.o[i] = 0.f;
+  } else {
+    const float qmax = seg == 0 ? 7.f : (seg == 1 ? 31.f : 127.f);
+    const float qmin = q.full_clamp ? -(qmax + 1.f) : -qmax;
+    const int sh = 127 + (m - 2) - E;
+#pragma unroll
+    for (int u = 0; u < 32; ++u) {
+      const uint32_t bits = (u & 1) ? (pr[u >> 1] & 0xFFFF0000u) : (pr[u >> 1] << 16);
+      float y = ldexpf(__uint_as_float(bits), sh);
+      if (RNA) {
+        const float tr = truncf(y);
+        y = fabsf(y - tr) >= 0.5f ? tr + copysignf(1.f, y) : tr;
+      } else {
+        y = rintf(y);
+      }
+      y = __builtin_amdgcn_fmed3f(y, qmin, qmax);
+      if (u & 1) v.o[u >> 1] = y; else v.e[u >> 1] = y;
+    }
+  }
+
+  uint8_t *prow = q.mant + row * q.out_rb;
+  uint8_t *op = q.mant + q.op_off + ((row >> 5) * ns) * (int64_t)kActStep + (row & 31) * 16;
+  uint8_t *sc = q.exp + q.sc_off + ((row >> 5) * ns) * (int64_t)kActScaleStep + (row & 31) * 4;
+  if (!pad) q.exp[row * q.out_erb + b] = (uint8_t)E;
+  const uint32_t Eu = pad ? 0u : (uint32_t)E;
+
+  if (seg == 0) {
+    const int st = idx >> 2, h = idx & 1, j = (idx >> 1) & 1;
+    uint8_t *o = op + st * kActStep + h * 512;
+    uint8_t *s = sc + st * kActScaleStep + h * 128;
+    if (!pad)
+      *(u4 *)(prow + 16LL * idx) =
+          u4{nibbles8(v, 0), nibbles8(v, 8), nibbles8(v, 16), nibbles8(v, 24)};
+    const v6u c = to_e3m2(v, 4.f);
+    if (j == 0) {
+      *(u4 *)o = u4{c[0], c[1], c[2], c[3]};
+      *(u2 *)(o + 1024) = u2{c[4], c[5]};
+      s[0] = (uint8_t)Eu;                    // byte 1 is the partner block's
+      *(uint16_t *)(s + 2) = 0;
+    } else {
+      *(u2 *)(o + 1024 + 8) = u2{c[0], c[1]};
+      *(u4 *)(o + 2048) = u4{c[2], c[3], c[4], c[5]};
+      s[1] = (uint8_t)Eu;
+    }
+  } else if (seg == 1) {
+    const int st = og.s4 + (idx >> 1), h = idx & 1;
+    uint8_t *o = op + st * kActStep + h * 512;
+    Blk hd, ld;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      hd.e[i] = floorf(v.e[i] * 0.125f);
+      hd.o[i] = floorf(v.o[i] * 0.125f);
+      ld.e[i] = fmaf(hd.e[i], -8.f, v.e[i]);
+      ld.o[i] = fmaf(hd.o[i], -8.f, v.o[i]);
+    }
+    if (!pad) {
+      uint8_t *p = prow + 16LL * og.n4 + 24LL * idx;
+      *(u2 *)p = u2{nibbles8(v, 0), nibbles8(v, 8)};
+      *(u2 *)(p + 8) = u2{nibbles8(v, 16), nibbles8(v, 24)};
+      *(u2 *)(p + 16) = u2{top_word(v, 0), top_word(v, 1)};
+    }
+    const v6u ch = to_e3m2(hd, 2.f);
+    const v6u cl = to_e3m2(ld, 16.f);
+    *(u4 *)o = u4{ch[0], ch[1], ch[2], ch[3]};
+    *(u4 *)(o + 1024) = u4{ch[4], ch[5], cl[0], cl[1]};
+    *(u4 *)(o + 2048) = u4{cl[2], cl[3], cl[4], cl[5]};
+    *(uint32_t *)(sc + st * kActScaleStep + h * 128) = Eu;
+  } else {
+    const int st = og.s4 + og.s6 + idx;
+    Blk hd, ld;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      hd.e[i] = floorf(v.e[i] * 0.0625f);
+      hd.o[i] = floorf(v.o[i] * 0.0625f);
+      ld.e[i] = fmaf(hd.e[i], -16.f, v.e[i]);
+      ld.o[i] = fmaf(hd.o[i], -16.f, v.o[i]);
+    }
+    uint8_t *p = prow + 16LL * og.n4 + 24LL * og.n6 + 32LL * idx;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+      *(u2 *)(p + 8 * d) = u2{bytes4(v, 8 * d), bytes4(v, 8 * d + 4)};
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      uint8_t *o = op + st * kActStep + h * 512;
+      *(u4 *)o = to_e4m3(hd, h, 4.f);
+      *(u4 *)(o + 1024) = to_e4m3(ld, h, 64.f);
+      *(u4 *)(o + 2048) = u4{0u, 0u, 0u, 0u};
+      *(uint32_t *)(sc + st * kActScaleStep + h * 128) = Eu;
+    }
+  }
+}
+
+template <bool RNA>
+__global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+  const int t = threadIdx.x;
+  const int nthr = blockDim.x;
+  const int K = (int)q.K;
+  const int rowB = 2 * (K + kRowPad);                // staged row stride (bytes)
+  const int lgR = q.lg_rows;
+  const int R = 1 << lgR;
+  const OpGeo og(q.n4, q.n6, q.n8);
+  const int nbp = og.n4p + og.n6p + og.n8;          // padded blocks per row
+  // XCD-aware order: consecutive row groups (whole 32-row operand tiles)
+  // stay on one XCD, so its L2 completes every line of the tile.
+  int64_t w = blockIdx.x;
+  const int64_t nwg = gridDim.x;
+  if ((nwg & 7) == 0) w = (w & 7) * (nwg >> 3) + (w >> 3);
+  const int64_t r0 = w << lgR;
+
+  // Stage the permutation as byte offsets into a staged row (entries outside
+  // [0, K) point at the zero padding after the row), and the rows.
+  int32_t *soff = (int32_t *)(smem + R * rowB);
+  if (q.stage) {
+    for (int v = t; v < K / 4; v += nthr) {
+      const int4 p = *(const int4 *)(q.perm + 4 * v);
+      int4 o;
+      o.x = (unsigned)p.x < (unsigned)K ? 2 * p.x : 2 * K;
+      o.y = (unsigned)p.y < (unsigned)K ? 2 * p.y : 2 * K;
+      o.z = (unsigned)p.z < (unsigned)K ? 2 * p.z : 2 * K;
+      o.w = (unsigned)p.w < (unsigned)K ? 2 * p.w : 2 * K;
+      *(int4 *)(soff + 4 * v) = o;
+    }
+  }
+  if (q.vec16) {
+    const int vpr = K / 8;
+    for (int lr = 0; lr < R; ++lr) {
+      const bool live = r0 + lr < q.src_rows;
+      const uint16_t *src = q.src + (r0 + lr) * q.ld;
+      for (int c = t; c < vpr; c += nthr) {
+        u4 d = {0u, 0u, 0u, 0u};
+        if (live) d = *(const u4 *)(src + 8 * c);
+        *(u4 *)(smem + lr * rowB + 16 * c) = d;
+      }
+    }
+  } else {
+    for (int lr = 0; lr < R; ++lr) {
+      const bool live = r0 + lr < q.src_rows;
+      const uint16_t *src = q.src + (r0 + lr) * q.ld;
+      for (int c = t; c < K; c += nthr)
+        *(uint16_t *)(smem + lr * rowB + 2 * c) = live ? src[c] : (uint16_t)0;
+    }
+  }
+  if (t < R) *(u4 *)(smem + t * rowB + 2 * K) = u4{0u, 0u, 0u, 0u};
+  __syncthreads();
+
+  for (int it = t; it < (nbp << lgR); it += nthr) {
+    const int bp = it >> lgR;
+    const int lr = it & (R - 1);
+    const int64_t row = r0 + lr;
+    if (row < q.out_rows)
+      quantize_item<RNA>(q, og, bp, row, smem + lr * rowB, q.stage ? soff : nullptr);
+  }
+  // zero the padding of the packed and exponent rows
+  if (t < R) {
+    const int64_t row = r0 + t;
+    if (row < q.out_rows) {
+      for (int64_t z = q.row_used; z < q.canon_rb; ++z) q.mant[row * q.out_rb + z] = 0;
+      for (int64_t z = og.n4 + og.n6 + og.n8; z < q.canon_erb; ++z)
+        q.exp[row * q.out_erb + z] = 0;
+    }
+  }
+}
+
+// The permutation is staged (as byte offsets) when it fits beside one row.
+bool stage_perm(int64_t K, bool perm) {
+  return perm && 2 * (K + kRowPad) + 4 * K <= kLdsBudget;
+}
+
+int padded_blocks(int n4, int n6, int n8) {
+  const OpGeo og(n4, n6, n8);
+  return og.n4p + og.n6p + og.n8;
+}
+
+}  // namespace
+
+// Rows per workgroup: the largest power of two (at most 64) whose staged
+// rows fit the LDS budget with at most kMaxThreads items.
+int quantize_act_rows(int64_t K, int nbp, bool perm) {
+  const int64_t per = 2 * (K + kRowPad);
+  const int64_t fixed = stage_perm(K, perm) ? 4 * K : 0;
+  int r = 1;
+  while (r < 64 && 2 * r * per + fixed <= kLdsBudget && (int64_t)nbp * 2 * r <= kMaxThreads)
+    r *= 2;
+  return r;
+}
+
+int64_t quantize_act_lds(int64_t K, int nbp, bool perm) {
+  return (int64_t)quantize_act_rows(K, nbp, perm) * 2 * (K + kRowPad) +
+         (stage_perm(K, perm) ? 4 * K : 0);
+}
+
+hipError_t launch_quantize_act(const QuantArgs &args, hipStream_t stream) {
+  QuantArgs a = args;
+  const bool perm = a.perm != nullptr;
+  const int nbp = padded_blocks(a.n4, a.n6, a.n8);
+  const int R = quantize_act_rows(a.K, nbp, perm);
+  int lg = 0;
+  while ((1 << lg) < R) ++lg;
+  a.lg_rows = lg;
+  a.rows_per_wg = R;
+  a.stage = stage_perm(a.K, perm) ? 1 : 0;
+  const int64_t grid = (a.out_rows + R - 1) / R;
+  if (grid <= 0) return hipSuccess;
+  const int64_t lds = quantize_act_lds(a.K, nbp, perm);
+  if (lds > kMaxLds) return hipErrorInvalidValue;
+  const int64_t items = (int64_t)nbp * R;
+  const int threads = (int)(items >= kMaxThreads ? kMaxThreads : (items + 63) / 64 * 64);
+  const void *fn = a.ties_away ? (const void *)quantize_act_kernel<true>
+                               : (const void *)quantize_act_kernel<false>;
+  (void)hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
+  if (a.ties_away)
+    hipLaunchKernelGGL(quantize_act_kernel<true>, dim3((unsigned)grid), dim3(threads),
+                       (size_t)lds, stream, a);
+  else
+    hipLaunchKernelGGL(quantize_act_kernel<false>, dim3((unsigned)grid), dim3(threads),
+                       (size_t)lds, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace mxq
