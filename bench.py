@@ -13,7 +13,9 @@ step time), the GEMM kernel against the int8 matrix-core roofline (its
 duration from HIP events on the launch stream inside the timed region), the
 decode-shape GEMMs against the HBM roofline (M = 1, 4, 16 against both
 LLaMA-2-70B shapes, four weight copies rotated so the 256 MB last-level cache
-cannot hold them), and the CPU oracle timed on the host on a bounded sample.
+cannot hold them), the LLaMA-2-70B-shaped decoder layer at M=8192 (seven
+quantize + GEMM pairs and the K/V cache quantize on one stream, both width
+variants), and the CPU oracle timed on the host on a bounded sample.
 """
 from __future__ import annotations
 
@@ -159,6 +161,45 @@ def decode_bench(dev, which: str = "up", reps: int = 50):
     return out
 
 
+def layer_bench(dev, sensitive: bool, reps: int = 5):
+    """The config-5 decoder layer: seven online quantize + GEMM pairs and the
+    K/V cache quantize on one stream (inputs drawn on the device, weights
+    packed once before timing)."""
+    import numpy as np
+    import torch
+    from paper_2607_17733_amd import workloads as W
+    from paper_2607_17733_amd.layer import LayerSequence, Linear
+    M = 8192
+    specs = W.layer_specs(sensitive)
+    linears, xs = [], []
+    for s in specs:
+        w = W.device_weights(s, dev)
+        linears.append(Linear(s.name, s.K, s.N, s.widths,
+                              torch.from_numpy(s.perm).to(dev), w))
+        del w
+        xs.append(W.device_activations(s, M, dev))
+    kv = [W.device_kv(0, dev), W.device_kv(1, dev)]
+    seq = LayerSequence(linears, M, dev)
+    for _ in range(2):
+        seq.run(xs, kv)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        seq.run(xs, kv)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    return {"ms": ms, "effective_TOPs": seq.ops() / (ms * 1e-3) / 1e12,
+            "ops": seq.ops(),
+            "workload": "LLaMA-2-70B-shaped decoder layer, M=8192: q/k/v/o/gate/up/down "
+                        "(%s: %s) + 4-bit K/V cache quantize [32768, 128] x 2, one stream"
+                        % ("sensitive" if sensitive else "insensitive",
+                           ", ".join("%s %d/%d/%d" % (s.name, *np.bincount(
+                               s.widths, minlength=9)[[4, 6, 8]].tolist()) for s in specs))}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -166,6 +207,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-layer", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 512 MiB device copy (counter scaling)")
     args = ap.parse_args()
@@ -290,6 +332,10 @@ def main():
         log("decode bench")
         result["decode"] = {"up": decode_bench(dev, "up"),
                             "down": decode_bench(dev, "down")}
+    if not args.no_layer:
+        log("layer sequence")
+        result["layer"] = {"sensitive": layer_bench(dev, True),
+                           "insensitive": layer_bench(dev, False)}
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         result["cpu_baseline"] = cpu_baseline(case)

@@ -225,3 +225,64 @@ def random_case(seed: int, M: int, K: int, N: int, counts, perm: str = "random",
     return LinearCase("random_%d" % seed, M, K, N, to_bf16_bits(z),
                       to_bf16_bits(w), p, widths_from_counts(n4, n6, n8),
                       {"seed": seed})
+
+
+# --------------------------------------------------------------------------
+# Device-side generation for the full decoder layer (M = 8192): the same
+# recipe as make_linear (outlier channel scales, N(0, 0.02) weights,
+# permutation from the channel ranking), with the large tensors drawn by a
+# seeded torch generator on the GPU instead of numpy on the host.
+# --------------------------------------------------------------------------
+
+@dataclass
+class LayerLinearSpec:
+    name: str
+    K: int
+    N: int
+    widths: np.ndarray            # uint8 [K/32]
+    perm: np.ndarray              # int32 [K]
+    scales: np.ndarray            # float64 [K] per-channel activation scale
+    seed: int                     # torch generator seed of this linear
+
+
+def layer_specs(sensitive: bool):
+    """Formats of the seven linears of a LLaMA-2-70B-shaped decoder layer:
+    sensitive layers use 30 % 8-bit blocks, the others 5 %, both 10 % 6-bit."""
+    p8 = 0.30 if sensitive else 0.05
+    out = []
+    for j, (name, K, N) in enumerate(LAYER_LINEARS):
+        n4, n6, n8 = width_counts(K // BLOCK, 0.10, p8)
+        c = channel_scales(5, K)
+        perm = permutation_from_scales(5, c, n4, n6, n8)
+        out.append(LayerLinearSpec(name, K, N, widths_from_counts(n4, n6, n8), perm, c,
+                                   5000 + 10 * j + (1 if sensitive else 0)))
+    return out
+
+
+def device_activations(spec: LayerLinearSpec, M: int, device, seed_offset: int = 0):
+    """bf16 [M, K] activations z * c on the device (z ~ N(0, 1))."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(spec.seed + seed_offset)
+    z = torch.randn((M, spec.K), generator=g, device=device, dtype=torch.float32)
+    c = torch.from_numpy(spec.scales.astype(np.float32)).to(device)
+    return (z * c[None, :]).to(torch.bfloat16)
+
+
+def device_weights(spec: LayerLinearSpec, device, std: float = 0.02):
+    """bf16 [N, K] weights ~ N(0, std^2) on the device."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(spec.seed + 7)
+    w = torch.randn((spec.N, spec.K), generator=g, device=device, dtype=torch.float32)
+    return (w * std).to(torch.bfloat16)
+
+
+def device_kv(which: int, device, tokens: int = 4096, heads: int = 8, head_dim: int = 128):
+    """bf16 K (which=0) or V (which=1) cache [tokens * heads, head_dim] ~ N(0, 1)."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(5020 + which)
+    x = torch.randn((tokens * heads, head_dim), generator=g, device=device,
+                    dtype=torch.float32)
+    return x.to(torch.bfloat16)
