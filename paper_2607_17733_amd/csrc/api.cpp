@@ -56,17 +56,23 @@ int64_t row_used(const Segs &s) { return 16LL * s.n4 + 24LL * s.n6 + 32LL * s.n8
 int64_t canon_rb(const Segs &s) { return round_up(row_used(s), 16); }
 int64_t exp_rb(const mxq_fmt *f) { return round_up(f->K / MXQ_BLOCK, 16); }
 mxq::OpGeo op_geo(const Segs &s) { return mxq::OpGeo(s.n4, s.n6, s.n8); }
-// activation buffers: M packed rows, then the operand image (32-row tiles);
-// exponent buffers: M exponent rows, then the operand image's scale bytes
+mxq::DGeo d_geo(const Segs &s) { return mxq::DGeo(s.n4, s.n6, s.n8); }
+bool decode_batch(int64_t M) { return M > 0 && M <= MXQ_DECODE_MAX_M; }
+// activation buffers: M packed rows, then the operand image (32-row tiles
+// for the prefill GEMM, or the 16-row decode image for M <= 16);
+// exponent buffers: M exponent rows, then the prefill image's scale bytes
 int64_t act_bytes(const Segs &s, int64_t M) {
-  return M * canon_rb(s) + mxq::act_op_bytes(op_geo(s), M);
+  return M * canon_rb(s) + (decode_batch(M) ? mxq::ad_image_bytes(d_geo(s))
+                                            : mxq::act_op_bytes(op_geo(s), M));
 }
 int64_t act_exp_bytes(const mxq_fmt *f, const Segs &s, int64_t M) {
-  return M * exp_rb(f) + mxq::act_sc_bytes(op_geo(s), M);
+  return M * exp_rb(f) + (decode_batch(M) ? 0 : mxq::act_sc_bytes(op_geo(s), M));
 }
-// weights: packed slabs (N rounded to 16), tail padding, then the operand
-// image (N rounded to 128)
-int64_t w_packed(const Segs &s, int64_t N) { return round_up(N, 16) * row_used(s); }
+// weights: 16-column slabs in the stream layout (N rounded to 16), tail
+// padding, then the operand image (N rounded to 128)
+int64_t w_packed(const Segs &s, int64_t N) {
+  return round_up(N, 16) / 16 * mxq::wd_slab_bytes(d_geo(s));
+}
 int64_t w_op_off(const Segs &s, int64_t N) { return w_packed(s, N) + kWeightTailPad; }
 int64_t w_tile(const Segs &s) { return mxq::op_tile_bytes(op_geo(s)); }
 
@@ -109,10 +115,11 @@ mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows
   a.tail_pad = weights ? (int)kWeightTailPad : 0;
   a.vec16 = (ld % 8 == 0) ? 1 : 0;
   if (!weights) {
+    a.dimg = decode_batch(rows) ? 1 : 0;
     // the activation quantizer stages its rows in LDS: one row must fit
     const mxq::OpGeo og = op_geo(s);
-    if (mxq::quantize_act_lds(fmt->K, og.n4p + og.n6p + og.n8, fmt->perm != nullptr) >
-        mxq::kMaxLds)
+    if (mxq::quantize_act_lds(fmt->K, og.n4p + og.n6p + og.n8 + (og.n8 & 1),
+                              fmt->perm != nullptr) > mxq::kMaxLds)
       return MXQ_ERR_UNSUPPORTED;
     return launched(mxq::launch_quantize_act(a, (hipStream_t)stream));
   }

@@ -49,47 +49,102 @@ __host__ __device__ inline BlockInfo block_info(const Segs &s, int b) {
 }
 
 // ---------------------------------------------------------------------------
-// Packed weight layout.  Columns form slabs of 16.  Inside a slab, the
-// blocks of each width segment are grouped by four ("quads"; the last one
-// may hold 1-3 blocks).  A quad chunk stores, for each of the 64 matrix-core
-// lanes l = kg * 16 + c (c = column in the slab, kg = which 8 elements of the
-// block), the lane's bytes of every block of the quad back to back:
-//   4-bit: 4 bytes per block (8 nibbles, canonical nibble order);
-//   8-bit: 8 bytes per block;
-//   6-bit: a nibble plane (4 bytes per lane per block) followed by a plane of
-//          top-bit words (4 bytes per lane pair (kg>>1, c) per block, same
-//          word format as the activation layout).
-// A full slab is 16 * (16 n4 + 24 n6 + 32 n8) bytes.
+// Stream layout (decode GEMM).  Sixteen "lines" (16 weight columns = one
+// slab, or the 16 activation rows of a decode batch) are stored step by step
+// in the operand order of V_MFMA_SCALE_F32_16X16X128_F8F6F4, whose lane l =
+// 16 g + c (c = line) holds 32 elements of K-group g and supplies the E8M0
+// scale of K-block g of its line.  Steps: the 4-bit blocks four at a time
+// (padded with zero blocks to a multiple of 4), the 6-bit and the 8-bit
+// blocks two at a time (each padded to a multiple of 2).  A step chunk is
+// the 64 lanes' data (lane l at LB * l unless split into planes as noted),
+// then 64 scale bytes in lane order.
+//
+// With the block's E as E8M0 scale, the FP8 digits of a mantissa sum to
+// q * 2^-(m-2): e4m3(q/4) for 4-bit q; for q = 16h + l (h = floor(q/16),
+// l in [0, 15]) e4m3(h) and e4m3(l/16) for 6-bit, e4m3(h/4) and e4m3(l/64)
+// for 8-bit.  Weights keep the packed mantissas (4m bits per element) and
+// become these digits in registers:
+//   4-bit step s: lane (g, c) holds 16 bytes: elements 16(g&1)..16(g&1)+15 of
+//     block 4s+(g>>1) (bytes 0-7), then the same elements of block
+//     4s+2+(g>>1) (bytes 8-15), as nibbles: the dword of elements e0..e7 has
+//     byte k = (e_k & 15) | (e_{k+4} & 15) << 4.  Scale byte of lane
+//     (g, c): E of block 4s+g.
+//   6-bit step s: lane (g, c) holds 12 bytes for elements 16(g&1)+0..15 of
+//     block 2s+(g>>1): their low nibbles (8 bytes at 8 l, same nibble order)
+//     and a dword of their bits 4-5 (at 512 + 4 l: element t at bits
+//     8(t%4) + 2(t/4)).
+//   8-bit step s: lane (g, c) holds 16 bytes: the same 16 elements of block
+//     2s+(g>>1) as two's-complement bytes.
+//   6/8-bit scale byte of lane (g, c): E of block 2s+(g&1).
+// Activations (decode image, M <= 16) are stored as ready operands:
+//   4-bit step s: lane (g, r) holds block 4s+g of row r as 32 FP6 e3m2
+//     codes of q/4 (24 bytes: the first 16 at 16 l, the last 8 at
+//     1024 + 8 l); scale byte E of block 4s+g.
+//   6/8-bit step s: lane (g, r) holds elements 16(g&1)+0..15 of block
+//     2s+(g>>1): the e4m3 codes of their high digits (16 bytes) then of
+//     their low digits (16 bytes); scale byte E of block 2s+(g&1).
 // ---------------------------------------------------------------------------
-__host__ __device__ inline int64_t slab_bytes(const Segs &s) {
-  return 16LL * (16LL * s.n4 + 24LL * s.n6 + 32LL * s.n8);
-}
+constexpr int kStreamLanes = 64;
 
-__host__ __device__ inline int64_t seg_base(const Segs &s, int seg) {
-  return seg == 0 ? 0 : (seg == 1 ? 256LL * s.n4 : 256LL * s.n4 + 384LL * s.n6);
-}
-
-struct WLoc {
-  int64_t lo;   // offset (in the slab) of the lane's first byte for the block
-  int64_t hi;   // 6-bit only: offset of the lane pair's top-bit word
+struct DGeo {
+  int n4, n6, n8;
+  int S4, S6, S8, nsteps;
+  __host__ __device__ DGeo(int a, int b, int c)
+      : n4(a), n6(b), n8(c), S4((a + 3) / 4), S6((b + 1) / 2), S8((c + 1) / 2),
+        nsteps(S4 + S6 + S8) {}
 };
 
-// Location of (block, lane) inside a slab.
-__host__ __device__ inline WLoc w_loc(const Segs &s, const BlockInfo &bi,
-                                      int kg, int c) {
-  const int g = bi.idx >> 2, r = bi.idx & 3;
-  const int rg = min(4, bi.nseg - 4 * g);
-  const int64_t chunk = seg_base(s, bi.seg) + 256LL * bi.m * g;
-  const int lane = kg * 16 + c;
-  WLoc w;
-  if (bi.m == 6) {
-    w.lo = chunk + (int64_t)lane * rg * 4 + r * 4;
-    w.hi = chunk + 256LL * rg + (int64_t)((kg >> 1) * 16 + c) * rg * 4 + r * 4;
+// lane-data bytes of a weight / activation step of each segment
+__host__ __device__ constexpr int wd_lane_bytes(int seg) { return seg == 1 ? 12 : 16; }
+__host__ __device__ constexpr int ad_lane_bytes(int seg) { return seg == 0 ? 24 : 32; }
+__host__ __device__ constexpr int wd_chunk(int seg) { return kStreamLanes * (wd_lane_bytes(seg) + 1); }
+__host__ __device__ constexpr int ad_chunk(int seg) { return kStreamLanes * (ad_lane_bytes(seg) + 1); }
+
+// byte offset of step st in a weight slab / the activation decode image
+__host__ __device__ inline int64_t wd_step_off(const DGeo &d, int st) {
+  if (st <= d.S4) return (int64_t)wd_chunk(0) * st;
+  if (st <= d.S4 + d.S6) return (int64_t)wd_chunk(0) * d.S4 + (int64_t)wd_chunk(1) * (st - d.S4);
+  return (int64_t)wd_chunk(0) * d.S4 + (int64_t)wd_chunk(1) * d.S6 +
+         (int64_t)wd_chunk(2) * (st - d.S4 - d.S6);
+}
+__host__ __device__ inline int64_t ad_step_off(const DGeo &d, int st) {
+  if (st <= d.S4) return (int64_t)ad_chunk(0) * st;
+  return (int64_t)ad_chunk(0) * d.S4 + (int64_t)ad_chunk(1) * (st - d.S4);
+}
+__host__ __device__ inline int64_t wd_slab_bytes(const DGeo &d) { return wd_step_off(d, d.nsteps); }
+__host__ __device__ inline int64_t ad_image_bytes(const DGeo &d) { return ad_step_off(d, d.nsteps); }
+
+// Where block `idx` of segment `seg` lives in the stream layout: its step,
+// the lane group of each half (elements 16h..16h+15 sit in lane group
+// g0 + h), the byte offset of its elements inside a 4-bit lane (0 or 8) and
+// the lane groups whose scale byte is the block's exponent (one for 4-bit
+// blocks, two for 6/8-bit blocks).
+struct DLoc {
+  int st, g0, region, sg0, sg1;
+};
+__host__ __device__ inline DLoc d_loc(const DGeo &d, int seg, int idx) {
+  DLoc r;
+  if (seg == 0) {
+    r.st = idx >> 2;
+    r.g0 = 2 * (idx & 1);
+    r.region = 8 * ((idx >> 1) & 1);
+    r.sg0 = r.sg1 = idx & 3;
   } else {
-    w.lo = chunk + (int64_t)lane * rg * bi.m + r * bi.m;
-    w.hi = 0;
+    r.st = (seg == 1 ? d.S4 : d.S4 + d.S6) + (idx >> 1);
+    r.g0 = 2 * (idx & 1);
+    r.region = 0;
+    r.sg0 = idx & 1;
+    r.sg1 = r.sg0 + 2;
   }
-  return w;
+  return r;
+}
+
+// Weight stream nibble dword of eight mantissas q[0..7].
+__host__ __device__ inline uint32_t stream_nibbles(const int *q) {
+  uint32_t x = 0;
+  for (int k = 0; k < 4; ++k)
+    x |= (((uint32_t)q[k] & 15u) | (((uint32_t)q[k + 4] & 15u) << 4)) << (8 * k);
+  return x;
 }
 
 // ---------------------------------------------------------------------------
@@ -131,85 +186,42 @@ __device__ inline int quant_elem(uint32_t bits, int E, int m, int ties_away,
   return qi;
 }
 
-// Packing of 8 consecutive mantissas (one lane's group, elements 8kg..8kg+7
-// of a block).
-__device__ inline uint32_t pack_nibbles(const int *q) {
-  uint32_t x = 0;
-#pragma unroll
-  for (int t = 0; t < 8; ++t) x |= ((uint32_t)q[t] & 15u) << (4 * t);
-  return x;
-}
-
-// Top two bits of eight 6-bit mantissas, placed as in the top-bit word:
-// for an even group (kg even) bits 6-7 / 4-5 of bytes 0-3; for an odd group
-// bits 2-3 / 0-1.
-__device__ inline uint32_t pack_top2(const int *q, int odd) {
-  uint32_t y = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const uint32_t h0 = ((uint32_t)q[2 * j] & 63u) >> 4;
-    const uint32_t h1 = ((uint32_t)q[2 * j + 1] & 63u) >> 4;
-    y |= ((h0 << 6) | (h1 << 4)) << (8 * j);
-  }
-  return odd ? (y >> 4) : y;
-}
-
 // ---------------------------------------------------------------------------
-// Unpack one lane's 8 mantissas into an int8 matrix-core operand (two
-// dwords).  Each width is placed at the top of the byte, so every operand
-// byte equals q * 2^(8-m): the int32 product of a block then carries a factor
-// 2^(2(8-m)) and the scale of any block becomes 2^(Ea + Ew - 266)
-// independently of its width.  Element order inside the lane is
-// [0,2,4,6,1,3,5,7] for 4/6-bit and [0..7] for 8-bit; both operands of a
-// product use the same order, so the dot product is unchanged.
+// Element accessors (debug / parity kernels): mantissa t (0..31) of a block.
 // ---------------------------------------------------------------------------
-__device__ inline uint64_t unpack4(uint32_t x) {
-  const uint32_t ev = (x << 4) & 0xF0F0F0F0u;
-  const uint32_t od = x & 0xF0F0F0F0u;
-  return (uint64_t)ev | ((uint64_t)od << 32);
+__device__ inline int sext_bits(uint32_t v, int bits) {
+  const int sh = 32 - bits;
+  return ((int)(v << sh)) >> sh;
 }
 
-// x: nibble dword; y: top-bit word already shifted so that this lane's
-// elements sit in bits 6-7 (even) and 4-5 (odd) of each byte.
-__device__ inline uint64_t unpack6(uint32_t x, uint32_t y) {
-  const uint32_t ev = ((x << 2) & 0x3C3C3C3Cu) | (y & 0xC0C0C0C0u);
-  const uint32_t od = ((x >> 2) & 0x3C3C3C3Cu) | ((y << 2) & 0xC0C0C0C0u);
-  return (uint64_t)ev | ((uint64_t)od << 32);
-}
-
-// Block scale 2^(E - 133) as fp32 (exact; denormal for E < 7), NaN for the
-// E8M0 NaN code.  The product of an activation and a weight scale times the
-// int32 sum of the int8 operands is the block's contribution.
-__device__ inline float block_scale(int E) {
-  return E == 255 ? __builtin_nanf("") : ldexpf(1.0f, E - 133);
-}
-
-// Activation operand of (row, block, kg) from the canonical packed row.
-__device__ inline uint64_t load_act_operand(const uint8_t *row,
-                                            const BlockInfo &bi, int kg) {
+// Canonical packed activation row (layout in include/mxq.h).
+__device__ inline int act_elem(const uint8_t *row, const BlockInfo &bi, int t) {
   const uint8_t *p = row + bi.aoff;
-  if (bi.m == 4) {
-    return unpack4(*(const uint32_t *)(p + 4 * kg));
-  } else if (bi.m == 6) {
-    const uint32_t x = *(const uint32_t *)(p + 4 * kg);
-    const uint32_t y = *(const uint32_t *)(p + 16 + 4 * (kg >> 1));
-    return unpack6(x, (kg & 1) ? (y << 4) : y);
-  }
-  return *(const uint64_t *)(p + 8 * kg);
+  if (bi.m == 8) return (int)(int8_t)p[t];
+  const uint32_t nib = (p[t >> 1] >> (4 * (t & 1))) & 15u;
+  if (bi.m == 4) return sext_bits(nib, 4);
+  const int d = t >> 4, u = t & 15;
+  const int j = (u & 7) >> 1;
+  const int sh = (u < 8 ? 6 : 2) - 2 * (u & 1);
+  const uint32_t top = (p[16 + 4 * d + j] >> sh) & 3u;
+  return sext_bits(nib | (top << 4), 6);
 }
 
-// Weight operand of (slab, block, kg, c) from the packed weight layout.
-__device__ inline uint64_t load_w_operand(const uint8_t *slab, const Segs &s,
-                                          const BlockInfo &bi, int kg, int c) {
-  const WLoc w = w_loc(s, bi, kg, c);
-  if (bi.m == 4) return unpack4(*(const uint32_t *)(slab + w.lo));
-  if (bi.m == 6) {
-    const uint32_t x = *(const uint32_t *)(slab + w.lo);
-    const uint32_t y = *(const uint32_t *)(slab + w.hi);
-    return unpack6(x, (kg & 1) ? (y << 4) : y);
-  }
-  const uint32_t *p = (const uint32_t *)(slab + w.lo);
-  return (uint64_t)p[0] | ((uint64_t)p[1] << 32);
+// Weight slab in the stream layout (see DGeo); c = column within the slab.
+__device__ inline int wstream_elem(const uint8_t *slab, const DGeo &dg, const BlockInfo &bi,
+                                   int c, int t) {
+  const DLoc L = d_loc(dg, bi.seg, bi.idx);
+  const uint8_t *chunk = slab + wd_step_off(dg, L.st);
+  const int ln = 16 * (L.g0 + (t >> 4)) + c;
+  const int u = t & 15;                     // element within the half
+  if (bi.m == 8) return (int)(int8_t)chunk[16 * ln + u];
+  const int d = u >> 3, k = u & 7;
+  const uint8_t *nb = bi.m == 4 ? chunk + 16 * ln + L.region : chunk + 8 * ln;
+  const uint32_t nib = (nb[4 * d + (k & 3)] >> (4 * (k >> 2))) & 15u;
+  if (bi.m == 4) return sext_bits(nib, 4);
+  const uint32_t y = *(const uint32_t *)(chunk + 512 + 4 * ln);
+  const uint32_t top = (y >> (8 * (k & 3) + 4 * d + 2 * (k >> 2))) & 3u;
+  return sext_bits(nib | (top << 4), 6);
 }
 
 // ---------------------------------------------------------------------------

@@ -24,6 +24,7 @@ struct QuantArgs {
   int64_t canon_erb;       // exponent bytes per row
   int64_t op_off, sc_off;  // activations: offsets of the operand image in mant
                            // and of its scale bytes in exp
+  int dimg;                // activations: write the decode image (M <= 16)
   int64_t row_used;        // unpadded packed bytes per row
   int64_t slab_rows;       // weights: columns in the packed slabs (N rounded to 16)
   int64_t w_op;            // weights: offset of the operand image in the buffer

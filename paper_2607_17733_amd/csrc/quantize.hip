@@ -12,10 +12,11 @@
 // stages its source rows in LDS with 16-byte coalesced loads and gathers from
 // LDS, so the permutation never turns into scattered global loads.
 //
-// Every column is written twice: into the packed 16-column slabs the decode
-// GEMM streams, and into the 128-column tiles of the matrix-core operand
-// image (FP6/FP8 digits of each mantissa, the layout described with OpGeo)
-// with their E8M0 scale bytes, which the prefill GEMM reads.
+// Every column is written twice: into the 16-column slabs of the stream
+// layout (packed mantissas in the decode GEMM's lane order, see DGeo), and
+// into the 128-column tiles of the matrix-core operand image (FP6/FP8
+// digits of each mantissa, the layout described with OpGeo) with their E8M0
+// scale bytes, which the prefill GEMM reads.
 #include "mxq_device.h"
 #include "mxq_internal.h"
 
@@ -120,10 +121,15 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
     for (int u = 0; u < 8; ++u)
       qv[u] = quant_elem(bits[u], E, bi.m, q.ties_away, q.full_clamp);
 
-    const uint32_t nib = pack_nibbles(qv);
+    // stream-layout nibbles, and (6-bit) bits 4-5 of the half's 16
+    // elements: element 8d+k of the half at bits 8(k%4) + 4d + 2(k/4)
+    const uint32_t nib = stream_nibbles(qv);
     uint32_t top = 0;
     if (bi.m == 6) {
-      top = pack_top2(qv, kg & 1);
+      const int dd = kg & 1;
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        top |= (((uint32_t)qv[k] >> 4) & 3u) << (8 * (k & 3) + 4 * dd + 2 * (k >> 2));
       top |= __shfl_xor(top, 1);             // merge the lane pair's word
     }
     if (!live) continue;
@@ -148,25 +154,59 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
       const int c = (int)(row % kOpCols);
       uint8_t *tile = q.mant + q.w_op + (row / kOpCols) * q.w_tile;
       if (row < q.slab_rows) {
-        const int64_t slab = row >> 4;
-        uint8_t *base = q.mant + slab * slab_bytes(s);
-        const WLoc w = w_loc(s, bi, kg, (int)(row & 15));
+        // stream layout of the 16-column slab (decode GEMM)
+        const DGeo dg(q.n4, q.n6, q.n8);
+        const int c16 = (int)(row & 15);
+        uint8_t *slab = q.mant + (row >> 4) * wd_slab_bytes(dg);
+        const DLoc L = d_loc(dg, bi.seg, bi.idx);
+        uint8_t *chunk = slab + wd_step_off(dg, L.st);
+        const int lb = wd_lane_bytes(bi.seg);
+        const int dd = kg & 1;
+        const int ln = 16 * (L.g0 + (kg >> 1)) + c16;
         if (bi.m == 4) {
-          *(uint32_t *)(base + w.lo) = nib;
+          *(uint32_t *)(chunk + 16 * ln + L.region + 4 * dd) = nib;
         } else if (bi.m == 6) {
-          *(uint32_t *)(base + w.lo) = nib;
-          if (!(kg & 1)) *(uint32_t *)(base + w.hi) = top;
+          *(uint32_t *)(chunk + 8 * ln + 4 * dd) = nib;
+          if (dd == 0) *(uint32_t *)(chunk + 512 + 4 * ln) = top;
         } else {
-          *(uint32_t *)(base + w.lo) = lo8;
-          *(uint32_t *)(base + w.lo + 4) = hi8;
+          *(uint32_t *)(chunk + 16 * ln + 8 * dd) = lo8;
+          *(uint32_t *)(chunk + 16 * ln + 8 * dd + 4) = hi8;
         }
-        if (kg == 0) q.exp[row * q.out_erb + b] = (uint8_t)E;
-        if (g == 0)                          // zero the exponent row padding
+        if (kg == 0) {
+          chunk[64 * lb + 16 * L.sg0 + c16] = (uint8_t)E;
+          if (bi.seg) chunk[64 * lb + 16 * L.sg1 + c16] = (uint8_t)E;
+          q.exp[row * q.out_erb + b] = (uint8_t)E;
+        }
+        if (g == 0) {
           for (int64_t z = nb; z < q.out_erb; ++z) q.exp[row * q.out_erb + z] = 0;
+          // zero the stream padding blocks of this column
+          const int nseg[3] = {dg.n4, dg.n6, dg.n8};
+          const int npad[3] = {4 * dg.S4, 2 * dg.S6, 2 * dg.S8};
+          for (int sg = 0; sg < 3; ++sg) {
+            const int plb = wd_lane_bytes(sg);
+            for (int idx = nseg[sg]; idx < npad[sg]; ++idx) {
+              const DLoc P = d_loc(dg, sg, idx);
+              uint8_t *pc = slab + wd_step_off(dg, P.st);
+              for (int hh = 0; hh < 2; ++hh) {
+                const int pl = 16 * (P.g0 + hh) + c16;
+                if (sg == 0) {
+                  *(uint2 *)(pc + 16 * pl + P.region) = make_uint2(0, 0);
+                } else if (sg == 1) {
+                  *(uint2 *)(pc + 8 * pl) = make_uint2(0, 0);
+                  *(uint32_t *)(pc + 512 + 4 * pl) = 0;
+                } else {
+                  *(uint4 *)(pc + 16 * pl) = make_uint4(0, 0, 0, 0);
+                }
+              }
+              pc[64 * plb + 16 * P.sg0 + c16] = 0;
+              if (sg) pc[64 * plb + 16 * P.sg1 + c16] = 0;
+            }
+          }
+        }
       }
       if (row == 0 && g == 0)                // the packed section's tail padding
         for (int z = 0; z < q.tail_pad; ++z)
-          q.mant[q.slab_rows / 16 * slab_bytes(s) + z] = 0;
+          q.mant[q.slab_rows / 16 * wd_slab_bytes(DGeo(q.n4, q.n6, q.n8)) + z] = 0;
       // operand image (128-column tiles of per-step chunks)
       if (bi.m == 8) {
         uint32_t h0 = 0, h1 = 0, l0 = 0, l1 = 0;

@@ -180,19 +180,69 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
     }
   }
 
-  uint8_t *prow = q.mant + row * q.out_rb;
-  uint8_t *op = q.mant + q.op_off + ((row >> 5) * ns) * (int64_t)kActStep + (row & 31) * 16;
-  uint8_t *sc = q.exp + q.sc_off + ((row >> 5) * ns) * (int64_t)kActScaleStep + (row & 31) * 4;
   if (!pad) q.exp[row * q.out_erb + b] = (uint8_t)E;
   const uint32_t Eu = pad ? 0u : (uint32_t)E;
 
+  // packed row
+  uint8_t *prow = q.mant + row * q.out_rb;
+  if (!pad) {
+    if (seg == 0) {
+      *(u4 *)(prow + 16LL * idx) =
+          u4{nibbles8(v, 0), nibbles8(v, 8), nibbles8(v, 16), nibbles8(v, 24)};
+    } else if (seg == 1) {
+      uint8_t *p = prow + 16LL * og.n4 + 24LL * idx;
+      *(u2 *)p = u2{nibbles8(v, 0), nibbles8(v, 8)};
+      *(u2 *)(p + 8) = u2{nibbles8(v, 16), nibbles8(v, 24)};
+      *(u2 *)(p + 16) = u2{top_word(v, 0), top_word(v, 1)};
+    } else {
+      uint8_t *p = prow + 16LL * og.n4 + 24LL * og.n6 + 32LL * idx;
+#pragma unroll
+      for (int d = 0; d < 4; ++d)
+        *(u2 *)(p + 8 * d) = u2{bytes4(v, 8 * d), bytes4(v, 8 * d + 4)};
+    }
+  }
+
+  if (q.dimg) {
+    // decode image (M <= 16): the stream layout's ready operands, see DGeo
+    const DGeo dg(og.n4, og.n6, og.n8);
+    const DLoc L = d_loc(dg, seg, idx);
+    uint8_t *chunk = q.mant + q.op_off + ad_step_off(dg, L.st);
+    if (seg == 0) {
+      const int l = 16 * L.sg0 + (int)row;
+      const v6u c = to_e3m2(v, 4.f);
+      *(u4 *)(chunk + 16 * l) = u4{c[0], c[1], c[2], c[3]};
+      *(u2 *)(chunk + 1024 + 8 * l) = u2{c[4], c[5]};
+      chunk[1536 + l] = (uint8_t)Eu;
+    } else {
+      Blk hd, ld;                              // q = 16 h + l
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        hd.e[i] = floorf(v.e[i] * 0.0625f);
+        hd.o[i] = floorf(v.o[i] * 0.0625f);
+        ld.e[i] = fmaf(hd.e[i], -16.f, v.e[i]);
+        ld.o[i] = fmaf(hd.o[i], -16.f, v.o[i]);
+      }
+      // digits summing to q * 2^-(m-2): h + l/16 (6-bit), h/4 + l/64 (8-bit)
+      const float dh = seg == 1 ? 1.f : 4.f, dl = seg == 1 ? 16.f : 64.f;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int l = 16 * (L.g0 + h) + (int)row;
+        *(u4 *)(chunk + 32 * l) = to_e4m3(hd, h, dh);
+        *(u4 *)(chunk + 32 * l + 16) = to_e4m3(ld, h, dl);
+      }
+      chunk[2048 + 16 * L.sg0 + row] = (uint8_t)Eu;
+      chunk[2048 + 16 * L.sg1 + row] = (uint8_t)Eu;
+    }
+    return;
+  }
+
+  // prefill operand image (32-row tiles) and its scale bytes
+  uint8_t *op = q.mant + q.op_off + ((row >> 5) * ns) * (int64_t)kActStep + (row & 31) * 16;
+  uint8_t *sc = q.exp + q.sc_off + ((row >> 5) * ns) * (int64_t)kActScaleStep + (row & 31) * 4;
   if (seg == 0) {
     const int st = idx >> 2, h = idx & 1, j = (idx >> 1) & 1;
     uint8_t *o = op + st * kActStep + h * 512;
     uint8_t *s = sc + st * kActScaleStep + h * 128;
-    if (!pad)
-      *(u4 *)(prow + 16LL * idx) =
-          u4{nibbles8(v, 0), nibbles8(v, 8), nibbles8(v, 16), nibbles8(v, 24)};
     const v6u c = to_e3m2(v, 4.f);
     if (j == 0) {
       *(u4 *)o = u4{c[0], c[1], c[2], c[3]};
@@ -207,19 +257,13 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
   } else if (seg == 1) {
     const int st = og.s4 + (idx >> 1), h = idx & 1;
     uint8_t *o = op + st * kActStep + h * 512;
-    Blk hd, ld;
+    Blk hd, ld;                                // q = 8 h + l
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       hd.e[i] = floorf(v.e[i] * 0.125f);
       hd.o[i] = floorf(v.o[i] * 0.125f);
       ld.e[i] = fmaf(hd.e[i], -8.f, v.e[i]);
       ld.o[i] = fmaf(hd.o[i], -8.f, v.o[i]);
-    }
-    if (!pad) {
-      uint8_t *p = prow + 16LL * og.n4 + 24LL * idx;
-      *(u2 *)p = u2{nibbles8(v, 0), nibbles8(v, 8)};
-      *(u2 *)(p + 8) = u2{nibbles8(v, 16), nibbles8(v, 24)};
-      *(u2 *)(p + 16) = u2{top_word(v, 0), top_word(v, 1)};
     }
     const v6u ch = to_e3m2(hd, 2.f);
     const v6u cl = to_e3m2(ld, 16.f);
@@ -229,7 +273,7 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
     *(uint32_t *)(sc + st * kActScaleStep + h * 128) = Eu;
   } else {
     const int st = og.s4 + og.s6 + idx;
-    Blk hd, ld;
+    Blk hd, ld;                                // q = 16 h + l
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       hd.e[i] = floorf(v.e[i] * 0.0625f);
@@ -237,10 +281,6 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
       ld.e[i] = fmaf(hd.e[i], -16.f, v.e[i]);
       ld.o[i] = fmaf(hd.o[i], -16.f, v.o[i]);
     }
-    uint8_t *p = prow + 16LL * og.n4 + 24LL * og.n6 + 32LL * idx;
-#pragma unroll
-    for (int d = 0; d < 4; ++d)
-      *(u2 *)(p + 8 * d) = u2{bytes4(v, 8 * d), bytes4(v, 8 * d + 4)};
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       uint8_t *o = op + st * kActStep + h * 512;
@@ -262,7 +302,8 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
   const int lgR = q.lg_rows;
   const int R = 1 << lgR;
   const OpGeo og(q.n4, q.n6, q.n8);
-  const int nbp = og.n4p + og.n6p + og.n8;          // padded blocks per row
+  // padded blocks per row (the decode image pads the 8-bit blocks to pairs)
+  const int nbp = og.n4p + og.n6p + og.n8 + (q.dimg ? (og.n8 & 1) : 0);
   // XCD-aware order: consecutive row groups (whole 32-row operand tiles)
   // stay on one XCD, so its L2 completes every line of the tile.
   int64_t w = blockIdx.x;
@@ -331,7 +372,7 @@ bool stage_perm(int64_t K, bool perm) {
 
 int padded_blocks(int n4, int n6, int n8) {
   const OpGeo og(n4, n6, n8);
-  return og.n4p + og.n6p + og.n8;
+  return og.n4p + og.n6p + og.n8 + (og.n8 & 1);
 }
 
 }  // namespace

@@ -184,3 +184,156 @@ def decode_weights(img: np.ndarray, widths, N: int):
                               lambda st, h: w_lane_bytes(img, geo, st, h),
                               lambda st, h: w_scales(img, geo, st, h), weights=True)
     return q, E, ok and ok2
+
+
+# --------------------------------------------------------------------------
+# Stream layout (decode GEMM): weight slabs of 16 columns and the 16-row
+# activation decode image, step by step in the lane order of the 16x16x128
+# scaled matrix-core instruction (lane l = 16 g + line).
+# --------------------------------------------------------------------------
+
+W_LANE = {0: 16, 1: 12, 2: 16}
+A_LANE = {0: 24, 1: 32, 2: 32}
+LANES = 64
+
+
+class SGeo:
+    def __init__(self, widths):
+        w = np.asarray(widths)
+        self.n = [int((w == m).sum()) for m in (4, 6, 8)]
+        self.S = [-(-self.n[0] // 4), -(-self.n[1] // 2), -(-self.n[2] // 2)]
+        self.nb = len(w)
+        self.base = [0, self.n[0], self.n[0] + self.n[1]]   # first block of each segment
+
+    def steps(self):
+        """(segment, step within the segment) in stream order."""
+        for seg in range(3):
+            for s in range(self.S[seg]):
+                yield seg, s
+
+    def w_slab_bytes(self):
+        return sum(self.S[seg] * LANES * (W_LANE[seg] + 1) for seg in range(3))
+
+    def a_image_bytes(self):
+        return sum(self.S[seg] * LANES * (A_LANE[seg] + 1) for seg in range(3))
+
+
+def _sext(v, bits):
+    v = v.astype(np.int64)
+    return np.where(v >= (1 << (bits - 1)), v - (1 << bits), v)
+
+
+def _stream_nibbles(b8):
+    """[..., 8] nibble bytes of 16 elements (two dwords; byte k of dword d
+    holds elements 8d+k (low) and 8d+k+4 (high)) -> [..., 16] values 0..15."""
+    out = np.zeros(b8.shape[:-1] + (16,), np.int64)
+    for d in range(2):
+        for k in range(4):
+            byte = b8[..., 4 * d + k].astype(np.int64)
+            out[..., 8 * d + k] = byte & 15
+            out[..., 8 * d + k + 4] = byte >> 4
+    return out
+
+
+def decode_w_stream(img, widths, N):
+    """Weight slabs -> (q [Npad16, K], E [Npad16, nb], layout_ok)."""
+    g = SGeo(widths)
+    nsl = -(-N // 16)
+    sb = g.w_slab_bytes()
+    slabs = img[:nsl * sb].reshape(nsl, sb)
+    q = np.zeros((nsl * 16, g.nb * BLOCK), np.int64)
+    E = np.full((nsl * 16, g.nb), -1, np.int64)
+    ok = True
+    off = 0
+    for seg, s in g.steps():
+        lb = W_LANE[seg]
+        ch = slabs[:, off:off + LANES * (lb + 1)]
+        off += LANES * (lb + 1)
+        sc = ch[:, LANES * lb:].reshape(nsl, 4, 16).astype(np.int64)   # [slab, g, col]
+        for gg in range(4):
+            half = gg & 1
+            if seg == 0:
+                lane = ch[:, :LANES * 16].reshape(nsl, 4, 16, 16)[:, gg]   # [slab, col, 16]
+                parts = [(4 * s + (gg >> 1), lane[..., 0:8]), (4 * s + 2 + (gg >> 1), lane[..., 8:16])]
+                vals = [(blk, _sext(_stream_nibbles(p), 4)) for blk, p in parts]
+            else:
+                blk = 2 * s + (gg >> 1)
+                if seg == 1:
+                    nib = ch[:, :LANES * 8].reshape(nsl, 4, 16, 8)[:, gg]
+                    top = ch[:, 512:512 + LANES * 4].reshape(nsl, 4, 16, 4)[:, gg]
+                    y = top.astype(np.int64)
+                    y = y[..., 0] | (y[..., 1] << 8) | (y[..., 2] << 16) | (y[..., 3] << 24)
+                    lo = _stream_nibbles(nib)
+                    t2 = np.stack([(y >> (8 * (u % 4) + 2 * (u // 4))) & 3 for u in range(16)],
+                                  axis=-1)
+                    v = _sext(lo | (t2 << 4), 6)
+                else:
+                    v = _sext(ch[:, :LANES * 16].reshape(nsl, 4, 16, 16)[:, gg], 8)
+                vals = [(blk, v)]
+            for blk, v in vals:
+                v = v.reshape(nsl * 16, 16)
+                if blk < g.n[seg]:
+                    b = g.base[seg] + blk
+                    q[:, BLOCK * b + 16 * half: BLOCK * b + 16 * half + 16] = v
+                else:
+                    ok &= not v.any()
+        # scale bytes: lane group gg carries the exponent of block
+        # 4s+gg (4-bit) or 2s+(gg&1) (6/8-bit)
+        for gg in range(4):
+            blk = 4 * s + gg if seg == 0 else 2 * s + (gg & 1)
+            e = sc[:, gg].reshape(nsl * 16)
+            if blk < g.n[seg]:
+                b = g.base[seg] + blk
+                ok &= bool(np.all((E[:, b] == -1) | (E[:, b] == e)))
+                E[:, b] = e
+            else:
+                ok &= not e.any()
+    return q, E, ok
+
+
+def decode_act_dimg(img, widths, M):
+    """Activation decode image (16 rows) -> (q [M, K], E [M, nb], layout_ok)."""
+    g = SGeo(widths)
+    assert img.size == g.a_image_bytes()
+    q = np.zeros((16, g.nb * BLOCK), np.int64)
+    E = np.full((16, g.nb), -1, np.int64)
+    ok = True
+    off = 0
+    for seg, s in g.steps():
+        lb = A_LANE[seg]
+        ch = img[off:off + LANES * (lb + 1)]
+        off += LANES * (lb + 1)
+        sc = ch[LANES * lb:].reshape(4, 16).astype(np.int64)
+        for gg in range(4):
+            if seg == 0:
+                b24 = np.concatenate([ch[:1024].reshape(4, 16, 16)[gg],
+                                      ch[1024:1536].reshape(4, 16, 8)[gg]], axis=1)
+                v = fp6_values(b24) * 4
+                blk, lo, hi = 4 * s + gg, 0, 32
+            else:
+                lane = ch[:2048].reshape(4, 16, 32)[gg]
+                hv, lv = fp8_values(lane[:, :16]), fp8_values(lane[:, 16:])
+                # digits of q = 16 h + l summing to q 2^-(m-2): h + l/16
+                # (6-bit), h/4 + l/64 (8-bit)
+                f = 16 if seg == 1 else 64
+                hv, lv = hv[:M], lv[:M]
+                v = f * (hv + lv)
+                h, l = hv * f / 16, lv * f
+                ok &= bool(np.all((l >= 0) & (l <= 15) & (h == np.floor(v / 16))))
+                blk, lo, hi = 2 * s + (gg >> 1), 16 * (gg & 1), 16 * (gg & 1) + 16
+            v = v[:M]                       # rows past M are unspecified
+            if blk < g.n[seg]:
+                b = g.base[seg] + blk
+                q[:M, BLOCK * b + lo: BLOCK * b + hi] = v
+            else:
+                ok &= not np.any(v)
+        for gg in range(4):
+            blk = 4 * s + gg if seg == 0 else 2 * s + (gg & 1)
+            e = sc[gg]
+            if blk < g.n[seg]:
+                b = g.base[seg] + blk
+                ok &= bool(np.all((E[:M, b] == -1) | (E[:M, b] == e[:M])))
+                E[:, b] = e
+            else:
+                ok &= not e[:M].any()
+    return q[:M], E[:M], ok

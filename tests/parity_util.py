@@ -8,7 +8,8 @@ import numpy as np
 import torch
 
 import oracle
-from operand_decode import CHUNK, TILE_COLS, Geo, decode_act, decode_weights
+from operand_decode import (CHUNK, TILE_COLS, Geo, SGeo, decode_act, decode_act_dimg,
+                            decode_w_stream, decode_weights)
 from paper_2607_17733_amd import mxq
 from paper_2607_17733_amd.workloads import LinearCase
 
@@ -135,7 +136,11 @@ def check_quant_act(case, out, qa, ea, fmt):
     erows = ae[:M * cerb].reshape(M, cerb)
     assert np.array_equal(erows[:, :nb], ea), "activation exponents differ"
     assert not erows[:, nb:].any()
-    q, E, pad_ok = decode_act(am[M * canon:], ae[M * cerb:], case.widths, M)
+    if M <= mxq.DECODE_MAX_M:
+        assert ae.size == M * cerb
+        q, E, pad_ok = decode_act_dimg(am[M * canon:], case.widths, M)
+    else:
+        q, E, pad_ok = decode_act(am[M * canon:], ae[M * cerb:], case.widths, M)
     assert np.array_equal(q, qa), "activation operand image differs from the mantissas"
     assert np.array_equal(E, ea.astype(np.int64)), "activation scale bytes differ"
     assert pad_ok, "activation operand padding not zero"
@@ -149,6 +154,12 @@ def check_pack_w(case, out, qw, ew, fmt):
     assert np.array_equal(q.cpu().numpy(), qw), "weight mantissas differ"
     assert np.array_equal(e.cpu().numpy(), ew), "weight exponents differ"
     wm = out["w_mant"].cpu().numpy()
+    qs, es, ok = decode_w_stream(wm, case.widths, N)
+    assert ok, "weight stream layout / padding"
+    assert np.array_equal(qs[:N], qw), "weight slabs differ from the mantissas"
+    assert np.array_equal(es[:N], ew.astype(np.int64)), "weight slab scale bytes differ"
+    assert not qs[N:].any() and not es[N:].any(), "padding columns not zero"
+    assert not wm[-(-N // 16) * SGeo(case.widths).w_slab_bytes():][:64].any(), "tail padding"
     g = Geo(case.widths)
     size = -(-N // TILE_COLS) * CHUNK * g.nsteps
     qo, eo, ok = decode_weights(wm[wm.size - size:], case.widths, N)

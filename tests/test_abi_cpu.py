@@ -55,26 +55,42 @@ def op_steps(widths):
     return -(-n4 // 4) + -(-n6 // 2) + n8
 
 
+def stream_sizes(widths):
+    """Weight slab and activation decode-image bytes as include/mxq.h states
+    them: 4-bit blocks four per step, 6/8-bit blocks two per step; 64 lanes
+    of 16/12/16 (weights) or 24/32/32 (activations) bytes plus 64 scale
+    bytes per step."""
+    n4, n6, n8 = (sum(1 for w in widths if w == m) for m in (4, 6, 8))
+    S = (-(-n4 // 4), -(-n6 // 2), -(-n8 // 2))
+    wlane, alane = (16, 12, 16), (24, 32, 32)
+    return (sum(s * 64 * (l + 1) for s, l in zip(S, wlane)),
+            sum(s * 64 * (l + 1) for s, l in zip(S, alane)))
+
+
 def test_sizes(lib):
     w1 = [4] * 6 + [6, 8]
     f, _w = _fmt(256, w1)
-    assert lib.mxq_abi_version() == 2
+    assert lib.mxq_abi_version() == 3
     assert op_steps(w1) == 4
+    slab, dimg = stream_sizes(w1)
+    assert (slab, dimg) == (2 * 1088 + 832 + 1088, 2 * 1600 + 2 * 2112)
     assert lib.mxq_act_packed_bytes(ctypes.byref(f)) == 160
     assert lib.mxq_exp_row_bytes(ctypes.byref(f)) == 16
-    # M packed rows + 32-row operand tiles of 3072 bytes per step
-    assert lib.mxq_act_bytes(ctypes.byref(f), 16) == 16 * 160 + 1 * 4 * 3072
+    # M <= 16: M packed rows + the decode image; larger M: 32-row operand
+    # tiles of 3072 bytes per step
+    assert lib.mxq_act_bytes(ctypes.byref(f), 16) == 16 * 160 + dimg
+    assert lib.mxq_act_bytes(ctypes.byref(f), 1) == 160 + dimg
     assert lib.mxq_act_bytes(ctypes.byref(f), 33) == 33 * 160 + 2 * 4 * 3072
     assert lib.mxq_act_bytes(ctypes.byref(f), 0) == 0
     assert lib.mxq_act_bytes(ctypes.byref(f), -1) == -2
-    # M exponent rows + 256 scale bytes per (tile, step)
-    assert lib.mxq_act_exp_bytes(ctypes.byref(f), 16) == 16 * 16 + 1 * 4 * 256
+    # M exponent rows (+ 256 scale bytes per (tile, step) for M > 16)
+    assert lib.mxq_act_exp_bytes(ctypes.byref(f), 16) == 16 * 16
     assert lib.mxq_act_exp_bytes(ctypes.byref(f), 64) == 64 * 16 + 2 * 4 * 256
-    # packed slabs (N to 16) + 64-byte tail + 128-column operand tiles of
+    # stream slabs (N to 16) + 64-byte tail + 128-column operand tiles of
     # 13312 bytes per step
-    assert lib.mxq_weight_bytes(ctypes.byref(f), 256) == 256 * 152 + 64 + 2 * 4 * 13312
-    assert lib.mxq_weight_bytes(ctypes.byref(f), 250) == 256 * 152 + 64 + 2 * 4 * 13312
-    assert lib.mxq_weight_bytes(ctypes.byref(f), 129) == 144 * 152 + 64 + 2 * 4 * 13312
+    assert lib.mxq_weight_bytes(ctypes.byref(f), 256) == 16 * slab + 64 + 2 * 4 * 13312
+    assert lib.mxq_weight_bytes(ctypes.byref(f), 250) == 16 * slab + 64 + 2 * 4 * 13312
+    assert lib.mxq_weight_bytes(ctypes.byref(f), 129) == 9 * slab + 64 + 2 * 4 * 13312
     assert lib.mxq_weight_exp_bytes(ctypes.byref(f), 17) == 32 * 16
     w2 = [4] * 102 + [6] * 13 + [8] * 13
     f2, _w2 = _fmt(4096, w2)
