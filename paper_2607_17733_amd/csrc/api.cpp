@@ -160,6 +160,7 @@ mxq_status gemm_args(const mxq_fmt *fmt, int64_t M, int64_t N, const uint8_t *a_
   g->n4 = s.n4;
   g->n6 = s.n6;
   g->n8 = s.n8;
+  g->sm = fmt->clamp == MXQ_CLAMP_SYMMETRIC ? 1 : 0;
   return MXQ_OK;
 }
 
@@ -289,6 +290,7 @@ static mxq_status unpack_common(const mxq_fmt *fmt, int64_t rows, const uint8_t 
   a.n4 = s.n4;
   a.n6 = s.n6;
   a.n8 = s.n8;
+  a.sm = fmt->clamp == MXQ_CLAMP_SYMMETRIC ? 1 : 0;
   return launched(mxq::launch_unpack(a, weights, (hipStream_t)stream));
 }
 

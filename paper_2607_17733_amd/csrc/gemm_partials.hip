@@ -29,7 +29,7 @@ __global__ __launch_bounds__(kThreads) void gemm_partials_kernel(GemmArgs g) {
   const uint8_t *slab = g.w_mant + (j >> 4) * wd_slab_bytes(dg);
   int acc = 0;
   for (int t = 0; t < kBlock; ++t)
-    acc += act_elem(arow, bi, t) * wstream_elem(slab, dg, bi, (int)(j & 15), t);
+    acc += act_elem(arow, bi, t) * wstream_elem(slab, dg, bi, (int)(j & 15), t, g.sm != 0);
   g.p[f] = acc;
 }
 

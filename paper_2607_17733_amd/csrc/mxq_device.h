@@ -60,19 +60,24 @@ __host__ __device__ inline BlockInfo block_info(const Segs &s, int b) {
 // then 64 scale bytes in lane order.
 //
 // With the block's E as E8M0 scale, the FP8 digits of a mantissa sum to
-// q * 2^-(m-2): e4m3(q/4) for 4-bit q; for q = 16h + l (h = floor(q/16),
-// l in [0, 15]) e4m3(h) and e4m3(l/16) for 6-bit, e4m3(h/4) and e4m3(l/64)
-// for 8-bit.  Weights keep the packed mantissas (4m bits per element) and
-// become these digits in registers:
+// q * 2^-(m-2): e4m3(q/4) for a 4-bit q; two digits for 6- and 8-bit q.
+// Weights keep the packed mantissas (4m bits per element) and become these
+// digits in registers.  With the symmetric clamp (no -2^(m-1)) 4- and 6-bit
+// mantissas are stored sign-magnitude, so a digit is one 8-entry byte lookup
+// plus the sign bit: a 4-bit code is s|(|q|) (3 magnitude bits), a 6-bit code
+// a nibble s|(|q| mod 8) plus the 2-bit |q| div 8 (digits h/2 and l/16 of
+// |q| = 8h + l).  With the full clamp they are two's complement (q mod 16,
+// and bits 4-5: digits h and l/16 of q = 16h + l).  8-bit mantissas are two's
+// complement in both modes (digits h/4 and l/64 of q = 16h + l).
 //   4-bit step s: lane (g, c) holds 16 bytes: elements 16(g&1)..16(g&1)+15 of
 //     block 4s+(g>>1) (bytes 0-7), then the same elements of block
-//     4s+2+(g>>1) (bytes 8-15), as nibbles: the dword of elements e0..e7 has
-//     byte k = (e_k & 15) | (e_{k+4} & 15) << 4.  Scale byte of lane
+//     4s+2+(g>>1) (bytes 8-15), as nibble codes: the dword of elements
+//     e0..e7 has byte k = code(e_k) | code(e_{k+4}) << 4.  Scale byte of lane
 //     (g, c): E of block 4s+g.
 //   6-bit step s: lane (g, c) holds 12 bytes for elements 16(g&1)+0..15 of
-//     block 2s+(g>>1): their low nibbles (8 bytes at 8 l, same nibble order)
-//     and a dword of their bits 4-5 (at 512 + 4 l: element t at bits
-//     8(t%4) + 2(t/4)).
+//     block 2s+(g>>1): their nibble codes (8 bytes at 8 l, same nibble
+//     order) and a dword of their 2-bit codes (at 512 + 4 l: element t at
+//     bits 8(t%4) + 2(t/4)).
 //   8-bit step s: lane (g, c) holds 16 bytes: the same 16 elements of block
 //     2s+(g>>1) as two's-complement bytes.
 //   6/8-bit scale byte of lane (g, c): E of block 2s+(g&1).
@@ -139,11 +144,24 @@ __host__ __device__ inline DLoc d_loc(const DGeo &d, int seg, int idx) {
   return r;
 }
 
-// Weight stream nibble dword of eight mantissas q[0..7].
-__host__ __device__ inline uint32_t stream_nibbles(const int *q) {
+// Stream codes of a mantissa: the nibble (4-bit q, or the low part of a
+// 6-bit q) and the 2-bit high part of a 6-bit q; sm = sign-magnitude
+// (symmetric clamp), else two's complement.
+__host__ __device__ inline uint32_t stream_nibble(int q, int m, bool sm) {
+  if (!sm) return (uint32_t)q & 15u;
+  const uint32_t a = (uint32_t)(q < 0 ? -q : q);
+  return (q < 0 ? 8u : 0u) | (m == 4 ? a : (a & 7u));
+}
+__host__ __device__ inline uint32_t stream_top2(int q, bool sm) {
+  if (!sm) return ((uint32_t)q >> 4) & 3u;
+  return (uint32_t)(q < 0 ? -q : q) >> 3;
+}
+
+// Weight stream nibble dword of eight mantissas q[0..7] of width m.
+__host__ __device__ inline uint32_t stream_nibbles(const int *q, int m, bool sm) {
   uint32_t x = 0;
   for (int k = 0; k < 4; ++k)
-    x |= (((uint32_t)q[k] & 15u) | (((uint32_t)q[k + 4] & 15u) << 4)) << (8 * k);
+    x |= (stream_nibble(q[k], m, sm) | (stream_nibble(q[k + 4], m, sm) << 4)) << (8 * k);
   return x;
 }
 
@@ -207,9 +225,10 @@ __device__ inline int act_elem(const uint8_t *row, const BlockInfo &bi, int t) {
   return sext_bits(nib | (top << 4), 6);
 }
 
-// Weight slab in the stream layout (see DGeo); c = column within the slab.
+// Weight slab in the stream layout (see DGeo); c = column within the slab,
+// sm = sign-magnitude codes (symmetric clamp).
 __device__ inline int wstream_elem(const uint8_t *slab, const DGeo &dg, const BlockInfo &bi,
-                                   int c, int t) {
+                                   int c, int t, bool sm) {
   const DLoc L = d_loc(dg, bi.seg, bi.idx);
   const uint8_t *chunk = slab + wd_step_off(dg, L.st);
   const int ln = 16 * (L.g0 + (t >> 4)) + c;
@@ -218,9 +237,13 @@ __device__ inline int wstream_elem(const uint8_t *slab, const DGeo &dg, const Bl
   const int d = u >> 3, k = u & 7;
   const uint8_t *nb = bi.m == 4 ? chunk + 16 * ln + L.region : chunk + 8 * ln;
   const uint32_t nib = (nb[4 * d + (k & 3)] >> (4 * (k >> 2))) & 15u;
-  if (bi.m == 4) return sext_bits(nib, 4);
+  if (bi.m == 4) return sm ? ((nib & 8u) ? -(int)(nib & 7u) : (int)(nib & 7u)) : sext_bits(nib, 4);
   const uint32_t y = *(const uint32_t *)(chunk + 512 + 4 * ln);
   const uint32_t top = (y >> (8 * (k & 3) + 4 * d + 2 * (k >> 2))) & 3u;
+  if (sm) {
+    const int a = (int)(top * 8u + (nib & 7u));
+    return (nib & 8u) ? -a : a;
+  }
   return sext_bits(nib | (top << 4), 6);
 }
 

@@ -53,6 +53,7 @@ struct GemmArgs {
   int64_t w_tile;          // bytes per 128-column tile of that image
   int64_t npad;            // N rounded up to 16
   int n4, n6, n8;
+  int sm;                  // weight stream codes are sign-magnitude (symmetric clamp)
 };
 
 struct UnpackArgs {
@@ -64,6 +65,7 @@ struct UnpackArgs {
   int64_t a_rb, a_erb;     // activation layout
   int64_t npad;            // weight layout
   int n4, n6, n8;
+  int sm;                  // weight stream codes are sign-magnitude (symmetric clamp)
 };
 
 constexpr int64_t kMaxLds = 160 * 1024;   // LDS per workgroup on gfx950

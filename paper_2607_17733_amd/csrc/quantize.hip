@@ -121,15 +121,16 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
     for (int u = 0; u < 8; ++u)
       qv[u] = quant_elem(bits[u], E, bi.m, q.ties_away, q.full_clamp);
 
-    // stream-layout nibbles, and (6-bit) bits 4-5 of the half's 16
-    // elements: element 8d+k of the half at bits 8(k%4) + 4d + 2(k/4)
-    const uint32_t nib = stream_nibbles(qv);
+    // stream-layout nibble codes, and (6-bit) the 2-bit codes of the half's
+    // 16 elements: element 8d+k of the half at bits 8(k%4) + 4d + 2(k/4)
+    const bool sm = !q.full_clamp;
+    const uint32_t nib = stream_nibbles(qv, bi.m, sm);
     uint32_t top = 0;
     if (bi.m == 6) {
       const int dd = kg & 1;
 #pragma unroll
       for (int k = 0; k < 8; ++k)
-        top |= (((uint32_t)qv[k] >> 4) & 3u) << (8 * (k & 3) + 4 * dd + 2 * (k >> 2));
+        top |= stream_top2(qv[k], sm) << (8 * (k & 3) + 4 * dd + 2 * (k >> 2));
       top |= __shfl_xor(top, 1);             // merge the lane pair's word
     }
     if (!live) continue;

@@ -29,7 +29,7 @@ __global__ __launch_bounds__(kThreads) void unpack_kernel(UnpackArgs a) {
     const DGeo dg(a.n4, a.n6, a.n8);
     const uint8_t *slab = a.mant + (row >> 4) * wd_slab_bytes(dg);
     for (int t = 0; t < kBlock; ++t)
-      out[t] = (int8_t)wstream_elem(slab, dg, bi, (int)(row & 15), t);
+      out[t] = (int8_t)wstream_elem(slab, dg, bi, (int)(row & 15), t, a.sm != 0);
   }
   a.e[row * nb + b] = a.exp[row * a.a_erb + b];
 }

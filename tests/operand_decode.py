@@ -235,8 +235,14 @@ def _stream_nibbles(b8):
     return out
 
 
-def decode_w_stream(img, widths, N):
-    """Weight slabs -> (q [Npad16, K], E [Npad16, nb], layout_ok)."""
+def _sm_nibble(v):
+    """Sign-magnitude 4-bit codes (sign at bit 3) -> values."""
+    return np.where(v & 8, -(v & 7), v & 7)
+
+
+def decode_w_stream(img, widths, N, sm=True):
+    """Weight slabs -> (q [Npad16, K], E [Npad16, nb], layout_ok).  sm: 4- and
+    6-bit codes are sign-magnitude (symmetric clamp), else two's complement."""
     g = SGeo(widths)
     nsl = -(-N // 16)
     sb = g.w_slab_bytes()
@@ -255,7 +261,8 @@ def decode_w_stream(img, widths, N):
             if seg == 0:
                 lane = ch[:, :LANES * 16].reshape(nsl, 4, 16, 16)[:, gg]   # [slab, col, 16]
                 parts = [(4 * s + (gg >> 1), lane[..., 0:8]), (4 * s + 2 + (gg >> 1), lane[..., 8:16])]
-                vals = [(blk, _sext(_stream_nibbles(p), 4)) for blk, p in parts]
+                dec = _sm_nibble if sm else (lambda v: _sext(v, 4))
+                vals = [(blk, dec(_stream_nibbles(p))) for blk, p in parts]
             else:
                 blk = 2 * s + (gg >> 1)
                 if seg == 1:
@@ -266,7 +273,10 @@ def decode_w_stream(img, widths, N):
                     lo = _stream_nibbles(nib)
                     t2 = np.stack([(y >> (8 * (u % 4) + 2 * (u // 4))) & 3 for u in range(16)],
                                   axis=-1)
-                    v = _sext(lo | (t2 << 4), 6)
+                    if sm:      # |q| = 8 t2 + (lo & 7), sign at bit 3 of lo
+                        v = np.where(lo & 8, -(8 * t2 + (lo & 7)), 8 * t2 + (lo & 7))
+                    else:
+                        v = _sext(lo | (t2 << 4), 6)
                 else:
                     v = _sext(ch[:, :LANES * 16].reshape(nsl, 4, 16, 16)[:, gg], 8)
                 vals = [(blk, v)]

@@ -154,7 +154,7 @@ def check_pack_w(case, out, qw, ew, fmt):
     assert np.array_equal(q.cpu().numpy(), qw), "weight mantissas differ"
     assert np.array_equal(e.cpu().numpy(), ew), "weight exponents differ"
     wm = out["w_mant"].cpu().numpy()
-    qs, es, ok = decode_w_stream(wm, case.widths, N)
+    qs, es, ok = decode_w_stream(wm, case.widths, N, sm=fmt.clamp == 0)
     assert ok, "weight stream layout / padding"
     assert np.array_equal(qs[:N], qw), "weight slabs differ from the mantissas"
     assert np.array_equal(es[:N], ew.astype(np.int64)), "weight slab scale bytes differ"
