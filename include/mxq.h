@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define MXQ_ABI_VERSION 3
+#define MXQ_ABI_VERSION 4
 #define MXQ_BLOCK 32
 /* mxq_gemm uses the weight-streaming decode kernel for M <= this. */
 #define MXQ_DECODE_MAX_M 16

@@ -19,13 +19,13 @@
 // exact; a 6/8-bit block pair takes two instructions (the second with the
 // weight digits' halves swapped: h*h + l*l, then h*l + l*h).
 //
-// Work decomposition: one workgroup per 16-column slab, its nw waves taking
-// every nw-th step of each width segment (nw from 2 to 8, so that every slab
-// of the grid is resident at once at about 16 waves per CU).  Each wave
-// keeps two stages of loads in flight: the next stage (four 4-bit or two
-// 6/8-bit steps) is issued before the current one is converted and
-// multiplied.  The waves' fp32 accumulators meet in LDS in a fixed order.
-// Activation loads of rows >= M are predicated off.
+// Work decomposition: the kernel is bound by the number of vector memory
+// loads, so each load serves as many products as possible.  A workgroup
+// owns a pair of 16-column slabs (one activation load feeds both), its nw
+// waves (2 to 16, about 16 waves per CU with every pair resident) taking
+// every nw-th group of four steps of each width segment; a group's scale
+// bytes are one dword per lane and operand (op_sel picks the step).  The
+// waves' fp32 accumulators meet in LDS in a fixed order.
 #include <type_traits>
 
 #include "mxq_device.h"
@@ -110,16 +110,14 @@ __device__ inline uint32_t lut16(uint32_t s) {
   return __builtin_amdgcn_perm(hi, lo, sel);
 }
 
-constexpr int kU4 = 4;     // 4-bit steps per pipeline stage
-constexpr int kU68 = 2;    // 6/8-bit steps per pipeline stage
-constexpr int kMaxWaves = 8;
+constexpr int kMaxWaves = 16;
 
-__device__ inline v4f mfma(const v8i &a, const v8i &b, v4f acc, int fa, uint32_t as,
-                           uint32_t ws) {
-  if (fa == 3)
-    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, acc, 3, 0, 0, (int)as, 0,
-                                                            (int)ws);
-  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, acc, 0, 0, 0, (int)as, 0,
+// Block-scaled 16x16x128 product; the scale bytes of step K of a group sit
+// in byte K of the scale dwords (op_sel).  FA: format of A (3 = e3m2 FP6,
+// 0 = e4m3 FP8); B is e4m3.
+template <int FA, int K>
+__device__ inline v4f mfma(const v8i &a, const v8i &b, v4f acc, uint32_t as, uint32_t ws) {
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, acc, FA, 0, K, (int)as, K,
                                                           (int)ws);
 }
 
@@ -178,146 +176,142 @@ __device__ inline void digits68(const u4 &w, uint32_t (&hd)[4], uint32_t (&ld)[4
 
 template <bool SM>
 __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g) {
-  __shared__ v4f red[kMaxWaves][64];
+  __shared__ v4f red[kMaxWaves][2][64];
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int nw = blockDim.x >> 6;
   const int line = lane & 15;
   const DGeo d(g.n4, g.n6, g.n8);
-  const int64_t slab = blockIdx.x;
-  const uint8_t *wslab = g.w_mant + slab * wd_slab_bytes(d);
+  const int64_t nslab = g.npad / 16;
+  const int64_t slab0 = 2 * (int64_t)blockIdx.x;
+  const bool two = slab0 + 1 < nslab;
+  const int64_t sb = wd_slab_bytes(d);
+  const uint8_t *wsl0 = g.w_mant + slab0 * sb;
+  const uint8_t *wsl1 = two ? wsl0 + sb : wsl0;
   const uint8_t *aimg = g.a_mant + g.a_op;
-  const bool arow = line < g.M;
-  v4f acc = {0.f, 0.f, 0.f, 0.f};
-
   // Lanes of rows >= M read row 0's activation bytes (same addresses as a
   // live lane, so no extra traffic); their output rows are discarded.
-  const int alane = arow ? lane : (lane & ~15);
+  const int alane = line < g.M ? lane : (lane & ~15);
+  v4f acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
 
-  // Pipelined walk over the steps s0, s0 + nw, ... (< n) of one segment:
-  // "full" stages of U steps (every step present) alternate between two
-  // register buffers with no branch between a stage's loads and its use,
-  // so each stage waits only for its own loads; the last prefetch is
-  // clamped to the final stage.  The remaining steps run one at a time.
-  auto pipeline = [&](int s0, int U, int n, auto &&load, auto &&comp, auto &&tail) {
-    const int stride = nw * U;
-    const int nf = s0 + (U - 1) * nw < n ? (n - 1 - s0 - (U - 1) * nw) / stride + 1 : 0;
-    if (nf > 0) {
-      load(0, s0);
-      int i = 0;
-      for (; i + 1 < nf; i += 2) {
-        load(1, s0 + (i + 1) * stride);
-        comp(0);
-        load(0, s0 + (i + 2 < nf ? i + 2 : nf - 1) * stride);
-        comp(1);
+  // One group of up to four steps of a segment for both slabs: all loads
+  // first, then the products.  FULL groups carry no per-step guards.
+  auto group4 = [&](int gi, int nst) {
+    constexpr int sd = wd_step_data(0), ad = ad_step_data(0);
+    const uint8_t *g0 = wsl0 + grp_off(gi, sd), *g1 = wsl1 + grp_off(gi, sd);
+    const uint8_t *ga = aimg + grp_off(gi, ad);
+    const uint32_t sw0 = *(const uint32_t *)(g0 + 4 * lane);
+    const uint32_t sw1 = *(const uint32_t *)(g1 + 4 * lane);
+    const uint32_t sa = *(const uint32_t *)(ga + 4 * alane);
+    u4 x0[4], x1[4], p[4];
+    u2 q[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      x0[k] = x1[k] = p[k] = u4{0u, 0u, 0u, 0u};
+      q[k] = u2{0u, 0u};
+      if (k < nst) {
+        x0[k] = *(const u4 *)(g0 + kScaleBlock + k * sd + 16 * lane);
+        x1[k] = *(const u4 *)(g1 + kScaleBlock + k * sd + 16 * lane);
+        p[k] = *(const u4 *)(ga + kScaleBlock + k * ad + 16 * alane);
+        q[k] = *(const u2 *)(ga + kScaleBlock + k * ad + 1024 + 8 * alane);
       }
-      if (i < nf) comp(0);
     }
-    for (int sk = s0 + nf * stride; sk < n; sk += nw) tail(sk);
+    // steps past a short group are skipped: their scale bytes are
+    // unspecified (an E8M0 NaN would poison even zero products)
+    auto step = [&](auto kc) {
+      constexpr int k = decltype(kc)::value;
+      if (k >= nst) return;
+      const v8i a = {(int)p[k][0], (int)p[k][1], (int)p[k][2], (int)p[k][3],
+                     (int)q[k][0], (int)q[k][1], 0, 0};
+      acc0 = mfma<3, k>(a, digits4<SM>(x0[k]), acc0, sa, sw0);
+      acc1 = mfma<3, k>(a, digits4<SM>(x1[k]), acc1, sa, sw1);
+    };
+    step(std::integral_constant<int, 0>());
+    step(std::integral_constant<int, 1>());
+    step(std::integral_constant<int, 2>());
+    step(std::integral_constant<int, 3>());
   };
 
-  // 4-bit steps: A e3m2 (format 3) x W e4m3 (format 0), one instruction per
-  // step; the wave takes steps wave, wave + nw, ...
+  // 4-bit steps: A e3m2 (FP6) x W e4m3, one instruction per step and slab;
+  // the wave takes groups wave, wave + nw, ...
   {
-    u4 w[2][kU4], a0[2][kU4];
-    u2 a1[2][kU4];
-    uint32_t ws[2][kU4], as[2][kU4];
-    auto load = [&](int buf, int s) {
-#pragma unroll
-      for (int k = 0; k < kU4; ++k) {
-        const uint8_t *wc = wslab + (int64_t)(s + k * nw) * wd_chunk(0);
-        const uint8_t *ac = aimg + (int64_t)(s + k * nw) * ad_chunk(0);
-        w[buf][k] = *(const u4 *)(wc + 16 * lane);
-        ws[buf][k] = wc[1024 + lane];
-        a0[buf][k] = *(const u4 *)(ac + 16 * alane);
-        a1[buf][k] = *(const u2 *)(ac + 1024 + 8 * alane);
-        as[buf][k] = ac[1536 + alane];
-      }
-    };
-    auto comp = [&](int buf) {
-#pragma unroll
-      for (int k = 0; k < kU4; ++k) {
-        const v8i b = digits4<SM>(w[buf][k]);
-        const v8i a = {(int)a0[buf][k][0], (int)a0[buf][k][1], (int)a0[buf][k][2],
-                       (int)a0[buf][k][3], (int)a1[buf][k][0], (int)a1[buf][k][1], 0, 0};
-        acc = mfma(a, b, acc, 3, as[buf][k], ws[buf][k]);
-      }
-    };
-    auto tail = [&](int sk) {
-      const uint8_t *wc = wslab + (int64_t)sk * wd_chunk(0);
-      const uint8_t *ac = aimg + (int64_t)sk * ad_chunk(0);
-      const u4 x = *(const u4 *)(wc + 16 * lane);
-      const u4 p = *(const u4 *)(ac + 16 * alane);
-      const u2 q = *(const u2 *)(ac + 1024 + 8 * alane);
-      const v8i a = {(int)p[0], (int)p[1], (int)p[2], (int)p[3], (int)q[0], (int)q[1], 0, 0};
-      acc = mfma(a, digits4<SM>(x), acc, 3, ac[1536 + alane], wc[1024 + lane]);
-    };
-    pipeline(wave, kU4, d.S4, load, comp, tail);
+    const int S = d.S[0], nfg = S / kStreamGroup, rem = S % kStreamGroup;
+    for (int gi = wave; gi < nfg; gi += nw) group4(gi, kStreamGroup);
+    if (rem && wave == nfg % nw) group4(nfg, rem);
   }
 
   // 6-bit and 8-bit steps: FP8 digits on both sides, two instructions per
-  // step (the weight digits' halves swapped in the second)
+  // step and slab (the weight digits' halves swapped in the second)
   auto run68 = [&](auto segc) {
     constexpr int SEG = decltype(segc)::value;
-    constexpr int lb = wd_lane_bytes(SEG);
-    const int sb = SEG == 1 ? d.S4 : d.S4 + d.S6;
-    const int n = SEG == 1 ? d.S6 : d.S8;
-    const uint8_t *wseg = wslab + wd_step_off(d, sb);
-    const uint8_t *aseg = aimg + ad_step_off(d, sb);
-    u4 w[2][kU68], a0[2][kU68], a1[2][kU68];
-    uint32_t ws[2][kU68], as[2][kU68];
-    auto load1 = [&](int sk, u4 &wv, u4 &p0, u4 &p1, uint32_t &wsv, uint32_t &asv) {
-      const uint8_t *wc = wseg + (int64_t)sk * wd_chunk(SEG);
-      const uint8_t *ac = aseg + (int64_t)sk * ad_chunk(SEG);
-      if (SEG == 1) {
-        const u2 nb = *(const u2 *)(wc + 8 * lane);
-        wv = u4{nb[0], nb[1], *(const uint32_t *)(wc + 512 + 4 * lane), 0u};
-      } else {
-        wv = *(const u4 *)(wc + 16 * lane);
+    constexpr int sd = wd_step_data(SEG), ad = ad_step_data(SEG);
+    const uint8_t *w0 = wsl0 + wd_seg_off(d, SEG), *w1 = wsl1 + wd_seg_off(d, SEG);
+    const uint8_t *a0 = aimg + ad_seg_off(d, SEG);
+    auto group = [&](int gi, int nst) {
+      const uint8_t *g0 = w0 + grp_off(gi, sd), *g1 = w1 + grp_off(gi, sd);
+      const uint8_t *ga = a0 + grp_off(gi, ad);
+      const uint32_t sw0 = *(const uint32_t *)(g0 + 4 * lane);
+      const uint32_t sw1 = *(const uint32_t *)(g1 + 4 * lane);
+      const uint32_t sa = *(const uint32_t *)(ga + 4 * alane);
+      u4 x0[4], x1[4], p[4], r[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        x0[k] = x1[k] = p[k] = r[k] = u4{0u, 0u, 0u, 0u};
+        if (k < nst) {
+          const uint8_t *c0 = g0 + kScaleBlock + k * sd, *c1 = g1 + kScaleBlock + k * sd;
+          if (SEG == 1) {
+            const u2 n0 = *(const u2 *)(c0 + 8 * lane), n1 = *(const u2 *)(c1 + 8 * lane);
+            x0[k] = u4{n0[0], n0[1], *(const uint32_t *)(c0 + 512 + 4 * lane), 0u};
+            x1[k] = u4{n1[0], n1[1], *(const uint32_t *)(c1 + 512 + 4 * lane), 0u};
+          } else {
+            x0[k] = *(const u4 *)(c0 + 16 * lane);
+            x1[k] = *(const u4 *)(c1 + 16 * lane);
+          }
+          const uint8_t *ca = ga + kScaleBlock + k * ad + 32 * alane;
+          p[k] = *(const u4 *)ca;
+          r[k] = *(const u4 *)(ca + 16);
+        }
       }
-      wsv = wc[64 * lb + lane];
-      p0 = *(const u4 *)(ac + 32 * alane);
-      p1 = *(const u4 *)(ac + 32 * alane + 16);
-      asv = ac[2048 + alane];
+      auto step = [&](auto kc) {
+        constexpr int k = decltype(kc)::value;
+        if (k >= nst) return;
+        const v8i a = {(int)p[k][0], (int)p[k][1], (int)p[k][2], (int)p[k][3],
+                       (int)r[k][0], (int)r[k][1], (int)r[k][2], (int)r[k][3]};
+        uint32_t hd[4], ld[4];
+        digits68<SM, SEG>(x0[k], hd, ld);
+        v8i bhl = {(int)hd[0], (int)hd[1], (int)hd[2], (int)hd[3],
+                   (int)ld[0], (int)ld[1], (int)ld[2], (int)ld[3]};
+        v8i blh = {(int)ld[0], (int)ld[1], (int)ld[2], (int)ld[3],
+                   (int)hd[0], (int)hd[1], (int)hd[2], (int)hd[3]};
+        acc0 = mfma<0, k>(a, bhl, acc0, sa, sw0);
+        acc0 = mfma<0, k>(a, blh, acc0, sa, sw0);
+        digits68<SM, SEG>(x1[k], hd, ld);
+        bhl = v8i{(int)hd[0], (int)hd[1], (int)hd[2], (int)hd[3],
+                  (int)ld[0], (int)ld[1], (int)ld[2], (int)ld[3]};
+        blh = v8i{(int)ld[0], (int)ld[1], (int)ld[2], (int)ld[3],
+                  (int)hd[0], (int)hd[1], (int)hd[2], (int)hd[3]};
+        acc1 = mfma<0, k>(a, bhl, acc1, sa, sw1);
+        acc1 = mfma<0, k>(a, blh, acc1, sa, sw1);
+      };
+      step(std::integral_constant<int, 0>());
+      step(std::integral_constant<int, 1>());
+      step(std::integral_constant<int, 2>());
+      step(std::integral_constant<int, 3>());
     };
-    auto mul = [&](const u4 &wv, const u4 &p0, const u4 &p1, uint32_t wsv, uint32_t asv) {
-      uint32_t hd[4], ld[4];
-      digits68<SM, SEG>(wv, hd, ld);
-      const v8i a = {(int)p0[0], (int)p0[1], (int)p0[2], (int)p0[3],
-                     (int)p1[0], (int)p1[1], (int)p1[2], (int)p1[3]};
-      const v8i bhl = {(int)hd[0], (int)hd[1], (int)hd[2], (int)hd[3],
-                       (int)ld[0], (int)ld[1], (int)ld[2], (int)ld[3]};
-      const v8i blh = {(int)ld[0], (int)ld[1], (int)ld[2], (int)ld[3],
-                       (int)hd[0], (int)hd[1], (int)hd[2], (int)hd[3]};
-      acc = mfma(a, bhl, acc, 0, asv, wsv);
-      acc = mfma(a, blh, acc, 0, asv, wsv);
-    };
-    auto load = [&](int buf, int s) {
-#pragma unroll
-      for (int k = 0; k < kU68; ++k)
-        load1(s + k * nw, w[buf][k], a0[buf][k], a1[buf][k], ws[buf][k], as[buf][k]);
-    };
-    auto comp = [&](int buf) {
-#pragma unroll
-      for (int k = 0; k < kU68; ++k) mul(w[buf][k], a0[buf][k], a1[buf][k], ws[buf][k], as[buf][k]);
-    };
-    auto tail = [&](int sk) {
-      u4 wv, p0, p1;
-      uint32_t wsv, asv;
-      load1(sk, wv, p0, p1, wsv, asv);
-      mul(wv, p0, p1, wsv, asv);
-    };
-    pipeline(wave, kU68, n, load, comp, tail);
+    const int S = d.S[SEG], nfg = S / kStreamGroup, rem = S % kStreamGroup;
+    for (int gi = wave; gi < nfg; gi += nw) group(gi, kStreamGroup);
+    if (rem && wave == nfg % nw) group(nfg, rem);
   };
   run68(std::integral_constant<int, 1>());
   run68(std::integral_constant<int, 2>());
 
-  red[wave][lane] = acc;
+  red[wave][0][lane] = acc0;
+  red[wave][1][lane] = acc1;
   __syncthreads();
-  if (wave == 0) {
-    v4f y = red[0][lane];
-    for (int w = 1; w < nw; ++w) y += red[w][lane];
-    const int64_t col = slab * 16 + line;
+  if (wave < 2 && (wave == 0 || two)) {
+    v4f y = red[0][wave][lane];
+    for (int w = 1; w < nw; ++w) y += red[w][wave][lane];
+    const int64_t col = (slab0 + wave) * 16 + line;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int row = 4 * (lane >> 4) + i;
@@ -328,10 +322,10 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
 
 }  // namespace
 
-// Waves per workgroup (one workgroup per 16-column slab): enough for about
-// 16 waves per CU when every slab is resident at once (2 for 1792 slabs,
-// 8 for 512 slabs).
-static int decode_waves(int64_t slabs) {
+// Waves per workgroup (one workgroup per pair of 16-column slabs): enough
+// for about 16 waves per CU when every pair is resident at once (4 for 896
+// pairs, 16 for 256 pairs).
+static int decode_waves(int64_t pairs) {
   int cus = 256;
   int dev = 0;
   if (hipGetDevice(&dev) == hipSuccess) {
@@ -340,15 +334,15 @@ static int decode_waves(int64_t slabs) {
         n > 0)
       cus = n;
   }
-  int64_t w = (16LL * cus + slabs - 1) / slabs;
+  int64_t w = 16LL * cus / pairs;      // rounded down: every pair stays resident
   if (w < 2) w = 2;
   if (w > kMaxWaves) w = kMaxWaves;
   return (int)w;
 }
 
 hipError_t launch_gemm_decode(const GemmArgs &a, hipStream_t stream) {
-  const int64_t slabs = a.npad / 16;
-  dim3 grid((unsigned)slabs), block((unsigned)(64 * decode_waves(slabs)));
+  const int64_t pairs = (a.npad / 16 + 1) / 2;
+  dim3 grid((unsigned)pairs), block((unsigned)(64 * decode_waves(pairs)));
   if (a.sm)
     hipLaunchKernelGGL(gemm_decode_kernel<true>, grid, block, 0, stream, a);
   else

@@ -55,9 +55,11 @@ __host__ __device__ inline BlockInfo block_info(const Segs &s, int b) {
 // 16 g + c (c = line) holds 32 elements of K-group g and supplies the E8M0
 // scale of K-block g of its line.  Steps: the 4-bit blocks four at a time
 // (padded with zero blocks to a multiple of 4), the 6-bit and the 8-bit
-// blocks two at a time (each padded to a multiple of 2).  A step chunk is
-// the 64 lanes' data (lane l at LB * l unless split into planes as noted),
-// then 64 scale bytes in lane order.
+// blocks two at a time (each padded to a multiple of 2).  The steps of each
+// segment form groups of four (the last may be shorter): a 256-byte scale
+// block (lane l's scale bytes of the group's steps k = 0..3 at 4 l + k),
+// then each step's lane data (lane l at LB * l unless split into planes as
+// noted).
 //
 // With the block's E as E8M0 scale, the FP8 digits of a mantissa sum to
 // q * 2^-(m-2): e4m3(q/4) for a 4-bit q; two digits for 6- and 8-bit q.
@@ -90,44 +92,60 @@ __host__ __device__ inline BlockInfo block_info(const Segs &s, int b) {
 //     their low digits (16 bytes); scale byte E of block 2s+(g&1).
 // ---------------------------------------------------------------------------
 constexpr int kStreamLanes = 64;
+constexpr int kStreamGroup = 4;          // steps sharing one scale block
+constexpr int kScaleBlock = 256;         // 64 lanes x 4 scale bytes
 
 struct DGeo {
   int n4, n6, n8;
-  int S4, S6, S8, nsteps;
-  __host__ __device__ DGeo(int a, int b, int c)
-      : n4(a), n6(b), n8(c), S4((a + 3) / 4), S6((b + 1) / 2), S8((c + 1) / 2),
-        nsteps(S4 + S6 + S8) {}
+  int S[3];              // steps of each segment
+  int nsteps;
+  __host__ __device__ DGeo(int a, int b, int c) : n4(a), n6(b), n8(c) {
+    S[0] = (a + 3) / 4;
+    S[1] = (b + 1) / 2;
+    S[2] = (c + 1) / 2;
+    nsteps = S[0] + S[1] + S[2];
+  }
 };
 
 // lane-data bytes of a weight / activation step of each segment
 __host__ __device__ constexpr int wd_lane_bytes(int seg) { return seg == 1 ? 12 : 16; }
 __host__ __device__ constexpr int ad_lane_bytes(int seg) { return seg == 0 ? 24 : 32; }
-__host__ __device__ constexpr int wd_chunk(int seg) { return kStreamLanes * (wd_lane_bytes(seg) + 1); }
-__host__ __device__ constexpr int ad_chunk(int seg) { return kStreamLanes * (ad_lane_bytes(seg) + 1); }
+// bytes of the 64 lanes' data of one step
+__host__ __device__ constexpr int wd_step_data(int seg) { return kStreamLanes * wd_lane_bytes(seg); }
+__host__ __device__ constexpr int ad_step_data(int seg) { return kStreamLanes * ad_lane_bytes(seg); }
 
-// byte offset of step st in a weight slab / the activation decode image
-__host__ __device__ inline int64_t wd_step_off(const DGeo &d, int st) {
-  if (st <= d.S4) return (int64_t)wd_chunk(0) * st;
-  if (st <= d.S4 + d.S6) return (int64_t)wd_chunk(0) * d.S4 + (int64_t)wd_chunk(1) * (st - d.S4);
-  return (int64_t)wd_chunk(0) * d.S4 + (int64_t)wd_chunk(1) * d.S6 +
-         (int64_t)wd_chunk(2) * (st - d.S4 - d.S6);
+// A segment of S steps is a run of groups of kStreamGroup steps (the last one
+// may be shorter): each group is its scale block (lane l's scale byte for
+// step k of the group at 4 l + k) followed by its steps' lane data.
+__host__ __device__ inline int64_t seg_bytes(int S, int step_data) {
+  return (int64_t)S * step_data + (int64_t)((S + kStreamGroup - 1) / kStreamGroup) * kScaleBlock;
 }
-__host__ __device__ inline int64_t ad_step_off(const DGeo &d, int st) {
-  if (st <= d.S4) return (int64_t)ad_chunk(0) * st;
-  return (int64_t)ad_chunk(0) * d.S4 + (int64_t)ad_chunk(1) * (st - d.S4);
+__host__ __device__ inline int64_t grp_off(int g, int step_data) {
+  return (int64_t)g * (kStreamGroup * step_data + kScaleBlock);
 }
-__host__ __device__ inline int64_t wd_slab_bytes(const DGeo &d) { return wd_step_off(d, d.nsteps); }
-__host__ __device__ inline int64_t ad_image_bytes(const DGeo &d) { return ad_step_off(d, d.nsteps); }
+// byte offset of segment seg in a weight slab / the activation decode image
+__host__ __device__ inline int64_t wd_seg_off(const DGeo &d, int seg) {
+  int64_t o = 0;
+  for (int s = 0; s < seg; ++s) o += seg_bytes(d.S[s], wd_step_data(s));
+  return o;
+}
+__host__ __device__ inline int64_t ad_seg_off(const DGeo &d, int seg) {
+  int64_t o = 0;
+  for (int s = 0; s < seg; ++s) o += seg_bytes(d.S[s], ad_step_data(s));
+  return o;
+}
+__host__ __device__ inline int64_t wd_slab_bytes(const DGeo &d) { return wd_seg_off(d, 3); }
+__host__ __device__ inline int64_t ad_image_bytes(const DGeo &d) { return ad_seg_off(d, 3); }
 
-// Where block `idx` of segment `seg` lives in the stream layout: its step,
-// the lane group of each half (elements 16h..16h+15 sit in lane group
-// g0 + h), the byte offset of its elements inside a 4-bit lane (0 or 8) and
-// the lane groups whose scale byte is the block's exponent (one for 4-bit
-// blocks, two for 6/8-bit blocks).
+// Where block `idx` of segment `seg` lives in the stream layout: its step
+// within the segment, the lane group of each half (elements 16h..16h+15 sit
+// in lane group g0 + h), the byte offset of its elements inside a 4-bit lane
+// (0 or 8) and the lane groups whose scale byte is the block's exponent (one
+// for 4-bit blocks, two for 6/8-bit blocks).
 struct DLoc {
   int st, g0, region, sg0, sg1;
 };
-__host__ __device__ inline DLoc d_loc(const DGeo &d, int seg, int idx) {
+__host__ __device__ inline DLoc d_loc(int seg, int idx) {
   DLoc r;
   if (seg == 0) {
     r.st = idx >> 2;
@@ -135,13 +153,22 @@ __host__ __device__ inline DLoc d_loc(const DGeo &d, int seg, int idx) {
     r.region = 8 * ((idx >> 1) & 1);
     r.sg0 = r.sg1 = idx & 3;
   } else {
-    r.st = (seg == 1 ? d.S4 : d.S4 + d.S6) + (idx >> 1);
+    r.st = idx >> 1;
     r.g0 = 2 * (idx & 1);
     r.region = 0;
     r.sg0 = idx & 1;
     r.sg1 = r.sg0 + 2;
   }
   return r;
+}
+
+// Step st of a segment starting at `seg`: its data and its group's scales.
+__host__ __device__ inline int64_t step_data_off(int st, int step_data) {
+  return grp_off(st / kStreamGroup, step_data) + kScaleBlock +
+         (int64_t)(st % kStreamGroup) * step_data;
+}
+__host__ __device__ inline int64_t step_scale_off(int st, int step_data, int lane) {
+  return grp_off(st / kStreamGroup, step_data) + 4 * lane + st % kStreamGroup;
 }
 
 // Stream codes of a mantissa: the nibble (4-bit q, or the low part of a
@@ -229,8 +256,8 @@ __device__ inline int act_elem(const uint8_t *row, const BlockInfo &bi, int t) {
 // sm = sign-magnitude codes (symmetric clamp).
 __device__ inline int wstream_elem(const uint8_t *slab, const DGeo &dg, const BlockInfo &bi,
                                    int c, int t, bool sm) {
-  const DLoc L = d_loc(dg, bi.seg, bi.idx);
-  const uint8_t *chunk = slab + wd_step_off(dg, L.st);
+  const DLoc L = d_loc(bi.seg, bi.idx);
+  const uint8_t *chunk = slab + wd_seg_off(dg, bi.seg) + step_data_off(L.st, wd_step_data(bi.seg));
   const int ln = 16 * (L.g0 + (t >> 4)) + c;
   const int u = t & 15;                     // element within the half
   if (bi.m == 8) return (int)(int8_t)chunk[16 * ln + u];

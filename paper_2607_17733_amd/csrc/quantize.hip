@@ -159,9 +159,10 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
         const DGeo dg(q.n4, q.n6, q.n8);
         const int c16 = (int)(row & 15);
         uint8_t *slab = q.mant + (row >> 4) * wd_slab_bytes(dg);
-        const DLoc L = d_loc(dg, bi.seg, bi.idx);
-        uint8_t *chunk = slab + wd_step_off(dg, L.st);
-        const int lb = wd_lane_bytes(bi.seg);
+        const DLoc L = d_loc(bi.seg, bi.idx);
+        const int sd = wd_step_data(bi.seg);
+        uint8_t *segp = slab + wd_seg_off(dg, bi.seg);
+        uint8_t *chunk = segp + step_data_off(L.st, sd);
         const int dd = kg & 1;
         const int ln = 16 * (L.g0 + (kg >> 1)) + c16;
         if (bi.m == 4) {
@@ -174,20 +175,21 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
           *(uint32_t *)(chunk + 16 * ln + 8 * dd + 4) = hi8;
         }
         if (kg == 0) {
-          chunk[64 * lb + 16 * L.sg0 + c16] = (uint8_t)E;
-          if (bi.seg) chunk[64 * lb + 16 * L.sg1 + c16] = (uint8_t)E;
+          segp[step_scale_off(L.st, sd, 16 * L.sg0 + c16)] = (uint8_t)E;
+          if (bi.seg) segp[step_scale_off(L.st, sd, 16 * L.sg1 + c16)] = (uint8_t)E;
           q.exp[row * q.out_erb + b] = (uint8_t)E;
         }
         if (g == 0) {
           for (int64_t z = nb; z < q.out_erb; ++z) q.exp[row * q.out_erb + z] = 0;
           // zero the stream padding blocks of this column
           const int nseg[3] = {dg.n4, dg.n6, dg.n8};
-          const int npad[3] = {4 * dg.S4, 2 * dg.S6, 2 * dg.S8};
+          const int npad[3] = {4 * dg.S[0], 2 * dg.S[1], 2 * dg.S[2]};
           for (int sg = 0; sg < 3; ++sg) {
-            const int plb = wd_lane_bytes(sg);
+            const int psd = wd_step_data(sg);
+            uint8_t *pseg = slab + wd_seg_off(dg, sg);
             for (int idx = nseg[sg]; idx < npad[sg]; ++idx) {
-              const DLoc P = d_loc(dg, sg, idx);
-              uint8_t *pc = slab + wd_step_off(dg, P.st);
+              const DLoc P = d_loc(sg, idx);
+              uint8_t *pc = pseg + step_data_off(P.st, psd);
               for (int hh = 0; hh < 2; ++hh) {
                 const int pl = 16 * (P.g0 + hh) + c16;
                 if (sg == 0) {
@@ -199,9 +201,13 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
                   *(uint4 *)(pc + 16 * pl) = make_uint4(0, 0, 0, 0);
                 }
               }
-              pc[64 * plb + 16 * P.sg0 + c16] = 0;
-              if (sg) pc[64 * plb + 16 * P.sg1 + c16] = 0;
+              pseg[step_scale_off(P.st, psd, 16 * P.sg0 + c16)] = 0;
+              if (sg) pseg[step_scale_off(P.st, psd, 16 * P.sg1 + c16)] = 0;
             }
+            // the unused scale bytes of a short last group
+            const int S = dg.S[sg];
+            for (int st = S; st < (S + kStreamGroup - 1) / kStreamGroup * kStreamGroup; ++st)
+              for (int gg = 0; gg < 4; ++gg) pseg[step_scale_off(st, psd, 16 * gg + c16)] = 0;
           }
         }
       }

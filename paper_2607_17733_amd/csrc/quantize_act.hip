@@ -205,14 +205,16 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
   if (q.dimg) {
     // decode image (M <= 16): the stream layout's ready operands, see DGeo
     const DGeo dg(og.n4, og.n6, og.n8);
-    const DLoc L = d_loc(dg, seg, idx);
-    uint8_t *chunk = q.mant + q.op_off + ad_step_off(dg, L.st);
+    const DLoc L = d_loc(seg, idx);
+    const int sd = ad_step_data(seg);
+    uint8_t *segp = q.mant + q.op_off + ad_seg_off(dg, seg);
+    uint8_t *chunk = segp + step_data_off(L.st, sd);
     if (seg == 0) {
       const int l = 16 * L.sg0 + (int)row;
       const v6u c = to_e3m2(v, 4.f);
       *(u4 *)(chunk + 16 * l) = u4{c[0], c[1], c[2], c[3]};
       *(u2 *)(chunk + 1024 + 8 * l) = u2{c[4], c[5]};
-      chunk[1536 + l] = (uint8_t)Eu;
+      segp[step_scale_off(L.st, sd, l)] = (uint8_t)Eu;
     } else {
       Blk hd, ld;                              // q = 16 h + l
 #pragma unroll
@@ -230,8 +232,8 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
         *(u4 *)(chunk + 32 * l) = to_e4m3(hd, h, dh);
         *(u4 *)(chunk + 32 * l + 16) = to_e4m3(ld, h, dl);
       }
-      chunk[2048 + 16 * L.sg0 + row] = (uint8_t)Eu;
-      chunk[2048 + 16 * L.sg1 + row] = (uint8_t)Eu;
+      segp[step_scale_off(L.st, sd, 16 * L.sg0 + (int)row)] = (uint8_t)Eu;
+      segp[step_scale_off(L.st, sd, 16 * L.sg1 + (int)row)] = (uint8_t)Eu;
     }
     return;
   }

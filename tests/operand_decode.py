@@ -197,6 +197,9 @@ A_LANE = {0: 24, 1: 32, 2: 32}
 LANES = 64
 
 
+GROUP = 4          # steps sharing one 256-byte scale block
+
+
 class SGeo:
     def __init__(self, widths):
         w = np.asarray(widths)
@@ -205,17 +208,32 @@ class SGeo:
         self.nb = len(w)
         self.base = [0, self.n[0], self.n[0] + self.n[1]]   # first block of each segment
 
-    def steps(self):
-        """(segment, step within the segment) in stream order."""
-        for seg in range(3):
-            for s in range(self.S[seg]):
-                yield seg, s
+    @staticmethod
+    def seg_bytes(S, step_data):
+        return S * step_data + -(-S // GROUP) * LANES * 4
+
+    def w_seg_off(self, seg):
+        return sum(self.seg_bytes(self.S[s], LANES * W_LANE[s]) for s in range(seg))
+
+    def a_seg_off(self, seg):
+        return sum(self.seg_bytes(self.S[s], LANES * A_LANE[s]) for s in range(seg))
 
     def w_slab_bytes(self):
-        return sum(self.S[seg] * LANES * (W_LANE[seg] + 1) for seg in range(3))
+        return self.w_seg_off(3)
 
     def a_image_bytes(self):
-        return sum(self.S[seg] * LANES * (A_LANE[seg] + 1) for seg in range(3))
+        return self.a_seg_off(3)
+
+
+def _step(buf, seg_off, st, step_data):
+    """(lane data [step_data bytes], scale bytes [64] of the step) of a
+    segment starting at seg_off: groups of GROUP steps, each a scale block
+    (lane l's byte for step k at 4 l + k) then the steps' data."""
+    g = seg_off + (st // GROUP) * (GROUP * step_data + LANES * 4)
+    data = buf[..., g + LANES * 4 + (st % GROUP) * step_data:
+               g + LANES * 4 + (st % GROUP + 1) * step_data]
+    sc = buf[..., g: g + LANES * 4].reshape(buf.shape[:-1] + (LANES, 4))[..., st % GROUP]
+    return data, sc
 
 
 def _sext(v, bits):
@@ -250,54 +268,57 @@ def decode_w_stream(img, widths, N, sm=True):
     q = np.zeros((nsl * 16, g.nb * BLOCK), np.int64)
     E = np.full((nsl * 16, g.nb), -1, np.int64)
     ok = True
-    off = 0
-    for seg, s in g.steps():
-        lb = W_LANE[seg]
-        ch = slabs[:, off:off + LANES * (lb + 1)]
-        off += LANES * (lb + 1)
-        sc = ch[:, LANES * lb:].reshape(nsl, 4, 16).astype(np.int64)   # [slab, g, col]
-        for gg in range(4):
-            half = gg & 1
-            if seg == 0:
-                lane = ch[:, :LANES * 16].reshape(nsl, 4, 16, 16)[:, gg]   # [slab, col, 16]
-                parts = [(4 * s + (gg >> 1), lane[..., 0:8]), (4 * s + 2 + (gg >> 1), lane[..., 8:16])]
-                dec = _sm_nibble if sm else (lambda v: _sext(v, 4))
-                vals = [(blk, dec(_stream_nibbles(p))) for blk, p in parts]
-            else:
-                blk = 2 * s + (gg >> 1)
-                if seg == 1:
-                    nib = ch[:, :LANES * 8].reshape(nsl, 4, 16, 8)[:, gg]
-                    top = ch[:, 512:512 + LANES * 4].reshape(nsl, 4, 16, 4)[:, gg]
-                    y = top.astype(np.int64)
-                    y = y[..., 0] | (y[..., 1] << 8) | (y[..., 2] << 16) | (y[..., 3] << 24)
-                    lo = _stream_nibbles(nib)
-                    t2 = np.stack([(y >> (8 * (u % 4) + 2 * (u // 4))) & 3 for u in range(16)],
-                                  axis=-1)
-                    if sm:      # |q| = 8 t2 + (lo & 7), sign at bit 3 of lo
-                        v = np.where(lo & 8, -(8 * t2 + (lo & 7)), 8 * t2 + (lo & 7))
-                    else:
-                        v = _sext(lo | (t2 << 4), 6)
+    for seg in range(3):
+        sd = LANES * W_LANE[seg]
+        for s in range(g.S[seg]):
+            ch, scb = _step(slabs, g.w_seg_off(seg), s, sd)
+            sc = scb.reshape(nsl, 4, 16).astype(np.int64)          # [slab, g, col]
+            for gg in range(4):
+                half = gg & 1
+                if seg == 0:
+                    lane = ch.reshape(nsl, 4, 16, 16)[:, gg]        # [slab, col, 16]
+                    parts = [(4 * s + (gg >> 1), lane[..., 0:8]), (4 * s + 2 + (gg >> 1), lane[..., 8:16])]
+                    dec = _sm_nibble if sm else (lambda v: _sext(v, 4))
+                    vals = [(blk, dec(_stream_nibbles(p))) for blk, p in parts]
                 else:
-                    v = _sext(ch[:, :LANES * 16].reshape(nsl, 4, 16, 16)[:, gg], 8)
-                vals = [(blk, v)]
-            for blk, v in vals:
-                v = v.reshape(nsl * 16, 16)
+                    blk = 2 * s + (gg >> 1)
+                    if seg == 1:
+                        nib = ch[:, :LANES * 8].reshape(nsl, 4, 16, 8)[:, gg]
+                        top = ch[:, 512:512 + LANES * 4].reshape(nsl, 4, 16, 4)[:, gg]
+                        y = top.astype(np.int64)
+                        y = y[..., 0] | (y[..., 1] << 8) | (y[..., 2] << 16) | (y[..., 3] << 24)
+                        lo = _stream_nibbles(nib)
+                        t2 = np.stack([(y >> (8 * (u % 4) + 2 * (u // 4))) & 3 for u in range(16)],
+                                      axis=-1)
+                        if sm:      # |q| = 8 t2 + (lo & 7), sign at bit 3 of lo
+                            v = np.where(lo & 8, -(8 * t2 + (lo & 7)), 8 * t2 + (lo & 7))
+                        else:
+                            v = _sext(lo | (t2 << 4), 6)
+                    else:
+                        v = _sext(ch.reshape(nsl, 4, 16, 16)[:, gg], 8)
+                    vals = [(blk, v)]
+                for blk, v in vals:
+                    v = v.reshape(nsl * 16, 16)
+                    if blk < g.n[seg]:
+                        b = g.base[seg] + blk
+                        q[:, BLOCK * b + 16 * half: BLOCK * b + 16 * half + 16] = v
+                    else:
+                        ok &= not v.any()
+            # lane group gg carries the exponent of block 4s+gg (4-bit) or
+            # 2s+(gg&1) (6/8-bit)
+            for gg in range(4):
+                blk = 4 * s + gg if seg == 0 else 2 * s + (gg & 1)
+                e = sc[:, gg].reshape(nsl * 16)
                 if blk < g.n[seg]:
                     b = g.base[seg] + blk
-                    q[:, BLOCK * b + 16 * half: BLOCK * b + 16 * half + 16] = v
+                    ok &= bool(np.all((E[:, b] == -1) | (E[:, b] == e)))
+                    E[:, b] = e
                 else:
-                    ok &= not v.any()
-        # scale bytes: lane group gg carries the exponent of block
-        # 4s+gg (4-bit) or 2s+(gg&1) (6/8-bit)
-        for gg in range(4):
-            blk = 4 * s + gg if seg == 0 else 2 * s + (gg & 1)
-            e = sc[:, gg].reshape(nsl * 16)
-            if blk < g.n[seg]:
-                b = g.base[seg] + blk
-                ok &= bool(np.all((E[:, b] == -1) | (E[:, b] == e)))
-                E[:, b] = e
-            else:
-                ok &= not e.any()
+                    ok &= not e.any()
+        # scale bytes of the missing steps of a short last group are zero
+        for s in range(g.S[seg], -(-g.S[seg] // GROUP) * GROUP):
+            _, scb = _step(slabs, g.w_seg_off(seg), s, sd)
+            ok &= not scb.any()
     return q, E, ok
 
 
@@ -308,42 +329,39 @@ def decode_act_dimg(img, widths, M):
     q = np.zeros((16, g.nb * BLOCK), np.int64)
     E = np.full((16, g.nb), -1, np.int64)
     ok = True
-    off = 0
-    for seg, s in g.steps():
-        lb = A_LANE[seg]
-        ch = img[off:off + LANES * (lb + 1)]
-        off += LANES * (lb + 1)
-        sc = ch[LANES * lb:].reshape(4, 16).astype(np.int64)
-        for gg in range(4):
-            if seg == 0:
-                b24 = np.concatenate([ch[:1024].reshape(4, 16, 16)[gg],
-                                      ch[1024:1536].reshape(4, 16, 8)[gg]], axis=1)
-                v = fp6_values(b24) * 4
-                blk, lo, hi = 4 * s + gg, 0, 32
-            else:
-                lane = ch[:2048].reshape(4, 16, 32)[gg]
-                hv, lv = fp8_values(lane[:, :16]), fp8_values(lane[:, 16:])
-                # digits of q = 16 h + l summing to q 2^-(m-2): h + l/16
-                # (6-bit), h/4 + l/64 (8-bit)
-                f = 16 if seg == 1 else 64
-                hv, lv = hv[:M], lv[:M]
-                v = f * (hv + lv)
-                h, l = hv * f / 16, lv * f
-                ok &= bool(np.all((l >= 0) & (l <= 15) & (h == np.floor(v / 16))))
-                blk, lo, hi = 2 * s + (gg >> 1), 16 * (gg & 1), 16 * (gg & 1) + 16
-            v = v[:M]                       # rows past M are unspecified
-            if blk < g.n[seg]:
-                b = g.base[seg] + blk
-                q[:M, BLOCK * b + lo: BLOCK * b + hi] = v
-            else:
-                ok &= not np.any(v)
-        for gg in range(4):
-            blk = 4 * s + gg if seg == 0 else 2 * s + (gg & 1)
-            e = sc[gg]
-            if blk < g.n[seg]:
-                b = g.base[seg] + blk
-                ok &= bool(np.all((E[:M, b] == -1) | (E[:M, b] == e[:M])))
-                E[:, b] = e
-            else:
-                ok &= not e[:M].any()
+    for seg in range(3):
+        sd = LANES * A_LANE[seg]
+        for s in range(g.S[seg]):
+            ch, scb = _step(img, g.a_seg_off(seg), s, sd)
+            sc = scb.reshape(4, 16).astype(np.int64)
+            for gg in range(4):
+                if seg == 0:
+                    b24 = np.concatenate([ch[:1024].reshape(4, 16, 16)[gg],
+                                          ch[1024:1536].reshape(4, 16, 8)[gg]], axis=1)
+                    v = fp6_values(b24)[:M] * 4
+                    blk, lo, hi = 4 * s + gg, 0, 32
+                else:
+                    lane = ch[:2048].reshape(4, 16, 32)[gg]
+                    hv, lv = fp8_values(lane[:M, :16]), fp8_values(lane[:M, 16:])
+                    # digits of q = 16 h + l summing to q 2^-(m-2): h + l/16
+                    # (6-bit), h/4 + l/64 (8-bit)
+                    f = 16 if seg == 1 else 64
+                    v = f * (hv + lv)
+                    h, l = hv * f / 16, lv * f
+                    ok &= bool(np.all((l >= 0) & (l <= 15) & (h == np.floor(v / 16))))
+                    blk, lo, hi = 2 * s + (gg >> 1), 16 * (gg & 1), 16 * (gg & 1) + 16
+                if blk < g.n[seg]:           # rows past M are unspecified
+                    b = g.base[seg] + blk
+                    q[:M, BLOCK * b + lo: BLOCK * b + hi] = v
+                else:
+                    ok &= not np.any(v)
+            for gg in range(4):
+                blk = 4 * s + gg if seg == 0 else 2 * s + (gg & 1)
+                e = sc[gg]
+                if blk < g.n[seg]:
+                    b = g.base[seg] + blk
+                    ok &= bool(np.all((E[:M, b] == -1) | (E[:M, b] == e[:M])))
+                    E[:, b] = e
+                else:
+                    ok &= not e[:M].any()
     return q[:M], E[:M], ok

@@ -58,22 +58,22 @@ def op_steps(widths):
 def stream_sizes(widths):
     """Weight slab and activation decode-image bytes as include/mxq.h states
     them: 4-bit blocks four per step, 6/8-bit blocks two per step; 64 lanes
-    of 16/12/16 (weights) or 24/32/32 (activations) bytes plus 64 scale
-    bytes per step."""
+    of 16/12/16 (weights) or 24/32/32 (activations) bytes per step, and a
+    256-byte scale block per group of four steps of a segment."""
     n4, n6, n8 = (sum(1 for w in widths if w == m) for m in (4, 6, 8))
     S = (-(-n4 // 4), -(-n6 // 2), -(-n8 // 2))
     wlane, alane = (16, 12, 16), (24, 32, 32)
-    return (sum(s * 64 * (l + 1) for s, l in zip(S, wlane)),
-            sum(s * 64 * (l + 1) for s, l in zip(S, alane)))
+    return (sum(s * 64 * l + -(-s // 4) * 256 for s, l in zip(S, wlane)),
+            sum(s * 64 * l + -(-s // 4) * 256 for s, l in zip(S, alane)))
 
 
 def test_sizes(lib):
     w1 = [4] * 6 + [6, 8]
     f, _w = _fmt(256, w1)
-    assert lib.mxq_abi_version() == 3
+    assert lib.mxq_abi_version() == 4
     assert op_steps(w1) == 4
     slab, dimg = stream_sizes(w1)
-    assert (slab, dimg) == (2 * 1088 + 832 + 1088, 2 * 1600 + 2 * 2112)
+    assert (slab, dimg) == (2 * 1024 + 768 + 1024 + 3 * 256, 2 * 1536 + 2 * 2048 + 3 * 256)
     assert lib.mxq_act_packed_bytes(ctypes.byref(f)) == 160
     assert lib.mxq_exp_row_bytes(ctypes.byref(f)) == 16
     # M <= 16: M packed rows + the decode image; larger M: 32-row operand
