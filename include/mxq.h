@@ -25,10 +25,11 @@
  *   -127); a block holding Inf or NaN has E = 255 and zero mantissas.
  * GEMM: Y[i][j] = sum_b P[i][j][b] * 2^(sa[i][b] + sw[j][b]) with
  *   P[i][j][b] = sum_t qa[i][32b+t] * qw[j][32b+t] and s = E - 127 - (m - 2),
- *   accumulated in fp32.  Every elementary product is exact; the prefill
- *   kernel sums them on the block-scaled matrix cores (each block's E is the
- *   hardware scale), the decode kernel forms each P exactly in int32 and
- *   adds it scaled in fp32.  Any block with E == 255 on either side makes
+ *   accumulated in fp32.  Every elementary product is exact: both kernels
+ *   turn each mantissa into one or two FP6/FP8 "digits" whose sum is
+ *   q * 2^-(m - 2), multiply them on the block-scaled matrix cores with each
+ *   block's E as its E8M0 hardware scale, and accumulate in fp32.  Any block
+ *   with E == 255 on either side makes
  *   the outputs it touches NaN.  Results whose magnitude is below fp32's
  *   range (2^-149) flush towards zero.
  *
@@ -104,7 +105,8 @@ const char *mxq_status_str(int status);
  *
  * Activations (the output of mxq_quantize_act for M rows):
  *   a_mant: M packed rows of mxq_act_packed_bytes(fmt) bytes each, then the
- *   matrix-core operand image; mxq_act_bytes(fmt, M) in total.
+ *   matrix-core operand image: the prefill image (2) for M > 16, the decode
+ *   image (3) for 1 <= M <= 16; mxq_act_bytes(fmt, M) in total.
  *   (1) Packed row: the blocks in permuted order, block b taking 4 * m_b
  *   bytes, zero padded to a multiple of 16:
  *     4-bit: byte j holds element 2j in bits 0-3 and element 2j+1 in bits 4-7;
@@ -113,9 +115,9 @@ const char *mxq_status_str(int status);
  *            16d..16d+15, its byte j holds element 16d+2j in bits 6-7,
  *            16d+2j+1 in bits 4-5, 16d+8+2j in bits 2-3, 16d+9+2j in bits 0-1;
  *     8-bit: one two's-complement byte per element.
- *   (2) Operand image: every mantissa q of a block with width m as exact
- *   FP6 / FP8 "digits" whose sum is q * 2^-(m - 2), so that the block's
- *   E8M0 scale is E itself:
+ *   (2) Prefill image (M > 16): every mantissa q of a block with width m
+ *   as exact FP6 / FP8 "digits" whose sum is q * 2^-(m - 2), so that the
+ *   block's E8M0 scale is E itself:
  *     m = 4: one FP6 e3m2 element q/4;
  *     m = 6: h = floor(q/8), l = q - 8h; FP6 e3m2 elements h/2 and l/16;
  *     m = 8: h = floor(q/16), l = q - 16h; FP8 e4m3 elements h/4 and l/64.
@@ -133,21 +135,44 @@ const char *mxq_status_str(int status);
  *   M are unspecified).  Byte o of the lane data of (row r, step s, half h)
  *   is at ((r / 32) * nsteps + s) * 3072 + (o / 16) * 1024 + h * 512
  *   + (r % 32) * 16 + o % 16 of the operand image.
+ *   (3) Decode image (M <= 16), the "stream layout" of 16 lines (line =
+ *   row; rows past M are unspecified) in the lane order of the block-scaled
+ *   16x16x128 matrix-core instruction, lane l = 16 g + line.  Steps: the
+ *   4-bit blocks four at a time (padded to a multiple of 4), then the 6-bit
+ *   and then the 8-bit blocks two at a time (each padded to a multiple of 2).
+ *   Each segment is a run of groups of four steps (the last may be
+ *   shorter): a 256-byte scale block (lane l's byte for step k of the group
+ *   at 4 l + k), then the steps' lane data:
+ *     4-bit step s: lane (g, r) holds block 4s+g of row r as 32 e3m2 codes
+ *       of q/4 (first 16 bytes at 16 l, last 8 at 1024 + 8 l); its scale
+ *       byte is the E of block 4s+g;
+ *     6/8-bit step s: lane (g, r) holds elements 16(g&1)..16(g&1)+15 of
+ *       block 2s+(g>>1), at 32 l: the e4m3 codes of their high digits, then
+ *       of their low digits (q = 16h + l, h = floor(q/16): h and l/16 for
+ *       m = 6, h/4 and l/64 for m = 8); its scale byte is the E of block
+ *       2s+(g&1).
  *   a_exp: M rows of mxq_exp_row_bytes(fmt) bytes (block exponents E, byte b
- *   for block b, zero padded to a multiple of 16), then the operand image's
- *   scale bytes: for (row r, step s, half h) four bytes at
+ *   for block b, zero padded to a multiple of 16); for M > 16 then the
+ *   prefill image's scale bytes: for (row r, step s, half h) four bytes at
  *   ((r / 32) * nsteps + s) * 256 + h * 128 + (r % 32) * 4: the E of block
  *   4s'+h and of block 4s'+2+h for a 4-bit step, the E of the half's block
  *   and 0 for a 6-bit step, the block's E and 0 (both halves) for an 8-bit
  *   step, then two zero bytes; zero for padding blocks.
  *   mxq_act_exp_bytes(fmt, M) in total.
- *   The prefill GEMM reads the operand image; the decode GEMM,
- *   mxq_gemm_partials and mxq_unpack_act read the packed rows.
+ *   The GEMM reads the image; mxq_gemm_partials and mxq_unpack_act read the
+ *   packed rows.
  * Weights (mxq_pack_weights for N columns), mxq_weight_bytes(fmt, N):
- *   (1) packed slabs: columns in slabs of 16 (N rounded up; padding columns
- *   are zero), each slab holding its blocks grouped by four within each width
- *   segment, interleaved in matrix-core operand order (opaque: read it back
- *   with mxq_unpack_weights); 64 zero bytes follow;
+ *   (1) slabs of 16 columns (N rounded up; padding columns are zero) in
+ *   the stream layout of (3) above, line = column, but holding the packed
+ *   mantissas: per step 64 lanes of 16 / 12 / 16 bytes (4/6/8-bit), lane
+ *   (g, c) taking elements 16(g&1)..16(g&1)+15 of block 4s+(g>>1) then of
+ *   block 4s+2+(g>>1) (4-bit), or of block 2s+(g>>1) (6/8-bit, the 6-bit
+ *   codes as 8 nibble bytes at 8 l plus a 2-bit dword at 512 + 4 l); scale
+ *   bytes as in (3).  4-bit codes are sign-magnitude s|(|q|) under the
+ *   symmetric clamp and two's complement q mod 16 under the full clamp;
+ *   6-bit codes a nibble s|(|q| mod 8) and the 2-bit |q| div 8 (symmetric)
+ *   or q mod 16 and bits 4-5 (full); 8-bit codes two's-complement bytes.
+ *   Read it back with mxq_unpack_weights.  64 zero bytes follow;
  *   (2) the operand image, tiled by 128 columns (N rounded up; padding
  *   columns are zero): per tile, per step, 13312 bytes: lane data byte o of
  *   (column c of the tile, half h) at (o / 16) * 4096 + h * 2048 + c * 16
@@ -195,9 +220,9 @@ mxq_status mxq_pack_weights(const mxq_fmt *fmt, const uint16_t *w, int64_t N,
  *   w_mant/w_exp  DEVICE, from mxq_pack_weights with the same fmt and N.
  *   y             DEVICE float [M][ldy], ldy >= N; every y[i][j] with i < M,
  *                 j < N is written, nothing else.
- * M <= MXQ_DECODE_MAX_M runs the weight-streaming decode kernel (packed
- * weights, exact int32 block sums rescaled in fp32), larger M the tiled
- * prefill kernel (operand images on the block-scaled matrix cores).
+ * M <= MXQ_DECODE_MAX_M runs the weight-streaming decode kernel (the
+ * packed slabs turned into FP8 digits in registers, the decode image), larger
+ * M the tiled prefill kernel (both prefill images).
  */
 mxq_status mxq_gemm(const mxq_fmt *fmt, int64_t M, int64_t N,
                     const uint8_t *a_mant, const uint8_t *a_exp,
