@@ -16,21 +16,24 @@
 //   8-bit (1 block):  two FP8 instructions, [h|l].[h|l] and [h|l].[l|h].
 // The digit products are exact; only the fp32 accumulation rounds.
 //
-// Tiling: 256x128 outputs per workgroup of eight waves in two K groups.
-// Group g (waves 4g..4g+3) takes the steps s with s % 2 == g; within a group
-// wave r computes rows 64r..64r+63 x all 128 columns = 2x4 tiles of 32x32
-// with fp32 accumulators.  Two waves per SIMD (one of each group) keep the
-// matrix core busy while the other waits on memory or LDS; at the end the
-// groups' partial sums meet in LDS (fixed order: even steps + odd steps).
-//   - A: each lane loads its rows' 48-byte step data straight from the
-//     activation operand image (32-row tiles: every load of the wave reads
-//     one contiguous kilobyte) into registers, one own step ahead.
-//   - W: each group loads its next step's 13 KB chunk of the weight operand
-//     image (already in the LDS layout) into registers, stores it to LDS one
-//     iteration later (double buffer per group), and its lanes read it with
-//     16-byte reads.
-// Workgroup ids are remapped so that each XCD works on a contiguous range of
-// column tiles: its share of the weights stays in its L2.
+// Tiling: 256x128 outputs per workgroup of eight waves, two per SIMD; wave
+// (r, c) owns rows 64r..64r+63 x columns 64c..64c+63 = 2x2 tiles of 32x32
+// fp32 accumulators and runs every K step.
+//
+// Data path: each step's operands -- the eight 32-row activation blocks,
+// their scale blocks and the weight chunk, already in the layout the lanes
+// read -- are copied global -> LDS by the buffer unit's direct-to-LDS loads
+// (no registers), five 1 KB loads per wave and step, into a ring of four LDS
+// stages.  Loads run four steps ahead of the products and the operands of a
+// step are read from LDS into registers one step ahead, so neither latency
+// meets a matrix instruction.  A step waits for the wave's loads of the next
+// stage and its reads of the current one, meets the other waves at a
+// barrier (after which the next stage is complete and the current one is
+// free), then spreads the loads of step + 4 into the freed stage and the
+// reads of step + 1 between its products.  Two waves per SIMD keep the
+// matrix core busy while one of them waits at the barrier.
+// Workgroup ids are remapped so that each XCD owns a compact block of output
+// tiles: the activation rows and weight columns it reads stay in its L2.
 #include "mxq_device.h"
 #include "mxq_internal.h"
 
@@ -40,50 +43,98 @@ namespace {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
+typedef float v4f __attribute__((ext_vector_type(4)));
 typedef unsigned u4 __attribute__((ext_vector_type(4)));
-typedef unsigned u12 __attribute__((ext_vector_type(12)));   // one lane's 48 bytes
+typedef unsigned u2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int BM = 256, BN = kOpCols, NT = 512;
-constexpr int kChunkVec = kOpChunk / 16;     // 16-byte pieces per chunk (832)
 constexpr int kFmtFp8 = 0, kFmtFp6 = 3;      // e4m3, e3m2
-constexpr int kSmemVec = BM * BN * 4 / 16;   // 128 KB: the end reduction (W buffers alias it)
+constexpr int kStages = 4;                   // LDS ring; loads run kStages - 1 steps ahead
+// One stage: the eight activation tile blocks (3 KB each), their 256-byte
+// scale blocks, then the 13 KB weight chunk.
+constexpr int kStA = 0;
+constexpr int kStAScale = kStA + 8 * kActStep;              // 24576
+constexpr int kStW = kStAScale + 8 * kActScaleStep;         // 26624
+constexpr int kStage = kStW + kOpChunk;                     // 39936
+static_assert(kStage % 16 == 0 && kStages * kStage <= 160 * 1024, "LDS ring");
+// A step's 39 loads of 1 KB (24 activation, 2 activation scale, 13 weight),
+// plus one repeat of the last, as five per wave.
+constexpr int kDmaPerStep = 5;
 
-template <int S> struct Seg { static constexpr int v = S; };
+template <int S> struct Int { static constexpr int v = S; };
 
-__device__ inline u12 cat3(u4 a, u4 b, u4 c) {
-  return __builtin_shufflevector(__builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7),
-                                 __builtin_shufflevector(c, c, 0, 1, 2, 3, -1, -1, -1, -1),
-                                 0, 1, 2, 3, 4, 5, 6, 7, 8, 9, 10, 11);
+// A lane's 48 bytes of one step, read from its four planes (lane_plane_loc):
+// bytes 0-15 (lo), 16-23 (m0), 24-31 (m1), 32-47 (hi).  Every instruction
+// operand is made of whole pieces -- FP6 (lo, m0) and (m1, hi), FP8 (lo, m0,
+// m1) -- so the reads land in the operand registers.  The weights' second FP8
+// operand (m0, m1, hi) reads its middle again into m0b, m1b.
+struct Lane48 {
+  u4 lo;
+  u2 m0, m1;
+  u4 hi;
+  u2 m0b, m1b;
+};
+__device__ inline u4 wide(u2 a) { return __builtin_shufflevector(a, a, 0, 1, -1, -1); }
+__device__ inline u4 cat2(u2 a, u2 b) { return __builtin_shufflevector(a, b, 0, 1, 2, 3); }
+__device__ inline v8i fp6_lo(const Lane48 &x) {
+  return (v8i)__builtin_shufflevector(x.lo, wide(x.m0), 0, 1, 2, 3, 4, 5, -1, -1);
 }
-// Operand registers of one instruction out of a lane's 48 bytes:
-// bytes 0-23 / 24-47 (FP6), 0-31 / 16-47 (FP8).
-__device__ inline v8i fp6_lo(u12 x) { return (v8i)__builtin_shufflevector(x, x, 0, 1, 2, 3, 4, 5, -1, -1); }
-__device__ inline v8i fp6_hi(u12 x) { return (v8i)__builtin_shufflevector(x, x, 6, 7, 8, 9, 10, 11, -1, -1); }
-__device__ inline v8i fp8_lo(u12 x) { return (v8i)__builtin_shufflevector(x, x, 0, 1, 2, 3, 4, 5, 6, 7); }
-__device__ inline v8i fp8_hi(u12 x) { return (v8i)__builtin_shufflevector(x, x, 4, 5, 6, 7, 8, 9, 10, 11); }
+__device__ inline v8i fp6_hi(const Lane48 &x) {
+  return (v8i)__builtin_shufflevector(wide(x.m1), x.hi, 0, 1, 4, 5, 6, 7, -1, -1);
+}
+__device__ inline v8i fp8_lo(const Lane48 &x) {
+  return (v8i)__builtin_shufflevector(x.lo, cat2(x.m0, x.m1), 0, 1, 2, 3, 4, 5, 6, 7);
+}
+__device__ inline v8i fp8_hi(const Lane48 &x) {
+  return (v8i)__builtin_shufflevector(cat2(x.m0b, x.m1b), x.hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
 
 template <int FA, int SA, int SB>
 __device__ inline v16f mma(const v8i &a, const v8i &b, v16f c, int sa, int sb) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, FA, FA, SA, sa, SB, sb);
 }
 
-__global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mtiles,
-                                                             int ntiles) {
-  __shared__ __attribute__((aligned(16))) u4 smem[kSmemVec];
-  // W chunks during the K loop: [buffer][group][chunk]
-  u4 (*Wl)[2][kChunkVec] = (u4 (*)[2][kChunkVec])smem;
+// The LDS ring's synchronisation is explicit: the compiler neither knows
+// which direct-to-LDS load fills which stage nor may move LDS reads across
+// these points.
+template <int N>
+__device__ inline void wait_loads() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// ... and also until this wave's LDS reads have completed.
+template <int N>
+__device__ inline void wait_loads_lds() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(N) : "memory");
+}
+__device__ inline void barrier() { asm volatile("s_barrier" ::: "memory"); }
+// An address the compiler cannot relate to others: keeps the two 8-byte plane
+// reads of an operand from being fused into one read of both planes (which
+// would need register copies to split).
+__device__ inline int opaque(int v) {
+  asm("" : "+v"(v));
+  return v;
+}
+
+__global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles,
+                                                             int gm, int gn) {
+  __shared__ __attribute__((aligned(16))) u4 lds[kStages * kStage / 16];
 
   const int t = threadIdx.x, lane = t & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);     // wave-uniform
-  const int kg = wave >> 2, rw = wave & 3, tg = t & 255;   // K group, row block, thread in group
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);      // wave-uniform
   const int l32 = lane & 31, lh = lane >> 5;
   int mt, nt;
   {
+    // XCD x (workgroups pid % 8 == x) owns a block of (mtiles / gm) x
+    // (ntiles / gn) tiles, walked row by row.
     const int pid = blockIdx.x;
-    if ((ntiles & 7) == 0) {               // XCD x: column tiles [x*nx, (x+1)*nx)
-      const int nx = ntiles >> 3, x = pid & 7, loc = pid >> 3;
-      nt = x * nx + loc % nx;
-      mt = loc / nx;
+    if (gm > 0) {
+      const int x = pid & 7, loc = pid >> 3;
+      const int bm = mtiles / gm, bn = ntiles / gn;
+      mt = (x / gn) * bm + loc / bn;
+      nt = (x % gn) * bn + loc % bn;
     } else {
       mt = pid / ntiles;
       nt = pid - mt * ntiles;
@@ -92,182 +143,251 @@ __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mti
   const int64_t row0 = (int64_t)mt * BM, col0 = (int64_t)nt * BN;
   const OpGeo og(g.n4, g.n6, g.n8);
   const int nsteps = og.nsteps;
-  const int niter = (nsteps + 1) >> 1;     // iterations; group 1's last may be empty
 
-  // This wave's two 32-row tiles of the activation operand image (tiles past
-  // the last one read the last tile; those rows are never stored).  Lane
-  // (h, r) reads its 16-byte pieces at part * 1024 + h * 512 + r * 16.
-  const int64_t last = (g.M - 1) / kActRows;
-  const int64_t ta = min((row0 + rw * 64) / kActRows, last);
-  const int64_t tb = min((row0 + rw * 64) / kActRows + 1, last);
-  const uint8_t *aop0 = g.a_mant + g.a_op + ta * nsteps * kActStep + lh * 512 + l32 * 16;
-  const uint8_t *aop1 = g.a_mant + g.a_op + tb * nsteps * kActStep + lh * 512 + l32 * 16;
-  const uint8_t *asc0 = g.a_exp + g.a_sc + ta * nsteps * kActScaleStep + lh * 128 + l32 * 4;
-  const uint8_t *asc1 = g.a_exp + g.a_sc + tb * nsteps * kActScaleStep + lh * 128 + l32 * 4;
-  const uint8_t *wtile = g.w_mant + g.w_op + (int64_t)nt * g.w_tile;
+  // Wave (r, c): row block r (two 32-row tiles), column half c.
+  const int wr = wave >> 1, wc = wave & 1;
+  // The workgroup's eight 32-row tiles of the activation operand image
+  // (tiles past the last one load the last tile; those rows are never
+  // stored).
+  const int last = (int)((g.M - 1) / kActRows);
+  const int tile0 = (int)(row0 / kActRows);
+  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)(g.a_mant + g.a_op), 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)(g.a_exp + g.a_sc), 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)(g.w_mant + g.w_op + (int64_t)nt * g.w_tile), 0, 0x7fffffff, 0x00020000);
+  const int v16 = lane * 16;
+  char *const ring = (char *)lds;
+  auto tile_of = [&](int t) { return min(tile0 + t, last); };
+  // Scale gathers: lane l reads bytes (l % 16) * 16 .. +15 of the scale block
+  // of tile 4 h + l / 16 (h = 0, 1), whose step st block starts at
+  // (tile * nsteps + st) * 256; the per-lane part of that offset is fixed.
+  int vsc[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+    vsc[h] = tile_of(4 * h + (lane >> 4)) * nsteps * kActScaleStep + (lane & 15) * 16;
 
-  v16f acc[2][4];
+  // The step's loads are numbered 0..39: 0..23 activation tile n / 3,
+  // kilobyte n % 3; 24, 25 the scale blocks of tiles 4 (n - 24) .. +3;
+  // 26..38 weight kilobyte n - 26 (the last one the scale dwords); 39 repeats
+  // 38.  Wave w issues loads w + 8 j, j = 0..4; their descriptors are fixed
+  // but for the step offset (soff + st * sstep).
+  struct Load {
+    __amdgpu_buffer_rsrc_t rsrc;
+    int lds, voff, soff, sstep;
+  } ld[kDmaPerStep];
+#pragma unroll
+  for (int j = 0; j < kDmaPerStep; ++j) {
+    const int n = wave + 8 * j;
+    if (n < 24) {
+      const int t = n / 3, kb = n % 3;
+      ld[j] = {ra, kStA + t * kActStep + kb * 1024, v16, tile_of(t) * nsteps * kActStep + kb * 1024,
+               kActStep};
+    } else if (n < 26) {
+      const int h = n - 24;
+      ld[j] = {rs, kStAScale + 4 * h * kActScaleStep, vsc[h], 0, kActScaleStep};
+    } else {
+      const int kb = min(n - 26, 12);
+      ld[j] = {rw, kStW + kb * 1024, v16, kb * 1024, kOpChunk};
+    }
+  }
+  // This wave's load j (0..4) of step st into stage q.
+  auto issue = [&](int st, int q, int j) __attribute__((always_inline)) {
+    st = min(st, nsteps - 1);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(ld[j].rsrc, (lds_void *)(ring + q * kStage + ld[j].lds),
+                                             16, ld[j].voff, ld[j].soff + st * ld[j].sstep, 0, 0);
+  };
+
+  v16f acc[2][2];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int n = 0; n < 4; ++n) acc[a][n] = v16f{};
+    for (int n = 0; n < 2; ++n) acc[a][n] = v16f{};
 
-  // Per wave: W staging (one chunk piece set), A lane data and scales in a
-  // ring of two, indexed by the iteration's position relative to the start
-  // of the current segment.
-  u4 ws[4];
-  u12 xa[2][2];
-  uint32_t xs[2][2];
+  // All operands of one step in registers: the wave's two activation tiles
+  // and the four weight column tiles.
+  struct Ops {
+    Lane48 x[2], w[2];
+    uint32_t sa[2], sw[2];
+  } ops[2];
 
-  // The group's own step of iteration i (clamped: past the end it refetches
-  // the last step, which is not multiplied).
-  auto own = [&](int i) __attribute__((always_inline)) { return min(2 * i + kg, nsteps - 1); };
-  auto load_w = [&](int st) __attribute__((always_inline)) {
-    const u4 *src = (const u4 *)(wtile + (int64_t)st * kOpChunk);
+  // Read the operands of step st (stage st % 4) into ops[O]: the activation
+  // tiles, and weight column tile tn.
+  auto read_x = [&](auto o_tag, int st) __attribute__((always_inline)) {
+    constexpr int O = decltype(o_tag)::v;
+    const char *stage = ring + (st & 3) * kStage;
+    Ops &d = ops[O];
 #pragma unroll
-    for (int j = 0; j < 3; ++j) ws[j] = src[j * 256 + tg];
-    if (tg < 64) ws[3] = src[768 + tg];
+    for (int tm = 0; tm < 2; ++tm) {
+      const char *blk = stage + kStA + (wr * 2 + tm) * kActStep;     // 64 lanes
+      d.x[tm].lo = ((const u4 *)blk)[lane];
+      d.x[tm].m0 = ((const u2 *)(blk + 1024))[lane];
+      d.x[tm].m1 = ((const u2 *)(blk + opaque(1536)))[lane];
+      d.x[tm].hi = ((const u4 *)(blk + 2048))[lane];
+      d.sa[tm] = ((const uint32_t *)(stage + kStAScale))[(wr * 2 + tm) * 64 + lane];
+    }
   };
-  auto store_w = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int j = 0; j < 3; ++j) Wl[buf][kg][j * 256 + tg] = ws[j];
-    if (tg < 64) Wl[buf][kg][768 + tg] = ws[3];
+  auto read_w = [&](auto o_tag, int st, int tn) __attribute__((always_inline)) {
+    constexpr int O = decltype(o_tag)::v;
+    const char *W = ring + (st & 3) * kStage + kStW;                  // 256 lanes
+    Ops &d = ops[O];
+    const int L = lh * 128 + wc * 64 + tn * 32 + l32;
+    d.w[tn].lo = ((const u4 *)W)[L];
+    d.w[tn].m0 = ((const u2 *)(W + 4096))[L];
+    d.w[tn].m1 = ((const u2 *)(W + opaque(6144)))[L];
+    d.w[tn].hi = ((const u4 *)(W + 8192))[L];
+    d.w[tn].m0b = ((const u2 *)(W + opaque(4096)))[L];
+    d.w[tn].m1b = ((const u2 *)(W + opaque(6144)))[L];
+    d.sw[tn] = ((const uint32_t *)(W + 3 * kOpPart))[L];
   };
-  auto load_a = [&](int st, u12 (&x)[2], uint32_t (&s)[2]) __attribute__((always_inline)) {
-    const u4 *p0 = (const u4 *)(aop0 + (int64_t)st * kActStep);
-    const u4 *p1 = (const u4 *)(aop1 + (int64_t)st * kActStep);
-    x[0] = cat3(p0[0], p0[64], p0[128]);
-    x[1] = cat3(p1[0], p1[64], p1[128]);
-    s[0] = *(const uint32_t *)(asc0 + (int64_t)st * kActScaleStep);
-    s[1] = *(const uint32_t *)(asc1 + (int64_t)st * kActScaleStep);
-  };
-  // One column tile of the step's instructions (both row tiles).
-  auto mul_tile = [&](auto seg, const u12 (&x)[2], const uint32_t (&s)[2], u12 w, int sw,
-                      int tn) __attribute__((always_inline)) {
-    constexpr int SEG = decltype(seg)::v;
+  // The products of column tile tn (both row tiles) of one step from ops[O].
+  auto mul_tile = [&](auto seg, auto o_tag, int tn) __attribute__((always_inline)) {
+    constexpr int SEG = decltype(seg)::v, O = decltype(o_tag)::v;
     constexpr int NK = SEG == 1 ? 4 : 2;
+    const Ops &d = ops[O];
 #pragma unroll
     for (int k = 0; k < NK; ++k)
 #pragma unroll
       for (int tm = 0; tm < 2; ++tm) {
-        const int sa = (int)s[tm];
         v16f &c = acc[tm][tn];
+        const Lane48 &x = d.x[tm], &w = d.w[tn];
+        const int as = (int)d.sa[tm], ws = (int)d.sw[tn];
         if (SEG == 0) {          // block pairs (4s', 4s'+1), (4s'+2, 4s'+3): scale bytes 0, 1
-          if (k == 0) c = mma<kFmtFp6, 0, 0>(fp6_lo(x[tm]), fp6_lo(w), c, sa, sw);
-          else c = mma<kFmtFp6, 1, 1>(fp6_hi(x[tm]), fp6_hi(w), c, sa, sw);
+          if (k == 0) c = mma<kFmtFp6, 0, 0>(fp6_lo(x), fp6_lo(w), c, as, ws);
+          else c = mma<kFmtFp6, 1, 1>(fp6_hi(x), fp6_hi(w), c, as, ws);
         } else if (SEG == 1) {   // digit products hh, ll, hl, lh
-          const v8i av = (k == 0 || k == 2) ? fp6_lo(x[tm]) : fp6_hi(x[tm]);
+          const v8i av = (k == 0 || k == 2) ? fp6_lo(x) : fp6_hi(x);
           const v8i wv = (k == 0 || k == 3) ? fp6_lo(w) : fp6_hi(w);
-          c = mma<kFmtFp6, 0, 0>(av, wv, c, sa, sw);
+          c = mma<kFmtFp6, 0, 0>(av, wv, c, as, ws);
         } else {                 // [h|l].[h|l], [h|l].[l|h]
-          c = mma<kFmtFp8, 0, 0>(fp8_lo(x[tm]), k == 0 ? fp8_lo(w) : fp8_hi(w), c, sa, sw);
+          c = mma<kFmtFp8, 0, 0>(fp8_lo(x), k == 0 ? fp8_lo(w) : fp8_hi(w), c, as, ws);
         }
       }
   };
-  auto compute = [&](auto seg, const u12 (&x)[2], const uint32_t (&s)[2], int buf)
-      __attribute__((always_inline)) {
-    const u4 *W = Wl[buf][kg];
-    const uint32_t *scl = (const uint32_t *)&W[768];
+
+  // Step s multiplies from ops[O] (read during step s - 1).  Before that, the
+  // wave waits until its loads of stage s + 1 have landed and its reads of
+  // stage s (into ops[O]) have completed; after the barrier every wave is in
+  // that state, so stage s + 1 is complete and stage s is free.  Then, between
+  // the products, it issues the loads of step s + 4 into stage s % 4 and reads
+  // the operands of step s + 1 into ops[1 - O].
+  auto step = [&](auto seg, auto o_tag, int s) __attribute__((always_inline)) {
+    constexpr int O = decltype(o_tag)::v;
+    constexpr Int<1 - O> nx{};
+    const int sn = min(s + 1, nsteps - 1);
+    wait_loads_lds<2 * kDmaPerStep>();
+    barrier();
+    // Chunks in a fixed order (the scheduler may interleave within a chunk
+    // only): the products of column tile 0 with three of the loads of step
+    // s + 4 and the activation reads of step s + 1, then those of column tile
+    // 1 with the other two loads and the weight reads.
+    issue(s + 4, s & 3, 0);
+    issue(s + 4, s & 3, 1);
+    issue(s + 4, s & 3, 2);
+    read_x(nx, sn);
+    mul_tile(seg, o_tag, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    issue(s + 4, s & 3, 3);
+    issue(s + 4, s & 3, 4);
+    read_w(nx, sn, 0);
+    read_w(nx, sn, 1);
+    mul_tile(seg, o_tag, 1);
+  };
+  // The steps [b, e) of one segment, in pairs so that the operand sets
+  // alternate statically; after the last step the next step's operands are
+  // in ops[0].
+  auto run = [&](auto seg, int b, int e) __attribute__((always_inline)) {
+    int s = b;
+    for (; s + 2 <= e; s += 2) {
+      step(seg, Int<0>{}, s);
+      step(seg, Int<1>{}, s + 1);
+    }
+    if (s < e) {
+      step(seg, Int<0>{}, s);
+      ops[0] = ops[1];
+    }
+  };
+
+  // Prologue: the loads of steps 0..3, then the operands of step 0.
 #pragma unroll
-    for (int tn = 0; tn < 4; ++tn) {
-      const int c = tn * 32 + l32;
-      const u12 w = cat3(W[lh * 128 + c], W[256 + lh * 128 + c], W[512 + lh * 128 + c]);
-      mul_tile(seg, x, s, w, (int)scl[lh * 128 + c], tn);
-      // one column tile's operands live at a time (the other wave on the
-      // SIMD covers the LDS latency)
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  };
-
-  // Iteration i: the group's chunk of step own(i) is in Wl[i & 1][kg] and
-  // its A data in xc; stage the chunk of own(i+1) into Wl[(i+1) & 1][kg],
-  // fetch the chunk of own(i+2) and the A data of own(i+1); multiply own(i)
-  // unless it lies past the last step.  Group 0 fetches first and group 1
-  // multiplies first, so that after each barrier one group streams memory
-  // while the other keeps the matrix cores busy.
-  auto iteration = [&](auto seg, int i, const u12 (&xc)[2], const uint32_t (&sc)[2],
-                       u12 (&xn)[2], uint32_t (&sn)[2]) __attribute__((always_inline)) {
-    __syncthreads();
-    const bool mul = 2 * i + kg < nsteps;
-    if (kg == 1 && mul) compute(seg, xc, sc, i & 1);
-    store_w((i + 1) & 1);
-    load_w(own(i + 2));
-    load_a(own(i + 1), xn, sn);
-    if (kg == 0 && mul) compute(seg, xc, sc, i & 1);
-  };
-  // Iterations [ib, ie) whose own steps lie in one segment; ring slots
-  // relative to ib.
-  auto run = [&](auto seg, int ib, int ie) __attribute__((always_inline)) {
-    for (int i = ib; i < ie; i += 2) {
-      iteration(seg, i, xa[0], xs[0], xa[1], xs[1]);
-      if (i + 1 < ie) iteration(seg, i + 1, xa[1], xs[1], xa[0], xs[0]);
-    }
-  };
-  // After n iterations the next iteration's A data sits in slot n % 2.
-  auto realign = [&](int n) __attribute__((always_inline)) {
-    if (n & 1) {
+  for (int st = 0; st < 4; ++st)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const u12 tx = xa[0][j];
-        xa[0][j] = xa[1][j];
-        xa[1][j] = tx;
-        const uint32_t tsc = xs[0][j];
-        xs[0][j] = xs[1][j];
-        xs[1][j] = tsc;
-      }
-    }
-  };
+    for (int j = 0; j < kDmaPerStep; ++j) issue(st, st, j);
+  wait_loads_lds<3 * kDmaPerStep>();
+  barrier();
+  read_x(Int<0>{}, 0);
+#pragma unroll
+  for (int tn = 0; tn < 2; ++tn) read_w(Int<0>{}, 0, tn);
 
-  // Prologue: the group's chunk of own(0) in LDS, own(1)'s in the staging
-  // registers, A of own(0).
-  load_w(own(0));
-  load_a(own(0), xa[0], xs[0]);
-  store_w(0);
-  load_w(own(1));
-
-  // Iteration ranges of the group's own steps per segment: own step 2i+kg
-  // is in segment 0 while 2i+kg < e4, and so on.
   const int e4 = og.s4, e6 = og.s4 + og.s6;
-  const int i4 = (e4 - kg + 1) / 2, i6 = max(i4, (e6 - kg + 1) / 2);
-  run(Seg<0>{}, 0, i4);
-  realign(i4);
-  run(Seg<1>{}, i4, i6);
-  realign(i6 - i4);
-  run(Seg<2>{}, i6, niter);
+  run(Int<0>{}, 0, e4);
+  run(Int<1>{}, e4, e6);
+  run(Int<2>{}, e6, nsteps);
+  // The last steps' loads (of clamped steps) must land before the workgroup
+  // releases its LDS.
+  wait_loads<0>();
 
-  // Sum the two groups: group g finishes row tile tm = g of its row block;
-  // each wave hands its other row tile to the partner wave through LDS.
-  __syncthreads();
-  float *red = (float *)smem;              // [row block][tm][tn][r][lane]
-  auto finish = [&](auto mine_tag) __attribute__((always_inline)) {
-    constexpr int MINE = decltype(mine_tag)::v, OTHER = 1 - MINE;
+  // Epilogue through LDS: each wave writes its 64 x 64 tile row-major (row
+  // pitch 72 floats: the two row groups one instruction writes fall in
+  // disjoint banks) and reads it back as 16-byte row pieces, so the stores
+  // are 16 bytes per lane -- a quarter of the store instructions, which the
+  // address unit issues at a fixed rate per instruction.
+  constexpr int kPitch = 72;
+  static_assert(8 * 64 * kPitch * 4 <= kStages * kStage, "epilogue tile");
+  barrier();                                 // every wave is done with the ring
+  float *tile = (float *)ring + wave * 64 * kPitch;
 #pragma unroll
-    for (int tn = 0; tn < 4; ++tn)
+  for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < 2; ++tn)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
-        red[(((rw * 2 + OTHER) * 4 + tn) * 16 + r) * 64 + lane] = acc[OTHER][tn][r];
-    __syncthreads();
+        tile[(tm * 32 + 8 * (r >> 2) + 4 * lh + (r & 3)) * kPitch + tn * 32 + l32] = acc[tm][tn][r];
+  // only this wave reads its tile back
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  const int q = lane & 15, rq = lane >> 4;   // 4 columns 4q.., row 4 i + rq
+  const int64_t jc = col0 + wc * 64 + 4 * q;
+  // 16-byte stores when the wave's 64 columns are all inside Y and aligned
+  const bool vec = (g.ldy & 3) == 0 && ((uintptr_t)g.y & 15) == 0 &&
+                   col0 + wc * 64 + 64 <= g.N;
+  if (vec) {
 #pragma unroll
-    for (int tn = 0; tn < 4; ++tn) {
-      const int64_t j = col0 + tn * 32 + l32;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float v = acc[MINE][tn][r] + red[(((rw * 2 + MINE) * 4 + tn) * 16 + r) * 64 + lane];
-        const int64_t i = row0 + rw * 64 + MINE * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-        if (i < g.M && j < g.N) g.y[i * g.ldy + j] = v;
-      }
+    for (int i = 0; i < 16; ++i) {
+      const int rr = 4 * i + rq;
+      const int64_t row = row0 + wr * 64 + rr;
+      const v4f v = *(const v4f *)&tile[rr * kPitch + 4 * q];
+      if (row < g.M) __builtin_nontemporal_store(v, (v4f *)(g.y + row * g.ldy + jc));
     }
-  };
-  if (kg == 0) finish(Seg<0>{});
-  else finish(Seg<1>{});
+  } else {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int rr = 4 * i + rq;
+      const int64_t row = row0 + wr * 64 + rr;
+      if (row >= g.M) continue;
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (jc + c < g.N) g.y[row * g.ldy + jc + c] = tile[rr * kPitch + 4 * q + c];
+    }
+  }
 }
 
 }  // namespace
 
 hipError_t launch_gemm_prefill(const GemmArgs &a, hipStream_t stream) {
   const int mtiles = (int)((a.M + BM - 1) / BM), ntiles = (int)((a.N + BN - 1) / BN);
+  // Split the tile grid into 8 blocks (one per XCD) along rows x columns,
+  // minimising the bytes each XCD reads: an activation tile (256 rows) weighs
+  // twice a weight tile (128 columns).
+  int gm = 0, gn = 0, best = 0;
+  for (int m = 1; m <= 8; m *= 2) {
+    const int n = 8 / m;
+    if (mtiles % m || ntiles % n) continue;
+    const int cost = 2 * (mtiles / m) + ntiles / n;
+    if (gm == 0 || cost < best) gm = m, gn = n, best = cost;
+  }
   hipLaunchKernelGGL(gemm_prefill_kernel, dim3((unsigned)(mtiles * ntiles)), dim3(NT), 0,
-                     stream, a, mtiles, ntiles);
+                     stream, a, mtiles, ntiles, gm, gn);
   return hipGetLastError();
 }
 
