@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define MXQ_ABI_VERSION 5
+#define MXQ_ABI_VERSION 6
 #define MXQ_BLOCK 32
 /* mxq_gemm uses the weight-streaming decode kernel for M <= this. */
 #define MXQ_DECODE_MAX_M 16
@@ -132,13 +132,9 @@ const char *mxq_status_str(int status);
  *     8-bit step: the h codes of elements 16h..16h+15 (16 bytes), their l
  *       codes (16 bytes), 16 zero bytes.
  *   Rows are grouped in tiles of 32 (the last tile is padded; its rows past
- *   M are unspecified).  A (tile, step) block of 3072 bytes holds its 64
- *   lanes l = 32 h + r % 32 in four planes, so that every instruction
- *   operand (bytes 0-23 or 24-47 of FP6 lane data, 0-31 of FP8) is made of
- *   whole plane pieces: byte o of the lane data of (row r, step s, half h)
- *   is at ((r / 32) * nsteps + s) * 3072 + P(64, l, o), where
- *   P(L, l, o) = 16 l + o for o < 16, 16 L + 8 l + (o - 16) for o < 24,
- *   24 L + 8 l + (o - 24) for o < 32, 32 L + 16 l + (o - 32) otherwise.
+ *   M are unspecified).  Byte o of the lane data of (row r, step s, half h)
+ *   is at ((r / 32) * nsteps + s) * 3072 + (o / 16) * 1024 + h * 512
+ *   + (r % 32) * 16 + o % 16 of the operand image.
  *   (3) Decode image (M <= 16), the "stream layout" of 16 lines (line =
  *   row; rows past M are unspecified) in the lane order of the block-scaled
  *   16x16x128 matrix-core instruction, lane l = 16 g + line.  Steps: the
@@ -179,10 +175,10 @@ const char *mxq_status_str(int status);
  *   Read it back with mxq_unpack_weights.  64 zero bytes follow;
  *   (2) the operand image, tiled by 128 columns (N rounded up; padding
  *   columns are zero): per tile, per step, 13312 bytes: lane data byte o of
- *   (column c of the tile, half h) at P(256, 128 h + c, o) (P as for the
- *   activations), then the lane's scale bytes (the two of the activation
- *   layout, then two zero bytes) at 12288 + h * 512 + c * 4.  Weight lane
- *   data of an 8-bit step repeats the h codes in its last 16 bytes.
+ *   (column c of the tile, half h) at (o / 16) * 4096 + h * 2048 + c * 16
+ *   + o % 16, then the lane's scale bytes (the two of the activation layout,
+ *   then two zero bytes) at 12288 + h * 512 + c * 4.  Weight lane data of an
+ *   8-bit step repeats the h codes in its last 16 bytes.
  *   The weight exponents are one row of mxq_exp_row_bytes(fmt) bytes per
  *   (padded to 16) column: w_exp[j * mxq_exp_row_bytes + b].
  */

@@ -64,30 +64,25 @@ constexpr int kDmaPerStep = 5;
 
 template <int S> struct Int { static constexpr int v = S; };
 
-// A lane's 48 bytes of one step, read from its four planes (lane_plane_loc):
-// bytes 0-15 (lo), 16-23 (m0), 24-31 (m1), 32-47 (hi).  Every instruction
-// operand is made of whole pieces -- FP6 (lo, m0) and (m1, hi), FP8 (lo, m0,
-// m1) -- so the reads land in the operand registers.  The weights' second FP8
-// operand (m0, m1, hi) reads its middle again into m0b, m1b.
+// A lane's 48 bytes of one step, as three 16-byte pieces (one LDS read
+// each).  FP6 operands are bytes 0-23 and 24-47 and FP8 operands 0-31 and
+// 16-47, so the middle piece is split or shared; the register copies that
+// needs are cheaper than more, narrower LDS reads, which cost the same per
+// instruction.
 struct Lane48 {
-  u4 lo;
-  u2 m0, m1;
-  u4 hi;
-  u2 m0b, m1b;
+  u4 p[3];
 };
-__device__ inline u4 wide(u2 a) { return __builtin_shufflevector(a, a, 0, 1, -1, -1); }
-__device__ inline u4 cat2(u2 a, u2 b) { return __builtin_shufflevector(a, b, 0, 1, 2, 3); }
 __device__ inline v8i fp6_lo(const Lane48 &x) {
-  return (v8i)__builtin_shufflevector(x.lo, wide(x.m0), 0, 1, 2, 3, 4, 5, -1, -1);
+  return (v8i)__builtin_shufflevector(x.p[0], x.p[1], 0, 1, 2, 3, 4, 5, -1, -1);
 }
 __device__ inline v8i fp6_hi(const Lane48 &x) {
-  return (v8i)__builtin_shufflevector(wide(x.m1), x.hi, 0, 1, 4, 5, 6, 7, -1, -1);
+  return (v8i)__builtin_shufflevector(x.p[1], x.p[2], 2, 3, 4, 5, 6, 7, -1, -1);
 }
 __device__ inline v8i fp8_lo(const Lane48 &x) {
-  return (v8i)__builtin_shufflevector(x.lo, cat2(x.m0, x.m1), 0, 1, 2, 3, 4, 5, 6, 7);
+  return (v8i)__builtin_shufflevector(x.p[0], x.p[1], 0, 1, 2, 3, 4, 5, 6, 7);
 }
 __device__ inline v8i fp8_hi(const Lane48 &x) {
-  return (v8i)__builtin_shufflevector(cat2(x.m0b, x.m1b), x.hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return (v8i)__builtin_shufflevector(x.p[1], x.p[2], 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 template <int FA, int SA, int SB>
@@ -110,13 +105,6 @@ __device__ inline void wait_loads_lds() {
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(N) : "memory");
 }
 __device__ inline void barrier() { asm volatile("s_barrier" ::: "memory"); }
-// An address the compiler cannot relate to others: keeps the two 8-byte plane
-// reads of an operand from being fused into one read of both planes (which
-// would need register copies to split).
-__device__ inline int opaque(int v) {
-  asm("" : "+v"(v));
-  return v;
-}
 
 __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles,
                                                              int gm, int gn) {
@@ -220,11 +208,9 @@ __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mti
     Ops &d = ops[O];
 #pragma unroll
     for (int tm = 0; tm < 2; ++tm) {
-      const char *blk = stage + kStA + (wr * 2 + tm) * kActStep;     // 64 lanes
-      d.x[tm].lo = ((const u4 *)blk)[lane];
-      d.x[tm].m0 = ((const u2 *)(blk + 1024))[lane];
-      d.x[tm].m1 = ((const u2 *)(blk + opaque(1536)))[lane];
-      d.x[tm].hi = ((const u4 *)(blk + 2048))[lane];
+      const u4 *blk = (const u4 *)(stage + kStA + (wr * 2 + tm) * kActStep);   // 64 lanes
+#pragma unroll
+      for (int j = 0; j < 3; ++j) d.x[tm].p[j] = blk[j * 64 + lane];
       d.sa[tm] = ((const uint32_t *)(stage + kStAScale))[(wr * 2 + tm) * 64 + lane];
     }
   };
@@ -233,12 +219,8 @@ __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mti
     const char *W = ring + (st & 3) * kStage + kStW;                  // 256 lanes
     Ops &d = ops[O];
     const int L = lh * 128 + wc * 64 + tn * 32 + l32;
-    d.w[tn].lo = ((const u4 *)W)[L];
-    d.w[tn].m0 = ((const u2 *)(W + 4096))[L];
-    d.w[tn].m1 = ((const u2 *)(W + opaque(6144)))[L];
-    d.w[tn].hi = ((const u4 *)(W + 8192))[L];
-    d.w[tn].m0b = ((const u2 *)(W + opaque(4096)))[L];
-    d.w[tn].m1b = ((const u2 *)(W + opaque(6144)))[L];
+#pragma unroll
+    for (int j = 0; j < 3; ++j) d.w[tn].p[j] = ((const u4 *)W)[j * 256 + L];
     d.sw[tn] = ((const uint32_t *)(W + 3 * kOpPart))[L];
   };
   // The products of column tile tn (both row tiles) of one step from ops[O].

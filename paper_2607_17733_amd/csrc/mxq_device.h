@@ -317,31 +317,18 @@ struct OpGeo {
 // Weight operand image: 128-column tiles, each a run of per-step chunks of
 // kOpChunk bytes; a chunk holds three 16-byte parts of every (half, column)
 // lane and the lane's scale dword (byte 0: first scale, byte 1: second scale
-// of a 4-bit step), laid out as the prefill GEMM keeps it in LDS: lane
-// 128 h + c in the four planes of lane_plane_loc (4096 + 2048 + 2048 + 4096
-// bytes), scales at 12288 + h * 512 + c * 4.
+// of a 4-bit step), laid out as the prefill GEMM keeps it in LDS:
+//   part j at j * 4096 + h * 2048 + c * 16, scales at 12288 + h * 512 + c * 4.
 constexpr int kOpCols = 128;
 constexpr int kActRows = 32;
 constexpr int kActStep = 3072;       // operand bytes per (32-row tile, step)
 constexpr int kActScaleStep = 256;   // scale bytes per (32-row tile, step)
 
-// Lane data planes of a (tile, step) block with L lanes: lane bytes 0-15 at
-// l * 16, bytes 16-23 at 16 L + l * 8, bytes 24-31 at 24 L + l * 8, bytes
-// 32-47 at 32 L + l * 16.  Each plane is contiguous over the lanes, and every
-// instruction operand (FP6: bytes 0-23 or 24-47; FP8: 0-31) is made of whole
-// plane pieces.
-__host__ __device__ inline int64_t lane_plane_loc(int lanes, int l, int o) {
-  return o < 16 ? (int64_t)l * 16 + o
-                : o < 24 ? 16LL * lanes + l * 8 + (o - 16)
-                         : o < 32 ? 24LL * lanes + l * 8 + (o - 24)
-                                  : 32LL * lanes + l * 16 + (o - 32);
-}
 // Activation operand image: byte o (0..47) of lane data (row, st, h), and
-// scale byte j (0, 1) of (row, st, h).  A (32-row tile, step) block holds 64
-// lanes, lane 32 h + (row % 32).
+// scale byte j (0, 1) of (row, st, h).
 __host__ __device__ inline int64_t act_op_loc(int64_t row, int st, int nsteps, int h, int o) {
-  return ((row >> 5) * nsteps + st) * (int64_t)kActStep +
-         lane_plane_loc(64, 32 * h + (int)(row & 31), o);
+  return ((row >> 5) * nsteps + st) * (int64_t)kActStep + (o >> 4) * 1024 + h * 512 +
+         (row & 31) * 16 + (o & 15);
 }
 __host__ __device__ inline int64_t act_sc_loc(int64_t row, int st, int nsteps, int h, int j) {
   return ((row >> 5) * nsteps + st) * (int64_t)kActScaleStep + h * 128 + (row & 31) * 4 + j;
@@ -360,9 +347,8 @@ __host__ __device__ inline int64_t op_tile_bytes(const OpGeo &o) {
 }
 
 // Location (relative to its tile) of byte `o` (0..47) of lane (h, c) of step st.
-// A weight chunk holds 256 lanes, lane 128 h + c.
 __host__ __device__ inline int64_t w_op_loc(int st, int h, int c, int o) {
-  return (int64_t)kOpChunk * st + lane_plane_loc(256, 128 * h + c, o);
+  return (int64_t)kOpChunk * st + (o >> 4) * kOpPart + h * 2048 + c * 16 + (o & 15);
 }
 __host__ __device__ inline int64_t w_op_scale(int st, int h, int c) {
   return (int64_t)kOpChunk * st + 3 * kOpPart + h * 512 + c * 4;

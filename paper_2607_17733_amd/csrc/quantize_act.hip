@@ -239,31 +239,26 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
   }
 
   // prefill operand image (32-row tiles) and its scale bytes
-  // lane 32 h + r of a (tile, step) block: bytes 0-15 at lane * 16, 16-23 at
-  // 1024 + lane * 8, 24-31 at 1536 + lane * 8, 32-47 at 2048 + lane * 16
   uint8_t *op = q.mant + q.op_off + ((row >> 5) * ns) * (int64_t)kActStep + (row & 31) * 16;
-  uint8_t *mid = q.mant + q.op_off + ((row >> 5) * ns) * (int64_t)kActStep + 1024 + (row & 31) * 8;
   uint8_t *sc = q.exp + q.sc_off + ((row >> 5) * ns) * (int64_t)kActScaleStep + (row & 31) * 4;
   if (seg == 0) {
     const int st = idx >> 2, h = idx & 1, j = (idx >> 1) & 1;
     uint8_t *o = op + st * kActStep + h * 512;
-    uint8_t *m = mid + st * kActStep + h * 256;
     uint8_t *s = sc + st * kActScaleStep + h * 128;
     const v6u c = to_e3m2(v, 4.f);
     if (j == 0) {
       *(u4 *)o = u4{c[0], c[1], c[2], c[3]};
-      *(u2 *)m = u2{c[4], c[5]};
+      *(u2 *)(o + 1024) = u2{c[4], c[5]};
       s[0] = (uint8_t)Eu;                    // byte 1 is the partner block's
       *(uint16_t *)(s + 2) = 0;
     } else {
-      *(u2 *)(m + 512) = u2{c[0], c[1]};
+      *(u2 *)(o + 1024 + 8) = u2{c[0], c[1]};
       *(u4 *)(o + 2048) = u4{c[2], c[3], c[4], c[5]};
       s[1] = (uint8_t)Eu;
     }
   } else if (seg == 1) {
     const int st = og.s4 + (idx >> 1), h = idx & 1;
     uint8_t *o = op + st * kActStep + h * 512;
-    uint8_t *m = mid + st * kActStep + h * 256;
     Blk hd, ld;                                // q = 8 h + l
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
@@ -275,8 +270,7 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
     const v6u ch = to_e3m2(hd, 2.f);
     const v6u cl = to_e3m2(ld, 16.f);
     *(u4 *)o = u4{ch[0], ch[1], ch[2], ch[3]};
-    *(u2 *)m = u2{ch[4], ch[5]};
-    *(u2 *)(m + 512) = u2{cl[0], cl[1]};
+    *(u4 *)(o + 1024) = u4{ch[4], ch[5], cl[0], cl[1]};
     *(u4 *)(o + 2048) = u4{cl[2], cl[3], cl[4], cl[5]};
     *(uint32_t *)(sc + st * kActScaleStep + h * 128) = Eu;
   } else {
@@ -292,11 +286,8 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       uint8_t *o = op + st * kActStep + h * 512;
-      uint8_t *m = mid + st * kActStep + h * 256;
-      const u4 l4 = to_e4m3(ld, h, 64.f);
       *(u4 *)o = to_e4m3(hd, h, 4.f);
-      *(u2 *)m = u2{l4[0], l4[1]};
-      *(u2 *)(m + 512) = u2{l4[2], l4[3]};
+      *(u4 *)(o + 1024) = to_e4m3(ld, h, 64.f);
       *(u4 *)(o + 2048) = u4{0u, 0u, 0u, 0u};
       *(uint32_t *)(sc + st * kActScaleStep + h * 128) = Eu;
     }

@@ -130,19 +130,6 @@ def _decode_steps(geo, nb, rows, lane_of, scale_of, weights):
 ACT_STEP, ACT_SCALE_STEP, ACT_ROWS = 3072, 256, 32
 
 
-def plane_lanes(block: np.ndarray, lanes: int) -> np.ndarray:
-    """[..., 48 * lanes] bytes of a lane-plane block -> [..., lanes, 48] lane
-    data: bytes 0-15 of every lane (16 each), then bytes 16-23 (8 each), then
-    bytes 24-31 (8 each), then bytes 32-47 (16 each)."""
-    L = lanes
-    lead = block.shape[:-1]
-    p0 = block[..., :16 * L].reshape(lead + (L, 16))
-    p1 = block[..., 16 * L:24 * L].reshape(lead + (L, 8))
-    p2 = block[..., 24 * L:32 * L].reshape(lead + (L, 8))
-    p3 = block[..., 32 * L:48 * L].reshape(lead + (L, 16))
-    return np.concatenate([p0, p1, p2, p3], axis=-1)
-
-
 def decode_act(op_img: np.ndarray, sc_img: np.ndarray, widths, M: int):
     """Activation operand image (32-row tiles) and its scale bytes ->
     (q [M, K], E [M, nb], layout_ok)."""
@@ -150,12 +137,11 @@ def decode_act(op_img: np.ndarray, sc_img: np.ndarray, widths, M: int):
     nt = -(-M // ACT_ROWS)
     assert op_img.size == nt * geo.nsteps * ACT_STEP
     assert sc_img.size == nt * geo.nsteps * ACT_SCALE_STEP
-    t = op_img.reshape(nt, geo.nsteps, ACT_STEP)
+    t = op_img.reshape(nt, geo.nsteps, 3, 2, ACT_ROWS, 16)
     sct = sc_img.reshape(nt, geo.nsteps, 2, ACT_ROWS, 4)
 
     def lane_of(st, h):
-        lanes = plane_lanes(t[:, st], 64)                 # [nt, 64, 48]
-        return lanes[:, 32 * h:32 * h + 32].reshape(nt * ACT_ROWS, 48)[:M]
+        return t[:, st, :, h].transpose(0, 2, 1, 3).reshape(nt * ACT_ROWS, 48)[:M]
 
     def scale_of(st, h):
         return sct[:, st, h].reshape(nt * ACT_ROWS, 4)[:M]
@@ -173,8 +159,9 @@ def w_lane_bytes(img: np.ndarray, geo: Geo, st: int, h: int):
     tile = CHUNK * geo.nsteps
     ntiles = img.size // tile
     t = img[:ntiles * tile].reshape(ntiles, geo.nsteps, CHUNK)[:, st]
-    lanes = plane_lanes(t[:, :3 * PART], 2 * TILE_COLS)   # [ntiles, 256, 48]
-    return lanes[:, TILE_COLS * h:TILE_COLS * (h + 1)].reshape(ntiles * TILE_COLS, 48)
+    parts = [t[:, j * PART + h * 2048:j * PART + h * 2048 + 2048].reshape(ntiles, TILE_COLS, 16)
+             for j in range(3)]
+    return np.concatenate(parts, axis=2).reshape(ntiles * TILE_COLS, 48)
 
 
 def w_scales(img: np.ndarray, geo: Geo, st: int, h: int):
