@@ -16,24 +16,26 @@
 //   8-bit (1 block):  two FP8 instructions, [h|l].[h|l] and [h|l].[l|h].
 // The digit products are exact; only the fp32 accumulation rounds.
 //
-// Tiling: 256x128 outputs per workgroup of eight waves, two per SIMD; wave
-// (r, c) owns rows 64r..64r+63 x columns 64c..64c+63 = 2x2 tiles of 32x32
-// fp32 accumulators and runs every K step.
+// Tiling: 256x128 outputs per workgroup of eight waves in two K groups of
+// four, one wave of each group per SIMD.  Group g takes the steps s with
+// s % 2 == g; wave (g, r) owns rows 64r..64r+63 x all 128 columns = 2x4 tiles
+// of 32x32 fp32 accumulators, and the groups' partial sums meet in LDS at the
+// end.
 //
-// Data path: each step's operands -- the eight 32-row activation blocks,
-// their scale blocks and the weight chunk, already in the layout the lanes
-// read -- are copied global -> LDS by the buffer unit's direct-to-LDS loads
-// (no registers), five 1 KB loads per wave and step, into a ring of four LDS
-// stages.  Loads run four steps ahead of the products and the operands of a
-// step are read from LDS into registers one step ahead, so neither latency
-// meets a matrix instruction.  A step waits for the wave's loads of the next
-// stage and its reads of the current one, meets the other waves at a
-// barrier (after which the next stage is complete and the current one is
-// free), then spreads the loads of step + 4 into the freed stage and the
-// reads of step + 1 between its products.  Two waves per SIMD keep the
-// matrix core busy while one of them waits at the barrier.
-// Workgroup ids are remapped so that each XCD owns a compact block of output
-// tiles: the activation rows and weight columns it reads stay in its L2.
+// Data path, chosen by what gfx950 charges (measured): an LDS read costs the
+// same per instruction whatever its width, direct-to-LDS loads and LDS reads
+// serialise, and load instructions issue at a fixed rate per wave.  So:
+//   - activations go straight from the row-tiled operand image into
+//     registers -- each 32-row block is used by exactly one wave -- one
+//     iteration (two steps) ahead, in two register sets;
+//   - the weight chunk of each step (13 KB, already in the LDS layout) goes
+//     global -> LDS by direct-to-LDS loads into a ring of eight step stages,
+//     three iterations ahead; the four waves of a group read it per column
+//     tile, one tile ahead of the products.
+// One barrier per iteration; the kernel counts its own loads (vmcnt) to know
+// when a stage is complete.  Workgroup ids are remapped so that each XCD owns
+// a compact block of output tiles: the activation rows and weight columns it
+// reads stay in its L2.
 #include "mxq_device.h"
 #include "mxq_internal.h"
 
@@ -45,30 +47,25 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef unsigned u4 __attribute__((ext_vector_type(4)));
-typedef unsigned u2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int BM = 256, BN = kOpCols, NT = 512;
 constexpr int kFmtFp8 = 0, kFmtFp6 = 3;      // e4m3, e3m2
-constexpr int kStages = 4;                   // LDS ring; loads run kStages - 1 steps ahead
-// One stage: the eight activation tile blocks (3 KB each), their 256-byte
-// scale blocks, then the 13 KB weight chunk.
-constexpr int kStA = 0;
-constexpr int kStAScale = kStA + 8 * kActStep;              // 24576
-constexpr int kStW = kStAScale + 8 * kActScaleStep;         // 26624
-constexpr int kStage = kStW + kOpChunk;                     // 39936
-static_assert(kStage % 16 == 0 && kStages * kStage <= 160 * 1024, "LDS ring");
-// A step's 39 loads of 1 KB (24 activation, 2 activation scale, 13 weight),
-// plus one repeat of the last, as five per wave.
-constexpr int kDmaPerStep = 5;
+constexpr int kWStages = 8;                  // weight ring: 4 iterations of 2 steps
+constexpr int kRing = kWStages * kOpChunk;   // 106496 bytes
+// Reduction of the two groups: [column][row] floats, 256 rows + 4 padding.
+constexpr int kRedPitch = 260;
+static_assert(kRing <= 160 * 1024 && 128 * kRedPitch * 4 <= 160 * 1024, "LDS");
+// Loads per wave and iteration: 4 direct-to-LDS weight loads (the two steps'
+// 26 kilobytes and 6 repeats, over 8 waves), then 8 activation loads (two
+// 32-row tiles: three 16-byte parts and the scale dword each).
+constexpr int kWLoads = 4, kALoads = 8, kBundle = kWLoads + kALoads;
 
 template <int S> struct Int { static constexpr int v = S; };
 
-// A lane's 48 bytes of one step, as three 16-byte pieces (one LDS read
-// each).  FP6 operands are bytes 0-23 and 24-47 and FP8 operands 0-31 and
-// 16-47, so the middle piece is split or shared; the register copies that
-// needs are cheaper than more, narrower LDS reads, which cost the same per
-// instruction.
+// A lane's 48 bytes of one step, as three 16-byte pieces.  FP6 operands are
+// bytes 0-23 and 24-47 and FP8 operands 0-31 and 16-47, so the middle piece
+// is split or shared through register copies.
 struct Lane48 {
   u4 p[3];
 };
@@ -90,15 +87,9 @@ __device__ inline v16f mma(const v8i &a, const v8i &b, v16f c, int sa, int sb) {
   return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, FA, FA, SA, sa, SB, sb);
 }
 
-// The LDS ring's synchronisation is explicit: the compiler neither knows
-// which direct-to-LDS load fills which stage nor may move LDS reads across
+// The ring's synchronisation is explicit: the compiler does not know which
+// direct-to-LDS load fills which stage, and may not move LDS accesses across
 // these points.
-template <int N>
-__device__ inline void wait_loads() {
-  static_assert(N >= 0 && N < 64, "vmcnt");
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-// ... and also until this wave's LDS reads have completed.
 template <int N>
 __device__ inline void wait_loads_lds() {
   static_assert(N >= 0 && N < 64, "vmcnt");
@@ -106,13 +97,42 @@ __device__ inline void wait_loads_lds() {
 }
 __device__ inline void barrier() { asm volatile("s_barrier" ::: "memory"); }
 
+// 4x4 transpose within each quad of lanes: lane j of a quad holds v[i] = the
+// element of row i, column j; afterwards it holds row j, columns 0..3.
+template <int CTRL>
+__device__ inline float dpp(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL, 0xF,
+                                                             0xF, false));
+}
+__device__ inline v4f quad_transpose(v4f a, int j) {
+  // swap the off-diagonal 2x2 blocks with lane j ^ 2, then within them with j ^ 1
+  const bool b1 = j & 2, b0 = j & 1;
+  constexpr int kSwap2 = 0x4E, kSwap1 = 0xB1;   // quad_perm [2,3,0,1] and [1,0,3,2]
+  const float u0 = dpp<kSwap2>(b1 ? a[0] : a[2]);
+  const float u1 = dpp<kSwap2>(b1 ? a[1] : a[3]);
+  v4f x;
+  x[0] = b1 ? u0 : a[0];
+  x[1] = b1 ? u1 : a[1];
+  x[2] = b1 ? a[2] : u0;
+  x[3] = b1 ? a[3] : u1;
+  const float w0 = dpp<kSwap1>(b0 ? x[0] : x[1]);
+  const float w1 = dpp<kSwap1>(b0 ? x[2] : x[3]);
+  v4f y;
+  y[0] = b0 ? w0 : x[0];
+  y[1] = b0 ? x[1] : w0;
+  y[2] = b0 ? w1 : x[2];
+  y[3] = b0 ? x[3] : w1;
+  return y;
+}
+
 __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles,
                                                              int gm, int gn) {
-  __shared__ __attribute__((aligned(16))) u4 lds[kStages * kStage / 16];
-
+  __shared__ __attribute__((aligned(16))) u4 lds[(128 * kRedPitch * 4 > kRing ? 128 * kRedPitch * 4
+                                                                               : kRing) / 16];
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);      // wave-uniform
   const int l32 = lane & 31, lh = lane >> 5;
+  const int kg = wave >> 2, wr = wave & 3;                      // K group, row block
   int mt, nt;
   {
     // XCD x (workgroups pid % 8 == x) owns a block of (mtiles / gm) x
@@ -131,226 +151,211 @@ __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mti
   const int64_t row0 = (int64_t)mt * BM, col0 = (int64_t)nt * BN;
   const OpGeo og(g.n4, g.n6, g.n8);
   const int nsteps = og.nsteps;
+  char *const ring = (char *)lds;
 
-  // Wave (r, c): row block r (two 32-row tiles), column half c.
-  const int wr = wave >> 1, wc = wave & 1;
-  // The workgroup's eight 32-row tiles of the activation operand image
-  // (tiles past the last one load the last tile; those rows are never
-  // stored).
+  // This wave's two 32-row tiles (tiles past the last one load the last tile;
+  // those rows are never stored).
   const int last = (int)((g.M - 1) / kActRows);
-  const int tile0 = (int)(row0 / kActRows);
+  const int ta = min((int)(row0 / kActRows) + 2 * wr, last);
+  const int tb = min(ta + 1, last);
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
       (void *)(g.a_mant + g.a_op), 0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
       (void *)(g.a_exp + g.a_sc), 0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       (void *)(g.w_mant + g.w_op + (int64_t)nt * g.w_tile), 0, 0x7fffffff, 0x00020000);
-  const int v16 = lane * 16;
-  char *const ring = (char *)lds;
-  auto tile_of = [&](int t) { return min(tile0 + t, last); };
-  // Scale gathers: lane l reads bytes (l % 16) * 16 .. +15 of the scale block
-  // of tile 4 h + l / 16 (h = 0, 1), whose step st block starts at
-  // (tile * nsteps + st) * 256; the per-lane part of that offset is fixed.
-  int vsc[2];
-#pragma unroll
-  for (int h = 0; h < 2; ++h)
-    vsc[h] = tile_of(4 * h + (lane >> 4)) * nsteps * kActScaleStep + (lane & 15) * 16;
+  const int v16 = lane * 16, v4 = lane * 4;
 
-  // The step's loads are numbered 0..39: 0..23 activation tile n / 3,
-  // kilobyte n % 3; 24, 25 the scale blocks of tiles 4 (n - 24) .. +3;
-  // 26..38 weight kilobyte n - 26 (the last one the scale dwords); 39 repeats
-  // 38.  Wave w issues loads w + 8 j, j = 0..4; their descriptors are fixed
-  // but for the step offset (soff + st * sstep).
-  struct Load {
-    __amdgpu_buffer_rsrc_t rsrc;
-    int lds, voff, soff, sstep;
-  } ld[kDmaPerStep];
-#pragma unroll
-  for (int j = 0; j < kDmaPerStep; ++j) {
-    const int n = wave + 8 * j;
-    if (n < 24) {
-      const int t = n / 3, kb = n % 3;
-      ld[j] = {ra, kStA + t * kActStep + kb * 1024, v16, tile_of(t) * nsteps * kActStep + kb * 1024,
-               kActStep};
-    } else if (n < 26) {
-      const int h = n - 24;
-      ld[j] = {rs, kStAScale + 4 * h * kActScaleStep, vsc[h], 0, kActScaleStep};
-    } else {
-      const int kb = min(n - 26, 12);
-      ld[j] = {rw, kStW + kb * 1024, v16, kb * 1024, kOpChunk};
-    }
-  }
-  // This wave's load j (0..4) of step st into stage q.
-  auto issue = [&](int st, int q, int j) __attribute__((always_inline)) {
-    st = min(st, nsteps - 1);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(ld[j].rsrc, (lds_void *)(ring + q * kStage + ld[j].lds),
-                                             16, ld[j].voff, ld[j].soff + st * ld[j].sstep, 0, 0);
-  };
-
-  v16f acc[2][2];
+  v16f acc[2][4];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int n = 0; n < 2; ++n) acc[a][n] = v16f{};
+    for (int n = 0; n < 4; ++n) acc[a][n] = v16f{};
 
-  // All operands of one step in registers: the wave's two activation tiles
-  // and the four weight column tiles.
-  struct Ops {
-    Lane48 x[2], w[2];
-    uint32_t sa[2], sw[2];
-  } ops[2];
+  Lane48 xa[2][2];          // activation lane data: register set, row tile
+  uint32_t xs[2][2];        // activation scale dwords
 
-  // Read the operands of step st (stage st % 4) into ops[O]: the activation
-  // tiles, and weight column tile tn.
-  auto read_x = [&](auto o_tag, int st) __attribute__((always_inline)) {
-    constexpr int O = decltype(o_tag)::v;
-    const char *stage = ring + (st & 3) * kStage;
-    Ops &d = ops[O];
+  // Weight loads of iteration it (steps 2 it, 2 it + 1) into their stages:
+  // kilobytes n = 0..25 (13 per step), 26..31 repeat the last; wave w issues
+  // n = w + 8 j.
+  auto issue_w = [&](int it) __attribute__((always_inline)) {
 #pragma unroll
-    for (int tm = 0; tm < 2; ++tm) {
-      const u4 *blk = (const u4 *)(stage + kStA + (wr * 2 + tm) * kActStep);   // 64 lanes
-#pragma unroll
-      for (int j = 0; j < 3; ++j) d.x[tm].p[j] = blk[j * 64 + lane];
-      d.sa[tm] = ((const uint32_t *)(stage + kStAScale))[(wr * 2 + tm) * 64 + lane];
+    for (int j = 0; j < kWLoads; ++j) {
+      const int n = min(wave + 8 * j, 25);
+      const int st = min(2 * it + n / 13, nsteps - 1), kb = n % 13;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rw, (lds_void *)(ring + (st % kWStages) * kOpChunk + kb * 1024), 16, v16,
+          st * kOpChunk + kb * 1024, 0, 0);
     }
   };
-  auto read_w = [&](auto o_tag, int st, int tn) __attribute__((always_inline)) {
-    constexpr int O = decltype(o_tag)::v;
-    const char *W = ring + (st & 3) * kStage + kStW;                  // 256 lanes
-    Ops &d = ops[O];
-    const int L = lh * 128 + wc * 64 + tn * 32 + l32;
+  // Activation loads of the wave's step in iteration it, row tile tm, into
+  // register set S.
+  auto issue_a_half = [&](auto set_tag, int it, int tm) __attribute__((always_inline)) {
+    constexpr int S = decltype(set_tag)::v;
+    const int st = min(2 * it + kg, nsteps - 1);
+    const int blk = (tm == 0 ? ta : tb) * nsteps + st;
 #pragma unroll
-    for (int j = 0; j < 3; ++j) d.w[tn].p[j] = ((const u4 *)W)[j * 256 + L];
-    d.sw[tn] = ((const uint32_t *)(W + 3 * kOpPart))[L];
+    for (int j = 0; j < 3; ++j)
+      xa[S][tm].p[j] = __builtin_bit_cast(
+          u4, __builtin_amdgcn_raw_buffer_load_b128(ra, v16, blk * kActStep + j * 1024, 0));
+    xs[S][tm] = __builtin_amdgcn_raw_buffer_load_b32(rs, v4, blk * kActScaleStep, 0);
   };
-  // The products of column tile tn (both row tiles) of one step from ops[O].
-  auto mul_tile = [&](auto seg, auto o_tag, int tn) __attribute__((always_inline)) {
-    constexpr int SEG = decltype(seg)::v, O = decltype(o_tag)::v;
+
+  // The products of step s (this wave's) from register set S: per column
+  // tile, its weight operand read from the stage one tile ahead.
+  auto compute = [&](auto seg, auto set_tag, int s, auto &&hook) __attribute__((always_inline)) {
+    constexpr int SEG = decltype(seg)::v, S = decltype(set_tag)::v;
     constexpr int NK = SEG == 1 ? 4 : 2;
-    const Ops &d = ops[O];
+    const char *W = ring + (s % kWStages) * kOpChunk;          // 256 lanes
+    Lane48 w[2];
+    uint32_t sw[2];
+    auto read_w = [&](int o, int tn) __attribute__((always_inline)) {
+      const int L = lh * 128 + tn * 32 + l32;
 #pragma unroll
-    for (int k = 0; k < NK; ++k)
+      for (int j = 0; j < 3; ++j) w[o].p[j] = ((const u4 *)W)[j * 256 + L];
+      sw[o] = ((const uint32_t *)(W + 3 * kOpPart))[L];
+    };
+    read_w(0, 0);
 #pragma unroll
-      for (int tm = 0; tm < 2; ++tm) {
-        v16f &c = acc[tm][tn];
-        const Lane48 &x = d.x[tm], &w = d.w[tn];
-        const int as = (int)d.sa[tm], ws = (int)d.sw[tn];
-        if (SEG == 0) {          // block pairs (4s', 4s'+1), (4s'+2, 4s'+3): scale bytes 0, 1
-          if (k == 0) c = mma<kFmtFp6, 0, 0>(fp6_lo(x), fp6_lo(w), c, as, ws);
-          else c = mma<kFmtFp6, 1, 1>(fp6_hi(x), fp6_hi(w), c, as, ws);
-        } else if (SEG == 1) {   // digit products hh, ll, hl, lh
-          const v8i av = (k == 0 || k == 2) ? fp6_lo(x) : fp6_hi(x);
-          const v8i wv = (k == 0 || k == 3) ? fp6_lo(w) : fp6_hi(w);
-          c = mma<kFmtFp6, 0, 0>(av, wv, c, as, ws);
-        } else {                 // [h|l].[h|l], [h|l].[l|h]
-          c = mma<kFmtFp8, 0, 0>(fp8_lo(x), k == 0 ? fp8_lo(w) : fp8_hi(w), c, as, ws);
+    for (int tn = 0; tn < 4; ++tn) {
+      const int o = tn & 1;
+      if (tn < 3) read_w(o ^ 1, tn + 1);
+      hook(tn);
+#pragma unroll
+      for (int k = 0; k < NK; ++k)
+#pragma unroll
+        for (int tm = 0; tm < 2; ++tm) {
+          v16f &c = acc[tm][tn];
+          const Lane48 &x = xa[S][tm];
+          const int as = (int)xs[S][tm], ws = (int)sw[o];
+          if (SEG == 0) {          // block pairs (4s', 4s'+1), (4s'+2, 4s'+3): scale bytes 0, 1
+            if (k == 0) c = mma<kFmtFp6, 0, 0>(fp6_lo(x), fp6_lo(w[o]), c, as, ws);
+            else c = mma<kFmtFp6, 1, 1>(fp6_hi(x), fp6_hi(w[o]), c, as, ws);
+          } else if (SEG == 1) {   // digit products hh, ll, hl, lh
+            const v8i av = (k == 0 || k == 2) ? fp6_lo(x) : fp6_hi(x);
+            const v8i wv = (k == 0 || k == 3) ? fp6_lo(w[o]) : fp6_hi(w[o]);
+            c = mma<kFmtFp6, 0, 0>(av, wv, c, as, ws);
+          } else {                 // [h|l].[h|l], [h|l].[l|h]
+            c = mma<kFmtFp8, 0, 0>(fp8_lo(x), k == 0 ? fp8_lo(w[o]) : fp8_hi(w[o]), c, as, ws);
+          }
         }
-      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
   };
 
-  // Step s multiplies from ops[O] (read during step s - 1).  Before that, the
-  // wave waits until its loads of stage s + 1 have landed and its reads of
-  // stage s (into ops[O]) have completed; after the barrier every wave is in
-  // that state, so stage s + 1 is complete and stage s is free.  Then, between
-  // the products, it issues the loads of step s + 4 into stage s % 4 and reads
-  // the operands of step s + 1 into ops[1 - O].
-  auto step = [&](auto seg, auto o_tag, int s) __attribute__((always_inline)) {
-    constexpr int O = decltype(o_tag)::v;
-    constexpr Int<1 - O> nx{};
-    const int sn = min(s + 1, nsteps - 1);
-    wait_loads_lds<2 * kDmaPerStep>();
+  // Iteration it, activations of this wave's step in register set S.  Each
+  // iteration issues a bundle of loads, the activations of it + 1 (into the
+  // other register set) and then the weights of it + 3, spread over the
+  // products of its column tiles so that the matrix core keeps running while
+  // they queue.  Before the barrier the wave waits for its own weight loads
+  // of this iteration's stages (from the bundle of it - 3: two bundles, 24
+  // loads, have been issued since; 16 before the first) and for its LDS
+  // reads; after it every wave has, so both stages are complete and the
+  // previous iteration's stages are free for the weights of it + 3.  The
+  // activation loads of a bundle come first, so waiting for them never waits
+  // for the weights behind them.
+  auto iteration = [&](auto seg, auto set_tag, int it, bool mul) __attribute__((always_inline)) {
+    constexpr int S = decltype(set_tag)::v;
+    if (it > 0) wait_loads_lds<2 * kBundle>();
+    else wait_loads_lds<kWLoads + kALoads + kWLoads>();
     barrier();
-    // Chunks in a fixed order (the scheduler may interleave within a chunk
-    // only): the products of column tile 0 with three of the loads of step
-    // s + 4 and the activation reads of step s + 1, then those of column tile
-    // 1 with the other two loads and the weight reads.
-    issue(s + 4, s & 3, 0);
-    issue(s + 4, s & 3, 1);
-    issue(s + 4, s & 3, 2);
-    read_x(nx, sn);
-    mul_tile(seg, o_tag, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    issue(s + 4, s & 3, 3);
-    issue(s + 4, s & 3, 4);
-    read_w(nx, sn, 0);
-    read_w(nx, sn, 1);
-    mul_tile(seg, o_tag, 1);
-  };
-  // The steps [b, e) of one segment, in pairs so that the operand sets
-  // alternate statically; after the last step the next step's operands are
-  // in ops[0].
-  auto run = [&](auto seg, int b, int e) __attribute__((always_inline)) {
-    int s = b;
-    for (; s + 2 <= e; s += 2) {
-      step(seg, Int<0>{}, s);
-      step(seg, Int<1>{}, s + 1);
-    }
-    if (s < e) {
-      step(seg, Int<0>{}, s);
-      ops[0] = ops[1];
+    auto hook = [&](int tn) __attribute__((always_inline)) {
+      if (tn == 0) issue_a_half(Int<1 - S>{}, it + 1, 0);
+      else if (tn == 1) issue_a_half(Int<1 - S>{}, it + 1, 1);
+      else if (tn == 2) issue_w(it + 3);
+    };
+    if (mul) {
+      compute(seg, set_tag, 2 * it + kg, hook);
+    } else {
+      hook(0);
+      hook(1);
+      hook(2);
     }
   };
+  // Iterations [ib, ie) of one segment; register set = it % 2.
+  auto run = [&](auto seg, int ib, int ie) __attribute__((always_inline)) {
+    int it = ib;
+    if (it < ie && (it & 1)) iteration(seg, Int<1>{}, it++, true);
+    for (; it + 2 <= ie; it += 2) {
+      iteration(seg, Int<0>{}, it, true);
+      iteration(seg, Int<1>{}, it + 1, true);
+    }
+    if (it < ie) iteration(seg, Int<0>{}, it, true);
+  };
 
-  // Prologue: the loads of steps 0..3, then the operands of step 0.
-#pragma unroll
-  for (int st = 0; st < 4; ++st)
-#pragma unroll
-    for (int j = 0; j < kDmaPerStep; ++j) issue(st, st, j);
-  wait_loads_lds<3 * kDmaPerStep>();
-  barrier();
-  read_x(Int<0>{}, 0);
-#pragma unroll
-  for (int tn = 0; tn < 2; ++tn) read_w(Int<0>{}, 0, tn);
+  // Prologue: weights of iterations 0 and 1, then the bundle of iteration -1
+  // (activations of 0, weights of 2).
+  issue_w(0);
+  issue_w(1);
+  __builtin_amdgcn_sched_barrier(0);
+  issue_a_half(Int<0>{}, 0, 0);
+  issue_a_half(Int<0>{}, 0, 1);
+  __builtin_amdgcn_sched_barrier(0);
+  issue_w(2);
+  __builtin_amdgcn_sched_barrier(0);
 
+  // Group g's steps 2 it + g of segment [b, e) are the iterations
+  // [(b - g + 1) / 2, (e - g + 1) / 2).
   const int e4 = og.s4, e6 = og.s4 + og.s6;
-  run(Int<0>{}, 0, e4);
-  run(Int<1>{}, e4, e6);
-  run(Int<2>{}, e6, nsteps);
-  // The last steps' loads (of clamped steps) must land before the workgroup
-  // releases its LDS.
-  wait_loads<0>();
-
-  // Epilogue through LDS: each wave writes its 64 x 64 tile row-major (row
-  // pitch 72 floats: the two row groups one instruction writes fall in
-  // disjoint banks) and reads it back as 16-byte row pieces, so the stores
-  // are 16 bytes per lane -- a quarter of the store instructions, which the
-  // address unit issues at a fixed rate per instruction.
-  constexpr int kPitch = 72;
-  static_assert(8 * 64 * kPitch * 4 <= kStages * kStage, "epilogue tile");
+  const int i4 = (e4 - kg + 1) >> 1, i6 = (e6 - kg + 1) >> 1, i8 = (nsteps - kg + 1) >> 1;
+  run(Int<0>{}, 0, i4);
+  run(Int<1>{}, i4, i6);
+  run(Int<2>{}, i6, i8);
+  // Group 1 has one iteration less when nsteps is odd; it still meets the
+  // barrier of group 0's last iteration.
+  const int niter = (nsteps + 1) >> 1;
+  if (i8 < niter) {
+    if (i8 & 1) iteration(Int<2>{}, Int<1>{}, i8, false);
+    else iteration(Int<2>{}, Int<0>{}, i8, false);
+  }
+  wait_loads_lds<0>();
   barrier();                                 // every wave is done with the ring
-  float *tile = (float *)ring + wave * 64 * kPitch;
+
+  // Reduction: group 1 leaves its sums in LDS as [column][row] (four rows of
+  // a lane's tile are one 16-byte write), group 0 adds them, transposes each
+  // quad of lanes to row pieces of four columns, and stores 16 bytes a lane.
+  float *red = (float *)ring;
+  if (kg == 1) {
 #pragma unroll
-  for (int tm = 0; tm < 2; ++tm)
+    for (int tm = 0; tm < 2; ++tm)
 #pragma unroll
-    for (int tn = 0; tn < 2; ++tn)
+      for (int tn = 0; tn < 4; ++tn)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        tile[(tm * 32 + 8 * (r >> 2) + 4 * lh + (r & 3)) * kPitch + tn * 32 + l32] = acc[tm][tn][r];
-  // only this wave reads its tile back
-  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  const int q = lane & 15, rq = lane >> 4;   // 4 columns 4q.., row 4 i + rq
-  const int64_t jc = col0 + wc * 64 + 4 * q;
-  // 16-byte stores when the wave's 64 columns are all inside Y and aligned
-  const bool vec = (g.ldy & 3) == 0 && ((uintptr_t)g.y & 15) == 0 &&
-                   col0 + wc * 64 + 64 <= g.N;
-  if (vec) {
+        for (int q = 0; q < 4; ++q) {
+          const int rr = wr * 64 + tm * 32 + 8 * q + 4 * lh, cc = tn * 32 + l32;
+          *(v4f *)&red[cc * kRedPitch + rr] =
+              v4f{acc[tm][tn][4 * q], acc[tm][tn][4 * q + 1], acc[tm][tn][4 * q + 2],
+                  acc[tm][tn][4 * q + 3]};
+        }
+  }
+  barrier();
+  if (kg == 0) {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    const bool vec = (g.ldy & 3) == 0 && ((uintptr_t)g.y & 15) == 0 && col0 + BN <= g.N;
+    const int j = l32 & 3;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int rr = 4 * i + rq;
-      const int64_t row = row0 + wr * 64 + rr;
-      const v4f v = *(const v4f *)&tile[rr * kPitch + 4 * q];
-      if (row < g.M) __builtin_nontemporal_store(v, (v4f *)(g.y + row * g.ldy + jc));
-    }
-  } else {
+    for (int tm = 0; tm < 2; ++tm)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int rr = 4 * i + rq;
-      const int64_t row = row0 + wr * 64 + rr;
-      if (row >= g.M) continue;
+      for (int tn = 0; tn < 4; ++tn)
 #pragma unroll
-      for (int c = 0; c < 4; ++c)
-        if (jc + c < g.N) g.y[row * g.ldy + jc + c] = tile[rr * kPitch + 4 * q + c];
-    }
+        for (int q = 0; q < 4; ++q) {
+          const int rr = wr * 64 + tm * 32 + 8 * q + 4 * lh, cc = tn * 32 + l32;
+          const v4f o = *(const v4f *)&red[cc * kRedPitch + rr];
+          v4f s = v4f{acc[tm][tn][4 * q] + o[0], acc[tm][tn][4 * q + 1] + o[1],
+                      acc[tm][tn][4 * q + 2] + o[2], acc[tm][tn][4 * q + 3] + o[3]};
+          // lane (quad k, j) now: row rr + j, columns (cc & ~3) .. + 3
+          s = quad_transpose(s, j);
+          const int64_t row = row0 + rr + j, col = col0 + (cc & ~3);
+          if (row >= g.M) continue;
+          float *dst = g.y + row * g.ldy + col;
+          if (vec) {
+            __builtin_nontemporal_store(s, (v4f *)dst);
+          } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+              if (col + c < g.N) dst[c] = s[c];
+          }
+        }
   }
 }
 
