@@ -314,29 +314,61 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
   const int64_t r0 = w << lgR;
 
   // Stage the permutation as byte offsets into a staged row (entries outside
-  // [0, K) point at the zero padding after the row), and the rows.
+  // [0, K) point at the zero padding after the row), and the rows.  Each
+  // thread issues a batch of loads before it stores any of them, so the
+  // batch costs one memory latency instead of one per load.
+  constexpr int kBatch = 8;
   int32_t *soff = (int32_t *)(smem + R * rowB);
   if (q.stage) {
-    for (int v = t; v < K / 4; v += nthr) {
-      const int4 p = *(const int4 *)(q.perm + 4 * v);
-      int4 o;
-      o.x = (unsigned)p.x < (unsigned)K ? 2 * p.x : 2 * K;
-      o.y = (unsigned)p.y < (unsigned)K ? 2 * p.y : 2 * K;
-      o.z = (unsigned)p.z < (unsigned)K ? 2 * p.z : 2 * K;
-      o.w = (unsigned)p.w < (unsigned)K ? 2 * p.w : 2 * K;
-      *(int4 *)(soff + 4 * v) = o;
+    const int nv = K / 4;
+    for (int v0 = t; v0 < nv; v0 += nthr * kBatch) {
+      int4 p[kBatch];
+#pragma unroll
+      for (int k = 0; k < kBatch; ++k) {
+        const int v = v0 + k * nthr;
+        if (v < nv) p[k] = *(const int4 *)(q.perm + 4 * v);
+      }
+#pragma unroll
+      for (int k = 0; k < kBatch; ++k) {
+        const int v = v0 + k * nthr;
+        if (v >= nv) continue;
+        int4 o;
+        o.x = (unsigned)p[k].x < (unsigned)K ? 2 * p[k].x : 2 * K;
+        o.y = (unsigned)p[k].y < (unsigned)K ? 2 * p[k].y : 2 * K;
+        o.z = (unsigned)p[k].z < (unsigned)K ? 2 * p[k].z : 2 * K;
+        o.w = (unsigned)p[k].w < (unsigned)K ? 2 * p[k].w : 2 * K;
+        *(int4 *)(soff + 4 * v) = o;
+      }
     }
   }
   if (q.vec16) {
-    const int vpr = K / 8;
-    for (int lr = 0; lr < R; ++lr) {
-      const bool live = r0 + lr < q.src_rows;
-      const uint16_t *src = q.src + (r0 + lr) * q.ld;
-      for (int c = t; c < vpr; c += nthr) {
-        u4 d = {0u, 0u, 0u, 0u};
-        if (live) d = *(const u4 *)(src + 8 * c);
-        *(u4 *)(smem + lr * rowB + 16 * c) = d;
+    // vector v = lr * vpr + c, advanced by nthr without dividing per load
+    const int vpr = K / 8, nv = R * vpr;
+    const int dq = nthr / vpr, dr = nthr - dq * vpr;
+    int lr0 = t / vpr, c0 = t - lr0 * vpr;
+    for (int v0 = t; v0 < nv; v0 += nthr * kBatch) {
+      u4 d[kBatch];
+      int lrk[kBatch], ck[kBatch];
+      int lr = lr0, c = c0;
+#pragma unroll
+      for (int k = 0; k < kBatch; ++k) {
+        lrk[k] = lr;
+        ck[k] = c;
+        d[k] = u4{0u, 0u, 0u, 0u};
+        if (v0 + k * nthr < nv && r0 + lr < q.src_rows)
+          d[k] = *(const u4 *)(q.src + (r0 + lr) * q.ld + 8 * c);
+        c += dr;
+        lr += dq;
+        if (c >= vpr) {
+          c -= vpr;
+          ++lr;
+        }
       }
+      lr0 = lr;
+      c0 = c;
+#pragma unroll
+      for (int k = 0; k < kBatch; ++k)
+        if (v0 + k * nthr < nv) *(u4 *)(smem + lrk[k] * rowB + 16 * ck[k]) = d[k];
     }
   } else {
     for (int lr = 0; lr < R; ++lr) {
