@@ -31,7 +31,7 @@ struct QuantArgs {
   int64_t w_tile;          // weights: bytes per 128-column operand tile
   int tail_pad;            // weights: zero bytes after the last slab
   int stage;               // weights: stage source rows in LDS before the gather;
-                           // activations: stage the permutation in LDS
+                           // activations: unused
   int vec16;               // 16-byte source loads are aligned
   int rows_per_wg;         // filled by the launcher
   int lg_rows;             // activations: log2 of the rows per group

@@ -4,15 +4,15 @@
 // block of the permuted row gets one shared exponent E = floor(log2 max|x|)
 // + 127 and mantissas of its own width m in {4, 6, 8}.
 //
-// Work decomposition.  A workgroup owns R consecutive rows (4 for K = 4096,
+// Work decomposition.  A workgroup owns R consecutive rows (8 for K = 4096,
 // fewer for longer rows, up to 64 for short ones) and stages them in LDS with
-// 16-byte loads, together with the column permutation (as byte offsets into
-// a staged row) when it fits, so the permutation becomes an LDS gather.  A
-// thread owns one (row, block) and the workgroup has as many threads as
-// items (up to 1024), two workgroups per CU.  Lanes run over rows fastest,
-// so the rows of a block write contiguous runs of the 32-row operand tiles,
-// and consecutive workgroups (whole tiles) run on one XCD, whose L2 then
-// completes every line of the tile.
+// 16-byte loads, so the permutation becomes an LDS gather (entries outside
+// [0, K) clamp to the zero padding after the row).  A thread owns one (row,
+// block) item, at most two; a workgroup has up to 1024 threads and fills a
+// CU.  Lanes run over rows fastest, so the rows of a block write contiguous
+// runs of the 32-row operand tiles (whole 128-byte lines at R = 8), and
+// consecutive workgroups run on one XCD, whose L2 then completes every line
+// of the tile.
 //
 // Arithmetic.  The block maximum is taken on the integer |bf16| patterns (two
 // per register); the mantissas are computed in fp32, where every step is
@@ -35,7 +35,7 @@ typedef unsigned u4 __attribute__((ext_vector_type(4)));
 typedef unsigned u2 __attribute__((ext_vector_type(2)));
 
 constexpr int kMaxThreads = 1024;
-constexpr int kLdsBudget = 72 * 1024;   // two workgroups per CU
+constexpr int kLdsBudget = 144 * 1024;  // staged rows of one workgroup per CU
 constexpr int kRowPad = 8;              // zero bf16 elements after each staged row
 
 // A block of 32 values kept as its even and odd elements (the register
@@ -93,10 +93,10 @@ __device__ inline uint32_t top_word(const Blk &v, int d) {
 }
 
 // One (row, block) item: gather, quantize, pack, write.  sr is the staged
-// row in LDS, soff the staged permutation (byte offsets) or null.
+// row in LDS, followed by zero padding.
 template <bool RNA>
 __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp,
-                                     int64_t row, const uint8_t *sr, const int32_t *soff) {
+                                     int64_t row, const uint8_t *sr) {
   const int K = (int)q.K;
   const int ns = og.nsteps;
   int seg, idx, n;
@@ -120,17 +120,6 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
 #pragma unroll
       for (int k = 0; k < 4; ++k) pr[4 * u + k] = d[k];
     }
-  } else if (q.stage) {
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int4 o = *(const int4 *)(soff + p0 + 4 * u);
-      const uint32_t e0 = *(const uint16_t *)(sr + o.x);
-      const uint32_t e1 = *(const uint16_t *)(sr + o.y);
-      const uint32_t e2 = *(const uint16_t *)(sr + o.z);
-      const uint32_t e3 = *(const uint16_t *)(sr + o.w);
-      pr[2 * u] = e0 | (e1 << 16);
-      pr[2 * u + 1] = e2 | (e3 << 16);
-    }
   } else {
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
@@ -138,8 +127,8 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
       const int src[4] = {p.x, p.y, p.z, p.w};
       uint32_t e[4];
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
-        e[k] = (unsigned)src[k] < (unsigned)K ? *(const uint16_t *)(sr + 2 * src[k]) : 0u;
+      for (int k = 0; k < 4; ++k)   // out of range: the zero after the row
+        e[k] = *(const uint16_t *)(sr + 2 * min((unsigned)src[k], (unsigned)K));
       pr[2 * u] = e[0] | (e[1] << 16);
       pr[2 * u + 1] = e[2] | (e[3] << 16);
     }
@@ -313,34 +302,10 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
   if ((nwg & 7) == 0) w = (w & 7) * (nwg >> 3) + (w >> 3);
   const int64_t r0 = w << lgR;
 
-  // Stage the permutation as byte offsets into a staged row (entries outside
-  // [0, K) point at the zero padding after the row), and the rows.  Each
-  // thread issues a batch of loads before it stores any of them, so the
-  // batch costs one memory latency instead of one per load.
+  // Stage the rows.  Each thread issues a batch of loads before it stores
+  // any of them, so the batch costs one memory latency instead of one per
+  // load.
   constexpr int kBatch = 8;
-  int32_t *soff = (int32_t *)(smem + R * rowB);
-  if (q.stage) {
-    const int nv = K / 4;
-    for (int v0 = t; v0 < nv; v0 += nthr * kBatch) {
-      int4 p[kBatch];
-#pragma unroll
-      for (int k = 0; k < kBatch; ++k) {
-        const int v = v0 + k * nthr;
-        if (v < nv) p[k] = *(const int4 *)(q.perm + 4 * v);
-      }
-#pragma unroll
-      for (int k = 0; k < kBatch; ++k) {
-        const int v = v0 + k * nthr;
-        if (v >= nv) continue;
-        int4 o;
-        o.x = (unsigned)p[k].x < (unsigned)K ? 2 * p[k].x : 2 * K;
-        o.y = (unsigned)p[k].y < (unsigned)K ? 2 * p[k].y : 2 * K;
-        o.z = (unsigned)p[k].z < (unsigned)K ? 2 * p[k].z : 2 * K;
-        o.w = (unsigned)p[k].w < (unsigned)K ? 2 * p[k].w : 2 * K;
-        *(int4 *)(soff + 4 * v) = o;
-      }
-    }
-  }
   if (q.vec16) {
     // vector v = lr * vpr + c, advanced by nthr without dividing per load
     const int vpr = K / 8, nv = R * vpr;
@@ -386,7 +351,7 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
     const int lr = it & (R - 1);
     const int64_t row = r0 + lr;
     if (row < q.out_rows)
-      quantize_item<RNA>(q, og, bp, row, smem + lr * rowB, q.stage ? soff : nullptr);
+      quantize_item<RNA>(q, og, bp, row, smem + lr * rowB);
   }
   // zero the padding of the packed and exponent rows
   if (t < R) {
@@ -399,11 +364,6 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
   }
 }
 
-// The permutation is staged (as byte offsets) when it fits beside one row.
-bool stage_perm(int64_t K, bool perm) {
-  return perm && 2 * (K + kRowPad) + 4 * K <= kLdsBudget;
-}
-
 int padded_blocks(int n4, int n6, int n8) {
   const OpGeo og(n4, n6, n8);
   return og.n4p + og.n6p + og.n8 + (og.n8 & 1);
@@ -412,19 +372,19 @@ int padded_blocks(int n4, int n6, int n8) {
 }  // namespace
 
 // Rows per workgroup: the largest power of two (at most 64) whose staged
-// rows fit the LDS budget with at most kMaxThreads items.
+// rows fit the LDS budget with at most two items per thread.  More rows per
+// workgroup make longer contiguous runs in the operand tiles.
 int quantize_act_rows(int64_t K, int nbp, bool perm) {
+  (void)perm;
   const int64_t per = 2 * (K + kRowPad);
-  const int64_t fixed = stage_perm(K, perm) ? 4 * K : 0;
   int r = 1;
-  while (r < 64 && 2 * r * per + fixed <= kLdsBudget && (int64_t)nbp * 2 * r <= kMaxThreads)
+  while (r < 64 && 2 * r * per <= kLdsBudget && (int64_t)nbp * 2 * r <= 2 * kMaxThreads)
     r *= 2;
   return r;
 }
 
 int64_t quantize_act_lds(int64_t K, int nbp, bool perm) {
-  return (int64_t)quantize_act_rows(K, nbp, perm) * 2 * (K + kRowPad) +
-         (stage_perm(K, perm) ? 4 * K : 0);
+  return (int64_t)quantize_act_rows(K, nbp, perm) * 2 * (K + kRowPad);
 }
 
 hipError_t launch_quantize_act(const QuantArgs &args, hipStream_t stream) {
@@ -436,7 +396,7 @@ hipError_t launch_quantize_act(const QuantArgs &args, hipStream_t stream) {
   while ((1 << lg) < R) ++lg;
   a.lg_rows = lg;
   a.rows_per_wg = R;
-  a.stage = stage_perm(a.K, perm) ? 1 : 0;
+  a.stage = 0;
   const int64_t grid = (a.out_rows + R - 1) / R;
   if (grid <= 0) return hipSuccess;
   const int64_t lds = quantize_act_lds(a.K, nbp, perm);
