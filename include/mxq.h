@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define MXQ_ABI_VERSION 6
+#define MXQ_ABI_VERSION 7
 #define MXQ_BLOCK 32
 /* mxq_gemm uses the weight-streaming decode kernel for M <= this. */
 #define MXQ_DECODE_MAX_M 16
@@ -177,7 +177,8 @@ const char *mxq_status_str(int status);
  *   columns are zero): per tile, per step, 13312 bytes: lane data byte o of
  *   (column c of the tile, half h) at (o / 16) * 4096 + h * 2048 + c * 16
  *   + o % 16, then the lane's scale bytes (the two of the activation layout,
- *   then two zero bytes) at 12288 + h * 512 + c * 4.  Weight lane data of an
+ *   then two zero bytes) at 12288 + h * 512 + (c % 32) * 16 + (c / 32) * 4,
+ *   so a lane's four 32-column scale dwords are one 16-byte piece.  Weight lane data of an
  *   8-bit step repeats the h codes in its last 16 bytes.
  *   The weight exponents are one row of mxq_exp_row_bytes(fmt) bytes per
  *   (padded to 16) column: w_exp[j * mxq_exp_row_bytes + b].

@@ -59,7 +59,10 @@ static_assert(kRing <= 160 * 1024 && 128 * kRedPitch * 4 <= 160 * 1024, "LDS");
 // Loads per wave and iteration: 4 direct-to-LDS weight loads (the two steps'
 // 26 kilobytes and 6 repeats, over 8 waves), then 8 activation loads (two
 // 32-row tiles: three 16-byte parts and the scale dword each).
-constexpr int kWLoads = 4, kALoads = 8, kBundle = kWLoads + kALoads;
+constexpr int kWLoads = 4, kALoads = 8;
+// The fewest activation loads a bundle holds: 8-bit steps leave the third
+// part unread, so the compiler drops its load.
+constexpr int kMinALoads = 6;
 
 template <int S> struct Int { static constexpr int v = S; };
 
@@ -94,6 +97,11 @@ template <int N>
 __device__ inline void wait_loads_lds() {
   static_assert(N >= 0 && N < 64, "vmcnt");
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(N) : "memory");
+}
+template <int N>
+__device__ inline void wait_loads() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 __device__ inline void barrier() { asm volatile("s_barrier" ::: "memory"); }
 
@@ -201,25 +209,67 @@ __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mti
     xs[S][tm] = __builtin_amdgcn_raw_buffer_load_b32(rs, v4, blk * kActScaleStep, 0);
   };
 
-  // The products of step s (this wave's) from register set S: per column
-  // tile, its weight operand read from the stage one tile ahead.
-  auto compute = [&](auto seg, auto set_tag, int s, auto &&hook) __attribute__((always_inline)) {
+  // Weight operands: two column tiles in flight (w), and the scale dwords of
+  // the four column tiles of the current step (one 16-byte read).
+  Lane48 w[2];
+  u4 swc;
+  auto read_w = [&](const char *base, int o, int tn) __attribute__((always_inline)) {
+    const int L = lh * 128 + tn * 32 + l32;
+#pragma unroll
+    for (int j = 0; j < 3; ++j) w[o].p[j] = ((const u4 *)base)[j * 256 + L];
+  };
+  auto read_sw = [&](const char *base) __attribute__((always_inline)) {
+    return ((const u4 *)(base + 3 * kOpPart))[lh * 32 + l32];
+  };
+
+  // Iteration it: the products of this wave's step s = 2 it + kg from
+  // register set S, column tile by column tile, each tile's weight operand
+  // read one tile ahead.  Its first tile and the step's scales were read at
+  // the end of the previous iteration, so the products start at once.
+  //
+  // Each iteration issues a bundle of loads, the activations of it + 1 (into
+  // the other register set, around tiles 0 and 1) and then the weights of
+  // it + 3 (at tile 2), spread over the products so that the matrix core
+  // keeps running while they queue.  Between tiles 1 and 2 the workgroup
+  // meets at a barrier.  Before it each wave waits for its own weight loads
+  // of iteration it + 1 (at least 16 loads have been issued since them:
+  // the bundle of it - 1 and the activations of it + 1); after it the stages
+  // of it + 1 are complete, so tile 0 of the next step is read during tile 3,
+  // and every wave is past iteration it - 1, whose stages the weights of
+  // it + 3 then overwrite.
+  auto iteration = [&](auto seg, auto set_tag, int it, bool mul) __attribute__((always_inline)) {
     constexpr int SEG = decltype(seg)::v, S = decltype(set_tag)::v;
     constexpr int NK = SEG == 1 ? 4 : 2;
-    const char *W = ring + (s % kWStages) * kOpChunk;          // 256 lanes
-    Lane48 w[2];
-    uint32_t sw[2];
-    auto read_w = [&](int o, int tn) __attribute__((always_inline)) {
-      const int L = lh * 128 + tn * 32 + l32;
-#pragma unroll
-      for (int j = 0; j < 3; ++j) w[o].p[j] = ((const u4 *)W)[j * 256 + L];
-      sw[o] = ((const uint32_t *)(W + 3 * kOpPart))[L];
+    auto hook = [&](int tn) __attribute__((always_inline)) {
+      if (tn == 0) issue_a_half(Int<1 - S>{}, it + 1, 0);
+      else if (tn == 1) issue_a_half(Int<1 - S>{}, it + 1, 1);
+      else if (tn == 2) issue_w(it + 3);
     };
-    read_w(0, 0);
+    auto meet = [&]() __attribute__((always_inline)) {
+      wait_loads<kMinALoads + kWLoads + kMinALoads>();
+      barrier();
+    };
+    if (!mul) {
+      hook(0);
+      hook(1);
+      meet();
+      hook(2);
+      return;
+    }
+    const int s = 2 * it + kg;
+    const char *W = ring + (s % kWStages) * kOpChunk;            // 256 lanes
+    const char *Wn = ring + ((s + 2) % kWStages) * kOpChunk;     // the next step
+    const u4 sw = swc;
 #pragma unroll
     for (int tn = 0; tn < 4; ++tn) {
       const int o = tn & 1;
-      if (tn < 3) read_w(o ^ 1, tn + 1);
+      if (tn == 2) meet();
+      if (tn < 3) {
+        read_w(W, o ^ 1, tn + 1);
+      } else {
+        read_w(Wn, o ^ 1, 0);
+        swc = read_sw(Wn);
+      }
       hook(tn);
 #pragma unroll
       for (int k = 0; k < NK; ++k)
@@ -227,7 +277,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mti
         for (int tm = 0; tm < 2; ++tm) {
           v16f &c = acc[tm][tn];
           const Lane48 &x = xa[S][tm];
-          const int as = (int)xs[S][tm], ws = (int)sw[o];
+          const int as = (int)xs[S][tm], ws = (int)sw[tn];
           if (SEG == 0) {          // block pairs (4s', 4s'+1), (4s'+2, 4s'+3): scale bytes 0, 1
             if (k == 0) c = mma<kFmtFp6, 0, 0>(fp6_lo(x), fp6_lo(w[o]), c, as, ws);
             else c = mma<kFmtFp6, 1, 1>(fp6_hi(x), fp6_hi(w[o]), c, as, ws);
@@ -240,36 +290,6 @@ __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mti
           }
         }
       __builtin_amdgcn_sched_barrier(0);
-    }
-  };
-
-  // Iteration it, activations of this wave's step in register set S.  Each
-  // iteration issues a bundle of loads, the activations of it + 1 (into the
-  // other register set) and then the weights of it + 3, spread over the
-  // products of its column tiles so that the matrix core keeps running while
-  // they queue.  Before the barrier the wave waits for its own weight loads
-  // of this iteration's stages (from the bundle of it - 3: two bundles, 24
-  // loads, have been issued since; 16 before the first) and for its LDS
-  // reads; after it every wave has, so both stages are complete and the
-  // previous iteration's stages are free for the weights of it + 3.  The
-  // activation loads of a bundle come first, so waiting for them never waits
-  // for the weights behind them.
-  auto iteration = [&](auto seg, auto set_tag, int it, bool mul) __attribute__((always_inline)) {
-    constexpr int S = decltype(set_tag)::v;
-    if (it > 0) wait_loads_lds<2 * kBundle>();
-    else wait_loads_lds<kWLoads + kALoads + kWLoads>();
-    barrier();
-    auto hook = [&](int tn) __attribute__((always_inline)) {
-      if (tn == 0) issue_a_half(Int<1 - S>{}, it + 1, 0);
-      else if (tn == 1) issue_a_half(Int<1 - S>{}, it + 1, 1);
-      else if (tn == 2) issue_w(it + 3);
-    };
-    if (mul) {
-      compute(seg, set_tag, 2 * it + kg, hook);
-    } else {
-      hook(0);
-      hook(1);
-      hook(2);
     }
   };
   // Iterations [ib, ie) of one segment; register set = it % 2.
@@ -293,6 +313,11 @@ __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mti
   __builtin_amdgcn_sched_barrier(0);
   issue_w(2);
   __builtin_amdgcn_sched_barrier(0);
+  // the stages of iteration 0 (at least 14 loads since the weights of 0)
+  wait_loads<kWLoads + kMinALoads + kWLoads>();
+  barrier();
+  read_w(ring + kg * kOpChunk, 0, 0);
+  swc = read_sw(ring + kg * kOpChunk);
 
   // Group g's steps 2 it + g of segment [b, e) are the iterations
   // [(b - g + 1) / 2, (e - g + 1) / 2).

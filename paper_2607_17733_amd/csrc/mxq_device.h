@@ -318,7 +318,9 @@ struct OpGeo {
 // kOpChunk bytes; a chunk holds three 16-byte parts of every (half, column)
 // lane and the lane's scale dword (byte 0: first scale, byte 1: second scale
 // of a 4-bit step), laid out as the prefill GEMM keeps it in LDS:
-//   part j at j * 4096 + h * 2048 + c * 16, scales at 12288 + h * 512 + c * 4.
+//   part j at j * 4096 + h * 2048 + c * 16, scales at 12288 + h * 512 +
+//   (c % 32) * 16 + (c / 32) * 4 (a lane's four 32-column tiles' scale
+//   dwords are adjacent: one 16-byte LDS read per step).
 constexpr int kOpCols = 128;
 constexpr int kActRows = 32;
 constexpr int kActStep = 3072;       // operand bytes per (32-row tile, step)
@@ -351,7 +353,7 @@ __host__ __device__ inline int64_t w_op_loc(int st, int h, int c, int o) {
   return (int64_t)kOpChunk * st + (o >> 4) * kOpPart + h * 2048 + c * 16 + (o & 15);
 }
 __host__ __device__ inline int64_t w_op_scale(int st, int h, int c) {
-  return (int64_t)kOpChunk * st + 3 * kOpPart + h * 512 + c * 4;
+  return (int64_t)kOpChunk * st + 3 * kOpPart + h * 512 + (c & 31) * 16 + (c >> 5) * 4;
 }
 
 // FP6 e3m2 code of n/16 (|n| <= 32, n exactly representable).

@@ -168,7 +168,9 @@ def w_scales(img: np.ndarray, geo: Geo, st: int, h: int):
     tile = CHUNK * geo.nsteps
     ntiles = img.size // tile
     t = img[:ntiles * tile].reshape(ntiles, geo.nsteps, CHUNK)[:, st]
-    return t[:, 3 * PART + h * 512:3 * PART + h * 512 + 512].reshape(ntiles * TILE_COLS, 4)
+    # [lane (c % 32)][column tile (c / 32)][4 bytes] -> columns in order
+    s = t[:, 3 * PART + h * 512:3 * PART + h * 512 + 512].reshape(ntiles, 32, 4, 4)
+    return s.transpose(0, 2, 1, 3).reshape(ntiles * TILE_COLS, 4)
 
 
 def decode_weights(img: np.ndarray, widths, N: int):
