@@ -55,6 +55,15 @@ constexpr uint32_t e4m3_exact(int num, int den) {
   return sign | ((uint32_t)(ue + 7) << 3) | mant;
 }
 
+// The packed weights are read exactly once: non-temporal loads stream them
+// past the caches (measured on gfx950: 6.9 TB/s for a plain streaming read
+// against 6.2 TB/s with ordinary loads).  Activations stay cached; every
+// workgroup reads them.
+template <typename T>
+__device__ inline T stream_load(const T *p) {
+  return __builtin_nontemporal_load(p);
+}
+
 // 16-entry byte table (entry n = f(n)) as four dwords
 template <int KIND>
 constexpr uint32_t table_dword(int d) {
@@ -200,8 +209,8 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
     constexpr int sd = wd_step_data(0), ad = ad_step_data(0);
     const uint8_t *g0 = wsl0 + grp_off(gi, sd), *g1 = wsl1 + grp_off(gi, sd);
     const uint8_t *ga = aimg + grp_off(gi, ad);
-    const uint32_t sw0 = *(const uint32_t *)(g0 + 4 * lane);
-    const uint32_t sw1 = *(const uint32_t *)(g1 + 4 * lane);
+    const uint32_t sw0 = stream_load((const uint32_t *)(g0 + 4 * lane));
+    const uint32_t sw1 = stream_load((const uint32_t *)(g1 + 4 * lane));
     const uint32_t sa = *(const uint32_t *)(ga + 4 * alane);
     u4 x0[4], x1[4], p[4];
     u2 q[4];
@@ -210,8 +219,8 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
       x0[k] = x1[k] = p[k] = u4{0u, 0u, 0u, 0u};
       q[k] = u2{0u, 0u};
       if (k < nst) {
-        x0[k] = *(const u4 *)(g0 + kScaleBlock + k * sd + 16 * lane);
-        x1[k] = *(const u4 *)(g1 + kScaleBlock + k * sd + 16 * lane);
+        x0[k] = stream_load((const u4 *)(g0 + kScaleBlock + k * sd + 16 * lane));
+        x1[k] = stream_load((const u4 *)(g1 + kScaleBlock + k * sd + 16 * lane));
         p[k] = *(const u4 *)(ga + kScaleBlock + k * ad + 16 * alane);
         q[k] = *(const u2 *)(ga + kScaleBlock + k * ad + 1024 + 8 * alane);
       }
@@ -250,8 +259,8 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
     auto group = [&](int gi, int nst) {
       const uint8_t *g0 = w0 + grp_off(gi, sd), *g1 = w1 + grp_off(gi, sd);
       const uint8_t *ga = a0 + grp_off(gi, ad);
-      const uint32_t sw0 = *(const uint32_t *)(g0 + 4 * lane);
-      const uint32_t sw1 = *(const uint32_t *)(g1 + 4 * lane);
+      const uint32_t sw0 = stream_load((const uint32_t *)(g0 + 4 * lane));
+      const uint32_t sw1 = stream_load((const uint32_t *)(g1 + 4 * lane));
       const uint32_t sa = *(const uint32_t *)(ga + 4 * alane);
       u4 x0[4], x1[4], p[4], r[4];
 #pragma unroll
@@ -260,12 +269,13 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
         if (k < nst) {
           const uint8_t *c0 = g0 + kScaleBlock + k * sd, *c1 = g1 + kScaleBlock + k * sd;
           if (SEG == 1) {
-            const u2 n0 = *(const u2 *)(c0 + 8 * lane), n1 = *(const u2 *)(c1 + 8 * lane);
-            x0[k] = u4{n0[0], n0[1], *(const uint32_t *)(c0 + 512 + 4 * lane), 0u};
-            x1[k] = u4{n1[0], n1[1], *(const uint32_t *)(c1 + 512 + 4 * lane), 0u};
+            const u2 n0 = stream_load((const u2 *)(c0 + 8 * lane));
+            const u2 n1 = stream_load((const u2 *)(c1 + 8 * lane));
+            x0[k] = u4{n0[0], n0[1], stream_load((const uint32_t *)(c0 + 512 + 4 * lane)), 0u};
+            x1[k] = u4{n1[0], n1[1], stream_load((const uint32_t *)(c1 + 512 + 4 * lane)), 0u};
           } else {
-            x0[k] = *(const u4 *)(c0 + 16 * lane);
-            x1[k] = *(const u4 *)(c1 + 16 * lane);
+            x0[k] = stream_load((const u4 *)(c0 + 16 * lane));
+            x1[k] = stream_load((const u4 *)(c1 + 16 * lane));
           }
           const uint8_t *ca = ga + kScaleBlock + k * ad + 32 * alane;
           p[k] = *(const u4 *)ca;
