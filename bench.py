@@ -106,6 +106,52 @@ def burst_ms(fn, reps: int, warmup: int):
     return e0.elapsed_time(e1) / reps
 
 
+def peaks(dev, reps: int = 5):
+    """Achievable peaks on this machine: a streaming HBM read of 1 GiB and
+    register-resident matrix-core loops (int8, FP6, FP8)."""
+    import torch
+    from paper_2607_17733_amd import mxq
+    sink = mxq.peak_sink(dev)
+    buf = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    out = {}
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e-3
+
+    nbytes = buf.numel()
+    out["hbm_stream_read_GBps"] = nbytes / timed(lambda: mxq.peak_stream_read(buf, sink)) / 1e9
+    for kind in ("int8", "fp6", "fp8"):
+        ops = [0]
+
+        def run():
+            ops[0] = mxq.peak_mfma(kind, 400, sink)
+        t = timed(run)
+        out["mfma_%s_TOPs" % kind] = ops[0] / t / 1e12
+    del buf
+    return out
+
+
+def prefill_mfma_floor_us(meta, M: int, N: int, pk):
+    """The prefill GEMM's matrix-core time at the measured loop rates: per
+    32x32 output tile, 2 FP6 products per 4-bit step, 4 per 6-bit step and 2
+    FP8 products per 8-bit step (steps of 4, 2 and 1 blocks)."""
+    tiles = (M // 32) * (N // 32)
+    s4, s6, s8 = -(-meta["n4"] // 4), -(-meta["n6"] // 2), meta["n8"]
+    per = 2.0 * 32 * 32 * 64
+    n6 = tiles * (2 * s4 + 4 * s6)
+    n8 = tiles * 2 * s8
+    return (n6 * per / (pk["mfma_fp6_TOPs"] * 1e12) + n8 * per / (pk["mfma_fp8_TOPs"] * 1e12)) * 1e6
+
+
 def cpu_baseline(case, budget_s: float = 12.0):
     """The oracle, as it stands, on the host: quantize the whole activation
     matrix, then the blockwise GEMM on a sample of rows sized to the budget;
@@ -226,6 +272,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-layer", action="store_true")
+    ap.add_argument("--no-peaks", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 512 MiB device copy (counter scaling)")
     args = ap.parse_args()
@@ -351,10 +398,28 @@ def main():
                      "algorithmic_bytes": q_bytes},
         "pack_weights_ms": pack_ms,
     }
+    pk = None
+    if not args.no_peaks:
+        log("achievable peaks")
+        pk = peaks(dev)
+        floor = prefill_mfma_floor_us(case.meta, M, N, pk)
+        result["peaks"] = pk
+        result["roofline"]["achievable"] = {
+            "int8_loop_TOPs": pk["mfma_int8_TOPs"],
+            "frac_int8_loop": gemm_tops / pk["mfma_int8_TOPs"],
+            "kernel_mfma_floor_us": floor,
+            "frac_of_mfma_floor": floor / (gemm_ms * 1e3),
+        }
     if not args.no_decode:
         log("decode bench")
         result["decode"] = {"up": decode_bench(dev, "up"),
                             "down": decode_bench(dev, "down")}
+        if pk is not None:
+            for which in ("up", "down"):
+                for key, rec in result["decode"][which].items():
+                    if key.startswith("M"):
+                        rec["frac_achievable_hbm"] = (rec["packed_weight_GBps"] /
+                                                      pk["hbm_stream_read_GBps"])
     if not args.no_layer:
         log("layer sequence")
         result["layer"] = {"sensitive": layer_bench(dev, True),

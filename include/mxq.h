@@ -250,6 +250,30 @@ mxq_status mxq_gemm_partials(const mxq_fmt *fmt, int64_t M, int64_t N,
                              const uint8_t *w_mant, const uint8_t *w_exp,
                              int32_t *p, void *stream);
 
+/*
+ * Achievable-peak microbenchmarks, for the benchmark's roofline figures (not
+ * part of the quantize / GEMM path; the paper states no peaks, these price
+ * the kernels against what the same box reaches).
+ *   mxq_peak_sink_words: length, in 4-byte words, of the sink both take.
+ *   mxq_peak_stream_read: reads each of the `bytes` (a positive multiple of
+ *     16) of DEVICE buffer `buf` once, with 16-byte non-temporal loads;
+ *     `sink` DEVICE uint32 [mxq_peak_sink_words()], written (a checksum).
+ *   mxq_peak_mfma: register-resident matrix-core loop, `iters` products per
+ *     accumulator, eight accumulators per wave, sixteen waves per CU; kind
+ *     0 = dense int8 32x32x32, 1 = block-scaled FP6 e3m2 32x32x64, 2 =
+ *     block-scaled FP8 e4m3 32x32x64.  `*ops` (HOST) receives the
+ *     multiply-add ops (2 per product term) one launch performs; `sink`
+ *     DEVICE float [mxq_peak_sink_words()], written.
+ * Errors: MXQ_ERR_NULL (null pointer), MXQ_ERR_SHAPE (bytes not a positive
+ * multiple of 16, iters < 1, kind outside 0..2), MXQ_ERR_DEVICE (launch).
+ * Enqueued on `stream`; nothing is allocated.
+ */
+int64_t mxq_peak_sink_words(void);
+mxq_status mxq_peak_stream_read(const void *buf, int64_t bytes, uint32_t *sink,
+                                void *stream);
+mxq_status mxq_peak_mfma(int kind, int64_t iters, float *sink, int64_t *ops,
+                         void *stream);
+
 #ifdef __cplusplus
 }
 #endif

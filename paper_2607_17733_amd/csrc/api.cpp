@@ -304,4 +304,19 @@ mxq_status mxq_unpack_weights(const mxq_fmt *fmt, int64_t N, const uint8_t *w_ma
   return unpack_common(fmt, N, w_mant, w_exp, q, e, stream, true);
 }
 
+int64_t mxq_peak_sink_words(void) { return mxq::peak_sink_words(); }
+
+mxq_status mxq_peak_stream_read(const void *buf, int64_t bytes, uint32_t *sink, void *stream) {
+  if (!buf || !sink) return MXQ_ERR_NULL;
+  if (bytes <= 0 || bytes % 16) return MXQ_ERR_SHAPE;
+  return launched(mxq::launch_peak_stream(buf, bytes, sink, (hipStream_t)stream));
+}
+
+mxq_status mxq_peak_mfma(int kind, int64_t iters, float *sink, int64_t *ops, void *stream) {
+  if (!sink || !ops) return MXQ_ERR_NULL;
+  if (kind < 0 || kind > 2 || iters < 1) return MXQ_ERR_SHAPE;
+  *ops = mxq::peak_mfma_ops(kind, iters);
+  return launched(mxq::launch_peak_mfma(kind, iters, sink, (hipStream_t)stream));
+}
+
 }  // extern "C"

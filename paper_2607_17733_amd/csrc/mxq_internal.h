@@ -80,4 +80,10 @@ hipError_t launch_gemm_partials(const GemmArgs &args, hipStream_t s);
 hipError_t launch_gemm_decode(const GemmArgs &args, hipStream_t s);
 hipError_t launch_unpack(const UnpackArgs &args, bool weights, hipStream_t s);
 
+// Achievable-peak microbenchmarks (peaks.hip).
+int64_t peak_sink_words();
+int64_t peak_mfma_ops(int kind, int64_t iters);
+hipError_t launch_peak_stream(const void *buf, int64_t bytes, uint32_t *sink, hipStream_t s);
+hipError_t launch_peak_mfma(int kind, int64_t iters, float *sink, hipStream_t s);
+
 }  // namespace mxq

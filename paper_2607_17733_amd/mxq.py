@@ -48,6 +48,9 @@ _SIGS = {
     "mxq_gemm_partials": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P, _P, _P, _P]),
     "mxq_unpack_act": (ctypes.c_int, [_P, _I64, _P, _P, _P, _P, _P]),
     "mxq_unpack_weights": (ctypes.c_int, [_P, _I64, _P, _P, _P, _P, _P]),
+    "mxq_peak_sink_words": (_I64, []),
+    "mxq_peak_stream_read": (ctypes.c_int, [_P, _I64, _P, _P]),
+    "mxq_peak_mfma": (ctypes.c_int, [ctypes.c_int, _I64, _P, _P, _P]),
 }
 
 
@@ -225,3 +228,31 @@ def unpack_weights(w_mant, w_exp, fmt: Format, N: int):
     _check(lib().mxq_unpack_weights(fmt.ref, N, _ptr(w_mant), _ptr(w_exp), _ptr(q),
                                     _ptr(e), _stream()), "mxq_unpack_weights")
     return q, e
+
+
+# --------------------------------------------------------------------------
+# Achievable-peak microbenchmarks (measurement only)
+
+def peak_sink(device):
+    """A sink buffer large enough for the peak microbenchmarks."""
+    return torch.empty(int(lib().mxq_peak_sink_words()), dtype=torch.int32, device=device)
+
+
+def peak_stream_read(buf, sink):
+    """Read every byte of `buf` (a device tensor, nbytes % 16 == 0) once."""
+    nbytes = buf.numel() * buf.element_size()
+    _check(lib().mxq_peak_stream_read(_ptr(buf), nbytes, _ptr(sink), _stream()),
+           "mxq_peak_stream_read")
+    return nbytes
+
+
+PEAK_KINDS = {"int8": 0, "fp6": 1, "fp8": 2}
+
+
+def peak_mfma(kind: str, iters: int, sink):
+    """Matrix-core loop of `kind` ("int8", "fp6", "fp8"); returns the ops of
+    one launch."""
+    ops = ctypes.c_int64(0)
+    _check(lib().mxq_peak_mfma(PEAK_KINDS[kind], int(iters), _ptr(sink),
+                               ctypes.byref(ops), _stream()), "mxq_peak_mfma")
+    return ops.value

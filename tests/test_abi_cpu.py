@@ -145,3 +145,16 @@ def test_argument_validation_before_launch(lib):
     assert lib.mxq_gemm_partials(fr, 4, 4, p16, p16, p16, p16, bad, None) == 5
     assert lib.mxq_unpack_act(fr, 4, p16, p16, None, p16, None) == 1
     assert lib.mxq_status_str(5).decode().startswith("device pointer")
+
+
+def test_peak_microbenchmarks_validate_before_launch(lib):
+    from paper_2607_17733_amd.mxq import _SIGS  # noqa: F401  (signatures set by lib())
+    assert lib.mxq_peak_sink_words() >= 256 * 16 * 64
+    fake = ctypes.c_void_p(16)
+    ops = ctypes.c_int64(-1)
+    assert lib.mxq_peak_stream_read(None, 16, fake, None) == 1          # MXQ_ERR_NULL
+    assert lib.mxq_peak_stream_read(fake, 15, fake, None) == 2          # MXQ_ERR_SHAPE
+    assert lib.mxq_peak_stream_read(fake, 0, fake, None) == 2
+    assert lib.mxq_peak_mfma(3, 1, fake, ctypes.byref(ops), None) == 2
+    assert lib.mxq_peak_mfma(0, 0, fake, ctypes.byref(ops), None) == 2
+    assert lib.mxq_peak_mfma(0, 1, None, ctypes.byref(ops), None) == 1
