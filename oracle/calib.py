@@ -59,10 +59,13 @@ def ratio(d_in, s_layer, B: float) -> float:
     sum(2 * S_i * (d_i - 32)) for n layers of input widths d_i and layer
     sensitivities S_i, so that 32 8-bit columns per layer plus R * S_i *
     (d_i - 32) 6-bit columns average B bits."""
-    d = np.asarray(d_in, dtype=np.float64)
-    S = np.asarray(s_layer, dtype=np.float64)
-    n = len(d)
-    return ((B - 4.0) * d.sum() - 4.0 * BLOCK * n) / (2.0 * S * (d - BLOCK)).sum()
+    # plain sums in layer order (the allocation floors R * S * (d - 32), so
+    # the rounding order is part of the definition)
+    total, den = 0.0, 0.0
+    for d, S in zip(d_in, s_layer):
+        total += float(d)
+        den += 2.0 * float(S) * float(d - BLOCK)
+    return ((B - 4.0) * total - 4.0 * BLOCK * len(d_in)) / den
 
 
 def counts(d_in: int, R: float, s_layer: float, n8_blocks: int = 1):
