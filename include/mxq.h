@@ -251,6 +251,46 @@ mxq_status mxq_gemm_partials(const mxq_fmt *fmt, int64_t M, int64_t N,
                              int32_t *p, void *stream);
 
 /*
+ * Calibration: the offline step that produces a linear's permutation and
+ * width map from calibration activations (paper: Section 3, Algorithm 1;
+ * Section 4.2, Algorithm 2; Appendix A, Theorem A.1).
+ *   mxq_calib_colsq: column sensitivities of one calibration sample,
+ *     diag(X^T X): s[k] = sum over the rows of x[r][k]^2 in float64, the
+ *     rows summed in row order from zero; with `accumulate` the sample's sum
+ *     is added to s[k] (samples in call order), else it replaces it.
+ *     x DEVICE bf16 [rows][ldx], ldx >= K, read; s DEVICE double [K].
+ *   mxq_calib_ratio (HOST only): Theorem A.1's control parameter
+ *     R = ((B - 4) * sum d_i - 4 * 32 * n) / sum(2 * S_i * (d_i - 32)) for n
+ *     layers of input widths d_in[i] (multiples of 32) and layer
+ *     sensitivities s_layer[i], so that 32 8-bit columns per layer and
+ *     R * S_i * (d_i - 32) 6-bit ones average B bits.  Sums in layer order.
+ *   mxq_calib_counts (HOST only): Algorithm 2's split of a layer of d_in
+ *     columns into 32-column blocks: n8 = n8_blocks (the paper: 1), n6 =
+ *     floor(R * s_layer * (d_in - 32)) columns rounded down to whole blocks
+ *     and clamped to [0, d_in / 32 - n8], n4 the rest.
+ *   mxq_calib_perm: the permutation of Algorithm 2: columns sorted by
+ *     descending s (equal values in column order, NaN as +inf); the first
+ *     32 * n8_blocks are 8-bit, the next 32 * n6_blocks 6-bit, the rest
+ *     4-bit; perm lists the 4-bit columns, then the 6-bit, then the 8-bit,
+ *     each in sorted order, matching the width map [4]*n4 + [6]*n6 + [8]*n8.
+ *     s DEVICE double [K], read; perm DEVICE int32 [K], written; K a
+ *     multiple of 32.
+ * Errors: MXQ_ERR_NULL (null pointer), MXQ_ERR_SHAPE (rows < 0, K <= 0,
+ * ldx < K, widths not multiples of 32, block counts out of range, or a zero
+ * denominator in R), MXQ_ERR_DEVICE (launch).  Device work is enqueued on
+ * `stream`; nothing is allocated.
+ */
+mxq_status mxq_calib_colsq(const uint16_t *x, int64_t rows, int64_t ldx,
+                           int64_t K, double *s, int accumulate, void *stream);
+mxq_status mxq_calib_ratio(int32_t n, const int64_t *d_in,
+                           const double *s_layer, double B, double *R);
+mxq_status mxq_calib_counts(int64_t d_in, double R, double s_layer,
+                            int32_t n8_blocks, int32_t *n4, int32_t *n6,
+                            int32_t *n8);
+mxq_status mxq_calib_perm(const double *s, int64_t K, int32_t n6_blocks,
+                          int32_t n8_blocks, int32_t *perm, void *stream);
+
+/*
  * Achievable-peak microbenchmarks, for the benchmark's roofline figures (not
  * part of the quantize / GEMM path; the paper states no peaks, these price
  * the kernels against what the same box reaches).

@@ -4,6 +4,7 @@
 // synchronizes.
 #include <hip/hip_runtime.h>
 
+#include <math.h>
 #include <stdint.h>
 
 #include "../../include/mxq.h"
@@ -302,6 +303,54 @@ mxq_status mxq_unpack_act(const mxq_fmt *fmt, int64_t rows, const uint8_t *a_man
 mxq_status mxq_unpack_weights(const mxq_fmt *fmt, int64_t N, const uint8_t *w_mant,
                               const uint8_t *w_exp, int8_t *q, uint8_t *e, void *stream) {
   return unpack_common(fmt, N, w_mant, w_exp, q, e, stream, true);
+}
+
+mxq_status mxq_calib_colsq(const uint16_t *x, int64_t rows, int64_t ldx, int64_t K, double *s,
+                           int accumulate, void *stream) {
+  if (!x || !s) return MXQ_ERR_NULL;
+  if (rows < 0 || K <= 0 || ldx < K) return MXQ_ERR_SHAPE;
+  return launched(mxq::launch_calib_colsq(x, rows, ldx, K, s, accumulate != 0,
+                                          (hipStream_t)stream));
+}
+
+mxq_status mxq_calib_ratio(int32_t n, const int64_t *d_in, const double *s_layer, double B,
+                           double *R) {
+  if (!d_in || !s_layer || !R) return MXQ_ERR_NULL;
+  if (n < 1) return MXQ_ERR_SHAPE;
+  double total = 0.0, den = 0.0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (d_in[i] < 32 || d_in[i] % 32) return MXQ_ERR_SHAPE;
+    total += (double)d_in[i];
+    den += 2.0 * s_layer[i] * (double)(d_in[i] - 32);
+  }
+  if (!(den != 0.0)) return MXQ_ERR_SHAPE;   // every layer insensitive (or only 8-bit)
+  *R = ((B - 4.0) * total - 4.0 * 32.0 * (double)n) / den;
+  return MXQ_OK;
+}
+
+mxq_status mxq_calib_counts(int64_t d_in, double R, double s_layer, int32_t n8_blocks,
+                            int32_t *n4, int32_t *n6, int32_t *n8) {
+  if (!n4 || !n6 || !n8) return MXQ_ERR_NULL;
+  if (d_in < 32 || d_in % 32 || n8_blocks < 0) return MXQ_ERR_SHAPE;
+  const int64_t nb = d_in / 32;
+  const int64_t e = n8_blocks < nb ? n8_blocks : nb;
+  const double cols = floor(R * s_layer * (double)(d_in - 32));
+  int64_t six = 0;
+  if (cols > 0) six = cols >= (double)(nb * 32) ? nb : (int64_t)cols / 32;
+  if (six > nb - e) six = nb - e;
+  *n8 = (int32_t)e;
+  *n6 = (int32_t)six;
+  *n4 = (int32_t)(nb - e - six);
+  return MXQ_OK;
+}
+
+mxq_status mxq_calib_perm(const double *s, int64_t K, int32_t n6_blocks, int32_t n8_blocks,
+                          int32_t *perm, void *stream) {
+  if (!s || !perm) return MXQ_ERR_NULL;
+  if (K <= 0 || K % 32 || K > INT32_MAX || n6_blocks < 0 || n8_blocks < 0 ||
+      (int64_t)n6_blocks + n8_blocks > K / 32)
+    return MXQ_ERR_SHAPE;
+  return launched(mxq::launch_calib_perm(s, K, n6_blocks, n8_blocks, perm, (hipStream_t)stream));
 }
 
 int64_t mxq_peak_sink_words(void) { return mxq::peak_sink_words(); }

@@ -80,6 +80,12 @@ hipError_t launch_gemm_partials(const GemmArgs &args, hipStream_t s);
 hipError_t launch_gemm_decode(const GemmArgs &args, hipStream_t s);
 hipError_t launch_unpack(const UnpackArgs &args, bool weights, hipStream_t s);
 
+// Calibration (calib.hip).
+hipError_t launch_calib_colsq(const uint16_t *x, int64_t rows, int64_t ld, int64_t K, double *s,
+                              bool accumulate, hipStream_t s_);
+hipError_t launch_calib_perm(const double *s, int64_t K, int64_t n6, int64_t n8, int32_t *perm,
+                             hipStream_t stream);
+
 // Achievable-peak microbenchmarks (peaks.hip).
 int64_t peak_sink_words();
 int64_t peak_mfma_ops(int kind, int64_t iters);

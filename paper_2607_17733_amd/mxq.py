@@ -48,6 +48,11 @@ _SIGS = {
     "mxq_gemm_partials": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P, _P, _P, _P]),
     "mxq_unpack_act": (ctypes.c_int, [_P, _I64, _P, _P, _P, _P, _P]),
     "mxq_unpack_weights": (ctypes.c_int, [_P, _I64, _P, _P, _P, _P, _P]),
+    "mxq_calib_colsq": (ctypes.c_int, [_P, _I64, _I64, _I64, _P, ctypes.c_int, _P]),
+    "mxq_calib_ratio": (ctypes.c_int, [ctypes.c_int32, _P, _P, ctypes.c_double, _P]),
+    "mxq_calib_counts": (ctypes.c_int, [_I64, ctypes.c_double, ctypes.c_double,
+                                        ctypes.c_int32, _P, _P, _P]),
+    "mxq_calib_perm": (ctypes.c_int, [_P, _I64, ctypes.c_int32, ctypes.c_int32, _P, _P]),
     "mxq_peak_sink_words": (_I64, []),
     "mxq_peak_stream_read": (ctypes.c_int, [_P, _I64, _P, _P]),
     "mxq_peak_mfma": (ctypes.c_int, [ctypes.c_int, _I64, _P, _P, _P]),
@@ -256,3 +261,63 @@ def peak_mfma(kind: str, iters: int, sink):
     _check(lib().mxq_peak_mfma(PEAK_KINDS[kind], int(iters), _ptr(sink),
                                ctypes.byref(ops), _stream()), "mxq_peak_mfma")
     return ops.value
+
+
+# --------------------------------------------------------------------------
+# Calibration (offline): permutation and width map from calibration samples
+
+def calib_colsq(x, s=None, accumulate: bool = False):
+    """Column sensitivities of one calibration sample x (bf16 [rows, >=K]):
+    s[k] = sum_r x[r, k]^2 in float64 (added to s when accumulate)."""
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+        raise MxqError("calibration samples must be 2-D bf16 with unit column stride")
+    rows, K = x.shape
+    if s is None:
+        if accumulate:
+            raise MxqError("accumulate needs the running sensitivities")
+        s = torch.empty(K, dtype=torch.float64, device=x.device)
+    _check(lib().mxq_calib_colsq(_ptr(x), rows, x.stride(0), K, _ptr(s),
+                                 1 if accumulate else 0, _stream()), "mxq_calib_colsq")
+    return s
+
+
+def calib_ratio(d_in, s_layer, B: float) -> float:
+    """Theorem A.1's control parameter R for layers of widths d_in."""
+    n = len(d_in)
+    d = (ctypes.c_int64 * n)(*[int(v) for v in d_in])
+    sl = (ctypes.c_double * n)(*[float(v) for v in s_layer])
+    R = ctypes.c_double(0.0)
+    _check(lib().mxq_calib_ratio(n, d, sl, float(B), ctypes.byref(R)), "mxq_calib_ratio")
+    return R.value
+
+
+def calib_counts(d_in: int, R: float, s_layer: float, n8_blocks: int = 1):
+    """(n4, n6, n8) block counts of one layer (Algorithm 2)."""
+    out = [ctypes.c_int32(0) for _ in range(3)]
+    _check(lib().mxq_calib_counts(int(d_in), float(R), float(s_layer), int(n8_blocks),
+                                  *[ctypes.byref(v) for v in out]), "mxq_calib_counts")
+    return tuple(v.value for v in out)
+
+
+def calib_perm(s, n6: int, n8: int, perm=None):
+    """The permutation of Algorithm 2 (int32 device tensor [K])."""
+    if s.dtype != torch.float64 or s.dim() != 1:
+        raise MxqError("sensitivities must be a 1-D float64 tensor")
+    K = s.numel()
+    if perm is None:
+        perm = torch.empty(K, dtype=torch.int32, device=s.device)
+    _check(lib().mxq_calib_perm(_ptr(s), K, int(n6), int(n8), _ptr(perm), _stream()),
+           "mxq_calib_perm")
+    return perm
+
+
+def calibrate(samples, s_layer: float, R: float, n8_blocks: int = 1):
+    """One layer: sensitivities over the samples, the block counts and the
+    permutation.  Returns (perm int32 device tensor, widths list)."""
+    s = None
+    for i, x in enumerate(samples):
+        s = calib_colsq(x, s, accumulate=i > 0)
+    K = s.numel()
+    n4, n6, n8 = calib_counts(K, R, s_layer, n8_blocks)
+    perm = calib_perm(s, n6, n8)
+    return perm, [4] * n4 + [6] * n6 + [8] * n8
