@@ -152,6 +152,43 @@ def prefill_mfma_floor_us(meta, M: int, N: int, pk):
     return (n6 * per / (pk["mfma_fp6_TOPs"] * 1e12) + n8 * per / (pk["mfma_fp8_TOPs"] * 1e12)) * 1e6
 
 
+def calib_bench(dev, samples: int = 128, rows: int = 2048, K: int = 4096, reps: int = 3):
+    """Offline calibration of one attention-shape layer: column sensitivities
+    over `samples` calibration samples of `rows` tokens (the paper uses 128
+    samples), then the permutation; reported, not part of a step."""
+    import torch
+    from paper_2607_17733_amd import mxq
+    g = torch.Generator(device=dev)
+    g.manual_seed(1234)
+    x = torch.randn((samples, rows, K), generator=g, device=dev).to(torch.bfloat16)
+    work = torch.empty(samples * K, dtype=torch.float64, device=dev)
+    s = torch.empty(K, dtype=torch.float64, device=dev)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    ms = timed(lambda: mxq.calib_colsq_samples(x, s, work=work))
+    nbytes = x.numel() * 2
+    out = {"sensitivity_ms": ms, "sensitivity_GBps": nbytes / (ms * 1e-3) / 1e9,
+           "sensitivity_frac_hbm_peak": nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    del x, work
+    for kk in (4096, 28672):
+        sk = torch.rand(kk, generator=g, device=dev, dtype=torch.float64)
+        out["perm_K%d_us" % kk] = timed(lambda: mxq.calib_perm(sk, 2, 1)) * 1e3
+    out["workload"] = ("one layer, K=%d: %d samples x %d tokens bf16 (%.2f GB), then the "
+                       "permutation for K=4096 and K=28672" % (K, samples, rows, nbytes / 1e9))
+    return out
+
+
 def cpu_baseline(case, budget_s: float = 12.0):
     """The oracle, as it stands, on the host: quantize the whole activation
     matrix, then the blockwise GEMM on a sample of rows sized to the budget;
@@ -273,6 +310,7 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-layer", action="store_true")
     ap.add_argument("--no-peaks", action="store_true")
+    ap.add_argument("--no-calib", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 512 MiB device copy (counter scaling)")
     args = ap.parse_args()
@@ -410,6 +448,9 @@ def main():
             "kernel_mfma_floor_us": floor,
             "frac_of_mfma_floor": floor / (gemm_ms * 1e3),
         }
+    if not args.no_calib:
+        log("calibration")
+        result["calibration"] = calib_bench(dev)
     if not args.no_decode:
         log("decode bench")
         result["decode"] = {"up": decode_bench(dev, "up"),

@@ -259,6 +259,12 @@ mxq_status mxq_gemm_partials(const mxq_fmt *fmt, int64_t M, int64_t N,
  *     rows summed in row order from zero; with `accumulate` the sample's sum
  *     is added to s[k] (samples in call order), else it replaces it.
  *     x DEVICE bf16 [rows][ldx], ldx >= K, read; s DEVICE double [K].
+ *   mxq_calib_colsq_samples: the same for n_samples samples at once (sample
+ *     i at x + i * sample_stride elements, sample_stride >= rows * ldx):
+ *     each sample's sums go to row i of `work` (DEVICE double
+ *     [n_samples][K], caller-owned scratch), then are added to s in sample
+ *     order, so the result equals n_samples calls of mxq_calib_colsq.
+ *     n_samples in [1, 65535].
  *   mxq_calib_ratio (HOST only): Theorem A.1's control parameter
  *     R = ((B - 4) * sum d_i - 4 * 32 * n) / sum(2 * S_i * (d_i - 32)) for n
  *     layers of input widths d_in[i] (multiples of 32) and layer
@@ -282,6 +288,11 @@ mxq_status mxq_gemm_partials(const mxq_fmt *fmt, int64_t M, int64_t N,
  */
 mxq_status mxq_calib_colsq(const uint16_t *x, int64_t rows, int64_t ldx,
                            int64_t K, double *s, int accumulate, void *stream);
+mxq_status mxq_calib_colsq_samples(const uint16_t *x, int64_t n_samples,
+                                   int64_t rows, int64_t ldx,
+                                   int64_t sample_stride, int64_t K,
+                                   double *work, double *s, int accumulate,
+                                   void *stream);
 mxq_status mxq_calib_ratio(int32_t n, const int64_t *d_in,
                            const double *s_layer, double B, double *R);
 mxq_status mxq_calib_counts(int64_t d_in, double R, double s_layer,

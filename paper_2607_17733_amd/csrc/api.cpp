@@ -313,6 +313,17 @@ mxq_status mxq_calib_colsq(const uint16_t *x, int64_t rows, int64_t ldx, int64_t
                                           (hipStream_t)stream));
 }
 
+mxq_status mxq_calib_colsq_samples(const uint16_t *x, int64_t n_samples, int64_t rows,
+                                   int64_t ldx, int64_t sample_stride, int64_t K, double *work,
+                                   double *s, int accumulate, void *stream) {
+  if (!x || !s || !work) return MXQ_ERR_NULL;
+  if (n_samples < 1 || n_samples > 65535 || rows < 0 || K <= 0 || ldx < K ||
+      (n_samples > 1 && sample_stride < rows * ldx))
+    return MXQ_ERR_SHAPE;
+  return launched(mxq::launch_calib_colsq_samples(x, n_samples, rows, ldx, sample_stride, K,
+                                                  work, s, accumulate != 0, (hipStream_t)stream));
+}
+
 mxq_status mxq_calib_ratio(int32_t n, const int64_t *d_in, const double *s_layer, double B,
                            double *R) {
   if (!d_in || !s_layer || !R) return MXQ_ERR_NULL;

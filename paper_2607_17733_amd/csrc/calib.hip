@@ -53,6 +53,43 @@ __global__ __launch_bounds__(kCalThreads) void colsq_kernel(const uint16_t *__re
   s[k] = accumulate ? s[k] + part : part;
 }
 
+// Several samples at once (blockIdx.y = sample): each sample's sums, in row
+// order, go to its row of `part`; then the samples are added in order.
+__global__ __launch_bounds__(kCalThreads) void colsq_samples_kernel(
+    const uint16_t *__restrict__ x, int64_t rows, int64_t ld, int64_t sample_stride, int64_t K,
+    double *part) {
+  const int64_t k = (int64_t)blockIdx.x * kCalThreads + threadIdx.x;
+  if (k >= K) return;
+  const uint16_t *p = x + (int64_t)blockIdx.y * sample_stride + k;
+  double sum = 0.0;
+  int64_t r = 0;
+  for (; r + 8 <= rows; r += 8) {
+    uint16_t v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = p[(r + u) * ld];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const double d = bf16_to_f64(v[u]);
+      sum += d * d;
+    }
+  }
+  for (; r < rows; ++r) {
+    const double d = bf16_to_f64(p[r * ld]);
+    sum += d * d;
+  }
+  part[(int64_t)blockIdx.y * K + k] = sum;
+}
+
+__global__ __launch_bounds__(kCalThreads) void add_samples_kernel(const double *__restrict__ part,
+                                                                  int64_t n, int64_t K, double *s,
+                                                                  int accumulate) {
+  const int64_t k = (int64_t)blockIdx.x * kCalThreads + threadIdx.x;
+  if (k >= K) return;
+  double acc = accumulate ? s[k] + part[k] : part[k];
+  for (int64_t i = 1; i < n; ++i) acc = acc + part[i * K + k];
+  s[k] = acc;
+}
+
 __device__ inline double sort_key(double v) { return v != v ? __builtin_inf() : v; }
 
 __global__ __launch_bounds__(kCalThreads) void rank_perm_kernel(const double *__restrict__ s,
@@ -90,6 +127,19 @@ hipError_t launch_calib_colsq(const uint16_t *x, int64_t rows, int64_t ld, int64
   const int64_t blocks = (K + kCalThreads - 1) / kCalThreads;
   hipLaunchKernelGGL(colsq_kernel, dim3((unsigned)blocks), dim3(kCalThreads), 0, stream, x, rows,
                      ld, K, s, accumulate ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_calib_colsq_samples(const uint16_t *x, int64_t n, int64_t rows, int64_t ld,
+                                      int64_t sample_stride, int64_t K, double *part, double *s,
+                                      bool accumulate, hipStream_t stream) {
+  const int64_t blocks = (K + kCalThreads - 1) / kCalThreads;
+  hipLaunchKernelGGL(colsq_samples_kernel, dim3((unsigned)blocks, (unsigned)n), dim3(kCalThreads),
+                     0, stream, x, rows, ld, sample_stride, K, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(add_samples_kernel, dim3((unsigned)blocks), dim3(kCalThreads), 0, stream,
+                     part, n, K, s, accumulate ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -83,6 +83,9 @@ hipError_t launch_unpack(const UnpackArgs &args, bool weights, hipStream_t s);
 // Calibration (calib.hip).
 hipError_t launch_calib_colsq(const uint16_t *x, int64_t rows, int64_t ld, int64_t K, double *s,
                               bool accumulate, hipStream_t s_);
+hipError_t launch_calib_colsq_samples(const uint16_t *x, int64_t n, int64_t rows, int64_t ld,
+                                      int64_t sample_stride, int64_t K, double *part, double *s,
+                                      bool accumulate, hipStream_t stream);
 hipError_t launch_calib_perm(const double *s, int64_t K, int64_t n6, int64_t n8, int32_t *perm,
                              hipStream_t stream);
 

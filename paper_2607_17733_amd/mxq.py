@@ -49,6 +49,8 @@ _SIGS = {
     "mxq_unpack_act": (ctypes.c_int, [_P, _I64, _P, _P, _P, _P, _P]),
     "mxq_unpack_weights": (ctypes.c_int, [_P, _I64, _P, _P, _P, _P, _P]),
     "mxq_calib_colsq": (ctypes.c_int, [_P, _I64, _I64, _I64, _P, ctypes.c_int, _P]),
+    "mxq_calib_colsq_samples": (ctypes.c_int, [_P, _I64, _I64, _I64, _I64, _I64, _P, _P,
+                                               ctypes.c_int, _P]),
     "mxq_calib_ratio": (ctypes.c_int, [ctypes.c_int32, _P, _P, ctypes.c_double, _P]),
     "mxq_calib_counts": (ctypes.c_int, [_I64, ctypes.c_double, ctypes.c_double,
                                         ctypes.c_int32, _P, _P, _P]),
@@ -278,6 +280,24 @@ def calib_colsq(x, s=None, accumulate: bool = False):
         s = torch.empty(K, dtype=torch.float64, device=x.device)
     _check(lib().mxq_calib_colsq(_ptr(x), rows, x.stride(0), K, _ptr(s),
                                  1 if accumulate else 0, _stream()), "mxq_calib_colsq")
+    return s
+
+
+def calib_colsq_samples(x, s=None, accumulate: bool = False, work=None):
+    """Column sensitivities of a batch of samples x (bf16 [n, rows, >=K]),
+    summed in sample order (equal to one calib_colsq call per sample)."""
+    if x.dtype != torch.bfloat16 or x.dim() != 3 or x.stride(2) != 1:
+        raise MxqError("calibration samples must be 3-D bf16 with unit column stride")
+    n, rows, K = x.shape
+    if s is None:
+        if accumulate:
+            raise MxqError("accumulate needs the running sensitivities")
+        s = torch.empty(K, dtype=torch.float64, device=x.device)
+    if work is None:
+        work = torch.empty(n * K, dtype=torch.float64, device=x.device)
+    _check(lib().mxq_calib_colsq_samples(_ptr(x), n, rows, x.stride(1), x.stride(0), K,
+                                         _ptr(work), _ptr(s), 1 if accumulate else 0,
+                                         _stream()), "mxq_calib_colsq_samples")
     return s
 
 

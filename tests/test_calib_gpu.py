@@ -81,3 +81,20 @@ def test_calibrated_format_drives_the_path():
     qw, ew = oracle.quantize(w, perm=ref_perm, widths=ref_widths)
     yref = oracle.gemm(qa, ea, qw, ew, ref_widths)
     assert np.linalg.norm(y - yref) <= 1e-5 * np.linalg.norm(yref)
+
+
+@pytest.mark.parametrize("n,rows,K", [(1, 5, 64), (6, 37, 96), (16, 128, 4096)])
+def test_colsq_samples_equals_per_sample_calls(n, rows, K):
+    say("calib-colsq-samples", n, rows, K)
+    samples = _samples(n * 31 + rows, n, rows, K)
+    x = torch.stack([to_dev_bf16(b) for b in samples])
+    s0 = torch.from_numpy(np.arange(K, dtype=np.float64) * 0.5).cuda()
+    s = mxq.calib_colsq_samples(x, s0.clone(), accumulate=True)
+    torch.cuda.synchronize()
+    ref = np.arange(K, dtype=np.float64) * 0.5
+    for b in samples:
+        ref = ref + calib.sample_sensitivity(b)
+    assert np.array_equal(s.cpu().numpy(), ref)
+    s1 = mxq.calib_colsq_samples(x)
+    torch.cuda.synchronize()
+    assert np.array_equal(s1.cpu().numpy(), calib.column_sensitivity(samples))
