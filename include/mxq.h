@@ -202,6 +202,29 @@ mxq_status mxq_quantize_act(const mxq_fmt *fmt, const uint16_t *a, int64_t M,
                             void *stream);
 
 /*
+ * The activation quantizer fused with its producer, RMS normalisation (the
+ * paper keeps normalisation layers in 16-bit floating point, Appendix A.2,
+ * and quantizes the inputs of every decoder linear): the rows of x are
+ * normalised and then quantized exactly as mxq_quantize_act quantizes its
+ * input.  Per row, ms = sum of x^2 / K in float64 (each 32-element block in
+ * order, then the blocks in order); r = float32(1 / sqrt(ms + eps)) with the
+ * root and the division in IEEE float64; y = bf16(gain * bf16(x * r)) with
+ * float32 products and round-to-nearest-even.  The normalised rows are not
+ * written.
+ *   x     DEVICE bf16 [M][ldx], ldx >= K, read only.
+ *   gain  DEVICE bf16 [K], 16-byte aligned, read only.
+ *   eps   >= 0.
+ *   a_mant, a_exp as for mxq_quantize_act, written.
+ * Errors: as mxq_quantize_act, plus MXQ_ERR_NULL for a null gain and
+ * MXQ_ERR_SHAPE for a negative or NaN eps.
+ */
+mxq_status mxq_quantize_act_rmsnorm(const mxq_fmt *fmt, const uint16_t *x,
+                                    int64_t M, int64_t ldx,
+                                    const uint16_t *gain, float eps,
+                                    uint8_t *a_mant, uint8_t *a_exp,
+                                    void *stream);
+
+/*
  * Offline weight quantization and packing (same quantizer as the
  * activations; paper Section 5: weights of every decoder linear).
  *   w       DEVICE bf16 [N][ldw] (torch.nn.Linear layout: row j is output

@@ -81,7 +81,7 @@ mxq_status launched(hipError_t e) { return e == hipSuccess ? MXQ_OK : MXQ_ERR_DE
 
 mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows,
                            int64_t ld, uint8_t *mant, uint8_t *exp, void *stream,
-                           bool weights) {
+                           bool weights, const uint16_t *gain = nullptr, float eps = 0.f) {
   Segs s;
   mxq_status st = check_fmt(fmt, &s);
   if (st != MXQ_OK) return st;
@@ -89,7 +89,11 @@ mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows
   if (rows == 0) return MXQ_OK;
   if (!src || !mant || !exp) return MXQ_ERR_NULL;
   if (!aligned16(src) || !aligned16(mant) || !aligned16(exp)) return MXQ_ERR_ALIGN;
+  if (gain && !aligned16(gain)) return MXQ_ERR_ALIGN;
   mxq::QuantArgs a{};
+  a.rmsnorm = gain != nullptr;
+  a.gain = gain;
+  a.eps = eps;
   a.src = src;
   a.ld = ld;
   a.src_rows = rows;
@@ -120,7 +124,7 @@ mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows
     // the activation quantizer stages its rows in LDS: one row must fit
     const mxq::OpGeo og = op_geo(s);
     if (mxq::quantize_act_lds(fmt->K, og.n4p + og.n6p + og.n8 + (og.n8 & 1),
-                              fmt->perm != nullptr) > mxq::kMaxLds)
+                              fmt->perm != nullptr, gain != nullptr) > mxq::kMaxLds)
       return MXQ_ERR_UNSUPPORTED;
     return launched(mxq::launch_quantize_act(a, (hipStream_t)stream));
   }
@@ -233,6 +237,14 @@ mxq_status mxq_quantize_act(const mxq_fmt *fmt, const uint16_t *a, int64_t M,
                             int64_t lda, uint8_t *a_mant, uint8_t *a_exp,
                             void *stream) {
   return quantize_common(fmt, a, M, lda, a_mant, a_exp, stream, false);
+}
+
+mxq_status mxq_quantize_act_rmsnorm(const mxq_fmt *fmt, const uint16_t *x, int64_t M,
+                                    int64_t ldx, const uint16_t *gain, float eps,
+                                    uint8_t *a_mant, uint8_t *a_exp, void *stream) {
+  if (M > 0 && !gain) return MXQ_ERR_NULL;
+  if (!(eps >= 0.f)) return MXQ_ERR_SHAPE;
+  return quantize_common(fmt, x, M, ldx, a_mant, a_exp, stream, false, gain, eps);
 }
 
 mxq_status mxq_pack_weights(const mxq_fmt *fmt, const uint16_t *w, int64_t N,

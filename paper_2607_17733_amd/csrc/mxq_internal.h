@@ -35,6 +35,10 @@ struct QuantArgs {
   int vec16;               // 16-byte source loads are aligned
   int rows_per_wg;         // filled by the launcher
   int lg_rows;             // activations: log2 of the rows per group
+  // activations: RMS-normalise each row before quantizing (y = g * x / rms)
+  int rmsnorm;
+  const uint16_t *gain;    // bf16 [K]
+  float eps;
 };
 
 struct GemmArgs {
@@ -73,8 +77,8 @@ constexpr int64_t kMaxLds = 160 * 1024;   // LDS per workgroup on gfx950
 hipError_t launch_quantize(const QuantArgs &args, bool weights, hipStream_t s);
 int quantize_rows_per_wg(int64_t K);
 hipError_t launch_quantize_act(const QuantArgs &args, hipStream_t s);
-int quantize_act_rows(int64_t K, int padded_blocks, bool perm);
-int64_t quantize_act_lds(int64_t K, int padded_blocks, bool perm);
+int quantize_act_rows(int64_t K, int padded_blocks, bool perm, bool rmsnorm = false);
+int64_t quantize_act_lds(int64_t K, int padded_blocks, bool perm, bool rmsnorm = false);
 hipError_t launch_gemm_prefill(const GemmArgs &args, hipStream_t s);
 hipError_t launch_gemm_partials(const GemmArgs &args, hipStream_t s);
 hipError_t launch_gemm_decode(const GemmArgs &args, hipStream_t s);

@@ -283,6 +283,68 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
   }
 }
 
+__device__ inline float bf16f(uint32_t b) { return __uint_as_float(b << 16); }
+
+// float32 -> bf16 bits, round to nearest even (a NaN stays a quiet NaN)
+__device__ inline uint32_t to_bf16(float f) {
+  const uint32_t u = __float_as_uint(f);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// RMS normalisation of the R staged rows, in place (the fused producer of
+// the quantizer; Appendix A.2 keeps normalisation in 16-bit floating
+// point): per row, ms = sum of x^2 / K in float64 (each 32-element block
+// in order, then the blocks in order), r = float32(1 / sqrt(ms + eps)),
+// then y = bf16(g * bf16(x * r)) with float32 products.
+__device__ void rms_normalise(const QuantArgs &q, uint8_t *smem, int R, int rowB, int t,
+                              int nthr) {
+  const int K = (int)q.K, nbk = K / kBlock;
+  double *part = (double *)(smem + R * rowB);
+  float *rr = (float *)(part + R * nbk);
+  for (int it = t; it < R * nbk; it += nthr) {
+    const int lr = it / nbk, b = it - lr * nbk;
+    const u4 *xr = (const u4 *)(smem + lr * rowB + 64 * b);
+    double sum = 0.0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const u4 d = xr[u];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const double lo = (double)bf16f(d[j] & 0xFFFFu), hi = (double)bf16f(d[j] >> 16);
+        sum += lo * lo;
+        sum += hi * hi;
+      }
+    }
+    part[it] = sum;
+  }
+  __syncthreads();
+  if (t < R) {
+    double acc = 0.0;
+    for (int b = 0; b < nbk; ++b) acc += part[t * nbk + b];
+    rr[t] = (float)(1.0 / sqrt(acc / (double)K + (double)q.eps));
+  }
+  __syncthreads();
+  const int cpr = K / 8;                                 // 8-element chunks per row
+  for (int c = t; c < R * cpr; c += nthr) {
+    const int lr = c / cpr, k0 = (c - lr * cpr) * 8;
+    u4 *xp = (u4 *)(smem + lr * rowB + 2 * k0);
+    const u4 d = *xp;
+    const u4 gv = *(const u4 *)(q.gain + k0);
+    const float r = rr[lr];
+    u4 o;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t h0 = to_bf16(bf16f(d[j] & 0xFFFFu) * r), h1 = to_bf16(bf16f(d[j] >> 16) * r);
+      const uint32_t y0 = to_bf16(bf16f(gv[j] & 0xFFFFu) * bf16f(h0));
+      const uint32_t y1 = to_bf16(bf16f(gv[j] >> 16) * bf16f(h1));
+      o[j] = y0 | (y1 << 16);
+    }
+    *xp = o;
+  }
+  __syncthreads();
+}
+
 template <bool RNA>
 __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
@@ -345,6 +407,7 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
   }
   if (t < R) *(u4 *)(smem + t * rowB + 2 * K) = u4{0u, 0u, 0u, 0u};
   __syncthreads();
+  if (q.rmsnorm) rms_normalise(q, smem, R, rowB, t, nthr);
 
   for (int it = t; it < (nbp << lgR); it += nthr) {
     const int bp = it >> lgR;
@@ -374,24 +437,26 @@ int padded_blocks(int n4, int n6, int n8) {
 // Rows per workgroup: the largest power of two (at most 64) whose staged
 // rows fit the LDS budget with at most two items per thread.  More rows per
 // workgroup make longer contiguous runs in the operand tiles.
-int quantize_act_rows(int64_t K, int nbp, bool perm) {
+int quantize_act_rows(int64_t K, int nbp, bool perm, bool rmsnorm) {
   (void)perm;
-  const int64_t per = 2 * (K + kRowPad);
+  // a staged row, plus with RMS normalisation its block sums and its 1/rms
+  const int64_t per = 2 * (K + kRowPad) + (rmsnorm ? 8 * (K / kBlock) + 4 : 0);
   int r = 1;
   while (r < 64 && 2 * r * per <= kLdsBudget && (int64_t)nbp * 2 * r <= 2 * kMaxThreads)
     r *= 2;
   return r;
 }
 
-int64_t quantize_act_lds(int64_t K, int nbp, bool perm) {
-  return (int64_t)quantize_act_rows(K, nbp, perm) * 2 * (K + kRowPad);
+int64_t quantize_act_lds(int64_t K, int nbp, bool perm, bool rmsnorm) {
+  return (int64_t)quantize_act_rows(K, nbp, perm, rmsnorm) *
+         (2 * (K + kRowPad) + (rmsnorm ? 8 * (K / kBlock) + 4 : 0));
 }
 
 hipError_t launch_quantize_act(const QuantArgs &args, hipStream_t stream) {
   QuantArgs a = args;
   const bool perm = a.perm != nullptr;
   const int nbp = padded_blocks(a.n4, a.n6, a.n8);
-  const int R = quantize_act_rows(a.K, nbp, perm);
+  const int R = quantize_act_rows(a.K, nbp, perm, a.rmsnorm != 0);
   int lg = 0;
   while ((1 << lg) < R) ++lg;
   a.lg_rows = lg;
@@ -399,7 +464,7 @@ hipError_t launch_quantize_act(const QuantArgs &args, hipStream_t stream) {
   a.stage = 0;
   const int64_t grid = (a.out_rows + R - 1) / R;
   if (grid <= 0) return hipSuccess;
-  const int64_t lds = quantize_act_lds(a.K, nbp, perm);
+  const int64_t lds = quantize_act_lds(a.K, nbp, perm, a.rmsnorm != 0);
   if (lds > kMaxLds) return hipErrorInvalidValue;
   const int64_t items = (int64_t)nbp * R;
   const int threads = (int)(items >= kMaxThreads ? kMaxThreads : (items + 63) / 64 * 64);

@@ -43,6 +43,8 @@ _SIGS = {
     "mxq_weight_bytes": (_I64, [_P, _I64]),
     "mxq_weight_exp_bytes": (_I64, [_P, _I64]),
     "mxq_quantize_act": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P]),
+    "mxq_quantize_act_rmsnorm": (ctypes.c_int, [_P, _P, _I64, _I64, _P, ctypes.c_float,
+                                                 _P, _P, _P]),
     "mxq_pack_weights": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P]),
     "mxq_gemm": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P, _P, _P, _I64, _P]),
     "mxq_gemm_partials": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P, _P, _P, _P]),
@@ -174,6 +176,24 @@ def quantize_act(a, fmt: Format, out=None):
             raise MxqError("activation output buffers are too small")
     _check(lib().mxq_quantize_act(fmt.ref, _ptr(a), M, a.stride(0), _ptr(mant),
                                   _ptr(exp), _stream()), "mxq_quantize_act")
+    return mant, exp
+
+
+def quantize_act_rmsnorm(x, gain, eps: float, fmt: Format, out=None):
+    """RMS-normalise bf16 rows x with bf16 gain, then quantize them (one
+    kernel; the normalised rows are never written)."""
+    _bf16_2d(x, fmt.K, "activations")
+    if gain.dtype != torch.bfloat16 or gain.numel() < fmt.K or not gain.is_contiguous():
+        raise MxqError("gain must be a contiguous bf16 tensor of K elements")
+    M = x.shape[0]
+    if out is None:
+        mant = torch.empty(fmt.act_bytes(M), dtype=torch.uint8, device=x.device)
+        exp = torch.empty(fmt.act_exp_bytes(M), dtype=torch.uint8, device=x.device)
+    else:
+        mant, exp = out
+    _check(lib().mxq_quantize_act_rmsnorm(fmt.ref, _ptr(x), M, x.stride(0), _ptr(gain),
+                                          float(eps), _ptr(mant), _ptr(exp), _stream()),
+           "mxq_quantize_act_rmsnorm")
     return mant, exp
 
 
