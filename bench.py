@@ -189,6 +189,35 @@ def calib_bench(dev, samples: int = 128, rows: int = 2048, K: int = 4096, reps: 
     return out
 
 
+def fused_bench(dev, case, fmt, reps: int = 50):
+    """RMS normalisation fused into the quantizer against the two-kernel
+    path (torch's RMS normalisation to bf16, then the quantizer) on the
+    attention shape."""
+    import torch
+    import torch.nn.functional as F
+    from paper_2607_17733_amd import mxq
+    M, K = case.M, case.K
+    x = bf16_dev(case.a_bits, dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(4321)
+    gain = (torch.rand(K, generator=g, device=dev) + 0.5).to(torch.bfloat16)
+    am = torch.empty(fmt.act_bytes(M), dtype=torch.uint8, device=dev)
+    ae = torch.empty(fmt.act_exp_bytes(M), dtype=torch.uint8, device=dev)
+
+    def fused():
+        mxq.quantize_act_rmsnorm(x, gain, 1e-5, fmt, out=(am, ae))
+
+    def unfused():
+        mxq.quantize_act(F.rms_norm(x, (K,), gain, 1e-5), fmt, out=(am, ae))
+
+    out = {"fused_us": burst_ms(fused, reps, 10) * 1e3,
+           "unfused_us": burst_ms(unfused, reps, 10) * 1e3}
+    out["saved_bytes"] = 2 * 2 * M * K            # the normalised rows, written and read back
+    out["workload"] = ("RMS normalisation + quantize, M=%d K=%d; unfused = torch rms_norm "
+                       "to bf16, then mxq_quantize_act" % (M, K))
+    return out
+
+
 def cpu_baseline(case, budget_s: float = 12.0):
     """The oracle, as it stands, on the host: quantize the whole activation
     matrix, then the blockwise GEMM on a sample of rows sized to the budget;
@@ -311,6 +340,7 @@ def main():
     ap.add_argument("--no-layer", action="store_true")
     ap.add_argument("--no-peaks", action="store_true")
     ap.add_argument("--no-calib", action="store_true")
+    ap.add_argument("--no-fused", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 512 MiB device copy (counter scaling)")
     args = ap.parse_args()
@@ -448,6 +478,9 @@ def main():
             "kernel_mfma_floor_us": floor,
             "frac_of_mfma_floor": floor / (gemm_ms * 1e3),
         }
+    if not args.no_fused:
+        log("fused normalisation + quantize")
+        result["fused_rmsnorm_quantize"] = fused_bench(dev, case, fmt)
     if not args.no_calib:
         log("calibration")
         result["calibration"] = calib_bench(dev)
