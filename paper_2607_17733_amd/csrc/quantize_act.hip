@@ -285,11 +285,10 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
 
 __device__ inline float bf16f(uint32_t b) { return __uint_as_float(b << 16); }
 
-// float32 -> bf16 bits, round to nearest even (a NaN stays a quiet NaN)
+// float32 -> bf16 bits, round to nearest even (gfx950 converts a pair per
+// instruction; a NaN stays a NaN)
 __device__ inline uint32_t to_bf16(float f) {
-  const uint32_t u = __float_as_uint(f);
-  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
 // RMS normalisation of the R staged rows, in place (the fused producer of
@@ -320,8 +319,19 @@ __device__ void rms_normalise(const QuantArgs &q, uint8_t *smem, int R, int rowB
   }
   __syncthreads();
   if (t < R) {
+    // the block sums in order; loaded sixteen at a time so that only the
+    // additions form the dependent chain
+    const double *pp = part + t * nbk;
     double acc = 0.0;
-    for (int b = 0; b < nbk; ++b) acc += part[t * nbk + b];
+    int b = 0;
+    for (; b + 16 <= nbk; b += 16) {
+      double v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v[u] = pp[b + u];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) acc += v[u];
+    }
+    for (; b < nbk; ++b) acc += pp[b];
     rr[t] = (float)(1.0 / sqrt(acc / (double)K + (double)q.eps));
   }
   __syncthreads();
