@@ -60,3 +60,54 @@ def rmsnorm_bf16(x_bits, g_bits, eps) -> np.ndarray:
     h = f32_to_bf16(x32 * r[:, None])                         # float32 products
     g32 = bf16_to_f32(np.asarray(g_bits, dtype=np.uint16))
     return f32_to_bf16(g32[None, :] * bf16_to_f32(h))
+
+
+# --------------------------------------------------------------------------
+# SiLU(gate) * up before the quantizer (the down projection's producer)
+#
+# Reading: the exponential is not left to a math library, whose last-bit
+# results differ between machines; it is a fixed float32 evaluation, the
+# classic Cody-Waite reduction and a Taylor polynomial, with every operation
+# an IEEE float32 operation rounded on its own (no fused multiply-add):
+#   t  = clamp(t, -120, 120)
+#   k  = rint(t * (1/ln2))                     (float32 1/ln2 = 0x3FB8AA3B)
+#   r  = (t - k * LN2_HI) - k * LN2_LO         (0x3F317200, 0x35BFBE8E)
+#   p  = Horner over 1, 1, 1/2!, ..., 1/7! (float32 coefficients)
+#   e^t = ldexp(p, k)
+# silu(g) = g / (1 + e^(-g)); a = bf16(silu(g)); y = bf16(a * u), float32
+# products and round-to-nearest-even; a NaN gate gives a NaN.
+
+F32 = np.float32
+INV_LN2 = np.uint32(0x3FB8AA3B).view(np.float32)
+LN2_HI = np.uint32(0x3F317200).view(np.float32)
+LN2_LO = np.uint32(0x35BFBE8E).view(np.float32)
+EXP_COEF = [np.uint32(v).view(np.float32) for v in
+            (0x39500D01, 0x3AB60B61, 0x3C088889, 0x3D2AAAAB, 0x3E2AAAAB, 0x3F000000,
+             0x3F800000, 0x3F800000)]                # 1/7!, 1/6!, ..., 1/2!, 1, 1
+
+
+def exp32(t) -> np.ndarray:
+    """e^t as defined above (a NaN argument is not defined here; silu32
+    handles it)."""
+    t = np.asarray(t, dtype=F32)
+    t = np.clip(np.where(np.isnan(t), F32(0.0), t), F32(-120.0), F32(120.0))
+    k = np.rint(t * INV_LN2).astype(F32)
+    r = (t - k * LN2_HI) - k * LN2_LO
+    p = np.full_like(r, EXP_COEF[0])
+    for c in EXP_COEF[1:]:
+        p = p * r + c
+    with np.errstate(over="ignore"):
+        return np.ldexp(p, k.astype(np.int32)).astype(F32)
+
+
+def silu32(g) -> np.ndarray:
+    g = np.asarray(g, dtype=F32)
+    with np.errstate(over="ignore"):
+        s = g / (F32(1.0) + exp32(-g))
+    return np.where(np.isnan(g), F32(np.nan), s).astype(F32)
+
+
+def swiglu_bf16(g_bits, u_bits) -> np.ndarray:
+    """bf16(bf16(silu(g)) * u) as bf16 bits."""
+    a = f32_to_bf16(silu32(bf16_to_f32(g_bits)))
+    return f32_to_bf16(bf16_to_f32(a) * bf16_to_f32(u_bits))
