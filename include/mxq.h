@@ -225,6 +225,26 @@ mxq_status mxq_quantize_act_rmsnorm(const mxq_fmt *fmt, const uint16_t *x,
                                     void *stream);
 
 /*
+ * The activation quantizer fused with the down projection's producer,
+ * SiLU(gate) * up: the rows y = bf16(bf16(silu(g)) * u) (float32 product,
+ * round-to-nearest-even) are quantized exactly as mxq_quantize_act
+ * quantizes its input, without being written.  silu(g) = g / (1 + e^-g) in
+ * float32 with a fixed evaluation of e^t, so that every machine gets the same
+ * bits: t clamped to [-120, 120], k = rint(t * 0x3FB8AA3B), r = (t - k *
+ * 0x3F317200) - k * 0x35BFBE8E (float32 bit patterns of 1/ln2 and of ln2
+ * split in two), the degree-7 Taylor polynomial of e^r by Horner's rule,
+ * then 2^k; every operation rounded on its own, no fused multiply-add.  A
+ * NaN gate gives a NaN.
+ *   gate, up  DEVICE bf16 [M][ld], ld >= K, 16-byte aligned, read only.
+ *   a_mant, a_exp as for mxq_quantize_act, written.
+ * Errors: as mxq_quantize_act, plus MXQ_ERR_NULL for a null up.
+ */
+mxq_status mxq_quantize_act_swiglu(const mxq_fmt *fmt, const uint16_t *gate,
+                                   const uint16_t *up, int64_t M, int64_t ld,
+                                   uint8_t *a_mant, uint8_t *a_exp,
+                                   void *stream);
+
+/*
  * Offline weight quantization and packing (same quantizer as the
  * activations; paper Section 5: weights of every decoder linear).
  *   w       DEVICE bf16 [N][ldw] (torch.nn.Linear layout: row j is output

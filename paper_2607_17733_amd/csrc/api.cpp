@@ -81,7 +81,8 @@ mxq_status launched(hipError_t e) { return e == hipSuccess ? MXQ_OK : MXQ_ERR_DE
 
 mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows,
                            int64_t ld, uint8_t *mant, uint8_t *exp, void *stream,
-                           bool weights, const uint16_t *gain = nullptr, float eps = 0.f) {
+                           bool weights, const uint16_t *gain = nullptr, float eps = 0.f,
+                           const uint16_t *src2 = nullptr) {
   Segs s;
   mxq_status st = check_fmt(fmt, &s);
   if (st != MXQ_OK) return st;
@@ -90,10 +91,13 @@ mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows
   if (!src || !mant || !exp) return MXQ_ERR_NULL;
   if (!aligned16(src) || !aligned16(mant) || !aligned16(exp)) return MXQ_ERR_ALIGN;
   if (gain && !aligned16(gain)) return MXQ_ERR_ALIGN;
+  if (src2 && !aligned16(src2)) return MXQ_ERR_ALIGN;
   mxq::QuantArgs a{};
   a.rmsnorm = gain != nullptr;
   a.gain = gain;
   a.eps = eps;
+  a.swiglu = src2 != nullptr;
+  a.src2 = src2;
   a.src = src;
   a.ld = ld;
   a.src_rows = rows;
@@ -245,6 +249,13 @@ mxq_status mxq_quantize_act_rmsnorm(const mxq_fmt *fmt, const uint16_t *x, int64
   if (M > 0 && !gain) return MXQ_ERR_NULL;
   if (!(eps >= 0.f)) return MXQ_ERR_SHAPE;
   return quantize_common(fmt, x, M, ldx, a_mant, a_exp, stream, false, gain, eps);
+}
+
+mxq_status mxq_quantize_act_swiglu(const mxq_fmt *fmt, const uint16_t *gate,
+                                   const uint16_t *up, int64_t M, int64_t ld,
+                                   uint8_t *a_mant, uint8_t *a_exp, void *stream) {
+  if (M > 0 && !up) return MXQ_ERR_NULL;
+  return quantize_common(fmt, gate, M, ld, a_mant, a_exp, stream, false, nullptr, 0.f, up);
 }
 
 mxq_status mxq_pack_weights(const mxq_fmt *fmt, const uint16_t *w, int64_t N,

@@ -39,6 +39,9 @@ struct QuantArgs {
   int rmsnorm;
   const uint16_t *gain;    // bf16 [K]
   float eps;
+  // activations: the rows are SiLU(src) * src2 (gate and up, same layout)
+  int swiglu;
+  const uint16_t *src2;
 };
 
 struct GemmArgs {

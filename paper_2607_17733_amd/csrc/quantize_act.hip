@@ -291,6 +291,46 @@ __device__ inline uint32_t to_bf16(float f) {
   return __builtin_bit_cast(uint16_t, (__bf16)f);
 }
 
+// e^t in float32, evaluated the same way on every machine: the Cody-Waite
+// reduction t = k ln2 + r (ln2 split in two so that k * LN2_HI is exact)
+// and the Taylor polynomial of e^r to degree 7 (|r| <= ln2 / 2), every
+// operation rounded on its own (no fused multiply-add); then 2^k exactly.
+__device__ inline float exp32(float t) {
+#pragma clang fp contract(off)
+  constexpr float kInvLn2 = __builtin_bit_cast(float, 0x3FB8AA3Bu);
+  constexpr float kLn2Hi = __builtin_bit_cast(float, 0x3F317200u);
+  constexpr float kLn2Lo = __builtin_bit_cast(float, 0x35BFBE8Eu);
+  t = fminf(fmaxf(t, -120.f), 120.f);
+  const float k = rintf(t * kInvLn2);
+  const float r = (t - k * kLn2Hi) - k * kLn2Lo;
+  float p = __builtin_bit_cast(float, 0x39500D01u);                  // 1/7!
+  p = p * r + __builtin_bit_cast(float, 0x3AB60B61u);                // 1/6!
+  p = p * r + __builtin_bit_cast(float, 0x3C088889u);                // 1/5!
+  p = p * r + __builtin_bit_cast(float, 0x3D2AAAABu);                // 1/4!
+  p = p * r + __builtin_bit_cast(float, 0x3E2AAAABu);                // 1/3!
+  p = p * r + 0.5f;
+  p = p * r + 1.f;
+  p = p * r + 1.f;
+  return ldexpf(p, (int)k);
+}
+
+// bf16 bits of bf16(silu(g)) * u (float32 product, nearest-even), with
+// silu(g) = g / (1 + e^-g) (the producer of the down projection's input)
+__device__ inline uint32_t swiglu1(uint32_t g, uint32_t u) {
+#pragma clang fp contract(off)
+  const float gf = bf16f(g);
+  const float s = gf != gf ? __builtin_nanf("") : gf / (1.f + exp32(-gf));
+  return to_bf16(bf16f(to_bf16(s)) * bf16f(u));
+}
+
+__device__ inline u4 swiglu8(u4 g, u4 u) {
+  u4 o;
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    o[j] = swiglu1(g[j] & 0xFFFFu, u[j] & 0xFFFFu) | (swiglu1(g[j] >> 16, u[j] >> 16) << 16);
+  return o;
+}
+
 // RMS normalisation of the R staged rows, in place (the fused producer of
 // the quantizer; Appendix A.2 keeps normalisation in 16-bit floating
 // point): per row, ms = sum of x^2 / K in float64 (each 32-element block
@@ -392,8 +432,10 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
         lrk[k] = lr;
         ck[k] = c;
         d[k] = u4{0u, 0u, 0u, 0u};
-        if (v0 + k * nthr < nv && r0 + lr < q.src_rows)
+        if (v0 + k * nthr < nv && r0 + lr < q.src_rows) {
           d[k] = *(const u4 *)(q.src + (r0 + lr) * q.ld + 8 * c);
+          if (q.swiglu) d[k] = swiglu8(d[k], *(const u4 *)(q.src2 + (r0 + lr) * q.ld + 8 * c));
+        }
         c += dr;
         lr += dq;
         if (c >= vpr) {
@@ -411,8 +453,11 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
     for (int lr = 0; lr < R; ++lr) {
       const bool live = r0 + lr < q.src_rows;
       const uint16_t *src = q.src + (r0 + lr) * q.ld;
-      for (int c = t; c < K; c += nthr)
-        *(uint16_t *)(smem + lr * rowB + 2 * c) = live ? src[c] : (uint16_t)0;
+      for (int c = t; c < K; c += nthr) {
+        uint32_t v = live ? src[c] : 0u;
+        if (live && q.swiglu) v = swiglu1(v, q.src2[(r0 + lr) * q.ld + c]);
+        *(uint16_t *)(smem + lr * rowB + 2 * c) = (uint16_t)v;
+      }
     }
   }
   if (t < R) *(u4 *)(smem + t * rowB + 2 * K) = u4{0u, 0u, 0u, 0u};

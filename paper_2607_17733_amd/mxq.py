@@ -45,6 +45,7 @@ _SIGS = {
     "mxq_quantize_act": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P]),
     "mxq_quantize_act_rmsnorm": (ctypes.c_int, [_P, _P, _I64, _I64, _P, ctypes.c_float,
                                                  _P, _P, _P]),
+    "mxq_quantize_act_swiglu": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _P, _P, _P]),
     "mxq_pack_weights": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P]),
     "mxq_gemm": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P, _P, _P, _I64, _P]),
     "mxq_gemm_partials": (ctypes.c_int, [_P, _I64, _I64, _P, _P, _P, _P, _P, _P]),
@@ -194,6 +195,25 @@ def quantize_act_rmsnorm(x, gain, eps: float, fmt: Format, out=None):
     _check(lib().mxq_quantize_act_rmsnorm(fmt.ref, _ptr(x), M, x.stride(0), _ptr(gain),
                                           float(eps), _ptr(mant), _ptr(exp), _stream()),
            "mxq_quantize_act_rmsnorm")
+    return mant, exp
+
+
+def quantize_act_swiglu(gate, up, fmt: Format, out=None):
+    """Quantize SiLU(gate) * up (bf16 rows of the same shape and stride) in
+    one kernel; the product rows are never written."""
+    _bf16_2d(gate, fmt.K, "gate")
+    _bf16_2d(up, fmt.K, "up")
+    if up.shape != gate.shape or up.stride() != gate.stride():
+        raise MxqError("gate and up must have the same shape and strides")
+    M = gate.shape[0]
+    if out is None:
+        mant = torch.empty(fmt.act_bytes(M), dtype=torch.uint8, device=gate.device)
+        exp = torch.empty(fmt.act_exp_bytes(M), dtype=torch.uint8, device=gate.device)
+    else:
+        mant, exp = out
+    _check(lib().mxq_quantize_act_swiglu(fmt.ref, _ptr(gate), _ptr(up), M, gate.stride(0),
+                                         _ptr(mant), _ptr(exp), _stream()),
+           "mxq_quantize_act_swiglu")
     return mant, exp
 
 

@@ -58,3 +58,36 @@ def test_fused_equals_unfused_on_device():
     rb, erb = fmt.act_packed_bytes(), fmt.exp_row_bytes()
     assert torch.equal(am[:64 * rb], bm[:64 * rb])
     assert torch.equal(ae[:64 * erb], be[:64 * erb])
+
+
+SWIGLU_SHAPES = [
+    # M, K, N, (n4, n6, n8), perm
+    (1, 64, 32, (1, 0, 1), "random"),
+    (5, 256, 64, (6, 1, 1), "scales"),
+    (37, 1024, 96, (25, 5, 2), "identity"),
+    (300, 4096, 128, (102, 13, 13), "scales"),
+    (40, 28672, 64, (761, 90, 45), "random"),
+]
+
+
+@pytest.mark.parametrize("M,K,N,counts,perm", SWIGLU_SHAPES)
+def test_fused_swiglu_quantize(M, K, N, counts, perm):
+    say("fused-swiglu", M, K, N, counts, perm)
+    case = W.random_case(M * 29 + K, M, K, N, counts, perm=perm)
+    g = np.random.Generator(np.random.PCG64(K * 3 + M))
+    gate = g.normal(size=(M, K)) * 4
+    gate.flat[g.choice(M * K, size=min(64, M * K), replace=False)] = g.choice(
+        [-1000.0, -150.0, -90.0, 90.0, 150.0, 1000.0], size=min(64, M * K))
+    gate = fused.f32_to_bf16(gate.astype(np.float32))
+    up = fused.f32_to_bf16((g.normal(size=(M, K)) * g.uniform(0.5, 20, size=K)).astype(np.float32))
+    fmt = fmt_for(case)
+    am, ae = mxq.quantize_act_swiglu(to_dev_bf16(gate), to_dev_bf16(up), fmt)
+    wm, we = mxq.pack_weights(to_dev_bf16(case.w_bits), fmt)
+    y = mxq.gemm(am, ae, wm, we, fmt, M, N)
+    torch.cuda.synchronize()
+    act = fused.swiglu_bf16(gate, up)
+    qa, ea = oracle.quantize(act, perm=case.perm, widths=case.widths)
+    qw, ew = oracle.quantize(case.w_bits, perm=case.perm, widths=case.widths)
+    check_quant_act(case, {"a_mant": am, "a_exp": ae}, qa, ea, fmt)
+    Yref = oracle.gemm(qa, ea, qw, ew, case.widths)
+    check_gemm(y.cpu().numpy(), Yref, qa, ea, qw, ew, case.widths, case.name + "-swiglu")
