@@ -218,6 +218,38 @@ def fused_bench(dev, case, fmt, reps: int = 50):
     return out
 
 
+def swiglu_bench(dev, M: int = 2048, K: int = 28672, reps: int = 20):
+    """SiLU(gate)*up fused into the quantizer against torch's SiLU and product
+    followed by the quantizer, at the down projection's K (LLaMA-2-70B)."""
+    import numpy as np
+    import torch
+    import torch.nn.functional as F
+    from paper_2607_17733_amd import mxq
+    from paper_2607_17733_amd import workloads as W
+    case = W.decode(16, "down")                 # K = 28672 and its width map
+    fmt = mxq.Format(case.K, case.widths, torch.from_numpy(case.perm).to(dev))
+    g = torch.Generator(device=dev)
+    g.manual_seed(99)
+    gate = (torch.randn((M, K), generator=g, device=dev) * 3).to(torch.bfloat16)
+    up = torch.randn((M, K), generator=g, device=dev).to(torch.bfloat16)
+    am = torch.empty(fmt.act_bytes(M), dtype=torch.uint8, device=dev)
+    ae = torch.empty(fmt.act_exp_bytes(M), dtype=torch.uint8, device=dev)
+
+    def fused():
+        mxq.quantize_act_swiglu(gate, up, fmt, out=(am, ae))
+
+    def unfused():
+        mxq.quantize_act(F.silu(gate) * up, fmt, out=(am, ae))
+
+    out = {"fused_us": burst_ms(fused, reps, 5) * 1e3,
+           "unfused_us": burst_ms(unfused, reps, 5) * 1e3,
+           "saved_bytes": 2 * 2 * M * K,
+           "workload": "SiLU(gate)*up + quantize, M=%d K=%d (widths %d/%d/%d); unfused = "
+                       "torch silu(gate)*up in bf16, then mxq_quantize_act" % (
+                           M, K, case.meta["n4"], case.meta["n6"], case.meta["n8"])}
+    return out
+
+
 def cpu_baseline(case, budget_s: float = 12.0):
     """The oracle, as it stands, on the host: quantize the whole activation
     matrix, then the blockwise GEMM on a sample of rows sized to the budget;
@@ -481,6 +513,7 @@ def main():
     if not args.no_fused:
         log("fused normalisation + quantize")
         result["fused_rmsnorm_quantize"] = fused_bench(dev, case, fmt)
+        result["fused_swiglu_quantize"] = swiglu_bench(dev)
     if not args.no_calib:
         log("calibration")
         result["calibration"] = calib_bench(dev)
