@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define MXQ_ABI_VERSION 7
+#define MXQ_ABI_VERSION 8
 #define MXQ_BLOCK 32
 /* mxq_gemm uses the weight-streaming decode kernel for M <= this. */
 #define MXQ_DECODE_MAX_M 16
@@ -367,6 +367,49 @@ mxq_status mxq_peak_stream_read(const void *buf, int64_t bytes, uint32_t *sink,
                                 void *stream);
 mxq_status mxq_peak_mfma(int kind, int64_t iters, float *sink, int64_t *ops,
                          void *stream);
+
+/*
+ * Decode attention over an MXINT KV cache (MXSens Appendix A.2: K and V are
+ * quantized to MXINT with 32-element blocks along the head dimension, 4 to 8
+ * bits per block, and attention reads them).  One new token per sequence:
+ * for sequence b and query head h, with KV head k = h / G (G = Hq / Hkv),
+ *   s_t = scale * sum_d q[b][h][d] * K[b][t][k][d]   (t = 0..T-1),
+ *   o[b][h][d] = sum_t softmax(s)_t * V[b][t][k][d],
+ * where K and V are the dequantized cache values q * 2^(E - 127 - (m - 2)).
+ * Arithmetic is float32: each block's dot product, then its scale; an
+ * online softmax over chunks of 64 tokens; partial results merged in a
+ * fixed order, so repeated calls give identical results.
+ *   fmt     the cache format: K = 128 (the head dimension), perm NULL,
+ *           widths as for mxq_quantize_act (round and clamp do not matter
+ *           here).
+ *   q       DEVICE bf16 [B][Hq][128], read only.
+ *   B >= 0 (0: nothing to do), Hkv >= 1, Hq a multiple of Hkv with
+ *   Hq / Hkv <= 16, T >= 1.
+ *   scale   finite (usually 1 / sqrt(128)).
+ *   k_mant, v_mant   DEVICE, 16-byte aligned: packed rows of
+ *           mxq_act_packed_bytes(fmt) bytes (section (1) of the activation
+ *           layout above), row (b * T + t) * Hkv + k; the a_mant written by
+ *           mxq_quantize_act for M = B * T * Hkv rows of [.][128] serves
+ *           as is.  Read only.
+ *   k_exp, v_exp     DEVICE, 16-byte aligned: exponent rows of
+ *           mxq_exp_row_bytes(fmt) bytes, same row order (mxq_quantize_act's
+ *           a_exp).  Read only.
+ *   o       DEVICE float32 [B][Hq][128], written.
+ *   work    DEVICE, 16-byte aligned, work_bytes >= mxq_attn_work_bytes(...):
+ *           the caller's scratch for per-split partial results; its
+ *           contents need no initialisation and are overwritten.
+ * Errors: check_fmt's errors; MXQ_ERR_SHAPE for K != 128, a bad count, a
+ * non-finite scale or a short work buffer; MXQ_ERR_UNSUPPORTED for a
+ * permutation; MXQ_ERR_NULL; MXQ_ERR_ALIGN; MXQ_ERR_DEVICE on a failed
+ * launch.  Asynchronous on `stream`.
+ * mxq_attn_work_bytes returns the work size in bytes, or a negative
+ * mxq_status for invalid arguments.
+ */
+int64_t mxq_attn_work_bytes(const mxq_fmt *fmt, int64_t B, int64_t Hq, int64_t Hkv, int64_t T);
+mxq_status mxq_attn_decode(const mxq_fmt *fmt, const uint16_t *q, int64_t B, int64_t Hq,
+                           int64_t Hkv, int64_t T, float scale, const uint8_t *k_mant,
+                           const uint8_t *k_exp, const uint8_t *v_mant, const uint8_t *v_exp,
+                           float *o, float *work, int64_t work_bytes, void *stream);
 
 #ifdef __cplusplus
 }

@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libmxq.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["api.cpp", "quantize.hip", "quantize_act.hip", "gemm_prefill.hip", "gemm_partials.hip", "decode.hip", "unpack.hip", "peaks.hip", "calib.hip"]
+SOURCES = ["api.cpp", "quantize.hip", "quantize_act.hip", "gemm_prefill.hip", "gemm_partials.hip", "decode.hip", "unpack.hip", "peaks.hip", "calib.hip", "attn.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -402,4 +402,65 @@ mxq_status mxq_peak_mfma(int kind, int64_t iters, float *sink, int64_t *ops, voi
   return launched(mxq::launch_peak_mfma(kind, iters, sink, (hipStream_t)stream));
 }
 
+// Decode attention over the MXINT KV cache (MXSens Appendix A.2).
+static mxq_status attn_shape(const mxq_fmt *fmt, int64_t B, int64_t Hq, int64_t Hkv, int64_t T,
+                             Segs *sg) {
+  const mxq_status st = check_fmt(fmt, sg);
+  if (st != MXQ_OK) return st;
+  if (fmt->K != 128) return MXQ_ERR_SHAPE;
+  if (fmt->perm) return MXQ_ERR_UNSUPPORTED;
+  if (B < 0 || Hkv < 1 || Hq < Hkv || Hq % Hkv || Hq / Hkv > 16 || T < 1) return MXQ_ERR_SHAPE;
+  if (B > 65535 || Hkv > 65535 || Hq > INT32_MAX || T > (int64_t)1 << 40) return MXQ_ERR_SHAPE;
+  return MXQ_OK;
+}
+
+int64_t mxq_attn_work_bytes(const mxq_fmt *fmt, int64_t B, int64_t Hq, int64_t Hkv, int64_t T) {
+  Segs sg;
+  const mxq_status st = attn_shape(fmt, B, Hq, Hkv, T, &sg);
+  if (st != MXQ_OK) return -(int64_t)st;
+  if (B == 0) return 0;
+  const int64_t tps = mxq::attn_tokens_per_split(B, Hkv, T);
+  return B * Hq * ((T + tps - 1) / tps) * 130 * (int64_t)sizeof(float);
+}
+
+mxq_status mxq_attn_decode(const mxq_fmt *fmt, const uint16_t *q, int64_t B, int64_t Hq,
+                           int64_t Hkv, int64_t T, float scale, const uint8_t *k_mant,
+                           const uint8_t *k_exp, const uint8_t *v_mant, const uint8_t *v_exp,
+                           float *o, float *work, int64_t work_bytes, void *stream) {
+  Segs sg;
+  const mxq_status st = attn_shape(fmt, B, Hq, Hkv, T, &sg);
+  if (st != MXQ_OK) return st;
+  if (!(scale == scale) || scale == INFINITY || scale == -INFINITY) return MXQ_ERR_SHAPE;
+  if (B == 0) return MXQ_OK;
+  if (!q || !k_mant || !k_exp || !v_mant || !v_exp || !o || !work) return MXQ_ERR_NULL;
+  if (!aligned16(k_mant) || !aligned16(k_exp) || !aligned16(v_mant) || !aligned16(v_exp) ||
+      !aligned16(work) || ((uintptr_t)q & 1u) || ((uintptr_t)o & 3u))
+    return MXQ_ERR_ALIGN;
+  const int64_t tps = mxq::attn_tokens_per_split(B, Hkv, T);
+  const int64_t splits = (T + tps - 1) / tps;
+  if (splits > 65535 || work_bytes < B * Hq * splits * 130 * (int64_t)sizeof(float))
+    return MXQ_ERR_SHAPE;
+  mxq::AttnArgs a{};
+  a.q = q;
+  a.k_mant = k_mant;
+  a.k_exp = k_exp;
+  a.v_mant = v_mant;
+  a.v_exp = v_exp;
+  a.o = o;
+  a.work = work;
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.T = T;
+  a.G = (int)(Hq / Hkv);
+  a.scale = scale;
+  a.exp_bytes = exp_rb(fmt);
+  a.tokens_per_split = tps;
+  a.splits = (int)splits;
+  a.n4 = sg.n4;
+  a.n6 = sg.n6;
+  a.n8 = sg.n8;
+  return launched(mxq::launch_attn_decode(a, (hipStream_t)stream));
+}
+
 }  // extern "C"

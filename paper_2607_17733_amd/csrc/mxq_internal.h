@@ -102,4 +102,22 @@ int64_t peak_mfma_ops(int kind, int64_t iters);
 hipError_t launch_peak_stream(const void *buf, int64_t bytes, uint32_t *sink, hipStream_t s);
 hipError_t launch_peak_mfma(int kind, int64_t iters, float *sink, hipStream_t s);
 
+// Decode attention over an MXINT KV cache (attn.hip).
+struct AttnArgs {
+  const uint16_t *q;       // bf16 [B][Hq][128]
+  const uint8_t *k_mant, *k_exp, *v_mant, *v_exp;
+  float *o;                // [B][Hq][128]
+  float *work;             // [B][Hkv][splits][G][130]
+  int64_t B, Hq, Hkv, T;
+  int G;
+  float scale;
+  int64_t exp_bytes;       // exponent row stride
+  int64_t tokens_per_split;
+  int splits;
+  int n4, n6, n8;
+};
+
+int64_t attn_tokens_per_split(int64_t B, int64_t Hkv, int64_t T);
+hipError_t launch_attn_decode(const AttnArgs &args, hipStream_t s);
+
 }  // namespace mxq

@@ -61,6 +61,9 @@ _SIGS = {
     "mxq_peak_sink_words": (_I64, []),
     "mxq_peak_stream_read": (ctypes.c_int, [_P, _I64, _P, _P]),
     "mxq_peak_mfma": (ctypes.c_int, [ctypes.c_int, _I64, _P, _P, _P]),
+    "mxq_attn_work_bytes": (_I64, [_P, _I64, _I64, _I64, _I64]),
+    "mxq_attn_decode": (ctypes.c_int, [_P, _P, _I64, _I64, _I64, _I64, ctypes.c_float,
+                                       _P, _P, _P, _P, _P, _P, _I64, _P]),
 }
 
 
@@ -381,3 +384,34 @@ def calibrate(samples, s_layer: float, R: float, n8_blocks: int = 1):
     n4, n6, n8 = calib_counts(K, R, s_layer, n8_blocks)
     perm = calib_perm(s, n6, n8)
     return perm, [4] * n4 + [6] * n6 + [8] * n8
+
+
+def attn_work_bytes(fmt: Format, B: int, Hq: int, Hkv: int, T: int) -> int:
+    """Bytes of the scratch that mxq_attn_decode needs for these sizes."""
+    return _size(lib().mxq_attn_work_bytes(fmt.ref, B, Hq, Hkv, T), "mxq_attn_work_bytes")
+
+
+def attn_decode(q, k_cache, v_cache, fmt: Format, B: int, Hq: int, Hkv: int, T: int,
+                scale: float, out=None, work=None):
+    """Decode attention over an MXINT KV cache.  q: bf16 [B, Hq, 128] on the
+    device; k_cache, v_cache: (mant, exp) as returned by quantize_act for the
+    B * T * Hkv cache rows (row (b * T + t) * Hkv + h).  Returns float32
+    [B, Hq, 128] on the current stream."""
+    if not (isinstance(q, torch.Tensor) and q.is_cuda and q.dtype == torch.bfloat16
+            and q.is_contiguous() and q.numel() == B * Hq * 128):
+        raise MxqError("q must be a contiguous bf16 device tensor of B * Hq * 128 elements")
+    rows = B * T * Hkv
+    for mant, exp in (k_cache, v_cache):
+        if mant.numel() < rows * fmt.act_packed_bytes() or exp.numel() < rows * fmt.exp_row_bytes():
+            raise MxqError("KV cache buffers are too small for B * T * Hkv rows")
+    if out is None:
+        out = torch.empty((B, Hq, 128), dtype=torch.float32, device=q.device)
+    nw = attn_work_bytes(fmt, B, Hq, Hkv, T)
+    if work is None:
+        work = torch.empty(max(nw, 16), dtype=torch.uint8, device=q.device)
+    _check(lib().mxq_attn_decode(fmt.ref, _ptr(q), B, Hq, Hkv, T, float(scale),
+                                 _ptr(k_cache[0]), _ptr(k_cache[1]), _ptr(v_cache[0]),
+                                 _ptr(v_cache[1]), _ptr(out), _ptr(work), work.numel(),
+                                 _stream()), "mxq_attn_decode")
+    return out
+

@@ -286,3 +286,33 @@ def device_kv(which: int, device, tokens: int = 4096, heads: int = 8, head_dim: 
     x = torch.randn((tokens * heads, head_dim), generator=g, device=device,
                     dtype=torch.float32)
     return x.to(torch.bfloat16)
+
+
+def attn_inputs(seed: int, B: int, Hq: int, Hkv: int, T: int, head_dim: int = 128,
+                outlier_channels: int = 2, outlier_scale: float = 8.0):
+    """Decode-attention inputs as bf16 bit patterns: q [B, Hq, head_dim] and
+    the K and V caches [B * T * Hkv, head_dim] (row (b * T + t) * Hkv + h),
+    all N(0, 1); K has a few channels scaled up, as keys of trained models
+    show per-channel outliers."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence(7000 + seed)))
+    q = g.standard_normal((B, Hq, head_dim), dtype=np.float32)
+    k = g.standard_normal((B * T * Hkv, head_dim), dtype=np.float32)
+    v = g.standard_normal((B * T * Hkv, head_dim), dtype=np.float32)
+    if outlier_channels:
+        ch = g.choice(head_dim, size=outlier_channels, replace=False)
+        k[:, ch] *= outlier_scale
+    return to_bf16_bits(q), to_bf16_bits(k), to_bf16_bits(v)
+
+
+def device_attn_inputs(B: int, Hq: int, Hkv: int, T: int, device, head_dim: int = 128,
+                       outlier_scale: float = 8.0):
+    """The same distribution generated on the device (bf16 tensors), for sizes
+    whose host generation would dominate a benchmark."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(7100 + B * 131 + T)
+    q = torch.randn((B, Hq, head_dim), generator=g, device=device, dtype=torch.float32)
+    k = torch.randn((B * T * Hkv, head_dim), generator=g, device=device, dtype=torch.float32)
+    v = torch.randn((B * T * Hkv, head_dim), generator=g, device=device, dtype=torch.float32)
+    k[:, :2] *= outlier_scale
+    return q.to(torch.bfloat16), k.to(torch.bfloat16), v.to(torch.bfloat16)

@@ -70,7 +70,7 @@ def stream_sizes(widths):
 def test_sizes(lib):
     w1 = [4] * 6 + [6, 8]
     f, _w = _fmt(256, w1)
-    assert lib.mxq_abi_version() == 7
+    assert lib.mxq_abi_version() == 8
     assert op_steps(w1) == 4
     slab, dimg = stream_sizes(w1)
     assert (slab, dimg) == (2 * 1024 + 768 + 1024 + 3 * 256, 2 * 1536 + 2 * 2048 + 3 * 256)
@@ -158,3 +158,36 @@ def test_peak_microbenchmarks_validate_before_launch(lib):
     assert lib.mxq_peak_mfma(3, 1, fake, ctypes.byref(ops), None) == 2
     assert lib.mxq_peak_mfma(0, 0, fake, ctypes.byref(ops), None) == 2
     assert lib.mxq_peak_mfma(0, 1, None, ctypes.byref(ops), None) == 1
+
+
+def test_attention_validates_before_launch(lib):
+    f, _w = _fmt(128, [4, 4, 6, 8])
+    fr = ctypes.byref(f)
+    p16 = ctypes.c_void_p(4096)          # never dereferenced: validation fails first
+    bad = ctypes.c_void_p(4097)
+    big = 1 << 40
+
+    def call(fmt=fr, q=p16, B=2, Hq=8, Hkv=2, T=100, scale=0.1, k=p16, work=p16, wb=big):
+        return lib.mxq_attn_decode(fmt, q, B, Hq, Hkv, T, scale, k, p16, p16, p16, p16,
+                                   work, wb, None)
+
+    # per (sequence, query head) 130 floats per token split; splits <= ceil(T / 64)
+    for B, Hq, Hkv, T in [(1, 64, 8, 4096), (16, 64, 8, 4096), (3, 8, 2, 1), (2, 16, 1, 65)]:
+        n = lib.mxq_attn_work_bytes(fr, B, Hq, Hkv, T)
+        unit = B * Hq * 130 * 4
+        assert n > 0 and n % unit == 0 and n // unit <= -(-T // 64), (B, Hq, Hkv, T, n)
+    assert lib.mxq_attn_work_bytes(fr, 0, 8, 2, 10) == 0
+    assert lib.mxq_attn_work_bytes(fr, 1, 8, 3, 10) == -2            # Hq % Hkv
+    assert lib.mxq_attn_work_bytes(fr, 1, 34, 2, 10) == -2           # G > 16
+    assert lib.mxq_attn_work_bytes(fr, 1, 8, 2, 0) == -2             # T < 1
+    f2, _w2 = _fmt(256, [4] * 8)
+    assert lib.mxq_attn_work_bytes(ctypes.byref(f2), 1, 8, 2, 10) == -2   # head dim 256
+    assert call(B=0, q=None, k=None, work=None) == 0                 # empty batch: no-op
+    assert call(q=None) == 1
+    assert call(k=bad) == 5
+    assert call(work=bad) == 5
+    assert call(wb=16) == 2                                          # short work buffer
+    assert call(scale=float("inf")) == 2
+    assert call(scale=float("nan")) == 2
+    assert call(Hkv=3) == 2
+    assert call(T=0) == 2
