@@ -323,6 +323,74 @@ def decode_bench(dev, which: str = "up", reps: int = 50):
     return out
 
 
+def attn_bench(dev, reps: int = 50):
+    """Decode attention over the MXINT KV cache at the LLaMA-2-70B attention
+    shape: 64 query heads, 8 KV heads, head dim 128, 4096 cached tokens per
+    sequence, batches of 1, 4 and 16 sequences."""
+    import torch
+    from paper_2607_17733_amd import mxq
+    from paper_2607_17733_amd import workloads as W
+    Hq, Hkv, T, D = 64, 8, 4096, 128
+    out = {}
+    for widths in ([4, 4, 4, 4], [4, 4, 6, 8]):
+        fmt = mxq.Format(D, widths)
+        rb, erb = fmt.act_packed_bytes(), fmt.exp_row_bytes()
+        # bytes the attention needs per cache row: the mantissas and the four
+        # block exponents
+        row_alg = sum(4 * m for m in widths) + len(widths)
+        rec = {}
+        for B in (1, 4, 16):
+            rows = B * T * Hkv
+            per_copy = 2 * rows * (rb + erb)
+            R = max(2, -(-600_000_000 // per_copy))   # rotate > 2x the 256 MB last-level cache
+            q, k, v = W.device_attn_inputs(B * R, Hq, Hkv, T, dev)
+            q = q[:B].contiguous()
+            kc = mxq.quantize_act(k, fmt)
+            vc = mxq.quantize_act(v, fmt)
+            del k, v
+            o = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+            work = torch.empty(max(mxq.attn_work_bytes(fmt, B, Hq, Hkv, T), 16),
+                               dtype=torch.uint8, device=dev)
+
+            mxq.attn_decode(q, kc, vc, fmt, B, Hq, Hkv, T, D ** -0.5, out=o, work=work)
+            # the C ABI called directly with pre-marshalled arguments, so that
+            # host-side argument checks do not pace the launches
+            L = mxq.lib()
+            args = [(fmt.ref, mxq._ptr(q), B, Hq, Hkv, T, D ** -0.5,
+                     kc[0].data_ptr() + c * rows * rb, kc[1].data_ptr() + c * rows * erb,
+                     vc[0].data_ptr() + c * rows * rb, vc[1].data_ptr() + c * rows * erb,
+                     mxq._ptr(o), mxq._ptr(work), work.numel(), mxq._stream())
+                    for c in range(R)]
+
+            def call(i):
+                L.mxq_attn_decode(*args[i % R])
+            for i in range(2 * R):
+                call(i)
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for i in range(reps):
+                call(i)
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            alg = 2 * rows * row_alg + 2 * q.numel() + 4 * o.numel()
+            gbs = alg / (ms * 1e-3) / 1e9
+            rec["B%d" % B] = {"us": ms * 1e3, "algorithmic_bytes": alg, "GBps": gbs,
+                              "frac_hbm_peak": gbs / HBM_PEAK_GBS,
+                              "bf16_cache_bytes": 2 * rows * 2 * D, "rotated_copies": R}
+            del kc, vc, q
+            torch.cuda.empty_cache()
+        rec["widths"] = widths
+        out["w" + "".join(str(m) for m in widths)] = rec
+    out["workload"] = ("decode attention, 64 query / 8 KV heads, head dim 128, 4096 cached "
+                       "tokens per sequence, K and V MXINT (widths per 32-block of the head "
+                       "dimension), caches rotated so none stays in the last-level cache; "
+                       "bytes = mantissas + block exponents of K and V, q in, o out")
+    return out
+
+
 def layer_bench(dev, sensitive: bool, reps: int = 5):
     """The config-5 decoder layer: seven online quantize + GEMM pairs and the
     K/V cache quantize on one stream (inputs drawn on the device, weights
@@ -373,6 +441,7 @@ def main():
     ap.add_argument("--no-peaks", action="store_true")
     ap.add_argument("--no-calib", action="store_true")
     ap.add_argument("--no-fused", action="store_true")
+    ap.add_argument("--no-attn", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 512 MiB device copy (counter scaling)")
     args = ap.parse_args()
@@ -527,6 +596,15 @@ def main():
                     if key.startswith("M"):
                         rec["frac_achievable_hbm"] = (rec["packed_weight_GBps"] /
                                                       pk["hbm_stream_read_GBps"])
+    if not args.no_attn:
+        log("attention over the MXINT KV cache")
+        result["attention"] = attn_bench(dev)
+        if pk is not None:
+            for key, rec in result["attention"].items():
+                if isinstance(rec, dict):
+                    for b, r in rec.items():
+                        if b.startswith("B"):
+                            r["frac_achievable_hbm"] = r["GBps"] / pk["hbm_stream_read_GBps"]
     if not args.no_layer:
         log("layer sequence")
         result["layer"] = {"sensitive": layer_bench(dev, True),

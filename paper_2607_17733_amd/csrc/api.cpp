@@ -438,7 +438,7 @@ mxq_status mxq_attn_decode(const mxq_fmt *fmt, const uint16_t *q, int64_t B, int
     return MXQ_ERR_ALIGN;
   const int64_t tps = mxq::attn_tokens_per_split(B, Hkv, T);
   const int64_t splits = (T + tps - 1) / tps;
-  if (splits > 65535 || work_bytes < B * Hq * splits * 130 * (int64_t)sizeof(float))
+  if (splits > mxq::kAttnMaxSplits || work_bytes < B * Hq * splits * 130 * (int64_t)sizeof(float))
     return MXQ_ERR_SHAPE;
   mxq::AttnArgs a{};
   a.q = q;

@@ -117,6 +117,7 @@ struct AttnArgs {
   int n4, n6, n8;
 };
 
+constexpr int kAttnMaxSplits = 512;    // attn_tokens_per_split never asks for more
 int64_t attn_tokens_per_split(int64_t B, int64_t Hkv, int64_t T);
 hipError_t launch_attn_decode(const AttnArgs &args, hipStream_t s);
 

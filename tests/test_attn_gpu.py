@@ -106,6 +106,14 @@ def test_llama70b_cache_4k_batch16_sampled():
     _run(8, 16, 64, 8, 4096, [4, 4, 4, 4], seqs=[0, 15])
 
 
+def test_hundreds_of_token_splits():
+    # one sequence and one KV head over a 40000-token cache: about 300 splits
+    # merged by the combine step
+    fmt = mxq.Format(D, [4, 4, 4, 4])
+    assert mxq.attn_work_bytes(fmt, 1, 8, 1, 40000) // (8 * 130 * 4) > 256
+    _run(11, 1, 8, 1, 40000, [4, 4, 4, 4])
+
+
 def test_mixed_widths_long_cache():
     _run(9, 2, 64, 8, 2048, [4, 4, 4, 8])
 
