@@ -382,7 +382,7 @@ mxq_status mxq_peak_mfma(int kind, int64_t iters, float *sink, int64_t *ops,
  *   fmt     the cache format: K = 128 (the head dimension), perm NULL,
  *           widths as for mxq_quantize_act (round and clamp do not matter
  *           here).
- *   q       DEVICE bf16 [B][Hq][128], read only.
+ *   q       DEVICE bf16 [B][Hq][128], 16-byte aligned, read only.
  *   B >= 0 (0: nothing to do), Hkv >= 1, Hq a multiple of Hkv with
  *   Hq / Hkv <= 16, T >= 1.
  *   scale   finite (usually 1 / sqrt(128)).

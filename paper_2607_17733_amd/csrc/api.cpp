@@ -434,7 +434,7 @@ mxq_status mxq_attn_decode(const mxq_fmt *fmt, const uint16_t *q, int64_t B, int
   if (B == 0) return MXQ_OK;
   if (!q || !k_mant || !k_exp || !v_mant || !v_exp || !o || !work) return MXQ_ERR_NULL;
   if (!aligned16(k_mant) || !aligned16(k_exp) || !aligned16(v_mant) || !aligned16(v_exp) ||
-      !aligned16(work) || ((uintptr_t)q & 1u) || ((uintptr_t)o & 3u))
+      !aligned16(work) || !aligned16(q) || ((uintptr_t)o & 3u))
     return MXQ_ERR_ALIGN;
   const int64_t tps = mxq::attn_tokens_per_split(B, Hkv, T);
   const int64_t splits = (T + tps - 1) / tps;

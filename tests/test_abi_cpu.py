@@ -185,6 +185,7 @@ def test_attention_validates_before_launch(lib):
     assert call(B=0, q=None, k=None, work=None) == 0                 # empty batch: no-op
     assert call(q=None) == 1
     assert call(k=bad) == 5
+    assert call(q=ctypes.c_void_p(4098)) == 5                          # q not 16-byte aligned
     assert call(work=bad) == 5
     assert call(wb=16) == 2                                          # short work buffer
     assert call(scale=float("inf")) == 2
