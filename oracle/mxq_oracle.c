@@ -17,6 +17,11 @@
  *   - Section 1 (Introduction): shared power-of-two scale per block of 32.
  *   - Section 4.1 (Triplet quantization): each block carries exactly one
  *     mantissa width out of {4, 6, 8}; same-width columns fill whole blocks.
+ *   - Section 5 (average-bitwidth study, the LLaMA-2-7B table): a second
+ *     template uses MXINT3 in place of MXINT4 (widths {3, 6, 8}); a 3-bit
+ *     block follows the same rules with m = 3.  In the packed-row layout a
+ *     3-bit block is stored as the 4-bit block holding 2q, which has the
+ *     same values (2q * 2^(e - 2) = q * 2^(e - 1)).
  *   - Section 5.1 (MXSens results): the exponent is 8 bits per 32 elements,
  *     i.e. +0.25 bit per element; the widths therefore count storage bits,
  *     sign included (also the bit accounting in the proof of Theorem A.1).
@@ -93,7 +98,7 @@ static uint8_t quantize_block(const double *x, int m, int round_mode,
   return (uint8_t)(e + 127);
 }
 
-static int width_ok(int m) { return m == 4 || m == 6 || m == 8; }
+static int width_ok(int m) { return m == 3 || m == 4 || m == 6 || m == 8; }
 
 /*
  * Quantize `rows` rows of a bf16 matrix (row stride `ld` elements) along K.
@@ -254,7 +259,7 @@ int oracle_gemm_absbound(const int8_t *qa, const uint8_t *ea, const int8_t *qw,
  */
 int64_t oracle_act_row_bytes(const uint8_t *widths, int64_t nb) {
   int64_t bytes = 0;
-  for (int64_t b = 0; b < nb; ++b) bytes += 4 * (int64_t)widths[b];
+  for (int64_t b = 0; b < nb; ++b) bytes += 4 * (int64_t)(widths[b] == 3 ? 4 : widths[b]);
   return (bytes + 15) / 16 * 16;
 }
 
@@ -273,6 +278,13 @@ int oracle_pack_act(const int8_t *q, int64_t rows, int64_t K,
       uint8_t *blk = row + off;
       if (m == 8) {
         for (int t = 0; t < 32; ++t) blk[t] = (uint8_t)v[t];
+      } else if (m == 3) {
+        /* stored as the 4-bit block with mantissas 2q (the same values) */
+        for (int j = 0; j < 16; ++j) {
+          unsigned lo = (unsigned)(2 * v[2 * j]) & 15u;
+          unsigned hi = (unsigned)(2 * v[2 * j + 1]) & 15u;
+          blk[j] = (uint8_t)(lo | (hi << 4));
+        }
       } else {
         /* low nibble plane (the whole mantissa when m == 4) */
         for (int j = 0; j < 16; ++j) {
@@ -293,7 +305,7 @@ int oracle_pack_act(const int8_t *q, int64_t rows, int64_t K,
             }
         }
       }
-      off += 4 * m;
+      off += 4 * (m == 3 ? 4 : m);
     }
   }
   return 0;
