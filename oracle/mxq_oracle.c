@@ -281,9 +281,9 @@ int oracle_pack_act(const int8_t *q, int64_t rows, int64_t K,
       } else if (m == 3) {
         /* stored as the 4-bit block with mantissas 2q (the same values) */
         for (int j = 0; j < 16; ++j) {
-          unsigned lo = (unsigned)(2 * v[2 * j]) & 15u;
-          unsigned hi = (unsigned)(2 * v[2 * j + 1]) & 15u;
-          blk[j] = (uint8_t)(lo | (hi << 4));
+          unsigned even = (unsigned)(2 * v[2 * j]) & 15u;
+          unsigned odd = (unsigned)(2 * v[2 * j + 1]) & 15u;
+          blk[j] = (uint8_t)(even + 16u * odd);
         }
       } else {
         /* low nibble plane (the whole mantissa when m == 4) */
