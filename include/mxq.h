@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define MXQ_ABI_VERSION 8
+#define MXQ_ABI_VERSION 9
 #define MXQ_BLOCK 32
 /* mxq_gemm uses the weight-streaming decode kernel for M <= this. */
 #define MXQ_DECODE_MAX_M 16
@@ -65,7 +65,7 @@ typedef enum {
   MXQ_OK = 0,
   MXQ_ERR_NULL = 1,        /* a required pointer is NULL */
   MXQ_ERR_SHAPE = 2,       /* K % 32 != 0, K <= 0, negative sizes, ld < K/N */
-  MXQ_ERR_WIDTHS = 3,      /* a width not in {4,6,8}, or widths not grouped 4s,6s,8s */
+  MXQ_ERR_WIDTHS = 3,      /* a width not in {3,4,6,8}, or widths not non-decreasing */
   MXQ_ERR_PERM = 4,        /* reserved: permutations are not validated (see below) */
   MXQ_ERR_ALIGN = 5,       /* a device pointer is not 16-byte aligned */
   MXQ_ERR_UNSUPPORTED = 6, /* block != 32, unknown round/clamp mode */
@@ -80,8 +80,15 @@ typedef enum { MXQ_CLAMP_SYMMETRIC = 0, MXQ_CLAMP_FULL = 1 } mxq_clamp;
  *   K       reduction length, a positive multiple of 32.
  *   block   must be 32.
  *   round   mxq_round.   clamp   mxq_clamp.
- *   widths  HOST, K/32 entries, each 4, 6 or 8, non-decreasing (all 4-bit
- *           blocks, then all 6-bit, then all 8-bit; any count may be zero).
+ *   widths  HOST, K/32 entries, each 3, 4, 6 or 8, non-decreasing (3-bit,
+ *           then 4-bit, 6-bit and 8-bit blocks; any count may be zero).
+ *           Width 3 is the floor of the paper's 3-6-8 template (Section 5,
+ *           the average-bitwidth study): |q| <= 3 (symmetric) or -4..3
+ *           (full), LSB weight 2^(e - 1).  A 3-bit block is stored, in every
+ *           layout below, as the 4-bit block holding 2q (the same values:
+ *           2q * 2^(e - 2) = q * 2^(e - 1)); it counts as a 4-bit block in
+ *           the layouts' segment sizes, and mxq_unpack_* and
+ *           mxq_gemm_partials report it as that 4-bit block.
  *   perm    DEVICE int32[K] or NULL (identity).  Position p of the quantized
  *           row holds source column perm[p].  Entries outside [0, K) are read
  *           as +0.0 (never dereferenced); duplicates are allowed.

@@ -38,17 +38,20 @@ mxq_status check_fmt(const mxq_fmt *f, Segs *s) {
   if (f->perm && !aligned16(f->perm)) return MXQ_ERR_ALIGN;
   const int64_t nb = f->K / MXQ_BLOCK;
   int n[3] = {0, 0, 0};
+  int n3 = 0;
   int prev = 0;
   for (int64_t b = 0; b < nb; ++b) {
     const int m = f->widths[b];
-    if (m != 4 && m != 6 && m != 8) return MXQ_ERR_WIDTHS;
+    if (m != 3 && m != 4 && m != 6 && m != 8) return MXQ_ERR_WIDTHS;
     if (m < prev) return MXQ_ERR_WIDTHS;
     prev = m;
-    ++n[(m - 4) / 2];
+    if (m == 3) ++n3;
+    ++n[m == 3 ? 0 : (m - 4) / 2];
   }
   s->n4 = n[0];
   s->n6 = n[1];
   s->n8 = n[2];
+  s->n3 = n3;
   return MXQ_OK;
 }
 
@@ -110,6 +113,7 @@ mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows
   a.n4 = s.n4;
   a.n6 = s.n6;
   a.n8 = s.n8;
+  a.n3 = s.n3;
   a.ties_away = fmt->round == MXQ_ROUND_NEAREST_AWAY;
   a.full_clamp = fmt->clamp == MXQ_CLAMP_FULL;
   a.mant = mant;

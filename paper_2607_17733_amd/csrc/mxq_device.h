@@ -23,6 +23,7 @@ constexpr int kBlock = 32;
 // blocks (in that order along the permuted K).
 struct Segs {
   int n4, n6, n8;
+  int n3;       // of the n4 blocks, the first n3 hold 3-bit mantissas (stored as 2q)
 };
 
 struct BlockInfo {

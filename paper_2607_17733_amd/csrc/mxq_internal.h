@@ -15,6 +15,7 @@ struct QuantArgs {
   int64_t K;
   const int32_t *perm;     // device, K entries, or nullptr
   int n4, n6, n8;
+  int n3;                  // the first n3 of the 4-bit blocks are 3-bit (stored as 2q)
   int ties_away, full_clamp;
   uint8_t *mant;
   uint8_t *exp;

@@ -119,7 +119,8 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
     int qv[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u)
-      qv[u] = quant_elem(bits[u], E, bi.m, q.ties_away, q.full_clamp);
+      qv[u] = b < q.n3 ? 2 * quant_elem(bits[u], E, 3, q.ties_away, q.full_clamp)
+                       : quant_elem(bits[u], E, bi.m, q.ties_away, q.full_clamp);
 
     // stream-layout nibble codes, and (6-bit) the 2-bit codes of the half's
     // 16 elements: element 8d+k of the half at bits 8(k%4) + 4d + 2(k/4)

@@ -151,9 +151,13 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
 #pragma unroll
     for (int i = 0; i < 16; ++i) v.e[i] = v.o[i] = 0.f;
   } else {
-    const float qmax = seg == 0 ? 7.f : (seg == 1 ? 31.f : 127.f);
+    // a 3-bit block (the 3-6-8 template) is quantized with m = 3 and stored
+    // as the 4-bit block holding 2q, which has the same values
+    const bool three = seg == 0 && idx < q.n3;
+    const float qmax = three ? 3.f : (seg == 0 ? 7.f : (seg == 1 ? 31.f : 127.f));
     const float qmin = q.full_clamp ? -(qmax + 1.f) : -qmax;
-    const int sh = 127 + (m - 2) - E;
+    const int sh = 127 + (three ? 1 : m - 2) - E;
+    const float twice = three ? 2.f : 1.f;
 #pragma unroll
     for (int u = 0; u < 32; ++u) {
       const uint32_t bits = (u & 1) ? (pr[u >> 1] & 0xFFFF0000u) : (pr[u >> 1] << 16);
@@ -164,7 +168,7 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
       } else {
         y = rintf(y);
       }
-      y = __builtin_amdgcn_fmed3f(y, qmin, qmax);
+      y = __builtin_amdgcn_fmed3f(y, qmin, qmax) * twice;
       if (u & 1) v.o[u >> 1] = y; else v.e[u >> 1] = y;
     }
   }

@@ -70,7 +70,7 @@ def stream_sizes(widths):
 def test_sizes(lib):
     w1 = [4] * 6 + [6, 8]
     f, _w = _fmt(256, w1)
-    assert lib.mxq_abi_version() == 8
+    assert lib.mxq_abi_version() == 9
     assert op_steps(w1) == 4
     slab, dimg = stream_sizes(w1)
     assert (slab, dimg) == (2 * 1024 + 768 + 1024 + 3 * 256, 2 * 1536 + 2 * 2048 + 3 * 256)
@@ -102,7 +102,8 @@ def test_sizes(lib):
 
 
 def test_size_functions_match_oracle_layout(lib, oracle_lib):
-    for widths in ([4] * 3 + [6] * 1, [6] * 3, [8] * 5, [4] * 7 + [8]):
+    for widths in ([4] * 3 + [6] * 1, [6] * 3, [8] * 5, [4] * 7 + [8], [3] * 2 + [6] + [8],
+                   [3, 4, 4, 6]):
         f, _w = _fmt(32 * len(widths), widths)
         assert lib.mxq_act_packed_bytes(ctypes.byref(f)) == oracle_lib.act_row_bytes(widths)
 
@@ -112,6 +113,8 @@ def test_size_functions_match_oracle_layout(lib, oracle_lib):
     (dict(K=64, widths=[4, 5]), 3),              # bad width
     (dict(K=64, widths=[8, 4]), 3),              # not grouped
     (dict(K=64, widths=[6, 4]), 3),
+    (dict(K=64, widths=[4, 3]), 3),              # 3-bit blocks come first
+    (dict(K=64, widths=[2, 4]), 3),
     (dict(K=64, widths=[4, 4], block=16), 6),
     (dict(K=64, widths=[4, 4], round_=2), 6),
     (dict(K=64, widths=[4, 4], clamp=7), 6),

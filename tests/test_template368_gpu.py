@@ -1,0 +1,104 @@
+"""GPU parity of the 3-6-8 template (3-bit blocks in place of 4-bit ones, the
+paper's average-bitwidth study, Section 5) through the C ABI: the quantizer's
+packed rows and exponents bit-exact against the oracle (a 3-bit block is
+stored as the 4-bit block holding 2q), the weight pack, the prefill and
+decode GEMMs against the oracle GEMM, and attention over 3-bit caches."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_17733_amd import mxq
+from paper_2607_17733_amd import workloads as W
+from parity_util import check_gemm, say, to_dev_bf16
+from test_attn_gpu import _run as attn_run
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(seed, M, K, N, n3, n6, n8):
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence(9000 + seed)))
+    c = np.ones(K, np.float32)
+    c[g.choice(K, size=max(1, K // 64), replace=False)] = g.uniform(20, 100, max(1, K // 64))
+    a = W.to_bf16_bits(g.standard_normal((M, K), dtype=np.float32) * c)
+    w = W.to_bf16_bits(g.standard_normal((N, K), dtype=np.float32) * 0.02)
+    perm = np.argsort(-c, kind="stable")[::-1].astype(np.int32)   # large channels last (8-bit)
+    widths = [3] * n3 + [6] * n6 + [8] * n8
+    assert len(widths) * 32 == K
+    return a, w, perm, widths
+
+
+def _doubled(q, n3):
+    q = q.astype(np.int16).copy()
+    q[:, :32 * n3] *= 2
+    return q
+
+
+@pytest.mark.parametrize("clamp", ["sym", "full"])
+@pytest.mark.parametrize("M", [1, 16, 77])
+def test_quantizer_bytes(M, clamp):
+    a, _, perm, widths = _case(1, M, 512, 16, 12, 2, 2)
+    say("368 quantize M=%d clamp=%s" % (M, clamp))
+    fmt = mxq.Format(512, widths, torch.from_numpy(perm).cuda(), clamp=clamp)
+    mant, exp = mxq.quantize_act(to_dev_bf16(a), fmt)
+    torch.cuda.synchronize()
+    q, e = oracle.quantize(a, perm=perm, widths=widths, clamp_mode=1 if clamp == "full" else 0)
+    assert np.array_equal(mxq.packed_rows(mant, fmt, M).cpu().numpy(), oracle.pack_act(q, widths))
+    assert np.array_equal(mxq.exp_rows(exp, fmt, M).cpu().numpy()[:, :16], e)
+    qu, eu = mxq.unpack_act(mant, exp, fmt, M)
+    assert np.array_equal(qu.cpu().numpy(), _doubled(q, 12)) and np.array_equal(eu.cpu().numpy(), e)
+
+
+def test_weight_pack():
+    _, w, perm, widths = _case(2, 4, 1024, 200, 26, 4, 2)
+    fmt = mxq.Format(1024, widths, torch.from_numpy(perm).cuda())
+    wm, we = mxq.pack_weights(to_dev_bf16(w), fmt)
+    qu, eu = mxq.unpack_weights(wm, we, fmt, 200)
+    torch.cuda.synchronize()
+    q, e = oracle.quantize(w, perm=perm, widths=widths)
+    assert np.array_equal(qu.cpu().numpy()[:200], _doubled(q, 26))
+    assert np.array_equal(eu.cpu().numpy()[:200], e)
+
+
+@pytest.mark.parametrize("M", [1, 4, 16, 17, 300])
+def test_gemm(M):
+    K, N = 2048, 384
+    a, w, perm, widths = _case(3, M, K, N, 52, 8, 4)
+    say("368 gemm M=%d" % M)
+    fmt = mxq.Format(K, widths, torch.from_numpy(perm).cuda())
+    am, ae = mxq.quantize_act(to_dev_bf16(a), fmt)
+    wm, we = mxq.pack_weights(to_dev_bf16(w), fmt)
+    y = mxq.gemm(am, ae, wm, we, fmt, M, N)
+    torch.cuda.synchronize()
+    qa, ea = oracle.quantize(a, perm=perm, widths=widths)
+    qw, ew = oracle.quantize(w, perm=perm, widths=widths)
+    ref = oracle.gemm(qa, ea, qw, ew, widths)
+    # accumulation bounds of the same values as 4-bit blocks holding 2q
+    w4 = [4 if m == 3 else m for m in widths]
+    check_gemm(y.cpu().numpy(), ref, _doubled(qa, 52).astype(np.int8), ea,
+               _doubled(qw, 52).astype(np.int8), ew, w4, "3-6-8 gemm M=%d" % M)
+
+
+def test_template_matches_its_definition_at_the_attention_shape():
+    # the LLaMA-3-8B attention projection with the 3-6-8 template (102/13/13
+    # blocks), M = 2048: sampled rows and columns against the oracle
+    K = N = 4096
+    a, w, perm, widths = _case(4, 2048, K, N, 102, 13, 13)
+    fmt = mxq.Format(K, widths, torch.from_numpy(perm).cuda())
+    am, ae = mxq.quantize_act(to_dev_bf16(a), fmt)
+    wm, we = mxq.pack_weights(to_dev_bf16(w), fmt)
+    y = mxq.gemm(am, ae, wm, we, fmt, 2048, N)
+    torch.cuda.synchronize()
+    rows = np.array([0, 31, 32, 1000, 2047])
+    cols = np.array([0, 127, 128, 2049, 4095])
+    qa, ea = oracle.quantize(a[rows], perm=perm, widths=widths)
+    qw, ew = oracle.quantize(w[cols], perm=perm, widths=widths)
+    ref = oracle.gemm(qa, ea, qw, ew, widths)
+    w4 = [4 if m == 3 else m for m in widths]
+    check_gemm(y.cpu().numpy()[np.ix_(rows, cols)], ref, _doubled(qa, 102).astype(np.int8), ea,
+               _doubled(qw, 102).astype(np.int8), ew, w4, "3-6-8 attention shape")
+
+
+@pytest.mark.parametrize("widths", [[3, 3, 3, 3], [3, 3, 6, 8]])
+def test_attention_over_three_bit_cache(widths):
+    attn_run(20 + widths[2], 2, 64, 8, 600, widths)
