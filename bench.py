@@ -391,6 +391,32 @@ def attn_bench(dev, reps: int = 50):
     return out
 
 
+def template368_bench(dev, case, reps: int = 50):
+    """The attention-projection step with the 3-6-8 template: the same block
+    counts and permutation, 3-bit blocks in place of the 4-bit ones."""
+    import torch
+    from paper_2607_17733_amd import mxq
+    widths = [3 if m == 4 else int(m) for m in case.widths]
+    fmt = mxq.Format(case.K, widths, torch.from_numpy(case.perm).to(dev))
+    a = bf16_dev(case.a_bits, dev)
+    wm, we = mxq.pack_weights(bf16_dev(case.w_bits, dev), fmt)
+    am = torch.empty(fmt.act_bytes(case.M), dtype=torch.uint8, device=dev)
+    ae = torch.empty(fmt.act_exp_bytes(case.M), dtype=torch.uint8, device=dev)
+    y = torch.empty((case.M, case.N), dtype=torch.float32, device=dev)
+
+    def step():
+        mxq.quantize_act(a, fmt, out=(am, ae))
+        mxq.gemm(am, ae, wm, we, fmt, case.M, case.N, out=y)
+    ms = burst_ms(step, reps, 10)
+    ops = 2.0 * case.M * case.N * case.K
+    return {"ms_per_step": ms, "TOPs": ops / (ms * 1e-3) / 1e12,
+            "widths": [case.meta["n4"], case.meta["n6"], case.meta["n8"]],
+            "workload": "attention projection M=%d K=%d N=%d, 3-bit/6-bit/8-bit blocks "
+                        "%d/%d/%d (3-bit blocks stored as 4-bit blocks holding 2q)" % (
+                            case.M, case.K, case.N, case.meta["n4"], case.meta["n6"],
+                            case.meta["n8"])}
+
+
 def layer_bench(dev, sensitive: bool, reps: int = 5):
     """The config-5 decoder layer: seven online quantize + GEMM pairs and the
     K/V cache quantize on one stream (inputs drawn on the device, weights
@@ -442,6 +468,7 @@ def main():
     ap.add_argument("--no-calib", action="store_true")
     ap.add_argument("--no-fused", action="store_true")
     ap.add_argument("--no-attn", action="store_true")
+    ap.add_argument("--no-template", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 512 MiB device copy (counter scaling)")
     args = ap.parse_args()
@@ -596,6 +623,9 @@ def main():
                     if key.startswith("M"):
                         rec["frac_achievable_hbm"] = (rec["packed_weight_GBps"] /
                                                       pk["hbm_stream_read_GBps"])
+    if not args.no_template:
+        log("3-6-8 template")
+        result["template_368"] = template368_bench(dev, case)
     if not args.no_attn:
         log("attention over the MXINT KV cache")
         result["attention"] = attn_bench(dev)
