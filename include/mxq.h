@@ -9,7 +9,8 @@
  *     integers, so a block dot product is an integer multiply-accumulate
  *     followed by a power-of-two scaling.
  *   - Mixed mantissas (Section 4.1, Algorithm 2): each block has exactly one
- *     mantissa width out of {4, 6, 8}; columns are permuted so that
+ *     mantissa width out of {4, 6, 8} (or {3, 6, 8}, the Section 5
+ *     template); columns are permuted so that
  *     same-width columns fill whole blocks.  The widths and the permutation
  *     are the output of the offline sensitivity analysis (Algorithms 1-3,
  *     Theorem A.1) and are inputs here.  Weights and activations of a linear

@@ -9,8 +9,8 @@ Python implementation in exact rational arithmetic for tiny inputs.
 
 Paper: MXSens (arXiv 2607.17733), Section 2 (MXINT: 32-element blocks sharing a
 power-of-two scale, fixed-point integer elements), Section 4.1 (one mantissa
-width out of {4, 6, 8} per block), Section 5.1 (8-bit shared exponent,
-+0.25 bit per element).
+width out of {4, 6, 8} per block, or 3 in the 3-6-8 template of Section 5),
+Section 5.1 (8-bit shared exponent, +0.25 bit per element).
 """
 from __future__ import annotations
 

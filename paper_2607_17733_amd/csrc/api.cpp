@@ -188,7 +188,7 @@ const char *mxq_status_str(int status) {
     case MXQ_OK: return "ok";
     case MXQ_ERR_NULL: return "null pointer";
     case MXQ_ERR_SHAPE: return "invalid shape or leading dimension";
-    case MXQ_ERR_WIDTHS: return "invalid width map (widths must be 4, 6 or 8, grouped 4s, 6s, 8s)";
+    case MXQ_ERR_WIDTHS: return "invalid width map (widths must be 3, 4, 6 or 8, non-decreasing)";
     case MXQ_ERR_PERM: return "invalid permutation";
     case MXQ_ERR_ALIGN: return "device pointer not 16-byte aligned";
     case MXQ_ERR_UNSUPPORTED: return "unsupported block size, rounding or clamp mode";

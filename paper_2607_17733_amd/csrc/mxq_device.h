@@ -6,6 +6,7 @@
 // Format (MXSens, arXiv 2607.17733, Sections 2, 4.1, 5.1): 32-element blocks
 // along K, one 8-bit shared exponent E = floor(log2 max|x|) + 127 per block,
 // signed mantissas of m in {4, 6, 8} bits with LSB weight 2^(E-127-(m-2)).
+// (3-bit blocks are quantized with m = 3 and stored as 4-bit blocks holding 2q.)
 //
 // Everything is integer arithmetic on the bf16 bit pattern: no log2, no
 // float scaling (2^-s overflows fp32 for small s, and bf16 subnormals would

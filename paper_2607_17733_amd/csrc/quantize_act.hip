@@ -2,7 +2,8 @@
 //
 // MXSens (arXiv 2607.17733) Section 2 and Section 4.1: every 32-element
 // block of the permuted row gets one shared exponent E = floor(log2 max|x|)
-// + 127 and mantissas of its own width m in {4, 6, 8}.
+// + 127 and mantissas of its own width m in {4, 6, 8} (or 3, stored as 2q in
+// the 4-bit layout).
 //
 // Work decomposition.  A workgroup owns R consecutive rows (8 for K = 4096,
 // fewer for longer rows, up to 64 for short ones) and stages them in LDS with

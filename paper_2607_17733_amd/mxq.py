@@ -106,7 +106,8 @@ def _ptr(t):
 class Format:
     """Width map + permutation of one quantized linear (include/mxq.h mxq_fmt).
 
-    widths: K/32 entries in {4, 6, 8}, grouped 4s then 6s then 8s.
+    widths: K/32 entries in {3, 4, 6, 8}, non-decreasing (3-bit blocks, the
+            3-6-8 template, are stored as 4-bit blocks holding 2q).
     perm:   None (identity) or an int32 device tensor of K source columns.
     """
 
