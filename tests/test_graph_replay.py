@@ -53,3 +53,35 @@ def test_step_graph_replays_match_eager(M):
         assert torch.equal(y, ref[0]), "replay %d: GEMM output differs" % r
         assert torch.equal(am[:n_rows], ref[1]), "replay %d: packed rows differ" % r
         assert torch.equal(ae[:n_exp], ref[2]), "replay %d: exponent rows differ" % r
+
+
+def test_attention_graph_replays_match_eager():
+    # decode attention over an MXINT cache: its split partials live in the
+    # caller's work buffer, so a captured call replays without allocations
+    B, Hq, Hkv, T, D = 2, 16, 2, 700, 128
+    say("graph-replay attention", B, Hq, Hkv, T)
+    dev = torch.device("cuda:0")
+    qb, kb, vb = W.attn_inputs(41, B, Hq, Hkv, T)
+    fmt = mxq.Format(D, [4, 4, 6, 8])
+    kc = mxq.quantize_act(to_dev_bf16(kb), fmt)
+    vc = mxq.quantize_act(to_dev_bf16(vb), fmt)
+    q = to_dev_bf16(qb.reshape(-1, D)).reshape(B, Hq, D)
+    o = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+    work = torch.empty(mxq.attn_work_bytes(fmt, B, Hq, Hkv, T), dtype=torch.uint8, device=dev)
+
+    def step():
+        mxq.attn_decode(q, kc, vc, fmt, B, Hq, Hkv, T, D ** -0.5, out=o, work=work)
+
+    step()
+    torch.cuda.synchronize()
+    ref = o.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for r in range(4):
+        o.fill_(float("nan"))
+        work.fill_(0xA5)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(o, ref), "replay %d: attention output differs" % r
