@@ -102,3 +102,34 @@ def test_template_matches_its_definition_at_the_attention_shape():
 @pytest.mark.parametrize("widths", [[3, 3, 3, 3], [3, 3, 6, 8]])
 def test_attention_over_three_bit_cache(widths):
     attn_run(20 + widths[2], 2, 64, 8, 600, widths)
+
+
+@pytest.mark.parametrize("producer", ["rmsnorm", "swiglu"])
+@pytest.mark.parametrize("M", [5, 40])
+def test_fused_producers(producer, M):
+    # the quantizer fused with its producers quantizes 3-bit blocks the same way
+    from oracle import fused
+    K, N = 1024, 96
+    a, w, perm, widths = _case(5 + M, M, K, N, 26, 4, 2)
+    say("368 fused %s M=%d" % (producer, M))
+    g = np.random.Generator(np.random.PCG64(77 + M))
+    fmt = mxq.Format(K, widths, torch.from_numpy(perm).cuda())
+    if producer == "rmsnorm":
+        gain = fused.f32_to_bf16(g.uniform(0.25, 2.0, size=K).astype(np.float32))
+        am, ae = mxq.quantize_act_rmsnorm(to_dev_bf16(a), to_dev_bf16(gain), 1e-5, fmt)
+        x = fused.rmsnorm_bf16(a, gain, 1e-5)
+    else:
+        gate = fused.f32_to_bf16((g.normal(size=(M, K)) * 4).astype(np.float32))
+        am, ae = mxq.quantize_act_swiglu(to_dev_bf16(gate), to_dev_bf16(a), fmt)
+        x = fused.swiglu_bf16(gate, a)
+    wm, we = mxq.pack_weights(to_dev_bf16(w), fmt)
+    y = mxq.gemm(am, ae, wm, we, fmt, M, N)
+    torch.cuda.synchronize()
+    qa, ea = oracle.quantize(x, perm=perm, widths=widths)
+    qw, ew = oracle.quantize(w, perm=perm, widths=widths)
+    assert np.array_equal(mxq.packed_rows(am, fmt, M).cpu().numpy(), oracle.pack_act(qa, widths))
+    assert np.array_equal(mxq.exp_rows(ae, fmt, M).cpu().numpy()[:, :32], ea)
+    ref = oracle.gemm(qa, ea, qw, ew, widths)
+    w4 = [4 if m == 3 else m for m in widths]
+    check_gemm(y.cpu().numpy(), ref, _doubled(qa, 26).astype(np.int8), ea,
+               _doubled(qw, 26).astype(np.int8), ew, w4, "3-6-8 fused %s" % producer)
