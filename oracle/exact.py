@@ -105,3 +105,25 @@ def gemm_exact(qa, ea, qw, ew, widths):
                 acc += Fraction(p) * Fraction(2) ** s
             Y[i][j] = None if nan else acc
     return Y
+
+
+def absbound_exact(qa, ea, qw, ew, widths):
+    """Exact S[i][j] = sum_b |P_b| * 2^(sa+sw) as Fractions: the sum of the
+    magnitudes of the per-block terms of Y (blocks touching an E = 255
+    exponent are left out)."""
+    M, N = len(qa), len(qw)
+    nb = len(qa[0]) // BLOCK
+    S = [[Fraction(0)] * N for _ in range(M)]
+    for i in range(M):
+        for j in range(N):
+            acc = Fraction(0)
+            for b in range(nb):
+                if ea[i][b] == 255 or ew[j][b] == 255:
+                    continue
+                dq_a = dequantize_block(qa[i][b * BLOCK:(b + 1) * BLOCK], int(ea[i][b]),
+                                        int(widths[b]))
+                dq_w = dequantize_block(qw[j][b * BLOCK:(b + 1) * BLOCK], int(ew[j][b]),
+                                        int(widths[b]))
+                acc += abs(sum(x * y for x, y in zip(dq_a, dq_w)))
+            S[i][j] = acc
+    return S

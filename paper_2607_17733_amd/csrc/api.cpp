@@ -155,6 +155,13 @@ mxq_status gemm_args(const mxq_fmt *fmt, int64_t M, int64_t N, const uint8_t *a_
   if (!aligned16(a_mant) || !aligned16(a_exp) || !aligned16(w_mant) ||
       !aligned16(w_exp) || !aligned16(out))
     return MXQ_ERR_ALIGN;
+  // The prefill kernel addresses each wave's two 32-row activation tiles and
+  // each 128-column weight tile with 32-bit buffer offsets from a 64-bit base.
+  {
+    const mxq::OpGeo og = op_geo(s);
+    if (2LL * og.nsteps * mxq::kActStep > INT32_MAX || w_tile(s) > INT32_MAX)
+      return MXQ_ERR_SHAPE;
+  }
   *g = mxq::GemmArgs{};
   g->a_mant = a_mant;
   g->a_exp = a_exp;

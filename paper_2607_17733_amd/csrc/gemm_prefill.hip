@@ -163,13 +163,17 @@ __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mti
 
   // This wave's two 32-row tiles (tiles past the last one load the last tile;
   // those rows are never stored).
-  const int last = (int)((g.M - 1) / kActRows);
-  const int ta = min((int)(row0 / kActRows) + 2 * wr, last);
-  const int tb = min(ta + 1, last);
+  // The activation resources start at tile ta (64-bit arithmetic), so the
+  // 32-bit buffer offsets stay below 2 * nsteps * kActStep; the host rejects
+  // shapes where that exceeds INT32_MAX.
+  const int64_t last = (g.M - 1) / kActRows;
+  const int64_t ta = min(row0 / kActRows + 2 * wr, last);
+  const int dtb = (int)(min(ta + 1, last) - ta);          // 0 or 1: tile tb = ta + dtb
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)(g.a_mant + g.a_op), 0, 0x7fffffff, 0x00020000);
+      (void *)(g.a_mant + g.a_op + ta * nsteps * (int64_t)kActStep), 0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)(g.a_exp + g.a_sc), 0, 0x7fffffff, 0x00020000);
+      (void *)(g.a_exp + g.a_sc + ta * nsteps * (int64_t)kActScaleStep), 0, 0x7fffffff,
+      0x00020000);
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       (void *)(g.w_mant + g.w_op + (int64_t)nt * g.w_tile), 0, 0x7fffffff, 0x00020000);
   const int v16 = lane * 16, v4 = lane * 4;
@@ -201,7 +205,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_prefill_kernel(GemmArgs g, int mti
   auto issue_a_half = [&](auto set_tag, int it, int tm) __attribute__((always_inline)) {
     constexpr int S = decltype(set_tag)::v;
     const int st = min(2 * it + kg, nsteps - 1);
-    const int blk = (tm == 0 ? ta : tb) * nsteps + st;
+    const int blk = (tm == 0 ? 0 : dtb) * nsteps + st;
 #pragma unroll
     for (int j = 0; j < 3; ++j)
       xa[S][tm].p[j] = __builtin_bit_cast(

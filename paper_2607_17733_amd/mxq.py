@@ -167,18 +167,46 @@ def _bf16_2d(t, K, what):
     return t
 
 
+def _dev_bytes(t, n: int, what: str, dev=None):
+    """A contiguous uint8 device tensor of at least n bytes (on `dev`)."""
+    if not (isinstance(t, torch.Tensor) and t.is_cuda and t.dtype == torch.uint8
+            and t.is_contiguous()):
+        raise MxqError("%s must be a contiguous uint8 device tensor" % what)
+    if t.numel() < n:
+        raise MxqError("%s holds %d bytes, %d needed" % (what, t.numel(), n))
+    if dev is not None and t.device != dev:
+        raise MxqError("%s is on %s, not %s" % (what, t.device, dev))
+    return t
+
+
+def _act_out(out, fmt: Format, M: int, dev):
+    """The caller's (mant, exp) activation buffers, checked, or new ones."""
+    if out is None:
+        return (torch.empty(fmt.act_bytes(M), dtype=torch.uint8, device=dev),
+                torch.empty(fmt.act_exp_bytes(M), dtype=torch.uint8, device=dev))
+    mant, exp = out
+    _dev_bytes(mant, fmt.act_bytes(M), "activation mantissa buffer", dev)
+    _dev_bytes(exp, fmt.act_exp_bytes(M), "activation exponent buffer", dev)
+    return mant, exp
+
+
+def _gemm_operands(a_mant, a_exp, w_mant, w_exp, fmt: Format, M: int, N: int):
+    if M < 0 or N < 0:
+        raise MxqError("M and N must be non-negative")
+    dev = a_mant.device if isinstance(a_mant, torch.Tensor) else None
+    _dev_bytes(a_mant, fmt.act_bytes(M), "a_mant", dev)
+    _dev_bytes(a_exp, fmt.act_exp_bytes(M), "a_exp", dev)
+    _dev_bytes(w_mant, fmt.weight_bytes(N), "w_mant", dev)
+    _dev_bytes(w_exp, fmt.weight_exp_bytes(N), "w_exp", dev)
+    return dev
+
+
 def quantize_act(a, fmt: Format, out=None):
     """Online activation quantization: bf16 [M, >=K] -> (mant uint8
     [act_bytes(M)], exp uint8 [act_exp_bytes(M)]) on the current stream."""
     _bf16_2d(a, fmt.K, "activations")
     M = a.shape[0]
-    if out is None:
-        mant = torch.empty(fmt.act_bytes(M), dtype=torch.uint8, device=a.device)
-        exp = torch.empty(fmt.act_exp_bytes(M), dtype=torch.uint8, device=a.device)
-    else:
-        mant, exp = out
-        if mant.numel() < fmt.act_bytes(M) or exp.numel() < fmt.act_exp_bytes(M):
-            raise MxqError("activation output buffers are too small")
+    mant, exp = _act_out(out, fmt, M, a.device)
     _check(lib().mxq_quantize_act(fmt.ref, _ptr(a), M, a.stride(0), _ptr(mant),
                                   _ptr(exp), _stream()), "mxq_quantize_act")
     return mant, exp
@@ -190,12 +218,10 @@ def quantize_act_rmsnorm(x, gain, eps: float, fmt: Format, out=None):
     _bf16_2d(x, fmt.K, "activations")
     if gain.dtype != torch.bfloat16 or gain.numel() < fmt.K or not gain.is_contiguous():
         raise MxqError("gain must be a contiguous bf16 tensor of K elements")
+    if not gain.is_cuda or gain.device != x.device:
+        raise MxqError("gain must be on the activations' device")
     M = x.shape[0]
-    if out is None:
-        mant = torch.empty(fmt.act_bytes(M), dtype=torch.uint8, device=x.device)
-        exp = torch.empty(fmt.act_exp_bytes(M), dtype=torch.uint8, device=x.device)
-    else:
-        mant, exp = out
+    mant, exp = _act_out(out, fmt, M, x.device)
     _check(lib().mxq_quantize_act_rmsnorm(fmt.ref, _ptr(x), M, x.stride(0), _ptr(gain),
                                           float(eps), _ptr(mant), _ptr(exp), _stream()),
            "mxq_quantize_act_rmsnorm")
@@ -209,12 +235,10 @@ def quantize_act_swiglu(gate, up, fmt: Format, out=None):
     _bf16_2d(up, fmt.K, "up")
     if up.shape != gate.shape or up.stride() != gate.stride():
         raise MxqError("gate and up must have the same shape and strides")
+    if up.device != gate.device:
+        raise MxqError("gate and up must be on one device")
     M = gate.shape[0]
-    if out is None:
-        mant = torch.empty(fmt.act_bytes(M), dtype=torch.uint8, device=gate.device)
-        exp = torch.empty(fmt.act_exp_bytes(M), dtype=torch.uint8, device=gate.device)
-    else:
-        mant, exp = out
+    mant, exp = _act_out(out, fmt, M, gate.device)
     _check(lib().mxq_quantize_act_swiglu(fmt.ref, _ptr(gate), _ptr(up), M, gate.stride(0),
                                          _ptr(mant), _ptr(exp), _stream()),
            "mxq_quantize_act_swiglu")
@@ -246,10 +270,14 @@ def pack_weights(w, fmt: Format):
 
 def gemm(a_mant, a_exp, w_mant, w_exp, fmt: Format, M: int, N: int, out=None):
     """Y = Ahat @ What^T, fp32 [M, N]."""
+    dev = _gemm_operands(a_mant, a_exp, w_mant, w_exp, fmt, M, N)
     if out is None:
-        out = torch.empty((M, N), dtype=torch.float32, device=a_mant.device)
-    if out.dim() != 2 or out.stride(1) != 1 or out.dtype != torch.float32:
-        raise MxqError("out must be a 2-D fp32 tensor with unit column stride")
+        out = torch.empty((M, N), dtype=torch.float32, device=dev)
+    if not (isinstance(out, torch.Tensor) and out.is_cuda and out.device == dev
+            and out.dim() == 2 and out.stride(1) == 1 and out.dtype == torch.float32):
+        raise MxqError("out must be a 2-D fp32 device tensor with unit column stride")
+    if out.shape[0] < M or out.shape[1] < N:
+        raise MxqError("out is %s, smaller than [M, N] = [%d, %d]" % (tuple(out.shape), M, N))
     _check(lib().mxq_gemm(fmt.ref, M, N, _ptr(a_mant), _ptr(a_exp), _ptr(w_mant),
                           _ptr(w_exp), _ptr(out), out.stride(0), _stream()),
            "mxq_gemm")
@@ -258,7 +286,8 @@ def gemm(a_mant, a_exp, w_mant, w_exp, fmt: Format, M: int, N: int, out=None):
 
 def gemm_partials(a_mant, a_exp, w_mant, w_exp, fmt: Format, M: int, N: int):
     """Exact per-block int32 sums P[M, N, K/32] (debug / parity)."""
-    p = torch.empty((M, N, fmt.nb), dtype=torch.int32, device=a_mant.device)
+    dev = _gemm_operands(a_mant, a_exp, w_mant, w_exp, fmt, M, N)
+    p = torch.empty((M, N, fmt.nb), dtype=torch.int32, device=dev)
     _check(lib().mxq_gemm_partials(fmt.ref, M, N, _ptr(a_mant), _ptr(a_exp),
                                    _ptr(w_mant), _ptr(w_exp), _ptr(p), _stream()),
            "mxq_gemm_partials")
@@ -266,6 +295,8 @@ def gemm_partials(a_mant, a_exp, w_mant, w_exp, fmt: Format, M: int, N: int):
 
 
 def unpack_act(mant, exp, fmt: Format, rows: int):
+    _dev_bytes(mant, fmt.act_bytes(rows), "a_mant")
+    _dev_bytes(exp, fmt.act_exp_bytes(rows), "a_exp", mant.device)
     q = torch.empty((rows, fmt.K), dtype=torch.int8, device=mant.device)
     e = torch.empty((rows, fmt.nb), dtype=torch.uint8, device=mant.device)
     _check(lib().mxq_unpack_act(fmt.ref, rows, _ptr(mant), _ptr(exp), _ptr(q), _ptr(e),
@@ -274,6 +305,8 @@ def unpack_act(mant, exp, fmt: Format, rows: int):
 
 
 def unpack_weights(w_mant, w_exp, fmt: Format, N: int):
+    _dev_bytes(w_mant, fmt.weight_bytes(N), "w_mant")
+    _dev_bytes(w_exp, fmt.weight_exp_bytes(N), "w_exp", w_mant.device)
     q = torch.empty((N, fmt.K), dtype=torch.int8, device=w_mant.device)
     e = torch.empty((N, fmt.nb), dtype=torch.uint8, device=w_mant.device)
     _check(lib().mxq_unpack_weights(fmt.ref, N, _ptr(w_mant), _ptr(w_exp), _ptr(q),
@@ -415,4 +448,5 @@ def attn_decode(q, k_cache, v_cache, fmt: Format, B: int, Hq: int, Hkv: int, T: 
                                  _ptr(v_cache[1]), _ptr(out), _ptr(work), work.numel(),
                                  _stream()), "mxq_attn_decode")
     return out
+
 

@@ -288,6 +288,55 @@ def check_gemm_exact_rationals():
                 Fraction(2) ** -1074
 
 
+
+def check_absbound_exact_rationals():
+    """S = sum_b |P_b| 2^(sa+sw) (the scale of fp32 rounding that sets the
+    GEMM tolerance) equals the exact rational sum of the magnitudes of the
+    per-block dot products of the dequantized values, up to fp64 rounding."""
+    c, qa, ea, qw, ew = _quantized_case(12, 3, 160, 4, (2, 2, 1))
+    S = oracle.gemm_absbound(qa, ea, qw, ew, c.widths)
+    ex = exact.absbound_exact(qa.tolist(), ea.tolist(), qw.tolist(), ew.tolist(),
+                              c.widths.tolist())
+    for i in range(3):
+        for j in range(4):
+            err = abs(Fraction(float(S[i, j])) - ex[i][j])
+            assert err <= Fraction(8, 2 ** 53) * ex[i][j] + Fraction(2) ** -1074
+
+
+def _block_slice(q, e, b):
+    return (np.ascontiguousarray(q[:, b * BLOCK:(b + 1) * BLOCK]),
+            np.ascontiguousarray(e[:, b:b + 1]))
+
+
+def check_absbound_invariants():
+    """Invariants that fix S without restating it: S is the sum over blocks
+    of |Y_b| where Y_b is the (independently pinned) GEMM of that block
+    alone; S >= |Y|; flipping the sign of one block's activation mantissas
+    changes Y but not S; with non-negative mantissas S equals Y."""
+    c, qa, ea, qw, ew = _quantized_case(13, 5, 256, 6, (4, 2, 2))
+    widths = c.widths
+    S = oracle.gemm_absbound(qa, ea, qw, ew, widths)
+    Y = oracle.gemm(qa, ea, qw, ew, widths)
+    per_block = np.zeros_like(S)
+    for b in range(len(widths)):
+        a_b, ea_b = _block_slice(qa, ea, b)
+        w_b, ew_b = _block_slice(qw, ew, b)
+        per_block += np.abs(oracle.gemm(a_b, ea_b, w_b, ew_b, [int(widths[b])]))
+    assert np.allclose(S, per_block, rtol=1e-14, atol=0)
+    assert np.all(S >= np.abs(Y) * (1 - 1e-14))
+    # sign flip of block 1 of every activation row
+    qa2 = qa.copy()
+    qa2[:, BLOCK:2 * BLOCK] = -qa2[:, BLOCK:2 * BLOCK]
+    S2 = oracle.gemm_absbound(qa2, ea, qw, ew, widths)
+    Y2 = oracle.gemm(qa2, ea, qw, ew, widths)
+    assert np.array_equal(S2, S) and not np.allclose(Y2, Y)
+    # non-negative mantissas: every block term is >= 0, so S = Y
+    qa3, qw3 = np.abs(qa), np.abs(qw)
+    S3 = oracle.gemm_absbound(qa3, ea, qw3, ew, widths)
+    Y3 = oracle.gemm(qa3, ea, qw3, ew, widths)
+    assert np.allclose(S3, Y3, rtol=1e-14, atol=0)
+
+
 def check_gemm_textbook_case(seed=6):
     """All-8-bit blocks, identity permutation, inputs already on the MXINT
     grid: quantization is lossless, so the blockwise GEMM must equal a plain
@@ -444,7 +493,8 @@ ALL_CHECKS = [
     check_hand_cases_c, check_hand_cases_exact, check_exponent_bracketing,
     check_bruteforce_nearest, check_exact_agrees, check_symmetries,
     check_round_trip, check_gemm_vs_dequantized_matmul,
-    check_gemm_exact_rationals, check_gemm_textbook_case,
+    check_gemm_exact_rationals, check_absbound_exact_rationals,
+    check_absbound_invariants, check_gemm_textbook_case,
     check_gemm_permutation_invariance, check_permutation_gather,
     check_block_partials, check_gemm_nan,
     check_pack_layout, check_storage_accounting,

@@ -81,16 +81,34 @@ def mma_steps(widths):
     return 2 * g.s4 + 4 * g.s6 + 2 * g.s8
 
 
-def check_y(Y, Yref, S, nb, what="", T=None, steps=0):
-    """The GEMM tolerance: relative error 1e-5 (normwise) against the fp64
-    oracle, and elementwise a bound derived from the arithmetic:
-      - decode path (exact int32 block sums, one fp32 rescale-add each):
-        (nb + 2) 2^-24 S with S = sum_b |P_b| 2^(sa+sw);
-      - prefill path (exact digit products, fp32 accumulation inside each
-        matrix-core instruction): 2 * steps * 2^-24 * T, T from
-        digit_absbound, i.e. at most two roundings of the running absolute
-        sum per instruction;
-    plus nb 2^-126 for terms below fp32's normal range."""
+def a14_ratio(Y, Yref):
+    """Worst ratio of |Y - Y_ref| to the elementwise gate 1e-5 |Y_ref| +
+    1e-7 max|Y_ref| (allclose-style, the second term covering outputs that
+    cancel to near zero); <= 1 passes."""
+    Y = np.asarray(Y, np.float64)
+    Yref = np.asarray(Yref, np.float64)
+    keep = ~np.isnan(Yref)
+    if not keep.any():
+        return 0.0
+    err = np.abs(Y[keep] - Yref[keep])
+    gate = 1e-5 * np.abs(Yref[keep]) + 1e-7 * np.abs(Yref[keep]).max()
+    return float((err / np.maximum(gate, 1e-300)).max())
+
+
+def check_y(Y, Yref, S, nb, what="", T=None, steps=0, a14=True):
+    """The GEMM tolerance against the fp64 oracle:
+      - normwise relative error <= 1e-5;
+      - elementwise, the gate |Y - Y_ref| <= 1e-5 |Y_ref| + 1e-7 max|Y_ref|
+        (enforced unless a14=False, which only the deliberately adversarial
+        exponent-spread case uses; its ratio is always reported);
+      - elementwise, a bound derived from the arithmetic, always enforced:
+          decode path (exact int32 block sums, one fp32 rescale-add each):
+            (nb + 2) 2^-24 S with S = sum_b |P_b| 2^(sa+sw);
+          prefill path (exact digit products, fp32 accumulation inside each
+            matrix-core instruction): 2 * steps * 2^-24 * T, T from
+            digit_absbound, i.e. at most two roundings of the running
+            absolute sum per instruction;
+        plus nb 2^-126 for terms below fp32's normal range."""
     Y = Y.astype(np.float64)
     assert Y.shape == Yref.shape
     nan_ref = np.isnan(Yref)
@@ -107,15 +125,20 @@ def check_y(Y, Yref, S, nb, what="", T=None, steps=0):
         bound = np.maximum(bound, 2 * steps * 2.0 ** -24 * T[keep] + nb * 2.0 ** -126)
     worst = (err / bound).max()
     assert np.all(err <= bound), "%s: exceeds the accumulation bound (x%.3g)" % (what, worst)
+    gate = a14_ratio(Y, Yref)
+    say("%s: normwise %.3g, elementwise gate ratio %.3g, derived-bound ratio %.3g"
+        % (what, normwise, gate, worst))
+    if a14:
+        assert gate <= 1.0, "%s: elementwise 1e-5 gate exceeded (x%.3g)" % (what, gate)
     return normwise
 
 
-def check_gemm(Y, Yref, qa, ea, qw, ew, widths, what, rows=None, cols=None):
+def check_gemm(Y, Yref, qa, ea, qw, ew, widths, what, rows=None, cols=None, a14=True):
     """check_y with both accumulation bounds computed from the oracle's
     mantissas and exponents."""
     S = oracle.gemm_absbound(qa, ea, qw, ew, widths, rows=rows, cols=cols)
     T = digit_absbound(qa, ea, qw, ew, widths, rows=rows, cols=cols)
-    return check_y(Y, Yref, S, len(widths), what, T=T, steps=mma_steps(widths))
+    return check_y(Y, Yref, S, len(widths), what, T=T, steps=mma_steps(widths), a14=a14)
 
 
 def check_quant_act(case, out, qa, ea, fmt):

@@ -70,6 +70,45 @@ def test_floored_allocation_stays_within_budget():
             assert n8 == 1 and n4 >= 0 and n6 >= 0 and 32 * (n4 + n6 + n8) == di
 
 
+def _check_average_bits(avg_fn):
+    """average_bits against things other than itself: hand-counted layers,
+    the bits of the C oracle's packed rows (written by independent code from
+    the storage layout), and the paper's operating point (Section 5: one
+    8-bit block of 32 columns per layer gives 4.02-4.03 bits over
+    LLaMA-2-7B's seven linears, six with d_in 4096 and one with 11008)."""
+    import oracle
+    assert avg_fn([(127, 0, 1)]) == Fraction(127 * 4 + 8, 128)
+    assert avg_fn([(0, 3, 0)]) == 6.0 and avg_fn([(1, 1, 1)]) == 6.0
+    assert avg_fn([(2, 0, 0), (0, 0, 2)]) == 6.0
+    assert avg_fn([(3, 1, 0), (0, 0, 4)]) == Fraction(4 * 3 + 6 + 8 * 4, 8)
+    # (even 6-bit counts, so the packed rows carry no 16-byte padding)
+    for layers in ([(102, 14, 12)], [(90, 20, 18), (314, 66, 68)], [(6, 0, 2), (0, 2, 6)]):
+        bits = sum(8 * oracle.act_row_bytes([4] * a + [6] * b + [8] * c) for a, b, c in layers)
+        cols = sum(32 * (a + b + c) for a, b, c in layers)
+        assert abs(avg_fn(layers) - bits / cols) < 1e-12
+    d_in = [4096] * 6 + [11008]
+    avg = avg_fn([(d // 32 - 1, 0, 1) for d in d_in])
+    assert 4.02 <= avg <= 4.03
+
+
+def test_average_bits_pinned(oracle_lib):
+    _check_average_bits(calib.average_bits)
+
+
+@pytest.mark.parametrize("mutant", [
+    lambda L: sum(32 * (4 * a + 8 * b + 8 * c) for a, b, c in L) / sum(32 * (a + b + c) for a, b, c in L),
+    lambda L: sum(32 * (4 * a + 6 * b) for a, b, c in L) / sum(32 * (a + b + c) for a, b, c in L),
+    lambda L: sum(32 * (4 * a + 6 * b + 8 * c) for a, b, c in L) / sum(32 * (a + b) for a, b, c in L),
+    lambda L: sum(32 * (4 * a + 6 * b + 8 * c) + 8 * (a + b + c) for a, b, c in L)
+    / sum(32 * (a + b + c) for a, b, c in L),
+    lambda L: float(np.mean([(4 * a + 6 * b + 8 * c) / (a + b + c) for a, b, c in L])),
+], ids=["6-bit as 8", "8-bit dropped", "8-bit columns dropped", "exponent bits added",
+        "unweighted layer mean"])
+def test_average_bits_pin_catches_mutants(oracle_lib, mutant):
+    with pytest.raises(AssertionError):
+        _check_average_bits(mutant)
+
+
 def test_counts_clamp():
     assert calib.counts(256, 100.0, 1.0) == (0, 7, 1)       # all but the 8-bit block
     assert calib.counts(256, -3.0, 1.0) == (7, 0, 1)

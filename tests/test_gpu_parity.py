@@ -131,6 +131,41 @@ def test_special_values():
         _full_check(c2, identity=True)
 
 
+def _spread_case(seed, M, K, N, counts, spread=15):
+    """Every (row, block) of A and every (column, block) of W scaled by its
+    own 2^u, u uniform in [-spread, spread]: block exponents within one
+    matrix-core step differ by up to 2 * spread."""
+    g = np.random.default_rng(seed)
+    nb = K // 32
+    a = g.standard_normal((M, K)) * np.repeat(np.exp2(g.integers(-spread, spread + 1, (M, nb))),
+                                               32, axis=1)
+    w = 0.02 * g.standard_normal((N, K)) * np.repeat(
+        np.exp2(g.integers(-spread, spread + 1, (N, nb))), 32, axis=1)
+    return W.LinearCase("spread%d" % seed, M, K, N, W.to_bf16_bits(a.astype(np.float32)),
+                        W.to_bf16_bits(w.astype(np.float32)), np.arange(K, dtype=np.int32),
+                        W.widths_from_counts(*counts))
+
+
+@pytest.mark.parametrize("M", [8, 40])
+def test_wide_exponent_spread(M):
+    """Adversarial accumulation case: block exponents spread over 30 binades
+    inside every matrix-core step.  Bit-exact operands as everywhere; the
+    GEMM must meet the derived accumulation bound, while the 1e-5
+    elementwise gate is reported but not enforced (rounding in fp32 of terms
+    that far apart is not relative to the cancelled result)."""
+    case = _spread_case(100 + M, M, 512, 96, (8, 4, 4))
+    say(case.name, M, case.K, case.N, "exponent spread +-15")
+    fmt = fmt_for(case, identity=True)
+    out = gpu_run(case, fmt, want_partials=True)
+    qa, ea, qw, ew = oracle_quant(case, identity=True)
+    check_quant_act(case, out, qa, ea, fmt)
+    check_pack_w(case, out, qw, ew, fmt)
+    assert np.array_equal(out["p"].cpu().numpy(), oracle.block_partials(qa, qw))
+    assert (ea.max(axis=1).astype(int) - ea.min(axis=1)).min() >= 20
+    Yref = oracle.gemm(qa, ea, qw, ew, case.widths)
+    check_gemm(out["y"].cpu().numpy(), Yref, qa, ea, qw, ew, case.widths, case.name, a14=False)
+
+
 def test_deterministic_repeat():
     case = W.random_case(77, 300, 1024, 260, (24, 4, 4), perm="scales")
     say("determinism")

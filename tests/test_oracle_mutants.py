@@ -37,6 +37,18 @@ MUTANTS = [
      "(int64_t)qw[j * K + b * ORACLE_BLOCK + (31 - t)];"),
     ("gemm width offset", "int oracle_gemm(",
      "int sw = EW - 127 - (widths[b] - 2);", "int sw = EW - 127 - widths[b];"),
+    ("absbound drops the magnitude", "int oracle_gemm_absbound(",
+     "ldexp((double)(acc < 0 ? -acc : acc), sa + sw)", "ldexp((double)acc, sa + sw)"),
+    ("absbound exponent sign", "int oracle_gemm_absbound(",
+     "ldexp((double)(acc < 0 ? -acc : acc), sa + sw)",
+     "ldexp((double)(acc < 0 ? -acc : acc), sa - sw)"),
+    ("absbound drops last block", "int oracle_gemm_absbound(",
+     "for (int64_t b = 0; b < nb; ++b) {", "for (int64_t b = 0; b < nb - 1; ++b) {"),
+    ("absbound width offset", "int oracle_gemm_absbound(",
+     "int sw = ew[j * nb + b] - 127 - (widths[b] - 2);",
+     "int sw = ew[j * nb + b] - 127 - widths[b];"),
+    ("absbound doubles", "int oracle_gemm_absbound(",
+     "S[a * nc + c] = s;", "S[a * nc + c] = 2.0 * s;"),
     ("partials drop an element", "int oracle_block_partials(",
      "for (int t = 0; t < ORACLE_BLOCK; ++t)", "for (int t = 1; t < ORACLE_BLOCK; ++t)"),
     ("dequantize width offset", "int oracle_dequantize(",

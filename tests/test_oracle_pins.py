@@ -48,6 +48,14 @@ def test_gemm_exact_rationals(oracle_lib):
     pins.check_gemm_exact_rationals()
 
 
+def test_absbound_exact_rationals(oracle_lib):
+    pins.check_absbound_exact_rationals()
+
+
+def test_absbound_invariants(oracle_lib):
+    pins.check_absbound_invariants()
+
+
 def test_gemm_textbook_case(oracle_lib):
     pins.check_gemm_textbook_case()
 
