@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define MXQ_ABI_VERSION 9
+#define MXQ_ABI_VERSION 10
 #define MXQ_BLOCK 32
 /* mxq_gemm uses the weight-streaming decode kernel for M <= this. */
 #define MXQ_DECODE_MAX_M 16
@@ -70,7 +70,8 @@ typedef enum {
   MXQ_ERR_PERM = 4,        /* reserved: permutations are not validated (see below) */
   MXQ_ERR_ALIGN = 5,       /* a device pointer is not 16-byte aligned */
   MXQ_ERR_UNSUPPORTED = 6, /* block != 32, unknown round/clamp mode */
-  MXQ_ERR_DEVICE = 7       /* kernel launch or device query failed */
+  MXQ_ERR_DEVICE = 7,      /* kernel launch or device query failed */
+  MXQ_ERR_SCRATCH = 8      /* sizes exceed an allocation-free entry point's static scratch */
 } mxq_status;
 
 typedef enum { MXQ_ROUND_NEAREST_EVEN = 0, MXQ_ROUND_NEAREST_AWAY = 1 } mxq_round;
@@ -418,6 +419,28 @@ mxq_status mxq_attn_decode(const mxq_fmt *fmt, const uint16_t *q, int64_t B, int
                            int64_t Hkv, int64_t T, float scale, const uint8_t *k_mant,
                            const uint8_t *k_exp, const uint8_t *v_mant, const uint8_t *v_exp,
                            float *o, float *work, int64_t work_bytes, void *stream);
+
+/*
+ * mxq_attn_decode without a work buffer, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Arguments, results and errors are those
+ * of mxq_attn_decode (the same kernels, split the same way, so the outputs
+ * are identical), except that the per-split partial results live in a
+ * static device array of MXQ_ATTN_STATIC_WORK_BYTES per GPU, held from the
+ * library's first such call on that GPU until the process ends.  Calls whose
+ * mxq_attn_work_bytes exceeds MXQ_ATTN_STATIC_WORK_BYTES return
+ * MXQ_ERR_SCRATCH before anything is enqueued (B * Hq * splits * 520 bytes;
+ * about 2.1 MB for 64 query heads at any batch up to 16).  Every call on one
+ * GPU shares that GPU's array: calls that may overlap in time on one GPU
+ * (different streams, or different threads without ordering) race and must
+ * be serialised by the caller.  Nothing is allocated or freed, and no
+ * memory is set: the kernels overwrite the scratch they read.
+ */
+#define MXQ_ATTN_STATIC_WORK_BYTES (8LL << 20)
+mxq_status mxq_attn_decode_static(const mxq_fmt *fmt, const uint16_t *q, int64_t B, int64_t Hq,
+                                  int64_t Hkv, int64_t T, float scale, const uint8_t *k_mant,
+                                  const uint8_t *k_exp, const uint8_t *v_mant,
+                                  const uint8_t *v_exp, float *o, void *stream);
 
 #ifdef __cplusplus
 }

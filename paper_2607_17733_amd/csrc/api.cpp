@@ -186,6 +186,12 @@ mxq_status gemm_args(const mxq_fmt *fmt, int64_t M, int64_t N, const uint8_t *a_
 
 }  // namespace
 
+static mxq_status attn_common(const mxq_fmt *fmt, const uint16_t *q, int64_t B, int64_t Hq,
+                              int64_t Hkv, int64_t T, float scale, const uint8_t *k_mant,
+                              const uint8_t *k_exp, const uint8_t *v_mant, const uint8_t *v_exp,
+                              float *o, float *work, int64_t work_bytes, bool use_static,
+                              void *stream);
+
 extern "C" {
 
 int mxq_abi_version(void) { return MXQ_ABI_VERSION; }
@@ -200,6 +206,8 @@ const char *mxq_status_str(int status) {
     case MXQ_ERR_ALIGN: return "device pointer not 16-byte aligned";
     case MXQ_ERR_UNSUPPORTED: return "unsupported block size, rounding or clamp mode";
     case MXQ_ERR_DEVICE: return "device launch failure";
+    case MXQ_ERR_SCRATCH:
+      return "sizes exceed the static scratch of the allocation-free entry point";
     default: return "unknown status";
   }
 }
@@ -438,19 +446,45 @@ mxq_status mxq_attn_decode(const mxq_fmt *fmt, const uint16_t *q, int64_t B, int
                            int64_t Hkv, int64_t T, float scale, const uint8_t *k_mant,
                            const uint8_t *k_exp, const uint8_t *v_mant, const uint8_t *v_exp,
                            float *o, float *work, int64_t work_bytes, void *stream) {
+  return attn_common(fmt, q, B, Hq, Hkv, T, scale, k_mant, k_exp, v_mant, v_exp, o, work,
+                     work_bytes, false, stream);
+}
+
+mxq_status mxq_attn_decode_static(const mxq_fmt *fmt, const uint16_t *q, int64_t B, int64_t Hq,
+                                  int64_t Hkv, int64_t T, float scale, const uint8_t *k_mant,
+                                  const uint8_t *k_exp, const uint8_t *v_mant,
+                                  const uint8_t *v_exp, float *o, void *stream) {
+  return attn_common(fmt, q, B, Hq, Hkv, T, scale, k_mant, k_exp, v_mant, v_exp, o, nullptr,
+                     0, true, stream);
+}
+
+}  // extern "C"
+
+static mxq_status attn_common(const mxq_fmt *fmt, const uint16_t *q, int64_t B, int64_t Hq,
+                              int64_t Hkv, int64_t T, float scale, const uint8_t *k_mant,
+                              const uint8_t *k_exp, const uint8_t *v_mant, const uint8_t *v_exp,
+                              float *o, float *work, int64_t work_bytes, bool use_static,
+                              void *stream) {
   Segs sg;
   const mxq_status st = attn_shape(fmt, B, Hq, Hkv, T, &sg);
   if (st != MXQ_OK) return st;
   if (!(scale == scale) || scale == INFINITY || scale == -INFINITY) return MXQ_ERR_SHAPE;
   if (B == 0) return MXQ_OK;
-  if (!q || !k_mant || !k_exp || !v_mant || !v_exp || !o || !work) return MXQ_ERR_NULL;
+  if (!q || !k_mant || !k_exp || !v_mant || !v_exp || !o || (!use_static && !work))
+    return MXQ_ERR_NULL;
   if (!aligned16(k_mant) || !aligned16(k_exp) || !aligned16(v_mant) || !aligned16(v_exp) ||
-      !aligned16(work) || !aligned16(q) || ((uintptr_t)o & 3u))
+      (!use_static && !aligned16(work)) || !aligned16(q) || ((uintptr_t)o & 3u))
     return MXQ_ERR_ALIGN;
   const int64_t tps = mxq::attn_tokens_per_split(B, Hkv, T);
   const int64_t splits = (T + tps - 1) / tps;
-  if (splits > mxq::kAttnMaxSplits || work_bytes < B * Hq * splits * 130 * (int64_t)sizeof(float))
+  const int64_t need = B * Hq * splits * 130 * (int64_t)sizeof(float);
+  if (splits > mxq::kAttnMaxSplits) return MXQ_ERR_SHAPE;
+  if (use_static) {
+    if (need > mxq::kAttnStaticWorkBytes) return MXQ_ERR_SCRATCH;
+    if (mxq::attn_static_scratch(&work) != hipSuccess) return MXQ_ERR_DEVICE;
+  } else if (work_bytes < need) {
     return MXQ_ERR_SHAPE;
+  }
   mxq::AttnArgs a{};
   a.q = q;
   a.k_mant = k_mant;
@@ -473,5 +507,3 @@ mxq_status mxq_attn_decode(const mxq_fmt *fmt, const uint16_t *q, int64_t B, int
   a.n8 = sg.n8;
   return launched(mxq::launch_attn_decode(a, (hipStream_t)stream));
 }
-
-}  // extern "C"

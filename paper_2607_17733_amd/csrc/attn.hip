@@ -29,9 +29,41 @@
 // merged in a fixed order, so results do not depend on timing.  Each width mix
 // of the four blocks is its own instance, so block offsets and widths are
 // compile-time constants.
+#include <mutex>
+
 #include "mxq_internal.h"
 
 namespace mxq {
+
+// Per-split partial results of the allocation-free entry point: one array
+// per GPU, resident until the process ends.  In host code `scratch` names a
+// host-side stand-in, not device memory; its device address comes from
+// hipGetSymbolAddress, once per device, with that device current.
+static __device__ __align__(256) float scratch[kAttnStaticWorkBytes / sizeof(float)];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float *g_scratch_ptr[kMaxDevices] = {};
+
+}  // namespace
+
+hipError_t attn_static_scratch(float **ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = (float *)p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 namespace {
 

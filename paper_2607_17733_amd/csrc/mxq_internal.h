@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/mxq.h"
+
 namespace mxq {
 
 struct QuantArgs {
@@ -119,6 +121,11 @@ struct AttnArgs {
 };
 
 constexpr int kAttnMaxSplits = 512;    // attn_tokens_per_split never asks for more
+// Static per-device scratch of mxq_attn_decode_static (include/mxq.h).
+constexpr int64_t kAttnStaticWorkBytes = MXQ_ATTN_STATIC_WORK_BYTES;
+// The device address of this device's static scratch (looked up once per
+// device, with that device current).
+hipError_t attn_static_scratch(float **ptr);
 int64_t attn_tokens_per_split(int64_t B, int64_t Hkv, int64_t T);
 hipError_t launch_attn_decode(const AttnArgs &args, hipStream_t s);
 

@@ -64,6 +64,8 @@ _SIGS = {
     "mxq_attn_work_bytes": (_I64, [_P, _I64, _I64, _I64, _I64]),
     "mxq_attn_decode": (ctypes.c_int, [_P, _P, _I64, _I64, _I64, _I64, ctypes.c_float,
                                        _P, _P, _P, _P, _P, _P, _I64, _P]),
+    "mxq_attn_decode_static": (ctypes.c_int, [_P, _P, _I64, _I64, _I64, _I64, ctypes.c_float,
+                                              _P, _P, _P, _P, _P, _P]),
 }
 
 
@@ -450,3 +452,28 @@ def attn_decode(q, k_cache, v_cache, fmt: Format, B: int, Hq: int, Hkv: int, T: 
     return out
 
 
+
+ATTN_STATIC_WORK_BYTES = 8 << 20
+
+
+def attn_decode_static(q, k_cache, v_cache, fmt: Format, B: int, Hq: int, Hkv: int, T: int,
+                       scale: float, out):
+    """attn_decode without a work buffer: the library's static per-GPU
+    scratch holds the split results (calls overlapping on one GPU race).
+    `out` (float32 [B, Hq, 128], contiguous, on the device) is required, so
+    the call allocates nothing."""
+    if not (isinstance(q, torch.Tensor) and q.is_cuda and q.dtype == torch.bfloat16
+            and q.is_contiguous() and q.numel() == B * Hq * 128):
+        raise MxqError("q must be a contiguous bf16 device tensor of B * Hq * 128 elements")
+    if not (isinstance(out, torch.Tensor) and out.is_cuda and out.dtype == torch.float32
+            and out.is_contiguous() and out.numel() >= B * Hq * 128):
+        raise MxqError("out must be a contiguous float32 device tensor of B * Hq * 128 elements")
+    rows = B * T * Hkv
+    for mant, exp in (k_cache, v_cache):
+        if mant.numel() < rows * fmt.act_packed_bytes() or exp.numel() < rows * fmt.exp_row_bytes():
+            raise MxqError("KV cache buffers are too small for B * T * Hkv rows")
+    _check(lib().mxq_attn_decode_static(fmt.ref, _ptr(q), B, Hq, Hkv, T, float(scale),
+                                        _ptr(k_cache[0]), _ptr(k_cache[1]), _ptr(v_cache[0]),
+                                        _ptr(v_cache[1]), _ptr(out), _stream()),
+           "mxq_attn_decode_static")
+    return out

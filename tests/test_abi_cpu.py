@@ -70,7 +70,7 @@ def stream_sizes(widths):
 def test_sizes(lib):
     w1 = [4] * 6 + [6, 8]
     f, _w = _fmt(256, w1)
-    assert lib.mxq_abi_version() == 9
+    assert lib.mxq_abi_version() == 10
     assert op_steps(w1) == 4
     slab, dimg = stream_sizes(w1)
     assert (slab, dimg) == (2 * 1024 + 768 + 1024 + 3 * 256, 2 * 1536 + 2 * 2048 + 3 * 256)

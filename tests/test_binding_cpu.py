@@ -124,3 +124,17 @@ def test_abi_rejects_offsets_beyond_32_bits():
     st2 = lib.mxq_gemm_partials(ctypes.byref(f2), 64, 128, fake, fake, fake, fake, fake, None)
     assert st2 == 2
 
+
+def test_static_attention_rejects_oversize_on_the_host():
+    """mxq_attn_decode_static refuses sizes whose split results exceed its
+    static scratch with MXQ_ERR_SCRATCH, before any device call."""
+    lib = mxq.lib()
+    w = np.array([4, 4, 4, 4], np.uint8)
+    f = mxq._Fmt(128, 32, 0, 0, 0, w.ctypes.data_as(ctypes.c_void_p).value, None)
+    B, Hq, Hkv, T = 300, 64, 8, 64
+    assert lib.mxq_attn_work_bytes(ctypes.byref(f), B, Hq, Hkv, T) > mxq.ATTN_STATIC_WORK_BYTES
+    fake = ctypes.c_void_p(1 << 20)
+    st = lib.mxq_attn_decode_static(ctypes.byref(f), fake, B, Hq, Hkv, T, ctypes.c_float(0.1),
+                                    fake, fake, fake, fake, fake, None)
+    assert st == 8
+    assert b"static scratch" in lib.mxq_status_str(8)
