@@ -31,6 +31,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 INT8_PEAK_TOPS = 5000.0          # MI355X dense int8 matrix-core peak
+FP6_PEAK_TOPS = 10100.0          # MI355X dense FP6 / FP4 matrix-core peak
+FP8_PEAK_TOPS = 5000.0           # MI355X dense FP8 matrix-core peak
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E
 
 # Sources of the prefill GEMM kernel: the HBM traffic stored under profiles/
@@ -140,16 +142,105 @@ def peaks(dev, reps: int = 5):
     return out
 
 
-def prefill_mfma_floor_us(meta, M: int, N: int, pk):
-    """The prefill GEMM's matrix-core time at the measured loop rates: per
-    32x32 output tile, 2 FP6 products per 4-bit step, 4 per 6-bit step and 2
-    FP8 products per 8-bit step (steps of 4, 2 and 1 blocks)."""
-    tiles = (M // 32) * (N // 32)
+def prefill_issue(meta, M: int, N: int):
+    """Matrix-core instructions the prefill GEMM issues (32x32x64, 131072 ops
+    each): per 32x32 output tile, 2 FP6 per 4-bit step (four blocks), 4 FP6
+    per 6-bit step (two blocks) and 2 FP8 per 8-bit step (one block)."""
+    tiles = -(-M // 32) * -(-N // 32)
     s4, s6, s8 = -(-meta["n4"] // 4), -(-meta["n6"] // 2), meta["n8"]
-    per = 2.0 * 32 * 32 * 64
-    n6 = tiles * (2 * s4 + 4 * s6)
-    n8 = tiles * 2 * s8
-    return (n6 * per / (pk["mfma_fp6_TOPs"] * 1e12) + n8 * per / (pk["mfma_fp8_TOPs"] * 1e12)) * 1e6
+    return {"fp6": tiles * (2 * s4 + 4 * s6), "fp8": tiles * 2 * s8, "ops_per_instr": 131072}
+
+
+def prefill_peak_times_us(meta, M: int, N: int, pk=None):
+    """Times the prefill GEMM would take at the matrix cores' peaks:
+      dtype_us   the algorithmic work (2*M*N*32 per block) of each block at
+                 the datasheet peak of the dtype its block runs on (FP6 for
+                 4- and 6-bit blocks, FP8 for 8-bit blocks);
+      issued_us  the instructions actually issued at the datasheet peaks;
+      measured_floor_us  the same at the loop rates measured on this machine."""
+    per_block = 2.0 * M * N * 32
+    dtype_us = per_block * ((meta["n4"] + meta["n6"]) / (FP6_PEAK_TOPS * 1e12) +
+                            meta["n8"] / (FP8_PEAK_TOPS * 1e12)) * 1e6
+    iss = prefill_issue(meta, M, N)
+    o = iss["ops_per_instr"]
+    out = {"dtype_us": dtype_us,
+           "issued_us": (iss["fp6"] * o / (FP6_PEAK_TOPS * 1e12) +
+                         iss["fp8"] * o / (FP8_PEAK_TOPS * 1e12)) * 1e6}
+    if pk is not None:
+        out["measured_floor_us"] = (iss["fp6"] * o / (pk["mfma_fp6_TOPs"] * 1e12) +
+                                    iss["fp8"] * o / (pk["mfma_fp8_TOPs"] * 1e12)) * 1e6
+    return out
+
+
+def _rotated(t, copies: int):
+    """`copies` distinct device buffers with t's contents."""
+    return [t] + [t.clone() for _ in range(copies - 1)]
+
+
+def prefill_leg(dev, case, reps: int, warmup: int, pk=None, rotate_bytes: int = 0):
+    """One prefill linear: quantize + GEMM per step, and each kernel alone
+    in a back-to-back burst (HIP events on the launch stream).  With
+    rotate_bytes the quantizer is also timed over enough distinct input and
+    output buffers to exceed that many bytes, so its rate is HBM's."""
+    import torch
+    from paper_2607_17733_amd import mxq
+    M, K, N = case.M, case.K, case.N
+    fmt = mxq.Format(K, case.widths, torch.from_numpy(case.perm).to(dev))
+    a = bf16_dev(case.a_bits, dev)
+    wm, we = mxq.pack_weights(bf16_dev(case.w_bits, dev), fmt)
+    am = torch.empty(fmt.act_bytes(M), dtype=torch.uint8, device=dev)
+    ae = torch.empty(fmt.act_exp_bytes(M), dtype=torch.uint8, device=dev)
+    y = torch.empty((M, N), dtype=torch.float32, device=dev)
+
+    def quantize():
+        mxq.quantize_act(a, fmt, out=(am, ae))
+
+    def gemm():
+        mxq.gemm(am, ae, wm, we, fmt, M, N, out=y)
+
+    def step():
+        quantize()
+        gemm()
+    step_ms = burst_ms(step, reps, warmup)
+    gemm_ms = burst_ms(gemm, reps, warmup)
+    quant_ms = burst_ms(quantize, reps, warmup)
+    ops = 2.0 * M * N * K
+    meta = {"n4": int((case.widths <= 4).sum()), "n6": int((case.widths == 6).sum()),
+            "n8": int((case.widths == 8).sum())}
+    t = prefill_peak_times_us(meta, M, N, pk)
+    gemm_us = gemm_ms * 1e3
+    q_bytes = 2 * M * K + fmt.act_bytes(M) + fmt.act_exp_bytes(M)
+    rec = {"M": M, "K": K, "N": N, "widths": [meta["n4"], meta["n6"], meta["n8"]],
+           "step_us": step_ms * 1e3, "step_TOPs": ops / (step_ms * 1e-3) / 1e12,
+           "gemm_us": gemm_us, "gemm_TOPs": ops / (gemm_ms * 1e-3) / 1e12,
+           "frac_int8_peak": ops / (gemm_ms * 1e-3) / 1e12 / INT8_PEAK_TOPS,
+           "frac_dtype_peak": t["dtype_us"] / gemm_us,
+           "frac_issued_peak": t["issued_us"] / gemm_us,
+           "quantize_us": quant_ms * 1e3,
+           "quantize_algorithmic_bytes": q_bytes,
+           "quantize_GBps_cached": q_bytes / (quant_ms * 1e-3) / 1e9,
+           "weight_bytes": wm.numel() + we.numel(),
+           "weight_bits_per_element": 8.0 * (wm.numel() + we.numel()) / (N * K)}
+    rec.update({k: v for k, v in t.items()})
+    if rotate_bytes:
+        per = 2 * M * K + am.numel() + ae.numel()
+        R = max(2, -(-rotate_bytes // per))
+        ins = _rotated(a, R)
+        outs = [(am, ae)] + [(torch.empty_like(am), torch.empty_like(ae)) for _ in range(R - 1)]
+        it = [0]
+
+        def quant_rot():
+            i = it[0] % R
+            it[0] += 1
+            mxq.quantize_act(ins[i], fmt, out=outs[i])
+        qr_ms = burst_ms(quant_rot, max(reps, 2 * R), 2 * R)
+        rec["quantize_rotated"] = {"us": qr_ms * 1e3, "copies": R,
+                                   "GBps": q_bytes / (qr_ms * 1e-3) / 1e9,
+                                   "frac_hbm_peak": q_bytes / (qr_ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+        del ins, outs
+    del a, wm, we, am, ae, y
+    torch.cuda.empty_cache()
+    return rec
 
 
 def calib_bench(dev, samples: int = 128, rows: int = 2048, K: int = 4096, reps: int = 3):
@@ -250,32 +341,92 @@ def swiglu_bench(dev, M: int = 2048, K: int = 28672, reps: int = 20):
     return out
 
 
-def cpu_baseline(case, budget_s: float = 12.0):
-    """The oracle, as it stands, on the host: quantize the whole activation
-    matrix, then the blockwise GEMM on a sample of rows sized to the budget;
-    the step time is extrapolated linearly in M."""
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+_MLP = []
+
+
+def mlp_cases():
+    """The LLaMA-3-8B MLP linears at M=4096 (generated once per run)."""
+    if not _MLP:
+        from paper_2607_17733_amd import workloads as W
+        _MLP.extend([W.mlp_gate_up(), W.mlp_down()])
+    return _MLP
+
+
+def oracle_case_times(case, rows=None):
+    """The oracle as it stands on one linear: activation quantize, weight
+    quantize (the pack), and the blockwise GEMM over all rows or the first
+    `rows` rows (then extrapolated linearly in M)."""
     import numpy as np
     import oracle
-    oracle.build(force=False)
     t0 = time.perf_counter()
-    qa, ea = oracle.quantize(case.a_bits, perm=case.perm, widths=case.widths)
+    qa, ea = oracle.quantize(case.a_bits if rows is None else case.a_bits[:rows],
+                             perm=case.perm, widths=case.widths)
+    if rows is not None:
+        rows = qa.shape[0]
     t_quant = time.perf_counter() - t0
+    t0 = time.perf_counter()
     qw, ew = oracle.quantize(case.w_bits, perm=case.perm, widths=case.widths)
-    rows = 8
+    t_pack = time.perf_counter() - t0
     t0 = time.perf_counter()
-    oracle.gemm(qa, ea, qw, ew, case.widths, rows=np.arange(rows))
-    t_probe = time.perf_counter() - t0
-    rows = int(min(case.M, max(8, rows * budget_s / max(t_probe, 1e-3))))
-    t0 = time.perf_counter()
-    oracle.gemm(qa, ea, qw, ew, case.widths, rows=np.arange(rows))
+    oracle.gemm(qa, ea, qw, ew, case.widths)
     t_gemm = time.perf_counter() - t0
-    t_step = t_quant + t_gemm * case.M / rows
-    tops = 2.0 * case.M * case.N * case.K / t_step / 1e12
-    return {"value": tops, "unit": "TOP/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": "quantize all %d rows (%.2f s) + blockwise GEMM on %d of %d rows "
-                      "(%.2f s), step time extrapolated linearly in M" %
-                      (case.M, t_quant, rows, case.M, t_gemm)}
+    n = case.M if rows is None else rows
+    scale = case.M / n
+    step = (t_quant + t_gemm) * scale
+    rec = {"M": case.M, "K": case.K, "N": case.N, "threads": oracle.num_threads(),
+           "quantize_s": t_quant * scale, "pack_s": t_pack, "gemm_s": t_gemm * scale,
+           "TOPs": 2.0 * case.M * case.N * case.K / step / 1e12}
+    if rows is not None:
+        rec["extrapolated"] = "first %d of %d rows, linear in M" % (n, case.M)
+    return rec
+
+
+def oracle_plan(layer: bool = False):
+    """The oracle timed on the host cores: full runs of the tiny linear, the
+    attention projection, both MLP linears and the decode linears (M = 1, 4,
+    16), one-thread runs of the tiny linear and the decode linears at M = 16,
+    and (with `layer`) a 256-row sample of the 70B-shaped layer."""
+    import oracle
+    from paper_2607_17733_amd import workloads as W
+    oracle.build(force=False)
+    nthreads = oracle.num_threads()
+    out = {"cpu_model": cpu_model(), "threads": nthreads}
+    out["tiny"] = oracle_case_times(W.tiny())
+    out["attn_proj"] = oracle_case_times(W.attn_proj())
+    out["mlp_gate_up"] = oracle_case_times(mlp_cases()[0])
+    out["mlp_down"] = oracle_case_times(mlp_cases()[1])
+    for which in ("up", "down"):
+        base = W.decode(16, which)
+        for M in (1, 4, 16):
+            c = W.LinearCase(base.name, M, base.K, base.N, base.a_bits[:M], base.w_bits,
+                             base.perm, base.widths, base.meta)
+            out["decode_%s_M%d" % (which, M)] = oracle_case_times(c)
+    oracle.set_threads(1)
+    try:
+        out["tiny_1thread"] = oracle_case_times(W.tiny())
+        for which in ("up", "down"):
+            out["decode_%s_M16_1thread" % which] = oracle_case_times(W.decode(16, which))
+    finally:
+        oracle.set_threads(nthreads)
+    if layer:
+        rec = {}
+        for j in range(len(W.LAYER_LINEARS)):
+            c = W.layer_linear(j, True, M=256)
+            c.M = 8192                         # the layer's M; 256 rows are computed
+            rec[c.name] = oracle_case_times(c, rows=256)
+        out["layer_sensitive"] = rec
+    return out
 
 
 def decode_bench(dev, which: str = "up", reps: int = 50):
@@ -469,6 +620,9 @@ def main():
     ap.add_argument("--no-fused", action="store_true")
     ap.add_argument("--no-attn", action="store_true")
     ap.add_argument("--no-template", action="store_true")
+    ap.add_argument("--no-mlp", action="store_true")
+    ap.add_argument("--oracle-layer", action="store_true",
+                    help="also time the oracle on a 256-row sample of the 70B layer")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 512 MiB device copy (counter scaling)")
     args = ap.parse_args()
@@ -598,14 +752,38 @@ def main():
     if not args.no_peaks:
         log("achievable peaks")
         pk = peaks(dev)
-        floor = prefill_mfma_floor_us(case.meta, M, N, pk)
         result["peaks"] = pk
+    t = prefill_peak_times_us(case.meta, M, N, pk)
+    gemm_us = gemm_ms * 1e3
+    result["roofline"]["frac_dtype_peak"] = t["dtype_us"] / gemm_us
+    result["roofline"]["frac_issued_peak"] = t["issued_us"] / gemm_us
+    result["roofline"]["dtype_peak_note"] = (
+        "frac = algorithmic ops against the dense int8 peak; frac_dtype_peak = the "
+        "time the algorithmic ops of each block take at the datasheet peak of the "
+        "dtype that block runs on (FP6 10.1 PF for 4- and 6-bit blocks, FP8 5.0 PF for "
+        "8-bit blocks), %.2f us, over the launch time; frac_issued_peak = the "
+        "instructions actually issued (digit products included) at those peaks, "
+        "%.2f us, over the launch time" % (t["dtype_us"], t["issued_us"]))
+    if pk is not None:
         result["roofline"]["achievable"] = {
             "int8_loop_TOPs": pk["mfma_int8_TOPs"],
             "frac_int8_loop": gemm_tops / pk["mfma_int8_TOPs"],
-            "kernel_mfma_floor_us": floor,
-            "frac_of_mfma_floor": floor / (gemm_ms * 1e3),
+            "kernel_mfma_floor_us": t["measured_floor_us"],
+            "frac_of_mfma_floor": t["measured_floor_us"] / gemm_us,
         }
+    result["weight_bits_per_element"] = 8.0 * (wm.numel() + we.numel()) / (N * K)
+    if not args.no_mlp:
+        log("MLP linears (gate/up, down) at M=4096")
+        result["mlp"] = {"gate_up": prefill_leg(dev, mlp_cases()[0], 20, 5, pk),
+                         "down": prefill_leg(dev, mlp_cases()[1], 20, 5, pk)}
+    log("paper operating point and rotated quantizer at the attention shape")
+    pp = W.make_linear(2, "paper_point_127_0_1", M, K, N, 0.0, 0.0, counts=(127, 0, 1))
+    result["paper_point"] = prefill_leg(dev, pp, args.steps, args.warmup, pk)
+    result["paper_point"]["workload"] = (
+        "the paper's operating point (one 8-bit block of 32 columns, the rest 4-bit: "
+        "127/0/1 blocks) at the attention-projection shape M=2048 K=N=4096")
+    result["quantize"]["rotated"] = prefill_leg(
+        dev, case, 10, 2, pk, rotate_bytes=600 << 20)["quantize_rotated"]
     if not args.no_fused:
         log("fused normalisation + quantize")
         result["fused_rmsnorm_quantize"] = fused_bench(dev, case, fmt)
@@ -641,7 +819,15 @@ def main():
                            "insensitive": layer_bench(dev, False)}
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
-        result["cpu_baseline"] = cpu_baseline(case)
+        plan = oracle_plan(layer=args.oracle_layer)
+        att = plan["attn_proj"]
+        result["cpu_baseline"] = {
+            "value": att["TOPs"], "unit": "TOP/s", "cores": att["threads"], "kind": "oracle",
+            "cpu_model": plan["cpu_model"],
+            "sample": "the whole step on the host: quantize all %d rows (%.2f s) + blockwise "
+                      "GEMM on all %d rows (%.2f s); the other linears under oracle_plan"
+                      % (M, att["quantize_s"], M, att["gemm_s"])}
+        result["oracle_plan"] = plan
     print(json.dumps(result), flush=True)
 
 

@@ -80,6 +80,8 @@ def _declare(lib):
     lib.oracle_pack_act.argtypes = [P, I64, I64, P, P]
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = I
+    lib.oracle_set_threads.argtypes = [I]
+    lib.oracle_set_threads.restype = None
     for f in ("oracle_quantize", "oracle_dequantize", "oracle_block_partials",
               "oracle_gemm", "oracle_gemm_absbound", "oracle_pack_act"):
         getattr(lib, f).restype = I
@@ -194,3 +196,8 @@ def pack_act(q, widths):
 def num_threads() -> int:
     """Threads the oracle's OpenMP loops use."""
     return int(_load().oracle_num_threads())
+
+
+def set_threads(n: int) -> None:
+    """Threads for the oracle's OpenMP loops (for timing at a stated count)."""
+    _load().oracle_set_threads(int(n))

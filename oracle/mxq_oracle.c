@@ -319,3 +319,13 @@ int oracle_num_threads(void) {
   return 1;
 #endif
 }
+
+/* Threads for the OpenMP loops above (timing of the oracle at a stated core
+ * count); a no-op without OpenMP. */
+void oracle_set_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
