@@ -19,9 +19,9 @@
  *     mantissa width out of {4, 6, 8}; same-width columns fill whole blocks.
  *   - Section 5 (average-bitwidth study, the LLaMA-2-7B table): a second
  *     template uses MXINT3 in place of MXINT4 (widths {3, 6, 8}); a 3-bit
- *     block follows the same rules with m = 3.  In the packed-row layout a
- *     3-bit block is stored as the 4-bit block holding 2q, which has the
- *     same values (2q * 2^(e - 2) = q * 2^(e - 1)).
+ *     block follows the same rules with m = 3.  Its storage follows its
+ *     bits (the table's average bitwidths count 3 bits per element): 12
+ *     bytes per block in the packed-row layout.
  *   - Section 5.1 (MXSens results): the exponent is 8 bits per 32 elements,
  *     i.e. +0.25 bit per element; the widths therefore count storage bits,
  *     sign included (also the bit accounting in the proof of Theorem A.1).
@@ -259,7 +259,8 @@ int oracle_gemm_absbound(const int8_t *qa, const uint8_t *ea, const int8_t *qw,
  */
 int64_t oracle_act_row_bytes(const uint8_t *widths, int64_t nb) {
   int64_t bytes = 0;
-  for (int64_t b = 0; b < nb; ++b) bytes += 4 * (int64_t)(widths[b] == 3 ? 4 : widths[b]);
+  /* 32 mantissas of m bits: 4 m bytes per block (12 for the 3-bit blocks) */
+  for (int64_t b = 0; b < nb; ++b) bytes += 4 * (int64_t)widths[b];
   return (bytes + 15) / 16 * 16;
 }
 
@@ -279,11 +280,12 @@ int oracle_pack_act(const int8_t *q, int64_t rows, int64_t K,
       if (m == 8) {
         for (int t = 0; t < 32; ++t) blk[t] = (uint8_t)v[t];
       } else if (m == 3) {
-        /* stored as the 4-bit block with mantissas 2q (the same values) */
-        for (int j = 0; j < 16; ++j) {
-          unsigned even = (unsigned)(2 * v[2 * j]) & 15u;
-          unsigned odd = (unsigned)(2 * v[2 * j + 1]) & 15u;
-          blk[j] = (uint8_t)(even + 16u * odd);
+        /* 96 bits, little-endian: element t's 3-bit two's complement field
+           at bits 3t .. 3t + 2 */
+        for (int t = 0; t < 32; ++t) {
+          unsigned f = (unsigned)v[t] & 7u;
+          for (int k = 0; k < 3; ++k)
+            if ((f >> k) & 1u) blk[(3 * t + k) / 8] |= (uint8_t)(1u << ((3 * t + k) % 8));
         }
       } else {
         /* low nibble plane (the whole mantissa when m == 4) */
@@ -305,7 +307,7 @@ int oracle_pack_act(const int8_t *q, int64_t rows, int64_t K,
             }
         }
       }
-      off += 4 * (m == 3 ? 4 : m);
+      off += 4 * m;
     }
   }
   return 0;

@@ -1,7 +1,8 @@
 """Pins of the oracle's 3-bit blocks (the 3-6-8 template of the paper's
 average-bitwidth study, Section 5): a hand-worked block, a brute-force
 nearest-grid-point check, the GEMM against float64 products of the
-dequantized values, and the packed layout (2q in the 4-bit nibble plane)."""
+dequantized values, and the packed layout (12 bytes per block, element t's
+3-bit two's complement field at bits 3t .. 3t + 2)."""
 import numpy as np
 
 import oracle
@@ -72,16 +73,36 @@ def test_gemm_with_three_bit_blocks():
     np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-300)
 
 
-def test_three_bit_blocks_pack_as_doubled_four_bit():
+def test_three_bit_blocks_pack_at_twelve_bytes():
+    # 3 bits per element: a block of 32 takes 12 bytes; the row pads to 16
+    assert oracle.act_row_bytes([3]) == 16
+    assert oracle.act_row_bytes([3, 3, 8]) == 12 + 12 + 32 + 8
+    assert oracle.act_row_bytes([3, 3, 3, 3]) == 48
     g = np.random.Generator(np.random.PCG64(33))
     x = _bits(g.standard_normal((3, 96)))
     q, _ = oracle.quantize(x, widths=[3, 3, 8])
-    assert oracle.act_row_bytes([3, 3, 8]) == 16 + 16 + 32
     p = oracle.pack_act(q, [3, 3, 8])
+    assert p.shape == (3, 64)
     for blk in range(2):
-        nib = p[:, 16 * blk:16 * blk + 16]
-        lo = (nib & 15).astype(np.int8)
-        hi = (nib >> 4).astype(np.int8)
-        v = np.stack([lo, hi], axis=-1).reshape(3, 32)
-        v = np.where(v >= 8, v - 16, v)
-        assert np.array_equal(v, 2 * q[:, 32 * blk:32 * blk + 32])
+        # read the 96-bit little-endian integer field by field
+        v = [int.from_bytes(bytes(p[r, 12 * blk:12 * blk + 12]), "little") for r in range(3)]
+        for r in range(3):
+            for t in range(32):
+                f = (v[r] >> (3 * t)) & 7
+                assert (f - 8 if f >= 4 else f) == q[r, 32 * blk + t]
+    assert np.array_equal(p[:, 24:56].view(np.int8), q[:, 64:96])
+    assert not p[:, 56:].any()
+
+
+def test_three_bit_packing_hand_worked():
+    # elements 0..2 = 1, -1, -3 and the rest 0: fields 001, 111, 101 at bits
+    # 0, 3, 6; LSB first, bits 0-8 read 1 0 0 1 1 1 1 0 | 1: bytes 0x79, 0x01
+    # (the third field straddles the byte boundary)
+    q = np.zeros((1, 32), np.int8)
+    q[0, :3] = [1, -1, -3]
+    p = oracle.pack_act(q, [3])
+    assert list(p[0, :3]) == [0x79, 0x01, 0x00]
+    q[0, :] = 0
+    q[0, 31] = -4                                    # field 100 at bits 93..95
+    p = oracle.pack_act(q, [3])
+    assert list(p[0, :12]) == [0] * 11 + [0x80]
