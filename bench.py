@@ -440,11 +440,11 @@ def decode_bench(dev, which: str = "up", reps: int = 50):
     fmt = mxq.Format(case.K, case.widths, torch.from_numpy(case.perm).to(dev))
     wm0, we0 = mxq.pack_weights(bf16_dev(case.w_bits, dev), fmt)
     copies = [(wm0, we0)] + [(wm0.clone(), we0.clone()) for _ in range(3)]
-    # what the decode kernel streams: the packed slabs (4 * m bytes per block
-    # and column, N rounded to 16) and the exponent rows; the prefill operand
-    # image that follows the slabs is not read
-    n_pad = -(-case.N // 16) * 16
-    w_bytes = n_pad * sum(4 * int(m) for m in case.widths) + we0.numel()
+    # algorithmic bytes: the MXINT weights, 4 m bytes per block and column
+    # plus one exponent byte per block; the decode kernel streams the whole
+    # weight buffer (the same bits, blocks padded to whole steps)
+    w_bytes = case.N * sum(4 * int(m) + 1 for m in case.widths)
+    buf_bytes = wm0.numel() + we0.numel()
     out = {}
     for M in (1, 4, 16):
         am, ae = mxq.quantize_act(bf16_dev(case.a_bits[:M], dev), fmt)
@@ -471,6 +471,7 @@ def decode_bench(dev, which: str = "up", reps: int = 50):
                           which, case.K, case.N, case.meta["n4"], case.meta["n6"],
                           case.meta["n8"], w_bytes / 1e6)
     out["packed_weight_bytes"] = w_bytes
+    out["weight_buffer_bytes"] = buf_bytes
     return out
 
 
@@ -496,8 +497,8 @@ def attn_bench(dev, reps: int = 50):
             R = max(2, -(-600_000_000 // per_copy))   # rotate > 2x the 256 MB last-level cache
             q, k, v = W.device_attn_inputs(B * R, Hq, Hkv, T, dev)
             q = q[:B].contiguous()
-            kc = mxq.quantize_act(k, fmt)
-            vc = mxq.quantize_act(v, fmt)
+            kc = mxq.quantize_rows(k, fmt)
+            vc = mxq.quantize_rows(v, fmt)
             del k, v
             o = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
             work = torch.empty(max(mxq.attn_work_bytes(fmt, B, Hq, Hkv, T), 16),

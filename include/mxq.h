@@ -57,7 +57,7 @@
 extern "C" {
 #endif
 
-#define MXQ_ABI_VERSION 10
+#define MXQ_ABI_VERSION 11
 #define MXQ_BLOCK 32
 /* mxq_gemm uses the weight-streaming decode kernel for M <= this. */
 #define MXQ_DECODE_MAX_M 16
@@ -86,11 +86,10 @@ typedef enum { MXQ_CLAMP_SYMMETRIC = 0, MXQ_CLAMP_FULL = 1 } mxq_clamp;
  *           then 4-bit, 6-bit and 8-bit blocks; any count may be zero).
  *           Width 3 is the floor of the paper's 3-6-8 template (Section 5,
  *           the average-bitwidth study): |q| <= 3 (symmetric) or -4..3
- *           (full), LSB weight 2^(e - 1).  A 3-bit block is stored, in every
- *           layout below, as the 4-bit block holding 2q (the same values:
- *           2q * 2^(e - 2) = q * 2^(e - 1)); it counts as a 4-bit block in
- *           the layouts' segment sizes, and mxq_unpack_* and
- *           mxq_gemm_partials report it as that 4-bit block.
+ *           (full), LSB weight 2^(e - 1).  3-bit blocks form their own
+ *           segment in every layout below and take 3 bits per mantissa in
+ *           the packed rows and in the symmetric-clamp weights;
+ *           mxq_unpack_* and mxq_gemm_partials report their mantissas q.
  *   perm    DEVICE int32[K] or NULL (identity).  Position p of the quantized
  *           row holds source column perm[p].  Entries outside [0, K) are read
  *           as +0.0 (never dereferenced); duplicates are allowed.
@@ -112,85 +111,91 @@ const char *mxq_status_str(int status);
  * Sizes (bytes) of the buffers; negative mxq_status on a bad format or a
  * negative count.
  *
- * Activations (the output of mxq_quantize_act for M rows):
- *   a_mant: M packed rows of mxq_act_packed_bytes(fmt) bytes each, then the
- *   matrix-core operand image: the prefill image (2) for M > 16, the decode
- *   image (3) for 1 <= M <= 16; mxq_act_bytes(fmt, M) in total.
- *   (1) Packed row: the blocks in permuted order, block b taking 4 * m_b
- *   bytes, zero padded to a multiple of 16:
+ * Steps and lanes (shared by the GEMM layouts below).  The K-blocks of a
+ * width map form four segments in order: the 3-bit, 4-bit, 6-bit and 8-bit
+ * blocks.  Each segment is walked in steps, four blocks per step for 3- and
+ * 4-bit blocks and two for 6- and 8-bit blocks (s' = step index within the
+ * segment, blocks counted within the segment; a segment's last step is
+ * completed with zero blocks: mantissas 0, E = 0).  The steps of a segment
+ * form groups of four (the last may be shorter) that share scale words; the
+ * groups of all segments are numbered in order.  A step holds 64 "lanes"
+ * l = 16 g + r (lane group g = 0..3; r = row of a 16-row tile or column of a
+ * 16-column slab): the lane order of the gfx950 block-scaled 16x16x128
+ * matrix-core instruction.
+ *
+ * (A) mxq_quantize_act's output for M rows, the matrix-core operand image:
+ *   a_mant, mxq_act_bytes(fmt, M): ceil(M / 16) tiles of 16 rows (rows past
+ *   M are zero rows), each the steps in order, a step being 64 lanes of 24
+ *   bytes (3-, 4- and 6-bit steps) or 32 bytes (8-bit steps), lane l at
+ *   l * 24 (or 32).  FP6 lanes hold 32 e3m2 codes, element t at bits
+ *   6t..6t+5 of the 24 little-endian bytes; FP8 bytes are e4m3 codes.
+ *     3/4-bit step: lane (g, r) holds block 4s'+g of row r: the e3m2 codes
+ *       of the values q (4-bit) or 2q (3-bit);
+ *     6-bit step: with q = 8h + l, h = floor(q / 8): lane (2j, r) holds the
+ *       codes of h/2 and lane (2j+1, r) those of l/16 for block 2s'+j;
+ *     8-bit step: with q = 16h + l, h = floor(q / 16): for block 2s'+j,
+ *       lane (e, r) bytes 16j..16j+15 hold the codes of 2h and lane
+ *       (2+e, r) bytes 16j..16j+15 those of l/8, for elements 16e..16e+15
+ *       (e = 0, 1).
+ *   a_exp, mxq_act_exp_bytes(fmt, M): per tile, per group, 256 bytes: lane
+ *   l's byte for step k of the group at 4 l + k, the E of the block whose
+ *   codes the lane holds (block 4s'+g, or 2s'+(g >> 1) for 6/8-bit steps),
+ *   0 for zero blocks and for the missing steps of a short group.
+ *   So a lane's codes times 2^(E - 127) are q * 2^(E - 127) times 1 (4-bit),
+ *   2 (3-bit), 1/16 (6-bit, h/2 + l/16) or 1/8 (8-bit, 2h + l/8); the
+ *   weights' digits below carry the rest of 2^-(m - 2) per operand.
+ *
+ * (B) mxq_pack_weights' output for N columns, mxq_weight_bytes(fmt, N): the
+ *   one copy of the weights both GEMMs read, at the size of the mantissas
+ *   under the symmetric clamp (3, 4, 6 and 8 bits per element; the full
+ *   clamp's wider ranges take 4, 6, 8 and 8).
+ *   ceil(N / 128) super-slabs of 128 columns (padding columns are zero),
+ *   each the steps in order, a step being the chunks of its eight 16-column
+ *   slabs (slab n at n * C) of C bytes.  Weight codes: a 3/4-bit mantissa
+ *   is the FP6 code s|k (s = 32 if q < 0, k = |q|), e2m3 for 3-bit blocks
+ *   (the value q/8) and e3m2 for 4-bit blocks (q/16); a 6-bit mantissa,
+ *   |q| = 8h + l, is two e3m2 codes s|h and s|l (h/16 and l/16, the GEMM
+ *   scaling the high plane by 2^3); an 8-bit mantissa is one byte, sign-
+ *   magnitude s|(|q|) (s = 128) under the symmetric clamp and two's
+ *   complement under the full clamp, read as the e4m3 codes of its high
+ *   nibble h (signed, scaled by 2^4) and its low nibble l (sign-magnitude:
+ *   |q| = 16h + l; two's complement: q = 16h + l, 0 <= l <= 15), h/512 and
+ *   l/512.  With D0..D5 the six FP6 words of a lane (32 codes, element t at
+ *   bits 6t of D0..D5), symmetric-clamp codes keep only a few bits per
+ *   field and are stored "folded":
+ *     fold4(D) = D0 | (D1 & 0x18618618), D2 | (D1 & 0x61861861),
+ *                D3 | (D4 & 0x18618618), D5 | (D4 & 0x61861861)  (16 bytes)
+ *     fold3(D) = D0 | D1 >> 1, D3 | D4 >> 1, D2 | D5 << 3 | D5 >> 31
+ *     fold2(D) = D0 | D1 | D2, D3 | D4 | D5  (codes 0|h, h <= 3)
+ *   and the chunks are, for lane l = 16 g + c (column c of the slab):
+ *     3-bit, symmetric (C = 768): fold3 of block 4s'+g: its first two words
+ *       at 8 l, its third at 512 + 4 l; full (C = 1024): fold4 at 16 l;
+ *     4-bit, symmetric (C = 1024): fold4 of block 4s'+g at 16 l; full
+ *       (C = 1536): D0..D3 at 16 l, D4, D5 at 1024 + 8 l;
+ *     6-bit, for block 2s'+j and u = 16 j + c: fold4 of the low codes at
+ *       16 u, then, symmetric (C = 768), fold2 of the high codes without
+ *       their sign at 512 + 8 u (the sign is the low code's), full
+ *       (C = 1024), fold4 of the high codes at 512 + 16 u;
+ *     8-bit (C = 1024): block 2s'+j's 32 bytes at 32 (16 j + c).
+ *   w_exp, mxq_weight_exp_bytes(fmt, N): per super-slab, per group, 2048
+ *   bytes: lane l's 32 bytes at 32 l, slab n's byte for step k of the group
+ *   at 8 k + n: the E of block 4s'+g (3/4-bit) or 2s'+(g >> 1) (6/8-bit) of
+ *   column 16 n + c, 0 for zero blocks and missing steps.
+ *   Read it back with mxq_unpack_weights.
+ *
+ * (C) Packed rows (mxq_quantize_rows; the KV cache of mxq_attn_decode):
+ *   mxq_act_packed_bytes(fmt) bytes per row: the blocks in permuted order,
+ *   block b taking 4 * m_b bytes, zero padded to a multiple of 16:
+ *     3-bit: element t's 3-bit two's complement field at bits 3t..3t+2 of
+ *            the block's 96-bit little-endian integer (12 bytes);
  *     4-bit: byte j holds element 2j in bits 0-3 and element 2j+1 in bits 4-7;
  *     6-bit: 16 bytes of low nibbles in the 4-bit layout, then two 32-bit
  *            words of the signed top two bits: word d covers elements
  *            16d..16d+15, its byte j holds element 16d+2j in bits 6-7,
  *            16d+2j+1 in bits 4-5, 16d+8+2j in bits 2-3, 16d+9+2j in bits 0-1;
  *     8-bit: one two's-complement byte per element.
- *   (2) Prefill image (M > 16): every mantissa q of a block with width m
- *   as exact FP6 / FP8 "digits" whose sum is q * 2^-(m - 2), so that the
- *   block's E8M0 scale is E itself:
- *     m = 4: one FP6 e3m2 element q/4;
- *     m = 6: h = floor(q/8), l = q - 8h; FP6 e3m2 elements h/2 and l/16;
- *     m = 8: h = floor(q/16), l = q - 16h; FP8 e4m3 elements h/4 and l/64.
- *   K is walked in steps: the 4-bit blocks (padded with zero blocks to a
- *   multiple of 4) four at a time, the 6-bit blocks (padded to a multiple of
- *   2) two at a time, the 8-bit blocks one at a time; nsteps is the total.
- *   Step s gives each row two halves h = 0, 1 of 48 bytes ("lane data"):
- *     4-bit step: blocks 4s'+h then 4s'+2+h (s' = index within the
- *       segment), each as 32 e3m2 codes packed little-endian (element t at
- *       bits 6t of the 24 bytes);
- *     6-bit step: block 2s'+h as its h-digit codes, then its l-digit codes;
- *     8-bit step: the h codes of elements 16h..16h+15 (16 bytes), their l
- *       codes (16 bytes), 16 zero bytes.
- *   Rows are grouped in tiles of 32 (the last tile is padded; its rows past
- *   M are unspecified).  Byte o of the lane data of (row r, step s, half h)
- *   is at ((r / 32) * nsteps + s) * 3072 + (o / 16) * 1024 + h * 512
- *   + (r % 32) * 16 + o % 16 of the operand image.
- *   (3) Decode image (M <= 16), the "stream layout" of 16 lines (line =
- *   row; rows past M are unspecified) in the lane order of the block-scaled
- *   16x16x128 matrix-core instruction, lane l = 16 g + line.  Steps: the
- *   4-bit blocks four at a time (padded to a multiple of 4), then the 6-bit
- *   and then the 8-bit blocks two at a time (each padded to a multiple of 2).
- *   Each segment is a run of groups of four steps (the last may be
- *   shorter): a 256-byte scale block (lane l's byte for step k of the group
- *   at 4 l + k), then the steps' lane data:
- *     4-bit step s: lane (g, r) holds block 4s+g of row r as 32 e3m2 codes
- *       of q/4 (first 16 bytes at 16 l, last 8 at 1024 + 8 l); its scale
- *       byte is the E of block 4s+g;
- *     6/8-bit step s: lane (g, r) holds elements 16(g&1)..16(g&1)+15 of
- *       block 2s+(g>>1), at 32 l: the e4m3 codes of their high digits, then
- *       of their low digits (q = 16h + l, h = floor(q/16): h and l/16 for
- *       m = 6, h/4 and l/64 for m = 8); its scale byte is the E of block
- *       2s+(g&1).
- *   a_exp: M rows of mxq_exp_row_bytes(fmt) bytes (block exponents E, byte b
- *   for block b, zero padded to a multiple of 16); for M > 16 then the
- *   prefill image's scale bytes: for (row r, step s, half h) four bytes at
- *   ((r / 32) * nsteps + s) * 256 + h * 128 + (r % 32) * 4: the E of block
- *   4s'+h and of block 4s'+2+h for a 4-bit step, the E of the half's block
- *   and 0 for a 6-bit step, the block's E and 0 (both halves) for an 8-bit
- *   step, then two zero bytes; zero for padding blocks.
- *   mxq_act_exp_bytes(fmt, M) in total.
- *   The GEMM reads the image; mxq_gemm_partials and mxq_unpack_act read the
- *   packed rows.
- * Weights (mxq_pack_weights for N columns), mxq_weight_bytes(fmt, N):
- *   (1) slabs of 16 columns (N rounded up; padding columns are zero) in
- *   the stream layout of (3) above, line = column, but holding the packed
- *   mantissas: per step 64 lanes of 16 / 12 / 16 bytes (4/6/8-bit), lane
- *   (g, c) taking elements 16(g&1)..16(g&1)+15 of block 4s+(g>>1) then of
- *   block 4s+2+(g>>1) (4-bit), or of block 2s+(g>>1) (6/8-bit, the 6-bit
- *   codes as 8 nibble bytes at 8 l plus a 2-bit dword at 512 + 4 l); scale
- *   bytes as in (3).  4-bit codes are sign-magnitude s|(|q|) under the
- *   symmetric clamp and two's complement q mod 16 under the full clamp;
- *   6-bit codes a nibble s|(|q| mod 8) and the 2-bit |q| div 8 (symmetric)
- *   or q mod 16 and bits 4-5 (full); 8-bit codes two's-complement bytes.
- *   Read it back with mxq_unpack_weights.  64 zero bytes follow;
- *   (2) the operand image, tiled by 128 columns (N rounded up; padding
- *   columns are zero): per tile, per step, 13312 bytes: lane data byte o of
- *   (column c of the tile, half h) at (o / 16) * 4096 + h * 2048 + c * 16
- *   + o % 16, then the lane's scale bytes (the two of the activation layout,
- *   then two zero bytes) at 12288 + h * 512 + (c % 32) * 16 + (c / 32) * 4,
- *   so a lane's four 32-column scale dwords are one 16-byte piece.  Weight lane data of an
- *   8-bit step repeats the h codes in its last 16 bytes.
- *   The weight exponents are one row of mxq_exp_row_bytes(fmt) bytes per
- *   (padded to 16) column: w_exp[j * mxq_exp_row_bytes + b].
+ *   Exponent rows of mxq_exp_row_bytes(fmt) bytes: byte b = the E of block
+ *   b, zero padded to a multiple of 16.
  */
 int64_t mxq_act_packed_bytes(const mxq_fmt *fmt);
 int64_t mxq_exp_row_bytes(const mxq_fmt *fmt);
@@ -201,7 +206,8 @@ int64_t mxq_weight_exp_bytes(const mxq_fmt *fmt, int64_t N);
 
 /*
  * Online activation quantization (paper: Section 5, activations of every
- * decoder linear and the KV cache are quantized to MXINT; Section 4.1 widths).
+ * decoder linear are quantized to MXINT; Section 4.1 widths), into the
+ * GEMM's operand image (layout (A) above).
  *   a       DEVICE bf16 [M][lda], lda >= K, read only.
  *   a_mant  DEVICE uint8 [mxq_act_bytes(fmt, M)], written.
  *   a_exp   DEVICE uint8 [mxq_act_exp_bytes(fmt, M)], written.
@@ -209,6 +215,20 @@ int64_t mxq_weight_exp_bytes(const mxq_fmt *fmt, int64_t N);
 mxq_status mxq_quantize_act(const mxq_fmt *fmt, const uint16_t *a, int64_t M,
                             int64_t lda, uint8_t *a_mant, uint8_t *a_exp,
                             void *stream);
+
+/*
+ * The same quantizer writing packed rows (layout (C) above; paper Appendix
+ * A.2: the KV cache is quantized to MXINT as well): the rows that
+ * mxq_attn_decode reads, and the input of mxq_unpack_act and
+ * mxq_gemm_partials.
+ *   a       DEVICE bf16 [M][lda], lda >= K, read only.
+ *   rows    DEVICE uint8 [M * mxq_act_packed_bytes(fmt)], written.
+ *   exps    DEVICE uint8 [M * mxq_exp_row_bytes(fmt)], written.
+ * Errors: as mxq_quantize_act.
+ */
+mxq_status mxq_quantize_rows(const mxq_fmt *fmt, const uint16_t *a, int64_t M,
+                             int64_t lda, uint8_t *rows, uint8_t *exps,
+                             void *stream);
 
 /*
  * The activation quantizer fused with its producer, RMS normalisation (the
@@ -268,14 +288,18 @@ mxq_status mxq_pack_weights(const mxq_fmt *fmt, const uint16_t *w, int64_t N,
 /*
  * MXINT GEMM, Y = Ahat * What^T in fp32 (paper Sections 2 and 6: integer
  * block products, power-of-two block scales).
- *   a_mant/a_exp  DEVICE, from mxq_quantize_act with the same fmt and the
- *                 same M (the operand image's offset depends on M).
+ *   a_mant/a_exp  DEVICE, from mxq_quantize_act (or its fused variants) with
+ *                 the same fmt and at least M rows.
  *   w_mant/w_exp  DEVICE, from mxq_pack_weights with the same fmt and N.
  *   y             DEVICE float [M][ldy], ldy >= N; every y[i][j] with i < M,
  *                 j < N is written, nothing else.
- * M <= MXQ_DECODE_MAX_M runs the weight-streaming decode kernel (the
- * packed slabs turned into FP8 digits in registers, the decode image), larger
- * M the tiled prefill kernel (both prefill images).
+ * M <= MXQ_DECODE_MAX_M runs the weight-streaming decode kernel, larger M
+ * the tiled prefill kernel; both read the same buffers.  The weights' high
+ * digit planes take the scale E + 3 (6-bit) or E + 4 (8-bit), which the
+ * E8M0 format holds up to 254: a 6-bit weight block with E >= 252 or an
+ * 8-bit one with E >= 251 (|w| >= 2^124) makes the outputs it touches NaN.
+ * Errors: MXQ_ERR_SHAPE also when sixteen 16-row activation tiles or a
+ * weight super-slab exceed 2^31 - 1 bytes (K of about four million or more).
  */
 mxq_status mxq_gemm(const mxq_fmt *fmt, int64_t M, int64_t N,
                     const uint8_t *a_mant, const uint8_t *a_exp,
@@ -283,13 +307,17 @@ mxq_status mxq_gemm(const mxq_fmt *fmt, int64_t M, int64_t N,
                     int64_t ldy, void *stream);
 
 /*
- * Debug / parity entry points (not on the hot path).
- * mxq_unpack_act / mxq_unpack_weights: packed -> canonical mantissas
- *   q DEVICE int8 [rows][K] (permuted order) and exponents e DEVICE uint8
- *   [rows][K/32].
- * mxq_gemm_partials: the exact per-block int32 sums
- *   p DEVICE int32 [M][N][K/32], from the packed mantissas on int8 matrix
- *   cores (one exact int32 sum per block).
+ * Debug / parity entry points (not on the hot path; they restate Section 2's
+ * block arithmetic one element at a time).
+ * mxq_unpack_act: packed rows and exponent rows (mxq_quantize_rows) ->
+ *   mantissas q DEVICE int8 [rows][K] (permuted order) and exponents e
+ *   DEVICE uint8 [rows][K/32].
+ * mxq_unpack_weights: the same from mxq_pack_weights' buffers.
+ * mxq_gemm_partials: the exact per-block integer sums
+ *   P[i][j][b] = sum_t qa[i][32b+t] * qw[j][32b+t] (Section 2's integer
+ *   block product) as p DEVICE int32 [M][N][K/32], one thread per sum, from
+ *   packed rows (a_mant/a_exp as written by mxq_quantize_rows for M rows)
+ *   and the packed weights.
  */
 mxq_status mxq_unpack_act(const mxq_fmt *fmt, int64_t rows,
                           const uint8_t *a_mant, const uint8_t *a_exp,
@@ -396,13 +424,13 @@ mxq_status mxq_peak_mfma(int kind, int64_t iters, float *sink, int64_t *ops,
  *   Hq / Hkv <= 16, T >= 1.
  *   scale   finite (usually 1 / sqrt(128)).
  *   k_mant, v_mant   DEVICE, 16-byte aligned: packed rows of
- *           mxq_act_packed_bytes(fmt) bytes (section (1) of the activation
- *           layout above), row (b * T + t) * Hkv + k; the a_mant written by
- *           mxq_quantize_act for M = B * T * Hkv rows of [.][128] serves
- *           as is.  Read only.
+ *           mxq_act_packed_bytes(fmt) bytes (layout (C) above), row
+ *           (b * T + t) * Hkv + k; the rows written by mxq_quantize_rows
+ *           for M = B * T * Hkv rows of [.][128] serve as they are.  Read
+ *           only.
  *   k_exp, v_exp     DEVICE, 16-byte aligned: exponent rows of
- *           mxq_exp_row_bytes(fmt) bytes, same row order (mxq_quantize_act's
- *           a_exp).  Read only.
+ *           mxq_exp_row_bytes(fmt) bytes, same row order (mxq_quantize_rows'
+ *           exps).  Read only.
  *   o       DEVICE float32 [B][Hq][128], written.
  *   work    DEVICE, 16-byte aligned, work_bytes >= mxq_attn_work_bytes(...):
  *           the caller's scratch for per-split partial results; its

@@ -4,7 +4,7 @@ The compute path is the HIP library ``libmxq.so`` behind the C ABI in
 ``include/mxq.h``; ``paper_2607_17733_amd.mxq`` is its Python binding and
 ``paper_2607_17733_amd.workloads`` draws the seeded synthetic inputs.
 """
-_BINDING = ("Format", "MxqError", "quantize_act", "pack_weights", "gemm",
+_BINDING = ("Format", "MxqError", "quantize_act", "quantize_rows", "pack_weights", "gemm",
             "gemm_partials", "unpack_act", "unpack_weights", "lib")
 
 

@@ -55,36 +55,34 @@ mxq_status check_fmt(const mxq_fmt *f, Segs *s) {
   return MXQ_OK;
 }
 
-int64_t row_used(const Segs &s) { return 16LL * s.n4 + 24LL * s.n6 + 32LL * s.n8; }
+int64_t row_used(const Segs &s) { return mxq::packed_row_used(s); }
 // packed section and per-row exponent section
 int64_t canon_rb(const Segs &s) { return round_up(row_used(s), 16); }
 int64_t exp_rb(const mxq_fmt *f) { return round_up(f->K / MXQ_BLOCK, 16); }
-mxq::OpGeo op_geo(const Segs &s) { return mxq::OpGeo(s.n4, s.n6, s.n8); }
-mxq::DGeo d_geo(const Segs &s) { return mxq::DGeo(s.n4, s.n6, s.n8); }
-bool decode_batch(int64_t M) { return M > 0 && M <= MXQ_DECODE_MAX_M; }
-// activation buffers: M packed rows, then the operand image (32-row tiles
-// for the prefill GEMM, or the 16-row decode image for M <= 16);
-// exponent buffers: M exponent rows, then the prefill image's scale bytes
-int64_t act_bytes(const Segs &s, int64_t M) {
-  return M * canon_rb(s) + (decode_batch(M) ? mxq::ad_image_bytes(d_geo(s))
-                                            : mxq::act_op_bytes(op_geo(s), M));
+mxq::LGeo l_geo(const Segs &s) { return mxq::LGeo(s.n3, s.n4, s.n6, s.n8); }
+bool full_clamp(const mxq_fmt *f) { return f->clamp == MXQ_CLAMP_FULL; }
+// activation operand image: 16-row tiles, and their scale words
+int64_t act_tiles(int64_t M) { return (M + mxq::kATileRows - 1) / mxq::kATileRows; }
+int64_t act_bytes(const Segs &s, int64_t M) { return act_tiles(M) * mxq::a_tile_bytes(l_geo(s)); }
+int64_t act_exp_bytes(const Segs &s, int64_t M) {
+  return act_tiles(M) * mxq::a_tile_scale_bytes(l_geo(s));
 }
-int64_t act_exp_bytes(const mxq_fmt *f, const Segs &s, int64_t M) {
-  return M * exp_rb(f) + (decode_batch(M) ? 0 : mxq::act_sc_bytes(op_geo(s), M));
+// weights: 128-column super-slabs, and their scale words
+int64_t w_supers(int64_t N) { return (N + mxq::kWCols - 1) / mxq::kWCols; }
+int64_t w_bytes(const mxq_fmt *f, const Segs &s, int64_t N) {
+  return w_supers(N) * mxq::w_super_bytes(l_geo(s), full_clamp(f));
 }
-// weights: 16-column slabs in the stream layout (N rounded to 16), tail
-// padding, then the operand image (N rounded to 128)
-int64_t w_packed(const Segs &s, int64_t N) {
-  return round_up(N, 16) / 16 * mxq::wd_slab_bytes(d_geo(s));
+int64_t w_exp_bytes(const Segs &s, int64_t N) {
+  return w_supers(N) * mxq::w_super_scale_bytes(l_geo(s));
 }
-int64_t w_op_off(const Segs &s, int64_t N) { return w_packed(s, N) + kWeightTailPad; }
-int64_t w_tile(const Segs &s) { return mxq::op_tile_bytes(op_geo(s)); }
 
 mxq_status launched(hipError_t e) { return e == hipSuccess ? MXQ_OK : MXQ_ERR_DEVICE; }
 
+enum QuantKind { kWeights, kImage, kRows };
+
 mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows,
                            int64_t ld, uint8_t *mant, uint8_t *exp, void *stream,
-                           bool weights, const uint16_t *gain = nullptr, float eps = 0.f,
+                           QuantKind kind, const uint16_t *gain = nullptr, float eps = 0.f,
                            const uint16_t *src2 = nullptr) {
   Segs s;
   mxq_status st = check_fmt(fmt, &s);
@@ -104,10 +102,6 @@ mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows
   a.src = src;
   a.ld = ld;
   a.src_rows = rows;
-  a.out_rows = weights ? round_up(rows, mxq::kOpCols) : rows;
-  a.slab_rows = round_up(rows, 16);
-  a.w_op = weights ? w_op_off(s, rows) : 0;
-  a.w_tile = w_tile(s);
   a.K = fmt->K;
   a.perm = fmt->perm;
   a.n4 = s.n4;
@@ -115,32 +109,37 @@ mxq_status quantize_common(const mxq_fmt *fmt, const uint16_t *src, int64_t rows
   a.n8 = s.n8;
   a.n3 = s.n3;
   a.ties_away = fmt->round == MXQ_ROUND_NEAREST_AWAY;
-  a.full_clamp = fmt->clamp == MXQ_CLAMP_FULL;
-  a.mant = mant;
-  a.exp = exp;
+  a.full_clamp = full_clamp(fmt);
+  a.vec16 = (ld % 8 == 0) ? 1 : 0;
+  if (kind == kWeights) {
+    a.out_rows = round_up(rows, mxq::kWCols);
+    a.mant = mant;
+    a.exp = exp;
+    return launched(mxq::launch_quantize(a, true, (hipStream_t)stream));
+  }
   a.canon_rb = canon_rb(s);
   a.canon_erb = exp_rb(fmt);
-  a.out_rb = weights ? 0 : canon_rb(s);
-  a.out_erb = exp_rb(fmt);
-  a.op_off = weights ? 0 : rows * canon_rb(s);
-  a.sc_off = weights ? 0 : rows * exp_rb(fmt);
   a.row_used = row_used(s);
-  a.tail_pad = weights ? (int)kWeightTailPad : 0;
-  a.vec16 = (ld % 8 == 0) ? 1 : 0;
-  if (!weights) {
-    a.dimg = decode_batch(rows) ? 1 : 0;
-    // the activation quantizer stages its rows in LDS: one row must fit
-    const mxq::OpGeo og = op_geo(s);
-    if (mxq::quantize_act_lds(fmt->K, og.n4p + og.n6p + og.n8 + (og.n8 & 1),
-                              fmt->perm != nullptr, gain != nullptr) > mxq::kMaxLds)
-      return MXQ_ERR_UNSUPPORTED;
-    return launched(mxq::launch_quantize_act(a, (hipStream_t)stream));
+  if (kind == kRows) {
+    a.write_rows = 1;
+    a.out_rows = rows;
+    a.mant = mant;
+    a.exp = exp;
+    a.out_rb = canon_rb(s);
+    a.out_erb = exp_rb(fmt);
+  } else {
+    a.write_image = 1;
+    a.out_rows = round_up(rows, mxq::kATileRows);
+    a.img = mant;
+    a.img_exp = exp;
+    a.a_tile = mxq::a_tile_bytes(l_geo(s));
+    a.a_tile_sc = mxq::a_tile_scale_bytes(l_geo(s));
   }
-  // Stage source rows in LDS for the permutation gather when they fit;
-  // longer rows gather straight from global memory.
-  const int R = mxq::quantize_rows_per_wg(fmt->K);
-  a.stage = (fmt->perm && (int64_t)R * fmt->K * 2 <= mxq::kMaxLds) ? 1 : 0;
-  return launched(mxq::launch_quantize(a, true, (hipStream_t)stream));
+  // the activation quantizer stages its rows in LDS: one row must fit
+  if (mxq::quantize_act_lds(fmt->K, mxq::quantize_act_padded_blocks(s.n3, s.n4, s.n6, s.n8),
+                            fmt->perm != nullptr, gain != nullptr) > mxq::kMaxLds)
+    return MXQ_ERR_UNSUPPORTED;
+  return launched(mxq::launch_quantize_act(a, (hipStream_t)stream));
 }
 
 mxq_status gemm_args(const mxq_fmt *fmt, int64_t M, int64_t N, const uint8_t *a_mant,
@@ -155,13 +154,13 @@ mxq_status gemm_args(const mxq_fmt *fmt, int64_t M, int64_t N, const uint8_t *a_
   if (!aligned16(a_mant) || !aligned16(a_exp) || !aligned16(w_mant) ||
       !aligned16(w_exp) || !aligned16(out))
     return MXQ_ERR_ALIGN;
-  // The prefill kernel addresses each wave's two 32-row activation tiles and
-  // each 128-column weight tile with 32-bit buffer offsets from a 64-bit base.
-  {
-    const mxq::OpGeo og = op_geo(s);
-    if (2LL * og.nsteps * mxq::kActStep > INT32_MAX || w_tile(s) > INT32_MAX)
-      return MXQ_ERR_SHAPE;
-  }
+  const mxq::LGeo lg = l_geo(s);
+  // The prefill kernel addresses a workgroup's 256 activation rows (16
+  // tiles) and one weight super-slab with 32-bit buffer offsets from a
+  // 64-bit base.
+  if (16 * mxq::a_tile_bytes(lg) > INT32_MAX ||
+      mxq::w_super_bytes(lg, full_clamp(fmt)) > INT32_MAX)
+    return MXQ_ERR_SHAPE;
   *g = mxq::GemmArgs{};
   g->a_mant = a_mant;
   g->a_exp = a_exp;
@@ -171,16 +170,15 @@ mxq_status gemm_args(const mxq_fmt *fmt, int64_t M, int64_t N, const uint8_t *a_
   g->N = N;
   g->a_rb = canon_rb(s);
   g->a_erb = exp_rb(fmt);
-  g->a_op = M * canon_rb(s);
-  g->a_sc = M * exp_rb(fmt);
-  g->w_erb = exp_rb(fmt);
-  g->w_op = w_op_off(s, N);
-  g->w_tile = w_tile(s);
-  g->npad = round_up(N, 16);
+  g->a_tile = mxq::a_tile_bytes(lg);
+  g->a_tile_sc = mxq::a_tile_scale_bytes(lg);
+  g->w_super = mxq::w_super_bytes(lg, full_clamp(fmt));
+  g->w_super_sc = mxq::w_super_scale_bytes(lg);
+  g->n3 = s.n3;
   g->n4 = s.n4;
   g->n6 = s.n6;
   g->n8 = s.n8;
-  g->sm = fmt->clamp == MXQ_CLAMP_SYMMETRIC ? 1 : 0;
+  g->full = full_clamp(fmt) ? 1 : 0;
   return MXQ_OK;
 }
 
@@ -225,7 +223,7 @@ int64_t mxq_act_exp_bytes(const mxq_fmt *fmt, int64_t M) {
   const mxq_status st = check_fmt(fmt, &s);
   if (st != MXQ_OK) return -(int64_t)st;
   if (M < 0) return -(int64_t)MXQ_ERR_SHAPE;
-  return act_exp_bytes(fmt, s, M);
+  return act_exp_bytes(s, M);
 }
 
 int64_t mxq_exp_row_bytes(const mxq_fmt *fmt) {
@@ -245,7 +243,7 @@ int64_t mxq_weight_bytes(const mxq_fmt *fmt, int64_t N) {
   const mxq_status st = check_fmt(fmt, &s);
   if (st != MXQ_OK) return -(int64_t)st;
   if (N < 0) return -(int64_t)MXQ_ERR_SHAPE;
-  return w_op_off(s, N) + round_up(N, mxq::kOpCols) / mxq::kOpCols * w_tile(s);
+  return w_bytes(fmt, s, N);
 }
 
 int64_t mxq_weight_exp_bytes(const mxq_fmt *fmt, int64_t N) {
@@ -253,13 +251,18 @@ int64_t mxq_weight_exp_bytes(const mxq_fmt *fmt, int64_t N) {
   const mxq_status st = check_fmt(fmt, &s);
   if (st != MXQ_OK) return -(int64_t)st;
   if (N < 0) return -(int64_t)MXQ_ERR_SHAPE;
-  return round_up(N, 16) * exp_rb(fmt);
+  return w_exp_bytes(s, N);
 }
 
 mxq_status mxq_quantize_act(const mxq_fmt *fmt, const uint16_t *a, int64_t M,
                             int64_t lda, uint8_t *a_mant, uint8_t *a_exp,
                             void *stream) {
-  return quantize_common(fmt, a, M, lda, a_mant, a_exp, stream, false);
+  return quantize_common(fmt, a, M, lda, a_mant, a_exp, stream, kImage);
+}
+
+mxq_status mxq_quantize_rows(const mxq_fmt *fmt, const uint16_t *a, int64_t M, int64_t lda,
+                             uint8_t *rows, uint8_t *exps, void *stream) {
+  return quantize_common(fmt, a, M, lda, rows, exps, stream, kRows);
 }
 
 mxq_status mxq_quantize_act_rmsnorm(const mxq_fmt *fmt, const uint16_t *x, int64_t M,
@@ -267,20 +270,20 @@ mxq_status mxq_quantize_act_rmsnorm(const mxq_fmt *fmt, const uint16_t *x, int64
                                     uint8_t *a_mant, uint8_t *a_exp, void *stream) {
   if (M > 0 && !gain) return MXQ_ERR_NULL;
   if (!(eps >= 0.f)) return MXQ_ERR_SHAPE;
-  return quantize_common(fmt, x, M, ldx, a_mant, a_exp, stream, false, gain, eps);
+  return quantize_common(fmt, x, M, ldx, a_mant, a_exp, stream, kImage, gain, eps);
 }
 
 mxq_status mxq_quantize_act_swiglu(const mxq_fmt *fmt, const uint16_t *gate,
                                    const uint16_t *up, int64_t M, int64_t ld,
                                    uint8_t *a_mant, uint8_t *a_exp, void *stream) {
   if (M > 0 && !up) return MXQ_ERR_NULL;
-  return quantize_common(fmt, gate, M, ld, a_mant, a_exp, stream, false, nullptr, 0.f, up);
+  return quantize_common(fmt, gate, M, ld, a_mant, a_exp, stream, kImage, nullptr, 0.f, up);
 }
 
 mxq_status mxq_pack_weights(const mxq_fmt *fmt, const uint16_t *w, int64_t N,
                             int64_t ldw, uint8_t *w_mant, uint8_t *w_exp,
                             void *stream) {
-  return quantize_common(fmt, w, N, ldw, w_mant, w_exp, stream, true);
+  return quantize_common(fmt, w, N, ldw, w_mant, w_exp, stream, kWeights);
 }
 
 mxq_status mxq_gemm(const mxq_fmt *fmt, int64_t M, int64_t N, const uint8_t *a_mant,
@@ -329,11 +332,13 @@ static mxq_status unpack_common(const mxq_fmt *fmt, int64_t rows, const uint8_t 
   a.K = fmt->K;
   a.a_rb = canon_rb(s);
   a.a_erb = exp_rb(fmt);
-  a.npad = round_up(rows, 16);
+  a.w_super = mxq::w_super_bytes(l_geo(s), full_clamp(fmt));
+  a.w_super_sc = mxq::w_super_scale_bytes(l_geo(s));
+  a.n3 = s.n3;
   a.n4 = s.n4;
   a.n6 = s.n6;
   a.n8 = s.n8;
-  a.sm = fmt->clamp == MXQ_CLAMP_SYMMETRIC ? 1 : 0;
+  a.full = full_clamp(fmt) ? 1 : 0;
   return launched(mxq::launch_unpack(a, weights, (hipStream_t)stream));
 }
 
@@ -502,6 +507,7 @@ static mxq_status attn_common(const mxq_fmt *fmt, const uint16_t *q, int64_t B, 
   a.exp_bytes = exp_rb(fmt);
   a.tokens_per_split = tps;
   a.splits = (int)splits;
+  a.n3 = sg.n3;
   a.n4 = sg.n4;
   a.n6 = sg.n6;
   a.n8 = sg.n8;

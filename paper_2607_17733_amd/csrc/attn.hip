@@ -78,14 +78,15 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kMaxG = 16;
 constexpr int kChunk = 32;         // tokens per wave step: the value product's reduction
 
-template <int N4, int N6, int N8>
+// The four blocks of a cache row (head dimension 128): N3 3-bit, N4 4-bit,
+// N6 6-bit and N8 8-bit blocks, in that order.
+template <int N3, int N4, int N6, int N8>
 struct Geo {
-  static constexpr int width(int b) { return b < N4 ? 4 : b < N4 + N6 ? 6 : 8; }
-  static constexpr int off(int b) {
-    return b < N4 ? 16 * b : b < N4 + N6 ? 16 * N4 + 24 * (b - N4)
-                                         : 16 * N4 + 24 * N6 + 32 * (b - N4 - N6);
+  static constexpr int width(int b) {
+    return b < N3 ? 3 : b < N3 + N4 ? 4 : b < N3 + N4 + N6 ? 6 : 8;
   }
-  static constexpr int kRow = (16 * N4 + 24 * N6 + 32 * N8 + 15) / 16 * 16;
+  static constexpr int off(int b) { return b == 0 ? 0 : off(b - 1) + 4 * width(b - 1); }
+  static constexpr int kRow = (off(4) + 15) / 16 * 16;
   static constexpr int kVec = kRow / 16;                  // 16-byte pieces per row
   // LDS row stride of 8k + 4 dwords: 16 lanes' 16-byte accesses hit distinct banks
   static constexpr int kLds = (kRow + 31) / 32 * 32 + 16;
@@ -104,7 +105,13 @@ __device__ inline float block_scale(uint32_t ex, int blk) {
 // Mantissas 8g .. 8g+7 of the block at p (a K row in LDS).
 template <int M>
 __device__ inline void mants8(const uint8_t *p, int g, int (&q)[8]) {
-  if (M == 8) {
+  if (M == 3) {
+    // elements 8g..8g+7: bits 24g..24g+23 of the block, bytes 3g..3g+2
+    const uint32_t w = (uint32_t)p[3 * g] | ((uint32_t)p[3 * g + 1] << 8) |
+                       ((uint32_t)p[3 * g + 2] << 16);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) q[j] = sext((w >> (3 * j)) & 7u, 3);
+  } else if (M == 8) {
     const u2 w = *(const u2 *)(p + 8 * g);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -132,6 +139,13 @@ __device__ inline void mants8(const uint8_t *p, int g, int (&q)[8]) {
 template <int M>
 __device__ inline int mant1(const uint8_t *p, int e) {
   if (M == 8) return (int)(int8_t)p[e];
+  if (M == 3) {
+    // bits 3e..3e+2; the byte after the block is read for e = 31 but its
+    // bits are shifted out (the row in LDS continues past the block)
+    const int bit = 3 * e;
+    const uint32_t v = (uint32_t)p[bit >> 3] | ((uint32_t)p[(bit >> 3) + 1] << 8);
+    return sext((v >> (bit & 7)) & 7u, 3);
+  }
   if (M == 4) return __builtin_amdgcn_sbfe((int)p[e >> 1], 4 * (e & 1), 4);
   const uint32_t nib = __builtin_amdgcn_ubfe((uint32_t)p[e >> 1], 4 * (e & 1), 4);
   const int u = e & 15;
@@ -182,9 +196,9 @@ __device__ inline void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <int N4, int N6, int N8>
+template <int N3, int N4, int N6, int N8>
 __global__ __launch_bounds__(kThreads, 2) void attn_decode_kernel(AttnArgs a) {
-  using Gm = Geo<N4, N6, N8>;
+  using Gm = Geo<N3, N4, N6, N8>;
   constexpr int kStage = 2 * kChunk * Gm::kLds;           // a wave's K rows, then V rows
   constexpr int kMerge = kWaves * kMaxG * kD * 4;
   constexpr int kPool = kWaves * kStage > kMerge ? kWaves * kStage : kMerge;
@@ -413,11 +427,29 @@ __global__ __launch_bounds__(kD * kCombGroups) void attn_combine_kernel(AttnArgs
   }
 }
 
-template <int N4, int N6, int N8>
+template <int N3, int N4, int N6, int N8>
 void launch_t(const AttnArgs &a, hipStream_t s) {
-  hipLaunchKernelGGL((attn_decode_kernel<N4, N6, N8>),
+  hipLaunchKernelGGL((attn_decode_kernel<N3, N4, N6, N8>),
                      dim3((unsigned)a.splits, (unsigned)a.Hkv, (unsigned)a.B), dim3(kThreads), 0,
                      s, a);
+}
+
+// The kernel for a row's width mix, code = 125 n3 + 25 n4 + 5 n6 + n8 (the
+// 35 mixes of four blocks).
+template <int C>
+bool dispatch(int code, const AttnArgs &a, hipStream_t s) {
+  constexpr int n3 = C / 125, n4 = C / 25 % 5, n6 = C / 5 % 5, n8 = C % 5;
+  if constexpr (n3 + n4 + n6 + n8 == 4) {
+    if (code == C) {
+      launch_t<n3, n4, n6, n8>(a, s);
+      return true;
+    }
+  }
+  if constexpr (C > 0) {
+    return dispatch<C - 1>(code, a, s);
+  } else {
+    return false;
+  }
 }
 
 }  // namespace
@@ -432,24 +464,9 @@ int64_t attn_tokens_per_split(int64_t B, int64_t Hkv, int64_t T) {
 }
 
 hipError_t launch_attn_decode(const AttnArgs &a, hipStream_t s) {
-  switch (a.n4 * 25 + a.n6 * 5 + a.n8) {
-    case 100: launch_t<4, 0, 0>(a, s); break;
-    case 80: launch_t<3, 1, 0>(a, s); break;
-    case 76: launch_t<3, 0, 1>(a, s); break;
-    case 60: launch_t<2, 2, 0>(a, s); break;
-    case 56: launch_t<2, 1, 1>(a, s); break;
-    case 52: launch_t<2, 0, 2>(a, s); break;
-    case 40: launch_t<1, 3, 0>(a, s); break;
-    case 36: launch_t<1, 2, 1>(a, s); break;
-    case 32: launch_t<1, 1, 2>(a, s); break;
-    case 28: launch_t<1, 0, 3>(a, s); break;
-    case 20: launch_t<0, 4, 0>(a, s); break;
-    case 16: launch_t<0, 3, 1>(a, s); break;
-    case 12: launch_t<0, 2, 2>(a, s); break;
-    case 8: launch_t<0, 1, 3>(a, s); break;
-    case 4: launch_t<0, 0, 4>(a, s); break;
-    default: return hipErrorInvalidValue;
-  }
+  const int n3 = a.n3, n4 = a.n4 - a.n3;
+  if (n3 < 0 || n4 < 0 || n3 + n4 + a.n6 + a.n8 != 4) return hipErrorInvalidValue;
+  if (!dispatch<500>(125 * n3 + 25 * n4 + 5 * a.n6 + a.n8, a, s)) return hipErrorInvalidValue;
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)a.Hq, (unsigned)a.B), dim3(kD * kCombGroups),

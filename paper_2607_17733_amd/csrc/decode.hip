@@ -1,31 +1,27 @@
 // decode.hip -- MXINT GEMM for decode shapes (M <= 16), streaming the
-// packed weights at HBM rate.
+// weights at HBM rate.
 //
 // Y[i][j] = sum_b 2^(sa[i][b] + sw[j][b]) * sum_t qa qw  (MXSens, arXiv
 // 2607.17733, Section 2: integer block products with power-of-two block
 // scales; Section 6: the memory cost is the packed weights).
 //
-// The weights stay packed in HBM (4m bits per element, stream layout in
-// mxq_device.h) and become FP8 e4m3 digits in registers.  With the block's
-// E as the E8M0 scale the digits must sum to q * 2^-(m-2): a 4-bit q becomes
-// e4m3(q/4); a 6-bit q two digits summing to q/16; an 8-bit q = 16h + l the
-// digits e4m3(h/4) and e4m3(l/64).  Sign-magnitude codes (symmetric clamp)
-// take one V_PERM_B32 over an 8-entry magnitude table plus the sign bit per
-// four codes; two's-complement nibbles a 16-entry table (three permutes).
-// The activations arrive as ready FP6/FP8 digits (decode image).
-// V_MFMA_SCALE_F32_16X16X128_F8F6F4 multiplies 16 rows by
-// 16 columns over four K-blocks and applies every block's E8M0 scale in
-// hardware, so no per-block rescale runs on the VALU.  Digit products are
-// exact; a 6/8-bit block pair takes two instructions (the second with the
-// weight digits' halves swapped: h*h + l*l, then h*l + l*h).
+// The weights are read in the one layout both GEMMs share (LGeo in
+// mxq_device.h): folded FP6 codes for 3- and 4-bit blocks, two digit planes
+// for 6-bit blocks, mantissa bytes for 8-bit blocks, at the MXINT size.  The
+// lane restores its FP6 operand with a few masks and shifts (FP8 digit codes
+// of an 8-bit block from its bytes), and V_MFMA_SCALE_F32_16X16X128_F8F6F4
+// multiplies 16 activation rows by 16 columns over four K-blocks, applying
+// every block's E8M0 scale in hardware.  A 6- or 8-bit step (two blocks,
+// each as its two digit planes) takes two instructions: the weights' high
+// plane in every lane (scale E + 3 or E + 4), then their low plane.  The
+// activations arrive as ready FP6/FP8 codes (the operand image).
 //
 // Work decomposition: the kernel is bound by the number of vector memory
 // loads, so each load serves as many products as possible.  A workgroup
-// owns a pair of 16-column slabs (one activation load feeds both), its nw
-// waves (2 to 16, about 16 waves per CU with every pair resident) taking
-// every nw-th group of four steps of each width segment; a group's scale
-// bytes are one dword per lane and operand (op_sel picks the step).  The
-// waves' fp32 accumulators meet in LDS in a fixed order.
+// owns a pair of 16-column slabs (one activation load feeds both); its nw
+// waves (2 to 16, about 16 waves per CU with every pair resident) take every
+// nw-th group of four steps; a group's scale bytes are one word per lane and
+// operand.  The waves' fp32 accumulators meet in LDS in a fixed order.
 #include <type_traits>
 
 #include "mxq_device.h"
@@ -39,281 +35,237 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef unsigned u4 __attribute__((ext_vector_type(4)));
 typedef unsigned u2 __attribute__((ext_vector_type(2)));
+typedef unsigned u3 __attribute__((ext_vector_type(3)));
 
+constexpr int kFmtE4M3 = 0, kFmtE2M3 = 2, kFmtE3M2 = 3;
+constexpr int kMaxWaves = 16;
 
-// FP8 e4m3 code of num / den (den a power of two; the value must be exact).
-constexpr uint32_t e4m3_exact(int num, int den) {
-  if (num == 0) return 0;
-  const uint32_t sign = num < 0 ? 0x80u : 0u;
-  int a = num < 0 ? -num : num;
-  int e = 0;                               // a / den = (a / 2^p) * 2^(p - log2 den)
-  while ((a >> e) > 1) ++e;                // a in [2^e, 2^(e+1))
-  int lg = 0;
-  while ((1 << lg) < den) ++lg;
-  const int ue = e - lg;                   // unbiased exponent of the value
-  const uint32_t mant = (uint32_t)(((a << 3) >> e) & 7);
-  return sign | ((uint32_t)(ue + 7) << 3) | mant;
-}
-
-// The packed weights are read exactly once: non-temporal loads stream them
-// past the caches (measured on gfx950: 6.9 TB/s for a plain streaming read
-// against 6.2 TB/s with ordinary loads).  Activations stay cached; every
-// workgroup reads them.
+// The weights are read exactly once: non-temporal loads stream them past the
+// caches.  Activations stay cached; every workgroup reads them.
 template <typename T>
 __device__ inline T stream_load(const T *p) {
   return __builtin_nontemporal_load(p);
 }
 
-// 16-entry byte table (entry n = f(n)) as four dwords
-template <int KIND>
-constexpr uint32_t table_dword(int d) {
-  uint32_t v = 0;
-  for (int k = 0; k < 4; ++k) {
-    const int n = 4 * d + k;
-    const int sn = n < 8 ? n : n - 16;     // two's-complement nibble
-    uint32_t c = 0;
-    if (KIND == 0) c = e4m3_exact(sn, 4);        // 4-bit q -> q/4; 8-bit high h -> h/4
-    if (KIND == 1) c = e4m3_exact(n, 16);        // 6-bit low digit l -> l/16
-    if (KIND == 2) c = e4m3_exact(n, 64);        // 8-bit low digit l -> l/64
-    v |= c << (8 * k);
-  }
-  return v;
-}
-
-// 2-bit signed high digit h of a 6-bit mantissa -> e4m3(h): h = 0, 1, -2, -1
-constexpr uint32_t kTop6 = e4m3_exact(0, 1) | (e4m3_exact(1, 1) << 8) |
-                           (e4m3_exact(-2, 1) << 16) | (e4m3_exact(-1, 1) << 24);
-
-// Sign-magnitude codes (symmetric clamp): 8-entry magnitude tables, entry
-// k = e4m3(k / den), as two dwords; the 2-bit high part of a 6-bit
-// magnitude (|q| div 8) -> e4m3(h/2).
-constexpr uint32_t mag_dword(int den, int d) {
-  uint32_t v = 0;
-  for (int k = 0; k < 4; ++k) v |= e4m3_exact(4 * d + k, den) << (8 * k);
-  return v;
-}
-constexpr uint32_t kTop6m = e4m3_exact(0, 2) | (e4m3_exact(1, 2) << 8) |
-                            (e4m3_exact(2, 2) << 16) | (e4m3_exact(3, 2) << 24);
-
-// e4m3 digits of the low / high nibble codes of x (sign at bit 3 of each
-// nibble, magnitude index in bits 0-2): one byte permute and the sign bit.
-template <int DEN>
-__device__ inline uint32_t mag_lo(uint32_t x) {
-  const uint32_t c = __builtin_amdgcn_perm(mag_dword(DEN, 1), mag_dword(DEN, 0), x & 0x07070707u);
-  return c | ((x & 0x08080808u) << 4);
-}
-template <int DEN>
-__device__ inline uint32_t mag_hi(uint32_t x) {
-  const uint32_t c =
-      __builtin_amdgcn_perm(mag_dword(DEN, 1), mag_dword(DEN, 0), (x >> 4) & 0x07070707u);
-  return c | (x & 0x80808080u);
-}
-
-// Byte-wise lookup: byte k of s holds an index in its low nibble.
-template <int KIND>
-__device__ inline uint32_t lut16(uint32_t s) {
-  const uint32_t s7 = s & 0x07070707u;
-  const uint32_t lo = __builtin_amdgcn_perm(table_dword<KIND>(1), table_dword<KIND>(0), s7);
-  const uint32_t hi = __builtin_amdgcn_perm(table_dword<KIND>(3), table_dword<KIND>(2), s7);
-  const uint32_t sel = ((s >> 1) & 0x04040404u) | 0x03020100u;
-  return __builtin_amdgcn_perm(hi, lo, sel);
-}
-
-constexpr int kMaxWaves = 16;
-
-// Block-scaled 16x16x128 product; the scale bytes of step K of a group sit
-// in byte K of the scale dwords (op_sel).  FA: format of A (3 = e3m2 FP6,
-// 0 = e4m3 FP8); B is e4m3.
-template <int FA, int K>
+template <int FA, int FB, int K>
 __device__ inline v4f mfma(const v8i &a, const v8i &b, v4f acc, uint32_t as, uint32_t ws) {
-  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, acc, FA, 0, K, (int)as, K,
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, acc, FA, FB, K, (int)as, K,
                                                           (int)ws);
 }
 
-// FP8 digits of the 16 weight elements of a 4-bit lane (four nibble dwords).
-template <bool SM>
-__device__ inline v8i digits4(const u4 &w) {
-  v8i b;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    if (SM) {
-      b[2 * i] = (int)mag_lo<4>(w[i]);
-      b[2 * i + 1] = (int)mag_hi<4>(w[i]);
-    } else {
-      b[2 * i] = (int)lut16<0>(w[i]);
-      b[2 * i + 1] = (int)lut16<0>(w[i] >> 4);
-    }
-  }
-  return b;
+// E8M0 scale e + n, saturating at 255 (NaN), per byte of a scale word.
+template <int N>
+__device__ inline uint32_t scale_plus(uint32_t w) {
+  const uint32_t lo = (w & 0x00FF00FFu) + (N | (N << 16));
+  const uint32_t hi = ((w >> 8) & 0x00FF00FFu) + (N | (N << 16));
+  const uint32_t lo_s = lo | (((lo & 0x01000100u) >> 8) * 0xFFu);
+  const uint32_t hi_s = hi | (((hi & 0x01000100u) >> 8) * 0xFFu);
+  return (lo_s & 0x00FF00FFu) | ((hi_s & 0x00FF00FFu) << 8);
 }
 
-// High and low FP8 digits of the 16 elements of a 6- or 8-bit weight lane.
-template <bool SM, int SEG>
-__device__ inline void digits68(const u4 &w, uint32_t (&hd)[4], uint32_t (&ld)[4]) {
-  if (SEG == 1 && SM) {
-    // |q| = 8h + l: low digits l/16 from the nibble codes (with the sign),
-    // high digits h/2 from the 2-bit codes plus the same sign
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      ld[2 * i] = mag_lo<16>(w[i]);
-      ld[2 * i + 1] = mag_hi<16>(w[i]);
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t x = w[q >> 1];
-      const uint32_t sg = (q & 1) ? (x & 0x80808080u) : ((x & 0x08080808u) << 4);
-      hd[q] = __builtin_amdgcn_perm(0u, kTop6m, (w[2] >> (2 * q)) & 0x03030303u) | sg;
-    }
-  } else if (SEG == 1) {
-    // q = 16h + l: low digits from the nibbles, high from the 2-bit codes
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      ld[2 * i] = lut16<1>(w[i]);
-      ld[2 * i + 1] = lut16<1>(w[i] >> 4);
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      hd[q] = __builtin_amdgcn_perm(0u, kTop6, (w[2] >> (2 * q)) & 0x03030303u);
-  } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ld[i] = lut16<2>(w[i]);
-      hd[i] = lut16<0>(w[i] >> 4);
-    }
-  }
+__device__ inline v8i six(const uint32_t *d) {
+  return v8i{(int)d[0], (int)d[1], (int)d[2], (int)d[3], (int)d[4], (int)d[5], 0, 0};
 }
 
-template <bool SM>
+// FP8 digit codes of 4 mantissa bytes: the high plane (+-h/512) and the low
+// plane (+-l/512); sign-magnitude bytes (|q| = 16h + l) or, with FULL, two's
+// complement (h = q >> 4 signed, l = q & 15).
+template <bool FULL>
+__device__ inline uint32_t hi_codes(uint32_t w) {
+  if (!FULL) return ((w >> 4) & 0x07070707u) | (w & 0x80808080u);
+  const uint32_t x = (w >> 4) & 0x0F0F0F0Fu;
+  const uint32_t s = (x >> 3) & 0x01010101u;
+  const uint32_t mag = (x ^ (s * 0x0Fu)) + s;
+  return mag | (s << 7);
+}
+template <bool FULL>
+__device__ inline uint32_t lo_codes(uint32_t w) {
+  return FULL ? (w & 0x0F0F0F0Fu) : (w & 0x8F8F8F8Fu);
+}
+
+template <bool FULL>
 __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g) {
   __shared__ v4f red[kMaxWaves][2][64];
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int nw = blockDim.x >> 6;
-  const int line = lane & 15;
-  const DGeo d(g.n4, g.n6, g.n8);
-  const int64_t nslab = g.npad / 16;
-  const int64_t slab0 = 2 * (int64_t)blockIdx.x;
-  const bool two = slab0 + 1 < nslab;
-  const int64_t sb = wd_slab_bytes(d);
-  const uint8_t *wsl0 = g.w_mant + slab0 * sb;
-  const uint8_t *wsl1 = two ? wsl0 + sb : wsl0;
-  const uint8_t *aimg = g.a_mant + g.a_op;
+  const int grp = lane >> 4, line = lane & 15;
+  const LGeo lg(g.n3, g.n4, g.n6, g.n8);
+  const int64_t pair = blockIdx.x;
+  const int64_t ss = pair >> 2;                      // super-slab
+  const int n0 = 2 * (int)(pair & 3);                // first slab of the pair
+  const bool two = (pair * 32 + 16) < g.N;           // the second slab has columns
+  const uint8_t *wsup = g.w_mant + ss * g.w_super;
+  const uint8_t *wsc = g.w_exp + ss * g.w_super_sc + 32 * lane;
   // Lanes of rows >= M read row 0's activation bytes (same addresses as a
   // live lane, so no extra traffic); their output rows are discarded.
   const int alane = line < g.M ? lane : (lane & ~15);
   v4f acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
 
-  // One group of up to four steps of a segment for both slabs: all loads
-  // first, then the products.  FULL groups carry no per-step guards.
-  auto group4 = [&](int gi, int nst) {
-    constexpr int sd = wd_step_data(0), ad = ad_step_data(0);
-    const uint8_t *g0 = wsl0 + grp_off(gi, sd), *g1 = wsl1 + grp_off(gi, sd);
-    const uint8_t *ga = aimg + grp_off(gi, ad);
-    const uint32_t sw0 = stream_load((const uint32_t *)(g0 + 4 * lane));
-    const uint32_t sw1 = stream_load((const uint32_t *)(g1 + 4 * lane));
-    const uint32_t sa = *(const uint32_t *)(ga + 4 * alane);
-    u4 x0[4], x1[4], p[4];
-    u2 q[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      x0[k] = x1[k] = p[k] = u4{0u, 0u, 0u, 0u};
-      q[k] = u2{0u, 0u};
-      if (k < nst) {
-        x0[k] = stream_load((const u4 *)(g0 + kScaleBlock + k * sd + 16 * lane));
-        x1[k] = stream_load((const u4 *)(g1 + kScaleBlock + k * sd + 16 * lane));
-        p[k] = *(const u4 *)(ga + kScaleBlock + k * ad + 16 * alane);
-        q[k] = *(const u2 *)(ga + kScaleBlock + k * ad + 1024 + 8 * alane);
-      }
-    }
-    // steps past a short group are skipped: their scale bytes are
-    // unspecified (an E8M0 NaN would poison even zero products)
-    auto step = [&](auto kc) {
-      constexpr int k = decltype(kc)::value;
-      if (k >= nst) return;
-      const v8i a = {(int)p[k][0], (int)p[k][1], (int)p[k][2], (int)p[k][3],
-                     (int)q[k][0], (int)q[k][1], 0, 0};
-      acc0 = mfma<3, k>(a, digits4<SM>(x0[k]), acc0, sa, sw0);
-      acc1 = mfma<3, k>(a, digits4<SM>(x1[k]), acc1, sa, sw1);
-    };
-    step(std::integral_constant<int, 0>());
-    step(std::integral_constant<int, 1>());
-    step(std::integral_constant<int, 2>());
-    step(std::integral_constant<int, 3>());
-  };
-
-  // 4-bit steps: A e3m2 (FP6) x W e4m3, one instruction per step and slab;
-  // the wave takes groups wave, wave + nw, ...
-  {
-    const int S = d.S[0], nfg = S / kStreamGroup, rem = S % kStreamGroup;
-    for (int gi = wave; gi < nfg; gi += nw) group4(gi, kStreamGroup);
-    if (rem && wave == nfg % nw) group4(nfg, rem);
-  }
-
-  // 6-bit and 8-bit steps: FP8 digits on both sides, two instructions per
-  // step and slab (the weight digits' halves swapped in the second)
-  auto run68 = [&](auto segc) {
+  auto run_group = [&](auto segc, int gi) {
     constexpr int SEG = decltype(segc)::value;
-    constexpr int sd = wd_step_data(SEG), ad = ad_step_data(SEG);
-    const uint8_t *w0 = wsl0 + wd_seg_off(d, SEG), *w1 = wsl1 + wd_seg_off(d, SEG);
-    const uint8_t *a0 = aimg + ad_seg_off(d, SEG);
-    auto group = [&](int gi, int nst) {
-      const uint8_t *g0 = w0 + grp_off(gi, sd), *g1 = w1 + grp_off(gi, sd);
-      const uint8_t *ga = a0 + grp_off(gi, ad);
-      const uint32_t sw0 = stream_load((const uint32_t *)(g0 + 4 * lane));
-      const uint32_t sw1 = stream_load((const uint32_t *)(g1 + 4 * lane));
-      const uint32_t sa = *(const uint32_t *)(ga + 4 * alane);
-      u4 x0[4], x1[4], p[4], r[4];
+    constexpr int CB = w_chunk_bytes(SEG, FULL);
+    const int gl = gi - lg.G0[SEG];
+    const int nst = min(4, lg.S[SEG] - 4 * gl);
+    // the lane's scale bytes of the group: byte 8 k + n for step k, slab n;
+    // sw[sl] gathers the four steps' bytes of slab n0 + sl
+    const u4 s0 = stream_load((const u4 *)(wsc + (int64_t)gi * 2048));
+    const u4 s1 = stream_load((const u4 *)(wsc + (int64_t)gi * 2048 + 16));
+    // step k's byte of slab b lies in dword 2k + b / 4
+    uint32_t sw[2];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        x0[k] = x1[k] = p[k] = r[k] = u4{0u, 0u, 0u, 0u};
-        if (k < nst) {
-          const uint8_t *c0 = g0 + kScaleBlock + k * sd, *c1 = g1 + kScaleBlock + k * sd;
-          if (SEG == 1) {
-            const u2 n0 = stream_load((const u2 *)(c0 + 8 * lane));
-            const u2 n1 = stream_load((const u2 *)(c1 + 8 * lane));
-            x0[k] = u4{n0[0], n0[1], stream_load((const uint32_t *)(c0 + 512 + 4 * lane)), 0u};
-            x1[k] = u4{n1[0], n1[1], stream_load((const uint32_t *)(c1 + 512 + 4 * lane)), 0u};
-          } else {
-            x0[k] = stream_load((const u4 *)(c0 + 16 * lane));
-            x1[k] = stream_load((const u4 *)(c1 + 16 * lane));
-          }
-          const uint8_t *ca = ga + kScaleBlock + k * ad + 32 * alane;
-          p[k] = *(const u4 *)ca;
-          r[k] = *(const u4 *)(ca + 16);
+    for (int sl = 0; sl < 2; ++sl) {
+      const int b = n0 + sl;
+      const uint32_t d0 = b < 4 ? s0[0] : s0[1], d1 = b < 4 ? s0[2] : s0[3];
+      const uint32_t d2 = b < 4 ? s1[0] : s1[1], d3 = b < 4 ? s1[2] : s1[3];
+      const int sh = 8 * (b & 3);
+      sw[sl] = ((d0 >> sh) & 0xFFu) | (((d1 >> sh) & 0xFFu) << 8) | (((d2 >> sh) & 0xFFu) << 16) |
+               (((d3 >> sh) & 0xFFu) << 24);
+    }
+    const uint32_t sa = *(const uint32_t *)(g.a_exp + (int64_t)gi * 256 + 4 * alane);
+    const uint8_t *wseg = wsup + w_seg_base<SEG, FULL>(lg) + (int64_t)(4 * gl) * kWSlabs * CB +
+                          (int64_t)n0 * CB;
+    const uint8_t *aseg = g.a_mant + a_seg_base<SEG>(lg) +
+                          (int64_t)(4 * gl) * kLanes * a_lane_bytes(SEG) +
+                          (int64_t)a_lane_bytes(SEG) * alane;
+    // raw loads of step k (fields a segment does not use stay unread)
+    struct Raw {
+      u4 a0, a1;            // activation lane data (24 or 32 bytes)
+      u4 p[2], h[2];        // weight bytes of the two slabs
+      u2 x[2];
+      uint32_t z[2];
+    };
+    auto load = [&](int k) __attribute__((always_inline)) {
+      Raw r;
+      const uint8_t *w0 = wseg + (int64_t)k * kWSlabs * CB;
+      const uint8_t *ap = aseg + (int64_t)k * kLanes * a_lane_bytes(SEG);
+      if (SEG == 3) {
+        r.a0 = *(const u4 *)ap;
+        r.a1 = *(const u4 *)(ap + 16);
+      } else {
+        const u3 av = *(const u3 *)ap, aw = *(const u3 *)(ap + 12);
+        r.a0 = u4{av[0], av[1], av[2], aw[0]};
+        r.a1 = u4{aw[1], aw[2], 0u, 0u};
+      }
+#pragma unroll
+      for (int sl = 0; sl < 2; ++sl) {
+        const uint8_t *w = (sl && two) ? w0 + CB : w0;
+        if (SEG == 0 && !FULL) {
+          r.x[sl] = stream_load((const u2 *)(w + 8 * lane));
+          r.z[sl] = stream_load((const uint32_t *)(w + 512 + 4 * lane));
+        } else if (SEG <= 1) {
+          r.p[sl] = stream_load((const u4 *)(w + 16 * lane));
+          if (SEG == 1 && FULL) r.x[sl] = stream_load((const u2 *)(w + 1024 + 8 * lane));
+        } else if (SEG == 2) {
+          const int jc = 16 * (grp >> 1) + line;
+          r.p[sl] = stream_load((const u4 *)(w + 16 * jc));
+          if (FULL) r.h[sl] = stream_load((const u4 *)(w + 512 + 16 * jc));
+          else r.x[sl] = stream_load((const u2 *)(w + 512 + 8 * jc));
+        } else {
+          r.p[sl] = stream_load((const u4 *)(w + 32 * line + 16 * (grp & 1)));
+          r.h[sl] = stream_load((const u4 *)(w + 32 * (16 + line) + 16 * (grp & 1)));
         }
       }
-      auto step = [&](auto kc) {
-        constexpr int k = decltype(kc)::value;
-        if (k >= nst) return;
-        const v8i a = {(int)p[k][0], (int)p[k][1], (int)p[k][2], (int)p[k][3],
-                       (int)r[k][0], (int)r[k][1], (int)r[k][2], (int)r[k][3]};
-        uint32_t hd[4], ld[4];
-        digits68<SM, SEG>(x0[k], hd, ld);
-        v8i bhl = {(int)hd[0], (int)hd[1], (int)hd[2], (int)hd[3],
-                   (int)ld[0], (int)ld[1], (int)ld[2], (int)ld[3]};
-        v8i blh = {(int)ld[0], (int)ld[1], (int)ld[2], (int)ld[3],
-                   (int)hd[0], (int)hd[1], (int)hd[2], (int)hd[3]};
-        acc0 = mfma<0, k>(a, bhl, acc0, sa, sw0);
-        acc0 = mfma<0, k>(a, blh, acc0, sa, sw0);
-        digits68<SM, SEG>(x1[k], hd, ld);
-        bhl = v8i{(int)hd[0], (int)hd[1], (int)hd[2], (int)hd[3],
-                  (int)ld[0], (int)ld[1], (int)ld[2], (int)ld[3]};
-        blh = v8i{(int)ld[0], (int)ld[1], (int)ld[2], (int)ld[3],
-                  (int)hd[0], (int)hd[1], (int)hd[2], (int)hd[3]};
-        acc1 = mfma<0, k>(a, bhl, acc1, sa, sw1);
-        acc1 = mfma<0, k>(a, blh, acc1, sa, sw1);
-      };
-      step(std::integral_constant<int, 0>());
-      step(std::integral_constant<int, 1>());
-      step(std::integral_constant<int, 2>());
-      step(std::integral_constant<int, 3>());
+      return r;
     };
-    const int S = d.S[SEG], nfg = S / kStreamGroup, rem = S % kStreamGroup;
-    for (int gi = wave; gi < nfg; gi += nw) group(gi, kStreamGroup);
-    if (rem && wave == nfg % nw) group(nfg, rem);
+    auto compute = [&](auto kc, const Raw &r) __attribute__((always_inline)) {
+      constexpr int k = decltype(kc)::value;
+      const v8i a = {(int)r.a0[0], (int)r.a0[1], (int)r.a0[2], (int)r.a0[3],
+                     (int)r.a1[0], (int)r.a1[1], (int)r.a1[2], (int)r.a1[3]};
+      if (SEG <= 1) {
+        uint32_t d[2][6];
+#pragma unroll
+        for (int sl = 0; sl < 2; ++sl) {
+          if (SEG == 0 && !FULL) {
+            const uint32_t x[3] = {r.x[sl][0], r.x[sl][1], r.z[sl]};
+            unfold3(x, d[sl]);
+          } else if (SEG == 1 && FULL) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) d[sl][i] = r.p[sl][i];
+            d[sl][4] = r.x[sl][0];
+            d[sl][5] = r.x[sl][1];
+          } else {
+            const uint32_t x[4] = {r.p[sl][0], r.p[sl][1], r.p[sl][2], r.p[sl][3]};
+            unfold4(x, d[sl]);
+          }
+        }
+        constexpr int FB = SEG == 0 ? kFmtE2M3 : kFmtE3M2;
+        acc0 = mfma<kFmtE3M2, FB, k>(a, six(d[0]), acc0, sa, sw[0]);
+        acc1 = mfma<kFmtE3M2, FB, k>(a, six(d[1]), acc1, sa, sw[1]);
+      } else if (SEG == 2) {
+        // the weights' high plane in every lane (scale E + 3) gives the
+        // products hh and lh, their low plane (scale E) hl and ll
+#pragma unroll
+        for (int sl = 0; sl < 2; ++sl) {
+          const uint32_t xl[4] = {r.p[sl][0], r.p[sl][1], r.p[sl][2], r.p[sl][3]};
+          uint32_t L[6], H[6];
+          unfold4(xl, L);
+          if (FULL) {
+            const uint32_t xh[4] = {r.h[sl][0], r.h[sl][1], r.h[sl][2], r.h[sl][3]};
+            unfold4(xh, H);
+          } else {
+            const uint32_t xh[2] = {r.x[sl][0], r.x[sl][1]};
+            unfold2(xh, L, H);
+          }
+          const uint32_t e = sw[sl];
+          v4f &acc = sl ? acc1 : acc0;
+          acc = mfma<kFmtE3M2, kFmtE3M2, k>(a, six(H), acc, sa, scale_plus<3>(e));
+          acc = mfma<kFmtE3M2, kFmtE3M2, k>(a, six(L), acc, sa, e);
+        }
+      } else {
+        // the weights' high digits in every lane (scale E + 4), then their
+        // low digits (scale E)
+#pragma unroll
+        for (int sl = 0; sl < 2; ++sl) {
+          v8i bh, bl;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const uint32_t w = i < 4 ? r.p[sl][i] : r.h[sl][i - 4];
+            bh[i] = (int)hi_codes<FULL>(w);
+            bl[i] = (int)lo_codes<FULL>(w);
+          }
+          const uint32_t e = sw[sl];
+          v4f &acc = sl ? acc1 : acc0;
+          acc = mfma<kFmtE4M3, kFmtE4M3, k>(a, bh, acc, sa, scale_plus<4>(e));
+          acc = mfma<kFmtE4M3, kFmtE4M3, k>(a, bl, acc, sa, e);
+        }
+      }
+    };
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I3 = std::integral_constant<int, 3>;
+    if (nst == 4 && SEG <= 1) {
+      // a whole group: every load first, then the products
+      const Raw r0 = load(0), r1 = load(1), r2 = load(2), r3 = load(3);
+      compute(I0(), r0);
+      compute(I1(), r1);
+      compute(I2(), r2);
+      compute(I3(), r3);
+    } else if (nst == 4 && SEG == 2) {
+      // 6-bit steps carry half again the bytes: two steps of loads at a time
+      const Raw r0 = load(0), r1 = load(1);
+      compute(I0(), r0);
+      compute(I1(), r1);
+      const Raw r2 = load(2), r3 = load(3);
+      compute(I2(), r2);
+      compute(I3(), r3);
+    } else {
+      // 8-bit steps (twice the bytes) one at a time; steps past a short
+      // group are skipped
+      compute(I0(), load(0));
+      if (nst > 1) compute(I1(), load(1));
+      if (nst > 2) compute(I2(), load(2));
+      if (nst > 3) compute(I3(), load(3));
+    }
   };
-  run68(std::integral_constant<int, 1>());
-  run68(std::integral_constant<int, 2>());
+
+  for (int gi = wave; gi < lg.ngroups; gi += nw) {
+    if (gi < lg.G0[1]) run_group(std::integral_constant<int, 0>(), gi);
+    else if (gi < lg.G0[2]) run_group(std::integral_constant<int, 1>(), gi);
+    else if (gi < lg.G0[3]) run_group(std::integral_constant<int, 2>(), gi);
+    else run_group(std::integral_constant<int, 3>(), gi);
+  }
 
   red[wave][0][lane] = acc0;
   red[wave][1][lane] = acc1;
@@ -321,10 +273,10 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
   if (wave < 2 && (wave == 0 || two)) {
     v4f y = red[0][wave][lane];
     for (int w = 1; w < nw; ++w) y += red[w][wave][lane];
-    const int64_t col = (slab0 + wave) * 16 + line;
+    const int64_t col = pair * 32 + 16 * wave + line;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int row = 4 * (lane >> 4) + i;
+      const int row = 4 * grp + i;
       if (row < g.M && col < g.N) g.y[row * g.ldy + col] = y[i];
     }
   }
@@ -351,9 +303,9 @@ static int decode_waves(int64_t pairs) {
 }
 
 hipError_t launch_gemm_decode(const GemmArgs &a, hipStream_t stream) {
-  const int64_t pairs = (a.npad / 16 + 1) / 2;
+  const int64_t pairs = (a.N + 31) / 32;
   dim3 grid((unsigned)pairs), block((unsigned)(64 * decode_waves(pairs)));
-  if (a.sm)
+  if (a.full)
     hipLaunchKernelGGL(gemm_decode_kernel<true>, grid, block, 0, stream, a);
   else
     hipLaunchKernelGGL(gemm_decode_kernel<false>, grid, block, 0, stream, a);

@@ -3,9 +3,8 @@
 // (MXSens, arXiv 2607.17733, Section 2: the integer product of one block).
 //
 // A verification kernel, not on the hot path: one thread per (i, j, b)
-// reads the mantissas from the canonical packed activation row and the
-// weight slab (stream layout) and sums the 32 products in int32 (|P| <
-// 2^19, exact).
+// reads the mantissas from the canonical packed activation row and from the
+// weight layout, and sums the 32 products in int32 (|P| < 2^19, exact).
 #include "mxq_device.h"
 #include "mxq_internal.h"
 
@@ -22,14 +21,13 @@ __global__ __launch_bounds__(kThreads) void gemm_partials_kernel(GemmArgs g) {
   const int b = (int)(f % nb);
   const int64_t ij = f / nb;
   const int64_t i = ij / g.N, j = ij - i * g.N;
-  const Segs s{g.n4, g.n6, g.n8};
+  const Segs s{g.n4, g.n6, g.n8, g.n3};
   const BlockInfo bi = block_info(s, b);
-  const DGeo dg(g.n4, g.n6, g.n8);
+  const LGeo lg(g.n3, g.n4, g.n6, g.n8);
   const uint8_t *arow = g.a_mant + i * g.a_rb;
-  const uint8_t *slab = g.w_mant + (j >> 4) * wd_slab_bytes(dg);
   int acc = 0;
   for (int t = 0; t < kBlock; ++t)
-    acc += act_elem(arow, bi, t) * wstream_elem(slab, dg, bi, (int)(j & 15), t, g.sm != 0);
+    acc += act_elem(arow, bi, t) * w_elem(g.w_mant, lg, g.full != 0, j, b, t);
   g.p[f] = acc;
 }
 

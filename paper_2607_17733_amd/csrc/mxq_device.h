@@ -20,178 +20,240 @@ namespace mxq {
 
 constexpr int kBlock = 32;
 
-// Segment geometry of a width map grouped as n4 4-bit, n6 6-bit, n8 8-bit
-// blocks (in that order along the permuted K).
-struct Segs {
-  int n4, n6, n8;
-  int n3;       // of the n4 blocks, the first n3 hold 3-bit mantissas (stored as 2q)
-};
-
-struct BlockInfo {
-  int m;        // mantissa width
-  int seg;      // 0, 1, 2 for 4-, 6-, 8-bit
-  int idx;      // index of the block within its segment
-  int nseg;     // number of blocks in the segment
-  int64_t aoff; // byte offset of the block inside a packed activation row
-};
-
-__host__ __device__ inline BlockInfo block_info(const Segs &s, int b) {
-  BlockInfo r;
-  if (b < s.n4) {
-    r.m = 4; r.seg = 0; r.idx = b; r.nseg = s.n4;
-    r.aoff = 16LL * b;
-  } else if (b < s.n4 + s.n6) {
-    r.m = 6; r.seg = 1; r.idx = b - s.n4; r.nseg = s.n6;
-    r.aoff = 16LL * s.n4 + 24LL * r.idx;
-  } else {
-    r.m = 8; r.seg = 2; r.idx = b - s.n4 - s.n6; r.nseg = s.n8;
-    r.aoff = 16LL * s.n4 + 24LL * s.n6 + 32LL * r.idx;
-  }
-  return r;
-}
-
 // ---------------------------------------------------------------------------
-// Stream layout (decode GEMM).  Sixteen "lines" (16 weight columns = one
-// slab, or the 16 activation rows of a decode batch) are stored step by step
-// in the operand order of V_MFMA_SCALE_F32_16X16X128_F8F6F4, whose lane l =
-// 16 g + c (c = line) holds 32 elements of K-group g and supplies the E8M0
-// scale of K-block g of its line.  Steps: the 4-bit blocks four at a time
-// (padded with zero blocks to a multiple of 4), the 6-bit and the 8-bit
-// blocks two at a time (each padded to a multiple of 2).  The steps of each
-// segment form groups of four (the last may be shorter): a 256-byte scale
-// block (lane l's scale bytes of the group's steps k = 0..3 at 4 l + k),
-// then each step's lane data (lane l at LB * l unless split into planes as
-// noted).
+// Operand layouts of the GEMMs (include/mxq.h has the byte-exact statement).
 //
-// With the block's E as E8M0 scale, the FP8 digits of a mantissa sum to
-// q * 2^-(m-2): e4m3(q/4) for a 4-bit q; two digits for 6- and 8-bit q.
-// Weights keep the packed mantissas (4m bits per element) and become these
-// digits in registers.  With the symmetric clamp (no -2^(m-1)) 4- and 6-bit
-// mantissas are stored sign-magnitude, so a digit is one 8-entry byte lookup
-// plus the sign bit: a 4-bit code is s|(|q|) (3 magnitude bits), a 6-bit code
-// a nibble s|(|q| mod 8) plus the 2-bit |q| div 8 (digits h/2 and l/16 of
-// |q| = 8h + l).  With the full clamp they are two's complement (q mod 16,
-// and bits 4-5: digits h and l/16 of q = 16h + l).  8-bit mantissas are two's
-// complement in both modes (digits h/4 and l/64 of q = 16h + l).
-//   4-bit step s: lane (g, c) holds 16 bytes: elements 16(g&1)..16(g&1)+15 of
-//     block 4s+(g>>1) (bytes 0-7), then the same elements of block
-//     4s+2+(g>>1) (bytes 8-15), as nibble codes: the dword of elements
-//     e0..e7 has byte k = code(e_k) | code(e_{k+4}) << 4.  Scale byte of lane
-//     (g, c): E of block 4s+g.
-//   6-bit step s: lane (g, c) holds 12 bytes for elements 16(g&1)+0..15 of
-//     block 2s+(g>>1): their nibble codes (8 bytes at 8 l, same nibble
-//     order) and a dword of their 2-bit codes (at 512 + 4 l: element t at
-//     bits 8(t%4) + 2(t/4)).
-//   8-bit step s: lane (g, c) holds 16 bytes: the same 16 elements of block
-//     2s+(g>>1) as two's-complement bytes.
-//   6/8-bit scale byte of lane (g, c): E of block 2s+(g&1).
-// Activations (decode image, M <= 16) are stored as ready operands:
-//   4-bit step s: lane (g, r) holds block 4s+g of row r as 32 FP6 e3m2
-//     codes of q/4 (24 bytes: the first 16 at 16 l, the last 8 at
-//     1024 + 8 l); scale byte E of block 4s+g.
-//   6/8-bit step s: lane (g, r) holds elements 16(g&1)+0..15 of block
-//     2s+(g>>1): the e4m3 codes of their high digits (16 bytes) then of
-//     their low digits (16 bytes); scale byte E of block 2s+(g&1).
+// Both GEMMs run V_MFMA_SCALE_F32_16X16X128_F8F6F4: 16 rows x 16 columns x
+// 128 K, lane l = 16 g + r (lane group g, row / column r) holding 32 K-values
+// and supplying the E8M0 scale of K-block g of its row / column.  For FP6
+// the 32 values of lane group g are K 32g..32g+31; for FP8 they are K
+// 16g..16g+15 (bytes 0-15) and 64+16g..64+16g+15 (bytes 16-31).
+//
+// The K-blocks of a width map form four segments, 3-bit, 4-bit, 6-bit and
+// 8-bit blocks in that order.  A segment is walked in steps: four blocks per
+// step for 3- and 4-bit blocks (K-block g = block 4s+g), two per step for 6-
+// and 8-bit blocks, each split into two digit planes (K-blocks 2j and 2j+1
+// hold the high and low plane of block 2s+j).  Segments are zero padded to
+// whole steps; the steps of a segment form groups of four that share one
+// scale word per lane (byte k = step k of the group).
+//
+// Digits, with each block's E as its E8M0 scale (the extra +3 / +4 of the
+// weights' high planes applied by the GEMM, saturating at 255):
+//   3-bit  A: E3M2 code of 2q          W: E2M3 code s|k of q/8  (k = |q|)
+//   4-bit  A: E3M2 code of q           W: E3M2 code s|k of q/16
+//   6-bit  A: E3M2 h/2, l/16 (q = 8h+l, h = floor(q/8))
+//          W: E3M2 s|h and s|l of +-h/16 (scale +3) and +-l/16 (|q| = 8h+l)
+//   8-bit  A: E4M3 2h, l/8 (q = 16h+l, h = floor(q/16))
+//          W: E4M3 of +-h/512 (scale +4) and +-l/512: sign-magnitude bytes
+//             (|q| = 16h+l) under the symmetric clamp, two's complement (h
+//             signed, l = q mod 16) under the full clamp
+// Every digit product is exact and the four products of a 6- or 8-bit block
+// pair sum to qa qw 2^(sa+sw) with the scales shown.
+//
+// The weights' FP6 codes s|k have two zero bits per 6-bit field (one for a
+// 3-bit block: s000kk has three), so they are stored "folded" at 4 (3) bits
+// per element: the zero bits of one operand word hold the payload of
+// another, and the kernel restores the FP6 operand with masks and shifts.
 // ---------------------------------------------------------------------------
-constexpr int kStreamLanes = 64;
-constexpr int kStreamGroup = 4;          // steps sharing one scale block
-constexpr int kScaleBlock = 256;         // 64 lanes x 4 scale bytes
+constexpr int kSegs = 4;
+constexpr int kGroupSteps = 4;
+constexpr int kLanes = 64;
+constexpr int kWCols = 128;          // columns of a weight super-slab
+constexpr int kWSlabs = 8;           // 16-column slabs per super-slab
+constexpr int kATileRows = 16;
 
-struct DGeo {
-  int n4, n6, n8;
-  int S[3];              // steps of each segment
-  int nsteps;
-  __host__ __device__ DGeo(int a, int b, int c) : n4(a), n6(b), n8(c) {
-    S[0] = (a + 3) / 4;
-    S[1] = (b + 1) / 2;
-    S[2] = (c + 1) / 2;
-    nsteps = S[0] + S[1] + S[2];
+struct LGeo {
+  int nb[kSegs];     // blocks of each segment
+  int b0[kSegs];     // first block of the segment in the width map
+  int S[kSegs];      // steps of each segment
+  int st0[kSegs];    // first step of the segment
+  int G0[kSegs];     // first scale group of the segment
+  int nsteps, ngroups;
+  __host__ __device__ LGeo(int n3, int n4, int n6, int n8) {
+    nb[0] = n3; nb[1] = n4 - n3; nb[2] = n6; nb[3] = n8;
+    int b = 0, st = 0, gg = 0;
+    for (int s = 0; s < kSegs; ++s) {
+      b0[s] = b;
+      st0[s] = st;
+      G0[s] = gg;
+      S[s] = s < 2 ? (nb[s] + 3) / 4 : (nb[s] + 1) / 2;
+      b += nb[s];
+      st += S[s];
+      gg += (S[s] + kGroupSteps - 1) / kGroupSteps;
+    }
+    nsteps = st;
+    ngroups = gg;
+  }
+  __host__ __device__ int seg_of_step(int st) const {
+    return st < st0[1] ? 0 : st < st0[2] ? 1 : st < st0[3] ? 2 : 3;
+  }
+  // scale group and byte of global step st
+  __host__ __device__ int group_of(int st) const {
+    const int s = seg_of_step(st);
+    return G0[s] + (st - st0[s]) / kGroupSteps;
+  }
+  __host__ __device__ int byte_of(int st) const {
+    const int s = seg_of_step(st);
+    return (st - st0[s]) % kGroupSteps;
   }
 };
 
-// lane-data bytes of a weight / activation step of each segment
-__host__ __device__ constexpr int wd_lane_bytes(int seg) { return seg == 1 ? 12 : 16; }
-__host__ __device__ constexpr int ad_lane_bytes(int seg) { return seg == 0 ? 24 : 32; }
-// bytes of the 64 lanes' data of one step
-__host__ __device__ constexpr int wd_step_data(int seg) { return kStreamLanes * wd_lane_bytes(seg); }
-__host__ __device__ constexpr int ad_step_data(int seg) { return kStreamLanes * ad_lane_bytes(seg); }
-
-// A segment of S steps is a run of groups of kStreamGroup steps (the last one
-// may be shorter): each group is its scale block (lane l's scale byte for
-// step k of the group at 4 l + k) followed by its steps' lane data.
-__host__ __device__ inline int64_t seg_bytes(int S, int step_data) {
-  return (int64_t)S * step_data + (int64_t)((S + kStreamGroup - 1) / kStreamGroup) * kScaleBlock;
-}
-__host__ __device__ inline int64_t grp_off(int g, int step_data) {
-  return (int64_t)g * (kStreamGroup * step_data + kScaleBlock);
-}
-// byte offset of segment seg in a weight slab / the activation decode image
-__host__ __device__ inline int64_t wd_seg_off(const DGeo &d, int seg) {
+// Activation operand image: 16-row tiles, each the steps in order, each step
+// 64 lanes of alb bytes (lane l at l * alb).  Scales: per tile, per group, a
+// dword per lane.
+__host__ __device__ constexpr int a_lane_bytes(int seg) { return seg == 3 ? 32 : 24; }
+__host__ __device__ inline int64_t a_step_off(const LGeo &g, int st) {
+  const int s = g.seg_of_step(st);
   int64_t o = 0;
-  for (int s = 0; s < seg; ++s) o += seg_bytes(d.S[s], wd_step_data(s));
+  for (int k = 0; k < s; ++k) o += (int64_t)g.S[k] * kLanes * a_lane_bytes(k);
+  return o + (int64_t)(st - g.st0[s]) * kLanes * a_lane_bytes(s);
+}
+__host__ __device__ inline int64_t a_tile_bytes(const LGeo &g) {
+  int64_t o = 0;
+  for (int k = 0; k < kSegs; ++k) o += (int64_t)g.S[k] * kLanes * a_lane_bytes(k);
   return o;
 }
-__host__ __device__ inline int64_t ad_seg_off(const DGeo &d, int seg) {
+__host__ __device__ inline int64_t a_tile_scale_bytes(const LGeo &g) {
+  return (int64_t)g.ngroups * kLanes * 4;
+}
+
+// Weight super-slabs: 128 columns, each the steps in order, each step the
+// chunks of its 8 slabs (chunk n at n * w_chunk_bytes).  Scales: per
+// super-slab, per group, 2 KB: lane l's 32 bytes at 32 l, the byte of slab n
+// for step k of the group at 8 k + n.
+//   3-bit  symmetric: 64 lanes x 8 bytes (words X, Y) then 64 x 4 (word Z);
+//          full: as a 4-bit chunk (|q| <= 4 fits s|kkk)
+//   4-bit  symmetric: lane l's 16 folded bytes at 16 l; full: 64 x 16 then
+//          64 x 8 bytes of the raw 24-byte FP6 operand
+//   6-bit  per (block j, column c) of the step: the low plane (16 folded
+//          bytes at 16 (16 j + c)), then the high plane (symmetric: 8 bytes
+//          of 2-bit magnitudes at 512 + 8 (16 j + c), the sign taken from
+//          the low plane; full: 16 folded bytes at 512 + 16 (16 j + c))
+//   8-bit  per (block j, column c): 32 mantissa bytes at 32 (16 j + c)
+__host__ __device__ constexpr int w_chunk_bytes(int seg, bool full) {
+  return seg == 0 ? (full ? 1024 : 768)
+       : seg == 1 ? (full ? 1536 : 1024)
+       : seg == 2 ? (full ? 1024 : 768)
+       : 1024;
+}
+__host__ __device__ inline int64_t w_step_off(const LGeo &g, int st, bool full) {
+  const int s = g.seg_of_step(st);
   int64_t o = 0;
-  for (int s = 0; s < seg; ++s) o += seg_bytes(d.S[s], ad_step_data(s));
+  for (int k = 0; k < s; ++k) o += (int64_t)g.S[k] * kWSlabs * w_chunk_bytes(k, full);
+  return o + (int64_t)(st - g.st0[s]) * kWSlabs * w_chunk_bytes(s, full);
+}
+__host__ __device__ inline int64_t w_super_bytes(const LGeo &g, bool full) {
+  int64_t o = 0;
+  for (int k = 0; k < kSegs; ++k) o += (int64_t)g.S[k] * kWSlabs * w_chunk_bytes(k, full);
   return o;
 }
-__host__ __device__ inline int64_t wd_slab_bytes(const DGeo &d) { return wd_seg_off(d, 3); }
-__host__ __device__ inline int64_t ad_image_bytes(const DGeo &d) { return ad_seg_off(d, 3); }
+__host__ __device__ inline int64_t w_super_scale_bytes(const LGeo &g) {
+  return (int64_t)g.ngroups * kLanes * kWSlabs * 4;
+}
 
-// Where block `idx` of segment `seg` lives in the stream layout: its step
-// within the segment, the lane group of each half (elements 16h..16h+15 sit
-// in lane group g0 + h), the byte offset of its elements inside a 4-bit lane
-// (0 or 8) and the lane groups whose scale byte is the block's exponent (one
-// for 4-bit blocks, two for 6/8-bit blocks).
-struct DLoc {
-  int st, g0, region, sg0, sg1;
-};
-__host__ __device__ inline DLoc d_loc(int seg, int idx) {
-  DLoc r;
-  if (seg == 0) {
-    r.st = idx >> 2;
-    r.g0 = 2 * (idx & 1);
-    r.region = 8 * ((idx >> 1) & 1);
-    r.sg0 = r.sg1 = idx & 3;
-  } else {
-    r.st = idx >> 1;
-    r.g0 = 2 * (idx & 1);
-    r.region = 0;
-    r.sg0 = idx & 1;
-    r.sg1 = r.sg0 + 2;
+// Segment offsets with a compile-time segment (device code indexes the
+// geometry's arrays only with constants, so nothing spills to scratch).
+template <int SEG>
+__host__ __device__ inline int64_t a_seg_base(const LGeo &g) {
+  int64_t o = 0;
+#pragma unroll
+  for (int k = 0; k < SEG; ++k) o += (int64_t)g.S[k] * kLanes * a_lane_bytes(k);
+  return o;
+}
+template <int SEG, bool FULL>
+__host__ __device__ inline int64_t w_seg_base(const LGeo &g) {
+  int64_t o = 0;
+#pragma unroll
+  for (int k = 0; k < SEG; ++k) o += (int64_t)g.S[k] * kWSlabs * w_chunk_bytes(k, FULL);
+  return o;
+}
+
+// Fold masks: payload bits of the FP6 operand words (element t at bits 6t of
+// six words D0..D5; words 3-5 repeat the pattern of 0-2).
+//   4-bit s00kkk: X = D0 | (D1 & Z0), Y = D2 | (D1 & Z2) per 16 elements
+//   3-bit s000kk: X = D0 | D1 >> 1, Y = D3 | D4 >> 1,
+//                 Z = D2 | D5 << 3 | D5 >> 31 per 32 elements
+//   2-bit 0000hh: X = D0 | D1 | D2 per 16 elements (the sign is restored from
+//                 the low plane's word at the same position)
+constexpr uint32_t kF4P0 = 0xe79e79e7u, kF4Z0 = 0x18618618u;
+constexpr uint32_t kF4P2 = 0x9e79e79eu, kF4Z2 = 0x61861861u;
+constexpr uint32_t kF3A = 0xe38e38e3u, kF3B = 0x38e38e38u, kF3C = 0x8e38e38eu,
+                   kF3C31 = 0x0e38e38eu;
+constexpr uint32_t kF2Q0 = 0xc30c30c3u, kF2Q1 = 0x30c30c30u, kF2Q2 = 0x0c30c30cu;
+constexpr uint32_t kSgn0 = 0x20820820u, kSgn1 = 0x08208208u, kSgn2 = 0x82082082u;
+
+__host__ __device__ inline void fold4(const uint32_t *d, uint32_t *o) {
+  o[0] = d[0] | (d[1] & kF4Z0);
+  o[1] = d[2] | (d[1] & kF4Z2);
+  o[2] = d[3] | (d[4] & kF4Z0);
+  o[3] = d[5] | (d[4] & kF4Z2);
+}
+__host__ __device__ inline void unfold4(const uint32_t *x, uint32_t *d) {
+  d[0] = x[0] & kF4P0;
+  d[1] = (x[0] & kF4Z0) | (x[1] & kF4Z2);
+  d[2] = x[1] & kF4P2;
+  d[3] = x[2] & kF4P0;
+  d[4] = (x[2] & kF4Z0) | (x[3] & kF4Z2);
+  d[5] = x[3] & kF4P2;
+}
+__host__ __device__ inline void fold3(const uint32_t *d, uint32_t *o) {
+  o[0] = d[0] | (d[1] >> 1);
+  o[1] = d[3] | (d[4] >> 1);
+  o[2] = d[2] | (d[5] << 3) | (d[5] >> 31);
+}
+__host__ __device__ inline void unfold3(const uint32_t *x, uint32_t *d) {
+  d[0] = x[0] & kF3A;
+  d[1] = (x[0] << 1) & kF3B;
+  d[2] = x[2] & kF3C;
+  d[3] = x[1] & kF3A;
+  d[4] = (x[1] << 1) & kF3B;
+  d[5] = ((x[2] >> 3) & kF3C31) | (x[2] << 31);
+}
+__host__ __device__ inline void fold2(const uint32_t *d, uint32_t *o) {
+  o[0] = d[0] | d[1] | d[2];
+  o[1] = d[3] | d[4] | d[5];
+}
+// high plane from its 2-bit magnitudes and the low plane's signs
+__host__ __device__ inline void unfold2(const uint32_t *x, const uint32_t *lo, uint32_t *d) {
+  d[0] = (x[0] & kF2Q0) | (lo[0] & kSgn0);
+  d[1] = (x[0] & kF2Q1) | (lo[1] & kSgn1);
+  d[2] = (x[0] & kF2Q2) | (lo[2] & kSgn2);
+  d[3] = (x[1] & kF2Q0) | (lo[3] & kSgn0);
+  d[4] = (x[1] & kF2Q1) | (lo[4] & kSgn1);
+  d[5] = (x[1] & kF2Q2) | (lo[5] & kSgn2);
+}
+
+// 32 six-bit codes -> the six operand words (element t at bits 6t).
+__host__ __device__ inline void fp6_words(const uint32_t *c, uint32_t *d) {
+  for (int j = 0; j < 6; ++j) d[j] = 0;
+  for (int t = 0; t < 32; ++t) {
+    const int b = 6 * t, w = b >> 5, sh = b & 31;
+    d[w] |= (c[t] & 63u) << sh;
+    if (sh > 26) d[w + 1] |= (c[t] & 63u) >> (32 - sh);
   }
-  return r;
+}
+// and back
+__host__ __device__ inline uint32_t fp6_code(const uint32_t *d, int t) {
+  const int b = 6 * t, w = b >> 5, sh = b & 31;
+  uint32_t v = d[w] >> sh;
+  if (sh > 26) v |= d[w + 1] << (32 - sh);
+  return v & 63u;
 }
 
-// Step st of a segment starting at `seg`: its data and its group's scales.
-__host__ __device__ inline int64_t step_data_off(int st, int step_data) {
-  return grp_off(st / kStreamGroup, step_data) + kScaleBlock +
-         (int64_t)(st % kStreamGroup) * step_data;
+// Weight codes of one mantissa q of a block of width m (see above): the
+// FP6 code s|k of a 3/4-bit q; the high and low plane codes of a 6-bit q
+// (|q| = 8h + l); the byte of an 8-bit q.
+__host__ __device__ inline uint32_t w_code34(int q) {
+  return (q < 0 ? 32u : 0u) | (uint32_t)(q < 0 ? -q : q);
 }
-__host__ __device__ inline int64_t step_scale_off(int st, int step_data, int lane) {
-  return grp_off(st / kStreamGroup, step_data) + 4 * lane + st % kStreamGroup;
+__host__ __device__ inline void w_code6(int q, uint32_t &hi, uint32_t &lo) {
+  const uint32_t a = (uint32_t)(q < 0 ? -q : q), s = q < 0 ? 32u : 0u;
+  hi = s | (a >> 3);
+  lo = s | (a & 7u);
 }
-
-// Stream codes of a mantissa: the nibble (4-bit q, or the low part of a
-// 6-bit q) and the 2-bit high part of a 6-bit q; sm = sign-magnitude
-// (symmetric clamp), else two's complement.
-__host__ __device__ inline uint32_t stream_nibble(int q, int m, bool sm) {
-  if (!sm) return (uint32_t)q & 15u;
-  const uint32_t a = (uint32_t)(q < 0 ? -q : q);
-  return (q < 0 ? 8u : 0u) | (m == 4 ? a : (a & 7u));
-}
-__host__ __device__ inline uint32_t stream_top2(int q, bool sm) {
-  if (!sm) return ((uint32_t)q >> 4) & 3u;
-  return (uint32_t)(q < 0 ? -q : q) >> 3;
-}
-
-// Weight stream nibble dword of eight mantissas q[0..7] of width m.
-__host__ __device__ inline uint32_t stream_nibbles(const int *q, int m, bool sm) {
-  uint32_t x = 0;
-  for (int k = 0; k < 4; ++k)
-    x |= (stream_nibble(q[k], m, sm) | (stream_nibble(q[k + 4], m, sm) << 4)) << (8 * k);
-  return x;
+__host__ __device__ inline uint32_t w_code8(int q, bool full) {
+  if (full) return (uint32_t)q & 255u;
+  return (q < 0 ? 128u : 0u) | (uint32_t)(q < 0 ? -q : q);
 }
 
 // ---------------------------------------------------------------------------
@@ -234,17 +296,49 @@ __device__ inline int quant_elem(uint32_t bits, int E, int m, int ties_away,
 }
 
 // ---------------------------------------------------------------------------
-// Element accessors (debug / parity kernels): mantissa t (0..31) of a block.
+// Element accessors (debug / parity kernels).
 // ---------------------------------------------------------------------------
 __device__ inline int sext_bits(uint32_t v, int bits) {
   const int sh = 32 - bits;
   return ((int)(v << sh)) >> sh;
 }
 
+// Widths and canonical packed-row offsets of the blocks: the row holds the
+// blocks in order, block b taking 4 m_b bytes (12 for a 3-bit block).
+struct Segs {
+  int n4, n6, n8;
+  int n3;       // of the n4 blocks, the first n3 hold 3-bit mantissas
+};
+struct BlockInfo {
+  int m;        // mantissa width
+  int64_t aoff; // byte offset of the block inside a packed activation row
+};
+__host__ __device__ inline BlockInfo block_info(const Segs &s, int b) {
+  BlockInfo r;
+  if (b < s.n3) {
+    r.m = 3; r.aoff = 12LL * b;
+  } else if (b < s.n4) {
+    r.m = 4; r.aoff = 12LL * s.n3 + 16LL * (b - s.n3);
+  } else if (b < s.n4 + s.n6) {
+    r.m = 6; r.aoff = 12LL * s.n3 + 16LL * (s.n4 - s.n3) + 24LL * (b - s.n4);
+  } else {
+    r.m = 8; r.aoff = 12LL * s.n3 + 16LL * (s.n4 - s.n3) + 24LL * s.n6 + 32LL * (b - s.n4 - s.n6);
+  }
+  return r;
+}
+__host__ __device__ inline int64_t packed_row_used(const Segs &s) {
+  return 12LL * s.n3 + 16LL * (s.n4 - s.n3) + 24LL * s.n6 + 32LL * s.n8;
+}
+
 // Canonical packed activation row (layout in include/mxq.h).
 __device__ inline int act_elem(const uint8_t *row, const BlockInfo &bi, int t) {
   const uint8_t *p = row + bi.aoff;
   if (bi.m == 8) return (int)(int8_t)p[t];
+  if (bi.m == 3) {
+    const int bit = 3 * t;
+    const uint32_t v = (uint32_t)p[bit >> 3] | ((uint32_t)p[(bit >> 3) + 1 < 12 ? (bit >> 3) + 1 : 11] << 8);
+    return sext_bits((v >> (bit & 7)) & 7u, 3);
+  }
   const uint32_t nib = (p[t >> 1] >> (4 * (t & 1))) & 15u;
   if (bi.m == 4) return sext_bits(nib, 4);
   const int d = t >> 4, u = t & 15;
@@ -254,144 +348,76 @@ __device__ inline int act_elem(const uint8_t *row, const BlockInfo &bi, int t) {
   return sext_bits(nib | (top << 4), 6);
 }
 
-// Weight slab in the stream layout (see DGeo); c = column within the slab,
-// sm = sign-magnitude codes (symmetric clamp).
-__device__ inline int wstream_elem(const uint8_t *slab, const DGeo &dg, const BlockInfo &bi,
-                                   int c, int t, bool sm) {
-  const DLoc L = d_loc(bi.seg, bi.idx);
-  const uint8_t *chunk = slab + wd_seg_off(dg, bi.seg) + step_data_off(L.st, wd_step_data(bi.seg));
-  const int ln = 16 * (L.g0 + (t >> 4)) + c;
-  const int u = t & 15;                     // element within the half
-  if (bi.m == 8) return (int)(int8_t)chunk[16 * ln + u];
-  const int d = u >> 3, k = u & 7;
-  const uint8_t *nb = bi.m == 4 ? chunk + 16 * ln + L.region : chunk + 8 * ln;
-  const uint32_t nib = (nb[4 * d + (k & 3)] >> (4 * (k >> 2))) & 15u;
-  if (bi.m == 4) return sm ? ((nib & 8u) ? -(int)(nib & 7u) : (int)(nib & 7u)) : sext_bits(nib, 4);
-  const uint32_t y = *(const uint32_t *)(chunk + 512 + 4 * ln);
-  const uint32_t top = (y >> (8 * (k & 3) + 4 * d + 2 * (k >> 2))) & 3u;
-  if (sm) {
-    const int a = (int)(top * 8u + (nib & 7u));
-    return (nib & 8u) ? -a : a;
-  }
-  return sext_bits(nib | (top << 4), 6);
-}
-
-// ---------------------------------------------------------------------------
-// Matrix-core operand layout for the block-scaled MFMA
-// (V_MFMA_SCALE_F32_32X32X64_F8F6F4).  That instruction multiplies FP6/FP8
-// elements and applies one E8M0 scale per 32-element K-block of each operand
-// in hardware.  An MXINT mantissa becomes one or two exactly representable
-// "digits" whose weights are folded into the element values, so the block's
-// E8M0 scale byte is the MXINT shared exponent E itself (MXSens Section 2:
-// value = q * 2^(E - 127 - (m - 2))):
-//   m = 4: one FP6 e3m2 element q/4;
-//   m = 6: h = floor(q / 8), l = q - 8h: FP6 e3m2 elements h/2 and l/16;
-//   m = 8: h = floor(q / 16), l = q - 16h: FP8 e4m3 elements h/4 and l/64.
-// The product of two 6-bit (8-bit) blocks is the sum of the four digit
-// products, computed by four (two) instructions over the same registers.
-//
-// K is walked in "steps", each one K-group of the instruction per lane half
-// (lanes 32h..32h+31 hold rows / columns 0..31 of a 32-wide tile):
-//   4-bit: 4 blocks (two instructions, block pairs (4t, 4t+1), (4t+2, 4t+3));
-//   6-bit: a block pair, 8-bit: one block.
-// 4-bit blocks are padded to a multiple of 4 and 6-bit blocks to a multiple
-// of 2 with zero blocks.  Lane half h (lanes 32h..32h+31) of a step holds:
-//   4-bit step t: blocks 4t+h then 4t+2+h, 24 bytes each (48 bytes);
-//   6-bit pair p: block 2p+h as its h-digit plane then its l-digit plane
-//                 (24 bytes each);
-//   8-bit block:  h digits of elements 16h..16h+15, then their l digits
-//                 (32 bytes; weights repeat the h digits: 48 bytes).
-// FP6 elements are packed little-endian, element e of a block at bits 6e.
-// ---------------------------------------------------------------------------
-struct OpGeo {
-  int n4, n6, n8;
-  int n4p, n6p;          // padded segment lengths
-  int s4, s6, s8;        // steps per segment
-  int nsteps;
-  int64_t off6, off8;    // byte offsets of the 6- and 8-bit segments in a row
-  __host__ __device__ OpGeo(int a, int b, int c)
-      : n4(a), n6(b), n8(c), n4p((a + 3) & ~3), n6p((b + 1) & ~1), s4(n4p / 4),
-        s6(n6p / 2), s8(c), nsteps(s4 + s6 + c), off6(24LL * n4p),
-        off8(24LL * n4p + 48LL * n6p) {}
-  __host__ __device__ int seg(int st) const { return st < s4 ? 0 : (st < s4 + s6 ? 1 : 2); }
+// The block (block index b of the width map, segment seg, step st, position
+// within the step) a weight element belongs to.
+struct WLoc {
+  int seg, st, pos;   // pos: lane group (3/4-bit) or block of the pair (6/8-bit)
 };
-
-// Weight operand image: 128-column tiles, each a run of per-step chunks of
-// kOpChunk bytes; a chunk holds three 16-byte parts of every (half, column)
-// lane and the lane's scale dword (byte 0: first scale, byte 1: second scale
-// of a 4-bit step), laid out as the prefill GEMM keeps it in LDS:
-//   part j at j * 4096 + h * 2048 + c * 16, scales at 12288 + h * 512 +
-//   (c % 32) * 16 + (c / 32) * 4 (a lane's four 32-column tiles' scale
-//   dwords are adjacent: one 16-byte LDS read per step).
-constexpr int kOpCols = 128;
-constexpr int kActRows = 32;
-constexpr int kActStep = 3072;       // operand bytes per (32-row tile, step)
-constexpr int kActScaleStep = 256;   // scale bytes per (32-row tile, step)
-
-// Activation operand image: byte o (0..47) of lane data (row, st, h), and
-// scale byte j (0, 1) of (row, st, h).
-__host__ __device__ inline int64_t act_op_loc(int64_t row, int st, int nsteps, int h, int o) {
-  return ((row >> 5) * nsteps + st) * (int64_t)kActStep + (o >> 4) * 1024 + h * 512 +
-         (row & 31) * 16 + (o & 15);
-}
-__host__ __device__ inline int64_t act_sc_loc(int64_t row, int st, int nsteps, int h, int j) {
-  return ((row >> 5) * nsteps + st) * (int64_t)kActScaleStep + h * 128 + (row & 31) * 4 + j;
-}
-__host__ __device__ inline int64_t act_op_bytes(const OpGeo &o, int64_t rows) {
-  return (rows + kActRows - 1) / kActRows * o.nsteps * (int64_t)kActStep;
-}
-__host__ __device__ inline int64_t act_sc_bytes(const OpGeo &o, int64_t rows) {
-  return (rows + kActRows - 1) / kActRows * o.nsteps * (int64_t)kActScaleStep;
-}
-constexpr int kOpChunk = 13312;
-constexpr int kOpPart = 4096;
-
-__host__ __device__ inline int64_t op_tile_bytes(const OpGeo &o) {
-  return (int64_t)kOpChunk * o.nsteps;
+__host__ __device__ inline WLoc w_loc(const LGeo &g, int b) {
+  WLoc r;
+  int s = 3;
+  while (s > 0 && b < g.b0[s]) --s;
+  const int i = b - g.b0[s];
+  r.seg = s;
+  r.st = g.st0[s] + (s < 2 ? i / 4 : i / 2);
+  r.pos = s < 2 ? i % 4 : i % 2;
+  return r;
 }
 
-// Location (relative to its tile) of byte `o` (0..47) of lane (h, c) of step st.
-__host__ __device__ inline int64_t w_op_loc(int st, int h, int c, int o) {
-  return (int64_t)kOpChunk * st + (o >> 4) * kOpPart + h * 2048 + c * 16 + (o & 15);
-}
-__host__ __device__ inline int64_t w_op_scale(int st, int h, int c) {
-  return (int64_t)kOpChunk * st + 3 * kOpPart + h * 512 + (c & 31) * 16 + (c >> 5) * 4;
-}
-
-// FP6 e3m2 code of n/16 (|n| <= 32, n exactly representable).
-__host__ __device__ inline uint32_t e3m2_sixteenths(int n) {
-  const uint32_t a = (uint32_t)(n < 0 ? -n : n);
-  uint32_t mag = a;
-  if (a >= 4) {
-    const int e = 30 - __builtin_clz(a);      // floor(log2 a) - 1
-    mag = ((uint32_t)e << 2) | ((a >> (e - 1)) - 4u);
+// Mantissa t of block b of weight column `col` (any column of the padded
+// super-slabs), read back from the weight layout.
+__device__ inline int w_elem(const uint8_t *w_mant, const LGeo &g, bool full, int64_t col,
+                             int b, int t) {
+  const WLoc L = w_loc(g, b);
+  const int n = (int)((col % kWCols) >> 4), c = (int)(col & 15);
+  const uint8_t *chunk = w_mant + (col / kWCols) * w_super_bytes(g, full) +
+                         w_step_off(g, L.st, full) + (int64_t)n * w_chunk_bytes(L.seg, full);
+  uint32_t d[6], x[4];
+  if (L.seg <= 1) {
+    const int l = 16 * L.pos + c;
+    if (L.seg == 0 && !full) {
+      x[0] = *(const uint32_t *)(chunk + 8 * l);
+      x[1] = *(const uint32_t *)(chunk + 8 * l + 4);
+      x[2] = *(const uint32_t *)(chunk + 512 + 4 * l);
+      unfold3(x, d);
+    } else if (L.seg == 1 && full) {
+      for (int k = 0; k < 4; ++k) d[k] = *(const uint32_t *)(chunk + 16 * l + 4 * k);
+      for (int k = 0; k < 2; ++k) d[4 + k] = *(const uint32_t *)(chunk + 1024 + 8 * l + 4 * k);
+    } else {
+      for (int k = 0; k < 4; ++k) x[k] = *(const uint32_t *)(chunk + 16 * l + 4 * k);
+      unfold4(x, d);
+    }
+    const uint32_t code = fp6_code(d, t);
+    const int mag = (int)(code & 31u);
+    return (code & 32u) ? -mag : mag;
   }
-  return (n < 0 ? 32u : 0u) | mag;
-}
-
-// FP8 e4m3 code of n/64 (|n| <= 128, n exactly representable).
-__host__ __device__ inline uint32_t e4m3_sixtyfourths(int n) {
-  const uint32_t a = (uint32_t)(n < 0 ? -n : n);
-  if (a == 0) return 0;
-  const int e = 32 - __builtin_clz(a);        // floor(log2 a) + 1
-  const uint32_t mant = ((a << 3) >> (e - 1)) - 8u;
-  return (n < 0 ? 128u : 0u) | ((uint32_t)e << 3) | mant;
-}
-
-// Digits of one mantissa: d0 (the only one for m = 4) and d1.
-__host__ __device__ inline void mxint_digits(int q, int m, uint32_t &d0, uint32_t &d1) {
-  if (m == 4) {
-    d0 = e3m2_sixteenths(4 * q);
-    d1 = 0;
-  } else if (m == 6) {
-    const int h = q >> 3;                     // arithmetic: floor(q / 8)
-    d0 = e3m2_sixteenths(8 * h);
-    d1 = e3m2_sixteenths(q - 8 * h);
+  const int jc = 16 * L.pos + c;
+  if (L.seg == 3) {
+    const uint32_t v = chunk[32 * jc + t];
+    if (full) return (int)(int8_t)v;
+    return (v & 128u) ? -(int)(v & 127u) : (int)(v & 127u);
+  }
+  uint32_t lo[6], hi[6];
+  for (int k = 0; k < 4; ++k) x[k] = *(const uint32_t *)(chunk + 16 * jc + 4 * k);
+  unfold4(x, lo);
+  if (full) {
+    for (int k = 0; k < 4; ++k) x[k] = *(const uint32_t *)(chunk + 512 + 16 * jc + 4 * k);
+    unfold4(x, hi);
   } else {
-    const int h = q >> 4;
-    d0 = e4m3_sixtyfourths(16 * h);
-    d1 = e4m3_sixtyfourths(q - 16 * h);
+    for (int k = 0; k < 2; ++k) x[k] = *(const uint32_t *)(chunk + 512 + 8 * jc + 4 * k);
+    unfold2(x, lo, hi);
   }
+  const uint32_t cl = fp6_code(lo, t), ch = fp6_code(hi, t);
+  const int a = (int)(8 * (ch & 31u) + (cl & 31u));
+  return (cl & 32u) ? -a : a;
+}
+// The exponent of block b of column col, from the scale words.
+__device__ inline int w_exp_of(const uint8_t *w_exp, const LGeo &g, int64_t col, int b) {
+  const WLoc L = w_loc(g, b);
+  const int n = (int)((col % kWCols) >> 4), c = (int)(col & 15);
+  const int grp = g.group_of(L.st), k = g.byte_of(L.st);
+  const int lane = L.seg <= 1 ? 16 * L.pos + c : 16 * (2 * L.pos) + c;
+  return w_exp[(col / kWCols) * w_super_scale_bytes(g) + (int64_t)grp * 2048 + 32 * lane + 8 * k + n];
 }
 
 }  // namespace mxq

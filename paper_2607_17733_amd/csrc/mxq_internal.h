@@ -13,28 +13,27 @@ struct QuantArgs {
   const uint16_t *src;     // bf16 rows [src_rows][ld]
   int64_t ld;
   int64_t src_rows;        // rows with data (M, or N for weights)
-  int64_t out_rows;        // rows written (M, or N rounded up to 16)
+  int64_t out_rows;        // rows written (activations: M, or M rounded up to
+                           // 16 for the operand image; weights: N rounded up
+                           // to 128)
   int64_t K;
   const int32_t *perm;     // device, K entries, or nullptr
   int n4, n6, n8;
-  int n3;                  // the first n3 of the 4-bit blocks are 3-bit (stored as 2q)
+  int n3;                  // the first n3 of the n4 blocks are 3-bit
   int ties_away, full_clamp;
-  uint8_t *mant;
-  uint8_t *exp;
+  uint8_t *mant;           // canonical packed rows (activations), weight data
+  uint8_t *exp;            // exponent rows (activations), weight scale words
   int64_t out_rb;          // packed row stride (activations)
   int64_t out_erb;         // exponent row stride
   int64_t canon_rb;        // packed section bytes per row
   int64_t canon_erb;       // exponent bytes per row
-  int64_t op_off, sc_off;  // activations: offsets of the operand image in mant
-                           // and of its scale bytes in exp
-  int dimg;                // activations: write the decode image (M <= 16)
   int64_t row_used;        // unpadded packed bytes per row
-  int64_t slab_rows;       // weights: columns in the packed slabs (N rounded to 16)
-  int64_t w_op;            // weights: offset of the operand image in the buffer
-  int64_t w_tile;          // weights: bytes per 128-column operand tile
-  int tail_pad;            // weights: zero bytes after the last slab
-  int stage;               // weights: stage source rows in LDS before the gather;
-                           // activations: unused
+  // activations: which outputs to write
+  int write_rows, write_image;
+  uint8_t *img;            // operand image (16-row tiles)
+  uint8_t *img_exp;        // its scale words
+  int64_t a_tile, a_tile_sc;  // bytes per 16-row tile of each
+  int stage;               // weights: stage source rows in LDS before the gather
   int vec16;               // 16-byte source loads are aligned
   int rows_per_wg;         // filled by the launcher
   int lg_rows;             // activations: log2 of the rows per group
@@ -48,22 +47,18 @@ struct QuantArgs {
 };
 
 struct GemmArgs {
-  const uint8_t *a_mant;
-  const uint8_t *a_exp;
-  const uint8_t *w_mant;
-  const uint8_t *w_exp;
+  const uint8_t *a_mant;   // operand image (gemm) or packed rows (partials)
+  const uint8_t *a_exp;    // its scale words (gemm) or exponent rows (partials)
+  const uint8_t *w_mant;   // weight data
+  const uint8_t *w_exp;    // weight scale words
   float *y;                // [M][ldy] (gemm)
   int32_t *p;              // [M][N][nb] (partials)
   int64_t M, N, ldy;
-  int64_t a_rb, a_erb;     // packed activation row stride / exponent row stride
-  int64_t a_op, a_sc;      // offsets of the operand image in a_mant / of its
-                           // scale bytes in a_exp
-  int64_t w_erb;           // weight exponent row stride
-  int64_t w_op;            // offset of the weight operand image in w_mant
-  int64_t w_tile;          // bytes per 128-column tile of that image
-  int64_t npad;            // N rounded up to 16
-  int n4, n6, n8;
-  int sm;                  // weight stream codes are sign-magnitude (symmetric clamp)
+  int64_t a_rb, a_erb;     // packed activation row / exponent row strides (partials)
+  int64_t a_tile, a_tile_sc;      // operand image bytes per 16-row tile
+  int64_t w_super, w_super_sc;    // weight bytes per 128-column super-slab
+  int n3, n4, n6, n8;
+  int full;                // full clamp: the weights' full-range encodings
 };
 
 struct UnpackArgs {
@@ -73,16 +68,16 @@ struct UnpackArgs {
   uint8_t *e;              // [rows][nb]
   int64_t rows, K;
   int64_t a_rb, a_erb;     // activation layout
-  int64_t npad;            // weight layout
-  int n4, n6, n8;
-  int sm;                  // weight stream codes are sign-magnitude (symmetric clamp)
+  int64_t w_super, w_super_sc;  // weight layout
+  int n3, n4, n6, n8;
+  int full;
 };
 
 constexpr int64_t kMaxLds = 160 * 1024;   // LDS per workgroup on gfx950
 
 hipError_t launch_quantize(const QuantArgs &args, bool weights, hipStream_t s);
-int quantize_rows_per_wg(int64_t K);
 hipError_t launch_quantize_act(const QuantArgs &args, hipStream_t s);
+int quantize_act_padded_blocks(int n3, int n4, int n6, int n8);
 int quantize_act_rows(int64_t K, int padded_blocks, bool perm, bool rmsnorm = false);
 int64_t quantize_act_lds(int64_t K, int padded_blocks, bool perm, bool rmsnorm = false);
 hipError_t launch_gemm_prefill(const GemmArgs &args, hipStream_t s);
@@ -117,7 +112,7 @@ struct AttnArgs {
   int64_t exp_bytes;       // exponent row stride
   int64_t tokens_per_split;
   int splits;
-  int n4, n6, n8;
+  int n3, n4, n6, n8;
 };
 
 constexpr int kAttnMaxSplits = 512;    // attn_tokens_per_split never asks for more

@@ -5,18 +5,19 @@
 // exponent and one mantissa width, the same quantizer as the activations.
 //
 // Work decomposition: a thread owns 8 consecutive elements of a block (a
-// "group"), so the 4 threads of a block are adjacent lanes; the block
+// "quarter"), so the 4 threads of a block are adjacent lanes; the block
 // maximum is a 2-step xor-shuffle reduction of integer |bf16| bit patterns.
-// A workgroup owns one row (K >= 2048) or several whole rows (short K, e.g.
-// the 128-wide KV-cache rows).  With a column permutation the workgroup first
-// stages its source rows in LDS with 16-byte coalesced loads and gathers from
-// LDS, so the permutation never turns into scattered global loads.
+// A workgroup owns one row (K >= 2048) or several whole rows (short K).
+// With a column permutation the workgroup first stages its source rows in
+// LDS with 16-byte coalesced loads and gathers from LDS.
 //
-// Every column is written twice: into the 16-column slabs of the stream
-// layout (packed mantissas in the decode GEMM's lane order, see DGeo), and
-// into the 128-column tiles of the matrix-core operand image (FP6/FP8
-// digits of each mantissa, the layout described with OpGeo) with their E8M0
-// scale bytes, which the prefill GEMM reads.
+// Output: the weight layout of both GEMMs (LGeo in mxq_device.h), one copy
+// at the MXINT size: the folded FP6 codes of 3- and 4-bit blocks, the two
+// digit planes of 6-bit blocks, the mantissa bytes of 8-bit blocks, and the
+// scale words (each block's exponent E).  The four quarters of a block
+// assemble its FP6 operand words by xor-shuffles before folding them.  The
+// padding of the segments (up to whole steps) and of the columns (up to
+// whole 128-column super-slabs) is written as zeros.
 #include "mxq_device.h"
 #include "mxq_internal.h"
 
@@ -26,20 +27,40 @@ namespace {
 
 constexpr int kThreads = 256;
 
+// OR of the words of the 4 quarters of a block (adjacent lanes).
+__device__ inline void or4(uint32_t *d, int n) {
+  for (int k = 0; k < n; ++k) {
+    d[k] |= __shfl_xor(d[k], 1);
+    d[k] |= __shfl_xor(d[k], 2);
+  }
+}
+
+// The six operand words of 8 six-bit codes at elements 8kg..8kg+7 (the
+// other quarters' bits zero): the 48 bits start at bit 48 kg.
+__device__ inline void quarter_words(const uint32_t *c, int kg, uint32_t *d) {
+  uint64_t v = 0;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) v |= (uint64_t)(c[u] & 63u) << (6 * u);
+  v <<= 16 * (kg & 1);
+  const int w0 = (kg >> 1) * 3 + (kg & 1);
+  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+#pragma unroll
+  for (int j = 0; j < 6; ++j) d[j] = (j == w0 ? lo : 0u) | (j == w0 + 1 ? hi : 0u);
+}
+
 __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
   extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
   const int t = threadIdx.x;
   const int64_t K = q.K;
-  const int nb = (int)(K / kBlock);
-  const int G = 4 * nb;                      // groups per row
+  const LGeo lg(q.n3, q.n4, q.n6, q.n8);
+  const bool full = q.full_clamp != 0;
+  int npb = 0;                               // padded blocks of a column
+  for (int s = 0; s < kSegs; ++s) npb += lg.S[s] * (s < 2 ? 4 : 2);
+  const int G = 4 * npb;                     // quarters per column
   const int R = q.rows_per_wg;
   const int64_t row0 = (int64_t)blockIdx.x * R;
-  const Segs s{q.n4, q.n6, q.n8};
-  // LDS: [R][K] staged bf16 source rows (permuted path only).
-  uint16_t *srow = (uint16_t *)smem;
-  const OpGeo og(q.n4, q.n6, q.n8);
+  uint16_t *srow = (uint16_t *)smem;         // [R][K] staged source rows
 
-  // Stage the workgroup's source rows in LDS (permuted path only).
   if (q.stage) {
     const int64_t total = (int64_t)R * K;
     if (q.vec16) {
@@ -48,8 +69,7 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
         const int64_t col = v * 8 - (int64_t)lr * K;
         const int64_t row = row0 + lr;
         uint4 d = make_uint4(0, 0, 0, 0);
-        if (row < q.src_rows)
-          d = *(const uint4 *)(q.src + row * q.ld + col);
+        if (row < q.src_rows) d = *(const uint4 *)(q.src + row * q.ld + col);
         *(uint4 *)(srow + (int64_t)lr * K + col) = d;
       }
     } else {
@@ -65,29 +85,39 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
 
   for (int64_t f = t; f < (int64_t)R * G; f += kThreads) {
     const int lr = (int)(f / G);
-    const int g = (int)(f - (int64_t)lr * G);
-    const int64_t row = row0 + lr;
-    const bool live = row < q.out_rows;      // a whole block shares `live`
-    const int b = g >> 2, kg = g & 3;
-    const BlockInfo bi = block_info(s, b);
+    const int gq = (int)(f - (int64_t)lr * G);
+    const int64_t row = row0 + lr;           // the weight column
+    // the last workgroup's rows may pass the padded column count (a block's
+    // four quarters skip together, so the shuffles stay within live lanes)
+    if (row >= q.out_rows) continue;
+    const int pb = gq >> 2, kg = gq & 3;
+    // segment, step, position within the step, and the width-map block
+    int s = 0, rem = pb;
+    while (s < kSegs - 1 && rem >= lg.S[s] * (s < 2 ? 4 : 2)) {
+      rem -= lg.S[s] * (s < 2 ? 4 : 2);
+      ++s;
+    }
+    const int per = s < 2 ? 4 : 2;
+    const int st = lg.st0[s] + rem / per, pos = rem % per;
+    const bool real = rem < lg.nb[s];
+    const int b = lg.b0[s] + rem;
+    const int m = s == 0 ? 3 : s == 1 ? 4 : s == 2 ? 6 : 8;
+    const bool live = real && row < q.src_rows;
 
-    // Gather the 8 source elements of the group.
     uint32_t bits[8];
     const int64_t p0 = (int64_t)b * kBlock + 8 * kg;
-    if (!live || row >= q.src_rows) {
+    if (!live) {
 #pragma unroll
       for (int u = 0; u < 8; ++u) bits[u] = 0;
     } else if (q.perm) {
       const int4 pa = *(const int4 *)(q.perm + p0);
-      const int4 pb = *(const int4 *)(q.perm + p0 + 4);
-      const int src[8] = {pa.x, pa.y, pa.z, pa.w, pb.x, pb.y, pb.z, pb.w};
+      const int4 pc = *(const int4 *)(q.perm + p0 + 4);
+      const int src[8] = {pa.x, pa.y, pa.z, pa.w, pc.x, pc.y, pc.z, pc.w};
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const bool ok = src[u] >= 0 && (int64_t)src[u] < K;
         uint32_t v = 0;
-        if (ok)
-          v = q.stage ? srow[(int64_t)lr * K + src[u]]
-                      : q.src[row * q.ld + src[u]];
+        if (ok) v = q.stage ? srow[(int64_t)lr * K + src[u]] : q.src[row * q.ld + src[u]];
         bits[u] = v;
       }
     } else if (q.vec16) {
@@ -103,7 +133,6 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
       for (int u = 0; u < 8; ++u) bits[u] = q.src[row * q.ld + p0 + u];
     }
 
-    // Block maximum of |x| on the integer bit patterns.
     uint32_t amax = 0;
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
@@ -114,162 +143,84 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
     amax = o > amax ? o : amax;
     o = __shfl_xor(amax, 2);
     amax = o > amax ? o : amax;
-    const int E = block_exponent(amax);
-
+    const int E = live ? block_exponent(amax) : 0;
     int qv[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
-      qv[u] = b < q.n3 ? 2 * quant_elem(bits[u], E, 3, q.ties_away, q.full_clamp)
-                       : quant_elem(bits[u], E, bi.m, q.ties_away, q.full_clamp);
+    for (int u = 0; u < 8; ++u) qv[u] = live ? quant_elem(bits[u], E, m, q.ties_away, q.full_clamp) : 0;
 
-    // stream-layout nibble codes, and (6-bit) the 2-bit codes of the half's
-    // 16 elements: element 8d+k of the half at bits 8(k%4) + 4d + 2(k/4)
-    const bool sm = !q.full_clamp;
-    const uint32_t nib = stream_nibbles(qv, bi.m, sm);
-    uint32_t top = 0;
-    if (bi.m == 6) {
-      const int dd = kg & 1;
-#pragma unroll
-      for (int k = 0; k < 8; ++k)
-        top |= stream_top2(qv[k], sm) << (8 * (k & 3) + 4 * dd + 2 * (k >> 2));
-      top |= __shfl_xor(top, 1);             // merge the lane pair's word
-    }
-    if (!live) continue;
+    // where the block goes
+    const int64_t col = row;
+    const int n = (int)((col % kWCols) >> 4), c = (int)(col & 15);
+    uint8_t *chunk = q.mant + (col / kWCols) * w_super_bytes(lg, full) + w_step_off(lg, st, full) +
+                     (int64_t)n * w_chunk_bytes(s, full);
+    uint8_t *scl = q.exp + (col / kWCols) * w_super_scale_bytes(lg) +
+                   (int64_t)lg.group_of(st) * 2048 + 8 * lg.byte_of(st) + n;
 
-    uint32_t lo8 = 0, hi8 = 0;
+    if (s <= 1) {
+      uint32_t codes[8], d[6], x[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      lo8 |= ((uint32_t)qv[u] & 255u) << (8 * u);
-      hi8 |= ((uint32_t)qv[4 + u] & 255u) << (8 * u);
-    }
-    // digit codes of the 8 mantissas (MXINT -> FP6 / FP8 elements)
-    uint32_t d0[8], d1[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) mxint_digits(qv[u], bi.m, d0[u], d1[u]);
-    // step, lane half and (4-bit) pair of this block
-    int st, h, j = 0;
-    if (bi.m == 4) { st = bi.idx >> 2; h = bi.idx & 1; j = (bi.idx >> 1) & 1; }
-    else if (bi.m == 6) { st = og.s4 + (bi.idx >> 1); h = bi.idx & 1; }
-    else { st = og.s4 + og.s6 + bi.idx; h = kg >> 1; }
-
-    {
-      const int c = (int)(row % kOpCols);
-      uint8_t *tile = q.mant + q.w_op + (row / kOpCols) * q.w_tile;
-      if (row < q.slab_rows) {
-        // stream layout of the 16-column slab (decode GEMM)
-        const DGeo dg(q.n4, q.n6, q.n8);
-        const int c16 = (int)(row & 15);
-        uint8_t *slab = q.mant + (row >> 4) * wd_slab_bytes(dg);
-        const DLoc L = d_loc(bi.seg, bi.idx);
-        const int sd = wd_step_data(bi.seg);
-        uint8_t *segp = slab + wd_seg_off(dg, bi.seg);
-        uint8_t *chunk = segp + step_data_off(L.st, sd);
-        const int dd = kg & 1;
-        const int ln = 16 * (L.g0 + (kg >> 1)) + c16;
-        if (bi.m == 4) {
-          *(uint32_t *)(chunk + 16 * ln + L.region + 4 * dd) = nib;
-        } else if (bi.m == 6) {
-          *(uint32_t *)(chunk + 8 * ln + 4 * dd) = nib;
-          if (dd == 0) *(uint32_t *)(chunk + 512 + 4 * ln) = top;
-        } else {
-          *(uint32_t *)(chunk + 16 * ln + 8 * dd) = lo8;
-          *(uint32_t *)(chunk + 16 * ln + 8 * dd + 4) = hi8;
-        }
-        if (kg == 0) {
-          segp[step_scale_off(L.st, sd, 16 * L.sg0 + c16)] = (uint8_t)E;
-          if (bi.seg) segp[step_scale_off(L.st, sd, 16 * L.sg1 + c16)] = (uint8_t)E;
-          q.exp[row * q.out_erb + b] = (uint8_t)E;
-        }
-        if (g == 0) {
-          for (int64_t z = nb; z < q.out_erb; ++z) q.exp[row * q.out_erb + z] = 0;
-          // zero the stream padding blocks of this column
-          const int nseg[3] = {dg.n4, dg.n6, dg.n8};
-          const int npad[3] = {4 * dg.S[0], 2 * dg.S[1], 2 * dg.S[2]};
-          for (int sg = 0; sg < 3; ++sg) {
-            const int psd = wd_step_data(sg);
-            uint8_t *pseg = slab + wd_seg_off(dg, sg);
-            for (int idx = nseg[sg]; idx < npad[sg]; ++idx) {
-              const DLoc P = d_loc(sg, idx);
-              uint8_t *pc = pseg + step_data_off(P.st, psd);
-              for (int hh = 0; hh < 2; ++hh) {
-                const int pl = 16 * (P.g0 + hh) + c16;
-                if (sg == 0) {
-                  *(uint2 *)(pc + 16 * pl + P.region) = make_uint2(0, 0);
-                } else if (sg == 1) {
-                  *(uint2 *)(pc + 8 * pl) = make_uint2(0, 0);
-                  *(uint32_t *)(pc + 512 + 4 * pl) = 0;
-                } else {
-                  *(uint4 *)(pc + 16 * pl) = make_uint4(0, 0, 0, 0);
-                }
-              }
-              pseg[step_scale_off(P.st, psd, 16 * P.sg0 + c16)] = 0;
-              if (sg) pseg[step_scale_off(P.st, psd, 16 * P.sg1 + c16)] = 0;
-            }
-            // the unused scale bytes of a short last group
-            const int S = dg.S[sg];
-            for (int st = S; st < (S + kStreamGroup - 1) / kStreamGroup * kStreamGroup; ++st)
-              for (int gg = 0; gg < 4; ++gg) pseg[step_scale_off(st, psd, 16 * gg + c16)] = 0;
-          }
-        }
-      }
-      if (row == 0 && g == 0)                // the packed section's tail padding
-        for (int z = 0; z < q.tail_pad; ++z)
-          q.mant[q.slab_rows / 16 * wd_slab_bytes(DGeo(q.n4, q.n6, q.n8)) + z] = 0;
-      // operand image (128-column tiles of per-step chunks)
-      if (bi.m == 8) {
-        uint32_t h0 = 0, h1 = 0, l0 = 0, l1 = 0;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          h0 |= d0[u] << (8 * u); h1 |= d0[4 + u] << (8 * u);
-          l0 |= d1[u] << (8 * u); l1 |= d1[4 + u] << (8 * u);
-        }
-        const int o = 8 * (kg & 1);
-        *(uint2 *)(tile + w_op_loc(st, h, c, o)) = make_uint2(h0, h1);
-        *(uint2 *)(tile + w_op_loc(st, h, c, 16 + o)) = make_uint2(l0, l1);
-        *(uint2 *)(tile + w_op_loc(st, h, c, 32 + o)) = make_uint2(h0, h1);
+      for (int u = 0; u < 8; ++u) codes[u] = w_code34(qv[u]);
+      quarter_words(codes, kg, d);
+      or4(d, 6);
+      const int l = 16 * pos + c;
+      if (s == 0 && !full) {
+        fold3(d, x);
+        if (kg < 2) *(uint32_t *)(chunk + 8 * l + 4 * kg) = x[kg];
+        else if (kg == 2) *(uint32_t *)(chunk + 512 + 4 * l) = x[2];
+      } else if (s == 1 && full) {
+        *(uint32_t *)(chunk + 16 * l + 4 * kg) = d[kg];
+        if (kg < 2) *(uint32_t *)(chunk + 1024 + 8 * l + 4 * kg) = d[4 + kg];
       } else {
-        uint64_t v0 = 0, v1 = 0;
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          v0 |= (uint64_t)d0[u] << (6 * u);
-          v1 |= (uint64_t)d1[u] << (6 * u);
-        }
-        const int o = (bi.m == 4 ? 24 * j : 0) + 6 * kg;
-#pragma unroll
-        for (int k = 0; k < 3; ++k)
-          *(uint16_t *)(tile + w_op_loc(st, h, c, o + 2 * k)) = (uint16_t)(v0 >> (16 * k));
-        if (bi.m == 6)
-#pragma unroll
-          for (int k = 0; k < 3; ++k)
-            *(uint16_t *)(tile + w_op_loc(st, h, c, 24 + o + 2 * k)) = (uint16_t)(v1 >> (16 * k));
+        fold4(d, x);
+        *(uint32_t *)(chunk + 16 * l + 4 * kg) = x[kg];
       }
-      if (kg == 0) {                         // scale dword of the lane: bytes su0, su1, 0, 0
-        if (bi.m == 4) {
-          uint8_t *sp = tile + w_op_scale(st, h, c);
-          sp[j] = (uint8_t)E;
-          if (j == 0) *(uint16_t *)(sp + 2) = 0;
-        } else if (bi.m == 6) {
-          *(uint32_t *)(tile + w_op_scale(st, h, c)) = (uint32_t)E;
-        } else {
-          *(uint32_t *)(tile + w_op_scale(st, 0, c)) = (uint32_t)E;
-          *(uint32_t *)(tile + w_op_scale(st, 1, c)) = (uint32_t)E;
-        }
+      if (kg == 0) scl[32 * l] = (uint8_t)E;
+    } else if (s == 2) {
+      uint32_t ch[8], cl[8], dh[6], dl[6], x[4];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        w_code6(qv[u], ch[u], cl[u]);
+        if (!full) ch[u] &= 31u;             // the high plane keeps no sign
       }
-      if (g == 0) {                          // zero the pad blocks of the column
-        for (int i = og.n4; i < og.n4p; ++i) {
-          const int pst = i >> 2, ph = i & 1, pj = (i >> 1) & 1;
-          for (int z = 0; z < 24; z += 2)
-            *(uint16_t *)(tile + w_op_loc(pst, ph, c, 24 * pj + z)) = 0;
-          uint8_t *sp = tile + w_op_scale(pst, ph, c);
-          sp[pj] = 0;
-          if (pj == 0) *(uint16_t *)(sp + 2) = 0;
-        }
-        if (og.n6p > og.n6) {
-          const int pst = og.s4 + (og.n6 >> 1);
-          for (int z = 0; z < 48; z += 2)
-            *(uint16_t *)(tile + w_op_loc(pst, 1, c, z)) = 0;
-          *(uint32_t *)(tile + w_op_scale(pst, 1, c)) = 0;
-        }
+      quarter_words(cl, kg, dl);
+      quarter_words(ch, kg, dh);
+      or4(dl, 6);
+      or4(dh, 6);
+      const int jc = 16 * pos + c;
+      fold4(dl, x);
+      *(uint32_t *)(chunk + 16 * jc + 4 * kg) = x[kg];
+      if (full) {
+        fold4(dh, x);
+        *(uint32_t *)(chunk + 512 + 16 * jc + 4 * kg) = x[kg];
+      } else {
+        fold2(dh, x);
+        if (kg < 2) *(uint32_t *)(chunk + 512 + 8 * jc + 4 * kg) = x[kg];
+      }
+      if (kg == 0) {
+        scl[32 * (16 * (2 * pos) + c)] = (uint8_t)E;
+        scl[32 * (16 * (2 * pos + 1) + c)] = (uint8_t)E;
+      }
+    } else {
+      uint32_t w0 = 0, w1 = 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        w0 |= w_code8(qv[u], full) << (8 * u);
+        w1 |= w_code8(qv[4 + u], full) << (8 * u);
+      }
+      const int jc = 16 * pos + c;
+      *(uint2 *)(chunk + 32 * jc + 8 * kg) = make_uint2(w0, w1);
+      if (kg == 0) {
+        scl[32 * (16 * (2 * pos) + c)] = (uint8_t)E;
+        scl[32 * (16 * (2 * pos + 1) + c)] = (uint8_t)E;
+      }
+    }
+    // the unused scale bytes of a segment's short last group
+    if (kg == 0 && rem == 0) {
+      const int S = lg.S[s];
+      for (int k = S; k < (S + kGroupSteps - 1) / kGroupSteps * kGroupSteps; ++k) {
+        uint8_t *z = q.exp + (col / kWCols) * w_super_scale_bytes(lg) +
+                     (int64_t)(lg.G0[s] + k / kGroupSteps) * 2048 + 8 * (k % kGroupSteps) + n;
+        for (int gg = 0; gg < 4; ++gg) z[32 * (16 * gg + c)] = 0;
       }
     }
   }
@@ -277,28 +228,26 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(QuantArgs q) {
 
 }  // namespace
 
-hipError_t launch_quantize(const QuantArgs &args, bool weights,
-                           hipStream_t stream) {
+hipError_t launch_quantize(const QuantArgs &args, bool weights, hipStream_t stream) {
   if (!weights) return hipErrorInvalidValue;     // activations: launch_quantize_act
-  const int64_t K = args.K;
-  const int nb = (int)(K / kBlock);
-  const int G = 4 * nb;
+  const LGeo lg(args.n3, args.n4, args.n6, args.n8);
+  int npb = 0;
+  for (int s = 0; s < kSegs; ++s) npb += lg.S[s] * (s < 2 ? 4 : 2);
+  const int G = 4 * npb;
   QuantArgs a = args;
   a.rows_per_wg = G >= kThreads ? 1 : kThreads / G;
   const int64_t grid = (a.out_rows + a.rows_per_wg - 1) / a.rows_per_wg;
   if (grid <= 0) return hipSuccess;
-  const int64_t lds = a.stage ? (int64_t)a.rows_per_wg * K * 2 : 0;
+  // stage the source rows in LDS for the permutation gather when they fit;
+  // longer rows gather straight from global memory
+  a.stage = (a.perm && (int64_t)a.rows_per_wg * a.K * 2 <= kMaxLds) ? 1 : 0;
+  const int64_t lds = a.stage ? (int64_t)a.rows_per_wg * a.K * 2 : 0;
   if (lds > kMaxLds) return hipErrorInvalidValue;
   (void)hipFuncSetAttribute((const void *)quantize_kernel,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
-  hipLaunchKernelGGL(quantize_kernel, dim3((unsigned)grid), dim3(kThreads),
-                     (size_t)lds, stream, a);
+  hipLaunchKernelGGL(quantize_kernel, dim3((unsigned)grid), dim3(kThreads), (size_t)lds, stream,
+                     a);
   return hipGetLastError();
-}
-
-int quantize_rows_per_wg(int64_t K) {
-  const int64_t G = 4 * (K / kBlock);
-  return G >= kThreads ? 1 : (int)(kThreads / G);
 }
 
 }  // namespace mxq

@@ -93,20 +93,37 @@ __device__ inline uint32_t top_word(const Blk &v, int d) {
          ((e & 0x30303030u) >> 4);
 }
 
-// One (row, block) item: gather, quantize, pack, write.  sr is the staged
-// row in LDS, followed by zero padding.
+// The 3-bit two's-complement codes of the 32 elements, element t at bits 3t
+// of 96 bits (canonical packed row).
+__device__ inline void pack3(const Blk &v, uint32_t *w) {
+  w[0] = w[1] = w[2] = 0;
+#pragma unroll
+  for (int t = 0; t < 32; ++t) {
+    const uint32_t c = (uint32_t)(int)v[t] & 7u;
+    const int b = 3 * t;
+    w[b >> 5] |= c << (b & 31);
+    if ((b & 31) > 29) w[(b >> 5) + 1] |= c >> (32 - (b & 31));
+  }
+}
+
+// One (row, padded block) item: gather, quantize, write the canonical
+// packed row and exponent (q.write_rows) and / or the GEMM operand image
+// and its scale words (q.write_image).  sr is the staged row in LDS,
+// followed by zero padding.
 template <bool RNA>
-__device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp,
-                                     int64_t row, const uint8_t *sr) {
+__device__ inline void quantize_item(const QuantArgs &q, const LGeo &lg, int bp, int64_t row,
+                                     const uint8_t *sr) {
   const int K = (int)q.K;
-  const int ns = og.nsteps;
-  int seg, idx, n;
-  if (bp < og.n4p) { seg = 0; idx = bp; n = og.n4; }
-  else if (bp < og.n4p + og.n6p) { seg = 1; idx = bp - og.n4p; n = og.n6; }
-  else { seg = 2; idx = bp - og.n4p - og.n6p; n = og.n8; }
-  const bool pad = idx >= n;
-  const int m = 4 + 2 * seg;
-  const int b = seg == 0 ? idx : (seg == 1 ? og.n4 + idx : og.n4 + og.n6 + idx);
+  int s = 0, rem = bp;
+  while (s < kSegs - 1 && rem >= lg.S[s] * (s < 2 ? 4 : 2)) {
+    rem -= lg.S[s] * (s < 2 ? 4 : 2);
+    ++s;
+  }
+  const int per = s < 2 ? 4 : 2;
+  const int st = lg.st0[s] + rem / per, pos = rem % per;
+  const bool pad = rem >= lg.nb[s];
+  const int b = lg.b0[s] + rem;
+  const int m = s == 0 ? 3 : s == 1 ? 4 : s == 2 ? 6 : 8;
 
   // gather: pr[i] holds elements 2i (low half) and 2i+1 (high half)
   uint32_t pr[16];
@@ -152,13 +169,9 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
 #pragma unroll
     for (int i = 0; i < 16; ++i) v.e[i] = v.o[i] = 0.f;
   } else {
-    // a 3-bit block (the 3-6-8 template) is quantized with m = 3 and stored
-    // as the 4-bit block holding 2q, which has the same values
-    const bool three = seg == 0 && idx < q.n3;
-    const float qmax = three ? 3.f : (seg == 0 ? 7.f : (seg == 1 ? 31.f : 127.f));
+    const float qmax = (float)((1 << (m - 1)) - 1);
     const float qmin = q.full_clamp ? -(qmax + 1.f) : -qmax;
-    const int sh = 127 + (three ? 1 : m - 2) - E;
-    const float twice = three ? 2.f : 1.f;
+    const int sh = 127 + m - 2 - E;
 #pragma unroll
     for (int u = 0; u < 32; ++u) {
       const uint32_t bits = (u & 1) ? (pr[u >> 1] & 0xFFFF0000u) : (pr[u >> 1] << 16);
@@ -169,121 +182,95 @@ __device__ inline void quantize_item(const QuantArgs &q, const OpGeo &og, int bp
       } else {
         y = rintf(y);
       }
-      y = __builtin_amdgcn_fmed3f(y, qmin, qmax) * twice;
+      y = __builtin_amdgcn_fmed3f(y, qmin, qmax);
       if (u & 1) v.o[u >> 1] = y; else v.e[u >> 1] = y;
     }
   }
-
-  if (!pad) q.exp[row * q.out_erb + b] = (uint8_t)E;
   const uint32_t Eu = pad ? 0u : (uint32_t)E;
 
-  // packed row
-  uint8_t *prow = q.mant + row * q.out_rb;
-  if (!pad) {
-    if (seg == 0) {
-      *(u4 *)(prow + 16LL * idx) =
-          u4{nibbles8(v, 0), nibbles8(v, 8), nibbles8(v, 16), nibbles8(v, 24)};
-    } else if (seg == 1) {
-      uint8_t *p = prow + 16LL * og.n4 + 24LL * idx;
+  if (q.write_rows && !pad) {
+    q.exp[row * q.out_erb + b] = (uint8_t)E;
+    const Segs sg{q.n4, q.n6, q.n8, q.n3};
+    uint8_t *p = q.mant + row * q.out_rb + block_info(sg, b).aoff;
+    if (m == 3) {
+      uint32_t w[3];
+      pack3(v, w);
+      *(uint32_t *)p = w[0];
+      *(uint32_t *)(p + 4) = w[1];
+      *(uint32_t *)(p + 8) = w[2];
+    } else if (m == 4) {
+      *(u4 *)p = u4{nibbles8(v, 0), nibbles8(v, 8), nibbles8(v, 16), nibbles8(v, 24)};
+    } else if (m == 6) {
       *(u2 *)p = u2{nibbles8(v, 0), nibbles8(v, 8)};
       *(u2 *)(p + 8) = u2{nibbles8(v, 16), nibbles8(v, 24)};
       *(u2 *)(p + 16) = u2{top_word(v, 0), top_word(v, 1)};
     } else {
-      uint8_t *p = prow + 16LL * og.n4 + 24LL * og.n6 + 32LL * idx;
 #pragma unroll
       for (int d = 0; d < 4; ++d)
         *(u2 *)(p + 8 * d) = u2{bytes4(v, 8 * d), bytes4(v, 8 * d + 4)};
     }
   }
+  if (!q.write_image) return;
 
-  if (q.dimg) {
-    // decode image (M <= 16): the stream layout's ready operands, see DGeo
-    const DGeo dg(og.n4, og.n6, og.n8);
-    const DLoc L = d_loc(seg, idx);
-    const int sd = ad_step_data(seg);
-    uint8_t *segp = q.mant + q.op_off + ad_seg_off(dg, seg);
-    uint8_t *chunk = segp + step_data_off(L.st, sd);
-    if (seg == 0) {
-      const int l = 16 * L.sg0 + (int)row;
-      const v6u c = to_e3m2(v, 4.f);
-      *(u4 *)(chunk + 16 * l) = u4{c[0], c[1], c[2], c[3]};
-      *(u2 *)(chunk + 1024 + 8 * l) = u2{c[4], c[5]};
-      segp[step_scale_off(L.st, sd, l)] = (uint8_t)Eu;
-    } else {
-      Blk hd, ld;                              // q = 16 h + l
+  // operand image (16-row tiles) and its scale words
+  const int r = (int)(row & (kATileRows - 1));
+  uint8_t *stp = q.img + (row >> 4) * q.a_tile + a_step_off(lg, st);
+  uint8_t *scw = q.img_exp + (row >> 4) * q.a_tile_sc + (int64_t)lg.group_of(st) * 256 +
+                 lg.byte_of(st);
+  if (s <= 1) {
+    // E3M2 codes of q (4-bit) or of 2q (3-bit)
+    if (s == 0) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        hd.e[i] = floorf(v.e[i] * 0.0625f);
-        hd.o[i] = floorf(v.o[i] * 0.0625f);
-        ld.e[i] = fmaf(hd.e[i], -16.f, v.e[i]);
-        ld.o[i] = fmaf(hd.o[i], -16.f, v.o[i]);
+        v.e[i] *= 2.f;
+        v.o[i] *= 2.f;
       }
-      // digits summing to q * 2^-(m-2): h + l/16 (6-bit), h/4 + l/64 (8-bit)
-      const float dh = seg == 1 ? 1.f : 4.f, dl = seg == 1 ? 16.f : 64.f;
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int l = 16 * (L.g0 + h) + (int)row;
-        *(u4 *)(chunk + 32 * l) = to_e4m3(hd, h, dh);
-        *(u4 *)(chunk + 32 * l + 16) = to_e4m3(ld, h, dl);
-      }
-      segp[step_scale_off(L.st, sd, 16 * L.sg0 + (int)row)] = (uint8_t)Eu;
-      segp[step_scale_off(L.st, sd, 16 * L.sg1 + (int)row)] = (uint8_t)Eu;
     }
-    return;
-  }
-
-  // prefill operand image (32-row tiles) and its scale bytes
-  uint8_t *op = q.mant + q.op_off + ((row >> 5) * ns) * (int64_t)kActStep + (row & 31) * 16;
-  uint8_t *sc = q.exp + q.sc_off + ((row >> 5) * ns) * (int64_t)kActScaleStep + (row & 31) * 4;
-  if (seg == 0) {
-    const int st = idx >> 2, h = idx & 1, j = (idx >> 1) & 1;
-    uint8_t *o = op + st * kActStep + h * 512;
-    uint8_t *s = sc + st * kActScaleStep + h * 128;
-    const v6u c = to_e3m2(v, 4.f);
-    if (j == 0) {
-      *(u4 *)o = u4{c[0], c[1], c[2], c[3]};
-      *(u2 *)(o + 1024) = u2{c[4], c[5]};
-      s[0] = (uint8_t)Eu;                    // byte 1 is the partner block's
-      *(uint16_t *)(s + 2) = 0;
-    } else {
-      *(u2 *)(o + 1024 + 8) = u2{c[0], c[1]};
-      *(u4 *)(o + 2048) = u4{c[2], c[3], c[4], c[5]};
-      s[1] = (uint8_t)Eu;
-    }
-  } else if (seg == 1) {
-    const int st = og.s4 + (idx >> 1), h = idx & 1;
-    uint8_t *o = op + st * kActStep + h * 512;
-    Blk hd, ld;                                // q = 8 h + l
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      hd.e[i] = floorf(v.e[i] * 0.125f);
-      hd.o[i] = floorf(v.o[i] * 0.125f);
-      ld.e[i] = fmaf(hd.e[i], -8.f, v.e[i]);
-      ld.o[i] = fmaf(hd.o[i], -8.f, v.o[i]);
-    }
-    const v6u ch = to_e3m2(hd, 2.f);
-    const v6u cl = to_e3m2(ld, 16.f);
-    *(u4 *)o = u4{ch[0], ch[1], ch[2], ch[3]};
-    *(u4 *)(o + 1024) = u4{ch[4], ch[5], cl[0], cl[1]};
-    *(u4 *)(o + 2048) = u4{cl[2], cl[3], cl[4], cl[5]};
-    *(uint32_t *)(sc + st * kActScaleStep + h * 128) = Eu;
+    const int l = 16 * pos + r;
+    const v6u c = to_e3m2(v, 1.f);
+    *(u2 *)(stp + 24 * l) = u2{c[0], c[1]};
+    *(u2 *)(stp + 24 * l + 8) = u2{c[2], c[3]};
+    *(u2 *)(stp + 24 * l + 16) = u2{c[4], c[5]};
+    scw[4 * l] = (uint8_t)Eu;
   } else {
-    const int st = og.s4 + og.s6 + idx;
-    Blk hd, ld;                                // q = 16 h + l
+    Blk hd, ld;
+    const float f = s == 2 ? 0.125f : 0.0625f, base = s == 2 ? 8.f : 16.f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      hd.e[i] = floorf(v.e[i] * 0.0625f);
-      hd.o[i] = floorf(v.o[i] * 0.0625f);
-      ld.e[i] = fmaf(hd.e[i], -16.f, v.e[i]);
-      ld.o[i] = fmaf(hd.o[i], -16.f, v.o[i]);
+      hd.e[i] = floorf(v.e[i] * f);
+      hd.o[i] = floorf(v.o[i] * f);
+      ld.e[i] = fmaf(hd.e[i], -base, v.e[i]);
+      ld.o[i] = fmaf(hd.o[i], -base, v.o[i]);
     }
+    if (s == 2) {
+      // lane groups 2 pos (high plane h/2) and 2 pos + 1 (low plane l/16)
+      const int lh = 16 * (2 * pos) + r, ll = lh + 16;
+      const v6u ch = to_e3m2(hd, 2.f), cl = to_e3m2(ld, 16.f);
+      *(u2 *)(stp + 24 * lh) = u2{ch[0], ch[1]};
+      *(u2 *)(stp + 24 * lh + 8) = u2{ch[2], ch[3]};
+      *(u2 *)(stp + 24 * lh + 16) = u2{ch[4], ch[5]};
+      *(u2 *)(stp + 24 * ll) = u2{cl[0], cl[1]};
+      *(u2 *)(stp + 24 * ll + 8) = u2{cl[2], cl[3]};
+      *(u2 *)(stp + 24 * ll + 16) = u2{cl[4], cl[5]};
+    } else {
+      // E4M3 2h and l/8; lane group 2 plane + half holds elements
+      // 16 half..16 half + 15 of the plane, at byte 16 pos
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      uint8_t *o = op + st * kActStep + h * 512;
-      *(u4 *)o = to_e4m3(hd, h, 4.f);
-      *(u4 *)(o + 1024) = to_e4m3(ld, h, 64.f);
-      *(u4 *)(o + 2048) = u4{0u, 0u, 0u, 0u};
-      *(uint32_t *)(sc + st * kActScaleStep + h * 128) = Eu;
+      for (int e = 0; e < 2; ++e) {
+        *(u4 *)(stp + 32 * (16 * e + r) + 16 * pos) = to_e4m3(hd, e, 0.5f);
+        *(u4 *)(stp + 32 * (16 * (2 + e) + r) + 16 * pos) = to_e4m3(ld, e, 8.f);
+      }
+    }
+    scw[4 * (16 * (2 * pos) + r)] = (uint8_t)Eu;
+    scw[4 * (16 * (2 * pos + 1) + r)] = (uint8_t)Eu;
+  }
+  // the unused scale bytes of a segment's short last group
+  if (rem == 0) {
+    const int S = lg.S[s];
+    for (int k = S; k < (S + kGroupSteps - 1) / kGroupSteps * kGroupSteps; ++k) {
+      uint8_t *z = q.img_exp + (row >> 4) * q.a_tile_sc +
+                   (int64_t)(lg.G0[s] + k / kGroupSteps) * 256 + k % kGroupSteps;
+      for (int g = 0; g < 4; ++g) z[4 * (16 * g + r)] = 0;
     }
   }
 }
@@ -342,7 +329,7 @@ __device__ inline u4 swiglu8(u4 g, u4 u) {
 // in order, then the blocks in order), r = float32(1 / sqrt(ms + eps)),
 // then y = bf16(g * bf16(x * r)) with float32 products.
 __device__ void rms_normalise(const QuantArgs &q, uint8_t *smem, int R, int rowB, int t,
-                              int nthr) {
+                              int nthr, int64_t r0) {
   const int K = (int)q.K, nbk = K / kBlock;
   double *part = (double *)(smem + R * rowB);
   float *rr = (float *)(part + R * nbk);
@@ -377,7 +364,9 @@ __device__ void rms_normalise(const QuantArgs &q, uint8_t *smem, int R, int rowB
       for (int u = 0; u < 16; ++u) acc += v[u];
     }
     for (; b < nbk; ++b) acc += pp[b];
-    rr[t] = (float)(1.0 / sqrt(acc / (double)K + (double)q.eps));
+    // the zero rows past the input (operand-image padding) stay zero, also
+    // with eps = 0
+    rr[t] = r0 + t < q.src_rows ? (float)(1.0 / sqrt(acc / (double)K + (double)q.eps)) : 0.f;
   }
   __syncthreads();
   const int cpr = K / 8;                                 // 8-element chunks per row
@@ -409,9 +398,9 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
   const int rowB = 2 * (K + kRowPad);                // staged row stride (bytes)
   const int lgR = q.lg_rows;
   const int R = 1 << lgR;
-  const OpGeo og(q.n4, q.n6, q.n8);
-  // padded blocks per row (the decode image pads the 8-bit blocks to pairs)
-  const int nbp = og.n4p + og.n6p + og.n8 + (q.dimg ? (og.n8 & 1) : 0);
+  const LGeo lg(q.n3, q.n4, q.n6, q.n8);
+  int nbp = 0;                                       // padded blocks per row
+  for (int s = 0; s < kSegs; ++s) nbp += lg.S[s] * (s < 2 ? 4 : 2);
   // XCD-aware order: consecutive row groups (whole 32-row operand tiles)
   // stay on one XCD, so its L2 completes every line of the tile.
   int64_t w = blockIdx.x;
@@ -467,30 +456,36 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
   }
   if (t < R) *(u4 *)(smem + t * rowB + 2 * K) = u4{0u, 0u, 0u, 0u};
   __syncthreads();
-  if (q.rmsnorm) rms_normalise(q, smem, R, rowB, t, nthr);
+  if (q.rmsnorm) rms_normalise(q, smem, R, rowB, t, nthr, r0);
 
   for (int it = t; it < (nbp << lgR); it += nthr) {
     const int bp = it >> lgR;
     const int lr = it & (R - 1);
     const int64_t row = r0 + lr;
     if (row < q.out_rows)
-      quantize_item<RNA>(q, og, bp, row, smem + lr * rowB);
+      quantize_item<RNA>(q, lg, bp, row, smem + lr * rowB);
   }
   // zero the padding of the packed and exponent rows
-  if (t < R) {
+  if (q.write_rows && t < R) {
     const int64_t row = r0 + t;
-    if (row < q.out_rows) {
+    if (row < q.src_rows) {
       for (int64_t z = q.row_used; z < q.canon_rb; ++z) q.mant[row * q.out_rb + z] = 0;
-      for (int64_t z = og.n4 + og.n6 + og.n8; z < q.canon_erb; ++z)
+      for (int64_t z = q.n4 + q.n6 + q.n8; z < q.canon_erb; ++z)
         q.exp[row * q.out_erb + z] = 0;
     }
   }
 }
 
-int padded_blocks(int n4, int n6, int n8) {
-  const OpGeo og(n4, n6, n8);
-  return og.n4p + og.n6p + og.n8 + (og.n8 & 1);
+}  // namespace
+
+int quantize_act_padded_blocks(int n3, int n4, int n6, int n8) {
+  const LGeo lg(n3, n4, n6, n8);
+  int nbp = 0;
+  for (int s = 0; s < kSegs; ++s) nbp += lg.S[s] * (s < 2 ? 4 : 2);
+  return nbp;
 }
+
+namespace {
 
 }  // namespace
 
@@ -515,7 +510,7 @@ int64_t quantize_act_lds(int64_t K, int nbp, bool perm, bool rmsnorm) {
 hipError_t launch_quantize_act(const QuantArgs &args, hipStream_t stream) {
   QuantArgs a = args;
   const bool perm = a.perm != nullptr;
-  const int nbp = padded_blocks(a.n4, a.n6, a.n8);
+  const int nbp = quantize_act_padded_blocks(a.n3, a.n4, a.n6, a.n8);
   const int R = quantize_act_rows(a.K, nbp, perm, a.rmsnorm != 0);
   int lg = 0;
   while ((1 << lg) < R) ++lg;

@@ -1,7 +1,7 @@
-// unpack.hip -- debug decode of packed MXINT mantissas back to canonical
-// int8 values in permuted order, plus the exponents.  Used for parity
-// checks of the packed activation rows and the weight slabs; not on the hot
-// path.
+// unpack.hip -- debug decode of the stored mantissas back to int8 values in
+// permuted order, plus the exponents: the canonical packed activation rows,
+// and the weight layout of the GEMMs.  Used for parity checks; not on the
+// hot path.
 #include "mxq_device.h"
 #include "mxq_internal.h"
 
@@ -19,19 +19,18 @@ __global__ __launch_bounds__(kThreads) void unpack_kernel(UnpackArgs a) {
   if (f >= a.rows * nb) return;
   const int64_t row = f / nb;
   const int b = (int)(f - row * nb);
-  const Segs s{a.n4, a.n6, a.n8};
-  const BlockInfo bi = block_info(s, b);
   int8_t *out = a.q + row * a.K + (int64_t)b * kBlock;
   if (!WEIGHTS) {
+    const Segs s{a.n4, a.n6, a.n8, a.n3};
+    const BlockInfo bi = block_info(s, b);
     const uint8_t *p = a.mant + row * a.a_rb;
     for (int t = 0; t < kBlock; ++t) out[t] = (int8_t)act_elem(p, bi, t);
+    a.e[row * nb + b] = a.exp[row * a.a_erb + b];
   } else {
-    const DGeo dg(a.n4, a.n6, a.n8);
-    const uint8_t *slab = a.mant + (row >> 4) * wd_slab_bytes(dg);
-    for (int t = 0; t < kBlock; ++t)
-      out[t] = (int8_t)wstream_elem(slab, dg, bi, (int)(row & 15), t, a.sm != 0);
+    const LGeo lg(a.n3, a.n4, a.n6, a.n8);
+    for (int t = 0; t < kBlock; ++t) out[t] = (int8_t)w_elem(a.mant, lg, a.full != 0, row, b, t);
+    a.e[row * nb + b] = (uint8_t)w_exp_of(a.exp, lg, row, b);
   }
-  a.e[row * nb + b] = a.exp[row * a.a_erb + b];
 }
 
 }  // namespace

@@ -51,12 +51,13 @@ class LayerSequence:
             mxq.gemm(self.a_mant, self.a_exp, lin.w_mant, lin.w_exp, lin.fmt,
                      self.M, lin.N, out=y)
         if self.kv_out is None:
-            self.kv_out = [(torch.empty(self.kv_fmt.act_bytes(t.shape[0]), dtype=torch.uint8,
-                                        device=t.device),
-                            torch.empty(self.kv_fmt.act_exp_bytes(t.shape[0]),
-                                        dtype=torch.uint8, device=t.device)) for t in kv]
+            rb, erb = self.kv_fmt.act_packed_bytes(), self.kv_fmt.exp_row_bytes()
+            self.kv_out = [(torch.empty((t.shape[0], rb), dtype=torch.uint8, device=t.device),
+                            torch.empty((t.shape[0], erb), dtype=torch.uint8, device=t.device))
+                           for t in kv]
+        # the caches as packed rows, the layout attention reads
         for t, out in zip(kv, self.kv_out):
-            mxq.quantize_act(t, self.kv_fmt, out=out)
+            mxq.quantize_rows(t, self.kv_fmt, out=out)
         return self.ys, self.kv_out
 
     def ops(self) -> float:

@@ -43,6 +43,7 @@ _SIGS = {
     "mxq_weight_bytes": (_I64, [_P, _I64]),
     "mxq_weight_exp_bytes": (_I64, [_P, _I64]),
     "mxq_quantize_act": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P]),
+    "mxq_quantize_rows": (ctypes.c_int, [_P, _P, _I64, _I64, _P, _P, _P]),
     "mxq_quantize_act_rmsnorm": (ctypes.c_int, [_P, _P, _I64, _I64, _P, ctypes.c_float,
                                                  _P, _P, _P]),
     "mxq_quantize_act_swiglu": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _P, _P, _P]),
@@ -108,8 +109,8 @@ def _ptr(t):
 class Format:
     """Width map + permutation of one quantized linear (include/mxq.h mxq_fmt).
 
-    widths: K/32 entries in {3, 4, 6, 8}, non-decreasing (3-bit blocks, the
-            3-6-8 template, are stored as 4-bit blocks holding 2q).
+    widths: K/32 entries in {3, 4, 6, 8}, non-decreasing (3-bit blocks are
+            the floor of the 3-6-8 template).
     perm:   None (identity) or an int32 device tensor of K source columns.
     """
 
@@ -145,11 +146,11 @@ class Format:
         return _size(lib().mxq_exp_row_bytes(self.ref), "mxq_exp_row_bytes")
 
     def act_bytes(self, M: int) -> int:
-        """Activation buffer: M packed rows, then the operand image."""
+        """The activation operand image of M rows (mxq_quantize_act)."""
         return _size(lib().mxq_act_bytes(self.ref, M), "mxq_act_bytes")
 
     def act_exp_bytes(self, M: int) -> int:
-        """Exponent buffer: M exponent rows, then the operand scale bytes."""
+        """Its scale bytes."""
         return _size(lib().mxq_act_exp_bytes(self.ref, M), "mxq_act_exp_bytes")
 
     def weight_bytes(self, N: int) -> int:
@@ -247,16 +248,23 @@ def quantize_act_swiglu(gate, up, fmt: Format, out=None):
     return mant, exp
 
 
-def packed_rows(mant, fmt: Format, M: int):
-    """View of the packed activation rows [M, act_packed_bytes]."""
-    n = fmt.act_packed_bytes()
-    return mant[:M * n].view(M, n)
-
-
-def exp_rows(exp, fmt: Format, M: int):
-    """View of the activation block exponents [M, exp_row_bytes]."""
-    n = fmt.exp_row_bytes()
-    return exp[:M * n].view(M, n)
+def quantize_rows(a, fmt: Format, out=None):
+    """The quantizer writing packed rows: bf16 [M, >=K] -> (rows uint8
+    [M, act_packed_bytes], exps uint8 [M, exp_row_bytes]) -- the KV-cache
+    layout, and the input of unpack_act and gemm_partials."""
+    _bf16_2d(a, fmt.K, "activations")
+    M = a.shape[0]
+    rb, erb = fmt.act_packed_bytes(), fmt.exp_row_bytes()
+    if out is None:
+        rows = torch.empty((M, rb), dtype=torch.uint8, device=a.device)
+        exps = torch.empty((M, erb), dtype=torch.uint8, device=a.device)
+    else:
+        rows, exps = out
+        _dev_bytes(rows, M * rb, "packed row buffer", a.device)
+        _dev_bytes(exps, M * erb, "exponent row buffer", a.device)
+    _check(lib().mxq_quantize_rows(fmt.ref, _ptr(a), M, a.stride(0), _ptr(rows),
+                                   _ptr(exps), _stream()), "mxq_quantize_rows")
+    return rows, exps
 
 
 def pack_weights(w, fmt: Format):
@@ -286,9 +294,17 @@ def gemm(a_mant, a_exp, w_mant, w_exp, fmt: Format, M: int, N: int, out=None):
     return out
 
 
-def gemm_partials(a_mant, a_exp, w_mant, w_exp, fmt: Format, M: int, N: int):
-    """Exact per-block int32 sums P[M, N, K/32] (debug / parity)."""
-    dev = _gemm_operands(a_mant, a_exp, w_mant, w_exp, fmt, M, N)
+def gemm_partials(rows, exps, w_mant, w_exp, fmt: Format, M: int, N: int):
+    """Exact per-block int32 sums P[M, N, K/32] (debug / parity) from packed
+    rows (quantize_rows) and the packed weights."""
+    if M < 0 or N < 0:
+        raise MxqError("M and N must be non-negative")
+    dev = rows.device if isinstance(rows, torch.Tensor) else None
+    _dev_bytes(rows, M * fmt.act_packed_bytes(), "rows", dev)
+    _dev_bytes(exps, M * fmt.exp_row_bytes(), "exps", dev)
+    _dev_bytes(w_mant, fmt.weight_bytes(N), "w_mant", dev)
+    _dev_bytes(w_exp, fmt.weight_exp_bytes(N), "w_exp", dev)
+    a_mant, a_exp = rows, exps
     p = torch.empty((M, N, fmt.nb), dtype=torch.int32, device=dev)
     _check(lib().mxq_gemm_partials(fmt.ref, M, N, _ptr(a_mant), _ptr(a_exp),
                                    _ptr(w_mant), _ptr(w_exp), _ptr(p), _stream()),
@@ -297,8 +313,10 @@ def gemm_partials(a_mant, a_exp, w_mant, w_exp, fmt: Format, M: int, N: int):
 
 
 def unpack_act(mant, exp, fmt: Format, rows: int):
-    _dev_bytes(mant, fmt.act_bytes(rows), "a_mant")
-    _dev_bytes(exp, fmt.act_exp_bytes(rows), "a_exp", mant.device)
+    """Packed rows and exponent rows (quantize_rows) -> (q int8 [rows, K],
+    e uint8 [rows, K/32])."""
+    _dev_bytes(mant, rows * fmt.act_packed_bytes(), "rows")
+    _dev_bytes(exp, rows * fmt.exp_row_bytes(), "exps", mant.device)
     q = torch.empty((rows, fmt.K), dtype=torch.int8, device=mant.device)
     e = torch.empty((rows, fmt.nb), dtype=torch.uint8, device=mant.device)
     _check(lib().mxq_unpack_act(fmt.ref, rows, _ptr(mant), _ptr(exp), _ptr(q), _ptr(e),
@@ -430,8 +448,8 @@ def attn_work_bytes(fmt: Format, B: int, Hq: int, Hkv: int, T: int) -> int:
 def attn_decode(q, k_cache, v_cache, fmt: Format, B: int, Hq: int, Hkv: int, T: int,
                 scale: float, out=None, work=None):
     """Decode attention over an MXINT KV cache.  q: bf16 [B, Hq, 128] on the
-    device; k_cache, v_cache: (mant, exp) as returned by quantize_act for the
-    B * T * Hkv cache rows (row (b * T + t) * Hkv + h).  Returns float32
+    device; k_cache, v_cache: (rows, exps) as returned by quantize_rows for
+    the B * T * Hkv cache rows (row (b * T + t) * Hkv + h).  Returns float32
     [B, Hq, 128] on the current stream."""
     if not (isinstance(q, torch.Tensor) and q.is_cuda and q.dtype == torch.bfloat16
             and q.is_contiguous() and q.numel() == B * Hq * 128):
@@ -450,7 +468,6 @@ def attn_decode(q, k_cache, v_cache, fmt: Format, B: int, Hq: int, Hkv: int, T: 
                                  _ptr(v_cache[1]), _ptr(out), _ptr(work), work.numel(),
                                  _stream()), "mxq_attn_decode")
     return out
-
 
 
 ATTN_STATIC_WORK_BYTES = 8 << 20

@@ -1,369 +1,357 @@
-"""Host-side decoder of the matrix-core operand images (test infrastructure).
+"""Host-side decoders of the GEMM buffers (test infrastructure).
 
-Written from the layout that include/mxq.h documents, independently of the
-HIP sources: FP6 e3m2 and FP8 e4m3 codes are decoded from the OCP
-microscaling element definitions, and every mantissa is rebuilt from its
-digits, so a test can compare the images element by element with the
-oracle's mantissas and exponents.
+Written from the layouts that include/mxq.h states, independently of the HIP
+sources: the FP6 (e3m2, e2m3) and FP8 (e4m3) codes are decoded from the OCP
+microscaling element definitions, the folded weight words are unfolded by
+evaluating the header's fold formulas on single payload bits (so a fold that
+loses or merges a bit is detected, not assumed away), and every mantissa is
+rebuilt from its digits.  A test can then compare the buffers element by
+element with the oracle's mantissas and exponents.
 """
 from __future__ import annotations
 
 import numpy as np
 
 BLOCK = 32
-CHUNK = 13312          # bytes per step of a 128-column weight tile
-PART = 4096
-TILE_COLS = 128
+LANES = 64
+GROUP_STEPS = 4
+TILE_ROWS = 16
+SUPER_COLS = 128
+SLABS = 8
 
 
-def _e3m2_table():
-    t = np.zeros(64)
-    for c in range(64):
-        s, e, m = c >> 5, (c >> 2) & 7, c & 3
-        v = m / 4 * 2.0 ** -2 if e == 0 else (1 + m / 4) * 2.0 ** (e - 3)
-        t[c] = -v if s else v
-    return t
-
-
-def _e4m3_table():
-    t = np.zeros(256)
-    for c in range(256):
-        s, e, m = c >> 7, (c >> 3) & 15, c & 7
-        if e == 15 and m == 7:
+def _fp_table(ebits, mbits, bias, nan_code=None):
+    n = 1 << (1 + ebits + mbits)
+    t = np.zeros(n)
+    for c in range(n):
+        s, e, m = c >> (ebits + mbits), (c >> mbits) & ((1 << ebits) - 1), c & ((1 << mbits) - 1)
+        if nan_code is not None and (c & (n // 2 - 1)) == nan_code:
             t[c] = np.nan
             continue
-        v = m / 8 * 2.0 ** -6 if e == 0 else (1 + m / 8) * 2.0 ** (e - 7)
+        if e == 0:
+            v = m / (1 << mbits) * 2.0 ** (1 - bias)
+        else:
+            v = (1 + m / (1 << mbits)) * 2.0 ** (e - bias)
         t[c] = -v if s else v
     return t
 
 
-E3M2 = _e3m2_table()
-E4M3 = _e4m3_table()
+E3M2 = _fp_table(3, 2, 3)
+E2M3 = _fp_table(2, 3, 1)
+E4M3 = _fp_table(4, 3, 7, nan_code=0x7F)
 
 
-def fp6_values(b24: np.ndarray) -> np.ndarray:
-    """[..., 24] bytes -> [..., 32] decoded e3m2 values (element e at bits 6e)."""
-    bits = np.unpackbits(b24.astype(np.uint8), axis=-1, bitorder="little")
+def fp6_codes(b: np.ndarray) -> np.ndarray:
+    """[..., 24] bytes -> [..., 32] 6-bit codes (element t at bits 6t)."""
+    bits = np.unpackbits(np.ascontiguousarray(b, np.uint8), axis=-1, bitorder="little")
     bits = bits.reshape(bits.shape[:-1] + (32, 6)).astype(np.int64)
-    codes = (bits << np.arange(6)).sum(axis=-1)
-    return E3M2[codes]
+    return (bits << np.arange(6)).sum(axis=-1)
 
 
-def fp8_values(b: np.ndarray) -> np.ndarray:
-    return E4M3[b.astype(np.int64)]
+def _int_of(v, what):
+    r = np.rint(v)
+    assert np.all(np.isfinite(v)) and np.all(r == v), "%s: digit is not an integer" % what
+    return r.astype(np.int64)
 
 
 class Geo:
+    """Segments, steps and scale groups of a width map (header: "Steps and
+    lanes")."""
+
     def __init__(self, widths):
         w = np.asarray(widths)
-        self.n4, self.n6, self.n8 = (int((w == m).sum()) for m in (4, 6, 8))
-        self.n4p = -(-self.n4 // 4) * 4
-        self.n6p = -(-self.n6 // 2) * 2
-        self.s4, self.s6, self.s8 = self.n4p // 4, self.n6p // 2, self.n8
-        self.nsteps = self.s4 + self.s6 + self.s8
+        self.nb_total = len(w)
+        self.nb = [int((w == m).sum()) for m in (3, 4, 6, 8)]
+        self.per = [4, 4, 2, 2]
+        self.S = [-(-n // p) for n, p in zip(self.nb, self.per)]
+        self.b0 = list(np.cumsum([0] + self.nb[:3]))
+        self.st0 = list(np.cumsum([0] + self.S[:3]))
+        groups = [-(-S // GROUP_STEPS) for S in self.S]
+        self.G0 = list(np.cumsum([0] + groups[:3]))
+        self.ngroups = int(sum(groups))
+        self.nsteps = int(sum(self.S))
 
-    def blocks_of_step(self, st):
-        """[(block index or None for padding, half, position)] of step st.
-        position: 4-bit pair j (0/1); 6-bit and 8-bit 0."""
-        out = []
-        if st < self.s4:
-            for h in (0, 1):
-                for j in (0, 1):
-                    b = 4 * st + 2 * j + h
-                    out.append((b if b < self.n4 else None, h, j))
-        elif st < self.s4 + self.s6:
-            p = st - self.s4
-            for h in (0, 1):
-                i = 2 * p + h
-                out.append((self.n4 + i if i < self.n6 else None, h, 0))
-        else:
-            out.append((self.n4 + self.n6 + st - self.s4 - self.s6, None, 0))
-        return out
+    def steps(self):
+        """(segment, global step, step within the segment)."""
+        for seg in range(4):
+            for sl in range(self.S[seg]):
+                yield seg, self.st0[seg] + sl, sl
 
+    def block(self, seg, sl, j):
+        """Global block index of block j of step sl of a segment, or None
+        for a zero block."""
+        i = self.per[seg] * sl + j
+        return self.b0[seg] + i if i < self.nb[seg] else None
 
-def _decode_lane_block(lane, kind, j=0):
-    """q of one 4- or 6-bit block from a lane half's 48 bytes."""
-    if kind == 4:
-        return fp6_values(lane[..., 24 * j:24 * j + 24]) * 4
-    return (fp6_values(lane[..., 0:24]) + fp6_values(lane[..., 24:48])) * 16
+    def group_byte(self, seg, sl):
+        return self.G0[seg] + sl // GROUP_STEPS, sl % GROUP_STEPS
 
 
-def _decode_steps(geo, nb, rows, lane_of, scale_of, weights):
-    """Rebuild q [rows, K] and E [rows, nb] from per-step lane data
-    lane_of(st, h) -> [rows, 48] and scale_of(st, h) -> [rows, >=2]."""
-    q = np.zeros((rows, nb * BLOCK))
-    E = np.full((rows, nb), -1, dtype=np.int64)
-    ok = True
-    for st in range(geo.nsteps):
-        lanes = [lane_of(st, h) for h in (0, 1)]
-        scs = [scale_of(st, h) for h in (0, 1)]
-        for (b, h, j) in geo.blocks_of_step(st):
-            if st < geo.s4 + geo.s6:
-                kind = 4 if st < geo.s4 else 6
-                scale = scs[h][:, j].astype(np.int64)
+# --------------------------------------------------------------------------
+# (A) the activation operand image
+# --------------------------------------------------------------------------
+
+def act_lane_bytes(seg):
+    return 32 if seg == 3 else 24
+
+
+def act_tile_bytes(g: Geo):
+    return sum(g.S[s] * LANES * act_lane_bytes(s) for s in range(4))
+
+
+def decode_act(img: np.ndarray, sc: np.ndarray, widths, M: int):
+    """Activation image -> (q [M, K], E [M, nb], pad_ok): mantissas rebuilt
+    from their digits, exponents from the lanes' scale bytes; pad_ok is True
+    when rows past M, zero blocks and unused scale bytes are all zero."""
+    g = Geo(widths)
+    K = g.nb_total * BLOCK
+    tiles = -(-M // TILE_ROWS)
+    Mp = tiles * TILE_ROWS
+    tb, tsc = act_tile_bytes(g), g.ngroups * LANES * 4
+    assert img.size == tiles * tb and sc.size == tiles * tsc, "image sizes"
+    img = img.reshape(tiles, tb)
+    sc = sc.reshape(tiles, g.ngroups, LANES, 4)
+    q = np.zeros((Mp, K), np.int64)
+    E = np.zeros((Mp, g.nb_total), np.int64)
+    pad_ok = True
+    used = np.zeros(sc.shape, bool)
+    off = 0
+    for seg, st, sl in g.steps():
+        L = act_lane_bytes(seg)
+        lanes = img[:, off:off + LANES * L].reshape(tiles, 4, 16, L)   # [tile, g, r, bytes]
+        off += LANES * L
+        G, k = g.group_byte(seg, sl)
+        sbytes = sc[:, G, :, k].reshape(tiles, 4, 16).astype(np.int64)
+        used[:, G, :, k] = True
+        rows = (np.arange(tiles)[:, None] * TILE_ROWS + np.arange(16)[None, :]).reshape(-1)
+        if seg <= 1:
+            v = E3M2[fp6_codes(lanes)]                        # [tile, g, r, 32]
+            for j in range(4):
+                b = g.block(seg, sl, j)
+                vals = v[:, j].reshape(-1, 32)
+                e = sbytes[:, j].reshape(-1)
                 if b is None:
-                    part = lanes[h][:, 24 * j:24 * j + 24] if kind == 4 else lanes[h]
-                    ok &= not part.any() and not scale.any()
-                    if kind == 6:
-                        ok &= not scs[h][:, 1].any()
+                    pad_ok &= not vals.any() and not e.any()
                     continue
-                q[:, BLOCK * b:BLOCK * b + BLOCK] = _decode_lane_block(lanes[h], kind, j)
-                E[:, b] = scale
-                if kind == 6:
-                    ok &= not scs[h][:, 1].any()
+                qq = _int_of(vals / 2 if seg == 0 else vals, "3/4-bit activation")
+                q[rows, b * BLOCK:(b + 1) * BLOCK] = qq
+                E[rows, b] = e
+        elif seg == 2:
+            v = E3M2[fp6_codes(lanes)]
+            for j in range(2):
+                b = g.block(seg, sl, j)
+                vh = v[:, 2 * j].reshape(-1, 32)
+                vl = v[:, 2 * j + 1].reshape(-1, 32)
+                eh = sbytes[:, 2 * j].reshape(-1)
+                el = sbytes[:, 2 * j + 1].reshape(-1)
+                if b is None:
+                    pad_ok &= not vh.any() and not vl.any() and not eh.any() and not el.any()
+                    continue
+                h = _int_of(2 * vh, "6-bit high digit")
+                l = _int_of(16 * vl, "6-bit low digit")
+                assert np.all((l >= 0) & (l <= 7)), "6-bit low digit out of range"
+                q[rows, b * BLOCK:(b + 1) * BLOCK] = 8 * h + l
+                assert np.array_equal(eh, el), "6-bit scale bytes of the two planes differ"
+                E[rows, b] = eh
+        else:
+            for j in range(2):
+                b = g.block(seg, sl, j)
+                hi = np.concatenate([lanes[:, e, :, 16 * j:16 * j + 16] for e in (0, 1)], axis=-1)
+                lo = np.concatenate([lanes[:, 2 + e, :, 16 * j:16 * j + 16] for e in (0, 1)],
+                                    axis=-1)
+                vh = E4M3[hi.reshape(-1, 32).astype(np.int64)]
+                vl = E4M3[lo.reshape(-1, 32).astype(np.int64)]
+                eh = sbytes[:, 2 * j].reshape(-1)
+                el = sbytes[:, 2 * j + 1].reshape(-1)
+                if b is None:
+                    pad_ok &= not hi.any() and not lo.any() and not eh.any() and not el.any()
+                    continue
+                h = _int_of(vh / 2, "8-bit high digit")
+                l = _int_of(8 * vl, "8-bit low digit")
+                assert np.all((l >= 0) & (l <= 15)), "8-bit low digit out of range"
+                q[rows, b * BLOCK:(b + 1) * BLOCK] = 16 * h + l
+                assert np.array_equal(eh, el), "8-bit scale bytes of the two planes differ"
+                E[rows, b] = eh
+    assert off == tb
+    pad_ok &= not q[M:].any() and not E[M:].any()
+    pad_ok &= not sc[~used].any()
+    return q[:M], E[:M], bool(pad_ok)
+
+
+# --------------------------------------------------------------------------
+# (B) the weights
+# --------------------------------------------------------------------------
+
+M32 = 0xFFFFFFFF
+F4Z0, F4Z2 = 0x18618618, 0x61861861
+
+
+def fold4(d):
+    return [d[0] | (d[1] & F4Z0), d[2] | (d[1] & F4Z2),
+            d[3] | (d[4] & F4Z0), d[5] | (d[4] & F4Z2)]
+
+
+def fold3(d):
+    return [d[0] | (d[1] >> 1), d[3] | (d[4] >> 1),
+            (d[2] | (d[5] << 3) | (d[5] >> 31)) & M32]
+
+
+def fold2(d):
+    return [d[0] | d[1] | d[2], d[3] | d[4] | d[5]]
+
+
+def _payload_bits(field_bits):
+    """Bit positions (of the 192-bit word sequence D0..D5) that a code with
+    the given set bits per 6-bit field may use."""
+    return [6 * t + f for t in range(32) for f in field_bits]
+
+
+def _fold_map(fold, field_bits):
+    """Evaluate a fold on each payload bit alone: the stored bit it lands on.
+    Fails if a payload bit is lost, lands on two bits, or two payload bits
+    share one stored bit."""
+    mp = {}
+    for p in _payload_bits(field_bits):
+        d = [0] * 6
+        d[p // 32] = 1 << (p % 32)
+        out = fold(d)
+        hits = [(w, b) for w, x in enumerate(out) for b in range(32) if (x >> b) & 1]
+        assert len(hits) == 1, "fold loses or duplicates payload bit %d" % p
+        mp[p] = hits[0][0] * 32 + hits[0][1]
+    assert len(set(mp.values())) == len(mp), "fold merges payload bits"
+    return mp
+
+
+# payload of the symmetric-clamp codes: s|k with k <= 7 (4-bit) or k <= 3
+# (3-bit, e2m3 s|k: k in the mantissa bits), and the sign-free 2-bit high
+# digits of 6-bit blocks
+_MAP4 = _fold_map(fold4, (0, 1, 2, 5))
+_MAP3 = _fold_map(fold3, (0, 1, 5))
+_MAP2 = _fold_map(fold2, (0, 1))
+
+
+def _unfold(words: np.ndarray, mp) -> np.ndarray:
+    """[..., n] uint32 stored words -> [..., 32] 6-bit codes."""
+    words = words.astype(np.uint64)
+    codes = np.zeros(words.shape[:-1] + (32,), np.int64)
+    for p, s in mp.items():
+        bit = (words[..., s // 32] >> np.uint64(s % 32)) & np.uint64(1)
+        codes[..., p // 6] |= bit.astype(np.int64) << (p % 6)
+    return codes
+
+
+def _raw_codes(words: np.ndarray) -> np.ndarray:
+    b = words.astype("<u4").view(np.uint8).reshape(words.shape[:-1] + (24,))
+    return fp6_codes(b)
+
+
+def w_chunk_bytes(seg, full):
+    return [(768, 1024), (1024, 1536), (768, 1024), (1024, 1024)][seg][int(full)]
+
+
+def w_super_bytes(g: Geo, full):
+    return sum(g.S[s] * SLABS * w_chunk_bytes(s, full) for s in range(4))
+
+
+def _words(b: np.ndarray) -> np.ndarray:
+    return np.ascontiguousarray(b).view("<u4")
+
+
+def decode_weights(wm: np.ndarray, we: np.ndarray, widths, N: int, full: bool):
+    """Weight buffers -> (q [Np, K], E [Np, nb], ok) for Np = N rounded up to
+    128; ok is False if a layout rule is broken (a zero block or padding
+    column that is not zero, a code outside its documented range, unused
+    scale bytes that are not zero)."""
+    g = Geo(widths)
+    K = g.nb_total * BLOCK
+    sup = -(-N // SUPER_COLS)
+    Np = sup * SUPER_COLS
+    sb, ssc = w_super_bytes(g, full), g.ngroups * 2048
+    assert wm.size == sup * sb and we.size == sup * ssc, "weight buffer sizes"
+    wm = wm.reshape(sup, sb)
+    sc = we.reshape(sup, g.ngroups, LANES, GROUP_STEPS, SLABS)     # [.., lane, k, slab]
+    q = np.zeros((Np, K), np.int64)
+    E = np.zeros((Np, g.nb_total), np.int64)
+    ok = True
+    used = np.zeros(sc.shape, bool)
+    off = 0
+    cols = (np.arange(sup)[:, None, None] * SUPER_COLS + 16 * np.arange(SLABS)[None, :, None]
+            + np.arange(16)[None, None, :])                          # [sup, slab, c]
+    for seg, st, sl in g.steps():
+        C = w_chunk_bytes(seg, full)
+        ch = wm[:, off:off + SLABS * C].reshape(sup, SLABS, C)
+        off += SLABS * C
+        G, k = g.group_byte(seg, sl)
+        sbytes = sc[:, G, :, k, :].astype(np.int64)                   # [sup, lane, slab]
+        used[:, G, :, k, :] = True
+        if seg <= 1:
+            if seg == 0 and not full:
+                xy = _words(ch[:, :, :512]).reshape(sup, SLABS, LANES, 2)
+                z = _words(ch[:, :, 512:768]).reshape(sup, SLABS, LANES, 1)
+                codes = _unfold(np.concatenate([xy, z], axis=-1), _MAP3)
+            elif seg == 1 and full:
+                a = _words(ch[:, :, :1024]).reshape(sup, SLABS, LANES, 4)
+                b = _words(ch[:, :, 1024:1536]).reshape(sup, SLABS, LANES, 2)
+                codes = _raw_codes(np.concatenate([a, b], axis=-1))
             else:
-                vals = []
-                for hf in (0, 1):
-                    ln = lanes[hf]
-                    if weights:
-                        ok &= bool(np.array_equal(ln[:, :16], ln[:, 32:48]))
-                    else:
-                        ok &= not ln[:, 32:48].any()
-                    vals.append((fp8_values(ln[:, :16]) + fp8_values(ln[:, 16:32])) * 64)
-                q[:, BLOCK * b:BLOCK * b + BLOCK] = np.concatenate(vals, axis=1)
-                ok &= bool(np.array_equal(scs[0][:, 0], scs[1][:, 0]))
-                ok &= not scs[0][:, 1].any() and not scs[1][:, 1].any()
-                E[:, b] = scs[0][:, 0]
-    return q, E, ok
-
-
-ACT_STEP, ACT_SCALE_STEP, ACT_ROWS = 3072, 256, 32
-
-
-def decode_act(op_img: np.ndarray, sc_img: np.ndarray, widths, M: int):
-    """Activation operand image (32-row tiles) and its scale bytes ->
-    (q [M, K], E [M, nb], layout_ok)."""
-    geo = Geo(widths)
-    nt = -(-M // ACT_ROWS)
-    assert op_img.size == nt * geo.nsteps * ACT_STEP
-    assert sc_img.size == nt * geo.nsteps * ACT_SCALE_STEP
-    t = op_img.reshape(nt, geo.nsteps, 3, 2, ACT_ROWS, 16)
-    sct = sc_img.reshape(nt, geo.nsteps, 2, ACT_ROWS, 4)
-
-    def lane_of(st, h):
-        return t[:, st, :, h].transpose(0, 2, 1, 3).reshape(nt * ACT_ROWS, 48)[:M]
-
-    def scale_of(st, h):
-        return sct[:, st, h].reshape(nt * ACT_ROWS, 4)[:M]
-
-    q, E, ok = _decode_steps(geo, len(widths), M, lane_of, scale_of, weights=False)
-    for st in range(geo.nsteps):
-        for h in (0, 1):
-            ok &= not scale_of(st, h)[:, 2:].any()
-    return q, E, ok
-
-
-def w_lane_bytes(img: np.ndarray, geo: Geo, st: int, h: int):
-    """Lane data (48 bytes) of step st, half h for every column of the weight
-    operand image img (1-D, all tiles).  Returns [ncols_padded, 48]."""
-    tile = CHUNK * geo.nsteps
-    ntiles = img.size // tile
-    t = img[:ntiles * tile].reshape(ntiles, geo.nsteps, CHUNK)[:, st]
-    parts = [t[:, j * PART + h * 2048:j * PART + h * 2048 + 2048].reshape(ntiles, TILE_COLS, 16)
-             for j in range(3)]
-    return np.concatenate(parts, axis=2).reshape(ntiles * TILE_COLS, 48)
-
-
-def w_scales(img: np.ndarray, geo: Geo, st: int, h: int):
-    tile = CHUNK * geo.nsteps
-    ntiles = img.size // tile
-    t = img[:ntiles * tile].reshape(ntiles, geo.nsteps, CHUNK)[:, st]
-    # [lane (c % 32)][column tile (c / 32)][4 bytes] -> columns in order
-    s = t[:, 3 * PART + h * 512:3 * PART + h * 512 + 512].reshape(ntiles, 32, 4, 4)
-    return s.transpose(0, 2, 1, 3).reshape(ntiles * TILE_COLS, 4)
-
-
-def decode_weights(img: np.ndarray, widths, N: int):
-    """Weight operand image -> (q [Npad128, K], E [Npad128, nb], layout_ok)."""
-    geo = Geo(widths)
-    tile = CHUNK * geo.nsteps
-    ntiles = img.size // tile
-    ok = True
-    for st in range(geo.nsteps):
-        for h in (0, 1):
-            ok &= not w_scales(img, geo, st, h)[:, 2:].any()
-    q, E, ok2 = _decode_steps(geo, len(widths), ntiles * TILE_COLS,
-                              lambda st, h: w_lane_bytes(img, geo, st, h),
-                              lambda st, h: w_scales(img, geo, st, h), weights=True)
-    return q, E, ok and ok2
-
-
-# --------------------------------------------------------------------------
-# Stream layout (decode GEMM): weight slabs of 16 columns and the 16-row
-# activation decode image, step by step in the lane order of the 16x16x128
-# scaled matrix-core instruction (lane l = 16 g + line).
-# --------------------------------------------------------------------------
-
-W_LANE = {0: 16, 1: 12, 2: 16}
-A_LANE = {0: 24, 1: 32, 2: 32}
-LANES = 64
-
-
-GROUP = 4          # steps sharing one 256-byte scale block
-
-
-class SGeo:
-    def __init__(self, widths):
-        w = np.asarray(widths)
-        self.n = [int((w == m).sum()) for m in (4, 6, 8)]
-        self.S = [-(-self.n[0] // 4), -(-self.n[1] // 2), -(-self.n[2] // 2)]
-        self.nb = len(w)
-        self.base = [0, self.n[0], self.n[0] + self.n[1]]   # first block of each segment
-
-    @staticmethod
-    def seg_bytes(S, step_data):
-        return S * step_data + -(-S // GROUP) * LANES * 4
-
-    def w_seg_off(self, seg):
-        return sum(self.seg_bytes(self.S[s], LANES * W_LANE[s]) for s in range(seg))
-
-    def a_seg_off(self, seg):
-        return sum(self.seg_bytes(self.S[s], LANES * A_LANE[s]) for s in range(seg))
-
-    def w_slab_bytes(self):
-        return self.w_seg_off(3)
-
-    def a_image_bytes(self):
-        return self.a_seg_off(3)
-
-
-def _step(buf, seg_off, st, step_data):
-    """(lane data [step_data bytes], scale bytes [64] of the step) of a
-    segment starting at seg_off: groups of GROUP steps, each a scale block
-    (lane l's byte for step k at 4 l + k) then the steps' data."""
-    g = seg_off + (st // GROUP) * (GROUP * step_data + LANES * 4)
-    data = buf[..., g + LANES * 4 + (st % GROUP) * step_data:
-               g + LANES * 4 + (st % GROUP + 1) * step_data]
-    sc = buf[..., g: g + LANES * 4].reshape(buf.shape[:-1] + (LANES, 4))[..., st % GROUP]
-    return data, sc
-
-
-def _sext(v, bits):
-    v = v.astype(np.int64)
-    return np.where(v >= (1 << (bits - 1)), v - (1 << bits), v)
-
-
-def _stream_nibbles(b8):
-    """[..., 8] nibble bytes of 16 elements (two dwords; byte k of dword d
-    holds elements 8d+k (low) and 8d+k+4 (high)) -> [..., 16] values 0..15."""
-    out = np.zeros(b8.shape[:-1] + (16,), np.int64)
-    for d in range(2):
-        for k in range(4):
-            byte = b8[..., 4 * d + k].astype(np.int64)
-            out[..., 8 * d + k] = byte & 15
-            out[..., 8 * d + k + 4] = byte >> 4
-    return out
-
-
-def _sm_nibble(v):
-    """Sign-magnitude 4-bit codes (sign at bit 3) -> values."""
-    return np.where(v & 8, -(v & 7), v & 7)
-
-
-def decode_w_stream(img, widths, N, sm=True):
-    """Weight slabs -> (q [Npad16, K], E [Npad16, nb], layout_ok).  sm: 4- and
-    6-bit codes are sign-magnitude (symmetric clamp), else two's complement."""
-    g = SGeo(widths)
-    nsl = -(-N // 16)
-    sb = g.w_slab_bytes()
-    slabs = img[:nsl * sb].reshape(nsl, sb)
-    q = np.zeros((nsl * 16, g.nb * BLOCK), np.int64)
-    E = np.full((nsl * 16, g.nb), -1, np.int64)
-    ok = True
-    for seg in range(3):
-        sd = LANES * W_LANE[seg]
-        for s in range(g.S[seg]):
-            ch, scb = _step(slabs, g.w_seg_off(seg), s, sd)
-            sc = scb.reshape(nsl, 4, 16).astype(np.int64)          # [slab, g, col]
-            for gg in range(4):
-                half = gg & 1
-                if seg == 0:
-                    lane = ch.reshape(nsl, 4, 16, 16)[:, gg]        # [slab, col, 16]
-                    parts = [(4 * s + (gg >> 1), lane[..., 0:8]), (4 * s + 2 + (gg >> 1), lane[..., 8:16])]
-                    dec = _sm_nibble if sm else (lambda v: _sext(v, 4))
-                    vals = [(blk, dec(_stream_nibbles(p))) for blk, p in parts]
-                else:
-                    blk = 2 * s + (gg >> 1)
-                    if seg == 1:
-                        nib = ch[:, :LANES * 8].reshape(nsl, 4, 16, 8)[:, gg]
-                        top = ch[:, 512:512 + LANES * 4].reshape(nsl, 4, 16, 4)[:, gg]
-                        y = top.astype(np.int64)
-                        y = y[..., 0] | (y[..., 1] << 8) | (y[..., 2] << 16) | (y[..., 3] << 24)
-                        lo = _stream_nibbles(nib)
-                        t2 = np.stack([(y >> (8 * (u % 4) + 2 * (u // 4))) & 3 for u in range(16)],
-                                      axis=-1)
-                        if sm:      # |q| = 8 t2 + (lo & 7), sign at bit 3 of lo
-                            v = np.where(lo & 8, -(8 * t2 + (lo & 7)), 8 * t2 + (lo & 7))
-                        else:
-                            v = _sext(lo | (t2 << 4), 6)
-                    else:
-                        v = _sext(ch.reshape(nsl, 4, 16, 16)[:, gg], 8)
-                    vals = [(blk, v)]
-                for blk, v in vals:
-                    v = v.reshape(nsl * 16, 16)
-                    if blk < g.n[seg]:
-                        b = g.base[seg] + blk
-                        q[:, BLOCK * b + 16 * half: BLOCK * b + 16 * half + 16] = v
-                    else:
-                        ok &= not v.any()
-            # lane group gg carries the exponent of block 4s+gg (4-bit) or
-            # 2s+(gg&1) (6/8-bit)
-            for gg in range(4):
-                blk = 4 * s + gg if seg == 0 else 2 * s + (gg & 1)
-                e = sc[:, gg].reshape(nsl * 16)
-                if blk < g.n[seg]:
-                    b = g.base[seg] + blk
-                    ok &= bool(np.all((E[:, b] == -1) | (E[:, b] == e)))
-                    E[:, b] = e
-                else:
-                    ok &= not e.any()
-        # scale bytes of the missing steps of a short last group are zero
-        for s in range(g.S[seg], -(-g.S[seg] // GROUP) * GROUP):
-            _, scb = _step(slabs, g.w_seg_off(seg), s, sd)
-            ok &= not scb.any()
-    return q, E, ok
-
-
-def decode_act_dimg(img, widths, M):
-    """Activation decode image (16 rows) -> (q [M, K], E [M, nb], layout_ok)."""
-    g = SGeo(widths)
-    assert img.size == g.a_image_bytes()
-    q = np.zeros((16, g.nb * BLOCK), np.int64)
-    E = np.full((16, g.nb), -1, np.int64)
-    ok = True
-    for seg in range(3):
-        sd = LANES * A_LANE[seg]
-        for s in range(g.S[seg]):
-            ch, scb = _step(img, g.a_seg_off(seg), s, sd)
-            sc = scb.reshape(4, 16).astype(np.int64)
-            for gg in range(4):
-                if seg == 0:
-                    b24 = np.concatenate([ch[:1024].reshape(4, 16, 16)[gg],
-                                          ch[1024:1536].reshape(4, 16, 8)[gg]], axis=1)
-                    v = fp6_values(b24)[:M] * 4
-                    blk, lo, hi = 4 * s + gg, 0, 32
-                else:
-                    lane = ch[:2048].reshape(4, 16, 32)[gg]
-                    hv, lv = fp8_values(lane[:M, :16]), fp8_values(lane[:M, 16:])
-                    # digits of q = 16 h + l summing to q 2^-(m-2): h + l/16
-                    # (6-bit), h/4 + l/64 (8-bit)
-                    f = 16 if seg == 1 else 64
-                    v = f * (hv + lv)
-                    h, l = hv * f / 16, lv * f
-                    ok &= bool(np.all((l >= 0) & (l <= 15) & (h == np.floor(v / 16))))
-                    blk, lo, hi = 2 * s + (gg >> 1), 16 * (gg & 1), 16 * (gg & 1) + 16
-                if blk < g.n[seg]:           # rows past M are unspecified
-                    b = g.base[seg] + blk
-                    q[:M, BLOCK * b + lo: BLOCK * b + hi] = v
-                else:
-                    ok &= not np.any(v)
-            for gg in range(4):
-                blk = 4 * s + gg if seg == 0 else 2 * s + (gg & 1)
-                e = sc[gg]
-                if blk < g.n[seg]:
-                    b = g.base[seg] + blk
-                    ok &= bool(np.all((E[:M, b] == -1) | (E[:M, b] == e[:M])))
-                    E[:, b] = e
-                else:
-                    ok &= not e[:M].any()
-    return q[:M], E[:M], ok
+                codes = _unfold(_words(ch).reshape(sup, SLABS, LANES, 4), _MAP4)
+            tab = E2M3 if seg == 0 else E3M2
+            mult = 8 if seg == 0 else 16
+            qall = _int_of(tab[codes] * mult, "3/4-bit weight")        # [sup, slab, lane, 32]
+            for j in range(4):
+                b = g.block(seg, sl, j)
+                qq = qall[:, :, 16 * j:16 * j + 16]                    # [sup, slab, c, 32]
+                e = sbytes[:, 16 * j:16 * j + 16, :].transpose(0, 2, 1)  # [sup, slab, c]
+                if b is None:
+                    ok &= not qq.any() and not e.any()
+                    continue
+                q[cols.reshape(-1), b * BLOCK:(b + 1) * BLOCK] = qq.reshape(-1, 32)
+                E[cols.reshape(-1), b] = e.reshape(-1)
+        elif seg == 2:
+            lo = _unfold(_words(ch[:, :, :512]).reshape(sup, SLABS, 32, 4), _MAP4)
+            vl = E3M2[lo]
+            if full:
+                hi = _unfold(_words(ch[:, :, 512:1024]).reshape(sup, SLABS, 32, 4), _MAP4)
+                vh = E3M2[hi]
+                ok &= bool(np.all((hi >> 5) == (lo >> 5)) or not full)
+            else:
+                hm = _unfold(_words(ch[:, :, 512:768]).reshape(sup, SLABS, 32, 2), _MAP2)
+                vh = np.where(lo >> 5, -1.0, 1.0) * E3M2[hm]
+            l = _int_of(np.abs(vl) * 16, "6-bit low weight digit")
+            h = _int_of(np.abs(vh) * 16, "6-bit high weight digit")
+            ok &= bool(np.all(l <= 7) and np.all(h <= (4 if full else 3)))
+            sign = np.where(lo >> 5, -1, 1)
+            qall = sign * (8 * h + l)                                  # [sup, slab, u, 32]
+            for j in range(2):
+                b = g.block(seg, sl, j)
+                qq = qall[:, :, 16 * j:16 * j + 16]
+                e0 = sbytes[:, 32 * j:32 * j + 16, :].transpose(0, 2, 1)
+                e1 = sbytes[:, 32 * j + 16:32 * j + 32, :].transpose(0, 2, 1)
+                ok &= bool(np.array_equal(e0, e1))
+                if b is None:
+                    ok &= not qq.any() and not e0.any()
+                    continue
+                q[cols.reshape(-1), b * BLOCK:(b + 1) * BLOCK] = qq.reshape(-1, 32)
+                E[cols.reshape(-1), b] = e0.reshape(-1)
+        else:
+            by = ch.reshape(sup, SLABS, 32, 32).astype(np.int64)       # [sup, slab, u, 32]
+            if full:
+                qall = np.where(by >= 128, by - 256, by)
+            else:
+                qall = np.where(by & 128, -(by & 127), by & 127)
+                ok &= not np.any(by == 128)                             # no -0 byte
+            for j in range(2):
+                b = g.block(seg, sl, j)
+                qq = qall[:, :, 16 * j:16 * j + 16]
+                e0 = sbytes[:, 32 * j:32 * j + 16, :].transpose(0, 2, 1)
+                e1 = sbytes[:, 32 * j + 16:32 * j + 32, :].transpose(0, 2, 1)
+                ok &= bool(np.array_equal(e0, e1))
+                if b is None:
+                    ok &= not qq.any() and not e0.any()
+                    continue
+                q[cols.reshape(-1), b * BLOCK:(b + 1) * BLOCK] = qq.reshape(-1, 32)
+                E[cols.reshape(-1), b] = e0.reshape(-1)
+    assert off == sb
+    ok &= not q[N:].any() and not E[N:].any()
+    ok &= not sc[~used].any()
+    return q, E, bool(ok)

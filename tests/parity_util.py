@@ -8,8 +8,7 @@ import numpy as np
 import torch
 
 import oracle
-from operand_decode import (CHUNK, TILE_COLS, Geo, SGeo, decode_act, decode_act_dimg,
-                            decode_w_stream, decode_weights)
+from operand_decode import Geo, decode_act, decode_weights
 from paper_2607_17733_amd import mxq
 from paper_2607_17733_amd.workloads import LinearCase
 
@@ -43,16 +42,19 @@ def oracle_quant(case: LinearCase, round_="rne", clamp="sym", identity=False):
 
 
 def gpu_run(case: LinearCase, fmt, want_partials=False, M=None):
-    """Quantize A, pack W and run the GEMM on the GPU; return host arrays."""
+    """Quantize A (operand image and packed rows), pack W and run the GEMM
+    on the GPU; return the device buffers."""
     a = to_dev_bf16(case.a_bits)
     w = to_dev_bf16(case.w_bits)
     M = case.M if M is None else M
     am, ae = mxq.quantize_act(a, fmt)
+    rows, exps = mxq.quantize_rows(a, fmt)
     wm, we = mxq.pack_weights(w, fmt)
     y = mxq.gemm(am, ae, wm, we, fmt, M, case.N)
-    out = {"a_mant": am, "a_exp": ae, "w_mant": wm, "w_exp": we, "y": y}
+    out = {"a_mant": am, "a_exp": ae, "rows": rows, "exps": exps, "w_mant": wm, "w_exp": we,
+           "y": y}
     if want_partials:
-        out["p"] = mxq.gemm_partials(am, ae, wm, we, fmt, M, case.N)
+        out["p"] = mxq.gemm_partials(rows, exps, wm, we, fmt, M, case.N)
     torch.cuda.synchronize()
     return out
 
@@ -61,9 +63,10 @@ def digit_absbound(qa, ea, qw, ew, widths, rows=None, cols=None):
     """T[i, j] = sum_k (|qa|+c)(|qw|+c) 2^(Ea+Ew-254-2(m-2)), an upper bound of
     the sum of |digit products| the matrix core accumulates for Y[i, j]: an
     m-bit mantissa q splits into digits with |8h| + |l| <= |q| + 14 (m = 6)
-    and |16h| + |l| <= |q| + 30 (m = 8); 4-bit mantissas are not split."""
+    and |16h| + |l| <= |q| + 30 (m = 8); 3- and 4-bit mantissas are not
+    split."""
     wb = np.asarray(widths)
-    c = np.repeat(np.select([wb == 4, wb == 6], [0, 14], 30), BLOCK).astype(np.float64)
+    c = np.repeat(np.select([wb <= 4, wb == 6], [0, 14], 30), BLOCK).astype(np.float64)
     off = 127 + (wb - 2)
     rows = np.arange(qa.shape[0]) if rows is None else np.asarray(rows)
     cols = np.arange(qw.shape[0]) if cols is None else np.asarray(cols)
@@ -75,10 +78,12 @@ def digit_absbound(qa, ea, qw, ew, widths, rows=None, cols=None):
 
 
 def mma_steps(widths):
-    """Matrix-core instructions accumulated into each output by the prefill
-    GEMM: two per 4-bit step, four per 6-bit pair, two per 8-bit block."""
+    """Matrix-core instructions accumulated into each output, the larger of
+    the two GEMMs' counts: the prefill kernel's 64-K instructions, two per
+    3/4-bit step (four blocks) and four per 6/8-bit step (two blocks, two
+    digit planes)."""
     g = Geo(widths)
-    return 2 * g.s4 + 4 * g.s6 + 2 * g.s8
+    return 2 * (g.S[0] + g.S[1]) + 4 * (g.S[2] + g.S[3])
 
 
 def a14_ratio(Y, Yref):
@@ -142,51 +147,40 @@ def check_gemm(Y, Yref, qa, ea, qw, ew, widths, what, rows=None, cols=None, a14=
 
 
 def check_quant_act(case, out, qa, ea, fmt):
-    """Bit-exact activation buffers: packed rows against the oracle's
-    packing, exponents, the operand image decoded back to mantissas and
-    scale bytes, zero padding, and mxq_unpack_act."""
+    """Bit-exact activation buffers: the operand image decoded on the host
+    back to mantissas and scale bytes (zero padding included) and, when
+    `out` holds them, the packed rows against the oracle's packing, the
+    exponent rows, and mxq_unpack_act."""
     M = case.M
     am = out["a_mant"].cpu().numpy()
     ae = out["a_exp"].cpu().numpy()
     nb = case.K // BLOCK
-    canon = fmt.act_packed_bytes()
-    cerb = fmt.exp_row_bytes()
     assert am.size == fmt.act_bytes(M) and ae.size == fmt.act_exp_bytes(M)
-    ref_bytes = oracle.pack_act(qa, case.widths)
-    assert ref_bytes.shape == (M, canon)
-    assert np.array_equal(am[:M * canon].reshape(M, canon), ref_bytes), \
-        "packed activation bytes differ"
-    erows = ae[:M * cerb].reshape(M, cerb)
-    assert np.array_equal(erows[:, :nb], ea), "activation exponents differ"
-    assert not erows[:, nb:].any()
-    if M <= mxq.DECODE_MAX_M:
-        assert ae.size == M * cerb
-        q, E, pad_ok = decode_act_dimg(am[M * canon:], case.widths, M)
-    else:
-        q, E, pad_ok = decode_act(am[M * canon:], ae[M * cerb:], case.widths, M)
+    q, E, pad_ok = decode_act(am, ae, case.widths, M)
     assert np.array_equal(q, qa), "activation operand image differs from the mantissas"
     assert np.array_equal(E, ea.astype(np.int64)), "activation scale bytes differ"
     assert pad_ok, "activation operand padding not zero"
-    qd, ed = mxq.unpack_act(out["a_mant"], out["a_exp"], fmt, M)
+    if "rows" not in out:
+        return
+    rows = out["rows"].cpu().numpy()
+    exps = out["exps"].cpu().numpy()
+    assert rows.shape == (M, fmt.act_packed_bytes())
+    assert np.array_equal(rows, oracle.pack_act(qa, case.widths)), "packed activation rows differ"
+    assert np.array_equal(exps[:, :nb], ea), "activation exponents differ"
+    assert not exps[:, nb:].any()
+    qd, ed = mxq.unpack_act(out["rows"], out["exps"], fmt, M)
     assert np.array_equal(qd.cpu().numpy(), qa) and np.array_equal(ed.cpu().numpy(), ea)
 
 
 def check_pack_w(case, out, qw, ew, fmt):
+    """Bit-exact weight buffers: mxq_unpack_weights, and the host decoder of
+    the documented layout (padding columns and zero blocks included)."""
     N = qw.shape[0]
     q, e = mxq.unpack_weights(out["w_mant"], out["w_exp"], fmt, N)
     assert np.array_equal(q.cpu().numpy(), qw), "weight mantissas differ"
     assert np.array_equal(e.cpu().numpy(), ew), "weight exponents differ"
-    wm = out["w_mant"].cpu().numpy()
-    qs, es, ok = decode_w_stream(wm, case.widths, N, sm=fmt.clamp == 0)
-    assert ok, "weight stream layout / padding"
-    assert np.array_equal(qs[:N], qw), "weight slabs differ from the mantissas"
-    assert np.array_equal(es[:N], ew.astype(np.int64)), "weight slab scale bytes differ"
-    assert not qs[N:].any() and not es[N:].any(), "padding columns not zero"
-    assert not wm[-(-N // 16) * SGeo(case.widths).w_slab_bytes():][:64].any(), "tail padding"
-    g = Geo(case.widths)
-    size = -(-N // TILE_COLS) * CHUNK * g.nsteps
-    qo, eo, ok = decode_weights(wm[wm.size - size:], case.widths, N)
-    assert ok, "weight operand image layout / padding"
-    assert np.array_equal(qo[:N], qw), "weight operand image differs from the mantissas"
+    qo, eo, ok = decode_weights(out["w_mant"].cpu().numpy(), out["w_exp"].cpu().numpy(),
+                                case.widths, N, full=fmt.clamp == 1)
+    assert ok, "weight layout / padding"
+    assert np.array_equal(qo[:N], qw), "weight buffer differs from the mantissas"
     assert np.array_equal(eo[:N], ew.astype(np.int64)), "weight scale bytes differ"
-    assert not qo[N:].any() and not eo[N:].any(), "padding columns not zero"

@@ -47,58 +47,69 @@ def _fmt(K, widths, round_=0, clamp=0, block=32, reserved=0):
     return f, w
 
 
-def op_steps(widths):
-    """Steps of the operand images as include/mxq.h states them: 4-bit
-    blocks padded to a multiple of 4 taken four at a time, 6-bit padded to a
-    multiple of 2 taken two at a time, 8-bit one at a time."""
-    n4, n6, n8 = (sum(1 for w in widths if w == m) for m in (4, 6, 8))
-    return -(-n4 // 4) + -(-n6 // 2) + n8
-
-
-def stream_sizes(widths):
-    """Weight slab and activation decode-image bytes as include/mxq.h states
-    them: 4-bit blocks four per step, 6/8-bit blocks two per step; 64 lanes
-    of 16/12/16 (weights) or 24/32/32 (activations) bytes per step, and a
-    256-byte scale block per group of four steps of a segment."""
-    n4, n6, n8 = (sum(1 for w in widths if w == m) for m in (4, 6, 8))
-    S = (-(-n4 // 4), -(-n6 // 2), -(-n8 // 2))
-    wlane, alane = (16, 12, 16), (24, 32, 32)
-    return (sum(s * 64 * l + -(-s // 4) * 256 for s, l in zip(S, wlane)),
-            sum(s * 64 * l + -(-s // 4) * 256 for s, l in zip(S, alane)))
+def layout_sizes(widths, M, N, full=False):
+    """Buffer sizes as include/mxq.h states them: four segments (3-, 4-, 6-,
+    8-bit blocks) of steps of four (3/4-bit) or two (6/8-bit) blocks, groups
+    of four steps; the activation image in 16-row tiles of 64 lanes x 24
+    (32 for 8-bit steps) bytes per step plus 256 scale bytes per group; the
+    weights in 128-column super-slabs of eight chunks per step plus 2048
+    scale bytes per group."""
+    n = [sum(1 for w in widths if w == m) for m in (3, 4, 6, 8)]
+    S = [-(-n[0] // 4), -(-n[1] // 4), -(-n[2] // 2), -(-n[3] // 2)]
+    groups = sum(-(-s // 4) for s in S)
+    tiles, supers = -(-M // 16), -(-N // 128)
+    chunk = [(768, 1024), (1024, 1536), (768, 1024), (1024, 1024)]
+    act = tiles * 64 * (24 * (S[0] + S[1] + S[2]) + 32 * S[3])
+    act_exp = tiles * groups * 256
+    wb = supers * 8 * sum(s * c[int(full)] for s, c in zip(S, chunk))
+    w_exp = supers * groups * 2048
+    return act, act_exp, wb, w_exp
 
 
 def test_sizes(lib):
     w1 = [4] * 6 + [6, 8]
     f, _w = _fmt(256, w1)
-    assert lib.mxq_abi_version() == 10
-    assert op_steps(w1) == 4
-    slab, dimg = stream_sizes(w1)
-    assert (slab, dimg) == (2 * 1024 + 768 + 1024 + 3 * 256, 2 * 1536 + 2 * 2048 + 3 * 256)
-    assert lib.mxq_act_packed_bytes(ctypes.byref(f)) == 160
-    assert lib.mxq_exp_row_bytes(ctypes.byref(f)) == 16
-    # M <= 16: M packed rows + the decode image; larger M: 32-row operand
-    # tiles of 3072 bytes per step
-    assert lib.mxq_act_bytes(ctypes.byref(f), 16) == 16 * 160 + dimg
-    assert lib.mxq_act_bytes(ctypes.byref(f), 1) == 160 + dimg
-    assert lib.mxq_act_bytes(ctypes.byref(f), 33) == 33 * 160 + 2 * 4 * 3072
-    assert lib.mxq_act_bytes(ctypes.byref(f), 0) == 0
-    assert lib.mxq_act_bytes(ctypes.byref(f), -1) == -2
-    # M exponent rows (+ 256 scale bytes per (tile, step) for M > 16)
-    assert lib.mxq_act_exp_bytes(ctypes.byref(f), 16) == 16 * 16
-    assert lib.mxq_act_exp_bytes(ctypes.byref(f), 64) == 64 * 16 + 2 * 4 * 256
-    # stream slabs (N to 16) + 64-byte tail + 128-column operand tiles of
-    # 13312 bytes per step
-    assert lib.mxq_weight_bytes(ctypes.byref(f), 256) == 16 * slab + 64 + 2 * 4 * 13312
-    assert lib.mxq_weight_bytes(ctypes.byref(f), 250) == 16 * slab + 64 + 2 * 4 * 13312
-    assert lib.mxq_weight_bytes(ctypes.byref(f), 129) == 9 * slab + 64 + 2 * 4 * 13312
-    assert lib.mxq_weight_exp_bytes(ctypes.byref(f), 17) == 32 * 16
+    fr = ctypes.byref(f)
+    assert lib.mxq_abi_version() == 11
+    # S = 0/2/1/1 steps, 3 groups: tiles of 64 x (3 x 24 + 32) bytes
+    assert layout_sizes(w1, 16, 128) == (6656, 768, 8 * (2 * 1024 + 768 + 1024), 3 * 2048)
+    assert lib.mxq_act_packed_bytes(fr) == 160
+    assert lib.mxq_exp_row_bytes(fr) == 16
+    for M in (1, 16, 17, 33, 64, 300):
+        act, act_exp, _, _ = layout_sizes(w1, M, 1)
+        assert lib.mxq_act_bytes(fr, M) == act
+        assert lib.mxq_act_exp_bytes(fr, M) == act_exp
+    assert lib.mxq_act_bytes(fr, 0) == 0
+    assert lib.mxq_act_bytes(fr, -1) == -2
+    for N in (1, 17, 128, 129, 250, 256):
+        _, _, wb, w_exp = layout_sizes(w1, 1, N)
+        assert lib.mxq_weight_bytes(fr, N) == wb
+        assert lib.mxq_weight_exp_bytes(fr, N) == w_exp
+    f_full, _wf = _fmt(256, w1, clamp=1)
+    assert lib.mxq_weight_bytes(ctypes.byref(f_full), 256) == layout_sizes(w1, 1, 256, True)[2]
     w2 = [4] * 102 + [6] * 13 + [8] * 13
     f2, _w2 = _fmt(4096, w2)
-    assert op_steps(w2) == 26 + 7 + 13
     assert lib.mxq_act_packed_bytes(ctypes.byref(f2)) == 2368   # 2360 rounded up to 16
     assert lib.mxq_exp_row_bytes(ctypes.byref(f2)) == 128
-    assert lib.mxq_act_bytes(ctypes.byref(f2), 2048) == 2048 * 2368 + 64 * 46 * 3072
-    assert lib.mxq_act_exp_bytes(ctypes.byref(f2), 2048) == 2048 * 128 + 64 * 46 * 256
+    assert lib.mxq_act_bytes(ctypes.byref(f2), 2048) == 128 * 64 * (24 * 33 + 32 * 7)
+    assert lib.mxq_act_exp_bytes(ctypes.byref(f2), 2048) == 128 * 11 * 256
+    w3 = [3] * 26 + [6] * 4 + [8] * 2
+    f3, _w3 = _fmt(1024, w3)
+    assert lib.mxq_act_packed_bytes(ctypes.byref(f3)) == 480   # 26 x 12 + 4 x 24 + 2 x 32 = 472
+    assert lib.mxq_weight_bytes(ctypes.byref(f3), 128) == layout_sizes(w3, 1, 128)[2]
+
+
+@pytest.mark.parametrize("counts,N", [((217, 26, 13), 28672), ((761, 90, 45), 8192)])
+def test_weights_at_mxint_size(lib, counts, N):
+    """The one weight copy is within 5 % of the MXINT bits (mantissas plus
+    one exponent byte per block) at the decode workload's 85/10/5 split."""
+    n4, n6, n8 = counts
+    widths = [4] * n4 + [6] * n6 + [8] * n8
+    f, _w = _fmt(32 * len(widths), widths)
+    stored = lib.mxq_weight_bytes(ctypes.byref(f), N) + lib.mxq_weight_exp_bytes(ctypes.byref(f), N)
+    mxint = N * sum(4 * m + 1 for m in widths)
+    assert stored <= 1.05 * mxint, stored / mxint
+    assert 8 * stored / (N * 32 * len(widths)) <= 4.9
 
 
 def test_size_functions_match_oracle_layout(lib, oracle_lib):

@@ -1,7 +1,7 @@
 """GPU parity of decode attention over the MXINT KV cache (C ABI
 mxq_attn_decode) against the float64 oracle in oracle/attn.py.
 
-The caches are quantized on the GPU by mxq_quantize_act (whose bit-exact
+The caches are quantized on the GPU by mxq_quantize_rows (whose bit-exact
 parity with the oracle's quantizer the quantizer tests establish) and by the
 oracle's quantizer for the reference; the test also checks that the two
 agree on the packed rows it reads, so the comparison is of the attention
@@ -38,8 +38,8 @@ def _run(seed, B, Hq, Hkv, T, widths, seqs=None):
     say("attn seed=%d B=%d Hq=%d Hkv=%d T=%d widths=%s" % (seed, B, Hq, Hkv, T, widths))
     qb, kb, vb = W.attn_inputs(seed, B, Hq, Hkv, T)
     fmt = mxq.Format(D, widths)
-    kc = mxq.quantize_act(to_dev_bf16(kb), fmt)
-    vc = mxq.quantize_act(to_dev_bf16(vb), fmt)
+    kc = mxq.quantize_rows(to_dev_bf16(kb), fmt)
+    vc = mxq.quantize_rows(to_dev_bf16(vb), fmt)
     scale = 1.0 / np.sqrt(D)
     o = mxq.attn_decode(to_dev_bf16(qb.reshape(-1, D)).reshape(B, Hq, D), kc, vc, fmt,
                         B, Hq, Hkv, T, scale)
@@ -64,7 +64,7 @@ def test_cache_rows_match_oracle_quantizer():
     widths = [4, 6, 8, 8]
     _, kb, _ = W.attn_inputs(1, 1, 4, 2, 70)
     fmt = mxq.Format(D, widths)
-    mant, exp = mxq.quantize_act(to_dev_bf16(kb), fmt)
+    mant, exp = mxq.quantize_rows(to_dev_bf16(kb), fmt)
     q, e = mxq.unpack_act(mant, exp, fmt, kb.shape[0])
     qo, eo = oracle.quantize(kb, widths=widths)
     assert np.array_equal(q.cpu().numpy(), qo) and np.array_equal(e.cpu().numpy(), eo)
@@ -122,8 +122,8 @@ def test_repeat_calls_identical():
     B, Hq, Hkv, T, widths = 2, 16, 2, 900, [4, 6, 6, 8]
     qb, kb, vb = W.attn_inputs(3, B, Hq, Hkv, T)
     fmt = mxq.Format(D, widths)
-    kc = mxq.quantize_act(to_dev_bf16(kb), fmt)
-    vc = mxq.quantize_act(to_dev_bf16(vb), fmt)
+    kc = mxq.quantize_rows(to_dev_bf16(kb), fmt)
+    vc = mxq.quantize_rows(to_dev_bf16(vb), fmt)
     q = to_dev_bf16(qb.reshape(-1, D)).reshape(B, Hq, D)
     a = mxq.attn_decode(q, kc, vc, fmt, B, Hq, Hkv, T, 0.1)
     b = mxq.attn_decode(q, kc, vc, fmt, B, Hq, Hkv, T, 0.1)
@@ -134,7 +134,7 @@ def test_repeat_calls_identical():
 def test_rejects_bad_arguments():
     fmt = mxq.Format(D, [4, 4, 4, 4])
     q = torch.zeros((1, 8, D), dtype=torch.bfloat16, device="cuda")
-    kc = mxq.quantize_act(torch.zeros((4 * 2, D), dtype=torch.bfloat16, device="cuda"), fmt)
+    kc = mxq.quantize_rows(torch.zeros((4 * 2, D), dtype=torch.bfloat16, device="cuda"), fmt)
     with pytest.raises(mxq.MxqError):                      # Hq not a multiple of Hkv
         mxq.attn_decode(q, kc, kc, fmt, 1, 8, 3, 4, 0.1)
     with pytest.raises(mxq.MxqError):                      # a cache shorter than its rows

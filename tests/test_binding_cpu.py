@@ -11,7 +11,8 @@ import torch
 
 from paper_2607_17733_amd import mxq
 
-LAUNCHING = {"mxq_quantize_act", "mxq_quantize_act_rmsnorm", "mxq_quantize_act_swiglu",
+LAUNCHING = {"mxq_quantize_act", "mxq_quantize_rows", "mxq_quantize_act_rmsnorm",
+             "mxq_quantize_act_swiglu",
              "mxq_pack_weights", "mxq_gemm", "mxq_gemm_partials", "mxq_unpack_act",
              "mxq_unpack_weights", "mxq_attn_decode"}
 
@@ -46,6 +47,12 @@ def _operands(fmt, M, N):
             _u8(fmt.weight_exp_bytes(N)))
 
 
+def _row_operands(fmt, M, N):
+    """The inputs of gemm_partials: packed rows, exponent rows, weights."""
+    return (_u8(M * fmt.act_packed_bytes()), _u8(M * fmt.exp_row_bytes()),
+            _u8(fmt.weight_bytes(N)), _u8(fmt.weight_exp_bytes(N)))
+
+
 FMT_ARGS = (256, [4] * 6 + [6, 8])
 
 
@@ -57,8 +64,10 @@ def test_gemm_rejects_short_operands(host_as_device, short, M):
     ops[short] = ops[short][:-1]
     with pytest.raises(mxq.MxqError, match="needed"):
         mxq.gemm(*ops, fmt, M, 48, out=torch.zeros((M, 48)))
+    rops = list(_row_operands(fmt, M, 48))
+    rops[short] = rops[short][:-1]
     with pytest.raises(mxq.MxqError, match="needed"):
-        mxq.gemm_partials(*ops, fmt, M, 48)
+        mxq.gemm_partials(*rops, fmt, M, 48)
 
 
 def test_gemm_rejects_small_or_wrong_out(host_as_device):
@@ -89,13 +98,19 @@ def test_quantizers_reject_short_outputs(host_as_device):
             mxq.quantize_act_rmsnorm(x, gain, 1e-5, fmt, out=out)
         with pytest.raises(mxq.MxqError, match="needed"):
             mxq.quantize_act_swiglu(x, x, fmt, out=out)
+    rows, exps = _u8(40 * fmt.act_packed_bytes()), _u8(40 * fmt.exp_row_bytes())
+    for out in ((rows[:-1], exps), (rows, exps[:-1])):
+        with pytest.raises(mxq.MxqError, match="needed"):
+            mxq.quantize_rows(x, fmt, out=out)
 
 
 def test_unpack_rejects_short_inputs(host_as_device):
     fmt = mxq.Format(*FMT_ARGS)
-    am, ae, wm, we = _operands(fmt, 40, 48)
+    rows, exps, wm, we = _row_operands(fmt, 40, 48)
     with pytest.raises(mxq.MxqError, match="needed"):
-        mxq.unpack_act(am[:-16], ae, fmt, 40)
+        mxq.unpack_act(rows[:-16], exps, fmt, 40)
+    with pytest.raises(mxq.MxqError, match="needed"):
+        mxq.unpack_act(rows, exps[:-1], fmt, 40)
     with pytest.raises(mxq.MxqError, match="needed"):
         mxq.unpack_weights(wm, we[:-1], fmt, 48)
 
@@ -108,21 +123,26 @@ def test_cpu_tensor_is_not_a_device_tensor():
 
 
 def test_abi_rejects_offsets_beyond_32_bits():
-    """A K so long that a wave's two activation tiles (or one 128-column
-    weight tile) span more than INT32_MAX bytes is refused with
+    """A K so long that sixteen 16-row activation tiles (a prefill
+    workgroup's rows) span more than INT32_MAX bytes is refused with
     MXQ_ERR_SHAPE before any pointer is touched."""
     lib = mxq.lib()
-    nb = 349526                        # 2 * nb * 3072 > 2^31 - 1 (8-bit steps)
-    w = np.full(nb, 8, np.uint8)
-    f = mxq._Fmt(32 * nb, 32, 0, 0, 0, w.ctypes.data_as(ctypes.c_void_p).value, None)
     fake = ctypes.c_void_p(1 << 20)    # aligned, never dereferenced
-    st = lib.mxq_gemm(ctypes.byref(f), 64, 128, fake, fake, fake, fake, fake, 128, None)
-    assert st == 2
-    w2 = np.full(nb - 1000, 8, np.uint8)
-    f2 = mxq._Fmt(32 * len(w2), 32, 0, 0, 0, w2.ctypes.data_as(ctypes.c_void_p).value, None)
-    # just inside the activation limit, but the 13 KB-per-step weight tile is not
-    st2 = lib.mxq_gemm_partials(ctypes.byref(f2), 64, 128, fake, fake, fake, fake, fake, None)
-    assert st2 == 2
+    for nb, rejected in ((131072, True), (131071, True), (131070, False)):
+        # 8-bit blocks: a 16-row tile holds 64 lanes x 32 bytes per two blocks
+        w = np.full(nb, 8, np.uint8)
+        f = mxq._Fmt(32 * nb, 32, 0, 0, 0, w.ctypes.data_as(ctypes.c_void_p).value, None)
+        tile = 64 * 32 * -(-nb // 2)
+        assert lib.mxq_act_bytes(ctypes.byref(f), 16) == tile
+        if rejected:
+            assert 16 * tile > 2 ** 31 - 1
+            st = lib.mxq_gemm(ctypes.byref(f), 64, 128, fake, fake, fake, fake, fake, 128, None)
+            assert st == 2
+            st = lib.mxq_gemm_partials(ctypes.byref(f), 64, 128, fake, fake, fake, fake, fake,
+                                       None)
+            assert st == 2
+        else:
+            assert 16 * tile <= 2 ** 31 - 1
 
 
 def test_static_attention_rejects_oversize_on_the_host():

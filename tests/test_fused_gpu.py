@@ -55,9 +55,10 @@ def test_fused_equals_unfused_on_device():
     y_bits = fused.rmsnorm_bf16(case.a_bits[:64], gain, 1e-5)      # a sample of rows
     bm, be = mxq.quantize_act(to_dev_bf16(y_bits), fmt)
     torch.cuda.synchronize()
-    rb, erb = fmt.act_packed_bytes(), fmt.exp_row_bytes()
-    assert torch.equal(am[:64 * rb], bm[:64 * rb])
-    assert torch.equal(ae[:64 * erb], be[:64 * erb])
+    # the first 64 rows are the image's first four 16-row tiles
+    tb, tsc = fmt.act_bytes(16), fmt.act_exp_bytes(16)
+    assert torch.equal(am[:4 * tb], bm[:4 * tb])
+    assert torch.equal(ae[:4 * tsc], be[:4 * tsc])
 
 
 SWIGLU_SHAPES = [

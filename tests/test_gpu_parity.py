@@ -1,9 +1,8 @@
 """GPU parity: the HIP path (through the C ABI) against the CPU oracle.
 
-Bit-exact: packed activation bytes, exponents, the matrix-core operand
-images of both operands (decoded on the host back to mantissas and scale
-bytes), unpacked weight mantissas and exponents, and the per-block int32
-sums.  GEMM outputs: relative error 1e-5 (normwise) against the fp64 oracle
+Bit-exact: the activation operand image and the weight buffers (decoded
+on the host back to mantissas and scale bytes), packed activation rows,
+exponents, unpacked mantissas and exponents, and the per-block int32 sums.  GEMM outputs: relative error 1e-5 (normwise) against the fp64 oracle
 and, elementwise, the accumulation bound of the path that ran.  Small shapes span several tiles and ragged tails; the workload
 shapes run at full size with sampled GEMM outputs.
 """
@@ -14,6 +13,7 @@ import torch
 import oracle
 from paper_2607_17733_amd import mxq
 from paper_2607_17733_amd import workloads as W
+from operand_decode import decode_act
 from parity_util import (check_gemm, check_pack_w, check_quant_act, fmt_for,
                          gpu_run, oracle_quant, say, to_dev_bf16)
 
@@ -76,7 +76,9 @@ def test_out_of_range_permutation_entries_read_zero():
     perm[[3, 100, 255]] = [256, -5, 1 << 30]
     say("oor-perm")
     fmtg = mxq.Format(case.K, case.widths, torch.from_numpy(perm).cuda())
-    am, ae = mxq.quantize_act(to_dev_bf16(case.a_bits), fmtg)
+    a = to_dev_bf16(case.a_bits)
+    am, ae = mxq.quantize_act(a, fmtg)
+    rows, exps = mxq.quantize_rows(a, fmtg)
     torch.cuda.synchronize()
     # oracle: the same gather from a source padded with a zero column
     src = np.zeros((case.M, case.K + 32), np.uint16)
@@ -84,9 +86,10 @@ def test_out_of_range_permutation_entries_read_zero():
     p2 = perm.copy()
     p2[[3, 100, 255]] = case.K
     qa, ea = oracle.quantize(src, K=case.K, perm=p2, widths=case.widths)
-    assert np.array_equal(mxq.packed_rows(am, fmtg, case.M).cpu().numpy(),
-                          oracle.pack_act(qa, case.widths))
-    assert np.array_equal(mxq.exp_rows(ae, fmtg, case.M).cpu().numpy()[:, :case.K // 32], ea)
+    assert np.array_equal(rows.cpu().numpy(), oracle.pack_act(qa, case.widths))
+    assert np.array_equal(exps.cpu().numpy()[:, :case.K // 32], ea)
+    q, E, pad_ok = decode_act(am.cpu().numpy(), ae.cpu().numpy(), case.widths, case.M)
+    assert np.array_equal(q, qa) and np.array_equal(E, ea) and pad_ok
 
 
 def test_strided_inputs_and_outputs():
@@ -103,8 +106,10 @@ def test_strided_inputs_and_outputs():
     mxq.gemm(am, ae, wm, we, fmt, 48, 40, out=y_big[:, :40])
     torch.cuda.synchronize()
     qa, ea, qw, ew = oracle_quant(case)
-    assert np.array_equal(mxq.packed_rows(am, fmt, 48).cpu().numpy(),
-                          oracle.pack_act(qa, case.widths))
+    rows, _ = mxq.quantize_rows(a_big[:, :256], fmt)
+    assert np.array_equal(rows.cpu().numpy(), oracle.pack_act(qa, case.widths))
+    q, _, _ = decode_act(am.cpu().numpy(), ae.cpu().numpy(), case.widths, 48)
+    assert np.array_equal(q, qa)
     Yref = oracle.gemm(qa, ea, qw, ew, case.widths)
     yb = y_big.cpu().numpy()
     check_gemm(yb[:, :40], Yref, qa, ea, qw, ew, case.widths, "strided")
@@ -239,10 +244,8 @@ def test_kv_cache_quantize():
         bits = W.kv_cache(which)
         say("kv", which, bits.shape)
         fmt = mxq.Format(128, [4, 4, 4, 4])
-        am, ae = mxq.quantize_act(to_dev_bf16(bits), fmt)
+        rows, exps = mxq.quantize_rows(to_dev_bf16(bits), fmt)
         torch.cuda.synchronize()
         q, e = oracle.quantize(bits, widths=[4, 4, 4, 4])
-        rows = bits.shape[0]
-        assert np.array_equal(mxq.packed_rows(am, fmt, rows).cpu().numpy(),
-                              oracle.pack_act(q, [4, 4, 4, 4]))
-        assert np.array_equal(mxq.exp_rows(ae, fmt, rows).cpu().numpy()[:, :4], e)
+        assert np.array_equal(rows.cpu().numpy(), oracle.pack_act(q, [4, 4, 4, 4]))
+        assert np.array_equal(exps.cpu().numpy()[:, :4], e)

@@ -63,8 +63,8 @@ def test_attention_graph_replays_match_eager():
     dev = torch.device("cuda:0")
     qb, kb, vb = W.attn_inputs(41, B, Hq, Hkv, T)
     fmt = mxq.Format(D, [4, 4, 6, 8])
-    kc = mxq.quantize_act(to_dev_bf16(kb), fmt)
-    vc = mxq.quantize_act(to_dev_bf16(vb), fmt)
+    kc = mxq.quantize_rows(to_dev_bf16(kb), fmt)
+    vc = mxq.quantize_rows(to_dev_bf16(vb), fmt)
     q = to_dev_bf16(qb.reshape(-1, D)).reshape(B, Hq, D)
     o = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
     work = torch.empty(mxq.attn_work_bytes(fmt, B, Hq, Hkv, T), dtype=torch.uint8, device=dev)

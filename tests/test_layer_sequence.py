@@ -52,9 +52,7 @@ def test_layer_sequence(sensitive):
         check_gemm(got.cpu().numpy(), Yref, qa, ea, qw, ew, s.widths, s.name)
 
     widths = [4, 4, 4, 4]
-    for t, (am, ae) in zip(kv, kvq):
+    for t, (rows, exps) in zip(kv, kvq):
         q, e = oracle.quantize(_bits(t), widths=widths)
-        n = t.shape[0]
-        assert np.array_equal(mxq.packed_rows(am, seq.kv_fmt, n).cpu().numpy(),
-                              oracle.pack_act(q, widths))
-        assert np.array_equal(mxq.exp_rows(ae, seq.kv_fmt, n).cpu().numpy()[:, :4], e)
+        assert np.array_equal(rows.cpu().numpy(), oracle.pack_act(q, widths))
+        assert np.array_equal(exps.cpu().numpy()[:, :4], e)

@@ -1,8 +1,9 @@
 """GPU parity of the 3-6-8 template (3-bit blocks in place of 4-bit ones, the
-paper's average-bitwidth study, Section 5) through the C ABI: the quantizer's
-packed rows and exponents bit-exact against the oracle (a 3-bit block is
-stored as the 4-bit block holding 2q), the weight pack, the prefill and
-decode GEMMs against the oracle GEMM, and attention over 3-bit caches."""
+paper's average-bitwidth study, Section 5) through the C ABI: the
+quantizer's packed rows (3-bit blocks at 12 bytes), exponents and operand
+image bit-exact against the oracle, the weight buffers (3 bits per element
+under the symmetric clamp), the prefill and decode GEMMs against the oracle
+GEMM, and attention over 3-bit caches."""
 import numpy as np
 import pytest
 import torch
@@ -10,6 +11,7 @@ import torch
 import oracle
 from paper_2607_17733_amd import mxq
 from paper_2607_17733_amd import workloads as W
+from operand_decode import decode_act, decode_weights
 from parity_util import check_gemm, say, to_dev_bf16
 from test_attn_gpu import _run as attn_run
 
@@ -28,36 +30,43 @@ def _case(seed, M, K, N, n3, n6, n8):
     return a, w, perm, widths
 
 
-def _doubled(q, n3):
-    q = q.astype(np.int16).copy()
-    q[:, :32 * n3] *= 2
-    return q
-
-
 @pytest.mark.parametrize("clamp", ["sym", "full"])
 @pytest.mark.parametrize("M", [1, 16, 77])
 def test_quantizer_bytes(M, clamp):
     a, _, perm, widths = _case(1, M, 512, 16, 12, 2, 2)
     say("368 quantize M=%d clamp=%s" % (M, clamp))
     fmt = mxq.Format(512, widths, torch.from_numpy(perm).cuda(), clamp=clamp)
-    mant, exp = mxq.quantize_act(to_dev_bf16(a), fmt)
+    am, ae = mxq.quantize_act(to_dev_bf16(a), fmt)
+    rows, exps = mxq.quantize_rows(to_dev_bf16(a), fmt)
     torch.cuda.synchronize()
     q, e = oracle.quantize(a, perm=perm, widths=widths, clamp_mode=1 if clamp == "full" else 0)
-    assert np.array_equal(mxq.packed_rows(mant, fmt, M).cpu().numpy(), oracle.pack_act(q, widths))
-    assert np.array_equal(mxq.exp_rows(exp, fmt, M).cpu().numpy()[:, :16], e)
-    qu, eu = mxq.unpack_act(mant, exp, fmt, M)
-    assert np.array_equal(qu.cpu().numpy(), _doubled(q, 12)) and np.array_equal(eu.cpu().numpy(), e)
+    assert rows.shape[1] == 12 * 12 + 24 * 2 + 32 * 2        # 3 bits per 3-bit element
+    assert np.array_equal(rows.cpu().numpy(), oracle.pack_act(q, widths))
+    assert np.array_equal(exps.cpu().numpy()[:, :16], e)
+    qu, eu = mxq.unpack_act(rows, exps, fmt, M)
+    assert np.array_equal(qu.cpu().numpy(), q) and np.array_equal(eu.cpu().numpy(), e)
+    qi, ei, pad_ok = decode_act(am.cpu().numpy(), ae.cpu().numpy(), widths, M)
+    assert np.array_equal(qi, q) and np.array_equal(ei, e) and pad_ok
 
 
-def test_weight_pack():
+@pytest.mark.parametrize("clamp", ["sym", "full"])
+def test_weight_pack(clamp):
     _, w, perm, widths = _case(2, 4, 1024, 200, 26, 4, 2)
-    fmt = mxq.Format(1024, widths, torch.from_numpy(perm).cuda())
+    fmt = mxq.Format(1024, widths, torch.from_numpy(perm).cuda(), clamp=clamp)
     wm, we = mxq.pack_weights(to_dev_bf16(w), fmt)
     qu, eu = mxq.unpack_weights(wm, we, fmt, 200)
     torch.cuda.synchronize()
-    q, e = oracle.quantize(w, perm=perm, widths=widths)
-    assert np.array_equal(qu.cpu().numpy()[:200], _doubled(q, 26))
+    q, e = oracle.quantize(w, perm=perm, widths=widths, clamp_mode=1 if clamp == "full" else 0)
+    assert np.array_equal(qu.cpu().numpy()[:200], q)
     assert np.array_equal(eu.cpu().numpy()[:200], e)
+    qd, ed, ok = decode_weights(wm.cpu().numpy(), we.cpu().numpy(), widths, 200,
+                                full=clamp == "full")
+    assert ok and np.array_equal(qd[:200], q) and np.array_equal(ed[:200], e)
+    if clamp == "sym":
+        # 3-bit blocks at 3 bits per element: 26 blocks = 7 steps of 768
+        # bytes per slab of 16 columns
+        steps = [(7, 768), (2, 768), (1, 1024)]
+        assert wm.numel() == 2 * 8 * sum(n * c for n, c in steps)
 
 
 @pytest.mark.parametrize("M", [1, 4, 16, 17, 300])
@@ -73,10 +82,7 @@ def test_gemm(M):
     qa, ea = oracle.quantize(a, perm=perm, widths=widths)
     qw, ew = oracle.quantize(w, perm=perm, widths=widths)
     ref = oracle.gemm(qa, ea, qw, ew, widths)
-    # accumulation bounds of the same values as 4-bit blocks holding 2q
-    w4 = [4 if m == 3 else m for m in widths]
-    check_gemm(y.cpu().numpy(), ref, _doubled(qa, 52).astype(np.int8), ea,
-               _doubled(qw, 52).astype(np.int8), ew, w4, "3-6-8 gemm M=%d" % M)
+    check_gemm(y.cpu().numpy(), ref, qa, ea, qw, ew, widths, "3-6-8 gemm M=%d" % M)
 
 
 def test_template_matches_its_definition_at_the_attention_shape():
@@ -94,9 +100,8 @@ def test_template_matches_its_definition_at_the_attention_shape():
     qa, ea = oracle.quantize(a[rows], perm=perm, widths=widths)
     qw, ew = oracle.quantize(w[cols], perm=perm, widths=widths)
     ref = oracle.gemm(qa, ea, qw, ew, widths)
-    w4 = [4 if m == 3 else m for m in widths]
-    check_gemm(y.cpu().numpy()[np.ix_(rows, cols)], ref, _doubled(qa, 102).astype(np.int8), ea,
-               _doubled(qw, 102).astype(np.int8), ew, w4, "3-6-8 attention shape")
+    check_gemm(y.cpu().numpy()[np.ix_(rows, cols)], ref, qa, ea, qw, ew, widths,
+               "3-6-8 attention shape")
 
 
 @pytest.mark.parametrize("widths", [[3, 3, 3, 3], [3, 3, 6, 8]])
@@ -127,9 +132,7 @@ def test_fused_producers(producer, M):
     torch.cuda.synchronize()
     qa, ea = oracle.quantize(x, perm=perm, widths=widths)
     qw, ew = oracle.quantize(w, perm=perm, widths=widths)
-    assert np.array_equal(mxq.packed_rows(am, fmt, M).cpu().numpy(), oracle.pack_act(qa, widths))
-    assert np.array_equal(mxq.exp_rows(ae, fmt, M).cpu().numpy()[:, :32], ea)
+    qi, ei, pad_ok = decode_act(am.cpu().numpy(), ae.cpu().numpy(), widths, M)
+    assert np.array_equal(qi, qa) and np.array_equal(ei, ea) and pad_ok
     ref = oracle.gemm(qa, ea, qw, ew, widths)
-    w4 = [4 if m == 3 else m for m in widths]
-    check_gemm(y.cpu().numpy(), ref, _doubled(qa, 26).astype(np.int8), ea,
-               _doubled(qw, 26).astype(np.int8), ew, w4, "3-6-8 fused %s" % producer)
+    check_gemm(y.cpu().numpy(), ref, qa, ea, qw, ew, widths, "3-6-8 fused %s" % producer)

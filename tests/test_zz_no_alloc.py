@@ -26,8 +26,8 @@ def _case(seed, B, Hq, Hkv, T, widths):
     say("no-alloc attn seed=%d B=%d Hq=%d Hkv=%d T=%d widths=%s" % (seed, B, Hq, Hkv, T, widths))
     qb, kb, vb = W.attn_inputs(seed, B, Hq, Hkv, T)
     fmt = mxq.Format(D, widths)
-    kc = mxq.quantize_act(to_dev_bf16(kb), fmt)
-    vc = mxq.quantize_act(to_dev_bf16(vb), fmt)
+    kc = mxq.quantize_rows(to_dev_bf16(kb), fmt)
+    vc = mxq.quantize_rows(to_dev_bf16(vb), fmt)
     q = to_dev_bf16(qb.reshape(-1, D)).reshape(B, Hq, D)
     return qb, kb, vb, fmt, kc, vc, q
 
