@@ -38,7 +38,7 @@ typedef unsigned u2 __attribute__((ext_vector_type(2)));
 typedef unsigned u3 __attribute__((ext_vector_type(3)));
 
 constexpr int kFmtE4M3 = 0, kFmtE2M3 = 2, kFmtE3M2 = 3;
-constexpr int kMaxWaves = 16;
+constexpr int kMaxWaves = 8;
 
 // The weights are read exactly once: non-temporal loads stream them past the
 // caches.  Activations stay cached; every workgroup reads them.
@@ -64,7 +64,10 @@ __device__ inline uint32_t scale_plus(uint32_t w) {
 }
 
 __device__ inline v8i six(const uint32_t *d) {
-  return v8i{(int)d[0], (int)d[1], (int)d[2], (int)d[3], (int)d[4], (int)d[5], 0, 0};
+  const u4 a = u4{d[0], d[1], d[2], d[3]};
+  const u2 b = u2{d[4], d[5]};
+  const u4 b4 = __builtin_shufflevector(b, b, 0, 1, -1, -1);
+  return (v8i)__builtin_shufflevector(a, b4, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 // FP8 digit codes of 4 mantissa bytes: the high plane (+-h/512) and the low
@@ -91,7 +94,14 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
   const int nw = blockDim.x >> 6;
   const int grp = lane >> 4, line = lane & 15;
   const LGeo lg(g.n3, g.n4, g.n6, g.n8);
-  const int64_t pair = blockIdx.x;
+  // The four slab pairs of a super-slab run on one XCD (workgroups b, b + 8,
+  // b + 16, b + 24 of a round-robin dispatch), so its L2 reads each step
+  // record of the super-slab and its scale block whole.
+  int64_t pair = blockIdx.x;
+  if ((gridDim.x & 31) == 0) {
+    const int64_t x = pair & 7, i = pair >> 3;
+    pair = (((i >> 2) << 3) + x) * 4 + (i & 3);
+  }
   const int64_t ss = pair >> 2;                      // super-slab
   const int n0 = 2 * (int)(pair & 3);                // first slab of the pair
   const bool two = (pair * 32 + 16) < g.N;           // the second slab has columns
@@ -143,9 +153,9 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
         r.a0 = *(const u4 *)ap;
         r.a1 = *(const u4 *)(ap + 16);
       } else {
-        const u3 av = *(const u3 *)ap, aw = *(const u3 *)(ap + 12);
-        r.a0 = u4{av[0], av[1], av[2], aw[0]};
-        r.a1 = u4{aw[1], aw[2], 0u, 0u};
+        r.a0 = *(const u4 *)ap;
+        const u2 aw = *(const u2 *)(ap + 16);
+        r.a1 = __builtin_shufflevector(aw, aw, 0, 1, -1, -1);
       }
 #pragma unroll
       for (int sl = 0; sl < 2; ++sl) {
@@ -243,7 +253,12 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
       compute(I2(), r2);
       compute(I3(), r3);
     } else if (nst == 4 && SEG == 2) {
-      // 6-bit steps carry half again the bytes: two steps of loads at a time
+      const Raw r0 = load(0), r1 = load(1), r2 = load(2), r3 = load(3);
+      compute(I0(), r0);
+      compute(I1(), r1);
+      compute(I2(), r2);
+      compute(I3(), r3);
+    } else if (nst == 4) {
       const Raw r0 = load(0), r1 = load(1);
       compute(I0(), r0);
       compute(I1(), r1);
