@@ -144,11 +144,12 @@ def peaks(dev, reps: int = 5):
 
 def prefill_issue(meta, M: int, N: int):
     """Matrix-core instructions the prefill GEMM issues (32x32x64, 131072 ops
-    each): per 32x32 output tile, 2 FP6 per 4-bit step (four blocks), 4 FP6
-    per 6-bit step (two blocks) and 2 FP8 per 8-bit step (one block)."""
-    tiles = -(-M // 32) * -(-N // 32)
-    s4, s6, s8 = -(-meta["n4"] // 4), -(-meta["n6"] // 2), meta["n8"]
-    return {"fp6": tiles * (2 * s4 + 4 * s6), "fp8": tiles * 2 * s8, "ops_per_instr": 131072}
+    each): per 32x32 output tile, 2 FP6 per 3/4-bit step (four blocks), 4 FP6
+    per 6-bit step and 4 FP8 per 8-bit step (two blocks each, two digit
+    planes).  Rows are padded to 256 and columns to 128 per workgroup."""
+    tiles = -(-M // 256) * 8 * -(-N // 128) * 4
+    s4, s6, s8 = -(-meta["n4"] // 4), -(-meta["n6"] // 2), -(-meta["n8"] // 2)
+    return {"fp6": tiles * (2 * s4 + 4 * s6), "fp8": tiles * 4 * s8, "ops_per_instr": 131072}
 
 
 def prefill_peak_times_us(meta, M: int, N: int, pk=None):
@@ -472,6 +473,8 @@ def decode_bench(dev, which: str = "up", reps: int = 50):
                           case.meta["n8"], w_bytes / 1e6)
     out["packed_weight_bytes"] = w_bytes
     out["weight_buffer_bytes"] = buf_bytes
+    out["weight_bits_per_element"] = 8.0 * buf_bytes / (case.N * case.K)
+    out["buffer_over_mxint"] = buf_bytes / w_bytes
     return out
 
 
@@ -544,12 +547,17 @@ def attn_bench(dev, reps: int = 50):
 
 
 def template368_bench(dev, case, reps: int = 50):
-    """The attention-projection step with the 3-6-8 template: the same block
-    counts and permutation, 3-bit blocks in place of the 4-bit ones."""
+    """The 3-6-8 template (3-bit blocks in place of the 4-bit ones, the same
+    counts and permutation): the attention-projection step, the bytes of its
+    weights and activation image against the 4-6-8 map's, and the
+    LLaMA-2-70B up-projection decode GEMM at M = 1, whose time follows the
+    weight bytes."""
     import torch
     from paper_2607_17733_amd import mxq
+    from paper_2607_17733_amd import workloads as W
     widths = [3 if m == 4 else int(m) for m in case.widths]
     fmt = mxq.Format(case.K, widths, torch.from_numpy(case.perm).to(dev))
+    fmt4 = mxq.Format(case.K, case.widths, torch.from_numpy(case.perm).to(dev))
     a = bf16_dev(case.a_bits, dev)
     wm, we = mxq.pack_weights(bf16_dev(case.w_bits, dev), fmt)
     am = torch.empty(fmt.act_bytes(case.M), dtype=torch.uint8, device=dev)
@@ -561,12 +569,45 @@ def template368_bench(dev, case, reps: int = 50):
         mxq.gemm(am, ae, wm, we, fmt, case.M, case.N, out=y)
     ms = burst_ms(step, reps, 10)
     ops = 2.0 * case.M * case.N * case.K
-    return {"ms_per_step": ms, "TOPs": ops / (ms * 1e-3) / 1e12,
-            "widths": [case.meta["n4"], case.meta["n6"], case.meta["n8"]],
-            "workload": "attention projection M=%d K=%d N=%d, 3-bit/6-bit/8-bit blocks "
-                        "%d/%d/%d (3-bit blocks stored as 4-bit blocks holding 2q)" % (
-                            case.M, case.K, case.N, case.meta["n4"], case.meta["n6"],
-                            case.meta["n8"])}
+    nk = case.N * case.K
+    out = {"ms_per_step": ms, "TOPs": ops / (ms * 1e-3) / 1e12,
+           "widths": [case.meta["n4"], case.meta["n6"], case.meta["n8"]],
+           "weight_bits_per_element": 8.0 * (fmt.weight_bytes(case.N) +
+                                             fmt.weight_exp_bytes(case.N)) / nk,
+           "weight_bits_per_element_468": 8.0 * (fmt4.weight_bytes(case.N) +
+                                                 fmt4.weight_exp_bytes(case.N)) / nk,
+           "activation_image_bytes": fmt.act_bytes(case.M) + fmt.act_exp_bytes(case.M),
+           "activation_image_bytes_468": fmt4.act_bytes(case.M) + fmt4.act_exp_bytes(case.M),
+           "workload": "attention projection M=%d K=%d N=%d, 3-bit/6-bit/8-bit blocks "
+                       "%d/%d/%d (3 bits per element in the weights)" % (
+                           case.M, case.K, case.N, case.meta["n4"], case.meta["n6"],
+                           case.meta["n8"])}
+    # decode: the up projection with its 4-bit blocks made 3-bit
+    dc = W.decode(1, "up")
+    rec = {}
+    for tag, ws in (("368", [3 if m == 4 else int(m) for m in dc.widths]),
+                    ("468", [int(m) for m in dc.widths])):
+        f = mxq.Format(dc.K, ws, torch.from_numpy(dc.perm).to(dev))
+        w0 = mxq.pack_weights(bf16_dev(dc.w_bits, dev), f)
+        copies = [w0] + [(w0[0].clone(), w0[1].clone()) for _ in range(3)]
+        xa, xe = mxq.quantize_act(bf16_dev(dc.a_bits[:1], dev), f)
+        yd = torch.empty((1, dc.N), dtype=torch.float32, device=dev)
+        it = [0]
+
+        def dstep():
+            wmc, wec = copies[it[0] % 4]
+            it[0] += 1
+            mxq.gemm(xa, xe, wmc, wec, f, 1, dc.N, out=yd)
+        dms = burst_ms(dstep, 40, 8)
+        nbytes = copies[0][0].numel() + copies[0][1].numel()
+        rec[tag] = {"us": dms * 1e3, "weight_buffer_bytes": nbytes,
+                    "GBps": nbytes / (dms * 1e-3) / 1e9}
+        del copies, w0
+    rec["workload"] = ("LLaMA-2-70B up-projection decode, M=1, K=%d N=%d, blocks %d/%d/%d "
+                       "(3- or 4-bit / 6-bit / 8-bit), 4 weight buffers rotated" % (
+                           dc.K, dc.N, dc.meta["n4"], dc.meta["n6"], dc.meta["n8"]))
+    out["decode_up_M1"] = rec
+    return out
 
 
 def layer_bench(dev, sensitive: bool, reps: int = 5):
@@ -734,13 +775,10 @@ def main():
             "kernel": "gemm_prefill (mxq_gemm, M > 16)",
             "bound": "mfma",
             "achieved": gemm_tops,
-            "peak": INT8_PEAK_TOPS,
             "unit": "TOP/s",
-            "frac": gemm_tops / INT8_PEAK_TOPS,
             "traffic": measured_traffic(),
-            "algorithmic": "2*M*N*K = %.4g ops per launch (MXINT multiply-adds, "
-                           "against the dense int8 peak)" % ops,
             "avg_launch_us": gemm_ms * 1e3,
+            "frac_int8_peak": gemm_tops / INT8_PEAK_TOPS,
         },
         "gemm_only_tops": gemm_tops,
         "quantize": {"us": quant_ms * 1e3,
@@ -756,15 +794,21 @@ def main():
         result["peaks"] = pk
     t = prefill_peak_times_us(case.meta, M, N, pk)
     gemm_us = gemm_ms * 1e3
-    result["roofline"]["frac_dtype_peak"] = t["dtype_us"] / gemm_us
+    # the contraction's own dtypes: 4- and 6-bit blocks run FP6, 8-bit blocks
+    # FP8, so the peak is the blend of their datasheet peaks over this width map
+    blended = ops / (t["dtype_us"] * 1e-6) / 1e12
+    result["roofline"]["peak"] = blended
+    result["roofline"]["frac"] = gemm_tops / blended
     result["roofline"]["frac_issued_peak"] = t["issued_us"] / gemm_us
-    result["roofline"]["dtype_peak_note"] = (
-        "frac = algorithmic ops against the dense int8 peak; frac_dtype_peak = the "
-        "time the algorithmic ops of each block take at the datasheet peak of the "
-        "dtype that block runs on (FP6 10.1 PF for 4- and 6-bit blocks, FP8 5.0 PF for "
-        "8-bit blocks), %.2f us, over the launch time; frac_issued_peak = the "
-        "instructions actually issued (digit products included) at those peaks, "
-        "%.2f us, over the launch time" % (t["dtype_us"], t["issued_us"]))
+    result["roofline"]["algorithmic"] = (
+        "2*M*N*K = %.4g ops per launch (MXINT multiply-adds); peak = the same ops "
+        "at the datasheet peak of the dtype each block runs on (FP6 10.1 POP/s for "
+        "the %d 4-bit and %d 6-bit blocks, FP8 5.0 POP/s for the %d 8-bit blocks), "
+        "%.2f us; frac_int8_peak prices them at the dense int8 peak (5.0 POP/s); "
+        "frac_issued_peak = the instructions actually issued (digit products "
+        "included) at their dtype peaks, %.2f us, over the launch time" % (
+            ops, case.meta["n4"], case.meta["n6"], case.meta["n8"], t["dtype_us"],
+            t["issued_us"]))
     if pk is not None:
         result["roofline"]["achievable"] = {
             "int8_loop_TOPs": pk["mfma_int8_TOPs"],
