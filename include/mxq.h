@@ -109,7 +109,13 @@ const char *mxq_status_str(int status);
 
 /*
  * Sizes (bytes) of the buffers; negative mxq_status on a bad format or a
- * negative count.
+ * negative count.  The algorithmic size of a quantized row is Section 2's
+ * MXINT storage: m bits per element of an m-bit block plus one 8-bit shared
+ * exponent per 32-element block (the 0.25 bits per element that Section 5.1
+ * adds to the average bitwidth).  The packed rows (C) hold exactly that,
+ * rounded up to 16 bytes, and the symmetric-clamp weights (B) within a few
+ * percent; the operand image (A) holds matrix-core digits instead (6 or 8
+ * bits per element and digit plane).
  *
  * Steps and lanes (shared by the GEMM layouts below).  The K-blocks of a
  * width map form four segments in order: the 3-bit, 4-bit, 6-bit and 8-bit
