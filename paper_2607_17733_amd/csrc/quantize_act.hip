@@ -106,23 +106,58 @@ __device__ inline void pack3(const Blk &v, uint32_t *w) {
   }
 }
 
+// a[s] for a per-thread segment index s, as selects: indexing a register
+// array with a thread's value would place the array in scratch memory.
+__device__ inline int pick4(const int (&a)[kSegs], int s) {
+  return s == 0 ? a[0] : s == 1 ? a[1] : s == 2 ? a[2] : a[3];
+}
+
+// Where padded block bp of a row goes: its segment, step, position in the
+// step, its block of the width map, and the step's offset in a 16-row tile
+// of the operand image and its scale group and byte.
+struct ItemGeo {
+  int s, rem, st, pos, b, k;
+  bool pad;
+  int step_off, group, byte;
+};
+__device__ inline ItemGeo item_geo(const LGeo &lg, int bp) {
+  ItemGeo g;
+  const int p0 = 4 * lg.S[0], p1 = p0 + 4 * lg.S[1], p2 = p1 + 2 * lg.S[2];
+  g.s = (bp >= p0) + (bp >= p1) + (bp >= p2);
+  g.rem = bp - (g.s == 0 ? 0 : g.s == 1 ? p0 : g.s == 2 ? p1 : p2);
+  const int two = g.s < 2 ? 2 : 1;                   // log2 blocks per step
+  g.k = g.rem >> two;
+  g.pos = g.rem & ((1 << two) - 1);
+  g.st = pick4(lg.st0, g.s) + g.k;
+  g.pad = g.rem >= pick4(lg.nb, g.s);
+  g.b = pick4(lg.b0, g.s) + g.rem;
+  const int sb = kLanes * a_lane_bytes(0);           // 3/4/6-bit step bytes
+  const int before = g.s == 0 ? 0 : g.s == 1 ? lg.S[0] : g.s == 2 ? lg.S[0] + lg.S[1]
+                                                                  : lg.S[0] + lg.S[1] + lg.S[2];
+  g.step_off = before * sb + g.k * (g.s == 3 ? kLanes * a_lane_bytes(3) : sb);
+  g.group = pick4(lg.G0, g.s) + (g.k >> 2);
+  g.byte = g.k & (kGroupSteps - 1);
+  return g;
+}
+
+// The 32 permutation entries of padded block bp (undefined for padding
+// blocks, which gather nothing).
+__device__ inline void load_perm(const QuantArgs &q, const ItemGeo &g, int4 (&pe)[8]) {
+  if (!q.perm || g.pad) return;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) pe[u] = *(const int4 *)(q.perm + g.b * kBlock + 4 * u);
+}
+
 // One (row, padded block) item: gather, quantize, write the canonical
 // packed row and exponent (q.write_rows) and / or the GEMM operand image
 // and its scale words (q.write_image).  sr is the staged row in LDS,
-// followed by zero padding.
+// followed by zero padding; pe holds the block's permutation entries.
 template <bool RNA>
-__device__ inline void quantize_item(const QuantArgs &q, const LGeo &lg, int bp, int64_t row,
-                                     const uint8_t *sr) {
+__device__ inline void quantize_item(const QuantArgs &q, const LGeo &lg, const ItemGeo &g,
+                                     const int4 (&pe)[8], int64_t row, const uint8_t *sr) {
   const int K = (int)q.K;
-  int s = 0, rem = bp;
-  while (s < kSegs - 1 && rem >= lg.S[s] * (s < 2 ? 4 : 2)) {
-    rem -= lg.S[s] * (s < 2 ? 4 : 2);
-    ++s;
-  }
-  const int per = s < 2 ? 4 : 2;
-  const int st = lg.st0[s] + rem / per, pos = rem % per;
-  const bool pad = rem >= lg.nb[s];
-  const int b = lg.b0[s] + rem;
+  const int s = g.s, rem = g.rem, pos = g.pos, b = g.b;
+  const bool pad = g.pad;
   const int m = s == 0 ? 3 : s == 1 ? 4 : s == 2 ? 6 : 8;
 
   // gather: pr[i] holds elements 2i (low half) and 2i+1 (high half)
@@ -141,14 +176,14 @@ __device__ inline void quantize_item(const QuantArgs &q, const LGeo &lg, int bp,
   } else {
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int4 p = *(const int4 *)(q.perm + p0 + 4 * u);
-      const int src[4] = {p.x, p.y, p.z, p.w};
-      uint32_t e[4];
-#pragma unroll
-      for (int k = 0; k < 4; ++k)   // out of range: the zero after the row
-        e[k] = *(const uint16_t *)(sr + 2 * min((unsigned)src[k], (unsigned)K));
-      pr[2 * u] = e[0] | (e[1] << 16);
-      pr[2 * u + 1] = e[2] | (e[3] << 16);
+      const int4 p = pe[u];
+      // out of range: the zero after the row
+      const uint32_t e0 = *(const uint16_t *)(sr + 2 * min((unsigned)p.x, (unsigned)K));
+      const uint32_t e1 = *(const uint16_t *)(sr + 2 * min((unsigned)p.y, (unsigned)K));
+      const uint32_t e2 = *(const uint16_t *)(sr + 2 * min((unsigned)p.z, (unsigned)K));
+      const uint32_t e3 = *(const uint16_t *)(sr + 2 * min((unsigned)p.w, (unsigned)K));
+      pr[2 * u] = e0 | (e1 << 16);
+      pr[2 * u + 1] = e2 | (e3 << 16);
     }
   }
 
@@ -214,9 +249,8 @@ __device__ inline void quantize_item(const QuantArgs &q, const LGeo &lg, int bp,
 
   // operand image (16-row tiles) and its scale words
   const int r = (int)(row & (kATileRows - 1));
-  uint8_t *stp = q.img + (row >> 4) * q.a_tile + a_step_off(lg, st);
-  uint8_t *scw = q.img_exp + (row >> 4) * q.a_tile_sc + (int64_t)lg.group_of(st) * 256 +
-                 lg.byte_of(st);
+  uint8_t *stp = q.img + (row >> 4) * q.a_tile + g.step_off;
+  uint8_t *scw = q.img_exp + (row >> 4) * q.a_tile_sc + g.group * 256 + g.byte;
   if (s <= 1) {
     // E3M2 codes of q (4-bit) or of 2q (3-bit)
     if (s == 0) {
@@ -266,10 +300,10 @@ __device__ inline void quantize_item(const QuantArgs &q, const LGeo &lg, int bp,
   }
   // the unused scale bytes of a segment's short last group
   if (rem == 0) {
-    const int S = lg.S[s];
+    const int S = pick4(lg.S, s), G0 = pick4(lg.G0, s);
     for (int k = S; k < (S + kGroupSteps - 1) / kGroupSteps * kGroupSteps; ++k) {
       uint8_t *z = q.img_exp + (row >> 4) * q.a_tile_sc +
-                   (int64_t)(lg.G0[s] + k / kGroupSteps) * 256 + k % kGroupSteps;
+                   (int64_t)(G0 + k / kGroupSteps) * 256 + k % kGroupSteps;
       for (int g = 0; g < 4; ++g) z[4 * (16 * g + r)] = 0;
     }
   }
@@ -408,6 +442,16 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
   if ((nwg & 7) == 0) w = (w & 7) * (nwg >> 3) + (w >> 3);
   const int64_t r0 = w << lgR;
 
+  // The first item's geometry and permutation entries, loaded while the
+  // rows are staged.
+  const int nit = nbp << lgR;
+  int4 pe[8];
+  ItemGeo g0{};
+  if (t < nit) {
+    g0 = item_geo(lg, t >> lgR);
+    load_perm(q, g0, pe);
+  }
+
   // Stage the rows.  Each thread issues a batch of loads before it stores
   // any of them, so the batch costs one memory latency instead of one per
   // load.
@@ -458,12 +502,14 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
   __syncthreads();
   if (q.rmsnorm) rms_normalise(q, smem, R, rowB, t, nthr, r0);
 
-  for (int it = t; it < (nbp << lgR); it += nthr) {
-    const int bp = it >> lgR;
+  for (int it = t; it < nit; it += nthr) {
     const int lr = it & (R - 1);
     const int64_t row = r0 + lr;
-    if (row < q.out_rows)
-      quantize_item<RNA>(q, lg, bp, row, smem + lr * rowB);
+    if (it != t) {
+      g0 = item_geo(lg, it >> lgR);
+      load_perm(q, g0, pe);
+    }
+    if (row < q.out_rows) quantize_item<RNA>(q, lg, g0, pe, row, smem + lr * rowB);
   }
   // zero the padding of the packed and exponent rows
   if (q.write_rows && t < R) {
