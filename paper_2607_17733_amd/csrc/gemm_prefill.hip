@@ -31,14 +31,18 @@
 // w owns rows 64w..64w+63 x all 128 columns = 2x4 tiles of 32x32 fp32
 // accumulators, and walks every step.
 //   - activations go straight from the image into registers -- each row is
-//     used by exactly one wave -- one step ahead, in two register sets, with
-//     the step's weight scale bytes;
+//     used by exactly one wave -- one step ahead, in two register sets;
+//   - the scale words (activation and weight) are loaded once per group of
+//     four steps, a group ahead;
 //   - the weight chunk of each step (8 slabs, 6 to 12 KB) goes global -> LDS
 //     by direct-to-LDS loads into a ring of eight step stages, four steps
-//     ahead; the four waves read it per column tile and K-chunk, one
-//     (tile, chunk) ahead of the products.
-// One barrier per step; the kernel counts its own loads (vmcnt) to know
-// when a stage is complete.  Workgroup ids are remapped so that each XCD owns
+//     ahead; the four waves read it per column tile and K-chunk, two
+//     (tile, chunk) positions ahead of the products, and restore each
+//     operand between the two halves of the previous position's products
+//     into alternating registers.
+// A step has no branch, so the compiler keeps this order.  One barrier per
+// step; the kernel counts its own loads (vmcnt) to know when a stage is
+// complete.  Workgroup ids are remapped so that each XCD owns
 // a compact block of output tiles: the activation rows and weight columns it
 // reads stay in its L2.
 #include "mxq_device.h"
@@ -63,7 +67,11 @@ constexpr int kASets = 2;                    // activation register sets (one ah
 // Loads per wave and step besides the weights: per 32-row tile and K-chunk
 // the lane data (two loads) and the scale word, then the step's weight
 // scale bytes (two).
-constexpr int kALoads = 2 * 2 * (2 + 1) + 2;
+constexpr int kALoads = 2 * 2 * 2;
+// Loads per wave and scale group: the activation scale word per 32-row tile
+// and K-chunk, then the group's weight scale bytes (two 16-byte pieces per
+// K-chunk).
+constexpr int kGLoads = 2 * 2 + 2 * 2;
 
 template <int S> struct Int { static constexpr int v = S; };
 
@@ -187,7 +195,8 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   const int64_t last = (g.M - 1) / kATileRows;
   const int64_t ta = min(row0 / kATileRows + 4 * wave, last);
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)(g.a_mant + ta * g.a_tile), 0, 0x7fffffff, 0x00020000);
+      (void *)(g.a_mant + ta * g.a_tile), 0,
+      (int)min((last + 1 - ta) * g.a_tile, (int64_t)0x7fffffff), 0x00020000);
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
       (void *)(g.a_exp + ta * g.a_tile_sc), 0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
@@ -212,10 +221,17 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   // step's weight scale bytes for each K-chunk (slab n at byte n).
   struct ASet {
     v8i d[2][2];
-    uint32_t sc[2][2];
-    u2 ws[2];
   };
   ASet xa[kASets];
+  // Scale words of a group of four steps: per 32-row tile and K-chunk the
+  // activation scale dword (byte k for step k), per K-chunk the lane's 32
+  // weight scale bytes (slab n's byte of step k at 8 k + n).  Set 0 serves
+  // the current group; set 1 receives the next group's.
+  struct GScale {
+    uint32_t sc[2][2];
+    u4 ws[2][2];
+  };
+  GScale gsc[2];
 
   // Offsets of step st in the images, its scale group and its byte, in
   // branch-free scalar arithmetic (a segment's steps before st are
@@ -224,13 +240,6 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
                 CB2 = w_chunk_bytes(2, FULL), CB3 = w_chunk_bytes(3, FULL);
   auto dseg = [&](int st, int k) __attribute__((always_inline)) {
     return min(max(st - lg.st0[k], 0), lg.S[k]);
-  };
-  auto seg_start = [&](int st) __attribute__((always_inline)) {
-    int ss = 0;
-    ss = st >= lg.st0[1] ? lg.st0[1] : ss;
-    ss = st >= lg.st0[2] ? lg.st0[2] : ss;
-    ss = st >= lg.st0[3] ? lg.st0[3] : ss;
-    return ss;
   };
   auto a_off = [&](int st) __attribute__((always_inline)) {
     // 24-byte lanes before the 8-bit segment, 32-byte lanes in it
@@ -253,10 +262,6 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
            ((dseg(st, 1) + (st >= lg.st0[2] ? 3 : 0)) >> 2) +
            ((dseg(st, 2) + (st >= lg.st0[3] ? 3 : 0)) >> 2) + (max(st - lg.st0[3], 0) >> 2);
   };
-  auto s_byte = [&](int st) __attribute__((always_inline)) { return (st - seg_start(st)) & 3; };
-  auto seg_of = [&](int st) __attribute__((always_inline)) {
-    return (st >= lg.st0[1] ? 1 : 0) + (st >= lg.st0[2] ? 1 : 0) + (st >= lg.st0[3] ? 1 : 0);
-  };
 
   // Weight loads of step st (clamped to the last) into its stage: pieces
   // n = 0 .. kPieces - 1 of 1 KB (pieces past the step's chunk bytes repeat
@@ -278,52 +283,63 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
     st = min(st, nsteps - 1);
     const int so = a_off(st);
     const bool wide = st >= lg.st0[3];
-    const int sgrp = s_grp(st);
 #pragma unroll
     for (int tm = 0; tm < 2; ++tm)
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
         const int lk = c ? lk1 : lk0;
         const int vb = vt[tm] * (int)g.a_tile;
-        u4 lo, hi;
-        if (wide) {
-          // chunk c = block c of the step: the high digits of the lane's 16
-          // elements (lane group lh, bytes 16 c) as K-block 0, their low
-          // digits (lane group 2 + lh) as K-block 1
-          lo = __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(
-                                          ra, vb + 32 * lk0 + 16 * c, so, 0));
-          hi = __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(
-                                          ra, vb + 32 * lk1 + 16 * c, so, 0));
-        } else {
-          lo = __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(ra, vb + 24 * lk, so, 0));
-          const u2 q = __builtin_bit_cast(
-              u2, __builtin_amdgcn_raw_buffer_load_b64(ra, vb + 24 * lk + 16, so, 0));
-          // the FP6 operand is six dwords: the last two stay undefined (no
-          // write, so no wait for an earlier load into those registers)
-          hi = __builtin_shufflevector(q, q, 0, 1, -1, -1);
-        }
+        // FP8 steps: chunk c = block c of the step: the high digits of the
+        // lane's 16 elements (lane group lh, bytes 16 c) as K-block 0, their
+        // low digits (lane group 2 + lh) as K-block 1.  FP6 steps: the lane's
+        // 24 bytes (the second load's last 8 bytes are not used; past the
+        // image they read zero).  The same two loads either way, so the
+        // step has no branch.
+        const int olo = wide ? 32 * lk0 + 16 * c : 24 * lk;
+        const int ohi = wide ? 32 * lk1 + 16 * c : 24 * lk + 16;
+        const u4 lo = __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(ra, vb + olo, so, 0));
+        const u4 hi = __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(ra, vb + ohi, so, 0));
         xa[S].d[tm][c] = (v8i)__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        xa[S].sc[tm][c] = __builtin_amdgcn_raw_buffer_load_b32(
-            rs, vt[tm] * (int)g.a_tile_sc + 4 * lk, sgrp * 256, 0);
       }
-    const int sb = sgrp * 2048 + 8 * s_byte(st);
+  };
+  // Scale loads of group grp (clamped to the last) into set G.
+  auto issue_g = [&](auto gset_tag, int grp) __attribute__((always_inline)) {
+    constexpr int G = decltype(gset_tag)::v;
+    grp = min(grp, lg.ngroups - 1);
+#pragma unroll
+    for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        gsc[G].sc[tm][c] = __builtin_amdgcn_raw_buffer_load_b32(
+            rs, vt[tm] * (int)g.a_tile_sc + 4 * (c ? lk1 : lk0), grp * 256, 0);
 #pragma unroll
     for (int c = 0; c < 2; ++c)
-      xa[S].ws[c] = __builtin_bit_cast(
-          u2, __builtin_amdgcn_raw_buffer_load_b64(rws, 32 * (c ? lk1 : lk0), sb, 0));
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        gsc[G].ws[c][h] = __builtin_bit_cast(
+            u4, __builtin_amdgcn_raw_buffer_load_b128(rws, 32 * (c ? lk1 : lk0) + 16 * h,
+                                                      grp * 2048, 0));
   };
 
-  // Weight operand of column tile tn, K-chunk c: the raw bytes of the lane
-  // (two (tile, chunk) pairs in flight), restored to FP6 / FP8 codes at use.
+  // Weight operand of column tile tn, K-chunk c (position p = 2 tn + c of
+  // a step): the lane's raw bytes, read from LDS two positions ahead into
+  // one of four slots, and its FP6 / FP8 codes, restored one position ahead
+  // into one of two operand registers, so that a restore never writes the
+  // registers the products in flight read.
   struct WRaw {
     u4 p, h;
     u2 q;
     uint32_t z;
   };
-  WRaw w[2];
-  auto read_w = [&](auto seg, const char *stage, int o, int tn, int c) __attribute__((always_inline)) {
+  struct WOp {
+    v8i b0, b1;                   // 3/4-bit: b0; 6/8-bit: high plane b0, low plane b1
+  };
+  WRaw w[4];
+  WOp bo[2];
+  auto read_w = [&](auto seg, const char *stage, int o, int p) __attribute__((always_inline)) {
     constexpr int SEG = decltype(seg)::v;
     constexpr int CB = w_chunk_bytes(SEG, FULL);
+    const int tn = p >> 1, c = p & 1;
     const char *ch = stage + (2 * tn + hx) * CB;
     const int lk = c ? lk1 : lk0;
     WRaw &r = w[o];
@@ -342,104 +358,118 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
       r.p = *(const u4 *)(ch + 32 * (16 * c + l16) + 16 * lh);
     }
   };
+  auto restore = [&](auto seg, int o, int ob) __attribute__((always_inline)) {
+    constexpr int SEG = decltype(seg)::v;
+    const WRaw &r = w[o];
+    WOp &B = bo[ob];
+    if (SEG <= 1) {
+      uint32_t d[6];
+      if (SEG == 0 && !FULL) {
+        const uint32_t f[3] = {r.q[0], r.q[1], r.z};
+        unfold3(f, d);
+      } else if (SEG == 1 && FULL) {
+        d[0] = r.p[0]; d[1] = r.p[1]; d[2] = r.p[2]; d[3] = r.p[3]; d[4] = r.q[0]; d[5] = r.q[1];
+      } else {
+        const uint32_t f[4] = {r.p[0], r.p[1], r.p[2], r.p[3]};
+        unfold4(f, d);
+      }
+      B.b0 = six(d);
+    } else if (SEG == 2) {
+      const uint32_t fl[4] = {r.p[0], r.p[1], r.p[2], r.p[3]};
+      uint32_t L[6], H[6];
+      unfold4(fl, L);
+      if (FULL) {
+        const uint32_t fh[4] = {r.h[0], r.h[1], r.h[2], r.h[3]};
+        unfold4(fh, H);
+      } else {
+        const uint32_t fh[2] = {r.q[0], r.q[1]};
+        unfold2(fh, L, H);
+      }
+      B.b0 = six(H);
+      B.b1 = six(L);
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        B.b0[k] = B.b0[4 + k] = (int)hi_codes<FULL>(r.p[k]);
+        B.b1[k] = B.b1[4 + k] = (int)lo_codes<FULL>(r.p[k]);
+      }
+    }
+  };
+  // The products of position p with operand register ob, first or second
+  // half: 3/4-bit: row tile 0 | 1; 6-bit: the weights' high plane in both K
+  // halves (scale E + 3) for both row tiles | their low plane (scale E);
+  // 8-bit: the high digits (scale E + 4) | the low digits.
+  auto products = [&](auto seg, const ASet &x, const uint32_t (&sa)[2][2], int k, int p, int ob,
+                      int half) __attribute__((always_inline)) {
+    constexpr int SEG = decltype(seg)::v;
+    const int tn = p >> 1, c = p & 1;
+    const int n = 2 * tn + hx;               // the lane's slab
+    // byte 8 k + n of the lane's 32 weight scale bytes
+    const uint32_t wd = gsc[0].ws[c][k >> 1][2 * (k & 1) + (n >> 2)];
+    const uint32_t e = (wd >> (8 * (n & 3))) & 0xFFu;
+    const WOp &B = bo[ob];
+    if (SEG <= 1) {
+      constexpr int FB = SEG == 0 ? kFmtE2M3 : kFmtE3M2;
+      const int tm = half;
+      acc[tm][tn] = mma<kFmtE3M2, FB>(x.d[tm][c], B.b0, acc[tm][tn], sa[tm][c], e);
+    } else if (SEG == 2) {
+#pragma unroll
+      for (int tm = 0; tm < 2; ++tm)
+        acc[tm][tn] = half == 0
+            ? mma<kFmtE3M2, kFmtE3M2>(x.d[tm][c], B.b0, acc[tm][tn], sa[tm][c], sat_plus<3>(e))
+            : mma<kFmtE3M2, kFmtE3M2>(x.d[tm][c], B.b1, acc[tm][tn], sa[tm][c], e);
+    } else {
+#pragma unroll
+      for (int tm = 0; tm < 2; ++tm)
+        acc[tm][tn] = half == 0
+            ? mma<kFmtE4M3, kFmtE4M3>(x.d[tm][c], B.b0, acc[tm][tn], sa[tm][c], sat_plus<4>(e))
+            : mma<kFmtE4M3, kFmtE4M3>(x.d[tm][c], B.b1, acc[tm][tn], sa[tm][c], e);
+    }
+  };
 
-  // Step s (register set S = s % 2): the products, column tile by column
-  // tile and K-chunk by K-chunk, each weight operand read one (tile, chunk)
-  // ahead.  At tile 0 the step issues the activation loads of step s + 1;
-  // between tiles 1 and 2 the workgroup meets at a barrier, then the step
-  // issues the weight loads of step s + 4.  Before the barrier each wave
-  // waits for its own weight loads of step s + 1: since them it has issued
-  // at most the activations of s - 1, s and s + 1 and the weights of s + 2
-  // and s + 3, and the activations of s - 1 were consumed by step s - 1, so
-  // at most two activation and two weight bundles may still be in flight
-  // (this also holds in the first steps, after the prologue).  After the
-  // barrier the stage of s + 1 is complete, so its first chunk is read
-  // during the last tile, and every wave is past step s - 1, whose stage
-  // ((s + 4) % 8 = (s - 4) % 8 is older still) the weight loads of s + 4
-  // may then overwrite.
-  auto step = [&](auto seg, auto set_tag, int s) __attribute__((always_inline)) {
-    constexpr int SEG = decltype(seg)::v, S = decltype(set_tag)::v;
+  // Step s (register set S = s % 2): the products position by position.  At
+  // position p the step reads the raw operand of p + 2 (positions 8 and 9
+  // are the next step's first two, read after the barrier), issues the
+  // first half of p's products, restores the operand of p + 1, then issues
+  // the second half.  At position 0 the step issues the activation loads of
+  // step s + 1; between positions 3 and 4 the workgroup meets at a barrier,
+  // then the step issues the weight loads of step s + 4.  Before the
+  // barrier each wave waits for its own weight loads of step s + 1: since
+  // them it has issued at most the activations of s - 1, s and s + 1 and the
+  // weights of s + 2 and s + 3, and the activations of s - 1 were consumed
+  // by step s - 1, so at most two activation and two weight bundles may
+  // still be in flight (this also holds in the first steps, after the
+  // prologue).  After the barrier the stage of s + 1 is complete, and every
+  // wave is past step s - 1, whose stage ((s + 4) % 8 = (s - 4) % 8 is older
+  // still) the weight loads of s + 4 may then overwrite.
+  auto step = [&](auto seg, auto set_tag, auto k_tag, int s, int grp) __attribute__((always_inline)) {
+    constexpr int S = decltype(set_tag)::v, K = decltype(k_tag)::v;
     const char *W = ring + (s % kWStages) * C::kStage;
+    const char *Wn = ring + ((s + 1) % kWStages) * C::kStage;
     const ASet &x = xa[S];
-    const int kb = (s - lg.st0[SEG]) & 3;
     uint32_t sa[2][2];
 #pragma unroll
     for (int tm = 0; tm < 2; ++tm)
 #pragma unroll
-      for (int c = 0; c < 2; ++c) sa[tm][c] = (x.sc[tm][c] >> (8 * kb)) & 0xFFu;
+      for (int c = 0; c < 2; ++c) sa[tm][c] = (gsc[0].sc[tm][c] >> (8 * K)) & 0xFFu;
 #pragma unroll
-    for (int tc = 0; tc < 8; ++tc) {
-      const int tn = tc >> 1, c = tc & 1, o = tc & 1;
-      if (tc == 4) {
+    for (int p = 0; p < 8; ++p) {
+      if (p == 4) {
         wait_loads<2 * kALoads + 2 * C::kWLoads>();
         barrier();
         issue_w(s + kWAhead);
       }
-      if (tc < 7) {
-        read_w(seg, W, o ^ 1, (tc + 1) >> 1, (tc + 1) & 1);
-      } else if (s + 1 < nsteps && seg_of(s + 1) == SEG) {
-        read_w(seg, ring + ((s + 1) % kWStages) * C::kStage, 0, 0, 0);
-      }
-      if (tc == 0) issue_a(Int<(S + 1) % kASets>{}, s + 1);
-      const int n = 2 * tn + hx;             // the lane's slab
-      const uint32_t e = (x.ws[c][n >> 2] >> (8 * (n & 3))) & 0xFFu;
-      const WRaw &r = w[o];
-      if (SEG <= 1) {
-        uint32_t d[6];
-        if (SEG == 0 && !FULL) {
-          const uint32_t f[3] = {r.q[0], r.q[1], r.z};
-          unfold3(f, d);
-        } else if (SEG == 1 && FULL) {
-          d[0] = r.p[0]; d[1] = r.p[1]; d[2] = r.p[2]; d[3] = r.p[3]; d[4] = r.q[0]; d[5] = r.q[1];
-        } else {
-          const uint32_t f[4] = {r.p[0], r.p[1], r.p[2], r.p[3]};
-          unfold4(f, d);
-        }
-        constexpr int FB = SEG == 0 ? kFmtE2M3 : kFmtE3M2;
-        const v8i b = six(d);
-#pragma unroll
-        for (int tm = 0; tm < 2; ++tm)
-          acc[tm][tn] = mma<kFmtE3M2, FB>(x.d[tm][c], b, acc[tm][tn], sa[tm][c], e);
-      } else if (SEG == 2) {
-        // the block's digit planes are the K halves of both operands: the
-        // weights' high plane in both halves (scale E + 3) gives hh and lh,
-        // their low plane (scale E) hl and ll
-        const uint32_t fl[4] = {r.p[0], r.p[1], r.p[2], r.p[3]};
-        uint32_t L[6], H[6];
-        unfold4(fl, L);
-        if (FULL) {
-          const uint32_t fh[4] = {r.h[0], r.h[1], r.h[2], r.h[3]};
-          unfold4(fh, H);
-        } else {
-          const uint32_t fh[2] = {r.q[0], r.q[1]};
-          unfold2(fh, L, H);
-        }
-        const v8i bh = six(H);
-#pragma unroll
-        for (int tm = 0; tm < 2; ++tm)
-          acc[tm][tn] = mma<kFmtE3M2, kFmtE3M2>(x.d[tm][c], bh, acc[tm][tn], sa[tm][c],
-                                                sat_plus<3>(e));
-        const v8i bl = six(L);
-#pragma unroll
-        for (int tm = 0; tm < 2; ++tm)
-          acc[tm][tn] = mma<kFmtE3M2, kFmtE3M2>(x.d[tm][c], bl, acc[tm][tn], sa[tm][c], e);
-      } else {
-        // the weights' high digits in both K halves (scale E + 4), then
-        // their low digits (scale E)
-        v8i bh, bl;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          bh[k] = bh[4 + k] = (int)hi_codes<FULL>(r.p[k]);
-          bl[k] = bl[4 + k] = (int)lo_codes<FULL>(r.p[k]);
-        }
-#pragma unroll
-        for (int tm = 0; tm < 2; ++tm)
-          acc[tm][tn] = mma<kFmtE4M3, kFmtE4M3>(x.d[tm][c], bh, acc[tm][tn], sa[tm][c],
-                                                sat_plus<4>(e));
-#pragma unroll
-        for (int tm = 0; tm < 2; ++tm)
-          acc[tm][tn] = mma<kFmtE4M3, kFmtE4M3>(x.d[tm][c], bl, acc[tm][tn], sa[tm][c], e);
-      }
+      // positions 8 and 9: the next step's (unused when that step starts a
+      // new segment, whose loop reads them again)
+      if (p + 2 < 8) read_w(seg, W, (p + 2) & 3, p + 2);
+      else read_w(seg, Wn, (p + 2) & 3, p - 6);
+      if (p == 0) issue_a(Int<(S + 1) % kASets>{}, s + 1);
+      if (p == 0 && K == 0) issue_g(Int<1>{}, grp + 1);
+      products(seg, x, sa, K, p, p & 1, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      restore(seg, (p + 1) & 3, (p + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
+      products(seg, x, sa, K, p, p & 1, 1);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -448,22 +478,34 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   // in a loop with one exit, then a last odd step.  `cur` is the set that
   // holds the next step's activations; a segment that starts with them in
   // set 1 first copies them to set 0 (at most three times per kernel).  The
-  // first step reads its own first weight chunk (the previous segment's
-  // last step does not).
+  // first step reads its own first two raw operands and restores the first.
   int cur = 0;
   auto run = [&](auto seg, int sb, int se) __attribute__((always_inline)) {
     if (sb >= se) return;
     if (cur) xa[0] = xa[1];
-    read_w(seg, ring + (sb % kWStages) * C::kStage, 0, 0, 0);
+    const char *W0 = ring + (sb % kWStages) * C::kStage;
+    read_w(seg, W0, 0, 0);
+    read_w(seg, W0, 1, 1);
+    restore(seg, 0, 0);
+    // groups of four steps (a segment starts a group): the first step of a
+    // group loads the next group's scales, which then replace the current
     int s = sb;
-    for (; s + 2 <= se; s += 2) {
-      step(seg, Int<0>{}, s);
-      step(seg, Int<1>{}, s + 1);
+    for (; s + 4 <= se; s += 4) {
+      const int grp = s_grp(s);
+      step(seg, Int<0>{}, Int<0>{}, s, grp);
+      step(seg, Int<1>{}, Int<1>{}, s + 1, grp);
+      step(seg, Int<0>{}, Int<2>{}, s + 2, grp);
+      step(seg, Int<1>{}, Int<3>{}, s + 3, grp);
+      gsc[0] = gsc[1];
     }
-    cur = 0;
-    if (s < se) {
-      step(seg, Int<0>{}, s);
-      cur = 1;
+    const int n = se - s;
+    cur = n & 1;
+    if (n > 0) {
+      const int grp = s_grp(s);
+      step(seg, Int<0>{}, Int<0>{}, s, grp);
+      if (n > 1) step(seg, Int<1>{}, Int<1>{}, s + 1, grp);
+      if (n > 2) step(seg, Int<0>{}, Int<2>{}, s + 2, grp);
+      gsc[0] = gsc[1];
     }
   };
 
@@ -472,10 +514,11 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   issue_w(0);
   issue_w(1);
   issue_a(Int<0>{}, 0);
+  issue_g(Int<0>{}, 0);
   issue_w(2);
   issue_w(3);
   __builtin_amdgcn_sched_barrier(0);
-  wait_loads<3 * C::kWLoads + kALoads>();
+  wait_loads<3 * C::kWLoads + kALoads + kGLoads>();
   barrier();
 
   run(Int<0>{}, 0, lg.st0[1]);
