@@ -84,9 +84,11 @@ template <bool FULL> struct Cfg {
 static_assert(Cfg<true>::kRing <= 160 * 1024, "LDS");
 static_assert(Cfg<true>::kPieces % kWaves == 0 && Cfg<false>::kPieces % kWaves == 0, "pieces");
 
-template <int FA, int FB>
+// The scale operands are dwords whose byte OA (activations) / OB (weights)
+// holds the E8M0 scale.
+template <int FA, int FB, int OA, int OB>
 __device__ inline v16f mma(const v8i &a, const v8i &b, v16f c, uint32_t sa, uint32_t sb) {
-  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, FA, FB, 0, (int)sa, 0, (int)sb);
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, FA, FB, OA, (int)sa, OB, (int)sb);
 }
 
 // The ring's synchronisation is explicit: the compiler does not know which
@@ -399,32 +401,54 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   // half: 3/4-bit: row tile 0 | 1; 6-bit: the weights' high plane in both K
   // halves (scale E + 3) for both row tiles | their low plane (scale E);
   // 8-bit: the high digits (scale E + 4) | the low digits.
-  auto products = [&](auto seg, const ASet &x, const uint32_t (&sa)[2][2], int k, int p, int ob,
-                      int half) __attribute__((always_inline)) {
-    constexpr int SEG = decltype(seg)::v;
+  // The activation scale of step k is byte k of the group's scale dword;
+  // the weight scale of slab n = 2 tn + hx is byte 8 k + n of the lane's 32
+  // bytes, i.e. byte 2 (tn & 1) of dword 2 k + (tn >> 1) once the lane's
+  // dwords are shifted right by 8 hx (done when a group's scales become
+  // current).  3- and 4-bit products select both bytes with the
+  // instruction's operand selects; 6- and 8-bit products add 3 or 4 to the
+  // weight scale first.
+  auto products = [&](auto seg, auto k_tag, const ASet &x, int p, int ob, int half)
+                      __attribute__((always_inline)) {
+    constexpr int SEG = decltype(seg)::v, K = decltype(k_tag)::v;
     const int tn = p >> 1, c = p & 1;
-    const int n = 2 * tn + hx;               // the lane's slab
-    // byte 8 k + n of the lane's 32 weight scale bytes
-    const uint32_t wd = gsc[0].ws[c][k >> 1][2 * (k & 1) + (n >> 2)];
-    const uint32_t e = (wd >> (8 * (n & 3))) & 0xFFu;
+    const uint32_t wd = gsc[0].ws[c][K >> 1][2 * (K & 1) + (tn >> 1)];
     const WOp &B = bo[ob];
     if (SEG <= 1) {
       constexpr int FB = SEG == 0 ? kFmtE2M3 : kFmtE3M2;
       const int tm = half;
-      acc[tm][tn] = mma<kFmtE3M2, FB>(x.d[tm][c], B.b0, acc[tm][tn], sa[tm][c], e);
-    } else if (SEG == 2) {
-#pragma unroll
-      for (int tm = 0; tm < 2; ++tm)
-        acc[tm][tn] = half == 0
-            ? mma<kFmtE3M2, kFmtE3M2>(x.d[tm][c], B.b0, acc[tm][tn], sa[tm][c], sat_plus<3>(e))
-            : mma<kFmtE3M2, kFmtE3M2>(x.d[tm][c], B.b1, acc[tm][tn], sa[tm][c], e);
+      acc[tm][tn] = (tn & 1)
+          ? mma<kFmtE3M2, FB, K, 2>(x.d[tm][c], B.b0, acc[tm][tn], gsc[0].sc[tm][c], wd)
+          : mma<kFmtE3M2, FB, K, 0>(x.d[tm][c], B.b0, acc[tm][tn], gsc[0].sc[tm][c], wd);
     } else {
+      const uint32_t e = (wd >> (16 * (tn & 1))) & 0xFFu;
 #pragma unroll
-      for (int tm = 0; tm < 2; ++tm)
-        acc[tm][tn] = half == 0
-            ? mma<kFmtE4M3, kFmtE4M3>(x.d[tm][c], B.b0, acc[tm][tn], sa[tm][c], sat_plus<4>(e))
-            : mma<kFmtE4M3, kFmtE4M3>(x.d[tm][c], B.b1, acc[tm][tn], sa[tm][c], e);
+      for (int tm = 0; tm < 2; ++tm) {
+        if (SEG == 2)
+          acc[tm][tn] = half == 0
+              ? mma<kFmtE3M2, kFmtE3M2, K, 0>(x.d[tm][c], B.b0, acc[tm][tn], gsc[0].sc[tm][c],
+                                              sat_plus<3>(e))
+              : mma<kFmtE3M2, kFmtE3M2, K, 0>(x.d[tm][c], B.b1, acc[tm][tn], gsc[0].sc[tm][c], e);
+        else
+          acc[tm][tn] = half == 0
+              ? mma<kFmtE4M3, kFmtE4M3, K, 0>(x.d[tm][c], B.b0, acc[tm][tn], gsc[0].sc[tm][c],
+                                              sat_plus<4>(e))
+              : mma<kFmtE4M3, kFmtE4M3, K, 0>(x.d[tm][c], B.b1, acc[tm][tn], gsc[0].sc[tm][c], e);
+      }
     }
+  };
+  // The next group's scales become current (the weight dwords shifted).
+  auto next_group = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int tm = 0; tm < 2; ++tm)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) gsc[0].sc[tm][c] = gsc[1].sc[tm][c];
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) gsc[0].ws[c][h][i] = gsc[1].ws[c][h][i] >> (8 * hx);
   };
 
   // Step s (register set S = s % 2): the products position by position.  At
@@ -447,11 +471,6 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
     const char *W = ring + (s % kWStages) * C::kStage;
     const char *Wn = ring + ((s + 1) % kWStages) * C::kStage;
     const ASet &x = xa[S];
-    uint32_t sa[2][2];
-#pragma unroll
-    for (int tm = 0; tm < 2; ++tm)
-#pragma unroll
-      for (int c = 0; c < 2; ++c) sa[tm][c] = (gsc[0].sc[tm][c] >> (8 * K)) & 0xFFu;
 #pragma unroll
     for (int p = 0; p < 8; ++p) {
       if (p == 4) {
@@ -465,11 +484,11 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
       else read_w(seg, Wn, (p + 2) & 3, p - 6);
       if (p == 0) issue_a(Int<(S + 1) % kASets>{}, s + 1);
       if (p == 0 && K == 0) issue_g(Int<1>{}, grp + 1);
-      products(seg, x, sa, K, p, p & 1, 0);
+      products(seg, k_tag, x, p, p & 1, 0);
       __builtin_amdgcn_sched_barrier(0);
       restore(seg, (p + 1) & 3, (p + 1) & 1);
       __builtin_amdgcn_sched_barrier(0);
-      products(seg, x, sa, K, p, p & 1, 1);
+      products(seg, k_tag, x, p, p & 1, 1);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
@@ -496,7 +515,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
       step(seg, Int<1>{}, Int<1>{}, s + 1, grp);
       step(seg, Int<0>{}, Int<2>{}, s + 2, grp);
       step(seg, Int<1>{}, Int<3>{}, s + 3, grp);
-      gsc[0] = gsc[1];
+      next_group();
     }
     const int n = se - s;
     cur = n & 1;
@@ -505,7 +524,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
       step(seg, Int<0>{}, Int<0>{}, s, grp);
       if (n > 1) step(seg, Int<1>{}, Int<1>{}, s + 1, grp);
       if (n > 2) step(seg, Int<0>{}, Int<2>{}, s + 2, grp);
-      gsc[0] = gsc[1];
+      next_group();
     }
   };
 
@@ -514,12 +533,13 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   issue_w(0);
   issue_w(1);
   issue_a(Int<0>{}, 0);
-  issue_g(Int<0>{}, 0);
+  issue_g(Int<1>{}, 0);
   issue_w(2);
   issue_w(3);
   __builtin_amdgcn_sched_barrier(0);
   wait_loads<3 * C::kWLoads + kALoads + kGLoads>();
   barrier();
+  next_group();
 
   run(Int<0>{}, 0, lg.st0[1]);
   run(Int<1>{}, lg.st0[1], lg.st0[2]);
