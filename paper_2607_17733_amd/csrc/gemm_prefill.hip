@@ -38,8 +38,8 @@
 //     by direct-to-LDS loads into a ring of eight step stages, four steps
 //     ahead; the four waves read it per column tile and K-chunk, two
 //     (tile, chunk) positions ahead of the products, and restore each
-//     operand between the two halves of the previous position's products
-//     into alternating registers.
+//     operand among the previous position's products (a few VALU
+//     instructions after each) into alternating registers.
 // A step has no branch, so the compiler keeps this order.  One barrier per
 // step; the kernel counts its own loads (vmcnt) to know when a stage is
 // complete.  Workgroup ids are remapped so that each XCD owns
@@ -467,7 +467,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   // wave is past step s - 1, whose stage ((s + 4) % 8 = (s - 4) % 8 is older
   // still) the weight loads of s + 4 may then overwrite.
   auto step = [&](auto seg, auto set_tag, auto k_tag, int s, int grp) __attribute__((always_inline)) {
-    constexpr int S = decltype(set_tag)::v, K = decltype(k_tag)::v;
+    constexpr int SEG = decltype(seg)::v, S = decltype(set_tag)::v, K = decltype(k_tag)::v;
     const char *W = ring + (s % kWStages) * C::kStage;
     const char *Wn = ring + ((s + 1) % kWStages) * C::kStage;
     const ASet &x = xa[S];
@@ -484,11 +484,28 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
       else read_w(seg, Wn, (p + 2) & 3, p - 6);
       if (p == 0) issue_a(Int<(S + 1) % kASets>{}, s + 1);
       if (p == 0 && K == 0) issue_g(Int<1>{}, grp + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      // the products interleaved with the next operand's restore: a wave
+      // hides a few VALU instructions behind each of its matrix-core
+      // products, not a long run of them
       products(seg, k_tag, x, p, p & 1, 0);
-      __builtin_amdgcn_sched_barrier(0);
       restore(seg, (p + 1) & 3, (p + 1) & 1);
-      __builtin_amdgcn_sched_barrier(0);
       products(seg, k_tag, x, p, p & 1, 1);
+      if (SEG <= 1) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 16, 0);
+      } else {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 24, 0);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
   };
