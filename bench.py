@@ -431,13 +431,13 @@ def oracle_plan(layer: bool = False):
 
 
 def decode_bench(dev, which: str = "up", reps: int = 50):
-    """Decode GEMM (M in 1, 4, 16) streaming packed weights of one
-    LLaMA-2-70B-shaped linear ("up": K=8192, N=28672; "down": K=28672,
-    N=8192)."""
+    """Decode GEMM (M in 1, 4, 16, and 64: four 16-row activation tiles per
+    weight read) streaming packed weights of one LLaMA-2-70B-shaped linear
+    ("up": K=8192, N=28672; "down": K=28672, N=8192)."""
     import torch
     from paper_2607_17733_amd import mxq
     from paper_2607_17733_amd import workloads as W
-    case = W.decode(16, which)
+    case = W.decode(64, which)
     fmt = mxq.Format(case.K, case.widths, torch.from_numpy(case.perm).to(dev))
     wm0, we0 = mxq.pack_weights(bf16_dev(case.w_bits, dev), fmt)
     copies = [(wm0, we0)] + [(wm0.clone(), we0.clone()) for _ in range(3)]
@@ -447,7 +447,7 @@ def decode_bench(dev, which: str = "up", reps: int = 50):
     w_bytes = case.N * sum(4 * int(m) + 1 for m in case.widths)
     buf_bytes = wm0.numel() + we0.numel()
     out = {}
-    for M in (1, 4, 16):
+    for M in (1, 4, 16, 64):
         am, ae = mxq.quantize_act(bf16_dev(case.a_bits[:M], dev), fmt)
         y = torch.empty((M, case.N), dtype=torch.float32, device=dev)
         for i in range(8):

@@ -57,10 +57,11 @@
 extern "C" {
 #endif
 
-#define MXQ_ABI_VERSION 11
+#define MXQ_ABI_VERSION 12
 #define MXQ_BLOCK 32
-/* mxq_gemm uses the weight-streaming decode kernel for M <= this. */
-#define MXQ_DECODE_MAX_M 16
+/* mxq_gemm uses the weight-streaming decode kernel for M <= this (up to
+ * four 16-row activation tiles per weight read). */
+#define MXQ_DECODE_MAX_M 64
 
 typedef enum {
   MXQ_OK = 0,
@@ -299,7 +300,8 @@ mxq_status mxq_pack_weights(const mxq_fmt *fmt, const uint16_t *w, int64_t N,
  *   w_mant/w_exp  DEVICE, from mxq_pack_weights with the same fmt and N.
  *   y             DEVICE float [M][ldy], ldy >= N; every y[i][j] with i < M,
  *                 j < N is written, nothing else.
- * M <= MXQ_DECODE_MAX_M runs the weight-streaming decode kernel, larger M
+ * M <= MXQ_DECODE_MAX_M runs the weight-streaming decode kernel (each
+ * weight step read once for all ceil(M / 16) activation tiles), larger M
  * the tiled prefill kernel; both read the same buffers.  The weights' high
  * digit planes take the scale E + 3 (6-bit) or E + 4 (8-bit), which the
  * E8M0 format holds up to 254: a 6-bit weight block with E >= 252 or an

@@ -17,7 +17,9 @@
 // activations arrive as ready FP6/FP8 codes (the operand image).
 //
 // Work decomposition: the kernel is bound by the number of vector memory
-// loads, so each load serves as many products as possible.  A workgroup
+// loads, so each load serves as many products as possible.  Each weight
+// step is read once for all of the launch's 16-row activation tiles (up to
+// four: M <= 64).  A workgroup
 // owns a pair of 16-column slabs (one activation load feeds both); its nw
 // waves (2 to 16, about 16 waves per CU with every pair resident) take every
 // nw-th group of four steps; a group's scale bytes are one word per lane and
@@ -39,6 +41,8 @@ typedef unsigned u3 __attribute__((ext_vector_type(3)));
 
 constexpr int kFmtE4M3 = 0, kFmtE2M3 = 2, kFmtE3M2 = 3;
 constexpr int kMaxWaves = 8;
+constexpr int kDecodeTiles = 4;             // 16-row activation tiles per launch
+static_assert(16 * kDecodeTiles == MXQ_DECODE_MAX_M, "decode rows");
 
 // The weights are read exactly once: non-temporal loads stream them past the
 // caches.  Activations stay cached; every workgroup reads them.
@@ -86,7 +90,8 @@ __device__ inline uint32_t lo_codes(uint32_t w) {
   return FULL ? (w & 0x0F0F0F0Fu) : (w & 0x8F8F8F8Fu);
 }
 
-template <bool FULL>
+// T: 16-row activation tiles (M <= 16 T).
+template <bool FULL, int T>
 __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g) {
   __shared__ v4f red[kMaxWaves][2][64];
   const int t = threadIdx.x, lane = t & 63;
@@ -107,10 +112,14 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
   const bool two = (pair * 32 + 16) < g.N;           // the second slab has columns
   const uint8_t *wsup = g.w_mant + ss * g.w_super;
   const uint8_t *wsc = g.w_exp + ss * g.w_super_sc + 32 * lane;
-  // Lanes of rows >= M read row 0's activation bytes (same addresses as a
+  // Lanes of rows >= M read the first row of their tile (same addresses as a
   // live lane, so no extra traffic); their output rows are discarded.
-  const int alane = line < g.M ? lane : (lane & ~15);
-  v4f acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  int alane[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) alane[t] = 16 * t + line < g.M ? lane : (lane & ~15);
+  v4f acc[T][2];
+#pragma unroll
+  for (int t = 0; t < T; ++t) acc[t][0] = acc[t][1] = v4f{0.f, 0.f, 0.f, 0.f};
 
   auto run_group = [&](auto segc, int gi) {
     constexpr int SEG = decltype(segc)::value;
@@ -132,15 +141,17 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
       sw[sl] = ((d0 >> sh) & 0xFFu) | (((d1 >> sh) & 0xFFu) << 8) | (((d2 >> sh) & 0xFFu) << 16) |
                (((d3 >> sh) & 0xFFu) << 24);
     }
-    const uint32_t sa = *(const uint32_t *)(g.a_exp + (int64_t)gi * 256 + 4 * alane);
+    uint32_t sa[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t)
+      sa[t] = *(const uint32_t *)(g.a_exp + t * g.a_tile_sc + (int64_t)gi * 256 + 4 * alane[t]);
     const uint8_t *wseg = wsup + w_seg_base<SEG, FULL>(lg) + (int64_t)(4 * gl) * kWSlabs * CB +
                           (int64_t)n0 * CB;
     const uint8_t *aseg = g.a_mant + a_seg_base<SEG>(lg) +
-                          (int64_t)(4 * gl) * kLanes * a_lane_bytes(SEG) +
-                          (int64_t)a_lane_bytes(SEG) * alane;
+                          (int64_t)(4 * gl) * kLanes * a_lane_bytes(SEG);
     // raw loads of step k (fields a segment does not use stay unread)
     struct Raw {
-      u4 a0, a1;            // activation lane data (24 or 32 bytes)
+      u4 a0[T], a1[T];      // activation lane data (24 or 32 bytes) per tile
       u4 p[2], h[2];        // weight bytes of the two slabs
       u2 x[2];
       uint32_t z[2];
@@ -148,14 +159,18 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
     auto load = [&](int k) __attribute__((always_inline)) {
       Raw r;
       const uint8_t *w0 = wseg + (int64_t)k * kWSlabs * CB;
-      const uint8_t *ap = aseg + (int64_t)k * kLanes * a_lane_bytes(SEG);
-      if (SEG == 3) {
-        r.a0 = *(const u4 *)ap;
-        r.a1 = *(const u4 *)(ap + 16);
-      } else {
-        r.a0 = *(const u4 *)ap;
-        const u2 aw = *(const u2 *)(ap + 16);
-        r.a1 = __builtin_shufflevector(aw, aw, 0, 1, -1, -1);
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        const uint8_t *ap = aseg + t * g.a_tile + (int64_t)k * kLanes * a_lane_bytes(SEG) +
+                            (int64_t)a_lane_bytes(SEG) * alane[t];
+        if (SEG == 3) {
+          r.a0[t] = *(const u4 *)ap;
+          r.a1[t] = *(const u4 *)(ap + 16);
+        } else {
+          r.a0[t] = *(const u4 *)ap;
+          const u2 aw = *(const u2 *)(ap + 16);
+          r.a1[t] = __builtin_shufflevector(aw, aw, 0, 1, -1, -1);
+        }
       }
 #pragma unroll
       for (int sl = 0; sl < 2; ++sl) {
@@ -180,8 +195,11 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
     };
     auto compute = [&](auto kc, const Raw &r) __attribute__((always_inline)) {
       constexpr int k = decltype(kc)::value;
-      const v8i a = {(int)r.a0[0], (int)r.a0[1], (int)r.a0[2], (int)r.a0[3],
-                     (int)r.a1[0], (int)r.a1[1], (int)r.a1[2], (int)r.a1[3]};
+      v8i a[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+        a[t] = v8i{(int)r.a0[t][0], (int)r.a0[t][1], (int)r.a0[t][2], (int)r.a0[t][3],
+                   (int)r.a1[t][0], (int)r.a1[t][1], (int)r.a1[t][2], (int)r.a1[t][3]};
       if (SEG <= 1) {
         uint32_t d[2][6];
 #pragma unroll
@@ -200,8 +218,11 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
           }
         }
         constexpr int FB = SEG == 0 ? kFmtE2M3 : kFmtE3M2;
-        acc0 = mfma<kFmtE3M2, FB, k>(a, six(d[0]), acc0, sa, sw[0]);
-        acc1 = mfma<kFmtE3M2, FB, k>(a, six(d[1]), acc1, sa, sw[1]);
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          acc[t][0] = mfma<kFmtE3M2, FB, k>(a[t], six(d[0]), acc[t][0], sa[t], sw[0]);
+          acc[t][1] = mfma<kFmtE3M2, FB, k>(a[t], six(d[1]), acc[t][1], sa[t], sw[1]);
+        }
       } else if (SEG == 2) {
         // the weights' high plane in every lane (scale E + 3) gives the
         // products hh and lh, their low plane (scale E) hl and ll
@@ -218,9 +239,11 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
             unfold2(xh, L, H);
           }
           const uint32_t e = sw[sl];
-          v4f &acc = sl ? acc1 : acc0;
-          acc = mfma<kFmtE3M2, kFmtE3M2, k>(a, six(H), acc, sa, scale_plus<3>(e));
-          acc = mfma<kFmtE3M2, kFmtE3M2, k>(a, six(L), acc, sa, e);
+#pragma unroll
+          for (int t = 0; t < T; ++t) {
+            acc[t][sl] = mfma<kFmtE3M2, kFmtE3M2, k>(a[t], six(H), acc[t][sl], sa[t], scale_plus<3>(e));
+            acc[t][sl] = mfma<kFmtE3M2, kFmtE3M2, k>(a[t], six(L), acc[t][sl], sa[t], e);
+          }
         }
       } else {
         // the weights' high digits in every lane (scale E + 4), then their
@@ -235,9 +258,11 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
             bl[i] = (int)lo_codes<FULL>(w);
           }
           const uint32_t e = sw[sl];
-          v4f &acc = sl ? acc1 : acc0;
-          acc = mfma<kFmtE4M3, kFmtE4M3, k>(a, bh, acc, sa, scale_plus<4>(e));
-          acc = mfma<kFmtE4M3, kFmtE4M3, k>(a, bl, acc, sa, e);
+#pragma unroll
+          for (int t = 0; t < T; ++t) {
+            acc[t][sl] = mfma<kFmtE4M3, kFmtE4M3, k>(a[t], bh, acc[t][sl], sa[t], scale_plus<4>(e));
+            acc[t][sl] = mfma<kFmtE4M3, kFmtE4M3, k>(a[t], bl, acc[t][sl], sa[t], e);
+          }
         }
       }
     };
@@ -245,20 +270,21 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
     using I1 = std::integral_constant<int, 1>;
     using I2 = std::integral_constant<int, 2>;
     using I3 = std::integral_constant<int, 3>;
-    if (nst == 4 && SEG <= 1) {
+    if (T == 1 && nst == 4 && SEG <= 1) {
       // a whole group: every load first, then the products
       const Raw r0 = load(0), r1 = load(1), r2 = load(2), r3 = load(3);
       compute(I0(), r0);
       compute(I1(), r1);
       compute(I2(), r2);
       compute(I3(), r3);
-    } else if (nst == 4 && SEG == 2) {
+    } else if (T == 1 && nst == 4 && SEG == 2) {
       const Raw r0 = load(0), r1 = load(1), r2 = load(2), r3 = load(3);
       compute(I0(), r0);
       compute(I1(), r1);
       compute(I2(), r2);
       compute(I3(), r3);
-    } else if (nst == 4) {
+    } else if (T <= 2 && nst == 4) {
+      // two steps in flight at a time (8-bit steps, or two activation tiles)
       const Raw r0 = load(0), r1 = load(1);
       compute(I0(), r0);
       compute(I1(), r1);
@@ -266,8 +292,8 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
       compute(I2(), r2);
       compute(I3(), r3);
     } else {
-      // 8-bit steps (twice the bytes) one at a time; steps past a short
-      // group are skipped
+      // one step at a time (three or four activation tiles, or a short
+      // group, whose steps past its end are skipped)
       compute(I0(), load(0));
       if (nst > 1) compute(I1(), load(1));
       if (nst > 2) compute(I2(), load(2));
@@ -282,17 +308,22 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
     else run_group(std::integral_constant<int, 3>(), gi);
   }
 
-  red[wave][0][lane] = acc0;
-  red[wave][1][lane] = acc1;
-  __syncthreads();
-  if (wave < 2 && (wave == 0 || two)) {
-    v4f y = red[0][wave][lane];
-    for (int w = 1; w < nw; ++w) y += red[w][wave][lane];
-    const int64_t col = pair * 32 + 16 * wave + line;
+  // the waves' sums meet in LDS in wave order, one tile at a time
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = 4 * grp + i;
-      if (row < g.M && col < g.N) g.y[row * g.ldy + col] = y[i];
+  for (int t = 0; t < T; ++t) {
+    if (t > 0) __syncthreads();
+    red[wave][0][lane] = acc[t][0];
+    red[wave][1][lane] = acc[t][1];
+    __syncthreads();
+    if (wave < 2 && (wave == 0 || two)) {
+      v4f y = red[0][wave][lane];
+      for (int w = 1; w < nw; ++w) y += red[w][wave][lane];
+      const int64_t col = pair * 32 + 16 * wave + line;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = 16 * t + 4 * grp + i;
+        if (row < g.M && col < g.N) g.y[row * g.ldy + col] = y[i];
+      }
     }
   }
 }
@@ -320,10 +351,19 @@ static int decode_waves(int64_t pairs) {
 hipError_t launch_gemm_decode(const GemmArgs &a, hipStream_t stream) {
   const int64_t pairs = (a.N + 31) / 32;
   dim3 grid((unsigned)pairs), block((unsigned)(64 * decode_waves(pairs)));
-  if (a.full)
-    hipLaunchKernelGGL(gemm_decode_kernel<true>, grid, block, 0, stream, a);
-  else
-    hipLaunchKernelGGL(gemm_decode_kernel<false>, grid, block, 0, stream, a);
+  const int64_t tiles = (a.M + 15) / 16;
+  if (tiles < 1 || tiles > kDecodeTiles) return hipErrorInvalidValue;
+  auto go = [&](auto kern) { hipLaunchKernelGGL(kern, grid, block, 0, stream, a); };
+  switch ((int)tiles * 2 + (a.full ? 1 : 0)) {
+    case 2: go(gemm_decode_kernel<false, 1>); break;
+    case 3: go(gemm_decode_kernel<true, 1>); break;
+    case 4: go(gemm_decode_kernel<false, 2>); break;
+    case 5: go(gemm_decode_kernel<true, 2>); break;
+    case 6: go(gemm_decode_kernel<false, 3>); break;
+    case 7: go(gemm_decode_kernel<true, 3>); break;
+    case 8: go(gemm_decode_kernel<false, 4>); break;
+    default: go(gemm_decode_kernel<true, 4>); break;
+  }
   return hipGetLastError();
 }
 

@@ -15,7 +15,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmxq.so")
 BLOCK = 32
-DECODE_MAX_M = 16
+DECODE_MAX_M = 64
 
 
 class MxqError(RuntimeError):

@@ -70,7 +70,7 @@ def test_sizes(lib):
     w1 = [4] * 6 + [6, 8]
     f, _w = _fmt(256, w1)
     fr = ctypes.byref(f)
-    assert lib.mxq_abi_version() == 11
+    assert lib.mxq_abi_version() == 12
     # S = 0/2/1/1 steps, 3 groups: tiles of 64 x (3 x 24 + 32) bytes
     assert layout_sizes(w1, 16, 128) == (6656, 768, 8 * (2 * 1024 + 768 + 1024), 3 * 2048)
     assert lib.mxq_act_packed_bytes(fr) == 160

@@ -51,6 +51,9 @@ SHAPES = [
     (16, 256, 256, (6, 1, 1), "scales"),
     (17, 256, 200, (4, 2, 2), "random"),
     (33, 512, 130, (8, 4, 4), "scales"),
+    (48, 512, 300, (8, 4, 4), "random"),
+    (64, 768, 160, (16, 4, 4), "scales"),
+    (65, 256, 96, (4, 2, 2), "identity"),
     (129, 384, 129, (0, 12, 0), "random"),
     (200, 320, 300, (0, 0, 10), "identity"),
     (257, 1024, 272, (24, 5, 3), "scales"),
@@ -215,9 +218,10 @@ def test_mlp_down_full():
 
 @pytest.mark.parametrize("which", ["up", "down"])
 def test_decode_full(which):
-    """LLaMA-2-70B decode shapes, M in {1, 4, 16}; the packed weights are
-    checked once, the GEMM at every M."""
-    base = W.decode(16, which)
+    """LLaMA-2-70B decode shapes, M in {1, 4, 16, 40, 64} (one to four
+    16-row activation tiles per weight read); the packed weights are checked
+    once, the GEMM at every M."""
+    base = W.decode(64, which)
     say(base.name, base.K, base.N)
     fmt = fmt_for(base)
     w = to_dev_bf16(base.w_bits)
@@ -226,7 +230,7 @@ def test_decode_full(which):
     check_pack_w(base, {"w_mant": wm, "w_exp": we}, qw, ew, fmt)
     g = np.random.default_rng(1)
     cols = np.unique(np.concatenate([[0, base.N - 1], g.choice(base.N, 2048, replace=False)]))
-    for M in (1, 4, 16):
+    for M in (1, 4, 16, 40, 64):
         say(base.name, "M=%d" % M)
         a_bits = base.a_bits[:M]
         am, ae = mxq.quantize_act(to_dev_bf16(a_bits), fmt)
