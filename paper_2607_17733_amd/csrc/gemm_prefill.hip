@@ -31,12 +31,14 @@
 // w owns rows 64w..64w+63 x all 128 columns = 2x4 tiles of 32x32 fp32
 // accumulators, and walks every step.
 //   - activations go straight from the image into registers -- each row is
-//     used by exactly one wave -- one step ahead, in two register sets;
+//     used by exactly one wave -- one step ahead, in two register sets, two
+//     loads in each of the step's first four positions;
 //   - the scale words (activation and weight) are loaded once per group of
-//     four steps, a group ahead;
+//     four steps, a group ahead, over three positions;
 //   - the weight chunk of each step (8 slabs, 6 to 12 KB) goes global -> LDS
 //     by direct-to-LDS loads into a ring of eight step stages, four steps
-//     ahead; the four waves read it per column tile and K-chunk, two
+//     ahead (a wave's share over two positions); the four waves read it per
+//     column tile and K-chunk, two
 //     (tile, chunk) positions ahead of the products, and restore each
 //     operand among the previous position's products (a few VALU
 //     instructions after each) into alternating registers.
@@ -267,60 +269,56 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
 
   // Weight loads of step st (clamped to the last) into its stage: pieces
   // n = 0 .. kPieces - 1 of 1 KB (pieces past the step's chunk bytes repeat
-  // its last piece); wave w issues n = w + 4 j.
-  auto issue_w = [&](int st) __attribute__((always_inline)) {
+  // its last piece); wave w issues n = w + 4 j for j in [j0, j1).
+  auto issue_w = [&](int st, int j0, int j1) __attribute__((always_inline)) {
     st = min(st, nsteps - 1);
     const int wo = w_off(st), np = w_pieces(st);
     char *stage = ring + (st % kWStages) * C::kStage;
 #pragma unroll
-    for (int j = 0; j < C::kWLoads; ++j) {
+    for (int j = j0; j < j1; ++j) {
       const int kb = min(wave + kWaves * j, np - 1);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void *)(stage + kb * 1024), 16, lane * 16,
                                                wo + kb * 1024, 0, 0);
     }
   };
-  // Activation loads of step st (clamped to the last) into register set S.
-  auto issue_a = [&](auto set_tag, int st) __attribute__((always_inline)) {
+  // Activation loads of step st (clamped to the last) into register set S,
+  // part = the (32-row tile, K-chunk) pair: tile part & 1, chunk part >> 1.
+  // A wave that issues its loads in bursts stalls on them; spread over the
+  // positions, they are accepted while the products run.
+  auto issue_a = [&](auto set_tag, int st, int part) __attribute__((always_inline)) {
     constexpr int S = decltype(set_tag)::v;
     st = min(st, nsteps - 1);
     const int so = a_off(st);
     const bool wide = st >= lg.st0[3];
-#pragma unroll
-    for (int tm = 0; tm < 2; ++tm)
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        const int lk = c ? lk1 : lk0;
-        const int vb = vt[tm] * (int)g.a_tile;
-        // FP8 steps: chunk c = block c of the step: the high digits of the
-        // lane's 16 elements (lane group lh, bytes 16 c) as K-block 0, their
-        // low digits (lane group 2 + lh) as K-block 1.  FP6 steps: the lane's
-        // 24 bytes (the second load's last 8 bytes are not used; past the
-        // image they read zero).  The same two loads either way, so the
-        // step has no branch.
-        const int olo = wide ? 32 * lk0 + 16 * c : 24 * lk;
-        const int ohi = wide ? 32 * lk1 + 16 * c : 24 * lk + 16;
-        const u4 lo = __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(ra, vb + olo, so, 0));
-        const u4 hi = __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(ra, vb + ohi, so, 0));
-        xa[S].d[tm][c] = (v8i)__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-      }
+    const int tm = part & 1, c = part >> 1;
+    const int lk = c ? lk1 : lk0;
+    const int vb = vt[tm] * (int)g.a_tile;
+    const int olo = wide ? 32 * lk0 + 16 * c : 24 * lk;
+    const int ohi = wide ? 32 * lk1 + 16 * c : 24 * lk + 16;
+    const u4 lo = __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(ra, vb + olo, so, 0));
+    const u4 hi = __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(ra, vb + ohi, so, 0));
+    xa[S].d[tm][c] = (v8i)__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   };
-  // Scale loads of group grp (clamped to the last) into set G.
-  auto issue_g = [&](auto gset_tag, int grp) __attribute__((always_inline)) {
+  // Scale loads of group grp (clamped to the last) into set G: part 0 the
+  // activation scale dwords, part 1 + c the weight scale bytes of K-chunk c.
+  auto issue_g = [&](auto gset_tag, int grp, int part) __attribute__((always_inline)) {
     constexpr int G = decltype(gset_tag)::v;
     grp = min(grp, lg.ngroups - 1);
+    if (part == 0) {
 #pragma unroll
-    for (int tm = 0; tm < 2; ++tm)
+      for (int tm = 0; tm < 2; ++tm)
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
-        gsc[G].sc[tm][c] = __builtin_amdgcn_raw_buffer_load_b32(
-            rs, vt[tm] * (int)g.a_tile_sc + 4 * (c ? lk1 : lk0), grp * 256, 0);
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
+        for (int c = 0; c < 2; ++c)
+          gsc[G].sc[tm][c] = __builtin_amdgcn_raw_buffer_load_b32(
+              rs, vt[tm] * (int)g.a_tile_sc + 4 * (c ? lk1 : lk0), grp * 256, 0);
+    } else {
+      const int c = part - 1;
 #pragma unroll
       for (int h = 0; h < 2; ++h)
         gsc[G].ws[c][h] = __builtin_bit_cast(
             u4, __builtin_amdgcn_raw_buffer_load_b128(rws, 32 * (c ? lk1 : lk0) + 16 * h,
                                                       grp * 2048, 0));
+    }
   };
 
   // Weight operand of column tile tn, K-chunk c (position p = 2 tn + c of
@@ -455,14 +453,16 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   // position p the step reads the raw operand of p + 2 (positions 8 and 9
   // are the next step's first two, read after the barrier), issues the
   // first half of p's products, restores the operand of p + 1, then issues
-  // the second half.  At position 0 the step issues the activation loads of
-  // step s + 1; between positions 3 and 4 the workgroup meets at a barrier,
-  // then the step issues the weight loads of step s + 4.  Before the
-  // barrier each wave waits for its own weight loads of step s + 1: since
-  // them it has issued at most the activations of s - 1, s and s + 1 and the
-  // weights of s + 2 and s + 3, and the activations of s - 1 were consumed
-  // by step s - 1, so at most two activation and two weight bundles may
-  // still be in flight (this also holds in the first steps, after the
+  // the second half.  Positions 0 to 3 issue the activation loads of step
+  // s + 1, one (tile, chunk) pair each; between positions 3 and 4 the
+  // workgroup meets at a barrier, then positions 4 and 6 issue the weight
+  // loads of step s + 4 (and positions 4 to 6 of a group's first step the
+  // next group's scale loads).  Before the barrier each wave waits for its
+  // own weight loads of step s + 1: since them it has issued the activations
+  // of s - 1, s and s + 1 and the weights of s + 2 and s + 3, perhaps with
+  // scale loads between them, so leaving at most two activation and two
+  // weight bundles in flight waits for them (and for the activations of
+  // s - 1, already consumed; this also holds in the first steps, after the
   // prologue).  After the barrier the stage of s + 1 is complete, and every
   // wave is past step s - 1, whose stage ((s + 4) % 8 = (s - 4) % 8 is older
   // still) the weight loads of s + 4 may then overwrite.
@@ -476,14 +476,15 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
       if (p == 4) {
         wait_loads<2 * kALoads + 2 * C::kWLoads>();
         barrier();
-        issue_w(s + kWAhead);
+        issue_w(s + kWAhead, 0, 1);
       }
+      if (p == 6) issue_w(s + kWAhead, 1, C::kWLoads);
       // positions 8 and 9: the next step's (unused when that step starts a
       // new segment, whose loop reads them again)
       if (p + 2 < 8) read_w(seg, W, (p + 2) & 3, p + 2);
       else read_w(seg, Wn, (p + 2) & 3, p - 6);
-      if (p == 0) issue_a(Int<(S + 1) % kASets>{}, s + 1);
-      if (p == 0 && K == 0) issue_g(Int<1>{}, grp + 1);
+      if (p < 4) issue_a(Int<(S + 1) % kASets>{}, s + 1, p);
+      if (p >= 4 && p < 7 && K == 0) issue_g(Int<1>{}, grp + 1, p - 4);
       __builtin_amdgcn_sched_barrier(0);
       // the products interleaved with the next operand's restore: a wave
       // hides a few VALU instructions behind each of its matrix-core
@@ -547,12 +548,12 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
 
   // Prologue: the weights of steps 0 and 1, the activations of step 0, the
   // weights of steps 2 and 3, and the wait for the stage of step 0.
-  issue_w(0);
-  issue_w(1);
-  issue_a(Int<0>{}, 0);
-  issue_g(Int<1>{}, 0);
-  issue_w(2);
-  issue_w(3);
+  issue_w(0, 0, C::kWLoads);
+  issue_w(1, 0, C::kWLoads);
+  for (int pp = 0; pp < 4; ++pp) issue_a(Int<0>{}, 0, pp);
+  for (int pp = 0; pp < 3; ++pp) issue_g(Int<1>{}, 0, pp);
+  issue_w(2, 0, C::kWLoads);
+  issue_w(3, 0, C::kWLoads);
   __builtin_amdgcn_sched_barrier(0);
   wait_loads<3 * C::kWLoads + kALoads + kGLoads>();
   barrier();
