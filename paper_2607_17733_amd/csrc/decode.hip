@@ -21,9 +21,11 @@
 // step is read once for all of the launch's 16-row activation tiles (up to
 // four: M <= 64).  A workgroup
 // owns a pair of 16-column slabs (one activation load feeds both); its nw
-// waves (2 to 16, about 16 waves per CU with every pair resident) take every
-// nw-th group of four steps; a group's scale bytes are one word per lane and
-// operand.  The waves' fp32 accumulators meet in LDS in a fixed order.
+// waves (2 to 8, the most at which every pair is resident by the kernel's
+// register occupancy) take every nw-th group of four steps; a group's scale
+// bytes are one word per lane and operand.  The waves' fp32 accumulators
+// meet in LDS in a fixed order.
+#include <atomic>
 #include <type_traits>
 
 #include "mxq_device.h"
@@ -330,10 +332,13 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
 
 }  // namespace
 
-// Waves per workgroup (one workgroup per pair of 16-column slabs): enough
-// for about 16 waves per CU when every pair is resident at once (4 for 896
-// pairs, 16 for 256 pairs).
+// Waves per workgroup (one workgroup per pair of 16-column slabs): the most
+// (up to kMaxWaves) at which every pair is resident at once, by the kernel's
+// own occupancy (queried once per kernel and size; every GPU this runs on is
+// the same model).
+template <bool FULL, int T>
 static int decode_waves(int64_t pairs) {
+  static std::atomic<int> per_cu[kMaxWaves + 1] = {};
   int cus = 256;
   int dev = 0;
   if (hipGetDevice(&dev) == hipSuccess) {
@@ -342,27 +347,44 @@ static int decode_waves(int64_t pairs) {
         n > 0)
       cus = n;
   }
-  int64_t w = 16LL * cus / pairs;      // rounded down: every pair stays resident
-  if (w < 2) w = 2;
-  if (w > kMaxWaves) w = kMaxWaves;
-  return (int)w;
+  for (int w = kMaxWaves; w > 2; --w) {
+    int per = per_cu[w].load(std::memory_order_relaxed);
+    if (per == 0) {
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, gemm_decode_kernel<FULL, T>, 64 * w,
+                                                       0) != hipSuccess || per <= 0)
+        break;
+      per_cu[w].store(per, std::memory_order_relaxed);
+    }
+    if ((int64_t)per * cus >= pairs) return w;
+  }
+  return 2;
 }
 
 hipError_t launch_gemm_decode(const GemmArgs &a, hipStream_t stream) {
   const int64_t pairs = (a.N + 31) / 32;
-  dim3 grid((unsigned)pairs), block((unsigned)(64 * decode_waves(pairs)));
   const int64_t tiles = (a.M + 15) / 16;
   if (tiles < 1 || tiles > kDecodeTiles) return hipErrorInvalidValue;
-  auto go = [&](auto kern) { hipLaunchKernelGGL(kern, grid, block, 0, stream, a); };
+  auto go = [&](auto fc, auto tc) {
+    constexpr bool FULL = decltype(fc)::value;
+    constexpr int T = decltype(tc)::value;
+    const dim3 grid((unsigned)pairs), block((unsigned)(64 * decode_waves<FULL, T>(pairs)));
+    hipLaunchKernelGGL((gemm_decode_kernel<FULL, T>), grid, block, 0, stream, a);
+  };
+  using F = std::false_type;
+  using Tr = std::true_type;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  using I4 = std::integral_constant<int, 4>;
   switch ((int)tiles * 2 + (a.full ? 1 : 0)) {
-    case 2: go(gemm_decode_kernel<false, 1>); break;
-    case 3: go(gemm_decode_kernel<true, 1>); break;
-    case 4: go(gemm_decode_kernel<false, 2>); break;
-    case 5: go(gemm_decode_kernel<true, 2>); break;
-    case 6: go(gemm_decode_kernel<false, 3>); break;
-    case 7: go(gemm_decode_kernel<true, 3>); break;
-    case 8: go(gemm_decode_kernel<false, 4>); break;
-    default: go(gemm_decode_kernel<true, 4>); break;
+    case 2: go(F(), I1()); break;
+    case 3: go(Tr(), I1()); break;
+    case 4: go(F(), I2()); break;
+    case 5: go(Tr(), I2()); break;
+    case 6: go(F(), I3()); break;
+    case 7: go(Tr(), I3()); break;
+    case 8: go(F(), I4()); break;
+    default: go(Tr(), I4()); break;
   }
   return hipGetLastError();
 }
