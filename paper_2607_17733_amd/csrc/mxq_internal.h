@@ -37,6 +37,7 @@ struct QuantArgs {
   int vec16;               // 16-byte source loads are aligned
   int rows_per_wg;         // filled by the launcher
   int lg_rows;             // activations: log2 of the rows per group
+  int perm_table;          // activations: gather through the LDS offset table
   // activations: RMS-normalise each row before quantizing (y = g * x / rms)
   int rmsnorm;
   const uint16_t *gain;    // bf16 [K]

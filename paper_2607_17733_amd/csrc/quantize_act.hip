@@ -8,8 +8,11 @@
 // Work decomposition.  A workgroup owns R consecutive rows (8 for K = 4096,
 // fewer for longer rows, up to 64 for short ones) and stages them in LDS with
 // 16-byte loads, so the permutation becomes an LDS gather (entries outside
-// [0, K) clamp to the zero padding after the row).  A thread owns one (row,
-// block) item, at most two; a workgroup has up to 1024 threads and fills a
+// [0, K) clamp to the zero padding after the row).  The workgroup first turns
+// the permutation into a table of 16-bit byte offsets in LDS (rows of at most
+// 32767 elements; longer rows read it from global memory per item).  A thread
+// owns one (row, block) item, at most two; its segment selects a code path
+// compiled for that width.  A workgroup has up to 1024 threads and fills a
 // CU.  Lanes run over rows fastest, so the rows of a block write contiguous
 // runs of the 32-row operand tiles (whole 128-byte lines at R = 8), and
 // consecutive workgroups run on one XCD, whose L2 then completes every line
@@ -38,6 +41,7 @@ typedef unsigned u2 __attribute__((ext_vector_type(2)));
 constexpr int kMaxThreads = 1024;
 constexpr int kLdsBudget = 144 * 1024;  // staged rows of one workgroup per CU
 constexpr int kRowPad = 8;              // zero bf16 elements after each staged row
+constexpr int64_t kPermTableMaxK = 32767;  // 16-bit byte offsets into a staged row
 
 // A block of 32 values kept as its even and odd elements (the register
 // layout the FP6 conversion takes).
@@ -106,59 +110,63 @@ __device__ inline void pack3(const Blk &v, uint32_t *w) {
   }
 }
 
-// a[s] for a per-thread segment index s, as selects: indexing a register
-// array with a thread's value would place the array in scratch memory.
-__device__ inline int pick4(const int (&a)[kSegs], int s) {
-  return s == 0 ? a[0] : s == 1 ? a[1] : s == 2 ? a[2] : a[3];
-}
-
-// Where padded block bp of a row goes: its segment, step, position in the
+// Where padded block rem of segment SEG goes: its step, position in the
 // step, its block of the width map, and the step's offset in a 16-row tile
-// of the operand image and its scale group and byte.
+// of the operand image and its scale group and byte.  The segment is a
+// compile-time constant, so every per-segment quantity is a constant index
+// into the width map's geometry.
 struct ItemGeo {
-  int s, rem, st, pos, b, k;
+  int s, rem, pos, b;
   bool pad;
   int step_off, group, byte;
 };
-__device__ inline ItemGeo item_geo(const LGeo &lg, int bp) {
+template <int SEG>
+__device__ inline ItemGeo item_geo_seg(const LGeo &lg, int rem) {
   ItemGeo g;
-  const int p0 = 4 * lg.S[0], p1 = p0 + 4 * lg.S[1], p2 = p1 + 2 * lg.S[2];
-  g.s = (bp >= p0) + (bp >= p1) + (bp >= p2);
-  g.rem = bp - (g.s == 0 ? 0 : g.s == 1 ? p0 : g.s == 2 ? p1 : p2);
-  const int two = g.s < 2 ? 2 : 1;                   // log2 blocks per step
-  g.k = g.rem >> two;
-  g.pos = g.rem & ((1 << two) - 1);
-  g.st = pick4(lg.st0, g.s) + g.k;
-  g.pad = g.rem >= pick4(lg.nb, g.s);
-  g.b = pick4(lg.b0, g.s) + g.rem;
-  const int sb = kLanes * a_lane_bytes(0);           // 3/4/6-bit step bytes
-  const int before = g.s == 0 ? 0 : g.s == 1 ? lg.S[0] : g.s == 2 ? lg.S[0] + lg.S[1]
-                                                                  : lg.S[0] + lg.S[1] + lg.S[2];
-  g.step_off = before * sb + g.k * (g.s == 3 ? kLanes * a_lane_bytes(3) : sb);
-  g.group = pick4(lg.G0, g.s) + (g.k >> 2);
-  g.byte = g.k & (kGroupSteps - 1);
+  constexpr int two = SEG < 2 ? 2 : 1;               // log2 blocks per step
+  const int k = rem >> two;
+  g.s = SEG;
+  g.rem = rem;
+  g.pos = rem & ((1 << two) - 1);
+  g.pad = rem >= lg.nb[SEG];
+  g.b = lg.b0[SEG] + rem;
+  constexpr int sb = kLanes * a_lane_bytes(0);       // 3/4/6-bit step bytes
+  int before = 0;
+#pragma unroll
+  for (int i = 0; i < SEG; ++i) before += lg.S[i];
+  g.step_off = before * sb + k * (SEG == 3 ? kLanes * a_lane_bytes(3) : sb);
+  g.group = lg.G0[SEG] + (k >> 2);
+  g.byte = k & (kGroupSteps - 1);
   return g;
 }
-
-// The 32 permutation entries of padded block bp (undefined for padding
-// blocks, which gather nothing).
-__device__ inline void load_perm(const QuantArgs &q, const ItemGeo &g, int4 (&pe)[8]) {
-  if (!q.perm || g.pad) return;
+// First padded block of each segment (P[0] = 0).
+struct SegStarts {
+  int P[kSegs];
+  __device__ explicit SegStarts(const LGeo &lg) {
+    P[0] = 0;
 #pragma unroll
-  for (int u = 0; u < 8; ++u) pe[u] = *(const int4 *)(q.perm + g.b * kBlock + 4 * u);
+    for (int i = 1; i < kSegs; ++i) P[i] = P[i - 1] + lg.S[i - 1] * (i - 1 < 2 ? 4 : 2);
+  }
+};
+__device__ inline ItemGeo item_geo(const LGeo &lg, const SegStarts &ss, int bp) {
+  if (bp < ss.P[1]) return item_geo_seg<0>(lg, bp);
+  if (bp < ss.P[2]) return item_geo_seg<1>(lg, bp - ss.P[1]);
+  if (bp < ss.P[3]) return item_geo_seg<2>(lg, bp - ss.P[2]);
+  return item_geo_seg<3>(lg, bp - ss.P[3]);
 }
 
 // One (row, padded block) item: gather, quantize, write the canonical
 // packed row and exponent (q.write_rows) and / or the GEMM operand image
 // and its scale words (q.write_image).  sr is the staged row in LDS,
-// followed by zero padding; pe holds the block's permutation entries.
-template <bool RNA>
+// followed by zero padding; pt is the permutation as byte offsets into a
+// staged row (two 16-bit offsets per dword), or null for the identity.
+template <bool RNA, int SEG>
 __device__ inline void quantize_item(const QuantArgs &q, const LGeo &lg, const ItemGeo &g,
-                                     const int4 (&pe)[8], int64_t row, const uint8_t *sr) {
-  const int K = (int)q.K;
-  const int s = g.s, rem = g.rem, pos = g.pos, b = g.b;
+                                     const uint32_t *pt, int64_t row, const uint8_t *sr) {
+  constexpr int s = SEG;
+  constexpr int m = s == 0 ? 3 : s == 1 ? 4 : s == 2 ? 6 : 8;
+  const int rem = g.rem, pos = g.pos, b = g.b;
   const bool pad = g.pad;
-  const int m = s == 0 ? 3 : s == 1 ? 4 : s == 2 ? 6 : 8;
 
   // gather: pr[i] holds elements 2i (low half) and 2i+1 (high half)
   uint32_t pr[16];
@@ -173,17 +181,34 @@ __device__ inline void quantize_item(const QuantArgs &q, const LGeo &lg, const I
 #pragma unroll
       for (int k = 0; k < 4; ++k) pr[4 * u + k] = d[k];
     }
+  } else if (pt) {
+    // the block's 32 byte offsets (entries outside [0, K) point at the zero
+    // after the row)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const u4 o = *(const u4 *)(pt + 16 * b + 4 * u);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        v2us x;
+        x.x = *(const uint16_t *)(sr + (o[k] & 0xFFFFu));
+        x.y = *(const uint16_t *)(sr + (o[k] >> 16));
+        pr[4 * u + k] = __builtin_bit_cast(uint32_t, x);
+      }
+    }
   } else {
+    // rows too long for the table: the entries from global memory, clamped
+    // to the zero after the row
+    const unsigned K = (unsigned)q.K;
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int4 p = pe[u];
-      // out of range: the zero after the row
-      const uint32_t e0 = *(const uint16_t *)(sr + 2 * min((unsigned)p.x, (unsigned)K));
-      const uint32_t e1 = *(const uint16_t *)(sr + 2 * min((unsigned)p.y, (unsigned)K));
-      const uint32_t e2 = *(const uint16_t *)(sr + 2 * min((unsigned)p.z, (unsigned)K));
-      const uint32_t e3 = *(const uint16_t *)(sr + 2 * min((unsigned)p.w, (unsigned)K));
-      pr[2 * u] = e0 | (e1 << 16);
-      pr[2 * u + 1] = e2 | (e3 << 16);
+      const int4 e = *(const int4 *)(q.perm + b * kBlock + 4 * u);
+      v2us x, y;
+      x.x = *(const uint16_t *)(sr + 2 * min((unsigned)e.x, K));
+      x.y = *(const uint16_t *)(sr + 2 * min((unsigned)e.y, K));
+      y.x = *(const uint16_t *)(sr + 2 * min((unsigned)e.z, K));
+      y.y = *(const uint16_t *)(sr + 2 * min((unsigned)e.w, K));
+      pr[2 * u] = __builtin_bit_cast(uint32_t, x);
+      pr[2 * u + 1] = __builtin_bit_cast(uint32_t, y);
     }
   }
 
@@ -198,13 +223,15 @@ __device__ inline void quantize_item(const QuantArgs &q, const LGeo &lg, const I
   const int E = block_exponent(amax);
 
   // mantissas as exact integer-valued floats: rint(x * 2^(127 + m - 2 - E)),
-  // clamped; a block holding Inf or NaN (E = 255) quantizes to zeros
-  Blk v;
+  // clamped; a block holding Inf or NaN (E = 255) quantizes to zeros, so
+  // its values are replaced by zeros first
   if (E == 255) {
 #pragma unroll
-    for (int i = 0; i < 16; ++i) v.e[i] = v.o[i] = 0.f;
-  } else {
-    const float qmax = (float)((1 << (m - 1)) - 1);
+    for (int i = 0; i < 16; ++i) pr[i] = 0;
+  }
+  Blk v;
+  {
+    constexpr float qmax = (float)((1 << (m - 1)) - 1);
     const float qmin = q.full_clamp ? -(qmax + 1.f) : -qmax;
     const int sh = 127 + m - 2 - E;
 #pragma unroll
@@ -225,8 +252,13 @@ __device__ inline void quantize_item(const QuantArgs &q, const LGeo &lg, const I
 
   if (q.write_rows && !pad) {
     q.exp[row * q.out_erb + b] = (uint8_t)E;
-    const Segs sg{q.n4, q.n6, q.n8, q.n3};
-    uint8_t *p = q.mant + row * q.out_rb + block_info(sg, b).aoff;
+    // the block's offset in the packed row: 12, 16, 24 or 32 bytes per block
+    const int64_t aoff = s == 0 ? 12LL * b
+                       : s == 1 ? 12LL * q.n3 + 16LL * (b - q.n3)
+                       : s == 2 ? 12LL * q.n3 + 16LL * (q.n4 - q.n3) + 24LL * (b - q.n4)
+                                : 12LL * q.n3 + 16LL * (q.n4 - q.n3) + 24LL * q.n6 +
+                                      32LL * (b - q.n4 - q.n6);
+    uint8_t *p = q.mant + row * q.out_rb + aoff;
     if (m == 3) {
       uint32_t w[3];
       pack3(v, w);
@@ -267,22 +299,28 @@ __device__ inline void quantize_item(const QuantArgs &q, const LGeo &lg, const I
     *(u2 *)(stp + 24 * l + 16) = u2{c[4], c[5]};
     scw[4 * l] = (uint8_t)Eu;
   } else {
-    Blk hd, ld;
-    const float f = s == 2 ? 0.125f : 0.0625f, base = s == 2 ? 8.f : 16.f;
+    // digits q = base h + l: the high digits first, then the low digits in
+    // the same registers (h is dead once its codes are formed)
+    Blk d;
+    constexpr float f = s == 2 ? 0.125f : 0.0625f, base = s == 2 ? 8.f : 16.f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      hd.e[i] = floorf(v.e[i] * f);
-      hd.o[i] = floorf(v.o[i] * f);
-      ld.e[i] = fmaf(hd.e[i], -base, v.e[i]);
-      ld.o[i] = fmaf(hd.o[i], -base, v.o[i]);
+      d.e[i] = floorf(v.e[i] * f);
+      d.o[i] = floorf(v.o[i] * f);
     }
     if (s == 2) {
       // lane groups 2 pos (high plane h/2) and 2 pos + 1 (low plane l/16)
       const int lh = 16 * (2 * pos) + r, ll = lh + 16;
-      const v6u ch = to_e3m2(hd, 2.f), cl = to_e3m2(ld, 16.f);
+      const v6u ch = to_e3m2(d, 2.f);
       *(u2 *)(stp + 24 * lh) = u2{ch[0], ch[1]};
       *(u2 *)(stp + 24 * lh + 8) = u2{ch[2], ch[3]};
       *(u2 *)(stp + 24 * lh + 16) = u2{ch[4], ch[5]};
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        d.e[i] = fmaf(d.e[i], -base, v.e[i]);
+        d.o[i] = fmaf(d.o[i], -base, v.o[i]);
+      }
+      const v6u cl = to_e3m2(d, 16.f);
       *(u2 *)(stp + 24 * ll) = u2{cl[0], cl[1]};
       *(u2 *)(stp + 24 * ll + 8) = u2{cl[2], cl[3]};
       *(u2 *)(stp + 24 * ll + 16) = u2{cl[4], cl[5]};
@@ -290,23 +328,40 @@ __device__ inline void quantize_item(const QuantArgs &q, const LGeo &lg, const I
       // E4M3 2h and l/8; lane group 2 plane + half holds elements
       // 16 half..16 half + 15 of the plane, at byte 16 pos
 #pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        *(u4 *)(stp + 32 * (16 * e + r) + 16 * pos) = to_e4m3(hd, e, 0.5f);
-        *(u4 *)(stp + 32 * (16 * (2 + e) + r) + 16 * pos) = to_e4m3(ld, e, 8.f);
+      for (int e = 0; e < 2; ++e)
+        *(u4 *)(stp + 32 * (16 * e + r) + 16 * pos) = to_e4m3(d, e, 0.5f);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        d.e[i] = fmaf(d.e[i], -base, v.e[i]);
+        d.o[i] = fmaf(d.o[i], -base, v.o[i]);
       }
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+        *(u4 *)(stp + 32 * (16 * (2 + e) + r) + 16 * pos) = to_e4m3(d, e, 8.f);
     }
     scw[4 * (16 * (2 * pos) + r)] = (uint8_t)Eu;
     scw[4 * (16 * (2 * pos + 1) + r)] = (uint8_t)Eu;
   }
   // the unused scale bytes of a segment's short last group
   if (rem == 0) {
-    const int S = pick4(lg.S, s), G0 = pick4(lg.G0, s);
+    const int S = lg.S[s], G0 = lg.G0[s];
     for (int k = S; k < (S + kGroupSteps - 1) / kGroupSteps * kGroupSteps; ++k) {
       uint8_t *z = q.img_exp + (row >> 4) * q.a_tile_sc +
                    (int64_t)(G0 + k / kGroupSteps) * 256 + k % kGroupSteps;
       for (int g = 0; g < 4; ++g) z[4 * (16 * g + r)] = 0;
     }
   }
+}
+
+// quantize_item for the item's segment (a branch that is uniform over a
+// wave except where its items straddle two segments)
+template <bool RNA>
+__device__ inline void quantize_item_any(const QuantArgs &q, const LGeo &lg, const ItemGeo &g,
+                                         const uint32_t *pt, int64_t row, const uint8_t *sr) {
+  if (g.s == 0) quantize_item<RNA, 0>(q, lg, g, pt, row, sr);
+  else if (g.s == 1) quantize_item<RNA, 1>(q, lg, g, pt, row, sr);
+  else if (g.s == 2) quantize_item<RNA, 2>(q, lg, g, pt, row, sr);
+  else quantize_item<RNA, 3>(q, lg, g, pt, row, sr);
 }
 
 __device__ inline float bf16f(uint32_t b) { return __uint_as_float(b << 16); }
@@ -442,14 +497,31 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
   if ((nwg & 7) == 0) w = (w & 7) * (nwg >> 3) + (w >> 3);
   const int64_t r0 = w << lgR;
 
-  // The first item's geometry and permutation entries, loaded while the
-  // rows are staged.
   const int nit = nbp << lgR;
-  int4 pe[8];
-  ItemGeo g0{};
-  if (t < nit) {
-    g0 = item_geo(lg, t >> lgR);
-    load_perm(q, g0, pe);
+  const SegStarts ss(lg);
+
+  // The permutation as byte offsets into a staged row, two per dword, in LDS
+  // after the rows (and the normalisation's sums); an entry outside [0, K)
+  // becomes the offset of the zero after the row.  A thread's first
+  // kPermPre groups of four entries are loaded before the rows, so their
+  // latency overlaps the rows' loads.
+  constexpr int kPermPre = 4;
+  uint32_t *pt = nullptr;
+  int4 pp[kPermPre];
+  auto put_perm = [&](int c, const int4 &e) {
+    const unsigned k = (unsigned)K;
+    const uint32_t o0 = 2u * min((unsigned)e.x, k), o1 = 2u * min((unsigned)e.y, k);
+    const uint32_t o2 = 2u * min((unsigned)e.z, k), o3 = 2u * min((unsigned)e.w, k);
+    *(u2 *)(pt + 2 * c) = u2{o0 | (o1 << 16), o2 | (o3 << 16)};
+  };
+  if (q.perm_table) {
+    const int rms = q.rmsnorm ? R * (8 * (K / kBlock) + 4) : 0;
+    pt = (uint32_t *)(smem + ((R * rowB + rms + 15) & ~15));
+#pragma unroll
+    for (int j = 0; j < kPermPre; ++j) {
+      const int c = t + j * nthr;
+      if (c < K / 4) pp[j] = *(const int4 *)(q.perm + 4 * c);
+    }
   }
 
   // Stage the rows.  Each thread issues a batch of loads before it stores
@@ -461,6 +533,7 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
     const int vpr = K / 8, nv = R * vpr;
     const int dq = nthr / vpr, dr = nthr - dq * vpr;
     int lr0 = t / vpr, c0 = t - lr0 * vpr;
+    const bool swiglu = q.swiglu != 0;
     for (int v0 = t; v0 < nv; v0 += nthr * kBatch) {
       u4 d[kBatch];
       int lrk[kBatch], ck[kBatch];
@@ -469,10 +542,13 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
       for (int k = 0; k < kBatch; ++k) {
         lrk[k] = lr;
         ck[k] = c;
-        d[k] = u4{0u, 0u, 0u, 0u};
-        if (v0 + k * nthr < nv && r0 + lr < q.src_rows) {
-          d[k] = *(const u4 *)(q.src + (r0 + lr) * q.ld + 8 * c);
-          if (q.swiglu) d[k] = swiglu8(d[k], *(const u4 *)(q.src2 + (r0 + lr) * q.ld + 8 * c));
+        if (v0 + k * nthr < nv) {
+          if (r0 + lr < q.src_rows) {
+            d[k] = *(const u4 *)(q.src + (r0 + lr) * q.ld + 8 * c);
+            if (swiglu) d[k] = swiglu8(d[k], *(const u4 *)(q.src2 + (r0 + lr) * q.ld + 8 * c));
+          } else {
+            d[k] = u4{0u, 0u, 0u, 0u};
+          }
         }
         c += dr;
         lr += dq;
@@ -498,6 +574,15 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
       }
     }
   }
+  if (pt) {
+#pragma unroll
+    for (int j = 0; j < kPermPre; ++j) {
+      const int c = t + j * nthr;
+      if (c < K / 4) put_perm(c, pp[j]);
+    }
+    for (int c = t + kPermPre * nthr; c < K / 4; c += nthr)
+      put_perm(c, *(const int4 *)(q.perm + 4 * c));
+  }
   if (t < R) *(u4 *)(smem + t * rowB + 2 * K) = u4{0u, 0u, 0u, 0u};
   __syncthreads();
   if (q.rmsnorm) rms_normalise(q, smem, R, rowB, t, nthr, r0);
@@ -505,11 +590,8 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
   for (int it = t; it < nit; it += nthr) {
     const int lr = it & (R - 1);
     const int64_t row = r0 + lr;
-    if (it != t) {
-      g0 = item_geo(lg, it >> lgR);
-      load_perm(q, g0, pe);
-    }
-    if (row < q.out_rows) quantize_item<RNA>(q, lg, g0, pe, row, smem + lr * rowB);
+    if (row < q.out_rows)
+      quantize_item_any<RNA>(q, lg, item_geo(lg, ss, it >> lgR), pt, row, smem + lr * rowB);
   }
   // zero the padding of the packed and exponent rows
   if (q.write_rows && t < R) {
@@ -531,26 +613,40 @@ int quantize_act_padded_blocks(int n3, int n4, int n6, int n8) {
   return nbp;
 }
 
-namespace {
+// Bytes per staged row: the row and its zero padding, plus with RMS
+// normalisation its block sums and its 1/rms.
+static int64_t row_lds(int64_t K, bool rmsnorm) {
+  return 2 * (K + kRowPad) + (rmsnorm ? 8 * (K / kBlock) + 4 : 0);
+}
 
-}  // namespace
+// The permutation's byte-offset table (16-bit offsets, so rows of at most
+// 32767 elements), with 16 bytes of alignment slack.
+static int64_t perm_table_lds(int64_t K) { return 2 * K + 16; }
 
 // Rows per workgroup: the largest power of two (at most 64) whose staged
-// rows fit the LDS budget with at most two items per thread.  More rows per
+// rows fit the LDS budget with at most two items per thread, halved while
+// the rows and the permutation table exceed the LDS.  More rows per
 // workgroup make longer contiguous runs in the operand tiles.
 int quantize_act_rows(int64_t K, int nbp, bool perm, bool rmsnorm) {
-  (void)perm;
-  // a staged row, plus with RMS normalisation its block sums and its 1/rms
-  const int64_t per = 2 * (K + kRowPad) + (rmsnorm ? 8 * (K / kBlock) + 4 : 0);
+  const int64_t per = row_lds(K, rmsnorm);
   int r = 1;
   while (r < 64 && 2 * r * per <= kLdsBudget && (int64_t)nbp * 2 * r <= 2 * kMaxThreads)
     r *= 2;
+  if (perm && K <= kPermTableMaxK)
+    while (r > 1 && r * per + perm_table_lds(K) > kMaxLds) r >>= 1;
   return r;
 }
 
+// Whether the permutation is gathered through the LDS table.
+static bool quantize_act_table(int64_t K, int nbp, bool perm, bool rmsnorm) {
+  return perm && K <= kPermTableMaxK &&
+         quantize_act_rows(K, nbp, perm, rmsnorm) * row_lds(K, rmsnorm) + perm_table_lds(K) <=
+             kMaxLds;
+}
+
 int64_t quantize_act_lds(int64_t K, int nbp, bool perm, bool rmsnorm) {
-  return (int64_t)quantize_act_rows(K, nbp, perm, rmsnorm) *
-         (2 * (K + kRowPad) + (rmsnorm ? 8 * (K / kBlock) + 4 : 0));
+  return (int64_t)quantize_act_rows(K, nbp, perm, rmsnorm) * row_lds(K, rmsnorm) +
+         (quantize_act_table(K, nbp, perm, rmsnorm) ? perm_table_lds(K) : 0);
 }
 
 hipError_t launch_quantize_act(const QuantArgs &args, hipStream_t stream) {
@@ -563,6 +659,7 @@ hipError_t launch_quantize_act(const QuantArgs &args, hipStream_t stream) {
   a.lg_rows = lg;
   a.rows_per_wg = R;
   a.stage = 0;
+  a.perm_table = quantize_act_table(a.K, nbp, perm, a.rmsnorm != 0) ? 1 : 0;
   const int64_t grid = (a.out_rows + R - 1) / R;
   if (grid <= 0) return hipSuccess;
   const int64_t lds = quantize_act_lds(a.K, nbp, perm, a.rmsnorm != 0);

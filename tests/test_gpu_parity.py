@@ -95,6 +95,31 @@ def test_out_of_range_permutation_entries_read_zero():
     assert np.array_equal(q, qa) and np.array_equal(E, ea) and pad_ok
 
 
+def test_long_rows_permutation_from_global_memory():
+    """Rows longer than 32767 elements gather the permutation from global
+    memory instead of the LDS offset table; an out-of-range entry still
+    reads zero."""
+    K = 33280
+    case = W.random_case(31, 5, K, 16, (K // 32 - 20, 12, 8), perm="random")
+    perm = case.perm.copy()
+    perm[[7, 20000]] = [K + 3, -1]
+    say("long-rows-perm", case.M, K)
+    fmtg = mxq.Format(K, case.widths, torch.from_numpy(perm).cuda())
+    a = to_dev_bf16(case.a_bits)
+    am, ae = mxq.quantize_act(a, fmtg)
+    rows, exps = mxq.quantize_rows(a, fmtg)
+    torch.cuda.synchronize()
+    src = np.zeros((case.M, K + 32), np.uint16)
+    src[:, :K] = case.a_bits
+    p2 = perm.copy()
+    p2[[7, 20000]] = K
+    qa, ea = oracle.quantize(src, K=K, perm=p2, widths=case.widths)
+    assert np.array_equal(rows.cpu().numpy(), oracle.pack_act(qa, case.widths))
+    assert np.array_equal(exps.cpu().numpy()[:, :K // 32], ea)
+    q, E, pad_ok = decode_act(am.cpu().numpy(), ae.cpu().numpy(), case.widths, case.M)
+    assert np.array_equal(q, qa) and np.array_equal(E, ea) and pad_ok
+
+
 def test_strided_inputs_and_outputs():
     case = W.random_case(12, 48, 256, 40, (6, 1, 1), perm="scales")
     say("strided")
