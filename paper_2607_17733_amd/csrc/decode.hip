@@ -20,11 +20,12 @@
 // loads, so each load serves as many products as possible.  Each weight
 // step is read once for all of the launch's 16-row activation tiles (up to
 // four: M <= 64).  A workgroup
-// owns a pair of 16-column slabs (one activation load feeds both); its nw
-// waves (2 to 8, the most at which every pair is resident by the kernel's
-// register occupancy) take every nw-th group of four steps; a group's scale
-// bytes are one word per lane and operand.  The waves' fp32 accumulators
-// meet in LDS in a fixed order.
+// owns a unit of four 16-column slabs, or two where four would leave CUs
+// without a workgroup (one activation load feeds all of them); its nw waves
+// (2 to 8, the most at which every unit is resident by the kernel's register
+// occupancy) take every nw-th group of four steps; a group's scale bytes are
+// one word per lane and operand.  The waves' fp32 accumulators meet in LDS
+// in a fixed order.
 #include <atomic>
 #include <type_traits>
 
@@ -92,26 +93,29 @@ __device__ inline uint32_t lo_codes(uint32_t w) {
   return FULL ? (w & 0x0F0F0F0Fu) : (w & 0x8F8F8F8Fu);
 }
 
-// T: 16-row activation tiles (M <= 16 T).
-template <bool FULL, int T>
+// T: 16-row activation tiles (M <= 16 T); SL: 16-column slabs per
+// workgroup (2 or 4: one activation load feeds all of them).
+template <bool FULL, int T, int SL>
 __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g) {
-  __shared__ v4f red[kMaxWaves][2][64];
+  __shared__ v4f red[kMaxWaves][SL][64];
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   const int nw = blockDim.x >> 6;
   const int grp = lane >> 4, line = lane & 15;
   const LGeo lg(g.n3, g.n4, g.n6, g.n8);
-  // The four slab pairs of a super-slab run on one XCD (workgroups b, b + 8,
-  // b + 16, b + 24 of a round-robin dispatch), so its L2 reads each step
-  // record of the super-slab and its scale block whole.
-  int64_t pair = blockIdx.x;
-  if ((gridDim.x & 31) == 0) {
-    const int64_t x = pair & 7, i = pair >> 3;
-    pair = (((i >> 2) << 3) + x) * 4 + (i & 3);
+  // The units of a super-slab run on one XCD (workgroups b, b + 8, ... of a
+  // round-robin dispatch), so its L2 reads each step record of the
+  // super-slab and its scale block whole.
+  constexpr int PPS = kWSlabs / SL;                  // units per super-slab
+  int64_t unit = blockIdx.x;
+  if ((gridDim.x % (8 * PPS)) == 0) {
+    const int64_t x = unit & 7, i = unit >> 3;
+    unit = ((i / PPS) * 8 + x) * PPS + (i % PPS);
   }
-  const int64_t ss = pair >> 2;                      // super-slab
-  const int n0 = 2 * (int)(pair & 3);                // first slab of the pair
-  const bool two = (pair * 32 + 16) < g.N;           // the second slab has columns
+  const int64_t ss = unit / PPS;                     // super-slab
+  const int n0 = SL * (int)(unit % PPS);             // first slab of the unit
+  // slabs past N (inside the padded super-slab) read the unit's first slab
+  auto live = [&](int sl) { return unit * 16 * SL + 16 * sl < g.N; };
   const uint8_t *wsup = g.w_mant + ss * g.w_super;
   const uint8_t *wsc = g.w_exp + ss * g.w_super_sc + 32 * lane;
   // Lanes of rows >= M read the first row of their tile (same addresses as a
@@ -119,9 +123,11 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
   int alane[T];
 #pragma unroll
   for (int t = 0; t < T; ++t) alane[t] = 16 * t + line < g.M ? lane : (lane & ~15);
-  v4f acc[T][2];
+  v4f acc[T][SL];
 #pragma unroll
-  for (int t = 0; t < T; ++t) acc[t][0] = acc[t][1] = v4f{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < T; ++t)
+#pragma unroll
+    for (int sl = 0; sl < SL; ++sl) acc[t][sl] = v4f{0.f, 0.f, 0.f, 0.f};
 
   auto run_group = [&](auto segc, int gi) {
     constexpr int SEG = decltype(segc)::value;
@@ -133,9 +139,9 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
     const u4 s0 = stream_load((const u4 *)(wsc + (int64_t)gi * 2048));
     const u4 s1 = stream_load((const u4 *)(wsc + (int64_t)gi * 2048 + 16));
     // step k's byte of slab b lies in dword 2k + b / 4
-    uint32_t sw[2];
+    uint32_t sw[SL];
 #pragma unroll
-    for (int sl = 0; sl < 2; ++sl) {
+    for (int sl = 0; sl < SL; ++sl) {
       const int b = n0 + sl;
       const uint32_t d0 = b < 4 ? s0[0] : s0[1], d1 = b < 4 ? s0[2] : s0[3];
       const uint32_t d2 = b < 4 ? s1[0] : s1[1], d3 = b < 4 ? s1[2] : s1[3];
@@ -154,9 +160,9 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
     // raw loads of step k (fields a segment does not use stay unread)
     struct Raw {
       u4 a0[T], a1[T];      // activation lane data (24 or 32 bytes) per tile
-      u4 p[2], h[2];        // weight bytes of the two slabs
-      u2 x[2];
-      uint32_t z[2];
+      u4 p[SL], h[SL];      // weight bytes of the slabs
+      u2 x[SL];
+      uint32_t z[SL];
     };
     auto load = [&](int k) __attribute__((always_inline)) {
       Raw r;
@@ -175,8 +181,8 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
         }
       }
 #pragma unroll
-      for (int sl = 0; sl < 2; ++sl) {
-        const uint8_t *w = (sl && two) ? w0 + CB : w0;
+      for (int sl = 0; sl < SL; ++sl) {
+        const uint8_t *w = live(sl) ? w0 + sl * CB : w0;
         if (SEG == 0 && !FULL) {
           r.x[sl] = stream_load((const u2 *)(w + 8 * lane));
           r.z[sl] = stream_load((const uint32_t *)(w + 512 + 4 * lane));
@@ -203,9 +209,9 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
         a[t] = v8i{(int)r.a0[t][0], (int)r.a0[t][1], (int)r.a0[t][2], (int)r.a0[t][3],
                    (int)r.a1[t][0], (int)r.a1[t][1], (int)r.a1[t][2], (int)r.a1[t][3]};
       if (SEG <= 1) {
-        uint32_t d[2][6];
+        uint32_t d[SL][6];
 #pragma unroll
-        for (int sl = 0; sl < 2; ++sl) {
+        for (int sl = 0; sl < SL; ++sl) {
           if (SEG == 0 && !FULL) {
             const uint32_t x[3] = {r.x[sl][0], r.x[sl][1], r.z[sl]};
             unfold3(x, d[sl]);
@@ -221,15 +227,15 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
         }
         constexpr int FB = SEG == 0 ? kFmtE2M3 : kFmtE3M2;
 #pragma unroll
-        for (int t = 0; t < T; ++t) {
-          acc[t][0] = mfma<kFmtE3M2, FB, k>(a[t], six(d[0]), acc[t][0], sa[t], sw[0]);
-          acc[t][1] = mfma<kFmtE3M2, FB, k>(a[t], six(d[1]), acc[t][1], sa[t], sw[1]);
-        }
+        for (int t = 0; t < T; ++t)
+#pragma unroll
+          for (int sl = 0; sl < SL; ++sl)
+            acc[t][sl] = mfma<kFmtE3M2, FB, k>(a[t], six(d[sl]), acc[t][sl], sa[t], sw[sl]);
       } else if (SEG == 2) {
         // the weights' high plane in every lane (scale E + 3) gives the
         // products hh and lh, their low plane (scale E) hl and ll
 #pragma unroll
-        for (int sl = 0; sl < 2; ++sl) {
+        for (int sl = 0; sl < SL; ++sl) {
           const uint32_t xl[4] = {r.p[sl][0], r.p[sl][1], r.p[sl][2], r.p[sl][3]};
           uint32_t L[6], H[6];
           unfold4(xl, L);
@@ -251,7 +257,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
         // the weights' high digits in every lane (scale E + 4), then their
         // low digits (scale E)
 #pragma unroll
-        for (int sl = 0; sl < 2; ++sl) {
+        for (int sl = 0; sl < SL; ++sl) {
           v8i bh, bl;
 #pragma unroll
           for (int i = 0; i < 8; ++i) {
@@ -314,13 +320,14 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
 #pragma unroll
   for (int t = 0; t < T; ++t) {
     if (t > 0) __syncthreads();
-    red[wave][0][lane] = acc[t][0];
-    red[wave][1][lane] = acc[t][1];
+#pragma unroll
+    for (int sl = 0; sl < SL; ++sl) red[wave][sl][lane] = acc[t][sl];
     __syncthreads();
-    if (wave < 2 && (wave == 0 || two)) {
-      v4f y = red[0][wave][lane];
-      for (int w = 1; w < nw; ++w) y += red[w][wave][lane];
-      const int64_t col = pair * 32 + 16 * wave + line;
+    for (int sl = wave; sl < SL; sl += nw) {
+      if (!live(sl)) continue;
+      v4f y = red[0][sl][lane];
+      for (int w = 1; w < nw; ++w) y += red[w][sl][lane];
+      const int64_t col = unit * 16 * SL + 16 * sl + line;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 16 * t + 4 * grp + i;
@@ -332,13 +339,30 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
 
 }  // namespace
 
-// Waves per workgroup (one workgroup per pair of 16-column slabs): the most
-// (up to kMaxWaves) at which every pair is resident at once, by the kernel's
-// own occupancy (queried once per kernel and size; every GPU this runs on is
-// the same model).
-template <bool FULL, int T>
-static int decode_waves(int64_t pairs) {
+// Waves per workgroup (one workgroup per unit of SL 16-column slabs): the
+// most (up to kMaxWaves) at which every unit is resident at once, by the
+// kernel's own occupancy (queried once per kernel and size; every GPU this
+// runs on is the same model).
+template <bool FULL, int T, int SL>
+static int decode_waves(int64_t units, int cus) {
   static std::atomic<int> per_cu[kMaxWaves + 1] = {};
+  for (int w = kMaxWaves; w > 2; --w) {
+    int per = per_cu[w].load(std::memory_order_relaxed);
+    if (per == 0) {
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, gemm_decode_kernel<FULL, T, SL>,
+                                                       64 * w, 0) != hipSuccess ||
+          per <= 0)
+        break;
+      per_cu[w].store(per, std::memory_order_relaxed);
+    }
+    if ((int64_t)per * cus >= units) return w;
+  }
+  return 2;
+}
+
+hipError_t launch_gemm_decode(const GemmArgs &a, hipStream_t stream) {
+  const int64_t tiles = (a.M + 15) / 16;
+  if (tiles < 1 || tiles > kDecodeTiles) return hipErrorInvalidValue;
   int cus = 256;
   int dev = 0;
   if (hipGetDevice(&dev) == hipSuccess) {
@@ -347,28 +371,21 @@ static int decode_waves(int64_t pairs) {
         n > 0)
       cus = n;
   }
-  for (int w = kMaxWaves; w > 2; --w) {
-    int per = per_cu[w].load(std::memory_order_relaxed);
-    if (per == 0) {
-      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, gemm_decode_kernel<FULL, T>, 64 * w,
-                                                       0) != hipSuccess || per <= 0)
-        break;
-      per_cu[w].store(per, std::memory_order_relaxed);
-    }
-    if ((int64_t)per * cus >= pairs) return w;
-  }
-  return 2;
-}
-
-hipError_t launch_gemm_decode(const GemmArgs &a, hipStream_t stream) {
-  const int64_t pairs = (a.N + 31) / 32;
-  const int64_t tiles = (a.M + 15) / 16;
-  if (tiles < 1 || tiles > kDecodeTiles) return hipErrorInvalidValue;
+  // four slabs per workgroup (half the activation loads per weight byte)
+  // when that still gives every CU a workgroup, else two
+  const bool quad = (a.N + 63) / 64 >= cus;
   auto go = [&](auto fc, auto tc) {
     constexpr bool FULL = decltype(fc)::value;
     constexpr int T = decltype(tc)::value;
-    const dim3 grid((unsigned)pairs), block((unsigned)(64 * decode_waves<FULL, T>(pairs)));
-    hipLaunchKernelGGL((gemm_decode_kernel<FULL, T>), grid, block, 0, stream, a);
+    if (quad) {
+      const int64_t units = (a.N + 63) / 64;
+      const dim3 grid((unsigned)units), block((unsigned)(64 * decode_waves<FULL, T, 4>(units, cus)));
+      hipLaunchKernelGGL((gemm_decode_kernel<FULL, T, 4>), grid, block, 0, stream, a);
+    } else {
+      const int64_t units = (a.N + 31) / 32;
+      const dim3 grid((unsigned)units), block((unsigned)(64 * decode_waves<FULL, T, 2>(units, cus)));
+      hipLaunchKernelGGL((gemm_decode_kernel<FULL, T, 2>), grid, block, 0, stream, a);
+    }
   };
   using F = std::false_type;
   using Tr = std::true_type;
