@@ -360,17 +360,18 @@ static int decode_waves(int64_t units, int cus) {
   return 2;
 }
 
+int device_cu_count() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) == hipSuccess &&
+      hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
+    return n;
+  return 256;
+}
+
 hipError_t launch_gemm_decode(const GemmArgs &a, hipStream_t stream) {
   const int64_t tiles = (a.M + 15) / 16;
   if (tiles < 1 || tiles > kDecodeTiles) return hipErrorInvalidValue;
-  int cus = 256;
-  int dev = 0;
-  if (hipGetDevice(&dev) == hipSuccess) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-        n > 0)
-      cus = n;
-  }
+  const int cus = device_cu_count();
   // four slabs per workgroup (half the activation loads per weight byte)
   // when that still gives every CU a workgroup, else two
   const bool quad = (a.N + 63) / 64 >= cus;

@@ -29,7 +29,10 @@
 // Tiling: 256x128 outputs per workgroup (one weight super-slab) of four
 // waves, one per SIMD, so that each wave has the whole register file: wave
 // w owns rows 64w..64w+63 x all 128 columns = 2x4 tiles of 32x32 fp32
-// accumulators, and walks every step.
+// accumulators, and walks every step.  Grids of fewer such workgroups than
+// the device has CUs take 128x128 tiles instead (wave w: rows 32w..32w+31,
+// 1x4 tiles; two workgroups per CU fit): twice the workgroups, each wave
+// half the products per step.
 //   - activations go straight from the image into registers -- each row is
 //     used by exactly one wave -- one step ahead, in two register sets, two
 //     loads in each of the step's first four positions;
@@ -50,6 +53,8 @@
 #include "mxq_device.h"
 #include "mxq_internal.h"
 
+#include <type_traits>
+
 namespace mxq {
 
 namespace {
@@ -61,19 +66,18 @@ typedef unsigned u4 __attribute__((ext_vector_type(4)));
 typedef unsigned u2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int BM = 256, BN = kWCols, NT = 256, kWaves = NT / 64;
+constexpr int BN = kWCols, NT = 256, kWaves = NT / 64;
 constexpr int kFmtE4M3 = 0, kFmtE2M3 = 2, kFmtE3M2 = 3;
 constexpr int kWStages = 8;                  // weight ring: one stage per step
 constexpr int kWAhead = 4;                   // weight stages loaded ahead
 constexpr int kASets = 2;                    // activation register sets (one ahead)
-// Loads per wave and step besides the weights: per 32-row tile and K-chunk
-// the lane data (two loads) and the scale word, then the step's weight
-// scale bytes (two).
-constexpr int kALoads = 2 * 2 * 2;
+// Activation loads per wave and step: per 32-row tile (TM of them) and
+// K-chunk the lane data (two loads).
+template <int TM> constexpr int kALoads = 2 * 2 * TM;
 // Loads per wave and scale group: the activation scale word per 32-row tile
 // and K-chunk, then the group's weight scale bytes (two 16-byte pieces per
 // K-chunk).
-constexpr int kGLoads = 2 * 2 + 2 * 2;
+template <int TM> constexpr int kGLoads = 2 * TM + 2 * 2;
 
 template <int S> struct Int { static constexpr int v = S; };
 
@@ -163,9 +167,12 @@ __device__ inline uint32_t lo_codes(uint32_t w) {
   return FULL ? (w & 0x0F0F0F0Fu) : (w & 0x8F8F8F8Fu);
 }
 
-template <bool FULL>
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
+// TM: 32-row tiles per wave (2: 256-row workgroup tiles, one workgroup per
+// CU; 1: 128-row tiles, two per CU).
+template <bool FULL, int TM>
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(3 - TM, 3 - TM)))
 void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
+  constexpr int BM = 128 * TM;
   using C = Cfg<FULL>;
   __shared__ __attribute__((aligned(16))) u4 lds[C::kRing / 16];
   const int t = threadIdx.x, lane = t & 63;
@@ -191,13 +198,13 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   const int nsteps = lg.nsteps;
   char *const ring = (char *)lds;
 
-  // This wave's rows: two 32-row tiles = four 16-row image tiles (tiles
+  // This wave's rows: TM 32-row tiles = 2 TM 16-row image tiles (tiles
   // past the last one read the last tile; those rows are never stored).  The
   // activation resources start at the wave's first 16-row tile (64-bit
   // arithmetic), so the 32-bit buffer offsets stay below 4 image tiles; the
   // host rejects shapes where 16 tiles pass INT32_MAX.
   const int64_t last = (g.M - 1) / kATileRows;
-  const int64_t ta = min(row0 / kATileRows + 4 * wave, last);
+  const int64_t ta = min(row0 / kATileRows + 2 * TM * wave, last);
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
       (void *)(g.a_mant + ta * g.a_tile), 0,
       (int)min((last + 1 - ta) * g.a_tile, (int64_t)0x7fffffff), 0x00020000);
@@ -210,13 +217,13 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   // The lane (lh, x) of a 32-wide tile reads, for K-chunk c, lane
   // lk(c) = 16 (2 c + lh) + x % 16 of 16-row image tile (or slab) 2 tm + x / 16.
   const int lk0 = 16 * lh + l16, lk1 = lk0 + 32;
-  int vt[2];                                 // the lane's image tile of row tile tm
+  int vt[TM];                                 // the lane's image tile of row tile tm
 #pragma unroll
-  for (int tm = 0; tm < 2; ++tm) vt[tm] = (int)(min(ta + 2 * tm + hx, last) - ta);
+  for (int tm = 0; tm < TM; ++tm) vt[tm] = (int)(min(ta + 2 * tm + hx, last) - ta);
 
-  v16f acc[2][4];
+  v16f acc[TM][4];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < TM; ++a)
 #pragma unroll
     for (int n = 0; n < 4; ++n) acc[a][n] = v16f{};
 
@@ -224,7 +231,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   // data (24 bytes of FP6 codes or 32 of FP8 codes) and the scale word; the
   // step's weight scale bytes for each K-chunk (slab n at byte n).
   struct ASet {
-    v8i d[2][2];
+    v8i d[TM][2];
   };
   ASet xa[kASets];
   // Scale words of a group of four steps: per 32-row tile and K-chunk the
@@ -232,7 +239,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   // weight scale bytes (slab n's byte of step k at 8 k + n).  Set 0 serves
   // the current group; set 1 receives the next group's.
   struct GScale {
-    uint32_t sc[2][2];
+    uint32_t sc[TM][2];
     u4 ws[2][2];
   };
   GScale gsc[2];
@@ -282,7 +289,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
     }
   };
   // Activation loads of step st (clamped to the last) into register set S,
-  // part = the (32-row tile, K-chunk) pair: tile part & 1, chunk part >> 1.
+  // part = the (32-row tile, K-chunk) pair: tile part % TM, chunk part / TM.
   // A wave that issues its loads in bursts stalls on them; spread over the
   // positions, they are accepted while the products run.
   auto issue_a = [&](auto set_tag, int st, int part) __attribute__((always_inline)) {
@@ -290,7 +297,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
     st = min(st, nsteps - 1);
     const int so = a_off(st);
     const bool wide = st >= lg.st0[3];
-    const int tm = part & 1, c = part >> 1;
+    const int tm = part % TM, c = part / TM;
     const int lk = c ? lk1 : lk0;
     const int vb = vt[tm] * (int)g.a_tile;
     const int olo = wide ? 32 * lk0 + 16 * c : 24 * lk;
@@ -306,7 +313,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
     grp = min(grp, lg.ngroups - 1);
     if (part == 0) {
 #pragma unroll
-      for (int tm = 0; tm < 2; ++tm)
+      for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
         for (int c = 0; c < 2; ++c)
           gsc[G].sc[tm][c] = __builtin_amdgcn_raw_buffer_load_b32(
@@ -415,13 +422,14 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
     if (SEG <= 1) {
       constexpr int FB = SEG == 0 ? kFmtE2M3 : kFmtE3M2;
       const int tm = half;
+      if (tm >= TM) return;
       acc[tm][tn] = (tn & 1)
           ? mma<kFmtE3M2, FB, K, 2>(x.d[tm][c], B.b0, acc[tm][tn], gsc[0].sc[tm][c], wd)
           : mma<kFmtE3M2, FB, K, 0>(x.d[tm][c], B.b0, acc[tm][tn], gsc[0].sc[tm][c], wd);
     } else {
       const uint32_t e = (wd >> (16 * (tn & 1))) & 0xFFu;
 #pragma unroll
-      for (int tm = 0; tm < 2; ++tm) {
+      for (int tm = 0; tm < TM; ++tm) {
         if (SEG == 2)
           acc[tm][tn] = half == 0
               ? mma<kFmtE3M2, kFmtE3M2, K, 0>(x.d[tm][c], B.b0, acc[tm][tn], gsc[0].sc[tm][c],
@@ -438,7 +446,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   // The next group's scales become current (the weight dwords shifted).
   auto next_group = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int tm = 0; tm < 2; ++tm)
+    for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
       for (int c = 0; c < 2; ++c) gsc[0].sc[tm][c] = gsc[1].sc[tm][c];
 #pragma unroll
@@ -474,7 +482,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
 #pragma unroll
     for (int p = 0; p < 8; ++p) {
       if (p == 4) {
-        wait_loads<2 * kALoads + 2 * C::kWLoads>();
+        wait_loads<2 * kALoads<TM> + 2 * C::kWLoads>();
         barrier();
         issue_w(s + kWAhead, 0, 1);
       }
@@ -483,7 +491,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
       // new segment, whose loop reads them again)
       if (p + 2 < 8) read_w(seg, W, (p + 2) & 3, p + 2);
       else read_w(seg, Wn, (p + 2) & 3, p - 6);
-      if (p < 4) issue_a(Int<(S + 1) % kASets>{}, s + 1, p);
+      if (p < 2 * TM) issue_a(Int<(S + 1) % kASets>{}, s + 1, p);
       if (p >= 4 && p < 7 && K == 0) issue_g(Int<1>{}, grp + 1, p - 4);
       __builtin_amdgcn_sched_barrier(0);
       // the products interleaved with the next operand's restore: a wave
@@ -550,12 +558,12 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   // weights of steps 2 and 3, and the wait for the stage of step 0.
   issue_w(0, 0, C::kWLoads);
   issue_w(1, 0, C::kWLoads);
-  for (int pp = 0; pp < 4; ++pp) issue_a(Int<0>{}, 0, pp);
+  for (int pp = 0; pp < 2 * TM; ++pp) issue_a(Int<0>{}, 0, pp);
   for (int pp = 0; pp < 3; ++pp) issue_g(Int<1>{}, 0, pp);
   issue_w(2, 0, C::kWLoads);
   issue_w(3, 0, C::kWLoads);
   __builtin_amdgcn_sched_barrier(0);
-  wait_loads<3 * C::kWLoads + kALoads + kGLoads>();
+  wait_loads<3 * C::kWLoads + kALoads<TM> + kGLoads<TM>>();
   barrier();
   next_group();
 
@@ -571,12 +579,12 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   const bool vec = (g.ldy & 3) == 0 && ((uintptr_t)g.y & 15) == 0 && col0 + BN <= g.N;
   const int j = l32 & 3;
 #pragma unroll
-  for (int tm = 0; tm < 2; ++tm)
+  for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
     for (int tn = 0; tn < 4; ++tn)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int rr = wave * 64 + tm * 32 + 8 * q + 4 * lh, cc = tn * 32 + l32;
+        const int rr = wave * 32 * TM + tm * 32 + 8 * q + 4 * lh, cc = tn * 32 + l32;
         v4f s = v4f{acc[tm][tn][4 * q], acc[tm][tn][4 * q + 1], acc[tm][tn][4 * q + 2],
                     acc[tm][tn][4 * q + 3]};
         // lane (quad k, j) now: row rr + j, columns (cc & ~3) .. + 3
@@ -597,23 +605,32 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
 }  // namespace
 
 hipError_t launch_gemm_prefill(const GemmArgs &a, hipStream_t stream) {
-  const int mtiles = (int)((a.M + BM - 1) / BM), ntiles = (int)((a.N + BN - 1) / BN);
-  // Split the tile grid into 8 blocks (one per XCD) along rows x columns,
-  // minimising the bytes each XCD reads: an activation tile (256 rows) weighs
-  // about twice a weight tile (128 columns).
-  int gm = 0, gn = 0, best = 0;
-  for (int m = 1; m <= 8; m *= 2) {
-    const int n = 8 / m;
-    if (mtiles % m || ntiles % n) continue;
-    const int cost = 2 * (mtiles / m) + ntiles / n;
-    if (gm == 0 || cost < best) gm = m, gn = n, best = cost;
-  }
-  if (a.full)
-    hipLaunchKernelGGL(gemm_prefill_kernel<true>, dim3((unsigned)(mtiles * ntiles)), dim3(NT), 0,
-                       stream, a, mtiles, ntiles, gm, gn);
-  else
-    hipLaunchKernelGGL(gemm_prefill_kernel<false>, dim3((unsigned)(mtiles * ntiles)), dim3(NT), 0,
-                       stream, a, mtiles, ntiles, gm, gn);
+  auto go = [&](auto fc, auto tc) {
+    constexpr bool FULL = decltype(fc)::value;
+    constexpr int TM = decltype(tc)::value;
+    constexpr int BM = 128 * TM;
+    const int mtiles = (int)((a.M + BM - 1) / BM), ntiles = (int)((a.N + BN - 1) / BN);
+    // Split the tile grid into 8 blocks (one per XCD) along rows x columns,
+    // minimising the bytes each XCD reads: an activation tile weighs about
+    // TM times a weight tile.
+    int gm = 0, gn = 0, best = 0;
+    for (int m = 1; m <= 8; m *= 2) {
+      const int n = 8 / m;
+      if (mtiles % m || ntiles % n) continue;
+      const int cost = TM * (mtiles / m) + ntiles / n;
+      if (gm == 0 || cost < best) gm = m, gn = n, best = cost;
+    }
+    hipLaunchKernelGGL((gemm_prefill_kernel<FULL, TM>), dim3((unsigned)(mtiles * ntiles)), dim3(NT),
+                       0, stream, a, mtiles, ntiles, gm, gn);
+  };
+  // 128-row tiles when 256-row tiles would leave CUs without a workgroup
+  // (measured at K = N = 4096: 29-33 us against 37-41 us for M = 65 to
+  // 1024; 256-row tiles are faster from one workgroup per CU up).  The
+  // full clamp's 12 KB weight stages fit one workgroup per CU only.
+  const int64_t wg256 = ((a.M + 255) / 256) * ((a.N + BN - 1) / BN);
+  if (a.full) go(std::true_type{}, std::integral_constant<int, 2>{});
+  else if (wg256 < device_cu_count()) go(std::false_type{}, std::integral_constant<int, 1>{});
+  else go(std::false_type{}, std::integral_constant<int, 2>{});
   return hipGetLastError();
 }
 

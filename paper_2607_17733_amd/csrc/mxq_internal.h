@@ -81,6 +81,8 @@ hipError_t launch_quantize_act(const QuantArgs &args, hipStream_t s);
 int quantize_act_padded_blocks(int n3, int n4, int n6, int n8);
 int quantize_act_rows(int64_t K, int padded_blocks, bool perm, bool rmsnorm = false);
 int64_t quantize_act_lds(int64_t K, int padded_blocks, bool perm, bool rmsnorm = false);
+// Compute units of the current device (256 if the query fails).
+int device_cu_count();
 hipError_t launch_gemm_prefill(const GemmArgs &args, hipStream_t s);
 hipError_t launch_gemm_partials(const GemmArgs &args, hipStream_t s);
 hipError_t launch_gemm_decode(const GemmArgs &args, hipStream_t s);

@@ -68,6 +68,24 @@ def test_random_shapes(M, K, N, counts, perm):
     _full_check(case)
 
 
+# Prefill kernel variants: small grids take 128-row workgroup tiles, grids of
+# at least one 256-row workgroup per CU (256 on MI355X) the 256-row tiles;
+# the full clamp always takes the 256-row tiles.  Ragged M and N in each.
+PREFILL_VARIANTS = [
+    # M, K, N, (n4, n6, n8), perm, round, clamp
+    (513, 256, 10900, (4, 2, 2), "random", "rne", "sym"),   # 3 x 86 256-row tiles
+    (100, 256, 200, (4, 2, 2), "random", "rne", "full"),
+    (300, 320, 150, (6, 2, 2), "scales", "rna", "full"),
+    (130, 384, 140, (0, 12, 0), "identity", "rna", "sym"),
+]
+
+
+@pytest.mark.parametrize("M,K,N,counts,perm,round_,clamp", PREFILL_VARIANTS)
+def test_prefill_variants(M, K, N, counts, perm, round_, clamp):
+    case = W.random_case(M * 11 + N, M, K, N, counts, perm=perm)
+    _full_check(case, round_, clamp)
+
+
 def test_identity_format_matches_explicit_identity():
     case = W.random_case(5, 40, 256, 64, (5, 2, 1), perm="identity")
     _full_check(case, identity=True)
@@ -147,7 +165,7 @@ def test_strided_inputs_and_outputs():
 def test_special_values():
     """Zero rows, subnormals, huge values, Inf and NaN blocks."""
     g = np.random.default_rng(3)
-    M, K, N = 24, 128, 32
+    M, K, N = 80, 128, 32                           # M > 64: the prefill kernel
     a = g.standard_normal((M, K)).astype(np.float32)
     a[0] = 0.0                                      # zero row
     a[1] = g.standard_normal(K) * 1e-39             # subnormal values
@@ -179,7 +197,7 @@ def _spread_case(seed, M, K, N, counts, spread=15):
                         W.widths_from_counts(*counts))
 
 
-@pytest.mark.parametrize("M", [8, 40])
+@pytest.mark.parametrize("M", [8, 40, 100])             # decode, decode, prefill
 def test_wide_exponent_spread(M):
     """Adversarial accumulation case: block exponents spread over 30 binades
     inside every matrix-core step.  Bit-exact operands as everywhere; the
