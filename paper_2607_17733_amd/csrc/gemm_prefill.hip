@@ -68,7 +68,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int BN = kWCols, NT = 256, kWaves = NT / 64;
 constexpr int kFmtE4M3 = 0, kFmtE2M3 = 2, kFmtE3M2 = 3;
-constexpr int kWStages = 8;                  // weight ring: one stage per step
+constexpr int kWStages = 8;                  // weight ring: one stage per step (a power of two)
 constexpr int kWAhead = 4;                   // weight stages loaded ahead
 constexpr int kASets = 2;                    // activation register sets (one ahead)
 // Activation loads per wave and step: per 32-row tile (TM of them) and
@@ -88,6 +88,7 @@ template <bool FULL> struct Cfg {
   static constexpr int kWLoads = kPieces / kWaves;        // per wave and step
 };
 static_assert(Cfg<true>::kRing <= 160 * 1024, "LDS");
+static_assert((kWStages & (kWStages - 1)) == 0, "stage index by mask");
 static_assert(Cfg<true>::kPieces % kWaves == 0 && Cfg<false>::kPieces % kWaves == 0, "pieces");
 
 // The scale operands are dwords whose byte OA (activations) / OB (weights)
@@ -244,9 +245,9 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   };
   GScale gsc[2];
 
-  // Offsets of step st in the images, its scale group and its byte, in
-  // branch-free scalar arithmetic (a segment's steps before st are
-  // clamp(st - st0, 0, S)).
+  // Offsets of step st in the images, in branch-free scalar arithmetic (a
+  // segment's steps before st are clamp(st - st0, 0, S)).  Scale groups are
+  // counted as the segments walk them (a segment's steps start a group).
   constexpr int CB0 = w_chunk_bytes(0, FULL), CB1 = w_chunk_bytes(1, FULL),
                 CB2 = w_chunk_bytes(2, FULL), CB3 = w_chunk_bytes(3, FULL);
   auto dseg = [&](int st, int k) __attribute__((always_inline)) {
@@ -267,12 +268,6 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
     cb = st >= lg.st0[3] ? CB3 : cb;
     return cb * kWSlabs / 1024;
   };
-  auto s_grp = [&](int st) __attribute__((always_inline)) {
-    // whole groups of the earlier segments, then the groups before st
-    return ((dseg(st, 0) + (st >= lg.st0[1] ? 3 : 0)) >> 2) +
-           ((dseg(st, 1) + (st >= lg.st0[2] ? 3 : 0)) >> 2) +
-           ((dseg(st, 2) + (st >= lg.st0[3] ? 3 : 0)) >> 2) + (max(st - lg.st0[3], 0) >> 2);
-  };
 
   // Weight loads of step st (clamped to the last) into its stage: pieces
   // n = 0 .. kPieces - 1 of 1 KB (pieces past the step's chunk bytes repeat
@@ -280,7 +275,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   auto issue_w = [&](int st, int j0, int j1) __attribute__((always_inline)) {
     st = min(st, nsteps - 1);
     const int wo = w_off(st), np = w_pieces(st);
-    char *stage = ring + (st % kWStages) * C::kStage;
+    char *stage = ring + (st & (kWStages - 1)) * C::kStage;
 #pragma unroll
     for (int j = j0; j < j1; ++j) {
       const int kb = min(wave + kWaves * j, np - 1);
@@ -476,8 +471,8 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   // still) the weight loads of s + 4 may then overwrite.
   auto step = [&](auto seg, auto set_tag, auto k_tag, int s, int grp) __attribute__((always_inline)) {
     constexpr int SEG = decltype(seg)::v, S = decltype(set_tag)::v, K = decltype(k_tag)::v;
-    const char *W = ring + (s % kWStages) * C::kStage;
-    const char *Wn = ring + ((s + 1) % kWStages) * C::kStage;
+    const char *W = ring + (s & (kWStages - 1)) * C::kStage;
+    const char *Wn = ring + ((s + 1) & (kWStages - 1)) * C::kStage;
     const ASet &x = xa[S];
 #pragma unroll
     for (int p = 0; p < 8; ++p) {
@@ -524,11 +519,11 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
   // holds the next step's activations; a segment that starts with them in
   // set 1 first copies them to set 0 (at most three times per kernel).  The
   // first step reads its own first two raw operands and restores the first.
-  int cur = 0;
+  int cur = 0, grpc = 0;
   auto run = [&](auto seg, int sb, int se) __attribute__((always_inline)) {
     if (sb >= se) return;
     if (cur) xa[0] = xa[1];
-    const char *W0 = ring + (sb % kWStages) * C::kStage;
+    const char *W0 = ring + (sb & (kWStages - 1)) * C::kStage;
     read_w(seg, W0, 0, 0);
     read_w(seg, W0, 1, 1);
     restore(seg, 0, 0);
@@ -536,7 +531,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
     // group loads the next group's scales, which then replace the current
     int s = sb;
     for (; s + 4 <= se; s += 4) {
-      const int grp = s_grp(s);
+      const int grp = grpc++;
       step(seg, Int<0>{}, Int<0>{}, s, grp);
       step(seg, Int<1>{}, Int<1>{}, s + 1, grp);
       step(seg, Int<0>{}, Int<2>{}, s + 2, grp);
@@ -546,7 +541,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
     const int n = se - s;
     cur = n & 1;
     if (n > 0) {
-      const int grp = s_grp(s);
+      const int grp = grpc++;
       step(seg, Int<0>{}, Int<0>{}, s, grp);
       if (n > 1) step(seg, Int<1>{}, Int<1>{}, s + 1, grp);
       if (n > 2) step(seg, Int<0>{}, Int<2>{}, s + 2, grp);
