@@ -652,11 +652,11 @@ def layer_bench(dev, sensitive: bool, reps: int = 5):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    # The defaults take about 25 ms of GPU time for the step: enough warm-up
-    # that the device runs at its steady clocks when the timed steps start
-    # (after 10 steps it is still about 10 % slower).
+    # The default warm-up is about 0.1 s of steps: the device reaches its
+    # steady clocks only after tens of milliseconds of work (after 10 steps
+    # a step still takes about 12 % longer, after 200 about 5 %).
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=2000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-layer", action="store_true")

@@ -34,9 +34,8 @@
 // 1x4 tiles; two workgroups per CU fit): twice the workgroups, each wave
 // half the products per step.
 //   - activations go straight from the image into registers -- each row is
-//     used by exactly one wave -- two steps ahead, in four register sets
-//     (one per step of a scale group), two loads in each of the step's
-//     first four positions;
+//     used by exactly one wave -- one step ahead, in two register sets, two
+//     loads in each of the step's first four positions;
 //   - the scale words (activation and weight) are loaded once per group of
 //     four steps, a group ahead, over three positions;
 //   - the weight chunk of each step (8 slabs, 6 to 12 KB) goes global -> LDS
@@ -71,8 +70,7 @@ constexpr int BN = kWCols, NT = 256, kWaves = NT / 64;
 constexpr int kFmtE4M3 = 0, kFmtE2M3 = 2, kFmtE3M2 = 3;
 constexpr int kWStages = 8;                  // weight ring: one stage per step (a power of two)
 constexpr int kWAhead = 4;                   // weight stages loaded ahead
-constexpr int kASets = 4;                    // activation register sets: one per step of a scale group
-constexpr int kAAhead = 2;                   // activation loads issued this many steps ahead
+constexpr int kASets = 2;                    // activation register sets (one ahead)
 // Activation loads per wave and step: per 32-row tile (TM of them) and
 // K-chunk the lane data (two loads).
 template <int TM> constexpr int kALoads = 2 * 2 * TM;
@@ -231,7 +229,8 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
     for (int n = 0; n < 4; ++n) acc[a][n] = v16f{};
 
   // Activation registers of one step: per 32-row tile and K-chunk the lane
-  // data (24 bytes of FP6 codes or 32 of FP8 codes).
+  // data (24 bytes of FP6 codes or 32 of FP8 codes) and the scale word; the
+  // step's weight scale bytes for each K-chunk (slab n at byte n).
   struct ASet {
     v8i d[TM][2];
   };
@@ -453,26 +452,23 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
         for (int i = 0; i < 4; ++i) gsc[0].ws[c][h][i] = gsc[1].ws[c][h][i] >> (8 * hx);
   };
 
-  // Step s (register set S = its position in the scale group): the
-  // products position by position.  At position p the step reads the raw
-  // operand of p + 2 (positions 8 and 9 are the next step's first two, read
-  // after the barrier), issues the first half of p's products, restores the
-  // operand of p + 1, then issues the second half.  Positions 0 to 3 issue
-  // the activation loads of step s + 2, one (tile, chunk) pair each, into
-  // set (S + 2) % 4: two steps of latency, since loads one step ahead still
-  // held the first products.  Between positions 3 and 4 the workgroup meets
-  // at a barrier, then positions 4 and 6 issue the weight loads of step
-  // s + 4 (and positions 4 to 6 of a group's first step the next group's
-  // scale loads).  Before the barrier each wave waits for its own weight
-  // loads of step s + 1: since them it has issued the activations loaded at
-  // s - 2, s - 1 and s and the weights of s + 2 and s + 3, perhaps with
+  // Step s (register set S = s % 2): the products position by position.  At
+  // position p the step reads the raw operand of p + 2 (positions 8 and 9
+  // are the next step's first two, read after the barrier), issues the
+  // first half of p's products, restores the operand of p + 1, then issues
+  // the second half.  Positions 0 to 3 issue the activation loads of step
+  // s + 1, one (tile, chunk) pair each; between positions 3 and 4 the
+  // workgroup meets at a barrier, then positions 4 and 6 issue the weight
+  // loads of step s + 4 (and positions 4 to 6 of a group's first step the
+  // next group's scale loads).  Before the barrier each wave waits for its
+  // own weight loads of step s + 1: since them it has issued the activations
+  // of s - 1, s and s + 1 and the weights of s + 2 and s + 3, perhaps with
   // scale loads between them, so leaving at most two activation and two
-  // weight bundles in flight waits for them (and for the activations loaded
-  // at s - 2, which this step has consumed; this also holds in the first
-  // steps, after the prologue).  After the barrier the stage of s + 1 is
-  // complete, and every wave is past step s - 1, whose stage ((s + 4) % 8 =
-  // (s - 4) % 8 is older still) the weight loads of s + 4 may then
-  // overwrite.
+  // weight bundles in flight waits for them (and for the activations of
+  // s - 1, already consumed; this also holds in the first steps, after the
+  // prologue).  After the barrier the stage of s + 1 is complete, and every
+  // wave is past step s - 1, whose stage ((s + 4) % 8 = (s - 4) % 8 is older
+  // still) the weight loads of s + 4 may then overwrite.
   auto step = [&](auto seg, auto set_tag, auto k_tag, int s, int grp) __attribute__((always_inline)) {
     constexpr int SEG = decltype(seg)::v, S = decltype(set_tag)::v, K = decltype(k_tag)::v;
     const char *W = ring + (s & (kWStages - 1)) * C::kStage;
@@ -490,7 +486,7 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
       // new segment, whose loop reads them again)
       if (p + 2 < 8) read_w(seg, W, (p + 2) & 3, p + 2);
       else read_w(seg, Wn, (p + 2) & 3, p - 6);
-      if (p < 2 * TM) issue_a(Int<(S + kAAhead) % kASets>{}, s + kAAhead, p);
+      if (p < 2 * TM) issue_a(Int<(S + 1) % kASets>{}, s + 1, p);
       if (p >= 4 && p < 7 && K == 0) issue_g(Int<1>{}, grp + 1, p - 4);
       __builtin_amdgcn_sched_barrier(0);
       // the products interleaved with the next operand's restore: a wave
@@ -518,27 +514,15 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
     }
   };
 
-  // Steps [sb, se) of one segment: groups of four steps, step k of a group
-  // in register set k, then the segment's last (1-4 step) group.  `cur` is
-  // the set that holds the segment's first step (the set after the previous
-  // segment's last step); the set after it holds the second.  A segment
-  // that starts elsewhere first moves them to sets 0 and 1 (at most three
-  // times per kernel).  The first step reads its own first two raw operands
-  // and restores the first.
+  // Steps [sb, se) of one segment: pairs of steps (register sets 0 and 1)
+  // in a loop with one exit, then a last odd step.  `cur` is the set that
+  // holds the next step's activations; a segment that starts with them in
+  // set 1 first copies them to set 0 (at most three times per kernel).  The
+  // first step reads its own first two raw operands and restores the first.
   int cur = 0, grpc = 0;
   auto run = [&](auto seg, int sb, int se) __attribute__((always_inline)) {
     if (sb >= se) return;
-    if (cur == 1) {
-      xa[0] = xa[1];
-      xa[1] = xa[2];
-    } else if (cur == 2) {
-      xa[0] = xa[2];
-      xa[1] = xa[3];
-    } else if (cur == 3) {
-      const ASet t0 = xa[0];
-      xa[0] = xa[3];
-      xa[1] = t0;
-    }
+    if (cur) xa[0] = xa[1];
     const char *W0 = ring + (sb & (kWStages - 1)) * C::kStage;
     read_w(seg, W0, 0, 0);
     read_w(seg, W0, 1, 1);
@@ -550,36 +534,31 @@ void gemm_prefill_kernel(GemmArgs g, int mtiles, int ntiles, int gm, int gn) {
       const int grp = grpc++;
       step(seg, Int<0>{}, Int<0>{}, s, grp);
       step(seg, Int<1>{}, Int<1>{}, s + 1, grp);
-      step(seg, Int<2>{}, Int<2>{}, s + 2, grp);
-      step(seg, Int<3>{}, Int<3>{}, s + 3, grp);
+      step(seg, Int<0>{}, Int<2>{}, s + 2, grp);
+      step(seg, Int<1>{}, Int<3>{}, s + 3, grp);
       next_group();
     }
     const int n = se - s;
-    cur = n & 3;
+    cur = n & 1;
     if (n > 0) {
       const int grp = grpc++;
       step(seg, Int<0>{}, Int<0>{}, s, grp);
       if (n > 1) step(seg, Int<1>{}, Int<1>{}, s + 1, grp);
-      if (n > 2) step(seg, Int<2>{}, Int<2>{}, s + 2, grp);
+      if (n > 2) step(seg, Int<0>{}, Int<2>{}, s + 2, grp);
       next_group();
     }
   };
 
-  // Prologue: the weights of steps 0 and 1, the activations of steps 0 and
-  // 1, the first group's scales, the weights of steps 2 and 3, and the wait
-  // for the stage of step 0.
+  // Prologue: the weights of steps 0 and 1, the activations of step 0, the
+  // weights of steps 2 and 3, and the wait for the stage of step 0.
   issue_w(0, 0, C::kWLoads);
   issue_w(1, 0, C::kWLoads);
   for (int pp = 0; pp < 2 * TM; ++pp) issue_a(Int<0>{}, 0, pp);
-  for (int pp = 0; pp < 2 * TM; ++pp) issue_a(Int<1>{}, 1, pp);
   for (int pp = 0; pp < 3; ++pp) issue_g(Int<1>{}, 0, pp);
   issue_w(2, 0, C::kWLoads);
   issue_w(3, 0, C::kWLoads);
   __builtin_amdgcn_sched_barrier(0);
-  // the stage of step 0: since its loads, the weights of step 1, the
-  // activations of steps 0 and 1, the scales and the weights of steps 2
-  // and 3
-  wait_loads<3 * C::kWLoads + 2 * kALoads<TM> + kGLoads<TM>>();
+  wait_loads<3 * C::kWLoads + kALoads<TM> + kGLoads<TM>>();
   barrier();
   next_group();
 
