@@ -466,6 +466,28 @@ def decode_bench(dev, which: str = "up", reps: int = 50):
         gbs = w_bytes / (ms * 1e-3) / 1e9
         out["M%d" % M] = {"us": ms * 1e3, "packed_weight_GBps": gbs,
                           "frac_hbm_peak": gbs / HBM_PEAK_GBS}
+    # What a pure streaming read reaches over the same bytes per launch (the
+    # buffer's size, four rotated copies): a short launch pays its ramp-up
+    # and tail, which the 1 GiB figure of `peaks` hides.
+    sink = mxq.peak_sink(dev)
+    srcs = [torch.empty(buf_bytes // 16 * 16, dtype=torch.uint8, device=dev) for _ in range(4)]
+    for b in srcs:
+        b.fill_(1)
+    for i in range(8):
+        mxq.peak_stream_read(srcs[i % 4], sink)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(reps):
+        mxq.peak_stream_read(srcs[i % 4], sink)
+    e1.record()
+    torch.cuda.synchronize()
+    s_us = e0.elapsed_time(e1) / reps * 1e3
+    del srcs
+    out["stream_read_same_bytes"] = {"us": s_us, "GBps": buf_bytes / (s_us * 1e-6) / 1e9}
+    for M in (1, 4, 16, 64):
+        out["M%d" % M]["frac_stream_read_same_bytes"] = s_us / out["M%d" % M]["us"]
     out["workload"] = "LLaMA-2-70B %s-projection decode K=%d N=%d widths %d/%d/%d, " \
                       "4 weight buffers rotated (%.1f MB of packed weights and " \
                       "exponents streamed per launch)" % (
