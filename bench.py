@@ -688,6 +688,7 @@ def main():
     ap.add_argument("--no-attn", action="store_true")
     ap.add_argument("--no-template", action="store_true")
     ap.add_argument("--no-mlp", action="store_true")
+    ap.add_argument("--no-paper-point", action="store_true")
     ap.add_argument("--oracle-layer", action="store_true",
                     help="also time the oracle on a 256-row sample of the 70B layer")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -846,11 +847,12 @@ def main():
         result["mlp"] = {"gate_up": prefill_leg(dev, mlp_cases()[0], 20, 5, pk),
                          "down": prefill_leg(dev, mlp_cases()[1], 20, 5, pk)}
     log("paper operating point and rotated quantizer at the attention shape")
-    pp = W.make_linear(2, "paper_point_127_0_1", M, K, N, 0.0, 0.0, counts=(127, 0, 1))
-    result["paper_point"] = prefill_leg(dev, pp, args.steps, args.warmup, pk)
-    result["paper_point"]["workload"] = (
-        "the paper's operating point (one 8-bit block of 32 columns, the rest 4-bit: "
-        "127/0/1 blocks) at the attention-projection shape M=2048 K=N=4096")
+    if not args.no_paper_point:
+        pp = W.make_linear(2, "paper_point_127_0_1", M, K, N, 0.0, 0.0, counts=(127, 0, 1))
+        result["paper_point"] = prefill_leg(dev, pp, args.steps, args.warmup, pk)
+        result["paper_point"]["workload"] = (
+            "the paper's operating point (one 8-bit block of 32 columns, the rest 4-bit: "
+            "127/0/1 blocks) at the attention-projection shape M=2048 K=N=4096")
     result["quantize"]["rotated"] = prefill_leg(
         dev, case, 10, 2, pk, rotate_bytes=600 << 20)["quantize_rotated"]
     if not args.no_fused:
