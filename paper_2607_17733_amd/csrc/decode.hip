@@ -278,25 +278,13 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
     using I1 = std::integral_constant<int, 1>;
     using I2 = std::integral_constant<int, 2>;
     using I3 = std::integral_constant<int, 3>;
-    if (T == 1 && nst == 4 && SEG <= 1) {
-      // a whole group: every load first, then the products
-      const Raw r0 = load(0), r1 = load(1), r2 = load(2), r3 = load(3);
-      compute(I0(), r0);
-      compute(I1(), r1);
-      compute(I2(), r2);
-      compute(I3(), r3);
-    } else if (T == 1 && nst == 4 && SEG == 2) {
-      const Raw r0 = load(0), r1 = load(1), r2 = load(2), r3 = load(3);
-      compute(I0(), r0);
-      compute(I1(), r1);
-      compute(I2(), r2);
-      compute(I3(), r3);
-    } else if (T <= 2 && nst == 4) {
-      // two steps in flight at a time (8-bit steps, or two activation tiles)
+    if (T <= 2 && nst == 4) {
+      // two steps in flight: each step's products, then the load two steps on
       const Raw r0 = load(0), r1 = load(1);
       compute(I0(), r0);
+      const Raw r2 = load(2);
       compute(I1(), r1);
-      const Raw r2 = load(2), r3 = load(3);
+      const Raw r3 = load(3);
       compute(I2(), r2);
       compute(I3(), r3);
     } else {
