@@ -94,7 +94,10 @@ __device__ inline uint32_t lo_codes(uint32_t w) {
 }
 
 // T: 16-row activation tiles (M <= 16 T); SL: 16-column slabs per
-// workgroup (2 or 4: one activation load feeds all of them).
+// workgroup (one activation load feeds all of them).  A unit is SL
+// consecutive slabs; with 2 or 4 it lies inside one 128-column super-slab,
+// with 5 to 7 (one unit per CU where that balances the CUs) it may cross
+// into the next super-slab.
 template <bool FULL, int T, int SL>
 __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g) {
   __shared__ v4f red[kMaxWaves][SL][64];
@@ -103,21 +106,32 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
   const int nw = blockDim.x >> 6;
   const int grp = lane >> 4, line = lane & 15;
   const LGeo lg(g.n3, g.n4, g.n6, g.n8);
-  // The units of a super-slab run on one XCD (workgroups b, b + 8, ... of a
-  // round-robin dispatch), so its L2 reads each step record of the
-  // super-slab and its scale block whole.
-  constexpr int PPS = kWSlabs / SL;                  // units per super-slab
+  // Aligned units: the units of a super-slab run on one XCD (workgroups b,
+  // b + 8, ... of a round-robin dispatch), so its L2 reads each step record
+  // of the super-slab and its scale block whole.  Crossing units: each XCD
+  // takes a contiguous range of units, whose super-slabs it then shares.
+  constexpr bool ALIGNED = kWSlabs % SL == 0;
   int64_t unit = blockIdx.x;
-  if ((gridDim.x % (8 * PPS)) == 0) {
-    const int64_t x = unit & 7, i = unit >> 3;
-    unit = ((i / PPS) * 8 + x) * PPS + (i % PPS);
+  if (ALIGNED) {
+    constexpr int PPS = kWSlabs / SL;                // units per super-slab
+    if ((gridDim.x % (8 * PPS)) == 0) {
+      const int64_t x = unit & 7, i = unit >> 3;
+      unit = ((i / PPS) * 8 + x) * PPS + (i % PPS);
+    }
+  } else if ((gridDim.x & 7) == 0) {
+    unit = (unit & 7) * (gridDim.x >> 3) + (unit >> 3);
   }
-  const int64_t ss = unit / PPS;                     // super-slab
-  const int n0 = SL * (int)(unit % PPS);             // first slab of the unit
+  const int64_t gs0 = unit * SL;                     // first slab of the unit
+  const int64_t ss = gs0 / kWSlabs;                  // its super-slab
+  const int n0 = (int)(gs0 % kWSlabs);               // its slab in the super-slab
   // slabs past N (inside the padded super-slab) read the unit's first slab
-  auto live = [&](int sl) { return unit * 16 * SL + 16 * sl < g.N; };
+  auto live = [&](int sl) { return gs0 * 16 + 16 * sl < g.N; };
+  // slab sl lies in super-slab ss + 1 when n0 + sl >= 8 (at most one
+  // crossing); cross: some live slab of the unit does
+  const bool cross = !ALIGNED && n0 + SL > kWSlabs && (ss + 1) * kWCols < g.N;
   const uint8_t *wsup = g.w_mant + ss * g.w_super;
   const uint8_t *wsc = g.w_exp + ss * g.w_super_sc + 32 * lane;
+  const uint8_t *wsc2 = cross ? wsc + g.w_super_sc : wsc;
   // Lanes of rows >= M read the first row of their tile (same addresses as a
   // live lane, so no extra traffic); their output rows are discarded.
   int alane[T];
@@ -135,16 +149,24 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
     const int gl = gi - lg.G0[SEG];
     const int nst = min(4, lg.S[SEG] - 4 * gl);
     // the lane's scale bytes of the group: byte 8 k + n for step k, slab n;
-    // sw[sl] gathers the four steps' bytes of slab n0 + sl
+    // sw[sl] gathers the four steps' bytes of slab n0 + sl (of the next
+    // super-slab's block past slab 7)
     const u4 s0 = stream_load((const u4 *)(wsc + (int64_t)gi * 2048));
     const u4 s1 = stream_load((const u4 *)(wsc + (int64_t)gi * 2048 + 16));
+    u4 t0 = s0, t1 = s1;
+    if (!ALIGNED) {
+      t0 = stream_load((const u4 *)(wsc2 + (int64_t)gi * 2048));
+      t1 = stream_load((const u4 *)(wsc2 + (int64_t)gi * 2048 + 16));
+    }
     // step k's byte of slab b lies in dword 2k + b / 4
     uint32_t sw[SL];
 #pragma unroll
     for (int sl = 0; sl < SL; ++sl) {
-      const int b = n0 + sl;
-      const uint32_t d0 = b < 4 ? s0[0] : s0[1], d1 = b < 4 ? s0[2] : s0[3];
-      const uint32_t d2 = b < 4 ? s1[0] : s1[1], d3 = b < 4 ? s1[2] : s1[3];
+      const bool hi = !ALIGNED && n0 + sl >= kWSlabs;
+      const int b = (n0 + sl) & (kWSlabs - 1);
+      const u4 x0 = hi ? t0 : s0, x1 = hi ? t1 : s1;
+      const uint32_t d0 = b < 4 ? x0[0] : x0[1], d1 = b < 4 ? x0[2] : x0[3];
+      const uint32_t d2 = b < 4 ? x1[0] : x1[1], d3 = b < 4 ? x1[2] : x1[3];
       const int sh = 8 * (b & 3);
       sw[sl] = ((d0 >> sh) & 0xFFu) | (((d1 >> sh) & 0xFFu) << 8) | (((d2 >> sh) & 0xFFu) << 16) |
                (((d3 >> sh) & 0xFFu) << 24);
@@ -182,7 +204,9 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
       }
 #pragma unroll
       for (int sl = 0; sl < SL; ++sl) {
-        const uint8_t *w = live(sl) ? w0 + sl * CB : w0;
+        // a slab past slab 7 lies in the next super-slab, at the same offset
+        const int64_t next = (!ALIGNED && n0 + sl >= kWSlabs) ? g.w_super - (int64_t)kWSlabs * CB : 0;
+        const uint8_t *w = live(sl) ? w0 + sl * CB + next : w0;
         if (SEG == 0 && !FULL) {
           r.x[sl] = stream_load((const u2 *)(w + 8 * lane));
           r.z[sl] = stream_load((const uint32_t *)(w + 512 + 4 * lane));
@@ -315,7 +339,7 @@ __global__ __launch_bounds__(64 * kMaxWaves) void gemm_decode_kernel(GemmArgs g)
       if (!live(sl)) continue;
       v4f y = red[0][sl][lane];
       for (int w = 1; w < nw; ++w) y += red[w][sl][lane];
-      const int64_t col = unit * 16 * SL + 16 * sl + line;
+      const int64_t col = gs0 * 16 + 16 * sl + line;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int row = 16 * t + 4 * grp + i;
@@ -361,12 +385,31 @@ hipError_t launch_gemm_decode(const GemmArgs &a, hipStream_t stream) {
   if (tiles < 1 || tiles > kDecodeTiles) return hipErrorInvalidValue;
   const int cus = device_cu_count();
   // four slabs per workgroup (half the activation loads per weight byte)
-  // when that still gives every CU a workgroup, else two
+  // when that still gives every CU a workgroup, else two; where the slabs
+  // come to 5 to 7 per CU (M <= 16), one unit of that many per CU, since four-slab
+  // units would give some CUs one unit and others two (the kernel takes as
+  // long as its busiest CUs: 448 four-slab units on 256 CUs ran 26.1 us,
+  // 512 ran 27.5 us)
   const bool quad = (a.N + 63) / 64 >= cus;
+  const int64_t nslabs = (a.N + 15) / 16;
+  const int64_t spc = (nslabs + cus - 1) / cus;
   auto go = [&](auto fc, auto tc) {
     constexpr bool FULL = decltype(fc)::value;
     constexpr int T = decltype(tc)::value;
-    if (quad) {
+    auto one_per_cu = [&](auto sc) {
+      constexpr int SL = decltype(sc)::value;
+      const int64_t units = (nslabs + SL - 1) / SL;
+      const dim3 grid((unsigned)units), block((unsigned)(64 * decode_waves<FULL, T, SL>(units, cus)));
+      hipLaunchKernelGGL((gemm_decode_kernel<FULL, T, SL>), grid, block, 0, stream, a);
+    };
+    // (one activation tile only: with more, units of 5 to 7 slabs spill)
+    if (T == 1 && spc >= 5 && spc <= 7) {
+      if constexpr (T == 1) {
+        if (spc == 7) one_per_cu(std::integral_constant<int, 7>{});
+        else if (spc == 6) one_per_cu(std::integral_constant<int, 6>{});
+        else one_per_cu(std::integral_constant<int, 5>{});
+      }
+    } else if (quad) {
       const int64_t units = (a.N + 63) / 64;
       const dim3 grid((unsigned)units), block((unsigned)(64 * decode_waves<FULL, T, 4>(units, cus)));
       hipLaunchKernelGGL((gemm_decode_kernel<FULL, T, 4>), grid, block, 0, stream, a);

@@ -285,6 +285,24 @@ def test_decode_full(which):
                    "decode M=%d" % M, cols=cols)
 
 
+# Decode with one unit of 5, 6 or 7 slabs per CU (the slab count of N comes
+# to 5-7 per CU on a 256-CU device): units cross from one 128-column
+# super-slab into the next; ragged N leaves dead slabs in the last unit.
+DECODE_UNIT_PER_CU = [
+    # M, K, N, (n4, n6, n8)
+    (1, 256, 28632, (4, 2, 2)),      # 7 slabs per CU, last slab ragged
+    (16, 256, 25000, (4, 2, 2)),     # 7 slabs per CU, last unit short
+    (7, 320, 24000, (6, 2, 2)),      # 6 slabs per CU
+    (3, 256, 17000, (4, 2, 2)),      # 5 slabs per CU
+]
+
+
+@pytest.mark.parametrize("M,K,N,counts", DECODE_UNIT_PER_CU)
+def test_decode_units_across_superslabs(M, K, N, counts):
+    case = W.random_case(M * 13 + N, M, K, N, counts, perm="random")
+    _full_check(case, partials=False)
+
+
 def test_kv_cache_quantize():
     """4-bit MXINT along the head dimension for a 4096-token, 8-head cache."""
     for which in (0, 1):
