@@ -21,7 +21,9 @@
 // step is read once for all of the launch's 16-row activation tiles (up to
 // four: M <= 64).  A workgroup
 // owns a unit of four 16-column slabs, or two where four would leave CUs
-// without a workgroup (one activation load feeds all of them); its nw waves
+// without a workgroup, or (M <= 16) one unit of 5 to 7 consecutive slabs
+// per CU where that balances the CUs (one activation load feeds all of
+// them); its nw waves
 // (2 to 8, the most at which every unit is resident by the kernel's register
 // occupancy) take every nw-th group of four steps; a group's scale bytes are
 // one word per lane and operand.  The waves' fp32 accumulators meet in LDS
