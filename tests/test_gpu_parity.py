@@ -303,6 +303,13 @@ def test_decode_units_across_superslabs(M, K, N, counts):
     _full_check(case, partials=False)
 
 
+def test_decode_units_across_superslabs_full_clamp():
+    """The full clamp's weight records (two's complement 8-bit digits, the
+    4-bit record's extra plane) through units that cross super-slabs."""
+    case = W.random_case(77, 9, 384, 27000, (6, 3, 3), perm="scales")
+    _full_check(case, "rna", "full", partials=False)
+
+
 def test_kv_cache_quantize():
     """4-bit MXINT along the head dimension for a 4096-token, 8-head cache."""
     for which in (0, 1):
