@@ -37,6 +37,7 @@ typedef short v2s __attribute__((ext_vector_type(2)));
 typedef unsigned short v2us __attribute__((ext_vector_type(2)));
 typedef unsigned u4 __attribute__((ext_vector_type(4)));
 typedef unsigned u2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kMaxThreads = 1024;
 constexpr int kLdsBudget = 144 * 1024;  // staged rows of one workgroup per CU
@@ -528,7 +529,22 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
   // any of them, so the batch costs one memory latency instead of one per
   // load.
   constexpr int kBatch = 8;
-  if (q.vec16) {
+  if (q.vec16 && !q.swiglu && K % 512 == 0) {
+    // Rows of whole 1 KB pieces go straight into LDS (direct-to-LDS loads,
+    // one piece per wave instruction), so no thread waits for its data
+    // before the permutation table is written.  Rows past the source's end
+    // read zeros: the buffer resource ends at its last row.
+    const int64_t live = q.src_rows > r0 ? q.src_rows - r0 : 0;
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(q.src + r0 * q.ld), 0, (int)min(live * q.ld * 2, (int64_t)0x7fffffff), 0x00020000);
+    const int per_row = K / 512;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6), nwaves = nthr >> 6;
+    for (int pc = wave; pc < R * per_row; pc += nwaves) {
+      const int lr = pc / per_row, j = pc - lr * per_row;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void *)(smem + lr * rowB + j * 1024), 16,
+                                               (t & 63) * 16, (int)(lr * q.ld * 2) + j * 1024, 0, 0);
+    }
+  } else if (q.vec16) {
     // vector v = lr * vpr + c, advanced by nthr without dividing per load
     const int vpr = K / 8, nv = R * vpr;
     const int dq = nthr / vpr, dr = nthr - dq * vpr;
@@ -584,6 +600,8 @@ __global__ __launch_bounds__(kMaxThreads) void quantize_act_kernel(QuantArgs q) 
       put_perm(c, *(const int4 *)(q.perm + 4 * c));
   }
   if (t < R) *(u4 *)(smem + t * rowB + 2 * K) = u4{0u, 0u, 0u, 0u};
+  // the direct-to-LDS loads are complete before the workgroup meets
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (q.rmsnorm) rms_normalise(q, smem, R, rowB, t, nthr, r0);
 
